@@ -1,0 +1,19 @@
+"""CPU oracle for the Z-order top-k attention forward (test infrastructure only).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
+``cpu_baseline`` leg may import this package; the product path never does.
+"""
+
+from .zeta_oracle import (  # noqa: F401
+    as_f32,
+    attend,
+    bf16_bits_to_f32,
+    forward,
+    interleave,
+    joint_range,
+    morton_encode,
+    quantise,
+    select_one,
+    select_topk,
+    sort_keys,
+)

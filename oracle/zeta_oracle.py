@@ -1,0 +1,272 @@
+"""CPU oracle for the ZETA Z-order top-k attention forward pass.
+
+TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import or run this module.  The
+product path (the HIP library and its Python binding) never touches it, and
+this module imports nothing from the product package.
+
+It is a plain, slow, obviously correct NumPy restatement of what the paper
+defines, one function per step, each citing the passage it follows:
+
+1. ``joint_range`` / ``quantise``: normalise each coordinate to an integer grid
+   of ``2**bits`` cells (Section 3.1, Z-order curves: normalisation and
+   discretisation to an integer grid, the formula floor((x - min)(2^b - 1) /
+   (max - min))).
+2. ``interleave``: the Z-order value of the integer coordinates (Section 3.1,
+   equation Z: bits interleaved most significant group first, axis 1 first in
+   each group).
+3. ``sort_keys``: keys sorted ascending by Z-value (Section 3.2.2; Algorithm 1,
+   Step 2), ties by position.
+4. ``select_topk`` / ``select_one``: per query, insertion point by binary search
+   among the keys it may see, then a window of k keys centred there
+   (Section 3.2.2, last two paragraphs; Algorithm 1, Steps 3-5).
+5. ``attend``: Adaptive Cauchy-softmax over the selected keys and the weighted
+   sum of their values (Section 3.3, equation cauchy; Section 3.4;
+   Appendix E.1, steps 1-4).
+
+Readings where the paper is silent or ambiguous (each is also listed in the
+design notes):
+
+* Quantisation is evaluated in float32, left to right, one IEEE rounding per
+  operation: den = hi - lo; t = x - lo; u = t * (2^b - 1); w = u / den;
+  code = clamp(floor(w), 0, 2^b - 1); code = 0 when den is not positive.
+* The range is per (batch, head, axis), joint over queries and keys, so both
+  share one grid (Section 3.2.2 maps keys and queries into the same 1-D space).
+  A caller-supplied range replaces it; values outside it clamp.
+* Equation Z puts coordinate 1 (axis 0 here) at the most significant bit of
+  each group of d bits; coordinates are read most significant bit first.
+* Sort ties are broken by ascending position (a stable sort).
+* The causal pool of query i is the exact prefix {0..i} (the chunk rule of
+  Section 3.2.2 in the limit of chunk size 1, diagonal included); the
+  non-causal pool is every key.
+* The insertion point p counts the pool keys with a code strictly below the
+  query's (torch.searchsorted's default left side).
+* The window holds min(k, |pool|) keys: floor(k/2) before p and the rest at or
+  after p, shifted inward at the pool's ends; it is emitted in (code,
+  position) order, padded with -1 to length k.
+* Distances use the unquantised q and k values; eps = gamma^2 > 0 is a scalar.
+
+Arithmetic: quantisation in float32 as above; attention in float64.
+"""
+
+from __future__ import annotations
+
+import bisect
+from typing import Optional, Tuple
+
+import numpy as np
+
+
+# ----------------------------------------------------------------------------
+# Input conversion
+# ----------------------------------------------------------------------------
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact float32 value of each bfloat16 bit pattern (the top half of a float32)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def as_f32(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Float32 values of an input array given as float32 or as bfloat16 bits."""
+    if dtype == "bf16":
+        return bf16_bits_to_f32(x)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float32)
+    raise ValueError(dtype)
+
+
+# ----------------------------------------------------------------------------
+# Step 1: normalise and discretise (Section 3.1, Z-order curves)
+# ----------------------------------------------------------------------------
+
+def joint_range(q: np.ndarray, k: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-segment, per-axis min and max over the queries and keys together.
+
+    q, k: float32 [S, N, d].  Returns (lo, hi), each float32 [S, d].
+    """
+    both = np.concatenate([q, k], axis=1)
+    return both.min(axis=1).astype(np.float32), both.max(axis=1).astype(np.float32)
+
+
+def quantise(x: np.ndarray, lo: np.ndarray, hi: np.ndarray, bits: int) -> np.ndarray:
+    """Integer grid coordinate of each value: floor((x - lo)(2^b - 1) / (hi - lo)).
+
+    x: float32 [..., d]; lo, hi: float32 broadcastable to x.  Evaluated in
+    float32 with one rounding per operation, clamped to [0, 2^b - 1]; a
+    non-positive range gives 0.  Returns uint32 of x's shape.
+    """
+    x = np.asarray(x, dtype=np.float32)
+    lo = np.asarray(lo, dtype=np.float32)
+    hi = np.asarray(hi, dtype=np.float32)
+    top = np.float32((1 << bits) - 1)
+    with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
+        den = (hi - lo).astype(np.float32)
+        t = (x - lo).astype(np.float32)
+        u = (t * top).astype(np.float32)
+        w = (u / den).astype(np.float32)
+        w = np.where(den > np.float32(0), w, np.float32(0))
+    c = np.clip(np.floor(w), np.float32(0), top)
+    return c.astype(np.uint32)
+
+
+# ----------------------------------------------------------------------------
+# Step 2: bit interleave (Section 3.1, equation Z)
+# ----------------------------------------------------------------------------
+
+def interleave(coords: np.ndarray, bits: int) -> np.ndarray:
+    """Z-order value of integer coordinates.
+
+    coords: uint [..., d], each below 2**bits.  The value is the bit string
+    b_{1,1} b_{2,1} .. b_{d,1} b_{1,2} .. b_{d,n}, where b_{a,1} is the most
+    significant bit of coordinate a.  Bit s (counted from the least
+    significant end) of coordinate a therefore lands at position
+    d*s + (d - 1 - a) of the result.  Returns uint64 of shape coords.shape[:-1].
+    """
+    coords = np.asarray(coords).astype(np.uint64)
+    d = coords.shape[-1]
+    z = np.zeros(coords.shape[:-1], dtype=np.uint64)
+    for a in range(d):
+        for s in range(bits):
+            bit = (coords[..., a] >> np.uint64(s)) & np.uint64(1)
+            z |= bit << np.uint64(d * s + (d - 1 - a))
+    return z
+
+
+def morton_encode(q: np.ndarray, k: np.ndarray, bits: int,
+                  range_lohi: Optional[Tuple[np.ndarray, np.ndarray]] = None):
+    """Z-order codes of queries and keys on one shared grid per segment.
+
+    q, k: float32 [S, N, d].  range_lohi: optional (lo, hi), each [S, d],
+    replacing the joint min/max.  Returns (q_codes, k_codes, lo, hi) with
+    codes as uint32 [S, N].
+    """
+    if range_lohi is None:
+        lo, hi = joint_range(q, k)
+    else:
+        lo, hi = (np.asarray(a, dtype=np.float32) for a in range_lohi)
+    qc = interleave(quantise(q, lo[:, None, :], hi[:, None, :], bits), bits)
+    kc = interleave(quantise(k, lo[:, None, :], hi[:, None, :], bits), bits)
+    return qc.astype(np.uint32), kc.astype(np.uint32), lo, hi
+
+
+# ----------------------------------------------------------------------------
+# Step 3: sort keys by Z-value (Section 3.2.2; Algorithm 1, Step 2)
+# ----------------------------------------------------------------------------
+
+def sort_keys(k_codes: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Ascending sort of each segment's key codes, ties by position.
+
+    k_codes: uint32 [S, N].  Returns (sorted_codes uint32 [S, N], perm int32
+    [S, N]) with sorted_codes[s] == k_codes[s][perm[s]].
+    """
+    perm = np.argsort(k_codes, axis=-1, kind="stable").astype(np.int32)
+    return np.take_along_axis(k_codes, perm, axis=-1), perm
+
+
+# ----------------------------------------------------------------------------
+# Step 4: candidate window per query (Section 3.2.2; Algorithm 1, Steps 3-5)
+# ----------------------------------------------------------------------------
+
+def _window(p: int, pool_size: int, k: int) -> Tuple[int, int]:
+    """Start and length of the k-window centred at insertion point p in a pool."""
+    m = min(k, pool_size)
+    s = min(max(p - k // 2, 0), pool_size - m)
+    return s, m
+
+
+def select_one(q_code: int, k_codes: np.ndarray, i: int, k: int, causal: bool) -> np.ndarray:
+    """Window of one query, straight from the definition (no incremental state).
+
+    k_codes: uint32 [N] of one segment; i: the query's position.  Returns
+    int32 [k]: key positions in (code, position) order, padded with -1.
+    """
+    n = len(k_codes)
+    pool = np.arange(i + 1 if causal else n, dtype=np.int64)
+    pc = k_codes[pool].astype(np.int64)
+    order = pool[np.lexsort((pool, pc))]  # by code, then by position
+    p = int(np.count_nonzero(pc < int(q_code)))
+    s, m = _window(p, len(pool), k)
+    out = np.full(k, -1, dtype=np.int32)
+    out[:m] = order[s:s + m]
+    return out
+
+
+def select_topk(q_codes: np.ndarray, k_codes: np.ndarray, k: int, causal: bool) -> np.ndarray:
+    """Windows of every query of every segment.
+
+    q_codes, k_codes: uint32 [S, N].  Returns int32 [S, N, k].  The causal
+    case keeps the pool {0..i} as a sorted Python list of (code, position)
+    keys, adding key i before answering query i; the non-causal case sorts
+    all keys once.  Both give exactly what ``select_one`` gives.
+    """
+    S, n = k_codes.shape
+    idx = np.full((S, n, k), -1, dtype=np.int32)
+    for seg in range(S):
+        kc = k_codes[seg].astype(np.int64)
+        qc = q_codes[seg].astype(np.int64)
+        if causal:
+            pool = []  # sorted keys code * 2^32 + position, i.e. (code, position) order
+            for i in range(n):
+                bisect.insort(pool, (int(kc[i]) << 32) | i)
+                p = bisect.bisect_left(pool, int(qc[i]) << 32)
+                s, m = _window(p, i + 1, k)
+                idx[seg, i, :m] = [e & 0xFFFFFFFF for e in pool[s:s + m]]
+        else:
+            order = np.argsort(kc, kind="stable")
+            sorted_codes = kc[order]
+            ps = np.searchsorted(sorted_codes, qc, side="left")
+            for i in range(n):
+                s, m = _window(int(ps[i]), n, k)
+                idx[seg, i, :m] = order[s:s + m]
+    return idx
+
+
+# ----------------------------------------------------------------------------
+# Step 5: Adaptive Cauchy-softmax attention over the window
+# (Section 3.3, equation cauchy; Section 3.4; Appendix E.1)
+# ----------------------------------------------------------------------------
+
+def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: float,
+           rows: Optional[np.ndarray] = None, block: int = 512) -> np.ndarray:
+    """o_i = sum_j S_ij v_j / sum_j S_ij with S_ij = 1 / (||q_i - k_j||^2 + eps).
+
+    q, k: [S, N, dk]; v: [S, N, dv] (float values of any float dtype); idx:
+    int32 [S, N, k] with -1 for empty slots (or [S, R, k] when ``rows`` gives
+    the R query positions it belongs to).  Computed in float64.  Returns
+    float64 [S, N, dv] (or [S, R, dv]).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    S = q.shape[0]
+    if rows is None:
+        rows = np.arange(q.shape[1])
+    out = np.zeros((S, len(rows), v.shape[-1]), dtype=np.float64)
+    for seg in range(S):
+        for r0 in range(0, len(rows), block):
+            rr = rows[r0:r0 + block]
+            ii = idx[seg, r0:r0 + len(rr)]
+            valid = ii >= 0
+            jj = np.where(valid, ii, 0)
+            diff = q[seg, rr][:, None, :] - k[seg][jj]  # [b, k, dk]
+            dist = np.sum(diff * diff, axis=-1)  # D_ij
+            score = np.where(valid, 1.0 / (dist + eps), 0.0)  # S_ij
+            z = score.sum(axis=1)  # Z_i
+            num = np.einsum("bk,bkd->bd", score, v[seg][jj])
+            out[seg, r0:r0 + len(rr)] = num / z[:, None]
+    return out
+
+
+# ----------------------------------------------------------------------------
+# The whole forward
+# ----------------------------------------------------------------------------
+
+def forward(q: np.ndarray, k: np.ndarray, v: np.ndarray, topk: int, eps: float, causal: bool,
+            bits: int, range_lohi=None) -> dict:
+    """All five steps for float32 inputs shaped [S, N, d]; returns every intermediate."""
+    qc, kc, lo, hi = morton_encode(q, k, bits, range_lohi)
+    sorted_codes, perm = sort_keys(kc)
+    idx = select_topk(qc, kc, topk, causal)
+    out = attend(q, k, v, idx, eps)
+    return dict(q_codes=qc, k_codes=kc, lo=lo, hi=hi, sorted_codes=sorted_codes, perm=perm,
+                idx=idx, out=out)

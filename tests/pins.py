@@ -1,0 +1,305 @@
+"""Pins that tie the CPU oracle to what the paper and mathematics fix.
+
+Each ``check_*`` function takes the oracle module (so a test can hand it a
+deliberately broken copy) and raises AssertionError when the oracle departs
+from a value or property that does not depend on the oracle itself:
+hand-worked values (``tests/golden/``), closed forms, invariants, special
+cases and brute force on tiny inputs.
+"""
+
+from __future__ import annotations
+
+import itertools
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rows(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                yield line.split()
+
+
+# ----------------------------------------------------------------------------
+# Encode: equation Z and the discretisation (Section 3.1)
+# ----------------------------------------------------------------------------
+
+def check_morton_golden(orc):
+    """Hand-worked Z-values of equation Z."""
+    for bits, c0, c1, c2, code in _rows("morton_codes.txt"):
+        bits = int(bits)
+        got = int(orc.interleave(np.array([[int(c0), int(c1), int(c2)]], dtype=np.uint32), bits)[0])
+        assert got == int(code, 16), (bits, c0, c1, c2, hex(got), code)
+
+
+def check_morton_bijection(orc):
+    """At b bits and d axes the full grid maps one-to-one onto [0, 2^(d b))."""
+    for d, bits in ((3, 2), (2, 3), (1, 5), (4, 2)):
+        grid = np.array(list(itertools.product(range(1 << bits), repeat=d)), dtype=np.uint32)
+        z = orc.interleave(grid, bits).astype(np.int64)
+        assert sorted(z.tolist()) == list(range(1 << (d * bits))), (d, bits)
+
+
+def check_morton_axis_order(orc):
+    """Incrementing the top bit of axis 0 outweighs every bit of the later axes,
+    and raising any one coordinate raises Z (monotone per axis)."""
+    rng = np.random.default_rng(11)
+    bits = 4
+    pts = rng.integers(0, 1 << bits, size=(500, 3)).astype(np.uint32)
+    z = orc.interleave(pts, bits).astype(np.int64)
+    for a in range(3):
+        up = pts.copy()
+        ok = up[:, a] < (1 << bits) - 1
+        up[ok, a] += 1
+        z2 = orc.interleave(up, bits).astype(np.int64)
+        assert np.all(z2[ok] > z[ok]), a
+    hi0 = np.array([[1 << (bits - 1), 0, 0]], dtype=np.uint32)
+    rest = np.array([[(1 << (bits - 1)) - 1, (1 << bits) - 1, (1 << bits) - 1]], dtype=np.uint32)
+    assert int(orc.interleave(hi0, bits)[0]) > int(orc.interleave(rest, bits)[0])
+
+
+def check_quantise_golden(orc):
+    """Hand-worked grid coordinates of the discretisation formula."""
+    for bits, lo, hi, x, code in _rows("quantise.txt"):
+        got = int(orc.quantise(np.float32(x), np.float32(lo), np.float32(hi), int(bits)))
+        assert got == int(code), (bits, lo, hi, x, got, code)
+
+
+def check_quantise_buckets(orc):
+    """On an exactly representable grid (lo=0, hi=2^b-1) every integer value
+    maps to itself and the float just below it to the cell below."""
+    for bits in (2, 6, 10):
+        top = (1 << bits) - 1
+        xs = np.arange(top + 1, dtype=np.float32)
+        got = orc.quantise(xs, np.float32(0), np.float32(top), bits)
+        assert np.array_equal(got, xs.astype(np.uint32)), bits
+        below = np.nextafter(xs[1:], np.float32(-np.inf))
+        got = orc.quantise(below, np.float32(0), np.float32(top), bits)
+        assert np.array_equal(got, np.arange(top, dtype=np.uint32)), bits
+
+
+def check_encode_joint_range(orc):
+    """Codes share one grid per segment: the smallest value of each axis over
+    q and k gets grid coordinate 0 and the largest 2^b - 1; a point holding the
+    per-axis minimum (maximum) of both sets gets code 0 (all ones)."""
+    rng = np.random.default_rng(5)
+    S, N, d, bits = 3, 40, 3, 10
+    q = rng.standard_normal((S, N, d)).astype(np.float32)
+    k = rng.standard_normal((S, N, d)).astype(np.float32) * 3 + 1
+    both = np.concatenate([q, k], axis=1)
+    lo, hi = both.min(axis=1), both.max(axis=1)
+    q[:, 0, :] = lo
+    k[:, 1, :] = hi
+    qc, kc, lo2, hi2 = orc.morton_encode(q, k, bits)
+    assert np.array_equal(lo2, lo) and np.array_equal(hi2, hi)
+    assert np.all(qc[:, 0] == 0)
+    assert np.all(kc[:, 1] == (1 << (d * bits)) - 1)
+    assert qc.dtype == np.uint32 and kc.dtype == np.uint32
+    # Caller range: values outside clamp to the grid's edges.
+    lo_c = np.zeros((S, d), np.float32)
+    hi_c = np.ones((S, d), np.float32)
+    qc, kc, _, _ = orc.morton_encode(np.full((S, 1, d), -5, np.float32),
+                                     np.full((S, 1, d), 5, np.float32), bits, (lo_c, hi_c))
+    assert np.all(qc == 0) and np.all(kc == (1 << (d * bits)) - 1)
+
+
+# ----------------------------------------------------------------------------
+# Sort (Section 3.2.2; Algorithm 1, Step 2)
+# ----------------------------------------------------------------------------
+
+def check_sort_invariants(orc):
+    """Sorted ascending, ties by ascending position, a permutation, and equal
+    to Python's own sort on the (code, position) pairs."""
+    rng = np.random.default_rng(3)
+    for n, code_bits in ((1, 4), (50, 2), (300, 6), (1000, 18)):
+        kc = rng.integers(0, 1 << code_bits, size=(2, n)).astype(np.uint32)
+        sc, perm = orc.sort_keys(kc)
+        for s in range(2):
+            assert sorted(perm[s].tolist()) == list(range(n))
+            assert np.array_equal(sc[s], kc[s][perm[s]])
+            expect = sorted(range(n), key=lambda j: (int(kc[s, j]), j))
+            assert perm[s].tolist() == expect
+
+
+# ----------------------------------------------------------------------------
+# Select (Section 3.2.2; Algorithm 1, Steps 3-5)
+# ----------------------------------------------------------------------------
+
+def _brute_window(kc, qc_i, i, k, causal):
+    """The window rule written out with plain Python on one query."""
+    pool = list(range(i + 1)) if causal else list(range(len(kc)))
+    ordered = sorted(pool, key=lambda j: (int(kc[j]), j))
+    p = sum(1 for j in pool if int(kc[j]) < int(qc_i))
+    m = min(k, len(pool))
+    start = p - k // 2
+    start = max(start, 0)
+    start = min(start, len(pool) - m)
+    return ordered[start:start + m] + [-1] * (k - m)
+
+
+def check_select_golden(orc):
+    """The six-token hand-worked example, both modes."""
+    rows = {r[0]: r[1:] for r in _rows("select_example.txt")}
+    k = int(rows["k"][0])
+    kc = np.array([[int(x) for x in rows["k_codes"]]], dtype=np.uint32)
+    qc = np.array([[int(x) for x in rows["q_codes"]]], dtype=np.uint32)
+    for mode, causal in (("causal", True), ("noncausal", False)):
+        expect = [[int(x) for x in grp.split()] for grp in " ".join(rows[mode]).split("|")]
+        got = orc.select_topk(qc, kc, k, causal)[0].tolist()
+        assert got == expect, (mode, got, expect)
+        for i in range(kc.shape[1]):
+            assert orc.select_one(int(qc[0, i]), kc[0], i, k, causal).tolist() == expect[i], (mode, i)
+
+
+def check_select_brute(orc):
+    """Brute force on tiny inputs with heavy code ties (2 and 3 code bits)."""
+    rng = np.random.default_rng(17)
+    for n, code_bits, k in ((1, 2, 1), (5, 2, 3), (17, 2, 4), (33, 3, 7), (64, 2, 8), (40, 3, 64), (48, 6, 16)):
+        kc = rng.integers(0, 1 << code_bits, size=(2, n)).astype(np.uint32)
+        qc = rng.integers(0, 1 << code_bits, size=(2, n)).astype(np.uint32)
+        for causal in (True, False):
+            got = orc.select_topk(qc, kc, k, causal)
+            for s in range(2):
+                for i in range(n):
+                    expect = _brute_window(kc[s], qc[s, i], i, k, causal)
+                    assert got[s, i].tolist() == expect, (n, code_bits, k, causal, s, i)
+                    one = orc.select_one(int(qc[s, i]), kc[s], i, k, causal)
+                    assert one.tolist() == expect, (n, k, causal, s, i)
+
+
+def check_select_invariants(orc):
+    """Count, distinctness, causality, and the window being a contiguous run of
+    the pool's (code, position) order that brackets the insertion point."""
+    rng = np.random.default_rng(23)
+    n, k = 200, 16
+    for code_bits in (3, 12):
+        kc = rng.integers(0, 1 << code_bits, size=(1, n)).astype(np.uint32)
+        qc = rng.integers(0, 1 << code_bits, size=(1, n)).astype(np.uint32)
+        for causal in (True, False):
+            idx = orc.select_topk(qc, kc, k, causal)[0]
+            for i in range(n):
+                row = idx[i]
+                L = i + 1 if causal else n
+                sel = [j for j in row.tolist() if j >= 0]
+                assert len(sel) == min(k, L)
+                assert np.all(row[len(sel):] == -1)
+                assert len(set(sel)) == len(sel)
+                if causal:
+                    assert max(sel) <= i
+                ordered = sorted(range(L), key=lambda j: (int(kc[0, j]), j))
+                start = ordered.index(sel[0])
+                assert ordered[start:start + len(sel)] == sel
+                p = sum(1 for j in range(L) if kc[0, j] < qc[0, i])
+                # With k >= 2 the keys on both sides of the insertion point are in.
+                if p >= 1:
+                    assert ordered[p - 1] in sel, (i, p)
+                if p < L:
+                    assert ordered[p] in sel, (i, p)
+
+
+def check_select_full_pool(orc):
+    """With k at least the pool size the window is the whole pool."""
+    rng = np.random.default_rng(29)
+    n = 37
+    kc = rng.integers(0, 64, size=(1, n)).astype(np.uint32)
+    qc = rng.integers(0, 64, size=(1, n)).astype(np.uint32)
+    for causal in (True, False):
+        idx = orc.select_topk(qc, kc, n + 3, causal)[0]
+        for i in range(n):
+            L = i + 1 if causal else n
+            sel = [j for j in idx[i].tolist() if j >= 0]
+            assert sorted(sel) == list(range(L))
+
+
+# ----------------------------------------------------------------------------
+# Attend (Section 3.3, equation cauchy; Section 3.4; Appendix E.1)
+# ----------------------------------------------------------------------------
+
+def check_attend_hand(orc):
+    """Two keys at squared distances 1 and 3 from q, eps = 1: scores 1/2 and
+    1/4, weights 2/3 and 1/3."""
+    q = np.zeros((1, 1, 3))
+    k = np.array([[[1.0, 0, 0], [1.0, 1.0, 1.0]]])
+    v = np.array([[[3.0, -6.0], [0.0, 9.0]]])
+    qq = np.concatenate([q, np.zeros((1, 1, 3))], axis=1)
+    idx = np.array([[[0, 1], [0, 1]]], dtype=np.int32)
+    out = orc.attend(qq, k, v, idx, 1.0)
+    assert np.allclose(out[0, 0], [2.0, -1.0], atol=1e-12), out[0, 0]
+    # A padded slot contributes nothing.
+    idx = np.array([[[0, -1], [1, -1]]], dtype=np.int32)
+    out = orc.attend(qq, k, v, idx, 1.0)
+    assert np.allclose(out[0], [[3.0, -6.0], [0.0, 9.0]], atol=1e-12)
+
+
+def _dense_cauchy(q, k, v, eps, causal):
+    """Dense Cauchy attention as one masked N x N matrix (float64)."""
+    d2 = ((q[:, None, :] - k[None, :, :]) ** 2).sum(-1)
+    s = 1.0 / (d2 + eps)
+    if causal:
+        s = np.tril(s)
+    return (s @ v) / s.sum(axis=1, keepdims=True)
+
+
+def check_attend_dense_limit(orc):
+    """With k >= N the method is dense (causal) Cauchy attention."""
+    rng = np.random.default_rng(31)
+    for n, causal in ((64, True), (96, False), (80, True)):
+        q = rng.standard_normal((2, n, 3)).astype(np.float32)
+        k = rng.standard_normal((2, n, 3)).astype(np.float32)
+        v = rng.standard_normal((2, n, 16)).astype(np.float32)
+        res = orc.forward(q, k, v, n + 5, 0.5, causal, 10)
+        for s in range(2):
+            ref = _dense_cauchy(q[s].astype(np.float64), k[s].astype(np.float64),
+                                v[s].astype(np.float64), 0.5, causal)
+            assert np.allclose(res["out"][s], ref, rtol=1e-12, atol=1e-12), (n, causal)
+
+
+def check_attend_special_cases(orc):
+    """Causal o_0 = v_0; huge eps gives the plain mean over the window;
+    identical keys give uniform weights; outputs stay inside the window's
+    per-component range."""
+    rng = np.random.default_rng(37)
+    n, k, dv = 120, 16, 8
+    q = rng.standard_normal((1, n, 3)).astype(np.float32)
+    kk = rng.standard_normal((1, n, 3)).astype(np.float32)
+    v = rng.standard_normal((1, n, dv)).astype(np.float32)
+    res = orc.forward(q, kk, v, k, 0.5, True, 10)
+    assert np.allclose(res["out"][0, 0], v[0, 0], atol=1e-15)
+    idx = res["idx"][0]
+    for i in range(n):
+        sel = idx[i][idx[i] >= 0]
+        rows64 = v[0][sel].astype(np.float64)
+        lo, hi = rows64.min(axis=0), rows64.max(axis=0)
+        assert np.all(res["out"][0, i] >= lo - 1e-12) and np.all(res["out"][0, i] <= hi + 1e-12)
+    out_big = orc.attend(q, kk, v, res["idx"], 1e12)[0]
+    for i in range(n):
+        sel = idx[i][idx[i] >= 0]
+        assert np.allclose(out_big[i], v[0][sel].astype(np.float64).mean(axis=0), atol=1e-9)
+    same = np.repeat(kk[:, :1, :], n, axis=1)
+    out_same = orc.attend(q, same, v, res["idx"], 0.5)[0]
+    for i in range(n):
+        sel = idx[i][idx[i] >= 0]
+        assert np.allclose(out_same[i], v[0][sel].astype(np.float64).mean(axis=0), atol=1e-12)
+
+
+ALL_PINS = [
+    check_morton_golden,
+    check_morton_bijection,
+    check_morton_axis_order,
+    check_quantise_golden,
+    check_quantise_buckets,
+    check_encode_joint_range,
+    check_sort_invariants,
+    check_select_golden,
+    check_select_brute,
+    check_select_invariants,
+    check_select_full_pool,
+    check_attend_hand,
+    check_attend_dense_limit,
+    check_attend_special_cases,
+]

@@ -1,0 +1,62 @@
+"""Plant plausible mistakes in a copy of the oracle and check the pins catch each.
+
+Every mutation is a textual edit of the oracle's source, executed into a fresh
+module on the CPU.  A mutation that no pin rejects would mean the pins leave
+that part of the oracle unchecked.
+"""
+
+import inspect
+import types
+
+import pytest
+
+import oracle.zeta_oracle as orc
+import pins
+
+MUTATIONS = {
+    "axis order reversed": ("d * s + (d - 1 - a)", "d * s + a"),
+    "least significant bit first": ("d * s + (d - 1 - a)", "d * (bits - 1 - s) + (d - 1 - a)"),
+    "grid of 2^b cells scale": ("top = np.float32((1 << bits) - 1)", "top = np.float32(1 << bits)"),
+    "round instead of floor": ("c = np.clip(np.floor(w)", "c = np.clip(np.round(w)"),
+    "range over queries only": ("both = np.concatenate([q, k], axis=1)", "both = q"),
+    "no zero-range guard": ("w = np.where(den > np.float32(0), w, np.float32(0))", "w = np.nan_to_num(w)"),
+    "unstable sort": ('perm = np.argsort(k_codes, axis=-1, kind="stable")',
+                      'perm = np.argsort(k_codes.astype(np.int64) * 4096 - np.arange(k_codes.shape[-1]), axis=-1)'),
+    "insertion on the right": ("p = bisect.bisect_left(pool, int(qc[i]) << 32)",
+                               "p = bisect.bisect_right(pool, (int(qc[i]) << 32) | 0xFFFFFFFF)"),
+    "searchsorted right": ('ps = np.searchsorted(sorted_codes, qc, side="left")',
+                           'ps = np.searchsorted(sorted_codes, qc, side="right")'),
+    "window leans right": ("s = min(max(p - k // 2, 0), pool_size - m)",
+                           "s = min(max(p - (k + 1) // 2, 0), pool_size - m)"),
+    "window truncated at end": ("s = min(max(p - k // 2, 0), pool_size - m)", "s = max(p - k // 2, 0)"),
+    "diagonal excluded": ("                bisect.insort(pool, (int(kc[i]) << 32) | i)\n"
+                          "                p = bisect.bisect_left(pool, int(qc[i]) << 32)\n",
+                          "                p = bisect.bisect_left(pool, int(qc[i]) << 32)\n"
+                          "                bisect.insort(pool, (int(kc[i]) << 32) | i)\n"),
+    "distance not squared": ("dist = np.sum(diff * diff, axis=-1)", "dist = np.sqrt(np.sum(diff * diff, axis=-1))"),
+    "eps squared": ("score = np.where(valid, 1.0 / (dist + eps), 0.0)",
+                    "score = np.where(valid, 1.0 / (dist + eps * eps), 0.0)"),
+    "padding not masked": ("score = np.where(valid, 1.0 / (dist + eps), 0.0)", "score = 1.0 / (dist + eps)"),
+    "not normalised": ("out[seg, r0:r0 + len(rr)] = num / z[:, None]", "out[seg, r0:r0 + len(rr)] = num"),
+    "query minus wrong row": ("diff = q[seg, rr][:, None, :] - k[seg][jj]", "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]"),
+}
+
+
+def _mutant(old, new):
+    src = inspect.getsource(orc)
+    assert src.count(old) == 1, f"mutation anchor not unique: {old!r}"
+    mod = types.ModuleType("zeta_oracle_mutant")
+    exec(compile(src.replace(old, new), "zeta_oracle_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_pins_reject_mutation(name):
+    mod = _mutant(*MUTATIONS[name])
+    caught = []
+    for check in pins.ALL_PINS:
+        try:
+            check(mod)
+        except Exception:  # noqa: BLE001 - any failure counts as caught
+            caught.append(check.__name__)
+    assert caught, f"no pin rejects the planted mistake {name!r}"
