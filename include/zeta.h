@@ -1,0 +1,164 @@
+/*
+ * zeta.h -- C ABI of the Z-order top-k attention forward pass (ZETA) for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The forward pass has four calls, run in this order on one stream:
+ *
+ *   zeta_morton_encode  -> Z-order codes of queries and keys
+ *   zeta_sort_keys      -> keys sorted by code per (batch, head)
+ *   zeta_select_topk    -> k candidate keys per query around its insertion point
+ *   zeta_topk_attn_fwd  -> Cauchy-softmax attention over the candidates
+ *
+ * Conventions shared by every call:
+ *
+ * - A "segment" is one (batch, head) pair; B*H segments are independent and
+ *   each holds N positions.  Tensors are dense, row-major, with no strides:
+ *   q and k are [B][H][N][d_k], v and out are [B][H][N][d_v], codes and
+ *   permutations are [B*H][N], idx is [B*H][N][topk].
+ * - Every pointer argument is device memory owned by the caller (the library
+ *   allocates nothing and keeps no state).  Workspace buffers are caller
+ *   supplied; their size comes from zeta_workspace_size.
+ * - Every call validates its arguments on the host, enqueues its kernels on
+ *   `stream` and returns without synchronising.  Faults inside a kernel
+ *   surface at the caller's next synchronisation.  A launch failure reported
+ *   by the runtime maps to ZETA_ERR_HIP.
+ * - Validation failures return before any GPU work is enqueued and before
+ *   any HIP runtime call; nothing is printed and no exception crosses the ABI.
+ * - Calls on distinct streams with distinct buffers may run concurrently.
+ * - Input floating-point values must be finite.
+ */
+#ifndef ZETA_H
+#define ZETA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ZETA_OK = 0,
+  ZETA_ERR_INVALID_ARG = 1, /* null pointer, size out of range, eps <= 0, aliasing */
+  ZETA_ERR_UNSUPPORTED = 2, /* valid but not compiled: d_k > 8, bits > 24, d_v, dtype, topk > 1024 */
+  ZETA_ERR_WORKSPACE = 3,   /* workspace null or smaller than the call needs */
+  ZETA_ERR_HIP = 4          /* the HIP runtime reported a launch error */
+} zeta_status_t;
+
+typedef enum { ZETA_F32 = 0, ZETA_BF16 = 1 } zeta_dtype_t;
+
+/* Largest supported values of the size parameters. */
+#define ZETA_MAX_DK 8
+#define ZETA_MAX_TOPK 1024
+#define ZETA_MAX_BITS 24 /* 2^bits - 1 and every grid coordinate exact in float32 */
+
+/*
+ * zeta_morton_encode -- Z-order codes of queries and keys (Section 3.1,
+ * Z-order curves and equation Z; Section 3.2.2 maps queries and keys into the
+ * same one-dimensional space).
+ *
+ * Each coordinate is discretised onto a grid of 2^bits cells,
+ *   code_a = clamp(floor((x_a - lo_a) * (2^bits - 1) / (hi_a - lo_a)), 0, 2^bits - 1),
+ * evaluated in float32 with one IEEE rounding per operation (subtract,
+ * multiply, divide, floor; no fused multiply-add), and 0 when hi_a <= lo_a.
+ * The d_k grid coordinates are then interleaved most significant bit first,
+ * axis 0 first within each group of d_k bits: bit s of coordinate a goes to
+ * bit d_k*s + (d_k - 1 - a) of the code.
+ *
+ *   q, k        [B][H][N][d_k] of `dtype` (float32, or bfloat16 bit patterns)
+ *   range_lohi  optional float32 [B*H][2][d_k]: per segment, lo then hi per
+ *               axis.  NULL selects the joint min/max over the segment's
+ *               queries and keys.  Values outside a given range clamp.
+ *   range_out   optional float32 [B*H][2][d_k]: receives the range used.
+ *   q_codes, k_codes  uint32 [B*H][N] outputs.
+ *   workspace   at least zeta_workspace_size(...) bytes (used only when
+ *               range_lohi is NULL).
+ *
+ * Requires 1 <= d_k <= ZETA_MAX_DK, 1 <= bits <= ZETA_MAX_BITS, d_k * bits <= 32,
+ * B, H, N >= 1 and B*H*N < 2^31.  Outputs must not overlap the inputs.
+ */
+zeta_status_t zeta_morton_encode(const void* q, const void* k, zeta_dtype_t dtype, int64_t B,
+                                 int64_t H, int64_t N, int d_k, int bits,
+                                 const float* range_lohi, float* range_out, uint32_t* q_codes,
+                                 uint32_t* k_codes, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/*
+ * zeta_sort_keys -- sort each segment's key codes ascending (Section 3.2.2,
+ * keys sorted in the one-dimensional space; Algorithm 1, Step 2; Appendix B
+ * names a radix sort).  Equal codes keep ascending position order (the sort is
+ * stable), so the result is fully determined.
+ *
+ *   k_codes       uint32 [n_segments][N], every code below 2^code_bits.
+ *   sorted_codes  uint32 [n_segments][N] output: k_codes[perm] per segment.
+ *   perm          int32  [n_segments][N] output: original positions.
+ *   code_bits     1..32, the number of significant low bits of each code.
+ *
+ * Outputs must not overlap k_codes.
+ */
+zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_t N, int code_bits,
+                             uint32_t* sorted_codes, int32_t* perm, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * zeta_select_topk -- candidate keys of every query (Section 3.2.2: the
+ * insertion point of the query's code among the sorted keys by binary search,
+ * then a window of k keys centred on it, with causal masking restricting each
+ * query to past keys; Algorithm 1, Steps 3-5).
+ *
+ * For query i the pool is {0..i} when causal (the diagonal included) and all
+ * N keys otherwise.  Let T be the pool in (code, position) order, L = |pool|,
+ * p = number of pool keys whose code is below the query's code,
+ * m = min(topk, L) and s = min(max(p - floor(topk/2), 0), L - m).  Then
+ * idx[seg][i][0..m) = positions of T[s .. s+m) in that order, and the rest of
+ * the row is -1.  The result is unique.
+ *
+ *   q_codes       uint32 [n_segments][N]
+ *   sorted_codes  uint32 [n_segments][N], perm int32 [n_segments][N]: the
+ *                 outputs of zeta_sort_keys for the same key codes.
+ *   idx           int32 [n_segments][N][topk] output.
+ *   topk          1..ZETA_MAX_TOPK; causal 0 or 1.
+ */
+zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes,
+                               const int32_t* perm, int64_t n_segments, int64_t N, int topk,
+                               int causal, int32_t* idx, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * zeta_topk_attn_fwd -- Adaptive Cauchy-softmax attention over each query's
+ * candidates (Section 3.3, equation cauchy; Section 3.4; Appendix E.1):
+ *   S_ij = 1 / (||q_i - k_j||^2 + eps)  for j in idx[i] (entries -1 skipped),
+ *   o_i  = sum_j S_ij v_j / sum_j S_ij.
+ * Distances use the unquantised q and k.  Accumulation is float32; a
+ * bfloat16 output is rounded to nearest even.  A row whose idx holds no
+ * valid entry is written as zeros.
+ *
+ *   q, k   [B][H][N][d_k], v [B][H][N][d_v], out [B][H][N][d_v], all `dtype`.
+ *   idx    int32 [B*H][N][topk]; valid entries (0 <= j < N) first, then -1.
+ *   eps    gamma^2: finite and > 0.
+ *
+ * Supported d_v: 32, 64, 128, 256.  out must not overlap the inputs.
+ */
+zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
+                                 int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
+                                 const int32_t* idx, float eps, void* out, hipStream_t stream);
+
+/*
+ * zeta_workspace_size -- bytes of device workspace that each of
+ * zeta_morton_encode, zeta_sort_keys and zeta_select_topk needs for this
+ * shape (the maximum over the three; one buffer serves all of them when they
+ * run in order on one stream).  Returns 0 for invalid shapes.
+ */
+size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk,
+                           int causal);
+
+/* Static, human-readable name of a status code. */
+const char* zeta_status_string(zeta_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ZETA_H */

@@ -1,0 +1,21 @@
+"""ZETA Z-order top-k attention forward for AMD Instinct MI355X (gfx950).
+
+The compute lives in ``libzeta.so`` (hand-written HIP kernels behind the C ABI
+of ``include/zeta.h``); ``zeta`` is its thin Python binding.
+"""
+
+from .zeta import (  # noqa: F401
+    EXPORTED,
+    ZetaError,
+    alloc_buffers,
+    forward,
+    library_path,
+    load_library,
+    workspace_for,
+    zeta_morton_encode,
+    zeta_select_topk,
+    zeta_sort_keys,
+    zeta_status_string,
+    zeta_topk_attn_fwd,
+    zeta_workspace_size,
+)

@@ -1,0 +1,195 @@
+// Adaptive Cauchy-softmax attention over each query's selected keys
+// (Section 3.3, equation cauchy; Section 3.4; Appendix E.1 steps 1-4):
+//   S_ij = 1 / (||q_i - k_j||^2 + eps),  o_i = sum_j S_ij v_j / sum_j S_ij.
+//
+// One wavefront per query.  d_k is 3, so scores are a handful of scalar FMAs
+// per candidate and there is no dense contraction for the matrix cores: the
+// kernel is a bandwidth-bound gather of k value rows per query.
+//   Phase 1: lane c takes candidates c, c+64, ...: reads the index, gathers
+//            the key row, computes S_ij in float32 and stages (j, S_ij) in LDS;
+//            a wavefront sum gives the normaliser.
+//   Phase 2: the wavefront splits into groups of LPR lanes, LPR = bytes per
+//            value row / 16, so one 16-byte load per lane moves 64/LPR whole
+//            rows per instruction; groups stride over the candidates, eight
+//            rows in flight per lane, accumulating in float32.
+//   Phase 3: xor-shuffles fold the groups; the first group scales by the
+//            normaliser and stores the row (bfloat16 rounded to nearest even).
+#include "device_common.h"
+#include "kernels.h"
+#include "layout.h"
+
+namespace zeta {
+namespace {
+
+template <typename T>
+struct Vec16;  // one 16-byte lane load of a value row, widened to float32
+
+template <>
+struct Vec16<float> {
+  static constexpr int kElems = 4;
+  __device__ __forceinline__ static void load(const float* p, float* f) {
+    const float4 x = *reinterpret_cast<const float4*>(p);
+    f[0] = x.x;
+    f[1] = x.y;
+    f[2] = x.z;
+    f[3] = x.w;
+  }
+  __device__ __forceinline__ static void store(float* p, const float* f) {
+    *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
+  }
+};
+
+template <>
+struct Vec16<uint16_t> {
+  static constexpr int kElems = 8;
+  __device__ __forceinline__ static void load(const uint16_t* p, float* f) {
+    const uint4 x = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ __forceinline__ static void store(uint16_t* p, const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = uint32_t(float_to_bf16_bits(f[2 * i])) | (uint32_t(float_to_bf16_bits(f[2 * i + 1])) << 16);
+    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+
+template <typename T, int DV>
+__global__ void __launch_bounds__(kAttWavesPerBlock * 64)
+    attend_kernel(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                  const int32_t* __restrict__ idx, int64_t total, int64_t N, int dk, int topk, float eps,
+                  T* __restrict__ out) {
+  constexpr int kE = Vec16<T>::kElems;        // elements per lane load
+  constexpr int kLpr = DV / kE;               // lanes per value row
+  constexpr int kGroups = 64 / kLpr;          // rows per wavefront load
+  constexpr int kUnroll = 8;                  // rows in flight per lane
+  static_assert(kLpr >= 1 && kLpr <= 64 && 64 % kLpr == 0, "row must split evenly over lanes");
+
+  extern __shared__ unsigned char s_raw[];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int32_t* s_j = reinterpret_cast<int32_t*>(s_raw) + wave * 2 * topk;
+  float* s_w = reinterpret_cast<float*>(s_j + topk);
+  const int grp = lane / kLpr;
+  const int sub = lane - grp * kLpr;
+
+  for (int64_t g = int64_t(blockIdx.x) * kAttWavesPerBlock + wave; g < total;
+       g += int64_t(gridDim.x) * kAttWavesPerBlock) {
+    const int64_t seg = g / N;
+    const T* kseg = k + seg * N * dk;
+    const T* vseg = v + seg * N * DV;
+
+    float qv[kMaxDk];
+#pragma unroll
+    for (int a = 0; a < kMaxDk; ++a) qv[a] = a < dk ? Elem<T>::load(q + g * dk + a) : 0.0f;
+
+    // Phase 1: scores.
+    float zsum = 0.0f;
+    int m = 0;  // one past the last valid slot
+    const int32_t* irow = idx + g * topk;
+    for (int c = lane; c < topk; c += 64) {
+      const int32_t j = irow[c];
+      const bool ok = j >= 0 && j < N;
+      float s = 0.0f;
+      if (ok) {
+        float d2 = 0.0f;
+        for (int a = 0; a < dk; ++a) {
+          const float diff = qv[a] - Elem<T>::load(kseg + int64_t(j) * dk + a);
+          d2 += diff * diff;
+        }
+        s = 1.0f / (d2 + eps);
+        m = c + 1;
+      }
+      s_j[c] = ok ? j : 0;
+      s_w[c] = s;
+      zsum += s;
+    }
+    zsum = wave_sum(zsum);
+    m = wave_max(m);
+    wave_lds_sync();
+
+    // Phase 2: weighted gather of value rows.
+    float acc[kE];
+#pragma unroll
+    for (int e = 0; e < kE; ++e) acc[e] = 0.0f;
+    const T* vsub = vseg + sub * kE;
+    int c = grp;
+    for (; c + (kUnroll - 1) * kGroups < m; c += kUnroll * kGroups) {
+      float rowv[kUnroll][kE];
+      float wv[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int cc = c + u * kGroups;
+        wv[u] = s_w[cc];
+        Vec16<T>::load(vsub + int64_t(s_j[cc]) * DV, rowv[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+        for (int e = 0; e < kE; ++e) acc[e] += wv[u] * rowv[u][e];
+    }
+    for (; c < m; c += kGroups) {
+      float rowv[kE];
+      const float w = s_w[c];
+      Vec16<T>::load(vsub + int64_t(s_j[c]) * DV, rowv);
+#pragma unroll
+      for (int e = 0; e < kE; ++e) acc[e] += w * rowv[e];
+    }
+
+    // Phase 3: fold the groups and store.
+#pragma unroll
+    for (int off = kLpr; off < 64; off <<= 1)
+#pragma unroll
+      for (int e = 0; e < kE; ++e) acc[e] += __shfl_xor(acc[e], off, 64);
+    if (grp == 0) {
+      const float inv = zsum > 0.0f ? 1.0f / zsum : 0.0f;
+#pragma unroll
+      for (int e = 0; e < kE; ++e) acc[e] *= inv;
+      Vec16<T>::store(out + g * DV + sub * kE, acc);
+    }
+    wave_lds_sync();
+  }
+}
+
+template <typename T, int DV>
+hipError_t launch_attend_t(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk,
+                           int topk, const int32_t* idx, float eps, void* out, hipStream_t stream) {
+  const int64_t total = S * N;
+  const int64_t want = ceil_div(total, kAttWavesPerBlock);
+  const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
+  const size_t lds = size_t(kAttWavesPerBlock) * 2 * topk * 4;
+  hipLaunchKernelGGL((attend_kernel<T, DV>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx,
+                     total, N, dk, topk, eps, static_cast<T*>(out));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool attend_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 256; }
+
+hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
+                         int64_t N, int dk, int dv, int topk, const int32_t* idx, float eps, void* out,
+                         hipStream_t stream) {
+#define ZETA_ATTEND_CASE(DVV)                                                                          \
+  case DVV:                                                                                            \
+    return is_bf16 ? launch_attend_t<uint16_t, DVV>(q, k, v, S, N, dk, topk, idx, eps, out, stream)   \
+                   : launch_attend_t<float, DVV>(q, k, v, S, N, dk, topk, idx, eps, out, stream);
+  switch (dv) {
+    ZETA_ATTEND_CASE(32)
+    ZETA_ATTEND_CASE(64)
+    ZETA_ATTEND_CASE(128)
+    ZETA_ATTEND_CASE(256)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef ZETA_ATTEND_CASE
+}
+
+}  // namespace zeta

@@ -1,0 +1,170 @@
+// Z-order encoding of queries and keys (Section 3.1, equation Z).
+//
+// Two kernels:
+//  1. range_partial: per (segment, chunk of rows) min/max of every axis over
+//     the chunk's query and key rows.  Consecutive threads read consecutive
+//     elements; the block is 64*d_k threads so each thread stays on one axis.
+//  2. encode: every block first folds its segment's partial ranges (a few
+//     dozen floats), then quantises and interleaves 256 query rows and 256 key
+//     rows.  Quantisation is float32 with one rounding per operation, matching
+//     the definition bit for bit.
+#include "device_common.h"
+#include "kernels.h"
+#include "layout.h"
+
+namespace zeta {
+namespace {
+
+template <typename T>
+__global__ void range_partial_kernel(const T* __restrict__ q, const T* __restrict__ k, int64_t N,
+                                     int dk, int64_t chunks, float* __restrict__ partial) {
+  const int64_t seg = blockIdx.x / chunks;
+  const int64_t chunk = blockIdx.x % chunks;
+  const int64_t r0 = chunk * kEncRowsPerChunk;
+  const int64_t r1 = (r0 + kEncRowsPerChunk < N) ? r0 + kEncRowsPerChunk : N;
+  const int tid = threadIdx.x;  // blockDim.x == 64 * dk
+  const int64_t e_end = r1 * dk;
+  const int64_t stride = int64_t(blockDim.x);
+  const T* qs = q + seg * N * dk;
+  const T* ks = k + seg * N * dk;
+  float lo = __builtin_huge_valf(), hi = -__builtin_huge_valf();
+  for (int64_t e = r0 * dk + tid; e < e_end; e += stride) {
+    float a = Elem<T>::load(qs + e);
+    float b = Elem<T>::load(ks + e);
+    lo = fminf(lo, fminf(a, b));
+    hi = fmaxf(hi, fmaxf(a, b));
+  }
+  __shared__ float s_lo[64 * kMaxDk];
+  __shared__ float s_hi[64 * kMaxDk];
+  s_lo[tid] = lo;
+  s_hi[tid] = hi;
+  __syncthreads();
+  if (tid < dk) {
+    float l = s_lo[tid], h = s_hi[tid];
+    for (int t = tid + dk; t < int(blockDim.x); t += dk) {
+      l = fminf(l, s_lo[t]);
+      h = fmaxf(h, s_hi[t]);
+    }
+    float* out = partial + (seg * chunks + chunk) * 2 * dk;
+    out[tid] = l;
+    out[dk + tid] = h;
+  }
+}
+
+// Grid coordinate of one value: floor((x - lo) * (2^bits - 1) / (hi - lo)),
+// clamped, in float32 with one rounding per operation.
+__device__ __forceinline__ uint32_t quantise(float x, float lo, float hi, int bits) {
+#pragma clang fp contract(off)
+  const uint32_t top = (1u << bits) - 1u;
+  const float den = hi - lo;
+  if (!(den > 0.0f)) return 0u;
+  const float t = x - lo;
+  const float u = t * float(top);
+  const float w = __fdiv_rn(u, den);
+  const float f = floorf(w);
+  if (!(f > 0.0f)) return 0u;
+  if (f >= float(top)) return top;
+  return uint32_t(f);
+}
+
+// Spread the low 10 bits of x to every third bit position.
+__device__ __forceinline__ uint32_t spread3(uint32_t x) {
+  x &= 0x3FFu;
+  x = (x | (x << 16)) & 0x030000FFu;
+  x = (x | (x << 8)) & 0x0300F00Fu;
+  x = (x | (x << 4)) & 0x030C30C3u;
+  x = (x | (x << 2)) & 0x09249249u;
+  return x;
+}
+
+template <typename T>
+__device__ __forceinline__ uint32_t encode_row(const T* row, const float* lo, const float* hi, int dk,
+                                               int bits) {
+  if (dk == 3) {
+    uint32_t c0 = quantise(Elem<T>::load(row + 0), lo[0], hi[0], bits);
+    uint32_t c1 = quantise(Elem<T>::load(row + 1), lo[1], hi[1], bits);
+    uint32_t c2 = quantise(Elem<T>::load(row + 2), lo[2], hi[2], bits);
+    return (spread3(c0) << 2) | (spread3(c1) << 1) | spread3(c2);
+  }
+  uint32_t z = 0;
+  for (int a = 0; a < dk; ++a) {
+    const uint32_t c = quantise(Elem<T>::load(row + a), lo[a], hi[a], bits);
+    for (int s = 0; s < bits; ++s) z |= ((c >> s) & 1u) << (dk * s + (dk - 1 - a));
+  }
+  return z;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) encode_kernel(const T* __restrict__ q, const T* __restrict__ k,
+                                                     int64_t N, int dk, int bits,
+                                                     const float* __restrict__ partial, int64_t chunks,
+                                                     const float* __restrict__ range_lohi,
+                                                     float* __restrict__ range_out,
+                                                     uint32_t* __restrict__ q_codes,
+                                                     uint32_t* __restrict__ k_codes,
+                                                     int64_t blocks_per_seg) {
+  const int64_t seg = blockIdx.x / blocks_per_seg;
+  const int64_t blk = blockIdx.x % blocks_per_seg;
+  __shared__ float s_lo[kMaxDk], s_hi[kMaxDk];
+  const int tid = threadIdx.x;
+  if (tid < dk) {
+    float lo, hi;
+    if (range_lohi != nullptr) {
+      lo = range_lohi[seg * 2 * dk + tid];
+      hi = range_lohi[seg * 2 * dk + dk + tid];
+    } else {
+      lo = __builtin_huge_valf();
+      hi = -__builtin_huge_valf();
+      const float* p = partial + seg * chunks * 2 * dk;
+      for (int64_t c = 0; c < chunks; ++c) {
+        lo = fminf(lo, p[c * 2 * dk + tid]);
+        hi = fmaxf(hi, p[c * 2 * dk + dk + tid]);
+      }
+    }
+    s_lo[tid] = lo;
+    s_hi[tid] = hi;
+    if (range_out != nullptr && blk == 0) {
+      range_out[seg * 2 * dk + tid] = lo;
+      range_out[seg * 2 * dk + dk + tid] = hi;
+    }
+  }
+  __syncthreads();
+  const int64_t r = blk * kEncRowsPerBlock + tid;
+  if (r < N) {
+    const int64_t off = seg * N + r;
+    q_codes[off] = encode_row(q + off * dk, s_lo, s_hi, dk, bits);
+    k_codes[off] = encode_row(k + off * dk, s_lo, s_hi, dk, bits);
+  }
+}
+
+template <typename T>
+hipError_t launch_encode_t(const T* q, const T* k, int64_t S, int64_t N, int dk, int bits,
+                           const float* range_lohi, float* range_out, uint32_t* q_codes,
+                           uint32_t* k_codes, void* workspace, hipStream_t stream) {
+  const EncodeWs ws = encode_ws(S, N, dk);
+  float* partial = nullptr;
+  if (range_lohi == nullptr) {
+    partial = reinterpret_cast<float*>(static_cast<char*>(workspace) + ws.partial_off);
+    hipLaunchKernelGGL(range_partial_kernel<T>, dim3(unsigned(S * ws.chunks)), dim3(64 * dk), 0,
+                       stream, q, k, N, dk, ws.chunks, partial);
+  }
+  const int64_t bps = ceil_div(N, kEncRowsPerBlock);
+  hipLaunchKernelGGL(encode_kernel<T>, dim3(unsigned(S * bps)), dim3(unsigned(kEncRowsPerBlock)), 0,
+                     stream, q, k, N, dk, bits, partial, ws.chunks, range_lohi, range_out, q_codes,
+                     k_codes, bps);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_encode(const void* q, const void* k, bool is_bf16, int64_t S, int64_t N, int dk,
+                         int bits, const float* range_lohi, float* range_out, uint32_t* q_codes,
+                         uint32_t* k_codes, void* workspace, hipStream_t stream) {
+  if (is_bf16)
+    return launch_encode_t(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), S, N, dk,
+                           bits, range_lohi, range_out, q_codes, k_codes, workspace, stream);
+  return launch_encode_t(static_cast<const float*>(q), static_cast<const float*>(k), S, N, dk, bits,
+                         range_lohi, range_out, q_codes, k_codes, workspace, stream);
+}
+
+}  // namespace zeta

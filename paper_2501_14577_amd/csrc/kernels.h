@@ -1,0 +1,33 @@
+// Kernel launchers (one translation unit per step).  Each enqueues its kernels
+// on `stream` and returns the runtime's launch status.  Arguments have already
+// been validated by the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace zeta {
+
+// Encode: optional joint-range reduction, then quantise + interleave.
+// is_bf16: q and k hold bfloat16 bit patterns, else float32.
+hipError_t launch_encode(const void* q, const void* k, bool is_bf16, int64_t S, int64_t N, int dk,
+                         int bits, const float* range_lohi, float* range_out, uint32_t* q_codes,
+                         uint32_t* k_codes, void* workspace, hipStream_t stream);
+
+// Stable LSD radix sort of each segment's codes.
+hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_bits,
+                       uint32_t* sorted_codes, int32_t* perm, void* workspace, hipStream_t stream);
+
+// Causal prefix lists (when needed) and the window of every query.
+hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                         int64_t S, int64_t N, int topk, bool causal, int32_t* idx, void* workspace,
+                         hipStream_t stream);
+
+// Cauchy-softmax attention over the selected rows.
+hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
+                         int64_t N, int dk, int dv, int topk, const int32_t* idx, float eps, void* out,
+                         hipStream_t stream);
+
+bool attend_supports(int dv);
+
+}  // namespace zeta

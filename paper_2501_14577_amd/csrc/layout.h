@@ -1,0 +1,133 @@
+// Host-side shape arithmetic shared by argument validation, workspace sizing
+// and the kernel launchers.  Pure C++: no HIP types, no device code.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace zeta {
+
+constexpr int kWave = 64;
+constexpr int kMaxDk = 8;       // largest d_k compiled
+constexpr int kMaxTopk = 1024;  // largest k compiled
+constexpr int kMaxBits = 24;    // grid cells per axis stay exact in float32
+
+// ---- encode ---------------------------------------------------------------
+// Rows of q (and of k) reduced by one block of the range kernel.
+constexpr int64_t kEncRowsPerChunk = 2048;
+// Rows of q (and of k) encoded by one block of the encode kernel.
+constexpr int64_t kEncRowsPerBlock = 256;
+
+// ---- sort -----------------------------------------------------------------
+// Keys per tile of the radix passes: 4 waves x 16 chunks of 64 keys.
+constexpr int kSortThreads = 256;
+constexpr int kSortChunks = 16;
+constexpr int64_t kSortTile = int64_t(kSortThreads) * kSortChunks;
+constexpr int kRadixMax = 256;  // digits of at most 8 bits
+
+// ---- select ---------------------------------------------------------------
+constexpr int kSelWavesPerBlock = 4;
+constexpr int kMaxLevels = 32;
+
+// ---- attend ---------------------------------------------------------------
+constexpr int kAttWavesPerBlock = 4;
+
+inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Smallest t with 2^t >= x (x >= 1).
+inline int ceil_log2(int64_t x) {
+  int t = 0;
+  while ((int64_t(1) << t) < x) ++t;
+  return t;
+}
+
+struct SortPlan {
+  int passes;      // radix passes
+  int digit_bits;  // bits per pass (the last pass may use fewer)
+  int64_t tiles;   // tiles per segment
+};
+
+inline SortPlan sort_plan(int64_t N, int code_bits) {
+  SortPlan p;
+  p.passes = (code_bits + 7) / 8;
+  p.digit_bits = (code_bits + p.passes - 1) / p.passes;
+  p.tiles = ceil_div(N, kSortTile);
+  return p;
+}
+
+// Doubling prefix lists used by causal selection.  List F_t holds the keys at
+// positions below 2^t in (code, position) order, for t0 <= t <= t_hi, where
+// 2^t0 >= topk and 2^t_hi < N.  F_t starts at entry 2^t - 2^t0 of its
+// segment's region of `cap` entries.  A query at position i reads
+// F_{max(t0, bitlen(i))} when that level exists and the full sorted list
+// otherwise; either list contains its whole causal pool and at least half of
+// the list's entries belong to the pool (or the list has under 2*topk entries).
+struct ListPlan {
+  int t0;
+  int t_hi;
+  int levels;   // t_hi - t0 + 1, or 0 when no list is needed
+  int64_t cap;  // entries per segment
+};
+
+inline ListPlan list_plan(int64_t N, int topk) {
+  ListPlan p;
+  p.t0 = ceil_log2(topk);
+  p.t_hi = ceil_log2(N) - 1;
+  if (p.t0 <= p.t_hi) {
+    p.levels = p.t_hi - p.t0 + 1;
+    p.cap = (int64_t(1) << (p.t_hi + 1)) - (int64_t(1) << p.t0);
+  } else {
+    p.levels = 0;
+    p.cap = 0;
+  }
+  return p;
+}
+
+// ---- workspace layouts (byte offsets into the caller's buffer) ------------
+
+struct EncodeWs {
+  int64_t chunks;
+  size_t partial_off, bytes;
+};
+inline EncodeWs encode_ws(int64_t S, int64_t N, int dk) {
+  EncodeWs w;
+  w.chunks = ceil_div(N, kEncRowsPerChunk);
+  w.partial_off = 0;
+  w.bytes = align_up(size_t(S) * size_t(w.chunks) * 2 * size_t(dk) * sizeof(float));
+  return w;
+}
+
+struct SortWs {
+  size_t hist_off, keys_off, pos_off, bytes;
+};
+inline SortWs sort_ws(int64_t S, int64_t N, int code_bits) {
+  SortPlan p = sort_plan(N, code_bits);
+  SortWs w;
+  w.hist_off = 0;
+  w.keys_off = align_up(size_t(S) * size_t(p.tiles) * kRadixMax * sizeof(uint32_t));
+  size_t buf = p.passes > 1 ? align_up(size_t(S) * size_t(N) * sizeof(uint32_t)) : 0;
+  w.pos_off = w.keys_off + buf;
+  w.bytes = w.pos_off + buf;
+  return w;
+}
+
+struct SelectWs {
+  size_t cnt_off, codes_off, pos_off, bytes;
+};
+inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
+  SelectWs w;
+  w.cnt_off = w.codes_off = w.pos_off = w.bytes = 0;
+  if (!causal) return w;
+  ListPlan lp = list_plan(N, topk);
+  if (lp.levels == 0) return w;
+  int64_t tiles = ceil_div(N, kSortTile);
+  w.codes_off = align_up(size_t(S) * size_t(tiles) * kMaxLevels * sizeof(uint32_t));
+  size_t buf = align_up(size_t(S) * size_t(lp.cap) * sizeof(uint32_t));
+  w.pos_off = w.codes_off + buf;
+  w.bytes = w.pos_off + buf;
+  return w;
+}
+
+}  // namespace zeta

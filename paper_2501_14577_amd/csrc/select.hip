@@ -1,0 +1,292 @@
+// Candidate window of every query (Section 3.2.2: binary search for the
+// query's insertion point among the sorted keys it may see, then a window of
+// k keys centred there; Algorithm 1, Steps 3-5).
+//
+// Causal pools {0..i} differ per query, so the window cannot be cut from the
+// full sorted list directly.  Instead of the paper's fixed chunks (which pick
+// a different, coarser pool), the keys are re-filed into doubling prefix
+// lists: F_t holds the keys at positions < 2^t in (code, position) order, for
+// 2^t0 >= k and 2^t < N.  Query i searches F_t with t = max(t0, bitlen(i))
+// (or the full list when no such level exists).  That list holds the whole
+// pool, in pool order, and at least half of its entries are in the pool, so
+// the wavefront that serves the query skips at most as many entries as it
+// keeps.  Filtering F_t by position <= i gives exactly the pool's order, so
+// the result is the definition's, not an approximation of it.
+//
+// Kernels:
+//   list_count:   per tile of the sorted list, how many keys fall in each F_t;
+//   list_scatter: stable compaction of each tile into every F_t it feeds
+//                 (one ballot per level and 64 keys; earlier tiles' counts
+//                 give the base);
+//   select:       one wavefront per query: a 64-way search for the insertion
+//                 point (three rounds for 2^16 keys), then ballot-compacted
+//                 scans to the right and left collecting the in-pool keys,
+//                 staged in LDS and written as one coalesced row.
+#include "device_common.h"
+#include "kernels.h"
+#include "layout.h"
+
+namespace zeta {
+namespace {
+
+__device__ __forceinline__ int bit_length(uint32_t x) { return x ? 32 - __clz(int(x)) : 0; }
+
+__global__ void __launch_bounds__(kSortThreads)
+    list_count_kernel(const int32_t* __restrict__ perm, int64_t N, int64_t tiles, int t0, int levels,
+                      uint32_t* __restrict__ cnt) {
+  const int64_t seg = blockIdx.x / tiles;
+  const int64_t tile = blockIdx.x % tiles;
+  const int tid = threadIdx.x;
+  __shared__ uint32_t h[kMaxLevels + 1];  // keys per bit length of their position
+  if (tid <= kMaxLevels) h[tid] = 0;
+  __syncthreads();
+  const int64_t e0 = tile * kSortTile;
+  const int64_t e1 = (e0 + kSortTile < N) ? e0 + kSortTile : N;
+  const int32_t* ps = perm + seg * N;
+  for (int64_t e = e0 + tid; e < e1; e += kSortThreads) atomicAdd(&h[bit_length(uint32_t(ps[e]))], 1u);
+  __syncthreads();
+  if (tid < levels) {
+    // Keys with position < 2^t are those whose bit length is <= t.
+    const int t = t0 + tid;
+    uint32_t c = 0;
+    for (int b = 0; b <= t; ++b) c += h[b];
+    cnt[(seg * tiles + tile) * kMaxLevels + tid] = c;
+  }
+}
+
+__global__ void __launch_bounds__(kSortThreads)
+    list_scatter_kernel(const uint32_t* __restrict__ sorted_codes, const int32_t* __restrict__ perm,
+                        int64_t N, int64_t tiles, int t0, int levels, int64_t cap,
+                        const uint32_t* __restrict__ cnt, uint32_t* __restrict__ list_codes,
+                        int32_t* __restrict__ list_pos) {
+  const int64_t seg = blockIdx.x / tiles;
+  const int64_t tile = blockIdx.x % tiles;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  __shared__ uint32_t s_before[kMaxLevels];                 // entries of earlier tiles per level
+  __shared__ uint32_t s_wave[kSortThreads / 64][kMaxLevels];  // per-wave counts, then prefixes
+
+  if (tid < levels) {
+    uint32_t b = 0;
+    const uint32_t* c = cnt + seg * tiles * kMaxLevels + tid;
+    for (int64_t t = 0; t < tile; ++t) b += c[t * kMaxLevels];
+    s_before[tid] = b;
+  }
+  const int64_t seg_off = seg * N;
+  const int64_t first = tile * kSortTile + int64_t(wave) * (kSortChunks * 64);
+  uint32_t code[kSortChunks];
+  int32_t pos[kSortChunks];
+#pragma unroll
+  for (int c = 0; c < kSortChunks; ++c) {
+    const int64_t e = first + c * 64 + lane;
+    const bool valid = e < N;
+    code[c] = valid ? sorted_codes[seg_off + e] : 0u;
+    pos[c] = valid ? perm[seg_off + e] : 0x7FFFFFFF;  // never below any 2^t
+  }
+  for (int l = 0; l < levels; ++l) {
+    const int32_t lim = int32_t(1) << (t0 + l);
+    uint32_t n = 0;
+#pragma unroll
+    for (int c = 0; c < kSortChunks; ++c) n += uint32_t(__popcll(wave_ballot(pos[c] < lim)));
+    if (lane == 0) s_wave[wave][l] = n;
+  }
+  __syncthreads();
+  if (tid < levels) {
+    uint32_t run = s_before[tid];
+#pragma unroll
+    for (int w = 0; w < kSortThreads / 64; ++w) {
+      const uint32_t t = s_wave[w][tid];
+      s_wave[w][tid] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+  uint32_t* lc = list_codes + seg * cap;
+  int32_t* lp = list_pos + seg * cap;
+  for (int l = 0; l < levels; ++l) {
+    const int t = t0 + l;
+    const int32_t lim = int32_t(1) << t;
+    const int64_t list_off = (int64_t(1) << t) - (int64_t(1) << t0);
+    uint32_t run = s_wave[wave][l];
+#pragma unroll
+    for (int c = 0; c < kSortChunks; ++c) {
+      const bool in = pos[c] < lim;
+      const uint64_t bal = wave_ballot(in);
+      if (in) {
+        const int64_t dst = list_off + run + lanes_below(bal);
+        lc[dst] = code[c];
+        lp[dst] = pos[c];
+      }
+      run += uint32_t(__popcll(bal));
+    }
+  }
+}
+
+// First index in codes[0..n) whose code is >= key, found by a wavefront:
+// each round 64 lanes probe evenly spaced entries and the ballot of "probe <
+// key" (a prefix of the lanes, the list being sorted) narrows the range 64x.
+__device__ __forceinline__ int32_t wave_lower_bound(const uint32_t* __restrict__ codes, int32_t n,
+                                                    uint32_t key, int lane) {
+  int32_t lo = 0, hi = n;
+  while (hi > lo) {
+    const int32_t len = hi - lo;
+    const int32_t stride = (len + 63) >> 6;
+    const int32_t x = lo + lane * stride;
+    const bool probe = x < hi;
+    const bool less = probe && codes[x] < key;
+    const int cnt = __popcll(wave_ballot(less));
+    if (cnt == 0) {
+      hi = lo;
+    } else {
+      const int32_t next_hi = lo + cnt * stride;
+      lo = lo + (cnt - 1) * stride + 1;
+      hi = next_hi < hi ? next_hi : hi;
+    }
+  }
+  return lo;
+}
+
+// Scan entries cur, cur+1, ... of pos[0..n) and append up to `need` in-pool
+// ones (position <= limit) to buf[got..].  Returns the new count; `cur` is
+// left just past the last entry taken (or at n).
+__device__ __forceinline__ int scan_right(const int32_t* __restrict__ pos, int32_t n, int32_t limit,
+                                          int32_t& cur, int need, int got, int32_t* buf, int lane) {
+  while (got < need && cur < n) {
+    const int32_t e = cur + lane;
+    const bool inr = e < n;
+    const int32_t pv = inr ? pos[e] : 0;
+    const bool ok = inr && pv <= limit;
+    const uint64_t bal = wave_ballot(ok);
+    const int avail = __popcll(bal);
+    const int want = need - got;
+    const int take = avail < want ? avail : want;
+    const int slot = int(lanes_below(bal));
+    if (ok && slot < take) buf[got + slot] = pv;
+    if (take < avail) {
+      // Stop just past the take-th in-pool entry of this chunk.
+      const uint64_t last = wave_ballot(ok && slot == take - 1);
+      cur = cur + (__ffsll((unsigned long long)last) - 1) + 1;
+    } else {
+      cur = cur + 64 < n ? cur + 64 : n;
+    }
+    got += take;
+  }
+  return got;
+}
+
+// Scan entries cur-1, cur-2, ... and collect up to `need` in-pool entries,
+// nearest first, into buf[cap_end-1], buf[cap_end-2], ... so that the
+// collected run ends at buf[cap_end-1] in ascending list order.
+__device__ __forceinline__ int scan_left(const int32_t* __restrict__ pos, int32_t limit, int32_t cur,
+                                         int need, int32_t* buf, int cap_end, int lane) {
+  int got = 0;
+  while (got < need && cur > 0) {
+    const int32_t start = cur - 64;
+    const int32_t e = start + lane;
+    const bool inr = e >= 0;
+    const int32_t pv = inr ? pos[e] : 0;
+    const bool ok = inr && pv <= limit;
+    const uint64_t bal = wave_ballot(ok);
+    const int avail = __popcll(bal);
+    const int want = need - got;
+    const int take = avail < want ? avail : want;
+    const int from_top = avail - 1 - int(lanes_below(bal));
+    if (ok && from_top < take) buf[cap_end - 1 - (got + from_top)] = pv;
+    got += take;
+    cur = start;
+  }
+  return got;
+}
+
+__global__ void __launch_bounds__(kSelWavesPerBlock * 64)
+    select_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
+                  const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
+                  const int32_t* __restrict__ list_pos, int64_t total, int64_t N, int topk, int causal,
+                  int t0, int t_hi, int64_t cap, int32_t* __restrict__ idx) {
+  extern __shared__ int32_t s_sel[];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int32_t* lbuf = s_sel + wave * 2 * topk;  // left part, filled from its end
+  int32_t* rbuf = lbuf + topk;              // right part, filled from its start
+  const int half = topk / 2;
+
+  for (int64_t g = int64_t(blockIdx.x) * kSelWavesPerBlock + wave; g < total;
+       g += int64_t(gridDim.x) * kSelWavesPerBlock) {
+    const int64_t seg = g / N;
+    const int32_t i = int32_t(g - seg * N);
+    const uint32_t key = q_codes[g];
+
+    const uint32_t* codes = sorted_codes + seg * N;
+    const int32_t* pos = perm + seg * N;
+    int32_t n = int32_t(N);
+    int32_t limit = int32_t(N);  // every position is in the non-causal pool
+    if (causal) {
+      limit = i;
+      const int bl = bit_length(uint32_t(i));
+      const int t = bl > t0 ? bl : t0;
+      if (t <= t_hi) {
+        const int64_t off = seg * cap + ((int64_t(1) << t) - (int64_t(1) << t0));
+        codes = list_codes + off;
+        pos = list_pos + off;
+        n = int32_t(1) << t;
+      }
+    }
+
+    const int32_t p = wave_lower_bound(codes, n, key, lane);
+    // floor(k/2) pool keys before p and the rest from p on, shifted inward
+    // when one side of the pool runs out.
+    const int need_r = topk - half;
+    int32_t cur_r = p;
+    int got_r = scan_right(pos, n, limit, cur_r, need_r, 0, rbuf, lane);
+    const int need_l = half + (need_r - got_r);
+    const int got_l = scan_left(pos, limit, p, need_l, lbuf, topk, lane);
+    if (got_l < need_l && got_r == need_r)
+      got_r = scan_right(pos, n, limit, cur_r, topk - got_l, got_r, rbuf, lane);
+    wave_lds_sync();
+
+    int32_t* row = idx + g * topk;
+    const int total_sel = got_l + got_r;
+    for (int c = lane; c < topk; c += 64) {
+      int32_t v = -1;
+      if (c < got_l)
+        v = lbuf[topk - got_l + c];
+      else if (c < total_sel)
+        v = rbuf[c - got_l];
+      row[c] = v;
+    }
+    wave_lds_sync();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                         int64_t S, int64_t N, int topk, bool causal, int32_t* idx, void* workspace,
+                         hipStream_t stream) {
+  const ListPlan lp = list_plan(N, topk);
+  const SelectWs ws = select_ws(S, N, topk, causal ? 1 : 0);
+  uint32_t* list_codes = nullptr;
+  int32_t* list_pos = nullptr;
+  if (causal && lp.levels > 0) {
+    char* wsb = static_cast<char*>(workspace);
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(wsb + ws.cnt_off);
+    list_codes = reinterpret_cast<uint32_t*>(wsb + ws.codes_off);
+    list_pos = reinterpret_cast<int32_t*>(wsb + ws.pos_off);
+    const int64_t tiles = ceil_div(N, kSortTile);
+    const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
+    hipLaunchKernelGGL(list_count_kernel, grid, block, 0, stream, perm, N, tiles, lp.t0, lp.levels, cnt);
+    hipLaunchKernelGGL(list_scatter_kernel, grid, block, 0, stream, sorted_codes, perm, N, tiles, lp.t0,
+                       lp.levels, lp.cap, cnt, list_codes, list_pos);
+  }
+  const int64_t total = S * N;
+  const int64_t want = ceil_div(total, kSelWavesPerBlock);
+  const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
+  const size_t lds = size_t(kSelWavesPerBlock) * 2 * topk * sizeof(int32_t);
+  hipLaunchKernelGGL(select_kernel, dim3(blocks), dim3(kSelWavesPerBlock * 64), lds, stream, q_codes,
+                     sorted_codes, perm, list_codes, list_pos, total, N, topk, causal ? 1 : 0, lp.t0,
+                     lp.t_hi, lp.cap, idx);
+  return hipGetLastError();
+}
+
+}  // namespace zeta

@@ -1,0 +1,160 @@
+// Stable segmented LSD radix sort of (code, position) pairs (Section 3.2.2;
+// Algorithm 1, Step 2; Appendix B sorts the codes with a radix sort).
+//
+// Every segment is cut into tiles of 4096 keys.  One pass over a digit of at
+// most 8 bits runs two kernels:
+//   hist:    per tile, the count of each digit value (LDS atomics);
+//   scatter: per tile, the digit's global base (an exclusive scan over digit
+//            values of the segment totals, plus the counts of earlier tiles),
+//            then a stable rank of every key inside the tile: each wavefront
+//            walks its 1024 keys in order, 64 at a time, finding same-digit
+//            lanes with one ballot per digit bit and counting them with
+//            mbcnt; per-wave running counts live in LDS.
+// A pass preserves the order of equal digits, so after the last pass equal
+// codes are in ascending position order.
+#include "device_common.h"
+#include "kernels.h"
+#include "layout.h"
+
+namespace zeta {
+namespace {
+
+__global__ void __launch_bounds__(kSortThreads)
+    radix_hist_kernel(const uint32_t* __restrict__ keys, int64_t N, int64_t tiles, int shift, int nbits,
+                      uint32_t* __restrict__ hist) {
+  const int64_t seg = blockIdx.x / tiles;
+  const int64_t tile = blockIdx.x % tiles;
+  const int tid = threadIdx.x;
+  __shared__ uint32_t h[kRadixMax];
+  h[tid] = 0;
+  __syncthreads();
+  const uint32_t mask = (1u << nbits) - 1u;
+  const int64_t t0 = tile * kSortTile;
+  const int64_t t1 = (t0 + kSortTile < N) ? t0 + kSortTile : N;
+  const uint32_t* ks = keys + seg * N;
+  for (int64_t e = t0 + tid; e < t1; e += kSortThreads) atomicAdd(&h[(ks[e] >> shift) & mask], 1u);
+  __syncthreads();
+  hist[(seg * tiles + tile) * kRadixMax + tid] = h[tid];
+}
+
+template <bool kHasPos>
+__global__ void __launch_bounds__(kSortThreads)
+    radix_scatter_kernel(const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ pos_in,
+                         int64_t N, int64_t tiles, int shift, int nbits,
+                         const uint32_t* __restrict__ hist, uint32_t* __restrict__ keys_out,
+                         int32_t* __restrict__ pos_out) {
+  const int64_t seg = blockIdx.x / tiles;
+  const int64_t tile = blockIdx.x % tiles;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const uint32_t mask = (1u << nbits) - 1u;
+
+  __shared__ uint32_t s_base[kRadixMax];              // first output slot of each digit in this tile
+  __shared__ uint32_t s_wcnt[kSortThreads / 64][kRadixMax];  // per-wave running / prefix counts
+  __shared__ uint32_t s_scan[4];
+
+  {
+    // Digit totals of the segment and counts of the tiles before this one.
+    const uint32_t* h = hist + seg * tiles * kRadixMax + tid;
+    uint32_t total = 0, before = 0;
+    for (int64_t t = 0; t < tiles; ++t) {
+      const uint32_t c = h[t * kRadixMax];
+      total += c;
+      before += (t < tile) ? c : 0u;
+    }
+    const uint32_t excl = block256_exclusive_scan(total, s_scan);
+    s_base[tid] = excl + before;
+#pragma unroll
+    for (int w = 0; w < kSortThreads / 64; ++w) s_wcnt[w][tid] = 0;
+  }
+  __syncthreads();
+
+  const int64_t seg_off = seg * N;
+  const int64_t first = tile * kSortTile + int64_t(wave) * (kSortChunks * 64);
+  uint32_t key[kSortChunks];
+  int32_t pos[kSortChunks];
+  uint32_t rank[kSortChunks];
+#pragma unroll
+  for (int c = 0; c < kSortChunks; ++c) {
+    const int64_t e = first + c * 64 + lane;
+    const bool valid = e < N;
+    const uint32_t kk = valid ? keys_in[seg_off + e] : 0u;
+    int32_t pp;
+    if (kHasPos)
+      pp = valid ? pos_in[seg_off + e] : 0;
+    else
+      pp = int32_t(e);
+    const uint32_t d = (kk >> shift) & mask;
+    uint64_t peers = wave_ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t ones = wave_ballot(bit);
+      peers &= bit ? ones : ~ones;
+    }
+    const uint32_t below = lanes_below(peers);
+    const uint32_t base = s_wcnt[wave][d];
+    if (valid && below == 0) s_wcnt[wave][d] = base + uint32_t(__popcll(peers));
+    key[c] = kk;
+    pos[c] = pp;
+    rank[c] = base + below;
+  }
+  __syncthreads();
+  {
+    uint32_t run = 0;
+#pragma unroll
+    for (int w = 0; w < kSortThreads / 64; ++w) {
+      const uint32_t t = s_wcnt[w][tid];
+      s_wcnt[w][tid] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < kSortChunks; ++c) {
+    const int64_t e = first + c * 64 + lane;
+    if (e < N) {
+      const uint32_t d = (key[c] >> shift) & mask;
+      const int64_t dst = int64_t(s_base[d]) + s_wcnt[wave][d] + rank[c];
+      keys_out[seg_off + dst] = key[c];
+      pos_out[seg_off + dst] = pos[c];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_bits,
+                       uint32_t* sorted_codes, int32_t* perm, void* workspace, hipStream_t stream) {
+  const SortPlan plan = sort_plan(N, code_bits);
+  const SortWs ws = sort_ws(S, N, code_bits);
+  char* wsb = static_cast<char*>(workspace);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(wsb + ws.hist_off);
+  uint32_t* tmp_keys = reinterpret_cast<uint32_t*>(wsb + ws.keys_off);
+  int32_t* tmp_pos = reinterpret_cast<int32_t*>(wsb + ws.pos_off);
+  const dim3 grid(unsigned(S * plan.tiles)), block(kSortThreads);
+
+  const uint32_t* src_keys = k_codes;
+  const int32_t* src_pos = nullptr;
+  for (int p = 0; p < plan.passes; ++p) {
+    const int shift = p * plan.digit_bits;
+    const int nbits = (code_bits - shift < plan.digit_bits) ? code_bits - shift : plan.digit_bits;
+    // The last pass lands in the caller's outputs; earlier passes alternate.
+    const bool to_out = ((plan.passes - 1 - p) % 2) == 0;
+    uint32_t* dst_keys = to_out ? sorted_codes : tmp_keys;
+    int32_t* dst_pos = to_out ? perm : tmp_pos;
+    hipLaunchKernelGGL(radix_hist_kernel, grid, block, 0, stream, src_keys, N, plan.tiles, shift, nbits,
+                       hist);
+    if (src_pos == nullptr)
+      hipLaunchKernelGGL(radix_scatter_kernel<false>, grid, block, 0, stream, src_keys, src_pos, N,
+                         plan.tiles, shift, nbits, hist, dst_keys, dst_pos);
+    else
+      hipLaunchKernelGGL(radix_scatter_kernel<true>, grid, block, 0, stream, src_keys, src_pos, N,
+                         plan.tiles, shift, nbits, hist, dst_keys, dst_pos);
+    src_keys = dst_keys;
+    src_pos = dst_pos;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace zeta

@@ -1,0 +1,125 @@
+// C ABI of the Z-order top-k attention forward: argument validation on the
+// host, then the kernel launchers.  Validation touches no HIP runtime call, so
+// every error path can be exercised without a GPU.
+#include <math.h>
+
+#include "../../include/zeta.h"
+#include "kernels.h"
+#include "layout.h"
+
+static_assert(ZETA_MAX_DK == zeta::kMaxDk, "d_k limit mismatch");
+static_assert(ZETA_MAX_TOPK == zeta::kMaxTopk, "topk limit mismatch");
+static_assert(ZETA_MAX_BITS == zeta::kMaxBits, "bits limit mismatch");
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;  // B*H*N limit (int32 positions, grid sizes)
+
+bool shape_ok(int64_t S, int64_t N) { return S >= 1 && N >= 1 && N <= kMaxElems && S <= kMaxElems / N; }
+
+bool dtype_known(zeta_dtype_t d) { return d == ZETA_F32 || d == ZETA_BF16; }
+
+zeta_status_t hip_status(hipError_t e) { return e == hipSuccess ? ZETA_OK : ZETA_ERR_HIP; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool bad_count(int64_t B, int64_t H, int64_t N) {
+  if (B < 1 || H < 1 || N < 1) return true;
+  if (B > kMaxElems / H) return true;
+  return !shape_ok(B * H, N);
+}
+
+}  // namespace
+
+extern "C" {
+
+zeta_status_t zeta_morton_encode(const void* q, const void* k, zeta_dtype_t dtype, int64_t B, int64_t H,
+                                 int64_t N, int d_k, int bits, const float* range_lohi, float* range_out,
+                                 uint32_t* q_codes, uint32_t* k_codes, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  if (!q || !k || !q_codes || !k_codes) return ZETA_ERR_INVALID_ARG;
+  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32) return ZETA_ERR_INVALID_ARG;
+  if (q_codes == k_codes) return ZETA_ERR_INVALID_ARG;
+  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
+  if (d_k > zeta::kMaxDk || bits > zeta::kMaxBits) return ZETA_ERR_UNSUPPORTED;
+  const int64_t S = B * H;
+  if (range_lohi == nullptr) {
+    const zeta::EncodeWs ws = zeta::encode_ws(S, N, d_k);
+    if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
+  }
+  return hip_status(zeta::launch_encode(q, k, dtype == ZETA_BF16, S, N, d_k, bits, range_lohi, range_out,
+                                        q_codes, k_codes, workspace, stream));
+}
+
+zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_t N, int code_bits,
+                             uint32_t* sorted_codes, int32_t* perm, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  if (!k_codes || !sorted_codes || !perm) return ZETA_ERR_INVALID_ARG;
+  if (!shape_ok(n_segments, N)) return ZETA_ERR_INVALID_ARG;
+  if (code_bits < 1 || code_bits > 32) return ZETA_ERR_INVALID_ARG;
+  if (static_cast<const void*>(k_codes) == static_cast<const void*>(sorted_codes) ||
+      static_cast<const void*>(k_codes) == static_cast<const void*>(perm) ||
+      static_cast<const void*>(sorted_codes) == static_cast<const void*>(perm))
+    return ZETA_ERR_INVALID_ARG;
+  const zeta::SortWs ws = zeta::sort_ws(n_segments, N, code_bits);
+  if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
+  return hip_status(zeta::launch_sort(k_codes, n_segments, N, code_bits, sorted_codes, perm, workspace, stream));
+}
+
+zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                               int64_t n_segments, int64_t N, int topk, int causal, int32_t* idx,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!q_codes || !sorted_codes || !perm || !idx) return ZETA_ERR_INVALID_ARG;
+  if (!shape_ok(n_segments, N)) return ZETA_ERR_INVALID_ARG;
+  if (topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (topk > zeta::kMaxTopk) return ZETA_ERR_UNSUPPORTED;
+  const zeta::SelectWs ws = zeta::select_ws(n_segments, N, topk, causal);
+  if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
+  return hip_status(zeta::launch_select(q_codes, sorted_codes, perm, n_segments, N, topk, causal != 0, idx,
+                                        workspace, stream));
+}
+
+zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
+                                 int64_t H, int64_t N, int d_k, int d_v, int topk, const int32_t* idx,
+                                 float eps, void* out, hipStream_t stream) {
+  if (!q || !k || !v || !idx || !out) return ZETA_ERR_INVALID_ARG;
+  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || d_v < 1 || topk < 1) return ZETA_ERR_INVALID_ARG;
+  if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
+  if (!aligned16(v) || !aligned16(out)) return ZETA_ERR_INVALID_ARG;
+  if (out == q || out == k || out == v) return ZETA_ERR_INVALID_ARG;
+  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
+  if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
+  return hip_status(zeta::launch_attend(q, k, v, dtype == ZETA_BF16, B * H, N, d_k, d_v, topk, idx, eps, out,
+                                        stream));
+}
+
+size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk, int causal) {
+  if (bad_count(B, H, N) || d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32 || topk < 1) return 0;
+  const int64_t S = B * H;
+  size_t bytes = zeta::encode_ws(S, N, d_k).bytes;
+  const size_t sb = zeta::sort_ws(S, N, d_k * bits).bytes;
+  const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
+  if (sb > bytes) bytes = sb;
+  if (lb > bytes) bytes = lb;
+  return bytes;
+}
+
+const char* zeta_status_string(zeta_status_t status) {
+  switch (status) {
+    case ZETA_OK:
+      return "ZETA_OK";
+    case ZETA_ERR_INVALID_ARG:
+      return "ZETA_ERR_INVALID_ARG";
+    case ZETA_ERR_UNSUPPORTED:
+      return "ZETA_ERR_UNSUPPORTED";
+    case ZETA_ERR_WORKSPACE:
+      return "ZETA_ERR_WORKSPACE";
+    case ZETA_ERR_HIP:
+      return "ZETA_ERR_HIP";
+  }
+  return "ZETA_ERR_UNKNOWN";
+}
+
+}  // extern "C"

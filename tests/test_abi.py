@@ -1,0 +1,147 @@
+"""The C ABI library: it loads, exports what include/zeta.h declares, sizes
+workspaces, and rejects bad arguments before any GPU work (no GPU needed).
+
+Every call below breaks exactly one rule and must return before touching the
+HIP runtime; pointers are dummies that the library never dereferences.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2501_14577_amd as zeta
+from paper_2501_14577_amd import zeta as zb
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "zeta.h")
+P = ctypes.c_void_p(0x10000)  # dummy, 256-byte aligned, never dereferenced
+P2 = ctypes.c_void_p(0x20000)
+P3 = ctypes.c_void_p(0x30000)
+P4 = ctypes.c_void_p(0x40000)
+NULL = None
+BIG = 1 << 40
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\S.*?\b(zeta_\w+)\(", text, flags=re.M)))
+
+
+def test_header_declares_the_four_calls_and_helpers():
+    syms = declared_symbols()
+    assert syms == sorted(zeta.EXPORTED), syms
+
+
+def test_library_exports_every_declared_symbol():
+    lib = zeta.load_library()
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_library_is_in_tree():
+    assert os.path.dirname(zeta.library_path()) == os.path.dirname(os.path.abspath(zb.__file__))
+
+
+def test_status_strings():
+    names = ["ZETA_OK", "ZETA_ERR_INVALID_ARG", "ZETA_ERR_UNSUPPORTED", "ZETA_ERR_WORKSPACE", "ZETA_ERR_HIP"]
+    for code, name in enumerate(names):
+        assert zeta.zeta_status_string(code) == name
+    assert zeta.zeta_status_string(99) == "ZETA_ERR_UNKNOWN"
+
+
+def test_workspace_size():
+    ws = zeta.zeta_workspace_size
+    assert ws(0, 1, 10, 3, 10, 4, 1) == 0
+    assert ws(1, 1, 10, 3, 11, 4, 1) == 0  # 33 code bits
+    assert ws(1, 1, 10, 0, 10, 4, 1) == 0
+    assert ws(1, 1, 10, 3, 10, 0, 1) == 0
+    # Long-context shape: the sort's ping-pong buffer (16 x 65536 x 8 B) dominates.
+    big = ws(1, 16, 65536, 3, 6, 128, 1)
+    assert big >= 16 * 65536 * 8
+    assert big % 256 == 0
+    assert ws(1, 16, 65536, 3, 6, 128, 0) <= big
+    # One tiny segment still gets a buffer for the range partials.
+    assert ws(1, 1, 1, 3, 10, 1, 1) > 0
+
+
+def _enc(**kw):
+    a = dict(q=P, k=P2, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, bits=10, range_lohi=NULL,
+             range_out=NULL, q_codes=P3, k_codes=P4, ws=P, ws_bytes=BIG, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_morton_encode(*a.values())
+
+
+def _sort(**kw):
+    a = dict(k_codes=P, S=2, N=100, code_bits=30, sorted_codes=P2, perm=P3, ws=P4, ws_bytes=BIG, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_sort_keys(*a.values())
+
+
+def _sel(**kw):
+    a = dict(q_codes=P, sorted_codes=P2, perm=P3, S=2, N=100, topk=8, causal=1, idx=P4, ws=P, ws_bytes=BIG,
+             stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_select_topk(*a.values())
+
+
+def _att(**kw):
+    a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, idx=P4,
+             eps=0.5, out=ctypes.c_void_p(0x50000), stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_topk_attn_fwd(*a.values())
+
+
+INV, UNS, WSP = zb.ZETA_ERR_INVALID_ARG, zb.ZETA_ERR_UNSUPPORTED, zb.ZETA_ERR_WORKSPACE
+
+ENCODE_CASES = [
+    (dict(q=NULL), INV), (dict(k=NULL), INV), (dict(q_codes=NULL), INV), (dict(k_codes=NULL), INV),
+    (dict(B=0), INV), (dict(H=-1), INV), (dict(N=0), INV), (dict(N=1 << 31), INV), (dict(B=1 << 20, N=1 << 12), INV),
+    (dict(d_k=0), INV), (dict(bits=0), INV), (dict(bits=11), INV), (dict(d_k=4, bits=9), INV),
+    (dict(k_codes=P3), INV), (dict(dtype=7), UNS), (dict(d_k=9, bits=3), UNS), (dict(d_k=1, bits=25), UNS),
+    (dict(ws=NULL), WSP), (dict(ws_bytes=8), WSP),
+]
+
+
+@pytest.mark.parametrize("kw,code", ENCODE_CASES, ids=[str(c[0]) for c in ENCODE_CASES])
+def test_encode_rejects(kw, code):
+    assert _enc(**kw) == code
+
+
+SORT_CASES = [
+    (dict(k_codes=NULL), INV), (dict(sorted_codes=NULL), INV), (dict(perm=NULL), INV),
+    (dict(S=0), INV), (dict(N=0), INV), (dict(N=1 << 31), INV), (dict(code_bits=0), INV), (dict(code_bits=33), INV),
+    (dict(sorted_codes=P), INV), (dict(perm=P), INV), (dict(perm=P2), INV),
+    (dict(ws=NULL), WSP), (dict(ws_bytes=100), WSP),
+]
+
+
+@pytest.mark.parametrize("kw,code", SORT_CASES, ids=[str(c[0]) for c in SORT_CASES])
+def test_sort_rejects(kw, code):
+    assert _sort(**kw) == code
+
+
+SELECT_CASES = [
+    (dict(q_codes=NULL), INV), (dict(sorted_codes=NULL), INV), (dict(perm=NULL), INV), (dict(idx=NULL), INV),
+    (dict(S=0), INV), (dict(N=0), INV), (dict(topk=0), INV), (dict(causal=2), INV),
+    (dict(topk=1025), UNS), (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP),
+]
+
+
+@pytest.mark.parametrize("kw,code", SELECT_CASES, ids=[str(c[0]) for c in SELECT_CASES])
+def test_select_rejects(kw, code):
+    assert _sel(**kw) == code
+
+
+ATTEND_CASES = [
+    (dict(q=NULL), INV), (dict(k=NULL), INV), (dict(v=NULL), INV), (dict(idx=NULL), INV), (dict(out=NULL), INV),
+    (dict(B=0), INV), (dict(N=0), INV), (dict(d_k=0), INV), (dict(d_v=0), INV), (dict(topk=0), INV),
+    (dict(eps=0.0), INV), (dict(eps=-1.0), INV), (dict(eps=float("inf")), INV), (dict(eps=float("nan")), INV),
+    (dict(v=ctypes.c_void_p(0x30008)), INV), (dict(out=ctypes.c_void_p(0x50004)), INV), (dict(out=P3), INV),
+    (dict(dtype=5), UNS), (dict(d_k=9), UNS), (dict(d_v=96), UNS), (dict(d_v=512), UNS), (dict(topk=2000), UNS),
+]
+
+
+@pytest.mark.parametrize("kw,code", ATTEND_CASES, ids=[str(c[0]) for c in ATTEND_CASES])
+def test_attend_rejects(kw, code):
+    assert _att(**kw) == code
