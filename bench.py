@@ -1,0 +1,239 @@
+"""Benchmark of the Z-order top-k attention forward on one MI355X.
+
+One step is the whole forward (encode, sort, select, attend: four C ABI calls
+on one stream) over one batch of the long-context workload (B=1, H=16,
+N=65536, d_k=3, d_v=128, k=128, bf16, 6 bits per axis, causal), with inputs,
+outputs and workspace resident in HBM before timing starts.
+
+Prints one JSON line: query-tokens/s (B*N per second) of the whole step, the
+attend kernel's achieved algorithmic bandwidth against the HBM peak (timed with
+HIP events on the stream it runs on), and the CPU oracle timed on a bounded
+sample of the same workload on the host's cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
+ATTEND_SRC = os.path.join(ROOT, "paper_2501_14577_amd", "csrc", "attend.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_long_context_traffic.txt")
+
+
+def elem_size(dtype: str) -> int:
+    return 2 if dtype == "bf16" else 4
+
+
+def candidates(w: workloads.Workload, causal: bool) -> int:
+    """Exact number of selected (query, key) pairs over the whole batch."""
+    N, k = w.N, w.topk
+    if not causal:
+        return w.segments * N * min(k, N)
+    i = np.arange(N, dtype=np.int64)
+    return int(w.segments * np.minimum(k, i + 1).sum())
+
+
+def attend_bytes(w: workloads.Workload, causal: bool) -> int:
+    """Algorithmic bytes of one attend launch: per query its q row, its k
+    indices and its output row, per selected pair one key row and one value
+    row; no reuse across queries is assumed."""
+    s, d = elem_size(w.dtype), w.dk
+    rows = w.segments * w.N
+    return rows * (d * s + 4 * w.topk + w.dv * s) + candidates(w, causal) * (d * s + w.dv * s)
+
+
+def step_bytes(w: workloads.Workload, causal: bool) -> int:
+    """Algorithmic bytes of the whole step: attend plus, per query row,
+    encode 4*d*s + 8, sort 16 per radix pass and select 4 + 8k."""
+    s, d = elem_size(w.dtype), w.dk
+    passes = (w.code_bits + 7) // 8
+    rows = w.segments * w.N
+    return attend_bytes(w, causal) + rows * ((4 * d * s + 8) + 16 * passes + (4 + 8 * w.topk))
+
+
+def read_traffic(launch_bytes: int):
+    """HBM bytes per attend launch from the committed rocprofv3 counter
+    summary, or None when absent or taken on a different attend source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            key, val = line.split(":", 1)
+            kv[key.strip()] = val.strip()
+    src = hashlib.sha256(open(ATTEND_SRC, "rb").read()).hexdigest()
+    if kv.get("attend_source_sha256") != src:
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w: workloads.Workload, causal: bool, x: dict, heads: int):
+    """The oracle, untuned, on the first ``heads`` (batch 0) segments: the
+    whole forward of each, one after another, in one process.  Scaled to
+    query-tokens/s as rows / H per second (one query token carries H rows)."""
+    import oracle
+
+    S = w.segments
+    heads = max(1, min(heads, S))
+    f = {n: oracle.as_f32(a, w.dtype).reshape(S, w.N, a.shape[-1])[:heads] for n, a in x.items()}
+    t0 = time.perf_counter()
+    oracle.forward(f["q"], f["k"], f["v"], w.topk, workloads.EPS_DEFAULT, causal, w.bits)
+    dt = time.perf_counter() - t0
+    rows = heads * w.N
+    return {
+        "value": rows / w.H / dt,
+        "unit": "query-tokens/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{heads} of {S} segments ({rows} query rows), whole oracle forward "
+                   f"({'causal' if causal else 'non-causal'}), one process, {dt:.1f} s; "
+                   f"scaled as rows/H per second"),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=5, help="workload number (parity cases 1-4, bench 5)")
+    ap.add_argument("--noncausal", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=3,
+                    help="segments in the oracle sample (0 skips the CPU baseline)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run a plain 1 GiB device copy first (for counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: every (batch, head) segment is independent, "
+              "so more GPUs would each run this same single-GPU step on their share.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2501_14577_amd as zeta
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        return 2
+    zeta.load_library()
+    dev = torch.device("cuda:0")
+    w = workloads.CONFIGS[args.config]
+    causal = not args.noncausal and True in w.causal
+    x = workloads.generate(w)
+
+    def to_dev(a):
+        if w.dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    q, k, v = to_dev(x["q"]), to_dev(x["k"]), to_dev(x["v"])
+    tdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    bufs = zeta.alloc_buffers(w.B, w.H, w.N, w.dv, w.topk, tdtype, dev)
+    ws = zeta.workspace_for(w.B, w.H, w.N, w.dk, w.bits, w.topk, causal, dev)
+    eps = workloads.EPS_DEFAULT
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    def step(ev=None):
+        qc, kc = zeta.zeta_morton_encode(q, k, w.bits, q_codes=bufs["q_codes"], k_codes=bufs["k_codes"],
+                                         workspace=ws)
+        sc, perm = zeta.zeta_sort_keys(kc, w.code_bits, sorted_codes=bufs["sorted_codes"], perm=bufs["perm"],
+                                       workspace=ws)
+        idx = zeta.zeta_select_topk(qc, sc, perm, w.topk, causal, idx=bufs["idx"], workspace=ws)
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_topk_attn_fwd(q, k, v, idx, eps, out=bufs["out"])
+        if ev is not None:
+            ev[1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    attend_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    tokens = w.B * w.N
+    a_bytes = attend_bytes(w, causal)
+    achieved = a_bytes / (attend_ms * 1e-3) / 1e9
+    s_bytes = step_bytes(w, causal)
+
+    cpu = None
+    if args.cpu_heads > 0:
+        cpu = cpu_baseline(w, causal, x, args.cpu_heads)
+
+    line = {
+        "metric": "query-tokens/sec for Z-order top-k attn fwd; % of HBM roofline",
+        "value": tokens / (ms_per_step * 1e-3),
+        "unit": "query-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: B={w.B} H={w.H} N={w.N} d_k={w.dk} d_v={w.dv} k={w.topk} {w.dtype} "
+                        f"{w.bits} bits/axis {'causal' if causal else 'non-causal'}",
+            "global_batch": w.B,
+            "seq_len": w.N,
+            "parallelism": "none (1 GPU)",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "attend",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": read_traffic(a_bytes),
+            "algorithmic_bytes_per_launch": a_bytes,
+            "attend_ms": attend_ms,
+        },
+        "step_hbm_frac": s_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "step_algorithmic_bytes": s_bytes,
+        "query_rows_per_s": w.segments * w.N / (ms_per_step * 1e-3),
+        "timed_wall_s": wall,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
