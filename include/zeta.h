@@ -5,7 +5,9 @@
  * The forward pass has four calls, run in this order on one stream:
  *
  *   zeta_morton_encode  -> Z-order codes of queries and keys
- *   zeta_sort_keys      -> keys sorted by code per (batch, head)
+ *   zeta_sort_keys      -> keys sorted by code per (batch, head); called on
+ *                          the query codes too, the permutation is a
+ *                          processing order for the next two calls
  *   zeta_select_topk    -> k candidate keys per query around its insertion point
  *   zeta_topk_attn_fwd  -> Cauchy-softmax attention over the candidates
  *
@@ -118,12 +120,18 @@ zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_
  *   q_codes       uint32 [n_segments][N]
  *   sorted_codes  uint32 [n_segments][N], perm int32 [n_segments][N]: the
  *                 outputs of zeta_sort_keys for the same key codes.
- *   idx           int32 [n_segments][N][topk] output.
+ *   q_order       optional int32 [n_segments][N]: the order in which queries
+ *                 are processed, a permutation of 0..N-1 per segment (NULL:
+ *                 position order).  It changes no result; the queries' own
+ *                 codes in ascending order (zeta_sort_keys applied to q_codes)
+ *                 give neighbouring queries overlapping windows and make the
+ *                 call faster.  Entries outside 0..N-1 are skipped.
+ *   idx           int32 [n_segments][N][topk] output, indexed by position.
  *   topk          1..ZETA_MAX_TOPK; causal 0 or 1.
  */
 zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes,
                                const int32_t* perm, int64_t n_segments, int64_t N, int topk,
-                               int causal, int32_t* idx, void* workspace,
+                               int causal, const int32_t* q_order, int32_t* idx, void* workspace,
                                size_t workspace_bytes, hipStream_t stream);
 
 /*
@@ -136,20 +144,25 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  * valid entry is written as zeros.
  *
  *   q, k   [B][H][N][d_k], v [B][H][N][d_v], out [B][H][N][d_v], all `dtype`.
- *   idx    int32 [B*H][N][topk]; valid entries (0 <= j < N) first, then -1.
- *   eps    gamma^2: finite and > 0.
+ *   idx      int32 [B*H][N][topk]; valid entries (0 <= j < N) first, then -1.
+ *   q_order  optional int32 [B*H][N] processing order, as for
+ *            zeta_select_topk (NULL: position order; no result depends on it).
+ *   eps      gamma^2: finite and > 0.
  *
- * Supported d_v: 32, 64, 128, 256.  out must not overlap the inputs.
+ * Supported d_v: 32, 64, 128, 256.  v and out must be 16-byte aligned; out
+ * must not overlap the inputs.
  */
 zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
                                  int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
-                                 const int32_t* idx, float eps, void* out, hipStream_t stream);
+                                 const int32_t* idx, const int32_t* q_order, float eps, void* out,
+                                 hipStream_t stream);
 
 /*
- * zeta_workspace_size -- bytes of device workspace that each of
- * zeta_morton_encode, zeta_sort_keys and zeta_select_topk needs for this
- * shape (the maximum over the three; one buffer serves all of them when they
- * run in order on one stream).  Returns 0 for invalid shapes.
+ * zeta_workspace_size -- bytes of device workspace enough for each of
+ * zeta_morton_encode, zeta_sort_keys and zeta_select_topk on this shape,
+ * where the sort may cover the query codes together with the key codes
+ * (2*B*H segments).  One buffer serves all calls run in order on one stream.
+ * Returns 0 for invalid shapes.
  */
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk,
                            int causal);

@@ -38,6 +38,17 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Workgroups are dispatched to the 8 XCDs round-robin (block b runs on XCD
+// b % 8).  This maps a hardware block index to a logical one so that each XCD
+// receives one contiguous range of logical blocks, keeping neighbouring work
+// (which shares data) under one L2.  A bijection on [0, nb).
+__device__ __forceinline__ int64_t xcd_contiguous_block(int64_t b, int64_t nb) {
+  constexpr int64_t kXcds = 8;
+  const int64_t per = nb / kXcds, extra = nb % kXcds;
+  const int64_t x = b % kXcds, l = b / kXcds;
+  return (x < extra) ? x * (per + 1) + l : extra * (per + 1) + (x - extra) * per + l;
+}
+
 // Exclusive prefix sum over a block of exactly 256 threads (one value each).
 // `scratch` must hold 4 words.  Contains block barriers: every thread calls it.
 __device__ __forceinline__ uint32_t block256_exclusive_scan(uint32_t x, uint32_t* scratch) {

@@ -18,15 +18,16 @@ hipError_t launch_encode(const void* q, const void* k, bool is_bf16, int64_t S, 
 hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_bits,
                        uint32_t* sorted_codes, int32_t* perm, void* workspace, hipStream_t stream);
 
-// Causal prefix lists (when needed) and the window of every query.
+// Causal prefix lists (when needed) and the window of every query.  q_order:
+// optional processing order (a permutation of 0..N-1 per segment).
 hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                         int64_t S, int64_t N, int topk, bool causal, int32_t* idx, void* workspace,
-                         hipStream_t stream);
+                         int64_t S, int64_t N, int topk, bool causal, const int32_t* q_order, int32_t* idx,
+                         void* workspace, hipStream_t stream);
 
 // Cauchy-softmax attention over the selected rows.
 hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
-                         int64_t N, int dk, int dv, int topk, const int32_t* idx, float eps, void* out,
-                         hipStream_t stream);
+                         int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
+                         float eps, void* out, hipStream_t stream);
 
 bool attend_supports(int dv);
 

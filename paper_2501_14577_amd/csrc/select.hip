@@ -18,7 +18,9 @@
 //   list_scatter: stable compaction of each tile into every F_t it feeds
 //                 (one ballot per level and 64 keys; earlier tiles' counts
 //                 give the base);
-//   select:       one wavefront per query: a 64-way search for the insertion
+//   select:       one wavefront per query (taken in an optional processing
+//                 order; Z-order keeps neighbouring wavefronts searching the
+//                 same stretch of the lists): a 64-way search for the insertion
 //                 point (three rounds for 2^16 keys), then ballot-compacted
 //                 scans to the right and left collecting the in-pool keys,
 //                 staged in LDS and written as one coalesced row.
@@ -203,7 +205,8 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
     select_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
                   const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                   const int32_t* __restrict__ list_pos, int64_t total, int64_t N, int topk, int causal,
-                  int t0, int t_hi, int64_t cap, int32_t* __restrict__ idx) {
+                  int t0, int t_hi, int64_t cap, const int32_t* __restrict__ q_order,
+                  int32_t* __restrict__ idx) {
   extern __shared__ int32_t s_sel[];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -211,10 +214,17 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
   int32_t* rbuf = lbuf + topk;              // right part, filled from its start
   const int half = topk / 2;
 
-  for (int64_t g = int64_t(blockIdx.x) * kSelWavesPerBlock + wave; g < total;
-       g += int64_t(gridDim.x) * kSelWavesPerBlock) {
-    const int64_t seg = g / N;
-    const int32_t i = int32_t(g - seg * N);
+  const int64_t nb = gridDim.x;
+  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kSelWavesPerBlock < total; blk += nb) {
+    const int64_t slot = blk * kSelWavesPerBlock + wave;
+    if (slot >= total) continue;
+    const int64_t seg = slot / N;
+    int32_t i = int32_t(slot - seg * N);
+    if (q_order != nullptr) {
+      i = q_order[slot];
+      if (i < 0 || i >= N) continue;  // not a permutation entry: nothing to do
+    }
+    const int64_t g = seg * N + i;
     const uint32_t key = q_codes[g];
 
     const uint32_t* codes = sorted_codes + seg * N;
@@ -262,8 +272,8 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
 }  // namespace
 
 hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                         int64_t S, int64_t N, int topk, bool causal, int32_t* idx, void* workspace,
-                         hipStream_t stream) {
+                         int64_t S, int64_t N, int topk, bool causal, const int32_t* q_order, int32_t* idx,
+                         void* workspace, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const SelectWs ws = select_ws(S, N, topk, causal ? 1 : 0);
   uint32_t* list_codes = nullptr;
@@ -285,7 +295,7 @@ hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, 
   const size_t lds = size_t(kSelWavesPerBlock) * 2 * topk * sizeof(int32_t);
   hipLaunchKernelGGL(select_kernel, dim3(blocks), dim3(kSelWavesPerBlock * 64), lds, stream, q_codes,
                      sorted_codes, perm, list_codes, list_pos, total, N, topk, causal ? 1 : 0, lp.t0,
-                     lp.t_hi, lp.cap, idx);
+                     lp.t_hi, lp.cap, q_order, idx);
   return hipGetLastError();
 }
 

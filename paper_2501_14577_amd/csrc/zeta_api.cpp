@@ -68,21 +68,21 @@ zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_
 }
 
 zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                               int64_t n_segments, int64_t N, int topk, int causal, int32_t* idx,
-                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                               int64_t n_segments, int64_t N, int topk, int causal, const int32_t* q_order,
+                               int32_t* idx, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!q_codes || !sorted_codes || !perm || !idx) return ZETA_ERR_INVALID_ARG;
   if (!shape_ok(n_segments, N)) return ZETA_ERR_INVALID_ARG;
   if (topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
   if (topk > zeta::kMaxTopk) return ZETA_ERR_UNSUPPORTED;
   const zeta::SelectWs ws = zeta::select_ws(n_segments, N, topk, causal);
   if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
-  return hip_status(zeta::launch_select(q_codes, sorted_codes, perm, n_segments, N, topk, causal != 0, idx,
-                                        workspace, stream));
+  return hip_status(zeta::launch_select(q_codes, sorted_codes, perm, n_segments, N, topk, causal != 0, q_order,
+                                        idx, workspace, stream));
 }
 
 zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
                                  int64_t H, int64_t N, int d_k, int d_v, int topk, const int32_t* idx,
-                                 float eps, void* out, hipStream_t stream) {
+                                 const int32_t* q_order, float eps, void* out, hipStream_t stream) {
   if (!q || !k || !v || !idx || !out) return ZETA_ERR_INVALID_ARG;
   if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
   if (d_k < 1 || d_v < 1 || topk < 1) return ZETA_ERR_INVALID_ARG;
@@ -91,15 +91,16 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
   if (out == q || out == k || out == v) return ZETA_ERR_INVALID_ARG;
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
-  return hip_status(zeta::launch_attend(q, k, v, dtype == ZETA_BF16, B * H, N, d_k, d_v, topk, idx, eps, out,
-                                        stream));
+  return hip_status(zeta::launch_attend(q, k, v, dtype == ZETA_BF16, B * H, N, d_k, d_v, topk, idx, q_order, eps,
+                                        out, stream));
 }
 
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk, int causal) {
   if (bad_count(B, H, N) || d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32 || topk < 1) return 0;
   const int64_t S = B * H;
   size_t bytes = zeta::encode_ws(S, N, d_k).bytes;
-  const size_t sb = zeta::sort_ws(S, N, d_k * bits).bytes;
+  // Room to sort the query codes together with the key codes (2*B*H segments).
+  const size_t sb = zeta::sort_ws(2 * S, N, d_k * bits).bytes;
   const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
   if (sb > bytes) bytes = sb;
   if (lb > bytes) bytes = lb;

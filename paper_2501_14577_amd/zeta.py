@@ -52,8 +52,8 @@ def load_library() -> ctypes.CDLL:
     vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     L.zeta_morton_encode.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     L.zeta_sort_keys.argtypes = [vp, i64, i64, i32, vp, vp, vp, sz, vp]
-    L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp, sz, vp]
-    L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, f32, vp, vp]
+    L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp]
+    L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, f32, vp, vp]
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
     for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_select_topk", "zeta_topk_attn_fwd"):
@@ -152,71 +152,80 @@ def zeta_sort_keys(k_codes: torch.Tensor, code_bits: int, *, sorted_codes: Optio
 
 
 def zeta_select_topk(q_codes: torch.Tensor, sorted_codes: torch.Tensor, perm: torch.Tensor, topk: int,
-                     causal: bool, *, idx: Optional[torch.Tensor] = None,
+                     causal: bool, *, q_order: Optional[torch.Tensor] = None, idx: Optional[torch.Tensor] = None,
                      workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Candidate window of every query -> idx int32 [..., N, topk] (-1 padded)."""
+    """Candidate window of every query -> idx int32 [..., N, topk] (-1 padded).
+
+    ``q_order`` (int32, shaped like ``q_codes``) is an optional processing
+    order; it does not change the result."""
     N = q_codes.shape[-1]
     S = q_codes.numel() // N
     if idx is None:
         idx = torch.empty((*q_codes.shape, topk), dtype=torch.int32, device=q_codes.device)
     if workspace is None:
         workspace = workspace_for(S, 1, N, 1, 1, topk, causal, q_codes.device)
-    _need_device(q_codes, sorted_codes, perm, idx, workspace)
+    _need_device(q_codes, sorted_codes, perm, q_order, idx, workspace)
     st = load_library().zeta_select_topk(_ptr(q_codes), _ptr(sorted_codes), _ptr(perm), S, N, topk,
-                                         int(bool(causal)), _ptr(idx), _ptr(workspace),
+                                         int(bool(causal)), _ptr(q_order), _ptr(idx), _ptr(workspace),
                                          workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_select_topk", st)
     return idx
 
 
 def zeta_topk_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, eps: float, *,
-                       out: Optional[torch.Tensor] = None) -> torch.Tensor:
+                       q_order: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Cauchy-softmax attention over idx -> out [B,H,N,d_v] in v's dtype."""
     B, H, N, dk = q.shape
     dv = v.shape[-1]
     topk = idx.shape[-1]
     if out is None:
         out = torch.empty((B, H, N, dv), dtype=v.dtype, device=v.device)
-    _need_device(q, k, v, idx, out)
+    _need_device(q, k, v, idx, q_order, out)
     if not (q.dtype == k.dtype == v.dtype == out.dtype):
         raise ValueError("q, k, v and out must share a dtype")
     st = load_library().zeta_topk_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dk, dv, topk,
-                                           _ptr(idx), float(eps), _ptr(out), _stream())
+                                           _ptr(idx), _ptr(q_order), float(eps), _ptr(out), _stream())
     _check("zeta_topk_attn_fwd", st)
     return out
 
 
 def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: float, causal: bool = True,
             bits: int = 10, *, workspace: Optional[torch.Tensor] = None, buffers: Optional[dict] = None,
-            return_intermediates: bool = False):
+            zorder: bool = True, return_intermediates: bool = False):
     """The whole forward: encode, sort, select, attend (four calls, one stream).
 
-    ``buffers`` may hold preallocated outputs (keys ``q_codes``, ``k_codes``,
-    ``sorted_codes``, ``perm``, ``idx``, ``out``) so that repeated calls
-    allocate nothing.
+    The query codes are sorted together with the key codes (one call over
+    2*B*H segments) and their order drives select and attend (``zorder``);
+    the result is the same either way.  ``buffers`` (from ``alloc_buffers``)
+    holds preallocated outputs so that repeated calls allocate nothing.
     """
     B, H, N, dk = q.shape
-    b = buffers if buffers is not None else {}
+    b = buffers if buffers is not None else alloc_buffers(B, H, N, v.shape[-1], topk, v.dtype, q.device)
     if workspace is None:
         workspace = workspace_for(B, H, N, dk, bits, topk, causal, q.device)
-    qc, kc = zeta_morton_encode(q, k, bits, q_codes=b.get("q_codes"), k_codes=b.get("k_codes"),
-                                workspace=workspace)
-    sc, perm = zeta_sort_keys(kc, dk * bits, sorted_codes=b.get("sorted_codes"), perm=b.get("perm"),
-                              workspace=workspace)
-    idx = zeta_select_topk(qc, sc, perm, topk, causal, idx=b.get("idx"), workspace=workspace)
-    out = zeta_topk_attn_fwd(q, k, v, idx, eps, out=b.get("out"))
+    qc, kc = zeta_morton_encode(q, k, bits, q_codes=b["codes"][0], k_codes=b["codes"][1], workspace=workspace)
+    if zorder:
+        sc2, perm2 = zeta_sort_keys(b["codes"], dk * bits, sorted_codes=b["sorted_codes2"], perm=b["perm2"],
+                                    workspace=workspace)
+        sc, perm, order = sc2[1], perm2[1], perm2[0]
+    else:
+        sc, perm = zeta_sort_keys(kc, dk * bits, sorted_codes=b["sorted_codes2"][1], perm=b["perm2"][1],
+                                  workspace=workspace)
+        order = None
+    idx = zeta_select_topk(qc, sc, perm, topk, causal, q_order=order, idx=b["idx"], workspace=workspace)
+    out = zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, out=b["out"])
     if return_intermediates:
-        return dict(q_codes=qc, k_codes=kc, sorted_codes=sc, perm=perm, idx=idx, out=out)
+        return dict(q_codes=qc, k_codes=kc, sorted_codes=sc, perm=perm, q_order=order, idx=idx, out=out)
     return out
 
 
 def alloc_buffers(B: int, H: int, N: int, dv: int, topk: int, dtype: torch.dtype, device) -> dict:
-    """Output buffers for ``forward(..., buffers=...)``."""
+    """Output buffers for ``forward(..., buffers=...)``.  Query and key codes
+    share one [2, B, H, N] tensor so that one sort call orders both."""
     return dict(
-        q_codes=torch.empty((B, H, N), dtype=torch.uint32, device=device),
-        k_codes=torch.empty((B, H, N), dtype=torch.uint32, device=device),
-        sorted_codes=torch.empty((B, H, N), dtype=torch.uint32, device=device),
-        perm=torch.empty((B, H, N), dtype=torch.int32, device=device),
+        codes=torch.empty((2, B, H, N), dtype=torch.uint32, device=device),
+        sorted_codes2=torch.empty((2, B, H, N), dtype=torch.uint32, device=device),
+        perm2=torch.empty((2, B, H, N), dtype=torch.int32, device=device),
         idx=torch.empty((B, H, N, topk), dtype=torch.int32, device=device),
         out=torch.empty((B, H, N, dv), dtype=dtype, device=device),
     )

@@ -56,9 +56,10 @@ def test_workspace_size():
     assert ws(1, 1, 10, 3, 11, 4, 1) == 0  # 33 code bits
     assert ws(1, 1, 10, 0, 10, 4, 1) == 0
     assert ws(1, 1, 10, 3, 10, 0, 1) == 0
-    # Long-context shape: the sort's ping-pong buffer (16 x 65536 x 8 B) dominates.
+    # Long-context shape: the sort's ping-pong buffer for query and key codes
+    # together (2 x 16 x 65536 x 8 B) dominates.
     big = ws(1, 16, 65536, 3, 6, 128, 1)
-    assert big >= 16 * 65536 * 8
+    assert big >= 2 * 16 * 65536 * 8
     assert big % 256 == 0
     assert ws(1, 16, 65536, 3, 6, 128, 0) <= big
     # One tiny segment still gets a buffer for the range partials.
@@ -79,15 +80,15 @@ def _sort(**kw):
 
 
 def _sel(**kw):
-    a = dict(q_codes=P, sorted_codes=P2, perm=P3, S=2, N=100, topk=8, causal=1, idx=P4, ws=P, ws_bytes=BIG,
-             stream=NULL)
+    a = dict(q_codes=P, sorted_codes=P2, perm=P3, S=2, N=100, topk=8, causal=1, q_order=NULL, idx=P4, ws=P,
+             ws_bytes=BIG, stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_select_topk(*a.values())
 
 
 def _att(**kw):
     a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, idx=P4,
-             eps=0.5, out=ctypes.c_void_p(0x50000), stream=NULL)
+             q_order=NULL, eps=0.5, out=ctypes.c_void_p(0x50000), stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_topk_attn_fwd(*a.values())
 

@@ -335,3 +335,55 @@ def test_forward_deterministic_and_complete():
         runs.append({n: t.view(torch.uint8).cpu().numpy() for n, t in b.items()})
     for n in runs[0]:
         assert np.array_equal(runs[0][n], runs[1][n]), n
+
+
+# ----------------------------------------------------------------------------
+# Processing order
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_processing_order_changes_nothing(causal):
+    """select and attend give bit-identical results in position order, in the
+    queries' Z-order and in a random order; entries outside 0..N-1 are skipped."""
+    cfg = 2
+    w, x, _ = inputs(cfg)
+    log(f"processing order config {cfg} causal={causal}")
+    oc = oracle_codes(cfg)
+    q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
+    qc, sc, perm = u32_to_dev(oc["q_codes"]), u32_to_dev(oc["sorted_codes"]), i32_to_dev(oc["perm"])
+    S = w.segments
+    zorder = i32_to_dev(np.argsort(oc["q_codes"], axis=1, kind="stable"))
+    rng = np.random.default_rng(9)
+    shuffled = i32_to_dev(np.stack([rng.permutation(w.N) for _ in range(S)]))
+    idx0 = zeta.zeta_select_topk(qc, sc, perm, w.topk, causal)
+    out0 = zeta.zeta_topk_attn_fwd(q, k, v, idx0.reshape(w.B, w.H, w.N, w.topk), 0.5)
+    for order in (zorder, shuffled):
+        idx1 = zeta.zeta_select_topk(qc, sc, perm, w.topk, causal, q_order=order)
+        out1 = zeta.zeta_topk_attn_fwd(q, k, v, idx0.reshape(w.B, w.H, w.N, w.topk), 0.5, q_order=order)
+        torch.cuda.synchronize()
+        assert torch.equal(idx0, idx1)
+        assert torch.equal(out0.view(torch.int16), out1.view(torch.int16))
+    # A partial order: rows whose slot holds an out-of-range entry stay untouched.
+    part = np.argsort(oc["q_codes"], axis=1, kind="stable").astype(np.int32)
+    part[:, ::3] = -1
+    idx2 = torch.full_like(idx0, -7)
+    zeta.zeta_select_topk(qc, sc, perm, w.topk, causal, q_order=i32_to_dev(part), idx=idx2)
+    torch.cuda.synchronize()
+    got, ref = host(idx2), host(idx0)
+    done = np.zeros((S, w.N), dtype=bool)
+    seg_ix, slot_ix = np.nonzero(part >= 0)
+    done[seg_ix, part[seg_ix, slot_ix]] = True
+    assert np.array_equal(got[done], ref[done])
+    assert np.all(got[~done] == -7)
+
+
+def test_forward_zorder_matches_position_order():
+    cfg = 4
+    w, x, _ = inputs(cfg)
+    log("forward z-order vs position order, config 4")
+    q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
+    a = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, zorder=True, return_intermediates=True)
+    b = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, zorder=False, return_intermediates=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a["idx"], b["idx"])
+    assert torch.equal(a["out"].view(torch.int16), b["out"].view(torch.int16))
