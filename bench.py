@@ -160,15 +160,17 @@ def main() -> int:
     codes, sorted2, perm2 = bufs["codes"], bufs["sorted_codes2"], bufs["perm2"]
 
     def step(ev=None):
-        # encode -> joint sort of query and key codes (the query permutation is
-        # the Z-order processing order) -> select -> attend
+        # encode -> joint sort of query and key codes -> the query Z-order
+        # regrouped by list level (processing order) -> select -> attend
         qc, kc = zeta.zeta_morton_encode(q, k, w.bits, q_codes=codes[0], k_codes=codes[1], workspace=ws)
         zeta.zeta_sort_keys(codes, w.code_bits, sorted_codes=sorted2, perm=perm2, workspace=ws)
-        idx = zeta.zeta_select_topk(qc, sorted2[1], perm2[1], w.topk, causal, q_order=perm2[0], idx=bufs["idx"],
+        order = zeta.zeta_query_order(perm2[0], w.N, w.segments, w.topk, causal, order_out=bufs["order"],
+                                      workspace=ws)
+        idx = zeta.zeta_select_topk(qc, sorted2[1], perm2[1], w.topk, causal, q_order=order, idx=bufs["idx"],
                                     workspace=ws)
         if ev is not None:
             ev[0].record()
-        zeta.zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=perm2[0], out=bufs["out"])
+        zeta.zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, out=bufs["out"])
         if ev is not None:
             ev[1].record()
 

@@ -6,8 +6,9 @@
  *
  *   zeta_morton_encode  -> Z-order codes of queries and keys
  *   zeta_sort_keys      -> keys sorted by code per (batch, head); called on
- *                          the query codes too, the permutation is a
- *                          processing order for the next two calls
+ *                          the query codes too, its permutation (regrouped
+ *                          by zeta_query_order) is a processing order for
+ *                          the next two calls
  *   zeta_select_topk    -> k candidate keys per query around its insertion point
  *   zeta_topk_attn_fwd  -> Cauchy-softmax attention over the candidates
  *
@@ -105,6 +106,30 @@ zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_
                              size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * zeta_query_order -- a processing order for zeta_select_topk and
+ * zeta_topk_attn_fwd that groups queries by the sorted key list they search.
+ *
+ * Causal selection searches, for a query at position i, the keys at
+ * positions below 2^t in code order, t = max(ceil(log2(topk)), bit length
+ * of i) (the full sorted list once 2^t >= N).  This call regroups the given
+ * order by that level, keeping the given order inside each level; for the
+ * Z-order of the query codes (the permutation zeta_sort_keys returns for
+ * them) consecutive queries then search one list with non-decreasing codes
+ * and share most of their candidates, which both later calls exploit.  Any
+ * permutation gives the same results; this one is the fast one.
+ *
+ *   q_order    int32 [n_segments][N] permutation per segment, or NULL for
+ *              position order.
+ *   order_out  int32 [n_segments][N] output; may be the same buffer as
+ *              q_order.
+ *   topk, causal  as for zeta_select_topk (non-causal: a copy of q_order).
+ *   workspace  at least zeta_workspace_size(...) bytes.
+ */
+zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64_t N, int topk,
+                               int causal, int32_t* order_out, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
+/*
  * zeta_select_topk -- candidate keys of every query (Section 3.2.2: the
  * insertion point of the query's code among the sorted keys by binary search,
  * then a window of k keys centred on it, with causal masking restricting each
@@ -159,7 +184,8 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
 
 /*
  * zeta_workspace_size -- bytes of device workspace enough for each of
- * zeta_morton_encode, zeta_sort_keys and zeta_select_topk on this shape,
+ * zeta_morton_encode, zeta_sort_keys, zeta_query_order and zeta_select_topk
+ * on this shape,
  * where the sort may cover the query codes together with the key codes
  * (2*B*H segments).  One buffer serves all calls run in order on one stream.
  * Returns 0 for invalid shapes.

@@ -27,6 +27,7 @@ constexpr int kRadixMax = 256;  // digits of at most 8 bits
 
 // ---- select ---------------------------------------------------------------
 constexpr int kSelWavesPerBlock = 4;
+constexpr int kSelRun = 32;  // consecutive processing-order slots served by one wavefront
 constexpr int kMaxLevels = 32;
 
 // ---- attend ---------------------------------------------------------------
@@ -122,11 +123,27 @@ inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
   if (!causal) return w;
   ListPlan lp = list_plan(N, topk);
   if (lp.levels == 0) return w;
-  int64_t tiles = ceil_div(N, kSortTile);
+  const int64_t tiles = ceil_div(N, kSortTile);
+  const size_t list = align_up(size_t(S) * size_t(lp.cap) * sizeof(uint32_t));
   w.codes_off = align_up(size_t(S) * size_t(tiles) * kMaxLevels * sizeof(uint32_t));
-  size_t buf = align_up(size_t(S) * size_t(lp.cap) * sizeof(uint32_t));
-  w.pos_off = w.codes_off + buf;
-  w.bytes = w.pos_off + buf;
+  w.pos_off = w.codes_off + list;
+  w.bytes = w.pos_off + list;
+  return w;
+}
+
+// Regrouping a processing order by list level: class keys, their sorted
+// copy, a copy of the given order and the radix pass's histograms.
+struct QueryOrderWs {
+  size_t cls_off, cls_sorted_off, given_off, phist_off, bytes;
+};
+inline QueryOrderWs query_order_ws(int64_t S, int64_t N) {
+  QueryOrderWs w;
+  const size_t per_query = align_up(size_t(S) * size_t(N) * sizeof(uint32_t));
+  w.cls_off = 0;
+  w.cls_sorted_off = per_query;
+  w.given_off = 2 * per_query;
+  w.phist_off = 3 * per_query;
+  w.bytes = w.phist_off + align_up(size_t(S) * size_t(ceil_div(N, kSortTile)) * kRadixMax * sizeof(uint32_t));
   return w;
 }
 

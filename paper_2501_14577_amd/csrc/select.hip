@@ -18,12 +18,22 @@
 //   list_scatter: stable compaction of each tile into every F_t it feeds
 //                 (one ballot per level and 64 keys; earlier tiles' counts
 //                 give the base);
-//   select:       one wavefront per query (taken in an optional processing
-//                 order; Z-order keeps neighbouring wavefronts searching the
-//                 same stretch of the lists): a 64-way search for the insertion
-//                 point (three rounds for 2^16 keys), then ballot-compacted
+//   select:       one wavefront serves a run of 32 consecutive queries of the
+//                 processing order, one after another: a 64-way search for
+//                 the insertion point (three rounds for 2^16 keys, or one
+//                 probe after the previous query's point when the list is
+//                 the same and the code no smaller), then ballot-compacted
 //                 scans to the right and left collecting the in-pool keys,
 //                 staged in LDS and written as one coalesced row.
+//
+// query_order (the zeta_query_order entry point) regroups a processing order,
+// typically the Z-order of the query codes, by the list each query searches,
+// keeping the given order inside each group (one stable radix pass on the
+// level).  A run of that order searches one list with non-decreasing codes, so
+// the queries reuse each other's cached entries and the search gallops from
+// the previous insertion point; attend's tiles share value rows the same way.
+#include <stdint.h>
+
 #include "device_common.h"
 #include "kernels.h"
 #include "layout.h"
@@ -125,12 +135,13 @@ __global__ void __launch_bounds__(kSortThreads)
   }
 }
 
-// First index in codes[0..n) whose code is >= key, found by a wavefront:
-// each round 64 lanes probe evenly spaced entries and the ballot of "probe <
-// key" (a prefix of the lanes, the list being sorted) narrows the range 64x.
-__device__ __forceinline__ int32_t wave_lower_bound(const uint32_t* __restrict__ codes, int32_t n,
+// First index in codes[lo..n) whose code is >= key, given that every entry
+// before lo is below key, found by a wavefront: each round 64 lanes probe
+// evenly spaced entries and the ballot of "probe < key" (a prefix of the
+// lanes, the list being sorted) narrows the range 64x.
+__device__ __forceinline__ int32_t wave_lower_bound(const uint32_t* __restrict__ codes, int32_t lo, int32_t n,
                                                     uint32_t key, int lane) {
-  int32_t lo = 0, hi = n;
+  int32_t hi = n;
   while (hi > lo) {
     const int32_t len = hi - lo;
     const int32_t stride = (len + 63) >> 6;
@@ -149,63 +160,116 @@ __device__ __forceinline__ int32_t wave_lower_bound(const uint32_t* __restrict__
   return lo;
 }
 
+// The same search when the answer is expected just after `lo` (the previous
+// query's insertion point in the same list, for a code no smaller): probe the
+// 64 entries from lo first, and fall back to the 64-way search beyond them.
+__device__ __forceinline__ int32_t wave_lower_bound_near(const uint32_t* __restrict__ codes, int32_t lo,
+                                                         int32_t n, uint32_t key, int lane) {
+  const int32_t x = lo + lane;
+  const bool less = x < n && codes[x] < key;
+  const int cnt = __popcll(wave_ballot(less));
+  if (cnt < 64) return lo + cnt;
+  return wave_lower_bound(codes, lo + 64, n, key, lane);
+}
+
+// Chunks of 64 list entries fetched on each side of the insertion point
+// before the scans start, so that the common case needs one round trip.
+constexpr int kPre = 2;
+
+// Append up to `need` in-pool entries (position <= limit), in list order,
+// from the 64 entries whose positions this wavefront holds in `pv` (entry
+// cur + lane; out-of-list lanes hold INT_MAX) to buf[got..].  Returns the new
+// count; `cur` ends just past the last entry taken, or 64 further on.
+__device__ __forceinline__ int take_right(int32_t pv, int32_t limit, int32_t n, int32_t& cur, int need, int got,
+                                          int32_t* buf) {
+  const bool ok = pv <= limit;
+  const uint64_t bal = wave_ballot(ok);
+  const int avail = __popcll(bal);
+  const int want = need - got;
+  const int take = avail < want ? avail : want;
+  const int slot = int(lanes_below(bal));
+  if (ok && slot < take) buf[got + slot] = pv;
+  if (take < avail) {
+    // Stop just past the take-th in-pool entry of this chunk.
+    const uint64_t last = wave_ballot(ok && slot == take - 1);
+    cur = cur + (__ffsll((unsigned long long)last) - 1) + 1;
+  } else {
+    cur = cur + 64 < n ? cur + 64 : n;
+  }
+  return got + take;
+}
+
+// Collect up to `need` in-pool entries, nearest first, from the 64 entries
+// cur-64 .. cur-1 held in `pv` (out-of-list lanes hold INT_MAX), into
+// buf[cap_end-1-got], buf[cap_end-2-got], ... so that the collected run ends at
+// buf[cap_end-1] in ascending list order.  Returns the new count.
+__device__ __forceinline__ int take_left(int32_t pv, int32_t limit, int need, int got, int32_t* buf, int cap_end) {
+  const bool ok = pv <= limit;
+  const uint64_t bal = wave_ballot(ok);
+  const int avail = __popcll(bal);
+  const int want = need - got;
+  const int take = avail < want ? avail : want;
+  const int from_top = avail - 1 - int(lanes_below(bal));
+  if (ok && from_top < take) buf[cap_end - 1 - (got + from_top)] = pv;
+  return got + take;
+}
+
 // Scan entries cur, cur+1, ... of pos[0..n) and append up to `need` in-pool
-// ones (position <= limit) to buf[got..].  Returns the new count; `cur` is
-// left just past the last entry taken (or at n).
+// ones to buf[got..].  Returns the new count; `cur` is left just past the
+// last entry taken (or at n).
 __device__ __forceinline__ int scan_right(const int32_t* __restrict__ pos, int32_t n, int32_t limit,
                                           int32_t& cur, int need, int got, int32_t* buf, int lane) {
   while (got < need && cur < n) {
     const int32_t e = cur + lane;
-    const bool inr = e < n;
-    const int32_t pv = inr ? pos[e] : 0;
-    const bool ok = inr && pv <= limit;
-    const uint64_t bal = wave_ballot(ok);
-    const int avail = __popcll(bal);
-    const int want = need - got;
-    const int take = avail < want ? avail : want;
-    const int slot = int(lanes_below(bal));
-    if (ok && slot < take) buf[got + slot] = pv;
-    if (take < avail) {
-      // Stop just past the take-th in-pool entry of this chunk.
-      const uint64_t last = wave_ballot(ok && slot == take - 1);
-      cur = cur + (__ffsll((unsigned long long)last) - 1) + 1;
-    } else {
-      cur = cur + 64 < n ? cur + 64 : n;
-    }
-    got += take;
+    const int32_t pv = e < n ? pos[e] : INT32_MAX;
+    got = take_right(pv, limit, n, cur, need, got, buf);
   }
   return got;
 }
 
 // Scan entries cur-1, cur-2, ... and collect up to `need` in-pool entries,
-// nearest first, into buf[cap_end-1], buf[cap_end-2], ... so that the
-// collected run ends at buf[cap_end-1] in ascending list order.
-__device__ __forceinline__ int scan_left(const int32_t* __restrict__ pos, int32_t limit, int32_t cur,
-                                         int need, int32_t* buf, int cap_end, int lane) {
-  int got = 0;
+// nearest first, after the `got` already collected (see take_left).
+__device__ __forceinline__ int scan_left(const int32_t* __restrict__ pos, int32_t limit, int32_t cur, int need,
+                                         int got, int32_t* buf, int cap_end, int lane) {
   while (got < need && cur > 0) {
-    const int32_t start = cur - 64;
-    const int32_t e = start + lane;
-    const bool inr = e >= 0;
-    const int32_t pv = inr ? pos[e] : 0;
-    const bool ok = inr && pv <= limit;
-    const uint64_t bal = wave_ballot(ok);
-    const int avail = __popcll(bal);
-    const int want = need - got;
-    const int take = avail < want ? avail : want;
-    const int from_top = avail - 1 - int(lanes_below(bal));
-    if (ok && from_top < take) buf[cap_end - 1 - (got + from_top)] = pv;
-    got += take;
-    cur = start;
+    const int32_t e = cur - 64 + lane;
+    const int32_t pv = e >= 0 ? pos[e] : INT32_MAX;
+    got = take_left(pv, limit, need, got, buf, cap_end);
+    cur -= 64;
   }
   return got;
+}
+
+// Level of the list a causal query at position i searches: t0..t_hi for the
+// prefix lists, t_hi + 1 for the full sorted list.
+__device__ __forceinline__ int query_level(int32_t i, int t0, int t_hi) {
+  const int bl = bit_length(uint32_t(i));
+  const int t = bl > t0 ? bl : t0;
+  return t <= t_hi ? t : t_hi + 1;
+}
+
+__global__ void __launch_bounds__(256)
+    level_class_kernel(const int32_t* __restrict__ q_order, int64_t total, int64_t N, int t0, int t_hi,
+                       uint32_t* __restrict__ cls) {
+  const int64_t slot = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (slot >= total) return;
+  const int32_t i = q_order[slot];
+  cls[slot] = (i >= 0 && i < N) ? uint32_t(query_level(i, t0, t_hi) - t0) : 0u;
+}
+
+// order_out[slot] = q_order[slot], or the slot's position when q_order is NULL.
+__global__ void __launch_bounds__(256)
+    copy_order_kernel(const int32_t* __restrict__ q_order, int64_t total, int64_t N, int32_t* __restrict__ order_out) {
+  const int64_t slot = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (slot >= total) return;
+  order_out[slot] = q_order != nullptr ? q_order[slot] : int32_t(slot % N);
 }
 
 __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
     select_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
                   const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                   const int32_t* __restrict__ list_pos, int64_t total, int64_t N, int topk, int causal,
-                  int t0, int t_hi, int64_t cap, const int32_t* __restrict__ q_order,
+                  int t0, int t_hi, int64_t cap, const int32_t* __restrict__ order,
                   int32_t* __restrict__ idx) {
   extern __shared__ int32_t s_sel[];
   const int lane = threadIdx.x & 63;
@@ -213,69 +277,138 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
   int32_t* lbuf = s_sel + wave * 2 * topk;  // left part, filled from its end
   int32_t* rbuf = lbuf + topk;              // right part, filled from its start
   const int half = topk / 2;
+  const int64_t runs = (total + kSelRun - 1) / kSelRun;
 
   const int64_t nb = gridDim.x;
-  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kSelWavesPerBlock < total; blk += nb) {
-    const int64_t slot = blk * kSelWavesPerBlock + wave;
-    if (slot >= total) continue;
-    const int64_t seg = slot / N;
-    int32_t i = int32_t(slot - seg * N);
-    if (q_order != nullptr) {
-      i = q_order[slot];
-      if (i < 0 || i >= N) continue;  // not a permutation entry: nothing to do
-    }
-    const int64_t g = seg * N + i;
-    const uint32_t key = q_codes[g];
-
-    const uint32_t* codes = sorted_codes + seg * N;
-    const int32_t* pos = perm + seg * N;
-    int32_t n = int32_t(N);
-    int32_t limit = int32_t(N);  // every position is in the non-causal pool
-    if (causal) {
-      limit = i;
-      const int bl = bit_length(uint32_t(i));
-      const int t = bl > t0 ? bl : t0;
-      if (t <= t_hi) {
-        const int64_t off = seg * cap + ((int64_t(1) << t) - (int64_t(1) << t0));
-        codes = list_codes + off;
-        pos = list_pos + off;
-        n = int32_t(1) << t;
+  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kSelWavesPerBlock < runs; blk += nb) {
+    const int64_t run = blk * kSelWavesPerBlock + wave;
+    if (run >= runs) continue;
+    const int64_t slot0 = run * kSelRun;
+    // This run's query positions and codes, one per lane, fetched together.
+    int32_t my_i = -1;
+    uint32_t my_key = 0;
+    {
+      const int64_t sl = slot0 + lane;
+      if (lane < kSelRun && sl < total) {
+        const int64_t sg = sl / N;
+        const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
+        if (ii >= 0 && ii < N) {
+          my_i = int32_t(ii);
+          my_key = q_codes[sg * N + ii];
+        }
       }
     }
+    const uint32_t* prev_codes = nullptr;
+    uint32_t prev_key = 0;
+    int32_t prev_p = 0;
+    for (int u = 0; u < kSelRun; ++u) {
+      const int64_t slot = slot0 + u;
+      if (slot >= total) break;
+      const int32_t i = __builtin_amdgcn_readlane(my_i, u);
+      const uint32_t key = uint32_t(__builtin_amdgcn_readlane(int32_t(my_key), u));
+      if (i < 0) continue;  // not a permutation entry: nothing to do
+      const int64_t seg = slot / N;
+      const int64_t g = seg * N + i;
 
-    const int32_t p = wave_lower_bound(codes, n, key, lane);
-    // floor(k/2) pool keys before p and the rest from p on, shifted inward
-    // when one side of the pool runs out.
-    const int need_r = topk - half;
-    int32_t cur_r = p;
-    int got_r = scan_right(pos, n, limit, cur_r, need_r, 0, rbuf, lane);
-    const int need_l = half + (need_r - got_r);
-    const int got_l = scan_left(pos, limit, p, need_l, lbuf, topk, lane);
-    if (got_l < need_l && got_r == need_r)
-      got_r = scan_right(pos, n, limit, cur_r, topk - got_l, got_r, rbuf, lane);
-    wave_lds_sync();
+      const uint32_t* codes = sorted_codes + seg * N;
+      const int32_t* pos = perm + seg * N;
+      int32_t n = int32_t(N);
+      int32_t limit = int32_t(N - 1);  // every position is in the non-causal pool
+      if (causal) {
+        limit = i;
+        const int t = query_level(i, t0, t_hi);
+        if (t <= t_hi) {
+          const int64_t off = seg * cap + ((int64_t(1) << t) - (int64_t(1) << t0));
+          codes = list_codes + off;
+          pos = list_pos + off;
+          n = int32_t(1) << t;
+        }
+      }
 
-    int32_t* row = idx + g * topk;
-    const int total_sel = got_l + got_r;
-    for (int c = lane; c < topk; c += 64) {
-      int32_t v = -1;
-      if (c < got_l)
-        v = lbuf[topk - got_l + c];
-      else if (c < total_sel)
-        v = rbuf[c - got_l];
-      row[c] = v;
+      const int32_t p = (codes == prev_codes && key >= prev_key) ? wave_lower_bound_near(codes, prev_p, n, key, lane)
+                                                                 : wave_lower_bound(codes, 0, n, key, lane);
+      prev_codes = codes;
+      prev_key = key;
+      prev_p = p;
+      // floor(k/2) pool keys before p and the rest from p on, shifted inward
+      // when one side of the pool runs out.  The first kPre chunks on each
+      // side are fetched together; further chunks are fetched as needed.
+      int32_t pre_r[kPre], pre_l[kPre];
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) {
+        const int32_t er = p + c * 64 + lane;
+        const int32_t el = p - (c + 1) * 64 + lane;
+        pre_r[c] = er < n ? pos[er] : INT32_MAX;
+        pre_l[c] = el >= 0 ? pos[el] : INT32_MAX;
+      }
+      const int need_r = topk - half;
+      int32_t cur_r = p;
+      int got_r = 0;
+#pragma unroll
+      for (int c = 0; c < kPre; ++c)
+        if (got_r < need_r && cur_r < n) got_r = take_right(pre_r[c], limit, n, cur_r, need_r, got_r, rbuf);
+      got_r = scan_right(pos, n, limit, cur_r, need_r, got_r, rbuf, lane);
+      const int need_l = half + (need_r - got_r);
+      int got_l = 0;
+      int32_t cur_l = p;
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) {
+        if (got_l < need_l && cur_l > 0) {
+          got_l = take_left(pre_l[c], limit, need_l, got_l, lbuf, topk);
+          cur_l -= 64;
+        }
+      }
+      got_l = scan_left(pos, limit, cur_l, need_l, got_l, lbuf, topk, lane);
+      if (got_l < need_l && got_r == need_r)
+        got_r = scan_right(pos, n, limit, cur_r, topk - got_l, got_r, rbuf, lane);
+      wave_lds_sync();
+
+      int32_t* row = idx + g * topk;
+      const int total_sel = got_l + got_r;
+      for (int c = lane; c < topk; c += 64) {
+        int32_t v = -1;
+        if (c < got_l)
+          v = lbuf[topk - got_l + c];
+        else if (c < total_sel)
+          v = rbuf[c - got_l];
+        row[c] = v;
+      }
+      wave_lds_sync();
     }
-    wave_lds_sync();
   }
 }
 
 }  // namespace
+
+hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int topk, bool causal, int32_t* order_out,
+                              void* workspace, hipStream_t stream) {
+  const ListPlan lp = list_plan(N, topk);
+  const int64_t total = S * N;
+  const unsigned blocks = unsigned(ceil_div(total, 256));
+  if (!causal || lp.levels == 0) {
+    // One list for every query: the given order (or position order) as is.
+    hipLaunchKernelGGL(copy_order_kernel, dim3(blocks), dim3(256), 0, stream, q_order, total, N, order_out);
+    return hipGetLastError();
+  }
+  const QueryOrderWs ws = query_order_ws(S, N);
+  char* wsb = static_cast<char*>(workspace);
+  uint32_t* cls = reinterpret_cast<uint32_t*>(wsb + ws.cls_off);
+  uint32_t* cls_sorted = reinterpret_cast<uint32_t*>(wsb + ws.cls_sorted_off);
+  int32_t* given = reinterpret_cast<int32_t*>(wsb + ws.given_off);
+  uint32_t* phist = reinterpret_cast<uint32_t*>(wsb + ws.phist_off);
+  hipLaunchKernelGGL(copy_order_kernel, dim3(blocks), dim3(256), 0, stream, q_order, total, N, given);
+  hipLaunchKernelGGL(level_class_kernel, dim3(blocks), dim3(256), 0, stream, given, total, N, lp.t0, lp.t_hi, cls);
+  int nbits = 1;
+  while ((1 << nbits) < lp.levels + 1) ++nbits;
+  return launch_stable_partition(cls, given, S, N, nbits, cls_sorted, order_out, phist, stream);
+}
 
 hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
                          int64_t S, int64_t N, int topk, bool causal, const int32_t* q_order, int32_t* idx,
                          void* workspace, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const SelectWs ws = select_ws(S, N, topk, causal ? 1 : 0);
+  const int64_t total = S * N;
   uint32_t* list_codes = nullptr;
   int32_t* list_pos = nullptr;
   if (causal && lp.levels > 0) {
@@ -289,8 +422,8 @@ hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, 
     hipLaunchKernelGGL(list_scatter_kernel, grid, block, 0, stream, sorted_codes, perm, N, tiles, lp.t0,
                        lp.levels, lp.cap, cnt, list_codes, list_pos);
   }
-  const int64_t total = S * N;
-  const int64_t want = ceil_div(total, kSelWavesPerBlock);
+  const int64_t runs = ceil_div(total, kSelRun);
+  const int64_t want = ceil_div(runs, kSelWavesPerBlock);
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const size_t lds = size_t(kSelWavesPerBlock) * 2 * topk * sizeof(int32_t);
   hipLaunchKernelGGL(select_kernel, dim3(blocks), dim3(kSelWavesPerBlock * 64), lds, stream, q_codes,

@@ -124,6 +124,16 @@ __global__ void __launch_bounds__(kSortThreads)
 
 }  // namespace
 
+hipError_t launch_stable_partition(const uint32_t* keys, const int32_t* vals, int64_t S, int64_t N, int nbits,
+                                   uint32_t* keys_out, int32_t* vals_out, uint32_t* hist, hipStream_t stream) {
+  const int64_t tiles = ceil_div(N, kSortTile);
+  const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
+  hipLaunchKernelGGL(radix_hist_kernel, grid, block, 0, stream, keys, N, tiles, 0, nbits, hist);
+  hipLaunchKernelGGL(radix_scatter_kernel<true>, grid, block, 0, stream, keys, vals, N, tiles, 0, nbits, hist,
+                     keys_out, vals_out);
+  return hipGetLastError();
+}
+
 hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_bits,
                        uint32_t* sorted_codes, int32_t* perm, void* workspace, hipStream_t stream) {
   const SortPlan plan = sort_plan(N, code_bits);

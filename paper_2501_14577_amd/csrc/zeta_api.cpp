@@ -67,6 +67,20 @@ zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_
   return hip_status(zeta::launch_sort(k_codes, n_segments, N, code_bits, sorted_codes, perm, workspace, stream));
 }
 
+zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64_t N, int topk, int causal,
+                               int32_t* order_out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!order_out) return ZETA_ERR_INVALID_ARG;
+  if (!shape_ok(n_segments, N)) return ZETA_ERR_INVALID_ARG;
+  if (topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (topk > zeta::kMaxTopk) return ZETA_ERR_UNSUPPORTED;
+  const zeta::ListPlan lp = zeta::list_plan(N, topk);
+  if (causal && lp.levels > 0) {
+    const zeta::QueryOrderWs ws = zeta::query_order_ws(n_segments, N);
+    if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
+  }
+  return hip_status(zeta::launch_query_order(q_order, n_segments, N, topk, causal != 0, order_out, workspace, stream));
+}
+
 zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
                                int64_t n_segments, int64_t N, int topk, int causal, const int32_t* q_order,
                                int32_t* idx, void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -102,8 +116,10 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
   // Room to sort the query codes together with the key codes (2*B*H segments).
   const size_t sb = zeta::sort_ws(2 * S, N, d_k * bits).bytes;
   const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
+  const size_t ob = zeta::query_order_ws(S, N).bytes;
   if (sb > bytes) bytes = sb;
   if (lb > bytes) bytes = lb;
+  if (ob > bytes) bytes = ob;
   return bytes;
 }
 

@@ -22,6 +22,7 @@ ZETA_F32, ZETA_BF16 = 0, 1
 EXPORTED = (
     "zeta_morton_encode",
     "zeta_sort_keys",
+    "zeta_query_order",
     "zeta_select_topk",
     "zeta_topk_attn_fwd",
     "zeta_workspace_size",
@@ -52,11 +53,13 @@ def load_library() -> ctypes.CDLL:
     vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     L.zeta_morton_encode.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     L.zeta_sort_keys.argtypes = [vp, i64, i64, i32, vp, vp, vp, sz, vp]
+    L.zeta_query_order.argtypes = [vp, i64, i64, i32, i32, vp, vp, sz, vp]
     L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp]
     L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, f32, vp, vp]
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
-    for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_select_topk", "zeta_topk_attn_fwd"):
+    for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
+                 "zeta_topk_attn_fwd"):
         getattr(L, name).restype = ctypes.c_int
     L.zeta_workspace_size.restype = sz
     L.zeta_status_string.restype = ctypes.c_char_p
@@ -151,6 +154,24 @@ def zeta_sort_keys(k_codes: torch.Tensor, code_bits: int, *, sorted_codes: Optio
     return sorted_codes, perm
 
 
+def zeta_query_order(q_order: Optional[torch.Tensor], N: int, S: int, topk: int, causal: bool, *,
+                     order_out: Optional[torch.Tensor] = None, device=None,
+                     workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Regroup a processing order (int32 [..., N]; None: position order) by the
+    list level each query searches -> int32 order of the same shape."""
+    dev = q_order.device if q_order is not None else device
+    if order_out is None:
+        shape = q_order.shape if q_order is not None else (S, N)
+        order_out = torch.empty(shape, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = workspace_for(S, 1, N, 1, 1, topk, causal, dev)
+    _need_device(q_order, order_out, workspace)
+    st = load_library().zeta_query_order(_ptr(q_order), S, N, topk, int(bool(causal)), _ptr(order_out),
+                                         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream())
+    _check("zeta_query_order", st)
+    return order_out
+
+
 def zeta_select_topk(q_codes: torch.Tensor, sorted_codes: torch.Tensor, perm: torch.Tensor, topk: int,
                      causal: bool, *, q_order: Optional[torch.Tensor] = None, idx: Optional[torch.Tensor] = None,
                      workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
@@ -195,8 +216,8 @@ def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: f
     """The whole forward: encode, sort, select, attend (four calls, one stream).
 
     The query codes are sorted together with the key codes (one call over
-    2*B*H segments) and their order drives select and attend (``zorder``);
-    the result is the same either way.  ``buffers`` (from ``alloc_buffers``)
+    2*B*H segments); their Z-order, regrouped by list level, drives select
+    and attend (``zorder``).  The result is the same either way.  ``buffers`` (from ``alloc_buffers``)
     holds preallocated outputs so that repeated calls allocate nothing.
     """
     B, H, N, dk = q.shape
@@ -207,7 +228,8 @@ def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: f
     if zorder:
         sc2, perm2 = zeta_sort_keys(b["codes"], dk * bits, sorted_codes=b["sorted_codes2"], perm=b["perm2"],
                                     workspace=workspace)
-        sc, perm, order = sc2[1], perm2[1], perm2[0]
+        sc, perm = sc2[1], perm2[1]
+        order = zeta_query_order(perm2[0], N, B * H, topk, causal, order_out=b["order"], workspace=workspace)
     else:
         sc, perm = zeta_sort_keys(kc, dk * bits, sorted_codes=b["sorted_codes2"][1], perm=b["perm2"][1],
                                   workspace=workspace)
@@ -226,6 +248,7 @@ def alloc_buffers(B: int, H: int, N: int, dv: int, topk: int, dtype: torch.dtype
         codes=torch.empty((2, B, H, N), dtype=torch.uint32, device=device),
         sorted_codes2=torch.empty((2, B, H, N), dtype=torch.uint32, device=device),
         perm2=torch.empty((2, B, H, N), dtype=torch.int32, device=device),
+        order=torch.empty((B, H, N), dtype=torch.int32, device=device),
         idx=torch.empty((B, H, N, topk), dtype=torch.int32, device=device),
         out=torch.empty((B, H, N, dv), dtype=dtype, device=device),
     )

@@ -79,6 +79,12 @@ def _sort(**kw):
     return zeta.load_library().zeta_sort_keys(*a.values())
 
 
+def _qord(**kw):
+    a = dict(q_order=P, S=2, N=100, topk=8, causal=1, order_out=P2, ws=P3, ws_bytes=BIG, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_query_order(*a.values())
+
+
 def _sel(**kw):
     a = dict(q_codes=P, sorted_codes=P2, perm=P3, S=2, N=100, topk=8, causal=1, q_order=NULL, idx=P4, ws=P,
              ws_bytes=BIG, stream=NULL)
@@ -146,3 +152,14 @@ ATTEND_CASES = [
 @pytest.mark.parametrize("kw,code", ATTEND_CASES, ids=[str(c[0]) for c in ATTEND_CASES])
 def test_attend_rejects(kw, code):
     assert _att(**kw) == code
+
+
+QORDER_CASES = [
+    (dict(order_out=NULL), INV), (dict(S=0), INV), (dict(N=0), INV), (dict(topk=0), INV), (dict(causal=3), INV),
+    (dict(topk=1025), UNS), (dict(ws=NULL), WSP), (dict(ws_bytes=16), WSP),
+]
+
+
+@pytest.mark.parametrize("kw,code", QORDER_CASES, ids=[str(c[0]) for c in QORDER_CASES])
+def test_query_order_rejects(kw, code):
+    assert _qord(**kw) == code

@@ -387,3 +387,66 @@ def test_forward_zorder_matches_position_order():
     torch.cuda.synchronize()
     assert torch.equal(a["idx"], b["idx"])
     assert torch.equal(a["out"].view(torch.int16), b["out"].view(torch.int16))
+
+
+# ----------------------------------------------------------------------------
+# Query order by list level; tiled and per-query attend kernels
+# ----------------------------------------------------------------------------
+
+def _expected_level_order(z, N, topk, causal):
+    """Regroup a per-segment order by the level of the list each query searches."""
+    t0 = max(0, (topk - 1).bit_length())
+    t_hi = (N - 1).bit_length() - 1
+    if not causal or t0 > t_hi:
+        return z
+    lvl = np.array([min(max(t0, i.bit_length()), t_hi + 1) for i in range(N)])
+    return np.stack([zs[np.argsort(lvl[zs], kind="stable")] for zs in z])
+
+
+@pytest.mark.parametrize("N,topk,causal", [(65536, 128, True), (5000, 64, True), (300, 1024, True), (777, 8, False),
+                                           (1, 1, True), (4097, 1, True)])
+def test_query_order(N, topk, causal):
+    log(f"query order N={N} k={topk} causal={causal}")
+    S = 3
+    rng = np.random.default_rng(N + topk)
+    z = np.stack([rng.permutation(N) for _ in range(S)]).astype(np.int32)
+    got = host(zeta.zeta_query_order(i32_to_dev(z), N, S, topk, causal))
+    assert np.array_equal(got, _expected_level_order(z, N, topk, causal))
+    pos = host(zeta.zeta_query_order(None, N, S, topk, causal, device=device()))
+    assert np.array_equal(pos, _expected_level_order(np.tile(np.arange(N, dtype=np.int32), (S, 1)), N, topk, causal))
+
+
+@pytest.mark.parametrize("cfg", [2, 4, 5])
+@pytest.mark.parametrize("order_kind", ["level", "shuffled"])
+def test_attend_kernels_agree(cfg, order_kind, monkeypatch):
+    """The tiled kernel (LDS-staged shared rows, global fallback for the rest)
+    and the per-query kernel both match the oracle; a shuffled order makes the
+    tiles share little, so most rows take the fallback."""
+    w, x, f = inputs(cfg)
+    log(f"attend kernels config {cfg} order {order_kind}")
+    oc = oracle_codes(cfg)
+    S = w.segments
+    if order_kind == "level":
+        z = np.argsort(oc["q_codes"], axis=1, kind="stable").astype(np.int32)
+        order = _expected_level_order(z, w.N, w.topk, True)
+    else:
+        rng = np.random.default_rng(cfg)
+        order = np.stack([rng.permutation(w.N) for _ in range(S)]).astype(np.int32)
+    sc, perm = u32_to_dev(oc["sorted_codes"]), i32_to_dev(oc["perm"])
+    idx = zeta.zeta_select_topk(u32_to_dev(oc["q_codes"]), sc, perm, w.topk, True, q_order=i32_to_dev(order))
+    q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
+    idx4 = idx.reshape(w.B, w.H, w.N, w.topk)
+    out_t = zeta.zeta_topk_attn_fwd(q, k, v, idx4, 0.5, q_order=i32_to_dev(order))
+    monkeypatch.setenv("ZETA_ATTEND", "direct")
+    out_d = zeta.zeta_topk_attn_fwd(q, k, v, idx4, 0.5, q_order=i32_to_dev(order))
+    torch.cuda.synchronize()
+    a, b = host(out_t).reshape(S, w.N, w.dv), host(out_d).reshape(S, w.N, w.dv)
+    assert np.abs(a - b).max() <= TOL[w.dtype]
+    ih = host(idx).reshape(S, w.N, w.topk)
+    if cfg != 5:
+        assert np.array_equal(ih, oracle_select(cfg, True))
+    rows = sample_rows(w.N, 64, cfg)
+    for s in range(0, S, max(1, S // 4)):
+        ref = oracle.attend(f["q"][s:s + 1], f["k"][s:s + 1], f["v"][s:s + 1], ih[s:s + 1, rows], 0.5, rows=rows)[0]
+        assert np.abs(a[s, rows] - ref).max() <= TOL[w.dtype], s
+        assert np.abs(b[s, rows] - ref).max() <= TOL[w.dtype], s
