@@ -1,14 +1,16 @@
 """Benchmark of the Z-order top-k attention forward on one MI355X.
 
-One step is the whole forward (encode, sort of the query and key codes,
-select, attend: four C ABI calls on one stream) over one batch of the long-context workload (B=1, H=16,
+One step is the whole forward (encode, sort of the query and key codes, the
+processing order, then select and attend in one pass: C ABI calls on one
+stream) over one batch of the long-context workload (B=1, H=16,
 N=65536, d_k=3, d_v=128, k=128, bf16, 6 bits per axis, causal), with inputs,
 outputs and workspace resident in HBM before timing starts.
 
 Prints one JSON line: query-tokens/s (B*N per second) of the whole step, the
-attend kernel's achieved algorithmic bandwidth against the HBM peak (timed with
-HIP events on the stream it runs on), and the CPU oracle timed on a bounded
-sample of the same workload on the host's cores.
+dominant kernel's achieved algorithmic bandwidth against the HBM peak (timed
+with HIP events on the stream it runs on), the same step through the separate
+select and attend calls, and the CPU oracle timed on a bounded sample of the
+same workload on the host's cores.
 """
 
 from __future__ import annotations
@@ -28,8 +30,9 @@ sys.path.insert(0, ROOT)
 import workloads  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
-ATTEND_SRC = os.path.join(ROOT, "paper_2501_14577_amd", "csrc", "attend.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_long_context_traffic.txt")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2501_14577_amd", "csrc", n)
+               for n in ("fused.hip", "select_device.h", "attend_device.h", "device_common.h")]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "select_attend_long_context_traffic.txt")
 
 
 def elem_size(dtype: str) -> int:
@@ -64,9 +67,17 @@ def step_bytes(w: workloads.Workload, causal: bool) -> int:
     return attend_bytes(w, causal) + rows * ((4 * d * s + 8) + 16 * passes + (4 + 8 * w.topk))
 
 
-def read_traffic(launch_bytes: int):
-    """HBM bytes per attend launch from the committed rocprofv3 counter
-    summary, or None when absent or taken on a different attend source."""
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
+
+
+def read_traffic():
+    """HBM bytes per launch of the one-pass select-and-attend kernel, from the
+    committed rocprofv3 counter summary; None when absent or taken on
+    different kernel sources."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     kv = {}
@@ -74,8 +85,7 @@ def read_traffic(launch_bytes: int):
         if ":" in line and not line.startswith("#"):
             key, val = line.split(":", 1)
             kv[key.strip()] = val.strip()
-    src = hashlib.sha256(open(ATTEND_SRC, "rb").read()).hexdigest()
-    if kv.get("attend_source_sha256") != src:
+    if kv.get("kernel_source_sha256") != kernel_source_hash():
         return None
     try:
         return int(float(kv["hbm_bytes_per_launch"]))
@@ -159,6 +169,19 @@ def main() -> int:
 
     codes, sorted2, perm2 = bufs["codes"], bufs["sorted_codes2"], bufs["perm2"]
 
+    def step_fused(ev=None):
+        # encode -> joint sort -> processing order -> select and attend in one pass
+        qc, kc = zeta.zeta_morton_encode(q, k, w.bits, q_codes=codes[0], k_codes=codes[1], workspace=ws)
+        zeta.zeta_sort_keys(codes, w.code_bits, sorted_codes=sorted2, perm=perm2, workspace=ws)
+        order = zeta.zeta_query_order(perm2[0], w.N, w.segments, w.topk, causal, order_out=bufs["order"],
+                                      workspace=ws)
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_select_attend_fwd(q, k, v, qc, sorted2[1], perm2[1], w.topk, causal, eps, q_order=order,
+                                    out=bufs["out"], workspace=ws)
+        if ev is not None:
+            ev[1].record()
+
     def step(ev=None):
         # encode -> joint sort of query and key codes -> the query Z-order
         # regrouped by list level (processing order) -> select -> attend
@@ -174,26 +197,29 @@ def main() -> int:
         if ev is not None:
             ev[1].record()
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        start.record()
+        for i in range(args.steps):
+            fn(evs[i])
+        stop.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        return (start.elapsed_time(stop) / args.steps, float(np.mean([a.elapsed_time(b) for a, b in evs])), wall)
 
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    start.record()
-    for i in range(args.steps):
-        step(evs[i])
-    stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-
-    ms_per_step = start.elapsed_time(stop) / args.steps
-    attend_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    four_ms, attend_ms, _ = timed(step)
+    ms_per_step, fused_ms, wall = timed(step_fused)
     tokens = w.B * w.N
     a_bytes = attend_bytes(w, causal)
-    achieved = a_bytes / (attend_ms * 1e-3) / 1e9
+    f_bytes = a_bytes + w.segments * w.N * 4  # plus each query's code, read instead of an index row
+    achieved = f_bytes / (fused_ms * 1e-3) / 1e9
     s_bytes = step_bytes(w, causal)
 
     cpu = None
@@ -222,14 +248,20 @@ def main() -> int:
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "attend",
+            "kernel": "select_attend (one pass)",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": read_traffic(a_bytes),
-            "algorithmic_bytes_per_launch": a_bytes,
+            "traffic": read_traffic(),
+            "algorithmic_bytes_per_launch": f_bytes,
+            "kernel_ms": fused_ms,
+        },
+        "four_call_path": {
+            "ms_per_step": four_ms,
+            "value": tokens / (four_ms * 1e-3),
             "attend_ms": attend_ms,
+            "attend_achieved_GBs": a_bytes / (attend_ms * 1e-3) / 1e9,
         },
         "step_hbm_frac": s_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "step_algorithmic_bytes": s_bytes,

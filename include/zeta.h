@@ -12,6 +12,9 @@
  *   zeta_select_topk    -> k candidate keys per query around its insertion point
  *   zeta_topk_attn_fwd  -> Cauchy-softmax attention over the candidates
  *
+ * zeta_select_attend_fwd runs the last two in one pass (the candidates never
+ * leave the chip); zeta_query_order prepares the fast processing order.
+ *
  * Conventions shared by every call:
  *
  * - A "segment" is one (batch, head) pair; B*H segments are independent and
@@ -147,9 +150,8 @@ zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64
  *                 outputs of zeta_sort_keys for the same key codes.
  *   q_order       optional int32 [n_segments][N]: the order in which queries
  *                 are processed, a permutation of 0..N-1 per segment (NULL:
- *                 position order).  It changes no result; the queries' own
- *                 codes in ascending order (zeta_sort_keys applied to q_codes)
- *                 give neighbouring queries overlapping windows and make the
+ *                 position order).  It changes no result; zeta_query_order
+ *                 gives neighbouring queries overlapping windows and makes the
  *                 call faster.  Entries outside 0..N-1 are skipped.
  *   idx           int32 [n_segments][N][topk] output, indexed by position.
  *   topk          1..ZETA_MAX_TOPK; causal 0 or 1.
@@ -171,7 +173,9 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  *   q, k   [B][H][N][d_k], v [B][H][N][d_v], out [B][H][N][d_v], all `dtype`.
  *   idx      int32 [B*H][N][topk]; valid entries (0 <= j < N) first, then -1.
  *   q_order  optional int32 [B*H][N] processing order, as for
- *            zeta_select_topk (NULL: position order; no result depends on it).
+ *            zeta_select_topk (NULL: position order).  Neighbouring queries
+ *            of zeta_query_order's order gather mostly the same value rows,
+ *            which then come from cache; the output bits do not depend on it.
  *   eps      gamma^2: finite and > 0.
  *
  * Supported d_v: 32, 64, 128, 256.  v and out must be 16-byte aligned; out
@@ -181,6 +185,26 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
                                  int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
                                  const int32_t* idx, const int32_t* q_order, float eps, void* out,
                                  hipStream_t stream);
+
+/*
+ * zeta_select_attend_fwd -- zeta_select_topk and zeta_topk_attn_fwd in one
+ * pass (same definitions, Section 3.2.2 and Algorithm 1, Steps 3-5; Section
+ * 3.3, equation cauchy; Section 3.4; Appendix E.1).  Each query's window stays
+ * on chip instead of travelling through an index tensor; `out` holds the same
+ * bits that the two calls would produce.
+ *
+ *   q, k, v, dtype, B, H, N, d_k, d_v, topk, eps, out: as for
+ *            zeta_topk_attn_fwd; causal as for zeta_select_topk.
+ *   q_codes, sorted_codes, perm, q_order: as for zeta_select_topk.
+ *   idx_out  optional int32 [B*H][N][topk]: receives the windows.
+ *   workspace  at least zeta_workspace_size(...) bytes.
+ */
+zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
+                                     int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
+                                     int causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
+                                     const int32_t* perm, const int32_t* q_order, float eps, void* out,
+                                     int32_t* idx_out, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream);
 
 /*
  * zeta_workspace_size -- bytes of device workspace enough for each of

@@ -13,6 +13,8 @@ from .zeta import (  # noqa: F401
     load_library,
     workspace_for,
     zeta_morton_encode,
+    zeta_query_order,
+    zeta_select_attend_fwd,
     zeta_select_topk,
     zeta_sort_keys,
     zeta_status_string,

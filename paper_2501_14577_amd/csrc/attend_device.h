@@ -1,0 +1,111 @@
+// Device-side row access shared by the attend and fused select-and-attend
+// kernels: 16-byte lane loads of value rows widened to float32, one-load key
+// and query rows for d_k = 3, and row offsets.
+#pragma once
+
+#include <stdint.h>
+
+#include "device_common.h"
+
+namespace zeta {
+namespace {
+
+template <typename T>
+struct Vec16;  // one 16-byte lane load of a value row, widened to float32
+
+template <>
+struct Vec16<float> {
+  static constexpr int kElems = 4;
+  __device__ __forceinline__ static void widen(const uint4& x, float* f) {
+    f[0] = __uint_as_float(x.x);
+    f[1] = __uint_as_float(x.y);
+    f[2] = __uint_as_float(x.z);
+    f[3] = __uint_as_float(x.w);
+  }
+  __device__ __forceinline__ static void store(float* p, const float* f) {
+    *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
+  }
+};
+
+template <>
+struct Vec16<uint16_t> {
+  static constexpr int kElems = 8;
+  __device__ __forceinline__ static void widen(const uint4& x, float* f) {
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ __forceinline__ static void store(uint16_t* p, const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = uint32_t(float_to_bf16_bits(f[2 * i])) | (uint32_t(float_to_bf16_bits(f[2 * i + 1])) << 16);
+    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+
+// The three coordinates of row `row` of a [rows][3] array, widened to
+// float32, with one memory instruction: a float32 row is one 12-byte load; a
+// bfloat16 row (6 bytes, 2-byte aligned) lies inside the 8 bytes starting at
+// the 4-byte boundary at or below it, except that the array's very last row
+// may end 2 bytes before that window does, so it is read element by element.
+struct alignas(4) Words2 {
+  uint32_t a, b;
+};
+struct alignas(4) Floats3 {
+  float x, y, z;
+};
+
+template <typename T>
+struct Row3;
+
+template <>
+struct Row3<float> {
+  __device__ __forceinline__ static void load(const float* base, int64_t row, int64_t /*rows*/, float* f) {
+    const Floats3 r = *reinterpret_cast<const Floats3*>(base + row * 3);
+    f[0] = r.x;
+    f[1] = r.y;
+    f[2] = r.z;
+  }
+};
+
+template <>
+struct Row3<uint16_t> {
+  __device__ __forceinline__ static void load(const uint16_t* base, int64_t row, int64_t rows, float* f) {
+    const int64_t e = row * 3;
+    const int64_t a = e & ~int64_t(1);
+    if (a + 4 <= rows * 3) {
+      const Words2 w = *reinterpret_cast<const Words2*>(base + a);
+      if (e == a) {
+        f[0] = __uint_as_float(w.a << 16);
+        f[1] = __uint_as_float(w.a & 0xFFFF0000u);
+        f[2] = __uint_as_float(w.b << 16);
+      } else {
+        f[0] = __uint_as_float(w.a & 0xFFFF0000u);
+        f[1] = __uint_as_float(w.b << 16);
+        f[2] = __uint_as_float(w.b & 0xFFFF0000u);
+      }
+    } else {
+      f[0] = bf16_bits_to_float(base[e]);
+      f[1] = bf16_bits_to_float(base[e + 1]);
+      f[2] = bf16_bits_to_float(base[e + 2]);
+    }
+  }
+};
+
+// Byte offset of a value row inside its segment: 32-bit when the segment's
+// values span less than 4 GiB, else 64-bit.
+template <bool kOff32>
+struct RowOff {
+  using type = int64_t;
+};
+template <>
+struct RowOff<true> {
+  using type = uint32_t;
+};
+
+}  // namespace
+}  // namespace zeta

@@ -35,6 +35,18 @@ hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, 
                          int64_t S, int64_t N, int topk, bool causal, const int32_t* q_order, int32_t* idx,
                          void* workspace, hipStream_t stream);
 
+// Doubling prefix lists of causal selection in the workspace (none when
+// every query searches the full list: *list_codes stays NULL).
+hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm, int64_t S, int64_t N, int topk,
+                               void* workspace, hipStream_t stream, const uint32_t** list_codes,
+                               const int32_t** list_pos);
+
+// Select and attend in one pass (idx_out optional).
+hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,
+                                int dk, int dv, int topk, bool causal, const uint32_t* q_codes,
+                                const uint32_t* sorted_codes, const int32_t* perm, const int32_t* q_order,
+                                float eps, void* out, int32_t* idx_out, void* workspace, hipStream_t stream);
+
 // Cauchy-softmax attention over the selected rows.
 hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
                          int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,

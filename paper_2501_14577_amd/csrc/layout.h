@@ -31,7 +31,7 @@ constexpr int kSelRun = 32;  // consecutive processing-order slots served by one
 constexpr int kMaxLevels = 32;
 
 // ---- attend ---------------------------------------------------------------
-constexpr int kAttWavesPerBlock = 4;
+constexpr int kAttWavesPerBlock = 8;
 
 inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 

@@ -37,11 +37,11 @@
 #include "device_common.h"
 #include "kernels.h"
 #include "layout.h"
+#include "select_device.h"
 
 namespace zeta {
 namespace {
 
-__device__ __forceinline__ int bit_length(uint32_t x) { return x ? 32 - __clz(int(x)) : 0; }
 
 __global__ void __launch_bounds__(kSortThreads)
     list_count_kernel(const int32_t* __restrict__ perm, int64_t N, int64_t tiles, int t0, int levels,
@@ -135,119 +135,6 @@ __global__ void __launch_bounds__(kSortThreads)
   }
 }
 
-// First index in codes[lo..n) whose code is >= key, given that every entry
-// before lo is below key, found by a wavefront: each round 64 lanes probe
-// evenly spaced entries and the ballot of "probe < key" (a prefix of the
-// lanes, the list being sorted) narrows the range 64x.
-__device__ __forceinline__ int32_t wave_lower_bound(const uint32_t* __restrict__ codes, int32_t lo, int32_t n,
-                                                    uint32_t key, int lane) {
-  int32_t hi = n;
-  while (hi > lo) {
-    const int32_t len = hi - lo;
-    const int32_t stride = (len + 63) >> 6;
-    const int32_t x = lo + lane * stride;
-    const bool probe = x < hi;
-    const bool less = probe && codes[x] < key;
-    const int cnt = __popcll(wave_ballot(less));
-    if (cnt == 0) {
-      hi = lo;
-    } else {
-      const int32_t next_hi = lo + cnt * stride;
-      lo = lo + (cnt - 1) * stride + 1;
-      hi = next_hi < hi ? next_hi : hi;
-    }
-  }
-  return lo;
-}
-
-// The same search when the answer is expected just after `lo` (the previous
-// query's insertion point in the same list, for a code no smaller): probe the
-// 64 entries from lo first, and fall back to the 64-way search beyond them.
-__device__ __forceinline__ int32_t wave_lower_bound_near(const uint32_t* __restrict__ codes, int32_t lo,
-                                                         int32_t n, uint32_t key, int lane) {
-  const int32_t x = lo + lane;
-  const bool less = x < n && codes[x] < key;
-  const int cnt = __popcll(wave_ballot(less));
-  if (cnt < 64) return lo + cnt;
-  return wave_lower_bound(codes, lo + 64, n, key, lane);
-}
-
-// Chunks of 64 list entries fetched on each side of the insertion point
-// before the scans start, so that the common case needs one round trip.
-constexpr int kPre = 2;
-
-// Append up to `need` in-pool entries (position <= limit), in list order,
-// from the 64 entries whose positions this wavefront holds in `pv` (entry
-// cur + lane; out-of-list lanes hold INT_MAX) to buf[got..].  Returns the new
-// count; `cur` ends just past the last entry taken, or 64 further on.
-__device__ __forceinline__ int take_right(int32_t pv, int32_t limit, int32_t n, int32_t& cur, int need, int got,
-                                          int32_t* buf) {
-  const bool ok = pv <= limit;
-  const uint64_t bal = wave_ballot(ok);
-  const int avail = __popcll(bal);
-  const int want = need - got;
-  const int take = avail < want ? avail : want;
-  const int slot = int(lanes_below(bal));
-  if (ok && slot < take) buf[got + slot] = pv;
-  if (take < avail) {
-    // Stop just past the take-th in-pool entry of this chunk.
-    const uint64_t last = wave_ballot(ok && slot == take - 1);
-    cur = cur + (__ffsll((unsigned long long)last) - 1) + 1;
-  } else {
-    cur = cur + 64 < n ? cur + 64 : n;
-  }
-  return got + take;
-}
-
-// Collect up to `need` in-pool entries, nearest first, from the 64 entries
-// cur-64 .. cur-1 held in `pv` (out-of-list lanes hold INT_MAX), into
-// buf[cap_end-1-got], buf[cap_end-2-got], ... so that the collected run ends at
-// buf[cap_end-1] in ascending list order.  Returns the new count.
-__device__ __forceinline__ int take_left(int32_t pv, int32_t limit, int need, int got, int32_t* buf, int cap_end) {
-  const bool ok = pv <= limit;
-  const uint64_t bal = wave_ballot(ok);
-  const int avail = __popcll(bal);
-  const int want = need - got;
-  const int take = avail < want ? avail : want;
-  const int from_top = avail - 1 - int(lanes_below(bal));
-  if (ok && from_top < take) buf[cap_end - 1 - (got + from_top)] = pv;
-  return got + take;
-}
-
-// Scan entries cur, cur+1, ... of pos[0..n) and append up to `need` in-pool
-// ones to buf[got..].  Returns the new count; `cur` is left just past the
-// last entry taken (or at n).
-__device__ __forceinline__ int scan_right(const int32_t* __restrict__ pos, int32_t n, int32_t limit,
-                                          int32_t& cur, int need, int got, int32_t* buf, int lane) {
-  while (got < need && cur < n) {
-    const int32_t e = cur + lane;
-    const int32_t pv = e < n ? pos[e] : INT32_MAX;
-    got = take_right(pv, limit, n, cur, need, got, buf);
-  }
-  return got;
-}
-
-// Scan entries cur-1, cur-2, ... and collect up to `need` in-pool entries,
-// nearest first, after the `got` already collected (see take_left).
-__device__ __forceinline__ int scan_left(const int32_t* __restrict__ pos, int32_t limit, int32_t cur, int need,
-                                         int got, int32_t* buf, int cap_end, int lane) {
-  while (got < need && cur > 0) {
-    const int32_t e = cur - 64 + lane;
-    const int32_t pv = e >= 0 ? pos[e] : INT32_MAX;
-    got = take_left(pv, limit, need, got, buf, cap_end);
-    cur -= 64;
-  }
-  return got;
-}
-
-// Level of the list a causal query at position i searches: t0..t_hi for the
-// prefix lists, t_hi + 1 for the full sorted list.
-__device__ __forceinline__ int query_level(int32_t i, int t0, int t_hi) {
-  const int bl = bit_length(uint32_t(i));
-  const int t = bl > t0 ? bl : t0;
-  return t <= t_hi ? t : t_hi + 1;
-}
-
 __global__ void __launch_bounds__(256)
     level_class_kernel(const int32_t* __restrict__ q_order, int64_t total, int64_t N, int t0, int t_hi,
                        uint32_t* __restrict__ cls) {
@@ -276,7 +163,6 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
   const int wave = threadIdx.x >> 6;
   int32_t* lbuf = s_sel + wave * 2 * topk;  // left part, filled from its end
   int32_t* rbuf = lbuf + topk;              // right part, filled from its start
-  const int half = topk / 2;
   const int64_t runs = (total + kSelRun - 1) / kSelRun;
 
   const int64_t nb = gridDim.x;
@@ -310,57 +196,14 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
       const int64_t seg = slot / N;
       const int64_t g = seg * N + i;
 
-      const uint32_t* codes = sorted_codes + seg * N;
-      const int32_t* pos = perm + seg * N;
-      int32_t n = int32_t(N);
-      int32_t limit = int32_t(N - 1);  // every position is in the non-causal pool
-      if (causal) {
-        limit = i;
-        const int t = query_level(i, t0, t_hi);
-        if (t <= t_hi) {
-          const int64_t off = seg * cap + ((int64_t(1) << t) - (int64_t(1) << t0));
-          codes = list_codes + off;
-          pos = list_pos + off;
-          n = int32_t(1) << t;
-        }
-      }
-
-      const int32_t p = (codes == prev_codes && key >= prev_key) ? wave_lower_bound_near(codes, prev_p, n, key, lane)
-                                                                 : wave_lower_bound(codes, 0, n, key, lane);
-      prev_codes = codes;
+      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap);
+      const int32_t p = (L.codes == prev_codes && key >= prev_key) ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
+                                                                   : wave_lower_bound(L.codes, 0, L.n, key, lane);
+      prev_codes = L.codes;
       prev_key = key;
       prev_p = p;
-      // floor(k/2) pool keys before p and the rest from p on, shifted inward
-      // when one side of the pool runs out.  The first kPre chunks on each
-      // side are fetched together; further chunks are fetched as needed.
-      int32_t pre_r[kPre], pre_l[kPre];
-#pragma unroll
-      for (int c = 0; c < kPre; ++c) {
-        const int32_t er = p + c * 64 + lane;
-        const int32_t el = p - (c + 1) * 64 + lane;
-        pre_r[c] = er < n ? pos[er] : INT32_MAX;
-        pre_l[c] = el >= 0 ? pos[el] : INT32_MAX;
-      }
-      const int need_r = topk - half;
-      int32_t cur_r = p;
-      int got_r = 0;
-#pragma unroll
-      for (int c = 0; c < kPre; ++c)
-        if (got_r < need_r && cur_r < n) got_r = take_right(pre_r[c], limit, n, cur_r, need_r, got_r, rbuf);
-      got_r = scan_right(pos, n, limit, cur_r, need_r, got_r, rbuf, lane);
-      const int need_l = half + (need_r - got_r);
-      int got_l = 0;
-      int32_t cur_l = p;
-#pragma unroll
-      for (int c = 0; c < kPre; ++c) {
-        if (got_l < need_l && cur_l > 0) {
-          got_l = take_left(pre_l[c], limit, need_l, got_l, lbuf, topk);
-          cur_l -= 64;
-        }
-      }
-      got_l = scan_left(pos, limit, cur_l, need_l, got_l, lbuf, topk, lane);
-      if (got_l < need_l && got_r == need_r)
-        got_r = scan_right(pos, n, limit, cur_r, topk - got_l, got_r, rbuf, lane);
+      int got_l, got_r;
+      select_window(L, p, topk, lbuf, rbuf, lane, got_l, got_r);
       wave_lds_sync();
 
       int32_t* row = idx + g * topk;
@@ -403,24 +246,38 @@ hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int 
   return launch_stable_partition(cls, given, S, N, nbits, cls_sorted, order_out, phist, stream);
 }
 
+hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm, int64_t S, int64_t N, int topk,
+                               void* workspace, hipStream_t stream, const uint32_t** list_codes,
+                               const int32_t** list_pos) {
+  const ListPlan lp = list_plan(N, topk);
+  *list_codes = nullptr;
+  *list_pos = nullptr;
+  if (lp.levels == 0) return hipSuccess;
+  const SelectWs ws = select_ws(S, N, topk, 1);
+  char* wsb = static_cast<char*>(workspace);
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(wsb + ws.cnt_off);
+  uint32_t* lc = reinterpret_cast<uint32_t*>(wsb + ws.codes_off);
+  int32_t* lpos = reinterpret_cast<int32_t*>(wsb + ws.pos_off);
+  const int64_t tiles = ceil_div(N, kSortTile);
+  const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
+  hipLaunchKernelGGL(list_count_kernel, grid, block, 0, stream, perm, N, tiles, lp.t0, lp.levels, cnt);
+  hipLaunchKernelGGL(list_scatter_kernel, grid, block, 0, stream, sorted_codes, perm, N, tiles, lp.t0, lp.levels,
+                     lp.cap, cnt, lc, lpos);
+  *list_codes = lc;
+  *list_pos = lpos;
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
                          int64_t S, int64_t N, int topk, bool causal, const int32_t* q_order, int32_t* idx,
                          void* workspace, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
-  const SelectWs ws = select_ws(S, N, topk, causal ? 1 : 0);
   const int64_t total = S * N;
-  uint32_t* list_codes = nullptr;
-  int32_t* list_pos = nullptr;
-  if (causal && lp.levels > 0) {
-    char* wsb = static_cast<char*>(workspace);
-    uint32_t* cnt = reinterpret_cast<uint32_t*>(wsb + ws.cnt_off);
-    list_codes = reinterpret_cast<uint32_t*>(wsb + ws.codes_off);
-    list_pos = reinterpret_cast<int32_t*>(wsb + ws.pos_off);
-    const int64_t tiles = ceil_div(N, kSortTile);
-    const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
-    hipLaunchKernelGGL(list_count_kernel, grid, block, 0, stream, perm, N, tiles, lp.t0, lp.levels, cnt);
-    hipLaunchKernelGGL(list_scatter_kernel, grid, block, 0, stream, sorted_codes, perm, N, tiles, lp.t0,
-                       lp.levels, lp.cap, cnt, list_codes, list_pos);
+  const uint32_t* list_codes = nullptr;
+  const int32_t* list_pos = nullptr;
+  if (causal) {
+    const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
+    if (e != hipSuccess) return e;
   }
   const int64_t runs = ceil_div(total, kSelRun);
   const int64_t want = ceil_div(runs, kSelWavesPerBlock);

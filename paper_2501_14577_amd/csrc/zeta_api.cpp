@@ -109,6 +109,26 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
                                         out, stream));
 }
 
+zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
+                                     int64_t H, int64_t N, int d_k, int d_v, int topk, int causal,
+                                     const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out,
+                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!q || !k || !v || !out || !q_codes || !sorted_codes || !perm) return ZETA_ERR_INVALID_ARG;
+  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || d_v < 1 || topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
+  if (!aligned16(v) || !aligned16(out)) return ZETA_ERR_INVALID_ARG;
+  if (out == q || out == k || out == v) return ZETA_ERR_INVALID_ARG;
+  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
+  if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
+  const int64_t S = B * H;
+  const zeta::SelectWs ws = zeta::select_ws(S, N, topk, causal);
+  if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
+  return hip_status(zeta::launch_select_attend(q, k, v, dtype == ZETA_BF16, S, N, d_k, d_v, topk, causal != 0, q_codes,
+                                               sorted_codes, perm, q_order, eps, out, idx_out, workspace, stream));
+}
+
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk, int causal) {
   if (bad_count(B, H, N) || d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32 || topk < 1) return 0;
   const int64_t S = B * H;

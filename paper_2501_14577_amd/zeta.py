@@ -25,6 +25,7 @@ EXPORTED = (
     "zeta_query_order",
     "zeta_select_topk",
     "zeta_topk_attn_fwd",
+    "zeta_select_attend_fwd",
     "zeta_workspace_size",
     "zeta_status_string",
 )
@@ -56,10 +57,12 @@ def load_library() -> ctypes.CDLL:
     L.zeta_query_order.argtypes = [vp, i64, i64, i32, i32, vp, vp, sz, vp]
     L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp]
     L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, f32, vp, vp]
+    L.zeta_select_attend_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, f32,
+                                         vp, vp, vp, sz, vp]
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
     for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
-                 "zeta_topk_attn_fwd"):
+                 "zeta_topk_attn_fwd", "zeta_select_attend_fwd"):
         getattr(L, name).restype = ctypes.c_int
     L.zeta_workspace_size.restype = sz
     L.zeta_status_string.restype = ctypes.c_char_p
@@ -210,14 +213,39 @@ def zeta_topk_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
     return out
 
 
+def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_codes: torch.Tensor,
+                           sorted_codes: torch.Tensor, perm: torch.Tensor, topk: int, causal: bool, eps: float, *,
+                           q_order: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                           idx_out: Optional[torch.Tensor] = None,
+                           workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Select and attend in one pass -> out [B,H,N,d_v]; ``idx_out`` (int32
+    [B,H,N,topk]) optionally receives the windows."""
+    B, H, N, dk = q.shape
+    dv = v.shape[-1]
+    if out is None:
+        out = torch.empty((B, H, N, dv), dtype=v.dtype, device=v.device)
+    if workspace is None:
+        workspace = workspace_for(B, H, N, dk, 1, topk, causal, q.device)
+    _need_device(q, k, v, q_codes, sorted_codes, perm, q_order, out, idx_out, workspace)
+    if not (q.dtype == k.dtype == v.dtype == out.dtype):
+        raise ValueError("q, k, v and out must share a dtype")
+    st = load_library().zeta_select_attend_fwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dk, dv, topk,
+                                               int(bool(causal)), _ptr(q_codes), _ptr(sorted_codes), _ptr(perm),
+                                               _ptr(q_order), float(eps), _ptr(out), _ptr(idx_out), _ptr(workspace),
+                                               workspace.numel() * workspace.element_size(), _stream())
+    _check("zeta_select_attend_fwd", st)
+    return out
+
+
 def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: float, causal: bool = True,
             bits: int = 10, *, workspace: Optional[torch.Tensor] = None, buffers: Optional[dict] = None,
-            zorder: bool = True, return_intermediates: bool = False):
+            zorder: bool = True, fused: bool = False, return_intermediates: bool = False):
     """The whole forward: encode, sort, select, attend (four calls, one stream).
 
     The query codes are sorted together with the key codes (one call over
     2*B*H segments); their Z-order, regrouped by list level, drives select
-    and attend (``zorder``).  The result is the same either way.  ``buffers`` (from ``alloc_buffers``)
+    and attend (``zorder``).  ``fused`` runs select and attend as one pass.
+    The result is the same either way.  ``buffers`` (from ``alloc_buffers``)
     holds preallocated outputs so that repeated calls allocate nothing.
     """
     B, H, N, dk = q.shape
@@ -234,8 +262,13 @@ def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: f
         sc, perm = zeta_sort_keys(kc, dk * bits, sorted_codes=b["sorted_codes2"][1], perm=b["perm2"][1],
                                   workspace=workspace)
         order = None
-    idx = zeta_select_topk(qc, sc, perm, topk, causal, q_order=order, idx=b["idx"], workspace=workspace)
-    out = zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, out=b["out"])
+    if fused:
+        idx = b["idx"] if return_intermediates else None
+        out = zeta_select_attend_fwd(q, k, v, qc, sc, perm, topk, causal, eps, q_order=order, out=b["out"],
+                                     idx_out=idx, workspace=workspace)
+    else:
+        idx = zeta_select_topk(qc, sc, perm, topk, causal, q_order=order, idx=b["idx"], workspace=workspace)
+        out = zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, out=b["out"])
     if return_intermediates:
         return dict(q_codes=qc, k_codes=kc, sorted_codes=sc, perm=perm, q_order=order, idx=idx, out=out)
     return out

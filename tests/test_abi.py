@@ -163,3 +163,26 @@ QORDER_CASES = [
 @pytest.mark.parametrize("kw,code", QORDER_CASES, ids=[str(c[0]) for c in QORDER_CASES])
 def test_query_order_rejects(kw, code):
     assert _qord(**kw) == code
+
+
+def _fused(**kw):
+    a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, causal=1, q_codes=P4,
+             sorted_codes=ctypes.c_void_p(0x60000), perm=ctypes.c_void_p(0x70000), q_order=NULL, eps=0.5,
+             out=ctypes.c_void_p(0x50000), idx_out=NULL, ws=ctypes.c_void_p(0x80000), ws_bytes=BIG, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_select_attend_fwd(*a.values())
+
+
+FUSED_CASES = [
+    (dict(q=NULL), INV), (dict(v=NULL), INV), (dict(out=NULL), INV), (dict(q_codes=NULL), INV),
+    (dict(sorted_codes=NULL), INV), (dict(perm=NULL), INV), (dict(B=0), INV), (dict(N=0), INV),
+    (dict(d_k=0), INV), (dict(topk=0), INV), (dict(causal=-1), INV), (dict(eps=0.0), INV),
+    (dict(eps=float("nan")), INV), (dict(v=ctypes.c_void_p(0x30004)), INV), (dict(out=P), INV),
+    (dict(dtype=9), UNS), (dict(d_k=9), UNS), (dict(d_v=48), UNS), (dict(topk=1025), UNS),
+    (dict(ws=NULL), WSP), (dict(ws_bytes=32), WSP),
+]
+
+
+@pytest.mark.parametrize("kw,code", FUSED_CASES, ids=[str(c[0]) for c in FUSED_CASES])
+def test_select_attend_rejects(kw, code):
+    assert _fused(**kw) == code

@@ -344,7 +344,8 @@ def test_forward_deterministic_and_complete():
 @pytest.mark.parametrize("causal", [True, False])
 def test_processing_order_changes_nothing(causal):
     """select and attend give bit-identical results in position order, in the
-    queries' Z-order and in a random order; entries outside 0..N-1 are skipped."""
+    queries' Z-order and in a random order; entries outside 0..N-1 are
+    skipped."""
     cfg = 2
     w, x, _ = inputs(cfg)
     log(f"processing order config {cfg} causal={causal}")
@@ -360,6 +361,7 @@ def test_processing_order_changes_nothing(causal):
     for order in (zorder, shuffled):
         idx1 = zeta.zeta_select_topk(qc, sc, perm, w.topk, causal, q_order=order)
         out1 = zeta.zeta_topk_attn_fwd(q, k, v, idx0.reshape(w.B, w.H, w.N, w.topk), 0.5, q_order=order)
+        torch.cuda.synchronize()
         torch.cuda.synchronize()
         assert torch.equal(idx0, idx1)
         assert torch.equal(out0.view(torch.int16), out1.view(torch.int16))
@@ -390,7 +392,7 @@ def test_forward_zorder_matches_position_order():
 
 
 # ----------------------------------------------------------------------------
-# Query order by list level; tiled and per-query attend kernels
+# Query order by list level
 # ----------------------------------------------------------------------------
 
 def _expected_level_order(z, N, topk, causal):
@@ -416,37 +418,44 @@ def test_query_order(N, topk, causal):
     assert np.array_equal(pos, _expected_level_order(np.tile(np.arange(N, dtype=np.int32), (S, 1)), N, topk, causal))
 
 
-@pytest.mark.parametrize("cfg", [2, 4, 5])
-@pytest.mark.parametrize("order_kind", ["level", "shuffled"])
-def test_attend_kernels_agree(cfg, order_kind, monkeypatch):
-    """The tiled kernel (LDS-staged shared rows, global fallback for the rest)
-    and the per-query kernel both match the oracle; a shuffled order makes the
-    tiles share little, so most rows take the fallback."""
+
+# ----------------------------------------------------------------------------
+# Select and attend in one pass
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cfg,causal", FORWARD)
+def test_select_attend_matches_two_calls(cfg, causal):
+    """The one-pass call gives the two calls' windows and output bits."""
     w, x, f = inputs(cfg)
-    log(f"attend kernels config {cfg} order {order_kind}")
-    oc = oracle_codes(cfg)
-    S = w.segments
-    if order_kind == "level":
-        z = np.argsort(oc["q_codes"], axis=1, kind="stable").astype(np.int32)
-        order = _expected_level_order(z, w.N, w.topk, True)
-    else:
-        rng = np.random.default_rng(cfg)
-        order = np.stack([rng.permutation(w.N) for _ in range(S)]).astype(np.int32)
-    sc, perm = u32_to_dev(oc["sorted_codes"]), i32_to_dev(oc["perm"])
-    idx = zeta.zeta_select_topk(u32_to_dev(oc["q_codes"]), sc, perm, w.topk, True, q_order=i32_to_dev(order))
+    log(f"select+attend config {cfg} causal={causal}")
     q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
-    idx4 = idx.reshape(w.B, w.H, w.N, w.topk)
-    out_t = zeta.zeta_topk_attn_fwd(q, k, v, idx4, 0.5, q_order=i32_to_dev(order))
-    monkeypatch.setenv("ZETA_ATTEND", "direct")
-    out_d = zeta.zeta_topk_attn_fwd(q, k, v, idx4, 0.5, q_order=i32_to_dev(order))
+    two = zeta.forward(q, k, v, w.topk, 0.5, causal, w.bits, return_intermediates=True)
+    one = zeta.forward(q, k, v, w.topk, 0.5, causal, w.bits, fused=True, return_intermediates=True)
     torch.cuda.synchronize()
-    a, b = host(out_t).reshape(S, w.N, w.dv), host(out_d).reshape(S, w.N, w.dv)
-    assert np.abs(a - b).max() <= TOL[w.dtype]
-    ih = host(idx).reshape(S, w.N, w.topk)
-    if cfg != 5:
-        assert np.array_equal(ih, oracle_select(cfg, True))
-    rows = sample_rows(w.N, 64, cfg)
-    for s in range(0, S, max(1, S // 4)):
-        ref = oracle.attend(f["q"][s:s + 1], f["k"][s:s + 1], f["v"][s:s + 1], ih[s:s + 1, rows], 0.5, rows=rows)[0]
-        assert np.abs(a[s, rows] - ref).max() <= TOL[w.dtype], s
-        assert np.abs(b[s, rows] - ref).max() <= TOL[w.dtype], s
+    assert torch.equal(two["idx"], one["idx"])
+    assert torch.equal(two["out"].view(torch.int16), one["out"].view(torch.int16))
+    if cfg == 1:
+        ref = oracle.forward(f["q"], f["k"], f["v"], w.topk, 0.5, causal, w.bits)
+        assert np.array_equal(host(one["idx"]).reshape(w.segments, w.N, w.topk), ref["idx"])
+        assert np.abs(host(one["out"]).reshape(w.segments, w.N, w.dv) - ref["out"]).max() <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("shape", EDGE, ids=[f"N{e['N']}-k{e['topk']}-dk{e['dk']}" for e in EDGE])
+@pytest.mark.parametrize("causal", [True, False])
+def test_select_attend_edges(shape, causal):
+    w = workloads.custom(B=2, H=1, seed=shape["N"] + shape["topk"], **shape)
+    log(f"select+attend edge {shape} causal={causal}")
+    x = workloads.generate(w)
+    S = w.segments
+    f = {n: oracle.as_f32(a, w.dtype).reshape(S, w.N, -1) for n, a in x.items()}
+    ref = oracle.forward(f["q"], f["k"], f["v"], w.topk, 0.5, causal, w.bits)
+    res = zeta.forward(to_dev(x["q"], w.dtype), to_dev(x["k"], w.dtype), to_dev(x["v"], w.dtype), w.topk, 0.5,
+                       causal, w.bits, fused=True, return_intermediates=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(res["idx"]).reshape(S, w.N, w.topk), ref["idx"])
+    assert np.abs(host(res["out"]).reshape(S, w.N, w.dv) - ref["out"]).max() <= TOL[w.dtype]
+    # Without the index output the result is the same.
+    out2 = zeta.forward(to_dev(x["q"], w.dtype), to_dev(x["k"], w.dtype), to_dev(x["v"], w.dtype), w.topk, 0.5,
+                        causal, w.bits, fused=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(out2).reshape(S, w.N, w.dv), host(res["out"]).reshape(S, w.N, w.dv))
