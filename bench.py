@@ -124,7 +124,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=5, help="workload number (parity cases 1-4, bench 5)")
     ap.add_argument("--noncausal", action="store_true")
-    ap.add_argument("--cpu-heads", type=int, default=3,
+    ap.add_argument("--cpu-heads", type=int, default=8,
                     help="segments in the oracle sample (0 skips the CPU baseline)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (for counter calibration)")
