@@ -124,7 +124,7 @@ zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_
  *   q_order    int32 [n_segments][N] permutation per segment, or NULL for
  *              position order.
  *   order_out  int32 [n_segments][N] output; may be the same buffer as
- *              q_order.
+ *              q_order, but must not otherwise overlap it (INVALID_ARG).
  *   topk, causal  as for zeta_select_topk (non-causal: a copy of q_order).
  *   workspace  at least zeta_workspace_size(...) bytes.
  */

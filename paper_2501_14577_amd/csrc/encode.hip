@@ -4,10 +4,12 @@
 //  1. range_partial: per (segment, chunk of rows) min/max of every axis over
 //     the chunk's query and key rows.  Consecutive threads read consecutive
 //     elements; the block is 64*d_k threads so each thread stays on one axis.
-//  2. encode: every block first folds its segment's partial ranges (a few
-//     dozen floats), then quantises and interleaves 256 query rows and 256 key
-//     rows.  Quantisation is float32 with one rounding per operation, matching
-//     the definition bit for bit.
+//  2. encode: every block first folds its segment's partial ranges (all
+//     threads load partials at once, then combine per axis in LDS), then
+//     quantises and interleaves 256 query rows and 256 key rows, each row read
+//     with one load.  Quantisation is float32 with one rounding per operation,
+//     matching the definition bit for bit.
+#include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"
 #include "layout.h"
@@ -77,15 +79,19 @@ __device__ __forceinline__ uint32_t spread3(uint32_t x) {
   return x;
 }
 
+// Code of row `r` of a [rows][dk] array.
 template <typename T>
-__device__ __forceinline__ uint32_t encode_row(const T* row, const float* lo, const float* hi, int dk,
-                                               int bits) {
+__device__ __forceinline__ uint32_t encode_row(const T* base, int64_t r, int64_t rows, const float* lo,
+                                               const float* hi, int dk, int bits) {
   if (dk == 3) {
-    uint32_t c0 = quantise(Elem<T>::load(row + 0), lo[0], hi[0], bits);
-    uint32_t c1 = quantise(Elem<T>::load(row + 1), lo[1], hi[1], bits);
-    uint32_t c2 = quantise(Elem<T>::load(row + 2), lo[2], hi[2], bits);
+    float x[3];
+    Row3<T>::load(base, r, rows, x);
+    const uint32_t c0 = quantise(x[0], lo[0], hi[0], bits);
+    const uint32_t c1 = quantise(x[1], lo[1], hi[1], bits);
+    const uint32_t c2 = quantise(x[2], lo[2], hi[2], bits);
     return (spread3(c0) << 2) | (spread3(c1) << 1) | spread3(c2);
   }
+  const T* row = base + r * dk;
   uint32_t z = 0;
   for (int a = 0; a < dk; ++a) {
     const uint32_t c = quantise(Elem<T>::load(row + a), lo[a], hi[a], bits);
@@ -102,38 +108,53 @@ __global__ void __launch_bounds__(256) encode_kernel(const T* __restrict__ q, co
                                                      float* __restrict__ range_out,
                                                      uint32_t* __restrict__ q_codes,
                                                      uint32_t* __restrict__ k_codes,
-                                                     int64_t blocks_per_seg) {
+                                                     int64_t blocks_per_seg, int64_t S) {
   const int64_t seg = blockIdx.x / blocks_per_seg;
   const int64_t blk = blockIdx.x % blocks_per_seg;
   __shared__ float s_lo[kMaxDk], s_hi[kMaxDk];
+  __shared__ float s_plo[kEncRowsPerBlock], s_phi[kEncRowsPerBlock];
   const int tid = threadIdx.x;
-  if (tid < dk) {
-    float lo, hi;
-    if (range_lohi != nullptr) {
-      lo = range_lohi[seg * 2 * dk + tid];
-      hi = range_lohi[seg * 2 * dk + dk + tid];
-    } else {
-      lo = __builtin_huge_valf();
-      hi = -__builtin_huge_valf();
+  if (range_lohi != nullptr) {
+    if (tid < dk) {
+      s_lo[tid] = range_lohi[seg * 2 * dk + tid];
+      s_hi[tid] = range_lohi[seg * 2 * dk + dk + tid];
+    }
+  } else {
+    // Fold the segment's partial ranges: every thread takes the partials of
+    // one axis (tid % dk) from chunks tid / dk, tid / dk + 256 / dk, ...
+    // (all loads independent), then threads of one axis combine in LDS.
+    const int per = kEncRowsPerBlock / dk;  // partials of one axis per round
+    const int a = tid % dk;
+    float lo = __builtin_huge_valf(), hi = -__builtin_huge_valf();
+    if (tid < per * dk) {
       const float* p = partial + seg * chunks * 2 * dk;
-      for (int64_t c = 0; c < chunks; ++c) {
-        lo = fminf(lo, p[c * 2 * dk + tid]);
-        hi = fmaxf(hi, p[c * 2 * dk + dk + tid]);
+      for (int64_t c = tid / dk; c < chunks; c += per) {
+        lo = fminf(lo, p[c * 2 * dk + a]);
+        hi = fmaxf(hi, p[c * 2 * dk + dk + a]);
       }
     }
-    s_lo[tid] = lo;
-    s_hi[tid] = hi;
-    if (range_out != nullptr && blk == 0) {
-      range_out[seg * 2 * dk + tid] = lo;
-      range_out[seg * 2 * dk + dk + tid] = hi;
+    s_plo[tid] = lo;
+    s_phi[tid] = hi;
+    __syncthreads();
+    if (tid < dk) {
+      for (int t = tid + dk; t < per * dk; t += dk) {
+        lo = fminf(lo, s_plo[t]);
+        hi = fmaxf(hi, s_phi[t]);
+      }
+      s_lo[tid] = lo;
+      s_hi[tid] = hi;
     }
   }
   __syncthreads();
+  if (range_out != nullptr && blk == 0 && tid < dk) {
+    range_out[seg * 2 * dk + tid] = s_lo[tid];
+    range_out[seg * 2 * dk + dk + tid] = s_hi[tid];
+  }
   const int64_t r = blk * kEncRowsPerBlock + tid;
   if (r < N) {
     const int64_t off = seg * N + r;
-    q_codes[off] = encode_row(q + off * dk, s_lo, s_hi, dk, bits);
-    k_codes[off] = encode_row(k + off * dk, s_lo, s_hi, dk, bits);
+    q_codes[off] = encode_row(q, off, S * N, s_lo, s_hi, dk, bits);
+    k_codes[off] = encode_row(k, off, S * N, s_lo, s_hi, dk, bits);
   }
 }
 
@@ -151,7 +172,7 @@ hipError_t launch_encode_t(const T* q, const T* k, int64_t S, int64_t N, int dk,
   const int64_t bps = ceil_div(N, kEncRowsPerBlock);
   hipLaunchKernelGGL(encode_kernel<T>, dim3(unsigned(S * bps)), dim3(unsigned(kEncRowsPerBlock)), 0,
                      stream, q, k, N, dk, bits, partial, ws.chunks, range_lohi, range_out, q_codes,
-                     k_codes, bps);
+                     k_codes, bps, S);
   return hipGetLastError();
 }
 

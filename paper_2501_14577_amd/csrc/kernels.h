@@ -18,11 +18,12 @@ hipError_t launch_encode(const void* q, const void* k, bool is_bf16, int64_t S, 
 hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_bits,
                        uint32_t* sorted_codes, int32_t* perm, void* workspace, hipStream_t stream);
 
-// One stable radix pass on the low nbits (<= 8) of keys, carrying vals: a
-// stable partition of each segment by that digit.  hist holds
-// S * ceil(N / kSortTile) * kRadixMax words.
-hipError_t launch_stable_partition(const uint32_t* keys, const int32_t* vals, int64_t S, int64_t N, int nbits,
-                                   uint32_t* keys_out, int32_t* vals_out, uint32_t* hist, hipStream_t stream);
+// One stable radix pass whose digit is the prefix-list level class of each
+// carried value (a query position; vals NULL: the positions 0..N-1): a stable
+// partition of each segment by list level.  hist holds
+// S * (ceil(N / kSortTile) + 1) * kRadixMax words.  vals_out must not alias vals.
+hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels,
+                                  int32_t* vals_out, uint32_t* hist, hipStream_t stream);
 
 // Regroup a processing order (NULL: position order) by the list level each
 // query searches in select, keeping the given order inside each level.

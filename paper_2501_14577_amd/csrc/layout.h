@@ -14,14 +14,15 @@ constexpr int kMaxBits = 24;    // grid cells per axis stay exact in float32
 
 // ---- encode ---------------------------------------------------------------
 // Rows of q (and of k) reduced by one block of the range kernel.
-constexpr int64_t kEncRowsPerChunk = 2048;
+constexpr int64_t kEncRowsPerChunk = 512;
 // Rows of q (and of k) encoded by one block of the encode kernel.
 constexpr int64_t kEncRowsPerBlock = 256;
 
 // ---- sort -----------------------------------------------------------------
-// Keys per tile of the radix passes: 4 waves x 16 chunks of 64 keys.
+// Keys per tile of the radix passes: 4 waves x 4 chunks of 64 keys (short
+// per-wave counting chains, many blocks in flight).
 constexpr int kSortThreads = 256;
-constexpr int kSortChunks = 16;
+constexpr int kSortChunks = 4;
 constexpr int64_t kSortTile = int64_t(kSortThreads) * kSortChunks;
 constexpr int kRadixMax = 256;  // digits of at most 8 bits
 
@@ -107,7 +108,8 @@ inline SortWs sort_ws(int64_t S, int64_t N, int code_bits) {
   SortPlan p = sort_plan(N, code_bits);
   SortWs w;
   w.hist_off = 0;
-  w.keys_off = align_up(size_t(S) * size_t(p.tiles) * kRadixMax * sizeof(uint32_t));
+  // Per-tile counts, then per-segment digit totals.
+  w.keys_off = align_up(size_t(S) * size_t(p.tiles + 1) * kRadixMax * sizeof(uint32_t));
   size_t buf = p.passes > 1 ? align_up(size_t(S) * size_t(N) * sizeof(uint32_t)) : 0;
   w.pos_off = w.keys_off + buf;
   w.bytes = w.pos_off + buf;
@@ -131,19 +133,16 @@ inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
-// Regrouping a processing order by list level: class keys, their sorted
-// copy, a copy of the given order and the radix pass's histograms.
+// Regrouping a processing order by list level: a copy of the given order
+// (when it is regrouped in place) and the radix pass's histograms.
 struct QueryOrderWs {
-  size_t cls_off, cls_sorted_off, given_off, phist_off, bytes;
+  size_t given_off, phist_off, bytes;
 };
 inline QueryOrderWs query_order_ws(int64_t S, int64_t N) {
   QueryOrderWs w;
-  const size_t per_query = align_up(size_t(S) * size_t(N) * sizeof(uint32_t));
-  w.cls_off = 0;
-  w.cls_sorted_off = per_query;
-  w.given_off = 2 * per_query;
-  w.phist_off = 3 * per_query;
-  w.bytes = w.phist_off + align_up(size_t(S) * size_t(ceil_div(N, kSortTile)) * kRadixMax * sizeof(uint32_t));
+  w.given_off = 0;
+  w.phist_off = align_up(size_t(S) * size_t(N) * sizeof(int32_t));
+  w.bytes = w.phist_off + align_up(size_t(S) * size_t(ceil_div(N, kSortTile) + 1) * kRadixMax * sizeof(uint32_t));
   return w;
 }
 

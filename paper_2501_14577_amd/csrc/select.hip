@@ -135,15 +135,6 @@ __global__ void __launch_bounds__(kSortThreads)
   }
 }
 
-__global__ void __launch_bounds__(256)
-    level_class_kernel(const int32_t* __restrict__ q_order, int64_t total, int64_t N, int t0, int t_hi,
-                       uint32_t* __restrict__ cls) {
-  const int64_t slot = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (slot >= total) return;
-  const int32_t i = q_order[slot];
-  cls[slot] = (i >= 0 && i < N) ? uint32_t(query_level(i, t0, t_hi) - t0) : 0u;
-}
-
 // order_out[slot] = q_order[slot], or the slot's position when q_order is NULL.
 __global__ void __launch_bounds__(256)
     copy_order_kernel(const int32_t* __restrict__ q_order, int64_t total, int64_t N, int32_t* __restrict__ order_out) {
@@ -235,15 +226,15 @@ hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int 
   }
   const QueryOrderWs ws = query_order_ws(S, N);
   char* wsb = static_cast<char*>(workspace);
-  uint32_t* cls = reinterpret_cast<uint32_t*>(wsb + ws.cls_off);
-  uint32_t* cls_sorted = reinterpret_cast<uint32_t*>(wsb + ws.cls_sorted_off);
-  int32_t* given = reinterpret_cast<int32_t*>(wsb + ws.given_off);
   uint32_t* phist = reinterpret_cast<uint32_t*>(wsb + ws.phist_off);
-  hipLaunchKernelGGL(copy_order_kernel, dim3(blocks), dim3(256), 0, stream, q_order, total, N, given);
-  hipLaunchKernelGGL(level_class_kernel, dim3(blocks), dim3(256), 0, stream, given, total, N, lp.t0, lp.t_hi, cls);
-  int nbits = 1;
-  while ((1 << nbits) < lp.levels + 1) ++nbits;
-  return launch_stable_partition(cls, given, S, N, nbits, cls_sorted, order_out, phist, stream);
+  const int32_t* given = q_order;
+  if (q_order != nullptr && q_order == order_out) {
+    // In place: partition from a copy.
+    int32_t* copy = reinterpret_cast<int32_t*>(wsb + ws.given_off);
+    hipLaunchKernelGGL(copy_order_kernel, dim3(blocks), dim3(256), 0, stream, q_order, total, N, copy);
+    given = copy;
+  }
+  return launch_level_partition(given, S, N, lp.t0, lp.t_hi, lp.levels, order_out, phist, stream);
 }
 
 hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm, int64_t S, int64_t N, int topk,

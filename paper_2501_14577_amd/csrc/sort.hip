@@ -1,13 +1,15 @@
 // Stable segmented LSD radix sort of (code, position) pairs (Section 3.2.2;
 // Algorithm 1, Step 2; Appendix B sorts the codes with a radix sort).
 //
-// Every segment is cut into tiles of 4096 keys.  One pass over a digit of at
-// most 8 bits runs two kernels:
+// Every segment is cut into tiles of 1024 keys.  One pass over a digit of at
+// most 8 bits runs three kernels:
 //   hist:    per tile, the count of each digit value (LDS atomics);
+//   scan:    per segment and digit value, the counts of earlier tiles
+//            (written over the tile counts) and the segment total;
 //   scatter: per tile, the digit's global base (an exclusive scan over digit
-//            values of the segment totals, plus the counts of earlier tiles),
+//            values of the segment totals, plus the earlier tiles' counts),
 //            then a stable rank of every key inside the tile: each wavefront
-//            walks its 1024 keys in order, 64 at a time, finding same-digit
+//            walks its 256 keys in order, 64 at a time, finding same-digit
 //            lanes with one ballot per digit bit and counting them with
 //            mbcnt; per-wave running counts live in LDS.
 // A pass preserves the order of equal digits, so after the last pass equal
@@ -15,13 +17,25 @@
 #include "device_common.h"
 #include "kernels.h"
 #include "layout.h"
+#include "select_device.h"
 
 namespace zeta {
 namespace {
 
+// Digit of an element: the key's bits [shift, shift+nbits) (kByLevel false), or
+// the prefix-list level class of the carried position (kByLevel true; the
+// level regrouping of a processing order, see query_level).
+template <bool kByLevel>
+__device__ __forceinline__ uint32_t radix_digit(uint32_t key, int32_t val, int shift, uint32_t mask, int t0,
+                                                int t_hi, int64_t N) {
+  if (kByLevel) return (val >= 0 && val < N) ? uint32_t(query_level(val, t0, t_hi) - t0) : 0u;
+  return (key >> shift) & mask;
+}
+
+template <bool kByLevel>
 __global__ void __launch_bounds__(kSortThreads)
-    radix_hist_kernel(const uint32_t* __restrict__ keys, int64_t N, int64_t tiles, int shift, int nbits,
-                      uint32_t* __restrict__ hist) {
+    radix_hist_kernel(const uint32_t* __restrict__ keys, const int32_t* __restrict__ vals, int64_t N, int64_t tiles,
+                      int shift, int nbits, int t0, int t_hi, uint32_t* __restrict__ hist) {
   const int64_t seg = blockIdx.x / tiles;
   const int64_t tile = blockIdx.x % tiles;
   const int tid = threadIdx.x;
@@ -29,20 +43,71 @@ __global__ void __launch_bounds__(kSortThreads)
   h[tid] = 0;
   __syncthreads();
   const uint32_t mask = (1u << nbits) - 1u;
-  const int64_t t0 = tile * kSortTile;
-  const int64_t t1 = (t0 + kSortTile < N) ? t0 + kSortTile : N;
-  const uint32_t* ks = keys + seg * N;
-  for (int64_t e = t0 + tid; e < t1; e += kSortThreads) atomicAdd(&h[(ks[e] >> shift) & mask], 1u);
+  const int64_t e0 = tile * kSortTile;
+  const int64_t e1 = (e0 + kSortTile < N) ? e0 + kSortTile : N;
+  for (int64_t e = e0 + tid; e < e1; e += kSortThreads) {
+    const uint32_t key = kByLevel ? 0u : keys[seg * N + e];
+    const int32_t val = kByLevel ? (vals != nullptr ? vals[seg * N + e] : int32_t(e)) : 0;
+    atomicAdd(&h[radix_digit<kByLevel>(key, val, shift, mask, t0, t_hi, N)], 1u);
+  }
   __syncthreads();
   hist[(seg * tiles + tile) * kRadixMax + tid] = h[tid];
 }
 
-template <bool kHasPos>
+// Tiles of one segment are split into kScanGroups contiguous groups; wave g
+// of the block sums group g for 64 digit values, the groups' sums are
+// combined through LDS, and each wave then rewrites its tiles' counts as
+// exclusive prefixes.  Grid: S * (kRadixMax / 64) blocks.
+constexpr int kScanGroups = kSortThreads / 64;
+constexpr int kScanBatch = 16;
+
+__global__ void __launch_bounds__(kSortThreads)
+    radix_scan_kernel(int64_t tiles, uint32_t* __restrict__ hist, uint32_t* __restrict__ totals) {
+  const int64_t seg = blockIdx.x / (kRadixMax / 64);
+  const int d = int(blockIdx.x % (kRadixMax / 64)) * 64 + (threadIdx.x & 63);
+  const int g = threadIdx.x >> 6;
+  const int64_t per = (tiles + kScanGroups - 1) / kScanGroups;
+  const int64_t t_begin = g * per < tiles ? g * per : tiles;
+  const int64_t t_end = t_begin + per < tiles ? t_begin + per : tiles;
+  uint32_t* h = hist + seg * tiles * kRadixMax + d;
+  __shared__ uint32_t s_sum[kScanGroups][64];
+
+  uint32_t sum = 0;
+  for (int64_t t = t_begin; t < t_end; t += kScanBatch) {
+    uint32_t c[kScanBatch];
+#pragma unroll
+    for (int j = 0; j < kScanBatch; ++j) c[j] = (t + j < t_end) ? h[(t + j) * kRadixMax] : 0u;
+#pragma unroll
+    for (int j = 0; j < kScanBatch; ++j) sum += c[j];
+  }
+  s_sum[g][threadIdx.x & 63] = sum;
+  __syncthreads();
+  uint32_t run = 0, total = 0;
+#pragma unroll
+  for (int j = 0; j < kScanGroups; ++j) {
+    const uint32_t x = s_sum[j][threadIdx.x & 63];
+    run += (j < g) ? x : 0u;
+    total += x;
+  }
+  if (g == 0) totals[seg * kRadixMax + d] = total;
+  for (int64_t t = t_begin; t < t_end; t += kScanBatch) {
+    uint32_t c[kScanBatch];
+#pragma unroll
+    for (int j = 0; j < kScanBatch; ++j) c[j] = (t + j < t_end) ? h[(t + j) * kRadixMax] : 0u;
+#pragma unroll
+    for (int j = 0; j < kScanBatch; ++j) {
+      if (t + j < t_end) h[(t + j) * kRadixMax] = run;
+      run += c[j];
+    }
+  }
+}
+
+template <bool kHasPos, bool kByLevel>
 __global__ void __launch_bounds__(kSortThreads)
     radix_scatter_kernel(const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ pos_in,
-                         int64_t N, int64_t tiles, int shift, int nbits,
-                         const uint32_t* __restrict__ hist, uint32_t* __restrict__ keys_out,
-                         int32_t* __restrict__ pos_out) {
+                         int64_t N, int64_t tiles, int shift, int nbits, int t0, int t_hi,
+                         const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals,
+                         uint32_t* __restrict__ keys_out, int32_t* __restrict__ pos_out) {
   const int64_t seg = blockIdx.x / tiles;
   const int64_t tile = blockIdx.x % tiles;
   const int tid = threadIdx.x;
@@ -56,14 +121,8 @@ __global__ void __launch_bounds__(kSortThreads)
 
   {
     // Digit totals of the segment and counts of the tiles before this one.
-    const uint32_t* h = hist + seg * tiles * kRadixMax + tid;
-    uint32_t total = 0, before = 0;
-    for (int64_t t = 0; t < tiles; ++t) {
-      const uint32_t c = h[t * kRadixMax];
-      total += c;
-      before += (t < tile) ? c : 0u;
-    }
-    const uint32_t excl = block256_exclusive_scan(total, s_scan);
+    const uint32_t before = hist[(seg * tiles + tile) * kRadixMax + tid];
+    const uint32_t excl = block256_exclusive_scan(totals[seg * kRadixMax + tid], s_scan);
     s_base[tid] = excl + before;
 #pragma unroll
     for (int w = 0; w < kSortThreads / 64; ++w) s_wcnt[w][tid] = 0;
@@ -79,13 +138,13 @@ __global__ void __launch_bounds__(kSortThreads)
   for (int c = 0; c < kSortChunks; ++c) {
     const int64_t e = first + c * 64 + lane;
     const bool valid = e < N;
-    const uint32_t kk = valid ? keys_in[seg_off + e] : 0u;
+    const uint32_t kk = (valid && !kByLevel) ? keys_in[seg_off + e] : 0u;
     int32_t pp;
     if (kHasPos)
       pp = valid ? pos_in[seg_off + e] : 0;
     else
       pp = int32_t(e);
-    const uint32_t d = (kk >> shift) & mask;
+    const uint32_t d = radix_digit<kByLevel>(kk, pp, shift, mask, t0, t_hi, N);
     uint64_t peers = wave_ballot(valid);
     for (int b = 0; b < nbits; ++b) {
       const bool bit = (d >> b) & 1u;
@@ -114,9 +173,9 @@ __global__ void __launch_bounds__(kSortThreads)
   for (int c = 0; c < kSortChunks; ++c) {
     const int64_t e = first + c * 64 + lane;
     if (e < N) {
-      const uint32_t d = (key[c] >> shift) & mask;
+      const uint32_t d = radix_digit<kByLevel>(key[c], pos[c], shift, mask, t0, t_hi, N);
       const int64_t dst = int64_t(s_base[d]) + s_wcnt[wave][d] + rank[c];
-      keys_out[seg_off + dst] = key[c];
+      if (!kByLevel) keys_out[seg_off + dst] = key[c];
       pos_out[seg_off + dst] = pos[c];
     }
   }
@@ -124,13 +183,22 @@ __global__ void __launch_bounds__(kSortThreads)
 
 }  // namespace
 
-hipError_t launch_stable_partition(const uint32_t* keys, const int32_t* vals, int64_t S, int64_t N, int nbits,
-                                   uint32_t* keys_out, int32_t* vals_out, uint32_t* hist, hipStream_t stream) {
+hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels,
+                                  int32_t* vals_out, uint32_t* hist, hipStream_t stream) {
   const int64_t tiles = ceil_div(N, kSortTile);
   const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
-  hipLaunchKernelGGL(radix_hist_kernel, grid, block, 0, stream, keys, N, tiles, 0, nbits, hist);
-  hipLaunchKernelGGL(radix_scatter_kernel<true>, grid, block, 0, stream, keys, vals, N, tiles, 0, nbits, hist,
-                     keys_out, vals_out);
+  int nbits = 1;
+  while ((1 << nbits) < levels + 1) ++nbits;
+  uint32_t* totals = hist + S * tiles * kRadixMax;
+  hipLaunchKernelGGL(radix_hist_kernel<true>, grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits, t0, t_hi,
+                     hist);
+  hipLaunchKernelGGL(radix_scan_kernel, dim3(unsigned(S * (kRadixMax / 64))), block, 0, stream, tiles, hist, totals);
+  if (vals != nullptr)
+    hipLaunchKernelGGL((radix_scatter_kernel<true, true>), grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits,
+                       t0, t_hi, hist, totals, nullptr, vals_out);
+  else
+    hipLaunchKernelGGL((radix_scatter_kernel<false, true>), grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits,
+                       t0, t_hi, hist, totals, nullptr, vals_out);
   return hipGetLastError();
 }
 
@@ -140,6 +208,7 @@ hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_b
   const SortWs ws = sort_ws(S, N, code_bits);
   char* wsb = static_cast<char*>(workspace);
   uint32_t* hist = reinterpret_cast<uint32_t*>(wsb + ws.hist_off);
+  uint32_t* totals = hist + S * plan.tiles * kRadixMax;
   uint32_t* tmp_keys = reinterpret_cast<uint32_t*>(wsb + ws.keys_off);
   int32_t* tmp_pos = reinterpret_cast<int32_t*>(wsb + ws.pos_off);
   const dim3 grid(unsigned(S * plan.tiles)), block(kSortThreads);
@@ -153,14 +222,16 @@ hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_b
     const bool to_out = ((plan.passes - 1 - p) % 2) == 0;
     uint32_t* dst_keys = to_out ? sorted_codes : tmp_keys;
     int32_t* dst_pos = to_out ? perm : tmp_pos;
-    hipLaunchKernelGGL(radix_hist_kernel, grid, block, 0, stream, src_keys, N, plan.tiles, shift, nbits,
-                       hist);
+    hipLaunchKernelGGL(radix_hist_kernel<false>, grid, block, 0, stream, src_keys, nullptr, N, plan.tiles, shift,
+                       nbits, 0, 0, hist);
+    hipLaunchKernelGGL(radix_scan_kernel, dim3(unsigned(S * (kRadixMax / 64))), block, 0, stream, plan.tiles, hist,
+                       totals);
     if (src_pos == nullptr)
-      hipLaunchKernelGGL(radix_scatter_kernel<false>, grid, block, 0, stream, src_keys, src_pos, N,
-                         plan.tiles, shift, nbits, hist, dst_keys, dst_pos);
+      hipLaunchKernelGGL((radix_scatter_kernel<false, false>), grid, block, 0, stream, src_keys, src_pos, N,
+                         plan.tiles, shift, nbits, 0, 0, hist, totals, dst_keys, dst_pos);
     else
-      hipLaunchKernelGGL(radix_scatter_kernel<true>, grid, block, 0, stream, src_keys, src_pos, N,
-                         plan.tiles, shift, nbits, hist, dst_keys, dst_pos);
+      hipLaunchKernelGGL((radix_scatter_kernel<true, false>), grid, block, 0, stream, src_keys, src_pos, N,
+                         plan.tiles, shift, nbits, 0, 0, hist, totals, dst_keys, dst_pos);
     src_keys = dst_keys;
     src_pos = dst_pos;
   }

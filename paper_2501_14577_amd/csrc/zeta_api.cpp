@@ -23,6 +23,12 @@ zeta_status_t hip_status(hipError_t e) { return e == hipSuccess ? ZETA_OK : ZETA
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// True when [a, a + bytes) and [b, b + bytes) share a byte.
+bool overlaps(const void* a, const void* b, size_t bytes) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + bytes && y < x + bytes;
+}
+
 bool bad_count(int64_t B, int64_t H, int64_t N) {
   if (B < 1 || H < 1 || N < 1) return true;
   if (B > kMaxElems / H) return true;
@@ -73,6 +79,10 @@ zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64
   if (!shape_ok(n_segments, N)) return ZETA_ERR_INVALID_ARG;
   if (topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
   if (topk > zeta::kMaxTopk) return ZETA_ERR_UNSUPPORTED;
+  // In place is allowed; a partial overlap is not.
+  if (q_order != nullptr && q_order != order_out &&
+      overlaps(q_order, order_out, size_t(n_segments) * size_t(N) * sizeof(int32_t)))
+    return ZETA_ERR_INVALID_ARG;
   const zeta::ListPlan lp = zeta::list_plan(N, topk);
   if (causal && lp.levels > 0) {
     const zeta::QueryOrderWs ws = zeta::query_order_ws(n_segments, N);

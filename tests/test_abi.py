@@ -157,6 +157,7 @@ def test_attend_rejects(kw, code):
 QORDER_CASES = [
     (dict(order_out=NULL), INV), (dict(S=0), INV), (dict(N=0), INV), (dict(topk=0), INV), (dict(causal=3), INV),
     (dict(topk=1025), UNS), (dict(ws=NULL), WSP), (dict(ws_bytes=16), WSP),
+    (dict(order_out=ctypes.c_void_p(0x10000 + 64)), INV),  # partial overlap with q_order
 ]
 
 
