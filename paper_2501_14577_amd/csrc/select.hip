@@ -76,14 +76,20 @@ __global__ void __launch_bounds__(kSortThreads)
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  __shared__ uint32_t s_before[kMaxLevels];                 // entries of earlier tiles per level
+  constexpr int kGroups = kSortThreads / kMaxLevels;
+  __shared__ uint32_t s_before[kGroups][kMaxLevels];           // entries of earlier tiles, by tile group
   __shared__ uint32_t s_wave[kSortThreads / 64][kMaxLevels];  // per-wave counts, then prefixes
 
-  if (tid < levels) {
+  {
+    // Entries of the earlier tiles per level: thread (g, l) sums the tiles
+    // t < tile with t % kGroups == g.
+    const int l = tid % kMaxLevels, g = tid / kMaxLevels;
     uint32_t b = 0;
-    const uint32_t* c = cnt + seg * tiles * kMaxLevels + tid;
-    for (int64_t t = 0; t < tile; ++t) b += c[t * kMaxLevels];
-    s_before[tid] = b;
+    if (l < levels) {
+      const uint32_t* c = cnt + seg * tiles * kMaxLevels + l;
+      for (int64_t t = g; t < tile; t += kGroups) b += c[t * kMaxLevels];
+    }
+    s_before[g][l] = b;
   }
   const int64_t seg_off = seg * N;
   const int64_t first = tile * kSortTile + int64_t(wave) * (kSortChunks * 64);
@@ -105,7 +111,9 @@ __global__ void __launch_bounds__(kSortThreads)
   }
   __syncthreads();
   if (tid < levels) {
-    uint32_t run = s_before[tid];
+    uint32_t run = 0;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) run += s_before[g][tid];
 #pragma unroll
     for (int w = 0; w < kSortThreads / 64; ++w) {
       const uint32_t t = s_wave[w][tid];
