@@ -31,7 +31,7 @@ import workloads  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2501_14577_amd", "csrc", n)
-               for n in ("fused.hip", "select_device.h", "attend_device.h", "device_common.h")]
+               for n in ("fused.hip", "tile.hip", "select_device.h", "attend_device.h", "device_common.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "select_attend_long_context_traffic.txt")
 
 
@@ -221,6 +221,7 @@ def main() -> int:
     f_bytes = a_bytes + w.segments * w.N * 4  # plus each query's code, read instead of an index row
     achieved = f_bytes / (fused_ms * 1e-3) / 1e9
     s_bytes = step_bytes(w, causal)
+    traffic = read_traffic()
 
     cpu = None
     if args.cpu_heads > 0:
@@ -248,14 +249,16 @@ def main() -> int:
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "select_attend (one pass)",
+            "kernel": "select_attend (one pass, 16-query matrix-core tiles)",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": read_traffic(),
+            "traffic": traffic,
             "algorithmic_bytes_per_launch": f_bytes,
             "kernel_ms": fused_ms,
+            # Bytes that actually crossed HBM (calibrated counters) per second.
+            "traffic_GBs": (traffic / (fused_ms * 1e-3) / 1e9) if traffic else None,
         },
         "four_call_path": {
             "ms_per_step": four_ms,

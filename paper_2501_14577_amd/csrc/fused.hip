@@ -247,6 +247,9 @@ hipError_t launch_select_attend(const void* q, const void* k, const void* v, boo
     const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
     if (e != hipSuccess) return e;
   }
+  if (is_bf16 && tile_supports(dv))
+    return launch_select_attend_tile(q, k, v, S, N, dk, dv, topk, causal, q_codes, sorted_codes, perm, list_codes,
+                                     list_pos, q_order, eps, out, idx_out, stream);
 #define ZETA_FUSED_CASE(DVV)                                                                                    \
   case DVV:                                                                                                     \
     return is_bf16 ? launch_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm,    \

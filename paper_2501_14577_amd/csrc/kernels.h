@@ -42,6 +42,15 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
                                void* workspace, hipStream_t stream, const uint32_t** list_codes,
                                const int32_t** list_pos);
 
+// bfloat16 one-pass select and attend on the matrix cores, 16 queries per
+// wavefront (the prefix lists already built when causal).
+bool tile_supports(int dv);
+hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
+                                     int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
+                                     const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
+                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out,
+                                     hipStream_t stream);
+
 // Select and attend in one pass (idx_out optional).
 hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,
                                 int dk, int dv, int topk, bool causal, const uint32_t* q_codes,

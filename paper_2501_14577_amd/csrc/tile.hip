@@ -1,0 +1,380 @@
+// Candidate selection and Cauchy-softmax attention for bfloat16 inputs, 16
+// queries at a time on the matrix cores (Section 3.2.2 and Algorithm 1,
+// Steps 3-5, for the windows; Section 3.3, equation cauchy, Section 3.4 and
+// Appendix E.1 for the attention).
+//
+// A query's window is a run of its sorted list: every in-pool entry of the
+// list range [a, b] around its insertion point (select_window_bounds).  In the
+// processing order of zeta_query_order, 16 consecutive queries search one list
+// at nearby insertion points, so their ranges overlap: together they span
+// about twice the window length where gathering per query would read 16
+// windows.  A wavefront takes such a tile and walks the union of its ranges
+// in chunks of 32 list entries.  For each chunk it
+//   - stages the entries' positions and key rows in LDS;
+//   - scores the 16 x 32 (query, entry) pairs, S = 1 / (|q - k|^2 + eps) when
+//     the entry lies in the query's window and pool, else 0;
+//   - loads each entry's value row once for the whole tile;
+//   - accumulates V^T (16 value columns x 32 entries) times S^T (32 entries x
+//     16 queries) with v_mfma_f32_16x16x32_bf16, once per 16 value columns.
+// Scores are float32; each is split into a bfloat16 high part and a bfloat16
+// remainder, and both products are accumulated, so the weights carry 16
+// significant bits and the products are exact in the float32 accumulator.
+// The normaliser sums the float32 scores.
+//
+// Operand layout of the 16x16x32 product (lane l, kg = l / 16):
+//   A (value columns x entries): lane l holds entries 8kg..8kg+7 of column
+//     l % 16;
+//   B (entries x queries): entries 8kg..8kg+7 of query l % 16;
+//   D (columns x queries): columns 4kg..4kg+3 of query l % 16.
+// Column c of block j is value element c * E + j (E = d_v / 16), so a lane
+// loads E consecutive elements of each of its 8 rows with one instruction and
+// ends with 4E consecutive outputs of one query.
+//
+// Chunks are aligned to multiples of 32 in the list and a query's scores are
+// zero outside its window, so its output depends only on its own window: the
+// result is the same whatever tile the query falls in, i.e. for any
+// processing order.
+#include "attend_device.h"
+#include "device_common.h"
+#include "kernels.h"
+#include "layout.h"
+#include "select_device.h"
+
+namespace zeta {
+namespace {
+
+constexpr int kTileQ = 16;     // queries per tile (product columns)
+constexpr int kChunk = 32;     // list entries per product step
+constexpr int kTileWaves = 4;  // wavefronts per block
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+union Frag {
+  uint32_t w[4];
+  bf16x8_t v;
+};
+
+__device__ __forceinline__ int wave_min_int(int x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const int y = __shfl_xor(x, off, 64);
+    x = y < x ? y : x;
+  }
+  return x;
+}
+
+// E consecutive bfloat16 elements (E / 2 words) from a 2E-byte aligned address.
+template <int W>
+__device__ __forceinline__ void load_words(const uint16_t* p, uint32_t (&o)[W]) {
+  if constexpr (W % 4 == 0) {
+#pragma unroll
+    for (int t = 0; t < W / 4; ++t) {
+      const uint4 x = reinterpret_cast<const uint4*>(p)[t];
+      o[4 * t] = x.x;
+      o[4 * t + 1] = x.y;
+      o[4 * t + 2] = x.z;
+      o[4 * t + 3] = x.w;
+    }
+  } else if constexpr (W == 2) {
+    const uint2 x = *reinterpret_cast<const uint2*>(p);
+    o[0] = x.x;
+    o[1] = x.y;
+  } else {
+    static_assert(W == 1, "unsupported row slice");
+    o[0] = *reinterpret_cast<const uint32_t*>(p);
+  }
+}
+
+template <int DV, int DK, bool kOff32>
+__global__ void __launch_bounds__(kTileWaves * 64)
+    select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                              const uint16_t* __restrict__ v, const uint32_t* __restrict__ q_codes,
+                              const uint32_t* __restrict__ sorted_codes, const int32_t* __restrict__ perm,
+                              const uint32_t* __restrict__ list_codes, const int32_t* __restrict__ list_pos,
+                              const int32_t* __restrict__ order, int64_t total, int64_t N, int dk_rt, int topk,
+                              int causal, int t0, int t_hi, int64_t cap, float eps, uint16_t* __restrict__ out,
+                              int32_t* __restrict__ idx_out) {
+  constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
+  constexpr int W = E / 2;    // 32-bit words per lane and row
+  constexpr int KD = DK > 0 ? DK : kMaxDk;
+  static_assert(E >= 2 && E % 2 == 0, "d_v must be a multiple of 32");
+  using Off = typename RowOff<kOff32>::type;
+  const int dk = DK > 0 ? DK : dk_rt;
+
+  __shared__ int32_t s_pos[kTileWaves][kChunk];
+  __shared__ float s_k[kTileWaves][kChunk][KD];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int qn = lane & (kTileQ - 1);  // this lane's query in the tile; also its value column in a block
+  const int kg = lane >> 4;            // this lane's entries in a chunk: 8kg .. 8kg+7
+  const int64_t tiles = (total + kTileQ - 1) / kTileQ;
+  const int64_t nb = gridDim.x;
+
+  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kTileWaves < tiles; blk += nb) {
+    const int64_t tile = blk * kTileWaves + wave;
+    if (tile >= tiles) continue;
+
+    // The tile's queries: lanes with equal qn hold the same one.
+    int32_t my_i = -1;
+    int64_t my_seg = 0;
+    uint32_t my_key = 0;
+    int my_lvl = 0;
+    {
+      const int64_t sl = tile * kTileQ + qn;
+      if (sl < total) {
+        const int64_t sg = sl / N;
+        const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
+        if (ii >= 0 && ii < N) {
+          my_i = int32_t(ii);
+          my_seg = sg;
+          my_key = q_codes[sg * N + ii];
+          my_lvl = causal ? query_level(my_i, t0, t_hi) : 0;
+        }
+      }
+    }
+    uint32_t pending = uint32_t(wave_ballot(my_i >= 0)) & 0xFFFFu;
+
+    // Queries that search one list form a group (nearly always the whole tile).
+    while (pending != 0u) {
+      const int leader = __ffs(int(pending)) - 1;
+      const int64_t g_seg = __builtin_amdgcn_readlane(int32_t(my_seg), leader);
+      const int g_lvl = __builtin_amdgcn_readlane(my_lvl, leader);
+      const int32_t g_i = __builtin_amdgcn_readlane(my_i, leader);
+      const uint32_t gmask =
+          uint32_t(wave_ballot(my_i >= 0 && my_seg == g_seg && my_lvl == g_lvl)) & pending;
+      pending &= ~gmask;
+      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, g_seg, N, g_i, causal, t0, t_hi, cap);
+
+      // Window bounds of every query of the group.
+      int32_t my_a = 0, my_b = -1;
+      {
+        const uint32_t* prev_codes = nullptr;
+        uint32_t prev_key = 0;
+        int32_t prev_p = 0;
+        for (uint32_t m = gmask; m != 0u; m &= m - 1u) {
+          const int u = __ffs(int(m)) - 1;
+          const int32_t i = __builtin_amdgcn_readlane(my_i, u);
+          const uint32_t key = uint32_t(__builtin_amdgcn_readlane(int32_t(my_key), u));
+          QueryList Lq = L;
+          Lq.limit = causal ? i : int32_t(N - 1);
+          const int32_t p = (prev_codes == Lq.codes && key >= prev_key)
+                                ? wave_lower_bound_near(Lq.codes, prev_p, Lq.n, key, lane)
+                                : wave_lower_bound(Lq.codes, 0, Lq.n, key, lane);
+          prev_codes = Lq.codes;
+          prev_key = key;
+          prev_p = p;
+          const WindowBounds wb = select_window_bounds(Lq, p, topk, lane);
+          if (qn == u) {
+            my_a = wb.a;
+            my_b = wb.b;
+          }
+          if (idx_out != nullptr) {
+            // The window's positions in list order, then -1.
+            int32_t* row = idx_out + (g_seg * N + i) * int64_t(topk);
+            int cnt = 0;
+            for (int32_t e0 = wb.a; e0 <= wb.b; e0 += 64) {
+              const int32_t e = e0 + lane;
+              const int32_t pv = e <= wb.b ? Lq.pos[e] : INT32_MAX;
+              const bool ok = pv <= Lq.limit;
+              const uint64_t bal = wave_ballot(ok);
+              if (ok) row[cnt + int(lanes_below(bal))] = pv;
+              cnt += __popcll(bal);
+            }
+            for (int c = cnt + lane; c < topk; c += 64) row[c] = -1;
+          }
+        }
+      }
+
+      const bool mine = ((gmask >> qn) & 1u) != 0u;
+      const int32_t my_lim = causal ? my_i : int32_t(N - 1);
+      float qv[KD];
+      if (mine) {
+        if constexpr (DK == 3) {
+          Row3<uint16_t>::load(q, g_seg * N + my_i, total, qv);
+        } else {
+#pragma unroll
+          for (int a = 0; a < KD; ++a) qv[a] = a < dk ? bf16_bits_to_float(q[(g_seg * N + my_i) * dk + a]) : 0.0f;
+        }
+      } else {
+#pragma unroll
+        for (int a = 0; a < KD; ++a) qv[a] = 0.0f;
+      }
+
+      f32x4_t acc[E];
+#pragma unroll
+      for (int j = 0; j < E; ++j) acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      float zpart = 0.0f;
+      const uint16_t* vseg = v + g_seg * N * DV;
+      const uint16_t* kseg = k + g_seg * N * dk;
+      const Off col = Off(qn * E);
+
+      // Walk the chunks that meet some window, in list order.
+      int c = wave_min_int(mine && my_a <= my_b ? my_a / kChunk : INT32_MAX);
+      while (c != INT32_MAX) {
+        const int32_t r0 = c * kChunk;
+        if (lane < kChunk) {
+          const int32_t r = r0 + lane;
+          const int32_t pv = r < L.n ? L.pos[r] : -1;
+          s_pos[wave][lane] = pv;
+          float kv[KD];
+          if (pv >= 0) {
+            if constexpr (DK == 3) {
+              Row3<uint16_t>::load(k, g_seg * N + pv, total, kv);
+            } else {
+#pragma unroll
+              for (int a = 0; a < KD; ++a) kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv) * dk + a]) : 0.0f;
+            }
+          } else {
+#pragma unroll
+            for (int a = 0; a < KD; ++a) kv[a] = 0.0f;
+          }
+#pragma unroll
+          for (int a = 0; a < KD; ++a) s_k[wave][lane][a] = kv[a];
+        }
+        wave_lds_sync();
+
+        Frag b_hi, b_lo;
+        uint32_t raw[8][W];
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) {
+          const int rr = kg * 8 + kk;
+          const int32_t r = r0 + rr;
+          const int32_t pv = s_pos[wave][rr];
+          const bool in = mine && r >= my_a && r <= my_b && pv >= 0 && pv <= my_lim;
+          float s = 0.0f;
+          if (in) {
+            float d2 = 0.0f;
+#pragma unroll
+            for (int a = 0; a < KD; ++a) {
+              if (a < dk) {
+                const float diff = qv[a] - s_k[wave][rr][a];
+                d2 = fmaf(diff, diff, d2);
+              }
+            }
+            s = 1.0f / (d2 + eps);
+          }
+          zpart += s;
+          const uint32_t hi = float_to_bf16_bits(s);
+          const uint32_t lo = float_to_bf16_bits(s - __uint_as_float(hi << 16));
+          if (kk & 1) {
+            b_hi.w[kk >> 1] |= hi << 16;
+            b_lo.w[kk >> 1] |= lo << 16;
+          } else {
+            b_hi.w[kk >> 1] = hi;
+            b_lo.w[kk >> 1] = lo;
+          }
+          // The row is needed when any query of the tile takes it.
+          const bool used = ((wave_ballot(in) >> (kg * 16)) & 0xFFFFull) != 0ull;
+          if (used) {
+            load_words<W>(vseg + (Off(pv) * Off(DV) + col), raw[kk]);
+          } else {
+#pragma unroll
+            for (int t = 0; t < W; ++t) raw[kk][t] = 0u;
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+          Frag a;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
+            a.w[t] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+          }
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_hi.v, acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_lo.v, acc[j], 0, 0, 0);
+        }
+        wave_lds_sync();
+
+        // Next chunk that meets a window.
+        const int nxt = c + 1;
+        const int cand = (mine && my_a <= my_b && my_b >= nxt * kChunk)
+                             ? (my_a / kChunk > nxt ? my_a / kChunk : nxt)
+                             : INT32_MAX;
+        c = wave_min_int(cand);
+      }
+
+      // Normalise and store: lane holds columns 4kg..4kg+3 of every block,
+      // i.e. value elements 4kg*E .. 4kg*E + 4E - 1 of query qn.
+      float z = zpart;
+      z += __shfl_xor(z, 16, 64);
+      z += __shfl_xor(z, 32, 64);
+      if (mine) {
+        const float inv = z > 0.0f ? 1.0f / z : 0.0f;
+        float o[4 * E];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < E; ++j) o[i * E + j] = acc[j][i] * inv;
+        uint16_t* dst = out + (g_seg * N + my_i) * int64_t(DV) + kg * 4 * E;
+#pragma unroll
+        for (int t = 0; t < 4 * E; t += 8) Vec16<uint16_t>::store(dst + t, o + t);
+      }
+    }
+  }
+}
+
+template <int DV, int DK>
+hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
+                         int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
+                         const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
+                         const int32_t* q_order, float eps, uint16_t* out, int32_t* idx_out, hipStream_t stream) {
+  const ListPlan lp = list_plan(N, topk);
+  const int64_t total = S * N;
+  const int64_t tiles = ceil_div(total, kTileQ);
+  const int64_t want = ceil_div(tiles, kTileWaves);
+  const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
+  const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
+  if (off32)
+    hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, true>), dim3(blocks), dim3(kTileWaves * 64), 0, stream, q,
+                       k, v, q_codes, sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk,
+                       causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap, eps, out, idx_out);
+  else
+    hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, false>), dim3(blocks), dim3(kTileWaves * 64), 0, stream,
+                       q, k, v, q_codes, sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk,
+                       causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap, eps, out, idx_out);
+  return hipGetLastError();
+}
+
+template <int DV>
+hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
+                          int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
+                          const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
+                          const int32_t* q_order, float eps, uint16_t* out, int32_t* idx_out, hipStream_t stream) {
+  if (dk == 3)
+    return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
+                                q_order, eps, out, idx_out, stream);
+  return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
+                              q_order, eps, out, idx_out, stream);
+}
+
+}  // namespace
+
+bool tile_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 256; }
+
+hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
+                                     int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
+                                     const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
+                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out,
+                                     hipStream_t stream) {
+  const uint16_t* qq = static_cast<const uint16_t*>(q);
+  const uint16_t* kk = static_cast<const uint16_t*>(k);
+  const uint16_t* vv = static_cast<const uint16_t*>(v);
+  uint16_t* oo = static_cast<uint16_t*>(out);
+#define ZETA_TILE_CASE(DVV) \
+  case DVV:                 \
+    return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos, \
+                               q_order, eps, oo, idx_out, stream);
+  switch (dv) {
+    ZETA_TILE_CASE(32)
+    ZETA_TILE_CASE(64)
+    ZETA_TILE_CASE(128)
+    ZETA_TILE_CASE(256)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef ZETA_TILE_CASE
+}
+
+}  // namespace zeta

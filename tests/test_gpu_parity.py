@@ -298,6 +298,9 @@ EDGE = [
     dict(N=1500, topk=33, dk=2, dv=256, dtype="f32", bits=16),
     dict(N=2049, topk=64, dk=4, dv=64, dtype="bf16", bits=8),
     dict(N=600, topk=1024, dk=3, dv=128, dtype="f32", bits=10),
+    dict(N=300, topk=16, dk=3, dv=32, dtype="bf16", bits=10),
+    dict(N=1000, topk=100, dk=5, dv=256, dtype="bf16", bits=5),
+    dict(N=700, topk=1024, dk=3, dv=128, dtype="bf16", bits=10),
 ]
 
 
@@ -389,6 +392,10 @@ def test_forward_zorder_matches_position_order():
     torch.cuda.synchronize()
     assert torch.equal(a["idx"], b["idx"])
     assert torch.equal(a["out"].view(torch.int16), b["out"].view(torch.int16))
+    c = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, zorder=True, fused=True)
+    d = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, zorder=False, fused=True)
+    torch.cuda.synchronize()
+    assert torch.equal(c.view(torch.int16), d.view(torch.int16))
 
 
 # ----------------------------------------------------------------------------
@@ -425,7 +432,10 @@ def test_query_order(N, topk, causal):
 
 @pytest.mark.parametrize("cfg,causal", FORWARD)
 def test_select_attend_matches_two_calls(cfg, causal):
-    """The one-pass call gives the two calls' windows and output bits."""
+    """The one-pass call selects the two calls' windows.  float32 outputs are
+    the two calls' bits; bfloat16 outputs (matrix-core products) are checked
+    against the oracle's attention over those windows and against the two
+    calls' output."""
     w, x, f = inputs(cfg)
     log(f"select+attend config {cfg} causal={causal}")
     q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
@@ -433,11 +443,44 @@ def test_select_attend_matches_two_calls(cfg, causal):
     one = zeta.forward(q, k, v, w.topk, 0.5, causal, w.bits, fused=True, return_intermediates=True)
     torch.cuda.synchronize()
     assert torch.equal(two["idx"], one["idx"])
-    assert torch.equal(two["out"].view(torch.int16), one["out"].view(torch.int16))
+    S = w.segments
+    if w.dtype == "f32":
+        assert torch.equal(two["out"].view(torch.int32), one["out"].view(torch.int32))
+    else:
+        out1, out2 = host(one["out"]).reshape(S, w.N, w.dv), host(two["out"]).reshape(S, w.N, w.dv)
+        assert np.abs(out1 - out2).max() <= TOL[w.dtype]
+        idx = host(one["idx"]).reshape(S, w.N, w.topk)
+        rows = sample_rows(w.N, 64, 77) if w.N > 4096 else None
+        for s in range(0, S, max(1, S // 8)):
+            ref = oracle.attend(f["q"][s:s + 1], f["k"][s:s + 1], f["v"][s:s + 1],
+                                (idx[s:s + 1, rows] if rows is not None else idx[s:s + 1]), 0.5, rows=rows)
+            got = out1[s, rows] if rows is not None else out1[s]
+            assert np.abs(got - ref[0]).max() <= TOL[w.dtype], s
     if cfg == 1:
         ref = oracle.forward(f["q"], f["k"], f["v"], w.topk, 0.5, causal, w.bits)
         assert np.array_equal(host(one["idx"]).reshape(w.segments, w.N, w.topk), ref["idx"])
         assert np.abs(host(one["out"]).reshape(w.segments, w.N, w.dv) - ref["out"]).max() <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("cfg,causal", [(2, True), (3, False), (4, True)])
+def test_select_attend_processing_order_changes_nothing(cfg, causal):
+    """A query's one-pass result depends only on its own window: position
+    order, Z-order, the level-regrouped Z-order and a random order give the
+    same output bits."""
+    w, x, _ = inputs(cfg)
+    log(f"select+attend processing order config {cfg} causal={causal}")
+    oc = oracle_codes(cfg)
+    q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
+    qc, sc, perm = u32_to_dev(oc["q_codes"]), u32_to_dev(oc["sorted_codes"]), i32_to_dev(oc["perm"])
+    S = w.segments
+    z = np.argsort(oc["q_codes"], axis=1, kind="stable").astype(np.int32)
+    rng = np.random.default_rng(11)
+    orders = [None, i32_to_dev(z), zeta.zeta_query_order(i32_to_dev(z), w.N, S, w.topk, causal),
+              i32_to_dev(np.stack([rng.permutation(w.N) for _ in range(S)]))]
+    outs = [zeta.zeta_select_attend_fwd(q, k, v, qc, sc, perm, w.topk, causal, 0.5, q_order=o) for o in orders]
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(outs[0].view(torch.int16), o.view(torch.int16))
 
 
 @pytest.mark.parametrize("shape", EDGE, ids=[f"N{e['N']}-k{e['topk']}-dk{e['dk']}" for e in EDGE])
