@@ -189,15 +189,24 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
 /*
  * zeta_select_attend_fwd -- zeta_select_topk and zeta_topk_attn_fwd in one
  * pass (same definitions, Section 3.2.2 and Algorithm 1, Steps 3-5; Section
- * 3.3, equation cauchy; Section 3.4; Appendix E.1).  Each query's window stays
- * on chip instead of travelling through an index tensor; `out` holds the same
- * bits that the two calls would produce.
+ * 3.3, equation cauchy; Section 3.4; Appendix E.1).  No index tensor is
+ * needed: the windows are kept as list-index bounds (8 bytes per query in the
+ * workspace) instead of k positions per query.
+ *
+ * float32: each query is served as by the two calls, and `out` holds their
+ * bits.  bfloat16: 16 neighbouring queries of the processing order share one
+ * pass over the union of their windows, and the weighted sum of value rows
+ * runs on the matrix cores (scores split into two bfloat16 parts, float32
+ * accumulation).  The output agrees with the two calls to float32 rounding,
+ * and a query's bits depend only on its own window, so they are the same for
+ * every processing order.
  *
  *   q, k, v, dtype, B, H, N, d_k, d_v, topk, eps, out: as for
  *            zeta_topk_attn_fwd; causal as for zeta_select_topk.
  *   q_codes, sorted_codes, perm, q_order: as for zeta_select_topk.
- *   idx_out  optional int32 [B*H][N][topk]: receives the windows.
- *   workspace  at least zeta_workspace_size(...) bytes.
+ *   idx_out  optional int32 [B*H][N][topk]: receives the windows, exactly as
+ *            zeta_select_topk writes them.
+ *   workspace  at least zeta_workspace_size(...) bytes, 16-byte aligned.
  */
 zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
                                      int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,

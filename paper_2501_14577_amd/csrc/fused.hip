@@ -247,9 +247,12 @@ hipError_t launch_select_attend(const void* q, const void* k, const void* v, boo
     const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
     if (e != hipSuccess) return e;
   }
-  if (is_bf16 && tile_supports(dv))
+  if (is_bf16 && tile_supports(dv)) {
+    int2* bounds = reinterpret_cast<int2*>(static_cast<char*>(workspace) +
+                                           fused_ws(S, N, topk, causal ? 1 : 0).bounds_off);
     return launch_select_attend_tile(q, k, v, S, N, dk, dv, topk, causal, q_codes, sorted_codes, perm, list_codes,
-                                     list_pos, q_order, eps, out, idx_out, stream);
+                                     list_pos, q_order, eps, out, idx_out, bounds, stream);
+  }
 #define ZETA_FUSED_CASE(DVV)                                                                                    \
   case DVV:                                                                                                     \
     return is_bf16 ? launch_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm,    \

@@ -133,6 +133,18 @@ inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
+// One-pass select and attend on the matrix cores: the prefix lists (as for
+// select), then each processing-order slot's window bounds (two int32).
+struct FusedWs {
+  size_t bounds_off, bytes;
+};
+inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
+  FusedWs w;
+  w.bounds_off = align_up(select_ws(S, N, topk, causal).bytes);
+  w.bytes = w.bounds_off + align_up(size_t(S) * size_t(N) * 2 * sizeof(int32_t));
+  return w;
+}
+
 // Regrouping a processing order by list level: a copy of the given order
 // (when it is regrouped in place) and the radix pass's histograms.
 struct QueryOrderWs {

@@ -86,24 +86,101 @@ __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t (&o)[W]) 
   }
 }
 
+// ---- window bounds ---------------------------------------------------------
+// One wavefront serves a run of kBndRun consecutive slots of the processing
+// order, as the select kernel does (galloping search from the previous
+// query's insertion point), and writes each query's window as list-index
+// bounds (a, b) at its slot; slots without a query get (0, -1).  With idx_out
+// it also writes the window's positions, as the select kernel would.
+constexpr int kBndRun = 32;
+constexpr int kBndWaves = 8;
+
+__global__ void __launch_bounds__(kBndWaves * 64)
+    window_bounds_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
+                         const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
+                         const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
+                         int64_t N, int topk, int causal, int t0, int t_hi, int64_t cap, int2* __restrict__ bounds,
+                         int32_t* __restrict__ idx_out) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t runs = (total + kBndRun - 1) / kBndRun;
+  const int64_t nb = gridDim.x;
+  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kBndWaves < runs; blk += nb) {
+    const int64_t run = blk * kBndWaves + wave;
+    if (run >= runs) continue;
+    const int64_t slot0 = run * kBndRun;
+    int32_t my_i = -1;
+    uint32_t my_key = 0;
+    {
+      const int64_t sl = slot0 + lane;
+      if (lane < kBndRun && sl < total) {
+        const int64_t sg = sl / N;
+        const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
+        if (ii >= 0 && ii < N) {
+          my_i = int32_t(ii);
+          my_key = q_codes[sg * N + ii];
+        }
+      }
+    }
+    int2 my_b = make_int2(0, -1);
+    const uint32_t* prev_codes = nullptr;
+    uint32_t prev_key = 0;
+    int32_t prev_p = 0;
+    for (int u = 0; u < kBndRun; ++u) {
+      const int64_t slot = slot0 + u;
+      if (slot >= total) break;
+      const int32_t i = __builtin_amdgcn_readlane(my_i, u);
+      const uint32_t key = uint32_t(__builtin_amdgcn_readlane(int32_t(my_key), u));
+      if (i < 0) continue;
+      const int64_t seg = slot / N;
+      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap);
+      const int32_t p = (L.codes == prev_codes && key >= prev_key) ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
+                                                                   : wave_lower_bound(L.codes, 0, L.n, key, lane);
+      prev_codes = L.codes;
+      prev_key = key;
+      prev_p = p;
+      const WindowBounds wb = select_window_bounds(L, p, topk, lane);
+      if (lane == u) my_b = make_int2(wb.a, wb.b);
+      if (idx_out != nullptr) {
+        // The window's positions in list order, then -1.
+        int32_t* row = idx_out + (seg * N + i) * int64_t(topk);
+        int cnt = 0;
+        for (int32_t e0 = wb.a; e0 <= wb.b; e0 += 64) {
+          const int32_t e = e0 + lane;
+          const int32_t pv = e <= wb.b ? L.pos[e] : INT32_MAX;
+          const bool ok = pv <= L.limit;
+          const uint64_t bal = wave_ballot(ok);
+          if (ok) row[cnt + int(lanes_below(bal))] = pv;
+          cnt += __popcll(bal);
+        }
+        for (int c = cnt + lane; c < topk; c += 64) row[c] = -1;
+      }
+    }
+    if (lane < kBndRun && slot0 + lane < total) bounds[slot0 + lane] = my_b;
+  }
+}
+
+// ---- attention over the windows ----------------------------------------------
+
 template <int DV, int DK, bool kOff32>
 __global__ void __launch_bounds__(kTileWaves * 64)
     select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-                              const uint16_t* __restrict__ v, const uint32_t* __restrict__ q_codes,
-                              const uint32_t* __restrict__ sorted_codes, const int32_t* __restrict__ perm,
-                              const uint32_t* __restrict__ list_codes, const int32_t* __restrict__ list_pos,
-                              const int32_t* __restrict__ order, int64_t total, int64_t N, int dk_rt, int topk,
-                              int causal, int t0, int t_hi, int64_t cap, float eps, uint16_t* __restrict__ out,
-                              int32_t* __restrict__ idx_out) {
+                              const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
+                              const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
+                              const int2* __restrict__ bounds, int64_t total, int64_t N, int dk_rt, int causal,
+                              int t0, int t_hi, int64_t cap, float eps, uint16_t* __restrict__ out) {
   constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
   constexpr int W = E / 2;    // 32-bit words per lane and row
   constexpr int KD = DK > 0 ? DK : kMaxDk;
+  constexpr int kStage = DK == 3 ? 16 : 4;  // chunks whose positions and key rows are staged at once
+  constexpr int kStageEntries = kStage * kChunk;
   static_assert(E >= 2 && E % 2 == 0, "d_v must be a multiple of 32");
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
 
-  __shared__ int32_t s_pos[kTileWaves][kChunk];
-  __shared__ float s_k[kTileWaves][kChunk][KD];
+  __shared__ int32_t s_ch[kTileWaves][kStage];
+  __shared__ int32_t s_pos[kTileWaves][kStageEntries];
+  __shared__ float s_k[kTileWaves][kStageEntries][KD];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -116,11 +193,11 @@ __global__ void __launch_bounds__(kTileWaves * 64)
     const int64_t tile = blk * kTileWaves + wave;
     if (tile >= tiles) continue;
 
-    // The tile's queries: lanes with equal qn hold the same one.
+    // The tile's queries and windows: lanes with equal qn hold the same one.
     int32_t my_i = -1;
     int64_t my_seg = 0;
-    uint32_t my_key = 0;
     int my_lvl = 0;
+    int32_t my_a = 0, my_b = -1;
     {
       const int64_t sl = tile * kTileQ + qn;
       if (sl < total) {
@@ -129,8 +206,10 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         if (ii >= 0 && ii < N) {
           my_i = int32_t(ii);
           my_seg = sg;
-          my_key = q_codes[sg * N + ii];
           my_lvl = causal ? query_level(my_i, t0, t_hi) : 0;
+          const int2 bb = bounds[sl];
+          my_a = bb.x;
+          my_b = bb.y;
         }
       }
     }
@@ -141,53 +220,17 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       const int leader = __ffs(int(pending)) - 1;
       const int64_t g_seg = __builtin_amdgcn_readlane(int32_t(my_seg), leader);
       const int g_lvl = __builtin_amdgcn_readlane(my_lvl, leader);
-      const int32_t g_i = __builtin_amdgcn_readlane(my_i, leader);
       const uint32_t gmask =
           uint32_t(wave_ballot(my_i >= 0 && my_seg == g_seg && my_lvl == g_lvl)) & pending;
       pending &= ~gmask;
-      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, g_seg, N, g_i, causal, t0, t_hi, cap);
-
-      // Window bounds of every query of the group.
-      int32_t my_a = 0, my_b = -1;
-      {
-        const uint32_t* prev_codes = nullptr;
-        uint32_t prev_key = 0;
-        int32_t prev_p = 0;
-        for (uint32_t m = gmask; m != 0u; m &= m - 1u) {
-          const int u = __ffs(int(m)) - 1;
-          const int32_t i = __builtin_amdgcn_readlane(my_i, u);
-          const uint32_t key = uint32_t(__builtin_amdgcn_readlane(int32_t(my_key), u));
-          QueryList Lq = L;
-          Lq.limit = causal ? i : int32_t(N - 1);
-          const int32_t p = (prev_codes == Lq.codes && key >= prev_key)
-                                ? wave_lower_bound_near(Lq.codes, prev_p, Lq.n, key, lane)
-                                : wave_lower_bound(Lq.codes, 0, Lq.n, key, lane);
-          prev_codes = Lq.codes;
-          prev_key = key;
-          prev_p = p;
-          const WindowBounds wb = select_window_bounds(Lq, p, topk, lane);
-          if (qn == u) {
-            my_a = wb.a;
-            my_b = wb.b;
-          }
-          if (idx_out != nullptr) {
-            // The window's positions in list order, then -1.
-            int32_t* row = idx_out + (g_seg * N + i) * int64_t(topk);
-            int cnt = 0;
-            for (int32_t e0 = wb.a; e0 <= wb.b; e0 += 64) {
-              const int32_t e = e0 + lane;
-              const int32_t pv = e <= wb.b ? Lq.pos[e] : INT32_MAX;
-              const bool ok = pv <= Lq.limit;
-              const uint64_t bal = wave_ballot(ok);
-              if (ok) row[cnt + int(lanes_below(bal))] = pv;
-              cnt += __popcll(bal);
-            }
-            for (int c = cnt + lane; c < topk; c += 64) row[c] = -1;
-          }
-        }
+      const int32_t* lpos = sorted_pos + g_seg * N;
+      int32_t ln = int32_t(N);
+      if (causal && g_lvl <= t_hi) {
+        lpos = list_pos + g_seg * cap + ((int64_t(1) << g_lvl) - (int64_t(1) << t0));
+        ln = int32_t(1) << g_lvl;
       }
 
-      const bool mine = ((gmask >> qn) & 1u) != 0u;
+      const bool mine = ((gmask >> qn) & 1u) != 0u && my_a <= my_b;
       const int32_t my_lim = causal ? my_i : int32_t(N - 1);
       float qv[KD];
       if (mine) {
@@ -210,89 +253,110 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       const uint16_t* kseg = k + g_seg * N * dk;
       const Off col = Off(qn * E);
 
-      // Walk the chunks that meet some window, in list order.
-      int c = wave_min_int(mine && my_a <= my_b ? my_a / kChunk : INT32_MAX);
+      // The chunks that meet some window, in list order, kStage at a time.
+      int c = wave_min_int(mine ? my_a / kChunk : INT32_MAX);
       while (c != INT32_MAX) {
-        const int32_t r0 = c * kChunk;
-        if (lane < kChunk) {
-          const int32_t r = r0 + lane;
-          const int32_t pv = r < L.n ? L.pos[r] : -1;
-          s_pos[wave][lane] = pv;
-          float kv[KD];
-          if (pv >= 0) {
-            if constexpr (DK == 3) {
-              Row3<uint16_t>::load(k, g_seg * N + pv, total, kv);
+        int nch = 0;
+        while (c != INT32_MAX && nch < kStage) {
+          if (lane == 0) s_ch[wave][nch] = c;
+          ++nch;
+          const int nxt = c + 1;
+          const int cand = (mine && my_b >= nxt * kChunk) ? (my_a / kChunk > nxt ? my_a / kChunk : nxt) : INT32_MAX;
+          c = wave_min_int(cand);
+        }
+        wave_lds_sync();
+
+        // Stage the positions, then the key rows, of all nch chunks.
+        {
+          int32_t pv[kStageEntries / 64];
+#pragma unroll
+          for (int t = 0; t < kStageEntries / 64; ++t) {
+            const int e = t * 64 + lane;
+            pv[t] = -1;
+            if (e < nch * kChunk) {
+              const int32_t r = s_ch[wave][e / kChunk] * kChunk + (e % kChunk);
+              if (r < ln) pv[t] = lpos[r];
+            }
+          }
+#pragma unroll
+          for (int t = 0; t < kStageEntries / 64; ++t) {
+            const int e = t * 64 + lane;
+            if (e < nch * kChunk) {
+              float kv[KD];
+              if (pv[t] >= 0) {
+                if constexpr (DK == 3) {
+                  Row3<uint16_t>::load(k, g_seg * N + pv[t], total, kv);
+                } else {
+#pragma unroll
+                  for (int a = 0; a < KD; ++a)
+                    kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv[t]) * dk + a]) : 0.0f;
+                }
+              } else {
+#pragma unroll
+                for (int a = 0; a < KD; ++a) kv[a] = 0.0f;
+              }
+              s_pos[wave][e] = pv[t];
+#pragma unroll
+              for (int a = 0; a < KD; ++a) s_k[wave][e][a] = kv[a];
+            }
+          }
+        }
+        wave_lds_sync();
+
+        for (int ch = 0; ch < nch; ++ch) {
+          const int32_t r0 = s_ch[wave][ch] * kChunk;
+          Frag b_hi, b_lo;
+          uint32_t raw[8][W];
+#pragma unroll
+          for (int kk = 0; kk < 8; ++kk) {
+            const int rr = ch * kChunk + kg * 8 + kk;
+            const int32_t r = r0 + kg * 8 + kk;
+            const int32_t pv = s_pos[wave][rr];
+            const bool in = mine && r >= my_a && r <= my_b && pv >= 0 && pv <= my_lim;
+            float s = 0.0f;
+            if (in) {
+              float d2 = 0.0f;
+#pragma unroll
+              for (int a = 0; a < KD; ++a) {
+                if (a < dk) {
+                  const float diff = qv[a] - s_k[wave][rr][a];
+                  d2 = fmaf(diff, diff, d2);
+                }
+              }
+              s = 1.0f / (d2 + eps);
+            }
+            zpart += s;
+            const uint32_t hi = float_to_bf16_bits(s);
+            const uint32_t lo = float_to_bf16_bits(s - __uint_as_float(hi << 16));
+            if (kk & 1) {
+              b_hi.w[kk >> 1] |= hi << 16;
+              b_lo.w[kk >> 1] |= lo << 16;
+            } else {
+              b_hi.w[kk >> 1] = hi;
+              b_lo.w[kk >> 1] = lo;
+            }
+            // The row is needed when any query of the tile takes it.
+            const bool used = ((wave_ballot(in) >> (kg * 16)) & 0xFFFFull) != 0ull;
+            if (used) {
+              load_words<W>(vseg + (Off(pv) * Off(DV) + col), raw[kk]);
             } else {
 #pragma unroll
-              for (int a = 0; a < KD; ++a) kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv) * dk + a]) : 0.0f;
+              for (int t = 0; t < W; ++t) raw[kk][t] = 0u;
             }
-          } else {
-#pragma unroll
-            for (int a = 0; a < KD; ++a) kv[a] = 0.0f;
           }
 #pragma unroll
-          for (int a = 0; a < KD; ++a) s_k[wave][lane][a] = kv[a];
+          for (int j = 0; j < E; ++j) {
+            Frag a;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
+              a.w[t] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+            }
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_hi.v, acc[j], 0, 0, 0);
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_lo.v, acc[j], 0, 0, 0);
+          }
         }
         wave_lds_sync();
-
-        Frag b_hi, b_lo;
-        uint32_t raw[8][W];
-#pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
-          const int rr = kg * 8 + kk;
-          const int32_t r = r0 + rr;
-          const int32_t pv = s_pos[wave][rr];
-          const bool in = mine && r >= my_a && r <= my_b && pv >= 0 && pv <= my_lim;
-          float s = 0.0f;
-          if (in) {
-            float d2 = 0.0f;
-#pragma unroll
-            for (int a = 0; a < KD; ++a) {
-              if (a < dk) {
-                const float diff = qv[a] - s_k[wave][rr][a];
-                d2 = fmaf(diff, diff, d2);
-              }
-            }
-            s = 1.0f / (d2 + eps);
-          }
-          zpart += s;
-          const uint32_t hi = float_to_bf16_bits(s);
-          const uint32_t lo = float_to_bf16_bits(s - __uint_as_float(hi << 16));
-          if (kk & 1) {
-            b_hi.w[kk >> 1] |= hi << 16;
-            b_lo.w[kk >> 1] |= lo << 16;
-          } else {
-            b_hi.w[kk >> 1] = hi;
-            b_lo.w[kk >> 1] = lo;
-          }
-          // The row is needed when any query of the tile takes it.
-          const bool used = ((wave_ballot(in) >> (kg * 16)) & 0xFFFFull) != 0ull;
-          if (used) {
-            load_words<W>(vseg + (Off(pv) * Off(DV) + col), raw[kk]);
-          } else {
-#pragma unroll
-            for (int t = 0; t < W; ++t) raw[kk][t] = 0u;
-          }
-        }
-#pragma unroll
-        for (int j = 0; j < E; ++j) {
-          Frag a;
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
-            a.w[t] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-          }
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_hi.v, acc[j], 0, 0, 0);
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_lo.v, acc[j], 0, 0, 0);
-        }
-        wave_lds_sync();
-
-        // Next chunk that meets a window.
-        const int nxt = c + 1;
-        const int cand = (mine && my_a <= my_b && my_b >= nxt * kChunk)
-                             ? (my_a / kChunk > nxt ? my_a / kChunk : nxt)
-                             : INT32_MAX;
-        c = wave_min_int(cand);
       }
 
       // Normalise and store: lane holds columns 4kg..4kg+3 of every block,
@@ -300,7 +364,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       float z = zpart;
       z += __shfl_xor(z, 16, 64);
       z += __shfl_xor(z, 32, 64);
-      if (mine) {
+      if (((gmask >> qn) & 1u) != 0u) {
         const float inv = z > 0.0f ? 1.0f / z : 0.0f;
         float o[4 * E];
 #pragma unroll
@@ -317,9 +381,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 
 template <int DV, int DK>
 hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
-                         int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
-                         const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                         const int32_t* q_order, float eps, uint16_t* out, int32_t* idx_out, hipStream_t stream) {
+                         int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
+                         const int32_t* q_order, const int2* bounds, float eps, uint16_t* out, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   const int64_t tiles = ceil_div(total, kTileQ);
@@ -328,25 +391,22 @@ hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v
   const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
   if (off32)
     hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, true>), dim3(blocks), dim3(kTileWaves * 64), 0, stream, q,
-                       k, v, q_codes, sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk,
-                       causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap, eps, out, idx_out);
+                       k, v, perm, list_pos, q_order, bounds, total, N, dk, causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap,
+                       eps, out);
   else
     hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, false>), dim3(blocks), dim3(kTileWaves * 64), 0, stream,
-                       q, k, v, q_codes, sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk,
-                       causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap, eps, out, idx_out);
+                       q, k, v, perm, list_pos, q_order, bounds, total, N, dk, causal ? 1 : 0, lp.t0, lp.t_hi,
+                       lp.cap, eps, out);
   return hipGetLastError();
 }
 
 template <int DV>
 hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
-                          int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
-                          const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                          const int32_t* q_order, float eps, uint16_t* out, int32_t* idx_out, hipStream_t stream) {
+                          int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
+                          const int32_t* q_order, const int2* bounds, float eps, uint16_t* out, hipStream_t stream) {
   if (dk == 3)
-    return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
-                                q_order, eps, out, idx_out, stream);
-  return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
-                              q_order, eps, out, idx_out, stream);
+    return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, eps, out, stream);
+  return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, eps, out, stream);
 }
 
 }  // namespace
@@ -356,16 +416,25 @@ bool tile_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 2
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
                                      int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out,
+                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out, int2* bounds,
                                      hipStream_t stream) {
+  const ListPlan lp = list_plan(N, topk);
+  const int64_t total = S * N;
+  {
+    const int64_t runs = ceil_div(total, kBndRun);
+    const int64_t want = ceil_div(runs, kBndWaves);
+    const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
+    hipLaunchKernelGGL(window_bounds_kernel, dim3(blocks), dim3(kBndWaves * 64), 0, stream, q_codes, sorted_codes,
+                       perm, list_codes, list_pos, q_order, total, N, topk, causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap,
+                       bounds, idx_out);
+  }
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);
   const uint16_t* vv = static_cast<const uint16_t*>(v);
   uint16_t* oo = static_cast<uint16_t*>(out);
 #define ZETA_TILE_CASE(DVV) \
   case DVV:                 \
-    return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos, \
-                               q_order, eps, oo, idx_out, stream);
+    return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, eps, oo, stream);
   switch (dv) {
     ZETA_TILE_CASE(32)
     ZETA_TILE_CASE(64)

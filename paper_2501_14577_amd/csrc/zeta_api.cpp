@@ -133,8 +133,15 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
   const int64_t S = B * H;
-  const zeta::SelectWs ws = zeta::select_ws(S, N, topk, causal);
-  if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
+  if (dtype == ZETA_BF16 && zeta::tile_supports(d_v)) {
+    // Lists and per-slot window bounds.
+    const zeta::FusedWs ws = zeta::fused_ws(S, N, topk, causal);
+    if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return ZETA_ERR_INVALID_ARG;
+  } else {
+    const zeta::SelectWs ws = zeta::select_ws(S, N, topk, causal);
+    if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
+  }
   return hip_status(zeta::launch_select_attend(q, k, v, dtype == ZETA_BF16, S, N, d_k, d_v, topk, causal != 0, q_codes,
                                                sorted_codes, perm, q_order, eps, out, idx_out, workspace, stream));
 }
@@ -147,6 +154,8 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
   const size_t sb = zeta::sort_ws(2 * S, N, d_k * bits).bytes;
   const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
   const size_t ob = zeta::query_order_ws(S, N).bytes;
+  const size_t fb = zeta::fused_ws(S, N, topk, causal ? 1 : 0).bytes;
+  if (fb > bytes) bytes = fb;
   if (sb > bytes) bytes = sb;
   if (lb > bytes) bytes = lb;
   if (ob > bytes) bytes = ob;

@@ -181,6 +181,7 @@ FUSED_CASES = [
     (dict(eps=float("nan")), INV), (dict(v=ctypes.c_void_p(0x30004)), INV), (dict(out=P), INV),
     (dict(dtype=9), UNS), (dict(d_k=9), UNS), (dict(d_v=48), UNS), (dict(topk=1025), UNS),
     (dict(ws=NULL), WSP), (dict(ws_bytes=32), WSP),
+    (dict(ws=ctypes.c_void_p(0x80008)), INV),  # bf16 one pass keeps 8-byte bounds in the workspace
 ]
 
 
