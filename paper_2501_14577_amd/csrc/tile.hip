@@ -8,30 +8,39 @@
 // processing order of zeta_query_order, 16 consecutive queries search one list
 // at nearby insertion points, so their ranges overlap: together they span
 // about twice the window length where gathering per query would read 16
-// windows.  A wavefront takes such a tile and walks the union of its ranges
-// in chunks of 32 list entries.  For each chunk it
-//   - stages the entries' positions and key rows in LDS;
-//   - scores the 16 x 32 (query, entry) pairs, S = 1 / (|q - k|^2 + eps) when
-//     the entry lies in the query's window and pool, else 0;
-//   - loads each entry's value row once for the whole tile;
-//   - accumulates V^T (16 value columns x 32 entries) times S^T (32 entries x
-//     16 queries) with v_mfma_f32_16x16x32_bf16, once per 16 value columns.
-// Scores are float32; each is split into a bfloat16 high part and a bfloat16
-// remainder, and both products are accumulated, so the weights carry 16
-// significant bits and the products are exact in the float32 accumulator.
+// windows.
+//
+// Two kernels:
+//  1. window_bounds: each query's range [a, b], 8 bytes per processing-order
+//     slot (the select kernel's search and scans, without the index row);
+//  2. the tile kernel: a wavefront takes 16 consecutive slots and walks the
+//     union of their ranges in chunks of 16 list entries.  The positions and
+//     key rows of up to 512 entries are staged in LDS in one burst.  Then for
+//     each chunk it
+//       - scores the 16 x 16 (query, entry) pairs, S = 1 / (|q - k|^2 + eps)
+//         when the entry lies in the query's range and pool, else 0;
+//       - loads each entry's value row once for the whole tile (the next
+//         chunk's rows load while the current chunk is multiplied);
+//       - accumulates V^T (16 value columns x 16 entries) times S^T (16
+//         entries x 16 queries) with v_mfma_f32_16x16x16_bf16, once per 16
+//         value columns.
+// Scores are float32 (hardware reciprocal, 1 ulp); each is split into a
+// bfloat16 high part and a bfloat16 remainder, and both products are
+// accumulated, so the weights carry 16 significant bits and the products are
+// exact in the float32 accumulator.
 // The normaliser sums the float32 scores.
 //
-// Operand layout of the 16x16x32 product (lane l, kg = l / 16):
-//   A (value columns x entries): lane l holds entries 8kg..8kg+7 of column
+// Operand layout of the 16x16x16 product (lane l, kg = l / 16):
+//   A (value columns x entries): lane l holds entries 4kg..4kg+3 of column
 //     l % 16;
-//   B (entries x queries): entries 8kg..8kg+7 of query l % 16;
+//   B (entries x queries): entries 4kg..4kg+3 of query l % 16;
 //   D (columns x queries): columns 4kg..4kg+3 of query l % 16.
 // Column c of block j is value element c * E + j (E = d_v / 16), so a lane
-// loads E consecutive elements of each of its 8 rows with one instruction and
+// loads E consecutive elements of each of its 4 rows with one instruction and
 // ends with 4E consecutive outputs of one query.
 //
-// Chunks are aligned to multiples of 32 in the list and a query's scores are
-// zero outside its window, so its output depends only on its own window: the
+// Chunks are aligned to multiples of 16 in the list and a query's scores are
+// zero outside its range, so its output depends only on its own window: the
 // result is the same whatever tile the query falls in, i.e. for any
 // processing order.
 #include "attend_device.h"
@@ -44,15 +53,15 @@ namespace zeta {
 namespace {
 
 constexpr int kTileQ = 16;     // queries per tile (product columns)
-constexpr int kChunk = 32;     // list entries per product step
+constexpr int kChunk = 16;     // list entries per product step
 constexpr int kTileWaves = 4;  // wavefronts per block
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-union Frag {
-  uint32_t w[4];
-  bf16x8_t v;
+union Frag {  // four bfloat16 values
+  uint32_t w[2];
+  s16x4_t v;
 };
 
 __device__ __forceinline__ int wave_min_int(int x) {
@@ -172,8 +181,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
   constexpr int W = E / 2;    // 32-bit words per lane and row
   constexpr int KD = DK > 0 ? DK : kMaxDk;
-  constexpr int kStage = DK == 3 ? 16 : 4;  // chunks whose positions and key rows are staged at once
-  constexpr int kStageEntries = kStage * kChunk;
+  constexpr int kStageEntries = DK == 3 ? 512 : 128;  // entries whose positions and key rows are staged at once
+  constexpr int kStage = kStageEntries / kChunk;
   static_assert(E >= 2 && E % 2 == 0, "d_v must be a multiple of 32");
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
@@ -185,7 +194,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int qn = lane & (kTileQ - 1);  // this lane's query in the tile; also its value column in a block
-  const int kg = lane >> 4;            // this lane's entries in a chunk: 8kg .. 8kg+7
+  const int kg = lane >> 4;            // this lane's entries in a chunk: 4kg .. 4kg+3
   const int64_t tiles = (total + kTileQ - 1) / kTileQ;
   const int64_t nb = gridDim.x;
 
@@ -253,6 +262,74 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       const uint16_t* kseg = k + g_seg * N * dk;
       const Off col = Off(qn * E);
 
+      // Window and pool tests as single unsigned compares: entry r is in the
+      // window when r - a <= b - a, its position in the pool when
+      // pos <= limit (a missing entry holds -1, i.e. 0xFFFFFFFF).
+      const uint32_t span = mine ? uint32_t(my_b - my_a) : 0u;
+      const int32_t a_eff = mine ? my_a : INT32_MIN;
+      const uint32_t lim_u = uint32_t(my_lim);
+
+      // Scores of this lane's 4 entries of staged chunk `ch` for its query,
+      // split into bfloat16 parts, and the loads of the entries' value rows.
+      // Branch-free, so that loads in flight can be counted across chunks: a
+      // chunk index at or past nch scores nothing, and every lane loads a
+      // row (a row nobody takes reads row 0, finite by contract, with weight
+      // 0).  The reciprocal is the hardware one (1 ulp).  A score s is split
+      // as hi = s with the low 16 bits cleared and lo = the same truncation
+      // of s - hi (exact), so hi + lo carries 16 significant bits of s.
+      auto prep = [&](int ch, int nch_, uint32_t(&raw)[4][W], uint32_t(&bh)[2], uint32_t(&bl)[2]) {
+        const bool live = ch < nch_;
+        const int chc = live ? ch : 0;
+        const int32_t r0 = s_ch[wave][chc] * kChunk;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const int rr = chc * kChunk + kg * 4 + kk;
+          const int32_t r = r0 + kg * 4 + kk;
+          const int32_t pv = s_pos[wave][rr];
+          const bool in = live && uint32_t(r - a_eff) <= span && uint32_t(pv) <= lim_u;
+          float d2 = 0.0f;
+#pragma unroll
+          for (int a = 0; a < KD; ++a) {
+            if (a < dk) {
+              const float diff = qv[a] - s_k[wave][rr][a];
+              d2 = fmaf(diff, diff, d2);
+            }
+          }
+          const float sc = in ? __builtin_amdgcn_rcpf(d2 + eps) : 0.0f;
+          zpart += sc;
+          const uint32_t hi = __float_as_uint(sc) & 0xFFFF0000u;
+          const uint32_t lo = __float_as_uint(sc - __uint_as_float(hi)) & 0xFFFF0000u;
+          if (kk & 1) {
+            bh[kk >> 1] |= hi;
+            bl[kk >> 1] |= lo;
+          } else {
+            bh[kk >> 1] = hi >> 16;
+            bl[kk >> 1] = lo >> 16;
+          }
+          const bool used = ((wave_ballot(in) >> (kg * 16)) & 0xFFFFull) != 0ull;
+          load_words<W>(vseg + (Off(used ? pv : 0) * Off(DV) + col), raw[kk]);
+        }
+      };
+      // acc[j] += V^T (block j) * S^T for one chunk, high and low score parts.
+      auto mma = [&](const uint32_t(&raw)[4][W], const uint32_t(&bh)[2], const uint32_t(&bl)[2]) {
+        Frag b_hi, b_lo;
+        b_hi.w[0] = bh[0];
+        b_hi.w[1] = bh[1];
+        b_lo.w[0] = bl[0];
+        b_lo.w[1] = bl[1];
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+          Frag a;
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
+            a.w[t] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+          }
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.v, b_hi.v, acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.v, b_lo.v, acc[j], 0, 0, 0);
+        }
+      };
+
       // The chunks that meet some window, in list order, kStage at a time.
       int c = wave_min_int(mine ? my_a / kChunk : INT32_MAX);
       while (c != INT32_MAX) {
@@ -303,58 +380,16 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         }
         wave_lds_sync();
 
-        for (int ch = 0; ch < nch; ++ch) {
-          const int32_t r0 = s_ch[wave][ch] * kChunk;
-          Frag b_hi, b_lo;
-          uint32_t raw[8][W];
-#pragma unroll
-          for (int kk = 0; kk < 8; ++kk) {
-            const int rr = ch * kChunk + kg * 8 + kk;
-            const int32_t r = r0 + kg * 8 + kk;
-            const int32_t pv = s_pos[wave][rr];
-            const bool in = mine && r >= my_a && r <= my_b && pv >= 0 && pv <= my_lim;
-            float s = 0.0f;
-            if (in) {
-              float d2 = 0.0f;
-#pragma unroll
-              for (int a = 0; a < KD; ++a) {
-                if (a < dk) {
-                  const float diff = qv[a] - s_k[wave][rr][a];
-                  d2 = fmaf(diff, diff, d2);
-                }
-              }
-              s = 1.0f / (d2 + eps);
-            }
-            zpart += s;
-            const uint32_t hi = float_to_bf16_bits(s);
-            const uint32_t lo = float_to_bf16_bits(s - __uint_as_float(hi << 16));
-            if (kk & 1) {
-              b_hi.w[kk >> 1] |= hi << 16;
-              b_lo.w[kk >> 1] |= lo << 16;
-            } else {
-              b_hi.w[kk >> 1] = hi;
-              b_lo.w[kk >> 1] = lo;
-            }
-            // The row is needed when any query of the tile takes it.
-            const bool used = ((wave_ballot(in) >> (kg * 16)) & 0xFFFFull) != 0ull;
-            if (used) {
-              load_words<W>(vseg + (Off(pv) * Off(DV) + col), raw[kk]);
-            } else {
-#pragma unroll
-              for (int t = 0; t < W; ++t) raw[kk][t] = 0u;
-            }
-          }
-#pragma unroll
-          for (int j = 0; j < E; ++j) {
-            Frag a;
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
-              a.w[t] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-            }
-            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_hi.v, acc[j], 0, 0, 0);
-            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b_lo.v, acc[j], 0, 0, 0);
-          }
+        // Value rows of chunk ch+1 load while chunk ch is multiplied.
+        const int nchu = __builtin_amdgcn_readfirstlane(nch);
+        uint32_t rA[4][W], rB[4][W], hA[2], lA[2], hB[2], lB[2];
+        prep(0, nchu, rA, hA, lA);
+        for (int ch = 0; ch < nchu; ch += 2) {
+          prep(ch + 1, nchu, rB, hB, lB);
+          mma(rA, hA, lA);
+          if (ch + 1 >= nchu) break;
+          prep(ch + 2, nchu, rA, hA, lA);
+          mma(rB, hB, lB);
         }
         wave_lds_sync();
       }
