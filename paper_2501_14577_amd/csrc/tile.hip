@@ -12,7 +12,8 @@
 //
 // Two kernels:
 //  1. window_bounds: each query's range [a, b], 8 bytes per processing-order
-//     slot (the select kernel's search and scans, without the index row);
+//     slot, one query per lane, reading a copy of the list around the run's
+//     insertion points in LDS;
 //  2. the tile kernel: a wavefront takes 16 consecutive slots and walks the
 //     union of their ranges in chunks of 16 list entries.  The positions and
 //     key rows of up to 512 entries are staged in LDS in one burst.  Then for
@@ -73,6 +74,17 @@ __device__ __forceinline__ int wave_min_int(int x) {
   return x;
 }
 
+// Lane `src`'s value of a pointer, read by every lane.  Each 32-bit half goes
+// through uint32_t: widening a negative int32 would sign-extend into the
+// high half.
+template <typename T>
+__device__ __forceinline__ T* readlane_ptr(T* p, int src) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int32_t(uint32_t(v)), src));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int32_t(uint32_t(v >> 32)), src));
+  return reinterpret_cast<T*>((uint64_t(hi) << 32) | uint64_t(lo));
+}
+
 // E consecutive bfloat16 elements (E / 2 words) from a 2E-byte aligned address.
 template <int W>
 __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t (&o)[W]) {
@@ -96,13 +108,64 @@ __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t (&o)[W]) 
 }
 
 // ---- window bounds ---------------------------------------------------------
-// One wavefront serves a run of kBndRun consecutive slots of the processing
-// order, as the select kernel does (galloping search from the previous
-// query's insertion point), and writes each query's window as list-index
-// bounds (a, b) at its slot; slots without a query get (0, -1).  With idx_out
-// it also writes the window's positions, as the select kernel would.
-constexpr int kBndRun = 32;
-constexpr int kBndWaves = 8;
+// Each lane serves one slot of the processing order (a run of 64 consecutive
+// slots per wavefront) and writes its query's window as list-index bounds
+// (a, b); slots without a query get (0, -1).  The window is select_window's,
+// found by the same steps one entry at a time: the lower bound of the code,
+// then up to k - floor(k/2) in-pool entries from it rightwards, floor(k/2)
+// plus the right side's shortfall leftwards, and more on the right when the
+// left side runs out.
+//
+// Consecutive slots search one list at nearby insertion points.  The list
+// range of kRegion entries around the run's first insertion point is copied
+// to LDS (codes and positions); a lane reads the list itself only outside it
+// or when its query searches another list.  With idx_out the run's windows
+// are also written as position rows, one wavefront-wide pass per query.
+constexpr int kBndWaves = 4;
+constexpr int kRegion = 1024;  // list entries staged per wavefront
+constexpr int kMargin = 384;   // of them before the run's first insertion point
+
+struct LaneList {
+  const uint32_t* codes;
+  const int32_t* pos;
+  const uint32_t* l_codes;  // LDS copy of [r0, r1), valid when staged
+  const int32_t* l_pos;
+  int32_t n, limit, r0, r1;
+  __device__ __forceinline__ uint32_t code(int32_t e) const {
+    return (e >= r0 && e < r1) ? l_codes[e - r0] : codes[e];
+  }
+  __device__ __forceinline__ int32_t position(int32_t e) const { return (e >= r0 && e < r1) ? l_pos[e - r0] : pos[e]; }
+};
+
+// Scan from entry e in direction dir (+1 or -1) for up to `need` in-pool
+// entries beyond the `got` already taken; records the first and last entry
+// taken (first only when got is 0).  Returns the new count; `e` ends just
+// past the last entry examined.
+__device__ __forceinline__ int lane_scan(const LaneList& L, int32_t& e, int dir, int need, int got, int32_t& first,
+                                         int32_t& last) {
+  constexpr int kStep = 8;
+  while (got < need && e >= 0 && e < L.n) {
+    int32_t v[kStep];
+#pragma unroll
+    for (int j = 0; j < kStep; ++j) {
+      const int32_t x = e + dir * j;
+      v[j] = (x >= 0 && x < L.n) ? L.position(x) : INT32_MAX;
+    }
+    int32_t stop = e + dir * kStep;
+#pragma unroll
+    for (int j = 0; j < kStep; ++j) {
+      const int32_t x = e + dir * j;
+      if (got < need && v[j] <= L.limit) {
+        if (got == 0) first = x;
+        last = x;
+        ++got;
+        if (got == need) stop = x + dir;
+      }
+    }
+    e = stop;
+  }
+  return got;
+}
 
 __global__ void __launch_bounds__(kBndWaves * 64)
     window_bounds_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
@@ -110,54 +173,128 @@ __global__ void __launch_bounds__(kBndWaves * 64)
                          const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
                          int64_t N, int topk, int causal, int t0, int t_hi, int64_t cap, int2* __restrict__ bounds,
                          int32_t* __restrict__ idx_out) {
+  __shared__ uint32_t s_codes[kBndWaves][kRegion];
+  __shared__ int32_t s_pos[kBndWaves][kRegion];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t runs = (total + kBndRun - 1) / kBndRun;
+  const int64_t runs = (total + 63) / 64;
   const int64_t nb = gridDim.x;
   for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kBndWaves < runs; blk += nb) {
     const int64_t run = blk * kBndWaves + wave;
     if (run >= runs) continue;
-    const int64_t slot0 = run * kBndRun;
+    const int64_t slot = run * 64 + lane;
     int32_t my_i = -1;
-    uint32_t my_key = 0;
-    {
-      const int64_t sl = slot0 + lane;
-      if (lane < kBndRun && sl < total) {
-        const int64_t sg = sl / N;
-        const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
-        if (ii >= 0 && ii < N) {
-          my_i = int32_t(ii);
-          my_key = q_codes[sg * N + ii];
-        }
+    uint32_t key = 0;
+    int64_t seg = 0;
+    if (slot < total) {
+      seg = slot / N;
+      const int64_t ii = order != nullptr ? int64_t(order[slot]) : slot - seg * N;
+      if (ii >= 0 && ii < N) {
+        my_i = int32_t(ii);
+        key = q_codes[seg * N + ii];
       }
     }
-    int2 my_b = make_int2(0, -1);
-    const uint32_t* prev_codes = nullptr;
-    uint32_t prev_key = 0;
-    int32_t prev_p = 0;
-    for (int u = 0; u < kBndRun; ++u) {
-      const int64_t slot = slot0 + u;
-      if (slot >= total) break;
-      const int32_t i = __builtin_amdgcn_readlane(my_i, u);
-      const uint32_t key = uint32_t(__builtin_amdgcn_readlane(int32_t(my_key), u));
-      if (i < 0) continue;
-      const int64_t seg = slot / N;
-      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap);
-      const int32_t p = (L.codes == prev_codes && key >= prev_key) ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
-                                                                   : wave_lower_bound(L.codes, 0, L.n, key, lane);
-      prev_codes = L.codes;
-      prev_key = key;
-      prev_p = p;
-      const WindowBounds wb = select_window_bounds(L, p, topk, lane);
-      if (lane == u) my_b = make_int2(wb.a, wb.b);
-      if (idx_out != nullptr) {
-        // The window's positions in list order, then -1.
-        int32_t* row = idx_out + (seg * N + i) * int64_t(topk);
+    const bool valid = my_i >= 0;
+    const uint64_t vmask = wave_ballot(valid);
+    if (vmask == 0ull) continue;
+    const QueryList Lq = query_list(sorted_codes, perm, list_codes, list_pos, seg, N, valid ? my_i : 0, causal, t0,
+                                    t_hi, cap);
+
+    // Stage the leader's list around the leader's insertion point.
+    const int leader = __ffsll((unsigned long long)vmask) - 1;
+    const uint32_t* g_codes = readlane_ptr(Lq.codes, leader);
+    const int32_t* g_pos = readlane_ptr(Lq.pos, leader);
+    const int32_t g_n = __builtin_amdgcn_readlane(Lq.n, leader);
+    const uint32_t g_key = uint32_t(__builtin_amdgcn_readlane(int32_t(key), leader));
+    const int32_t p0 = wave_lower_bound(g_codes, 0, g_n, g_key, lane);
+    const int32_t r0 = p0 - kMargin > 0 ? p0 - kMargin : 0;
+    const int32_t r1 = r0 + kRegion < g_n ? r0 + kRegion : g_n;
+    {
+      uint32_t cv[kRegion / 64];
+      int32_t pv[kRegion / 64];
+#pragma unroll
+      for (int t = 0; t < kRegion / 64; ++t) {
+        const int32_t e = r0 + t * 64 + lane;
+        cv[t] = e < r1 ? g_codes[e] : 0u;
+        pv[t] = e < r1 ? g_pos[e] : 0;
+      }
+#pragma unroll
+      for (int t = 0; t < kRegion / 64; ++t) {
+        s_codes[wave][t * 64 + lane] = cv[t];
+        s_pos[wave][t * 64 + lane] = pv[t];
+      }
+    }
+    wave_lds_sync();
+
+    LaneList L;
+    L.codes = Lq.codes;
+    L.pos = Lq.pos;
+    L.l_codes = s_codes[wave];
+    L.l_pos = s_pos[wave];
+    L.n = Lq.n;
+    L.limit = Lq.limit;
+    const bool staged = Lq.codes == g_codes;
+    L.r0 = staged ? r0 : 0;
+    L.r1 = staged ? r1 : 0;
+
+    // Lower bound of the code: in the staged range when it brackets the key.
+    int32_t p = 0;
+    bool found = false;
+    if (valid && staged && (r0 == 0 || s_codes[wave][0] < key) && (r1 == L.n || s_codes[wave][r1 - r0 - 1] >= key)) {
+      int32_t lo = r0, hi = r1;
+      while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (s_codes[wave][mid - r0] < key)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      p = lo;
+      found = true;
+    }
+    // The rest search the list itself, one query at a time, wavefront-wide.
+    for (uint64_t m = wave_ballot(valid && !found); m != 0ull; m &= m - 1ull) {
+      const int u = __ffsll((unsigned long long)m) - 1;
+      const uint32_t* uc_p = readlane_ptr(L.codes, u);
+      const int32_t un = __builtin_amdgcn_readlane(L.n, u);
+      const uint32_t uk = uint32_t(__builtin_amdgcn_readlane(int32_t(key), u));
+      const int32_t up = wave_lower_bound(uc_p, 0, un, uk, lane);
+      if (lane == u) p = up;
+    }
+
+    // The window, entry by entry.
+    int2 res = make_int2(0, -1);
+    if (valid) {
+      const int half = topk / 2;
+      const int need_r = topk - half;
+      // Right side: first and last entry taken; left side: nearest and
+      // farthest entry taken.
+      int32_t r_first = 0, r_last = -1, l_near = -1, l_far = 0;
+      int32_t cur_r = p;
+      int got_r = lane_scan(L, cur_r, +1, need_r, 0, r_first, r_last);
+      const int need_l = half + (need_r - got_r);
+      int32_t cur_l = p - 1;
+      const int got_l = lane_scan(L, cur_l, -1, need_l, 0, l_near, l_far);
+      if (got_l < need_l && got_r == need_r) got_r = lane_scan(L, cur_r, +1, topk - got_l, got_r, r_first, r_last);
+      if (got_l + got_r > 0) res = make_int2(got_l > 0 ? l_far : r_first, got_r > 0 ? r_last : l_near);
+    }
+    if (slot < total) bounds[slot] = res;
+
+    if (idx_out != nullptr) {
+      // The windows' positions in list order, then -1: one query at a time.
+      for (uint64_t m = vmask; m != 0ull; m &= m - 1ull) {
+        const int u = __ffsll((unsigned long long)m) - 1;
+        const int32_t* upos = readlane_ptr(L.pos, u);
+        const int32_t ua = __builtin_amdgcn_readlane(res.x, u), ub = __builtin_amdgcn_readlane(res.y, u);
+        const int32_t ulim = __builtin_amdgcn_readlane(L.limit, u);
+        const int32_t ui = __builtin_amdgcn_readlane(my_i, u);
+        const int64_t useg = (run * 64 + u) / N;
+        int32_t* row = idx_out + (useg * N + ui) * int64_t(topk);
         int cnt = 0;
-        for (int32_t e0 = wb.a; e0 <= wb.b; e0 += 64) {
+        for (int32_t e0 = ua; e0 <= ub; e0 += 64) {
           const int32_t e = e0 + lane;
-          const int32_t pv = e <= wb.b ? L.pos[e] : INT32_MAX;
-          const bool ok = pv <= L.limit;
+          const int32_t pv = e <= ub ? upos[e] : INT32_MAX;
+          const bool ok = pv <= ulim;
           const uint64_t bal = wave_ballot(ok);
           if (ok) row[cnt + int(lanes_below(bal))] = pv;
           cnt += __popcll(bal);
@@ -165,7 +302,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
         for (int c = cnt + lane; c < topk; c += 64) row[c] = -1;
       }
     }
-    if (lane < kBndRun && slot0 + lane < total) bounds[slot0 + lane] = my_b;
+    wave_lds_sync();
   }
 }
 
@@ -239,7 +376,9 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         ln = int32_t(1) << g_lvl;
       }
 
-      const bool mine = ((gmask >> qn) & 1u) != 0u && my_a <= my_b;
+      // A window outside the list (not produced by the bounds kernel) counts
+      // as empty.
+      const bool mine = ((gmask >> qn) & 1u) != 0u && 0 <= my_a && my_a <= my_b && my_b < ln;
       const int32_t my_lim = causal ? my_i : int32_t(N - 1);
       float qv[KD];
       if (mine) {
@@ -456,7 +595,7 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   {
-    const int64_t runs = ceil_div(total, kBndRun);
+    const int64_t runs = ceil_div(total, 64);
     const int64_t want = ceil_div(runs, kBndWaves);
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
     hipLaunchKernelGGL(window_bounds_kernel, dim3(blocks), dim3(kBndWaves * 64), 0, stream, q_codes, sorted_codes,
