@@ -58,6 +58,7 @@ constexpr int kChunk = 16;     // list entries per product step
 constexpr int kTileWaves = 4;  // wavefronts per block
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 union Frag {  // four bfloat16 values
@@ -412,19 +413,22 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // split into bfloat16 parts, and the loads of the entries' value rows.
       // Branch-free, so that loads in flight can be counted across chunks: a
       // chunk index at or past nch scores nothing, and every lane loads a
-      // row (a row nobody takes reads row 0, finite by contract, with weight
-      // 0).  The reciprocal is the hardware one (1 ulp).  A score s is split
-      // as hi = s with the low 16 bits cleared and lo = the same truncation
-      // of s - hi (exact), so hi + lo carries 16 significant bits of s.
+      // row (a missing entry reads row 0, finite by contract; a row no query
+      // takes has weight 0).  The reciprocal is the hardware one (1 ulp).  A
+      // score s is split as hi = bf16(s) and lo = bf16(s - hi), both rounded
+      // to nearest even; s - hi is exact, so hi + lo is within 2^-17 of s.
       auto prep = [&](int ch, int nch_, uint32_t(&raw)[4][W], uint32_t(&bh)[2], uint32_t(&bl)[2]) {
         const bool live = ch < nch_;
         const int chc = live ? ch : 0;
         const int32_t r0 = s_ch[wave][chc] * kChunk;
+        float sc[4];
+        int32_t pvs[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
           const int rr = chc * kChunk + kg * 4 + kk;
           const int32_t r = r0 + kg * 4 + kk;
           const int32_t pv = s_pos[wave][rr];
+          pvs[kk] = pv;
           const bool in = live && uint32_t(r - a_eff) <= span && uint32_t(pv) <= lim_u;
           float d2 = 0.0f;
 #pragma unroll
@@ -434,20 +438,22 @@ __global__ void __launch_bounds__(kTileWaves * 64)
               d2 = fmaf(diff, diff, d2);
             }
           }
-          const float sc = in ? __builtin_amdgcn_rcpf(d2 + eps) : 0.0f;
-          zpart += sc;
-          const uint32_t hi = __float_as_uint(sc) & 0xFFFF0000u;
-          const uint32_t lo = __float_as_uint(sc - __uint_as_float(hi)) & 0xFFFF0000u;
-          if (kk & 1) {
-            bh[kk >> 1] |= hi;
-            bl[kk >> 1] |= lo;
-          } else {
-            bh[kk >> 1] = hi >> 16;
-            bl[kk >> 1] = lo >> 16;
-          }
-          const bool used = ((wave_ballot(in) >> (kg * 16)) & 0xFFFFull) != 0ull;
-          load_words<W>(vseg + (Off(used ? pv : 0) * Off(DV) + col), raw[kk]);
+          const float rc = __builtin_amdgcn_rcpf(d2 + eps);
+          sc[kk] = in ? rc : 0.0f;
+          zpart += sc[kk];
         }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const bf16x2_t h = {(__bf16)sc[2 * t], (__bf16)sc[2 * t + 1]};
+          const uint32_t hw = __builtin_bit_cast(uint32_t, h);
+          const bf16x2_t l = {(__bf16)(sc[2 * t] - __uint_as_float(hw << 16)),
+                              (__bf16)(sc[2 * t + 1] - __uint_as_float(hw & 0xFFFF0000u))};
+          bh[t] = hw;
+          bl[t] = __builtin_bit_cast(uint32_t, l);
+        }
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          load_words<W>(vseg + (Off(pvs[kk] < 0 ? 0 : pvs[kk]) * Off(DV) + col), raw[kk]);
       };
       // acc[j] += V^T (block j) * S^T for one chunk, high and low score parts.
       auto mma = [&](const uint32_t(&raw)[4][W], const uint32_t(&bh)[2], const uint32_t(&bl)[2]) {
@@ -476,9 +482,16 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         while (c != INT32_MAX && nch < kStage) {
           if (lane == 0) s_ch[wave][nch] = c;
           ++nch;
+          // The next chunk: c + 1 when a window meets it (the common case),
+          // else the first chunk of the next window that lies beyond c.
           const int nxt = c + 1;
-          const int cand = (mine && my_b >= nxt * kChunk) ? (my_a / kChunk > nxt ? my_a / kChunk : nxt) : INT32_MAX;
-          c = wave_min_int(cand);
+          const int32_t lo = nxt * kChunk;
+          if (wave_ballot(mine && my_a < lo + kChunk && my_b >= lo) != 0ull) {
+            c = nxt;
+          } else {
+            const int cand = (mine && my_b >= lo) ? (my_a / kChunk > nxt ? my_a / kChunk : nxt) : INT32_MAX;
+            c = wave_min_int(cand);
+          }
         }
         wave_lds_sync();
 
@@ -545,9 +558,16 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int j = 0; j < E; ++j) o[i * E + j] = acc[j][i] * inv;
-        uint16_t* dst = out + (g_seg * N + my_i) * int64_t(DV) + kg * 4 * E;
+        // Rounded to bfloat16 (nearest even), two values per conversion.
+        uint32_t w[2 * E];
 #pragma unroll
-        for (int t = 0; t < 4 * E; t += 8) Vec16<uint16_t>::store(dst + t, o + t);
+        for (int t = 0; t < 2 * E; ++t) {
+          const bf16x2_t pr = {(__bf16)o[2 * t], (__bf16)o[2 * t + 1]};
+          w[t] = __builtin_bit_cast(uint32_t, pr);
+        }
+        uint4* dst = reinterpret_cast<uint4*>(out + (g_seg * N + my_i) * int64_t(DV) + kg * 4 * E);
+#pragma unroll
+        for (int t = 0; t < 2 * E; t += 4) dst[t / 4] = make_uint4(w[t], w[t + 1], w[t + 2], w[t + 3]);
       }
     }
   }
