@@ -25,6 +25,11 @@
 //       - accumulates V^T (16 value columns x 16 entries) times S^T (16
 //         entries x 16 queries) with v_mfma_f32_16x16x16_bf16, once per 16
 //         value columns.
+// Only the weighted sum runs on the matrix cores: it is a dense contraction
+// with reuse, since each staged value row is loaded once and serves all 16
+// queries of the tile (about half of the 16 x chunk scores are nonzero).  The
+// scores, distances over d_k = 3 coordinates, stay on the vector ALUs.
+//
 // Scores are float32 (hardware reciprocal, 1 ulp); each is split into a
 // bfloat16 high part and a bfloat16 remainder, and both products are
 // accumulated, so the weights carry 16 significant bits and the products are
@@ -344,14 +349,9 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
 
-  // Staged entry record for the distance product, as bfloat16: the key's
-  // coordinates, then |k|^2 split into a high and a low part, then zeros
-  // (8 values for d_k = 3, else 16).
-  constexpr int kRecW = DK == 3 ? 4 : 8;  // 32-bit words per record
-  constexpr int kRecQ = kRecW / 2;        // 8-byte quarters (4 dimensions each)
   __shared__ int32_t s_ch[kTileWaves][kStage];
-  __shared__ __align__(16) int32_t s_pos[kTileWaves][kStageEntries];
-  __shared__ __align__(16) uint32_t s_rec[kTileWaves][kStageEntries][kRecW];
+  __shared__ int32_t s_pos[kTileWaves][kStageEntries];
+  __shared__ float s_k[kTileWaves][kStageEntries][KD];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -417,28 +417,6 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
         for (int a = 0; a < KD; ++a) qv[a] = 0.0f;
       }
-      // Query side of the distance product: (-2q, 1, 1, 0, ...) as bfloat16
-      // (exact), this lane holding dimensions 4kg..4kg+3; and |q|^2 + eps.
-      float qq = 0.0f;
-#pragma unroll
-      for (int a = 0; a < KD; ++a)
-        if (a < dk) qq = fmaf(qv[a], qv[a], qq);
-      const float qe = qq + eps;
-      Frag qb;
-      {
-        uint32_t hv[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int d = kg * 4 + t;
-          float val = (d == dk || d == dk + 1) ? 1.0f : 0.0f;
-#pragma unroll
-          for (int a = 0; a < KD; ++a)
-            if (a < dk && a == d) val = -2.0f * qv[a];
-          hv[t] = uint32_t(__builtin_bit_cast(uint16_t, (__bf16)val));
-        }
-        qb.w[0] = hv[0] | (hv[1] << 16);
-        qb.w[1] = hv[2] | (hv[3] << 16);
-      }
 
       f32x4_t acc[E];
 #pragma unroll
@@ -467,26 +445,24 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         const bool live = ch < nch_;
         const int chc = live ? ch : 0;
         const int32_t r0 = s_ch[wave][chc] * kChunk;
-        // |k|^2 - 2 q.k for the chunk's 16 entries and the tile's 16 queries
-        // in one product: this lane receives its 4 entries for its query.
-        Frag ka;
-        {
-          const int qd = kg < kRecQ ? kg : 0;
-          const uint2 kw = *reinterpret_cast<const uint2*>(&s_rec[wave][chc * kChunk + qn][2 * qd]);
-          ka.w[0] = kg < kRecQ ? kw.x : 0u;
-          ka.w[1] = kg < kRecQ ? kw.y : 0u;
-        }
-        const f32x4_t dq =
-            __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ka.v, qb.v, f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, 0, 0, 0);
-        const int4 pv4 = *reinterpret_cast<const int4*>(&s_pos[wave][chc * kChunk + kg * 4]);
-        const int32_t pvs[4] = {pv4.x, pv4.y, pv4.z, pv4.w};
         float sc[4];
+        int32_t pvs[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
+          const int rr = chc * kChunk + kg * 4 + kk;
           const int32_t r = r0 + kg * 4 + kk;
-          const bool in = live && uint32_t(r - a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
-          // d^2 + eps = (|q|^2 + eps) + (|k|^2 - 2 q.k), at least eps.
-          const float rc = __builtin_amdgcn_rcpf(fmaxf(qe + dq[kk], eps));
+          const int32_t pv = s_pos[wave][rr];
+          pvs[kk] = pv;
+          const bool in = live && uint32_t(r - a_eff) <= span && uint32_t(pv) <= lim_u;
+          float d2 = 0.0f;
+#pragma unroll
+          for (int a = 0; a < KD; ++a) {
+            if (a < dk) {
+              const float diff = qv[a] - s_k[wave][rr][a];
+              d2 = fmaf(diff, diff, d2);
+            }
+          }
+          const float rc = __builtin_amdgcn_rcpf(d2 + eps);
           sc[kk] = in ? rc : 0.0f;
           zpart += sc[kk];
         }
@@ -559,64 +535,22 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           for (int t = 0; t < kStageEntries / 64; ++t) {
             const int e = t * 64 + lane;
             if (e < nch * kChunk) {
-              uint32_t kb[KD];  // key coordinates, bfloat16 bits
-#pragma unroll
-              for (int a = 0; a < KD; ++a) kb[a] = 0u;
+              float kv[KD];
               if (pv[t] >= 0) {
                 if constexpr (DK == 3) {
-                  // The 6-byte row inside the 8 bytes from the 4-byte boundary
-                  // at or below it (element-wise for the array's last row).
-                  const int64_t e3 = (g_seg * N + pv[t]) * 3;
-                  const int64_t al = e3 & ~int64_t(1);
-                  if (al + 4 <= total * 3) {
-                    const Words2 w = *reinterpret_cast<const Words2*>(k + al);
-                    if (e3 == al) {
-                      kb[0] = w.a & 0xFFFFu;
-                      kb[1] = w.a >> 16;
-                      kb[2] = w.b & 0xFFFFu;
-                    } else {
-                      kb[0] = w.a >> 16;
-                      kb[1] = w.b & 0xFFFFu;
-                      kb[2] = w.b >> 16;
-                    }
-                  } else {
-                    kb[0] = k[e3];
-                    kb[1] = k[e3 + 1];
-                    kb[2] = k[e3 + 2];
-                  }
+                  Row3<uint16_t>::load(k, g_seg * N + pv[t], total, kv);
                 } else {
 #pragma unroll
                   for (int a = 0; a < KD; ++a)
-                    if (a < dk) kb[a] = kseg[int64_t(pv[t]) * dk + a];
+                    kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv[t]) * dk + a]) : 0.0f;
                 }
-              }
-              float kk2 = 0.0f;
+              } else {
 #pragma unroll
-              for (int a = 0; a < KD; ++a) {
-                const float f = __uint_as_float(kb[a] << 16);
-                if (a < dk) kk2 = fmaf(f, f, kk2);
-              }
-              const uint32_t khi = uint32_t(__builtin_bit_cast(uint16_t, (__bf16)kk2));
-              const uint32_t klo = uint32_t(__builtin_bit_cast(uint16_t, (__bf16)(kk2 - __uint_as_float(khi << 16))));
-              uint32_t rec[kRecW];
-#pragma unroll
-              for (int w = 0; w < kRecW; ++w) {
-                uint32_t half[2];
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                  const int d = 2 * w + h;
-                  uint32_t x = (d == dk) ? khi : (d == dk + 1) ? klo : 0u;
-#pragma unroll
-                  for (int a = 0; a < KD; ++a)
-                    if (a < dk && a == d) x = kb[a];
-                  half[h] = x;
-                }
-                rec[w] = half[0] | (half[1] << 16);
+                for (int a = 0; a < KD; ++a) kv[a] = 0.0f;
               }
               s_pos[wave][e] = pv[t];
 #pragma unroll
-              for (int w = 0; w < kRecW; w += 4)
-                *reinterpret_cast<uint4*>(&s_rec[wave][e][w]) = make_uint4(rec[w], rec[w + 1], rec[w + 2], rec[w + 3]);
+              for (int a = 0; a < KD; ++a) s_k[wave][e][a] = kv[a];
             }
           }
         }
