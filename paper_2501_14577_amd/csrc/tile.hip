@@ -88,7 +88,11 @@ __device__ __forceinline__ T* readlane_ptr(T* p, int src) {
   const uint64_t v = reinterpret_cast<uint64_t>(p);
   const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int32_t(uint32_t(v)), src));
   const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int32_t(uint32_t(v >> 32)), src));
-  return reinterpret_cast<T*>((uint64_t(hi) << 32) | uint64_t(lo));
+  // Rebuilt as a global-memory pointer, so that loads through it are global
+  // loads rather than flat ones.
+  using G = __attribute__((address_space(1))) T;
+  G* g = (G*)((uint64_t(hi) << 32) | uint64_t(lo));
+  return (T*)g;
 }
 
 // E consecutive bfloat16 elements (E / 2 words) from a 2E-byte aligned address.
@@ -131,16 +135,22 @@ constexpr int kBndWaves = 4;
 constexpr int kRegion = 1024;  // list entries staged per wavefront
 constexpr int kMargin = 384;   // of them before the run's first insertion point
 
+// Each wavefront's copy of a list range, in LDS.  Declared at file scope and
+// indexed directly, so that every access compiles to an LDS instruction (a
+// pointer kept in a struct would lose the address space and go through the
+// slower flat path).
+__shared__ uint32_t s_bnd_codes[kBndWaves][kRegion];
+__shared__ int32_t s_bnd_pos[kBndWaves][kRegion];
+
 struct LaneList {
   const uint32_t* codes;
   const int32_t* pos;
-  const uint32_t* l_codes;  // LDS copy of [r0, r1), valid when staged
-  const int32_t* l_pos;
-  int32_t n, limit, r0, r1;
-  __device__ __forceinline__ uint32_t code(int32_t e) const {
-    return (e >= r0 && e < r1) ? l_codes[e - r0] : codes[e];
+  int wave;
+  int32_t n, limit, r0, r1;  // [r0, r1): the range copied to LDS (empty when not staged)
+  __device__ __forceinline__ int32_t staged_position(int32_t e) const { return s_bnd_pos[wave][e - r0]; }
+  __device__ __forceinline__ int32_t position(int32_t e) const {
+    return (e >= r0 && e < r1) ? s_bnd_pos[wave][e - r0] : pos[e];
   }
-  __device__ __forceinline__ int32_t position(int32_t e) const { return (e >= r0 && e < r1) ? l_pos[e - r0] : pos[e]; }
 };
 
 // Scan from entry e in direction dir (+1 or -1) for up to `need` in-pool
@@ -162,7 +172,7 @@ __device__ __forceinline__ int lane_scan(const LaneList& L, int32_t& e, int dir,
       const int32_t x = lo + j;  // ascending list order
       int32_t v;
       if (local)
-        v = L.l_pos[x - L.r0];
+        v = L.staged_position(x);
       else
         v = (x >= 0 && x < L.n) ? L.position(x) : INT32_MAX;
       mask |= (v <= L.limit ? 1u : 0u) << j;
@@ -198,8 +208,6 @@ __global__ void __launch_bounds__(kBndWaves * 64)
                          const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
                          int64_t N, int topk, int causal, int t0, int t_hi, int64_t cap, int2* __restrict__ bounds,
                          int32_t* __restrict__ idx_out) {
-  __shared__ uint32_t s_codes[kBndWaves][kRegion];
-  __shared__ int32_t s_pos[kBndWaves][kRegion];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t runs = (total + 63) / 64;
@@ -245,8 +253,8 @@ __global__ void __launch_bounds__(kBndWaves * 64)
       }
 #pragma unroll
       for (int t = 0; t < kRegion / 64; ++t) {
-        s_codes[wave][t * 64 + lane] = cv[t];
-        s_pos[wave][t * 64 + lane] = pv[t];
+        s_bnd_codes[wave][t * 64 + lane] = cv[t];
+        s_bnd_pos[wave][t * 64 + lane] = pv[t];
       }
     }
     wave_lds_sync();
@@ -254,8 +262,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
     LaneList L;
     L.codes = Lq.codes;
     L.pos = Lq.pos;
-    L.l_codes = s_codes[wave];
-    L.l_pos = s_pos[wave];
+    L.wave = wave;
     L.n = Lq.n;
     L.limit = Lq.limit;
     const bool staged = Lq.codes == g_codes;
@@ -265,11 +272,11 @@ __global__ void __launch_bounds__(kBndWaves * 64)
     // Lower bound of the code: in the staged range when it brackets the key.
     int32_t p = 0;
     bool found = false;
-    if (valid && staged && (r0 == 0 || s_codes[wave][0] < key) && (r1 == L.n || s_codes[wave][r1 - r0 - 1] >= key)) {
+    if (valid && staged && (r0 == 0 || s_bnd_codes[wave][0] < key) && (r1 == L.n || s_bnd_codes[wave][r1 - r0 - 1] >= key)) {
       int32_t lo = r0, hi = r1;
       while (lo < hi) {
         const int32_t mid = (lo + hi) >> 1;
-        if (s_codes[wave][mid - r0] < key)
+        if (s_bnd_codes[wave][mid - r0] < key)
           lo = mid + 1;
         else
           hi = mid;
@@ -350,8 +357,11 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   const int dk = DK > 0 ? DK : dk_rt;
 
   __shared__ int32_t s_ch[kTileWaves][kStage];
-  __shared__ int32_t s_pos[kTileWaves][kStageEntries];
-  __shared__ float s_k[kTileWaves][kStageEntries][KD];
+  // Key rows padded to a multiple of 4 floats, so 4 consecutive entries'
+  // positions and each key row are whole 16-byte LDS reads.
+  constexpr int KD4 = (KD + 3) / 4 * 4;
+  __shared__ __align__(16) int32_t s_pos[kTileWaves][kStageEntries];
+  __shared__ __align__(16) float s_k[kTileWaves][kStageEntries][KD4];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -447,18 +457,24 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         const int32_t r0 = s_ch[wave][chc] * kChunk;
         float sc[4];
         int32_t pvs[4];
+        {
+          const int4 p4 = *reinterpret_cast<const int4*>(&s_pos[wave][chc * kChunk + kg * 4]);
+          pvs[0] = p4.x;
+          pvs[1] = p4.y;
+          pvs[2] = p4.z;
+          pvs[3] = p4.w;
+        }
+        const float* krow = &s_k[wave][chc * kChunk + kg * 4][0];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const int rr = chc * kChunk + kg * 4 + kk;
           const int32_t r = r0 + kg * 4 + kk;
-          const int32_t pv = s_pos[wave][rr];
-          pvs[kk] = pv;
+          const int32_t pv = pvs[kk];
           const bool in = live && uint32_t(r - a_eff) <= span && uint32_t(pv) <= lim_u;
           float d2 = 0.0f;
 #pragma unroll
           for (int a = 0; a < KD; ++a) {
             if (a < dk) {
-              const float diff = qv[a] - s_k[wave][rr][a];
+              const float diff = qv[a] - krow[kk * KD4 + a];
               d2 = fmaf(diff, diff, d2);
             }
           }
@@ -550,7 +566,10 @@ __global__ void __launch_bounds__(kTileWaves * 64)
               }
               s_pos[wave][e] = pv[t];
 #pragma unroll
-              for (int a = 0; a < KD; ++a) s_k[wave][e][a] = kv[a];
+              for (int a = 0; a < KD4; a += 4)
+                *reinterpret_cast<float4*>(&s_k[wave][e][a]) =
+                    make_float4(kv[a], a + 1 < KD ? kv[a + 1] : 0.0f, a + 2 < KD ? kv[a + 2] : 0.0f,
+                                a + 3 < KD ? kv[a + 3] : 0.0f);
             }
           }
         }
