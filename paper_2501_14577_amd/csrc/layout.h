@@ -24,7 +24,7 @@ constexpr int64_t kEncRowsPerBlock = 256;
 constexpr int kSortThreads = 256;
 constexpr int kSortChunks = 4;
 constexpr int64_t kSortTile = int64_t(kSortThreads) * kSortChunks;
-constexpr int kRadixMax = 256;  // digits of at most 8 bits
+constexpr int kRadixMax = 512;  // digits of at most 9 bits
 
 // ---- select ---------------------------------------------------------------
 constexpr int kSelWavesPerBlock = 4;
@@ -53,7 +53,7 @@ struct SortPlan {
 
 inline SortPlan sort_plan(int64_t N, int code_bits) {
   SortPlan p;
-  p.passes = (code_bits + 7) / 8;
+  p.passes = (code_bits + 8) / 9;
   p.digit_bits = (code_bits + p.passes - 1) / p.passes;
   p.tiles = ceil_div(N, kSortTile);
   return p;

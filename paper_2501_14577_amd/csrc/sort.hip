@@ -2,7 +2,7 @@
 // Algorithm 1, Step 2; Appendix B sorts the codes with a radix sort).
 //
 // Every segment is cut into tiles of 1024 keys.  One pass over a digit of at
-// most 8 bits runs three kernels:
+// most 9 bits runs three kernels:
 //   hist:    per tile, the count of each digit value (LDS atomics);
 //   scan:    per segment and digit value, the counts of earlier tiles
 //            (written over the tile counts) and the segment total;
@@ -13,7 +13,8 @@
 //            lanes with one ballot per digit bit and counting them with
 //            mbcnt; per-wave running counts live in LDS.
 // A pass preserves the order of equal digits, so after the last pass equal
-// codes are in ascending position order.
+// codes are in ascending position order.  ceil(code_bits / 9) passes split
+// the bits evenly (18-bit codes: two passes of 9).
 #include "device_common.h"
 #include "kernels.h"
 #include "layout.h"
@@ -40,7 +41,7 @@ __global__ void __launch_bounds__(kSortThreads)
   const int64_t tile = blockIdx.x % tiles;
   const int tid = threadIdx.x;
   __shared__ uint32_t h[kRadixMax];
-  h[tid] = 0;
+  for (int d = tid; d < kRadixMax; d += kSortThreads) h[d] = 0;
   __syncthreads();
   const uint32_t mask = (1u << nbits) - 1u;
   const int64_t e0 = tile * kSortTile;
@@ -51,7 +52,7 @@ __global__ void __launch_bounds__(kSortThreads)
     atomicAdd(&h[radix_digit<kByLevel>(key, val, shift, mask, t0, t_hi, N)], 1u);
   }
   __syncthreads();
-  hist[(seg * tiles + tile) * kRadixMax + tid] = h[tid];
+  for (int d = tid; d < kRadixMax; d += kSortThreads) hist[(seg * tiles + tile) * kRadixMax + d] = h[d];
 }
 
 // Tiles of one segment are split into kScanGroups contiguous groups; wave g
@@ -119,13 +120,25 @@ __global__ void __launch_bounds__(kSortThreads)
   __shared__ uint32_t s_wcnt[kSortThreads / 64][kRadixMax];  // per-wave running / prefix counts
   __shared__ uint32_t s_scan[4];
 
+  constexpr int kPer = kRadixMax / kSortThreads;  // digit values per thread: tid*kPer ..
   {
     // Digit totals of the segment and counts of the tiles before this one.
-    const uint32_t before = hist[(seg * tiles + tile) * kRadixMax + tid];
-    const uint32_t excl = block256_exclusive_scan(totals[seg * kRadixMax + tid], s_scan);
-    s_base[tid] = excl + before;
+    uint32_t tot[kPer], bef[kPer], sum = 0;
 #pragma unroll
-    for (int w = 0; w < kSortThreads / 64; ++w) s_wcnt[w][tid] = 0;
+    for (int i = 0; i < kPer; ++i) {
+      const int d = tid * kPer + i;
+      tot[i] = totals[seg * kRadixMax + d];
+      bef[i] = hist[(seg * tiles + tile) * kRadixMax + d];
+      sum += tot[i];
+    }
+    uint32_t excl = block256_exclusive_scan(sum, s_scan);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      s_base[tid * kPer + i] = excl + bef[i];
+      excl += tot[i];
+#pragma unroll
+      for (int w = 0; w < kSortThreads / 64; ++w) s_wcnt[w][tid * kPer + i] = 0;
+    }
   }
   __syncthreads();
 
@@ -159,12 +172,13 @@ __global__ void __launch_bounds__(kSortThreads)
     rank[c] = base + below;
   }
   __syncthreads();
-  {
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
     uint32_t run = 0;
 #pragma unroll
     for (int w = 0; w < kSortThreads / 64; ++w) {
-      const uint32_t t = s_wcnt[w][tid];
-      s_wcnt[w][tid] = run;
+      const uint32_t t = s_wcnt[w][tid * kPer + i];
+      s_wcnt[w][tid * kPer + i] = run;
       run += t;
     }
   }
