@@ -44,13 +44,15 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
 
 // bfloat16 one-pass select and attend on the matrix cores, 16 queries per
 // wavefront (the prefix lists already built when causal): window bounds per
-// processing-order slot into `bounds` (S*N entries), then the tiles.
+// processing-order slot into `bounds` (S*N entries); for d_k = 3 the lists'
+// key rows in list order into keys_full (S*N) and keys_list (S*cap); then the
+// tiles.
 bool tile_supports(int dv);
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
                                      int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
                                      const int32_t* q_order, float eps, void* out, int32_t* idx_out, int2* bounds,
-                                     hipStream_t stream);
+                                     uint2* keys_full, uint2* keys_list, hipStream_t stream);
 
 // Select and attend in one pass (idx_out optional).
 hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,

@@ -135,13 +135,19 @@ inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
 
 // One-pass select and attend on the matrix cores: the prefix lists (as for
 // select), then each processing-order slot's window bounds (two int32).
+// For d_k = 3 it also keeps the key rows of the full sorted lists and of the
+// prefix lists in list order (8 bytes per entry).
 struct FusedWs {
-  size_t bounds_off, bytes;
+  size_t bounds_off, keys_full_off, keys_list_off, bytes;
 };
 inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
   FusedWs w;
   w.bounds_off = align_up(select_ws(S, N, topk, causal).bytes);
-  w.bytes = w.bounds_off + align_up(size_t(S) * size_t(N) * 2 * sizeof(int32_t));
+  w.keys_full_off = w.bounds_off + align_up(size_t(S) * size_t(N) * 2 * sizeof(int32_t));
+  w.keys_list_off = w.keys_full_off + align_up(size_t(S) * size_t(N) * 8);
+  const ListPlan lp = list_plan(N, topk);
+  const size_t lists = (causal && lp.levels > 0) ? size_t(S) * size_t(lp.cap) : 0;
+  w.bytes = w.keys_list_off + align_up(lists * 8);
   return w;
 }
 

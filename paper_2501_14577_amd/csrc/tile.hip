@@ -338,6 +338,55 @@ __global__ void __launch_bounds__(kBndWaves * 64)
   }
 }
 
+// ---- key rows in list order (d_k = 3) ----------------------------------------
+// Entry e of a sorted list gets the key row of its position, as three bfloat16
+// values in 8 bytes (x | y << 16, z), so that the tile kernel reads the key
+// rows of a list range with coalesced loads instead of gathering them by
+// position.  One thread per entry, over the full sorted lists (S*N entries)
+// and then the prefix lists (S*cap entries; cap is 0 when there are none, and
+// list_pos is then not read).
+__global__ void __launch_bounds__(256)
+    list_keys_kernel(const uint16_t* __restrict__ k, int64_t total, int64_t N, const int32_t* __restrict__ perm,
+                     const int32_t* __restrict__ list_pos, int64_t cap, int64_t S, uint2* __restrict__ keys_full,
+                     uint2* __restrict__ keys_list) {
+  const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t n_full = S * N;
+  int64_t seg, pv;
+  uint2* dst;
+  if (t < n_full) {
+    seg = t / N;
+    pv = perm[t];
+    dst = keys_full + t;
+  } else if (list_pos != nullptr && t < n_full + S * cap) {
+    const int64_t u = t - n_full;
+    seg = u / cap;
+    pv = list_pos[u];
+    dst = keys_list + u;
+  } else {
+    return;
+  }
+  const int64_t e3 = (seg * N + pv) * 3;
+  const int64_t al = e3 & ~int64_t(1);
+  uint32_t x, y, z;
+  if (al + 4 <= total * 3) {
+    const Words2 w = *reinterpret_cast<const Words2*>(k + al);
+    if (e3 == al) {
+      x = w.a & 0xFFFFu;
+      y = w.a >> 16;
+      z = w.b & 0xFFFFu;
+    } else {
+      x = w.a >> 16;
+      y = w.b & 0xFFFFu;
+      z = w.b >> 16;
+    }
+  } else {
+    x = k[e3];
+    y = k[e3 + 1];
+    z = k[e3 + 2];
+  }
+  *dst = make_uint2(x | (y << 16), z);
+}
+
 // ---- attention over the windows ----------------------------------------------
 
 template <int DV, int DK, bool kOff32>
@@ -345,7 +394,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
     select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                               const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
                               const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
-                              const int2* __restrict__ bounds, int64_t total, int64_t N, int dk_rt, int causal,
+                              const int2* __restrict__ bounds, const uint2* __restrict__ keys_full,
+                              const uint2* __restrict__ keys_list, int64_t total, int64_t N, int dk_rt, int causal,
                               int t0, int t_hi, int64_t cap, float eps, uint16_t* __restrict__ out) {
   constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
   constexpr int W = E / 2;    // 32-bit words per lane and row
@@ -405,9 +455,12 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           uint32_t(wave_ballot(my_i >= 0 && my_seg == g_seg && my_lvl == g_lvl)) & pending;
       pending &= ~gmask;
       const int32_t* lpos = sorted_pos + g_seg * N;
+      const uint2* lkey = keys_full + g_seg * N;  // key rows in list order (d_k = 3)
       int32_t ln = int32_t(N);
       if (causal && g_lvl <= t_hi) {
-        lpos = list_pos + g_seg * cap + ((int64_t(1) << g_lvl) - (int64_t(1) << t0));
+        const int64_t off = g_seg * cap + ((int64_t(1) << g_lvl) - (int64_t(1) << t0));
+        lpos = list_pos + off;
+        lkey = keys_list + off;
         ln = int32_t(1) << g_lvl;
       }
 
@@ -538,13 +591,18 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         // Stage the positions, then the key rows, of all nch chunks.
         {
           int32_t pv[kStageEntries / 64];
+          uint2 kw[kStageEntries / 64];  // d_k = 3: key rows read in list order with the positions
 #pragma unroll
           for (int t = 0; t < kStageEntries / 64; ++t) {
             const int e = t * 64 + lane;
             pv[t] = -1;
+            kw[t] = make_uint2(0u, 0u);
             if (e < nch * kChunk) {
               const int32_t r = s_ch[wave][e / kChunk] * kChunk + (e % kChunk);
-              if (r < ln) pv[t] = lpos[r];
+              if (r < ln) {
+                pv[t] = lpos[r];
+                if constexpr (DK == 3) kw[t] = lkey[r];
+              }
             }
           }
 #pragma unroll
@@ -554,7 +612,9 @@ __global__ void __launch_bounds__(kTileWaves * 64)
               float kv[KD];
               if (pv[t] >= 0) {
                 if constexpr (DK == 3) {
-                  Row3<uint16_t>::load(k, g_seg * N + pv[t], total, kv);
+                  kv[0] = __uint_as_float(kw[t].x << 16);
+                  kv[1] = __uint_as_float(kw[t].x & 0xFFFF0000u);
+                  kv[2] = __uint_as_float(kw[t].y << 16);
                 } else {
 #pragma unroll
                   for (int a = 0; a < KD; ++a)
@@ -619,7 +679,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 template <int DV, int DK>
 hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
                          int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
-                         const int32_t* q_order, const int2* bounds, float eps, uint16_t* out, hipStream_t stream) {
+                         const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
+                         float eps, uint16_t* out, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   const int64_t tiles = ceil_div(total, kTileQ);
@@ -628,22 +689,25 @@ hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v
   const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
   if (off32)
     hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, true>), dim3(blocks), dim3(kTileWaves * 64), 0, stream, q,
-                       k, v, perm, list_pos, q_order, bounds, total, N, dk, causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap,
-                       eps, out);
+                       k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk, causal ? 1 : 0, lp.t0,
+                       lp.t_hi, lp.cap, eps, out);
   else
     hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, false>), dim3(blocks), dim3(kTileWaves * 64), 0, stream,
-                       q, k, v, perm, list_pos, q_order, bounds, total, N, dk, causal ? 1 : 0, lp.t0, lp.t_hi,
-                       lp.cap, eps, out);
+                       q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk, causal ? 1 : 0,
+                       lp.t0, lp.t_hi, lp.cap, eps, out);
   return hipGetLastError();
 }
 
 template <int DV>
 hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
                           int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
-                          const int32_t* q_order, const int2* bounds, float eps, uint16_t* out, hipStream_t stream) {
+                          const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
+                          float eps, uint16_t* out, hipStream_t stream) {
   if (dk == 3)
-    return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, eps, out, stream);
-  return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, eps, out, stream);
+    return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, keys_list,
+                                eps, out, stream);
+  return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, keys_list,
+                              eps, out, stream);
 }
 
 }  // namespace
@@ -654,9 +718,17 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
                                      int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
                                      const int32_t* q_order, float eps, void* out, int32_t* idx_out, int2* bounds,
-                                     hipStream_t stream) {
+                                     uint2* keys_full, uint2* keys_list, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
+  if (dk == 3) {
+    // Prefix lists exist only for causal calls with levels.
+    const bool have_lists = causal && lp.levels > 0 && list_pos != nullptr;
+    const int64_t cap = have_lists ? lp.cap : 0;
+    const unsigned blocks = unsigned(ceil_div(total + S * cap, 256));
+    hipLaunchKernelGGL(list_keys_kernel, dim3(blocks), dim3(256), 0, stream, static_cast<const uint16_t*>(k), total, N,
+                       perm, have_lists ? list_pos : nullptr, cap, S, keys_full, keys_list);
+  }
   {
     const int64_t runs = ceil_div(total, 64);
     const int64_t want = ceil_div(runs, kBndWaves);
@@ -671,7 +743,8 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
   uint16_t* oo = static_cast<uint16_t*>(out);
 #define ZETA_TILE_CASE(DVV) \
   case DVV:                 \
-    return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, eps, oo, stream);
+    return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, \
+                               keys_list, eps, oo, stream);
   switch (dv) {
     ZETA_TILE_CASE(32)
     ZETA_TILE_CASE(64)
