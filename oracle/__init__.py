@@ -7,6 +7,7 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
 from .zeta_oracle import (  # noqa: F401
     as_f32,
     attend,
+    attend_bwd,
     bf16_bits_to_f32,
     forward,
     interleave,

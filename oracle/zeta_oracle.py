@@ -23,6 +23,9 @@ defines, one function per step, each citing the passage it follows:
 5. ``attend``: Adaptive Cauchy-softmax over the selected keys and the weighted
    sum of their values (Section 3.3, equation cauchy; Section 3.4;
    Appendix E.1, steps 1-4).
+6. ``attend_bwd``: the gradients of that attention with respect to q, k, v
+   and eps for fixed windows (Appendix E.2, summary of gradient
+   computations).
 
 Readings where the paper is silent or ambiguous (each is also listed in the
 design notes):
@@ -255,6 +258,59 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: fl
             num = np.einsum("bk,bkd->bd", score, v[seg][jj])
             out[seg, r0:r0 + len(rr)] = num / z[:, None]
     return out
+
+
+def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: float, dout: np.ndarray,
+               block: int = 512):
+    """Gradients of L = sum_i dout_i . o_i through the attention of ``attend``
+    (Appendix E.2, summary of gradient computations), for fixed windows idx.
+
+    With delta_ij = D_ij + eps, S_ij = 1 / delta_ij, Z_i = sum_j S_ij,
+    A_ij = S_ij / Z_i and o_i = sum_j A_ij v_j:
+      dL/dv_j   =  sum over queries i whose window holds j of A_ij dout_i
+      dL/dq_i   = -2 sum_j [dout_i . (v_j - o_i)] / Z_i (q_i - k_j) / delta_ij^2
+      dL/dk_j   =  2 sum over i of [dout_i . (v_j - o_i)] / Z_i (q_i - k_j) / delta_ij^2
+      dL/deps   = -sum_i sum_j [dout_i . (v_j - o_i)] / Z_i / delta_ij^2
+    o_i is recomputed here (it equals the forward output exactly in float64).
+    The selection itself has no gradient.
+
+    q, k: [S, N, dk]; v, dout: [S, N, dv]; idx: int32 [S, N, k] with -1 for
+    empty slots.  Computed in float64.  Returns (dq [S, N, dk], dk [S, N, dk],
+    dv [S, N, dv], deps float).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    dout = np.asarray(dout, dtype=np.float64)
+    S, N = q.shape[0], q.shape[1]
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    deps = 0.0
+    for seg in range(S):
+        for r0 in range(0, N, block):
+            rr = np.arange(r0, min(N, r0 + block))
+            ii = idx[seg, rr]
+            valid = ii >= 0
+            jj = np.where(valid, ii, 0)
+            diff = q[seg, rr][:, None, :] - k[seg][jj]  # q_i - k_j, [b, k, dk]
+            delta = np.sum(diff * diff, axis=-1) + eps  # delta_ij
+            score = np.where(valid, 1.0 / delta, 0.0)  # S_ij
+            z = score.sum(axis=1)  # Z_i
+            has = z > 0
+            zs = np.where(has, z, 1.0)
+            a = score / zs[:, None]  # A_ij
+            vj = v[seg][jj]  # [b, k, dv]
+            o = np.einsum("bk,bkd->bd", a, vj)  # o_i
+            du = dout[seg, rr]  # [b, dv]
+            g = np.einsum("bd,bkd->bk", du, vj) - np.einsum("bd,bd->b", du, o)[:, None]  # dout_i . (v_j - o_i)
+            w = np.where(valid, g / zs[:, None] / (delta * delta), 0.0)
+            dq[seg, rr] = -2.0 * np.einsum("bk,bkd->bd", w, diff)
+            sel = valid.ravel()
+            np.add.at(dk[seg], jj.ravel()[sel], (2.0 * w[:, :, None] * diff).reshape(-1, diff.shape[-1])[sel])
+            np.add.at(dv[seg], jj.ravel()[sel], (a[:, :, None] * du[:, None, :]).reshape(-1, du.shape[-1])[sel])
+            deps -= float(w.sum())
+    return dq, dk, dv, deps
 
 
 # ----------------------------------------------------------------------------

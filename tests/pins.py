@@ -287,6 +287,92 @@ def check_attend_special_cases(orc):
         assert np.allclose(out_same[i], v[0][sel].astype(np.float64).mean(axis=0), atol=1e-12)
 
 
+def _frac(t):
+    a, b = t.split("/")
+    return float(a) / float(b)
+
+
+def check_attend_bwd_golden(orc):
+    """The hand-worked two-candidate example in golden/attend_bwd_example.txt."""
+    rows = {}
+    for line in open(os.path.join(GOLDEN, "attend_bwd_example.txt")):
+        if line.strip() and not line.startswith("#"):
+            key, *vals = line.split()
+            rows[key] = vals
+    q = np.array([[[float(x) for x in rows["q"]]]])
+    k = np.array([[[float(x) for x in rows["k0"]], [float(x) for x in rows["k1"]]]])
+    v = np.array([[[float(x)] for x in rows["v"]]])
+    qq = np.concatenate([q, np.zeros((1, 1, 3))], axis=1)  # a second query row, unused (empty window)
+    idx = np.array([[[0, 1], [-1, -1]]], dtype=np.int32)
+    dout = np.array([[[float(rows["dout"][0])], [0.0]]])
+    dq, dk, dv, deps = orc.attend_bwd(qq, k, v, idx, float(rows["eps"][0]), dout)
+    assert np.allclose(dq[0, 0], [_frac(x) for x in rows["dq"]], atol=1e-12), dq[0, 0]
+    assert np.allclose(dk[0, 0], [_frac(x) for x in rows["dk0"]], atol=1e-12), dk[0, 0]
+    assert np.allclose(dk[0, 1], [_frac(x) for x in rows["dk1"]], atol=1e-12), dk[0, 1]
+    assert np.allclose(dv[0, :, 0], [_frac(x) for x in rows["dv"]], atol=1e-12), dv[0]
+    assert abs(deps - _frac(rows["deps"][0])) < 1e-12, deps
+    assert np.all(dq[0, 1] == 0.0)
+
+
+def _bwd_problem(seed, S=2, N=9, dk=3, dv=4, topk=4, causal=True):
+    rng = np.random.default_rng(seed)
+    q = rng.normal(size=(S, N, dk))
+    k = rng.normal(size=(S, N, dk))
+    v = rng.normal(size=(S, N, dv))
+    dout = rng.normal(size=(S, N, dv))
+    kc = rng.integers(0, 64, size=(S, N)).astype(np.uint32)
+    qc = rng.integers(0, 64, size=(S, N)).astype(np.uint32)
+    # Windows from a brute-force selection over the codes (any valid index sets would do).
+    idx = np.full((S, N, topk), -1, dtype=np.int32)
+    for s in range(S):
+        for i in range(N):
+            pool = sorted((int(kc[s, j]), j) for j in range(i + 1 if causal else N))
+            p = sum(1 for c, _ in pool if c < int(qc[s, i]))
+            m = min(topk, len(pool))
+            st = min(max(p - topk // 2, 0), len(pool) - m)
+            idx[s, i, :m] = [j for _, j in pool[st:st + m]]
+    return q, k, v, dout, idx
+
+
+def check_attend_bwd_finite_diff(orc):
+    """Every gradient equals the central difference of L = sum dout . o, with
+    o from orc.attend (Appendix E.1), in float64."""
+    eps = 0.7
+    q, k, v, dout, idx = _bwd_problem(71)
+    dq, dk, dv, deps = orc.attend_bwd(q, k, v, idx, eps, dout)
+
+    def loss(qx, kx, vx, e):
+        return float(np.sum(dout * orc.attend(qx, kx, vx, idx, e)))
+
+    h = 1e-6
+    for name, arr, grad in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        for flat in range(arr.size):
+            pos = np.unravel_index(flat, arr.shape)
+            a1, a2 = arr.copy(), arr.copy()
+            a1[pos] += h
+            a2[pos] -= h
+            args1 = {"q": q, "k": k, "v": v}
+            args2 = dict(args1)
+            args1[name], args2[name] = a1, a2
+            fd = (loss(args1["q"], args1["k"], args1["v"], eps) - loss(args2["q"], args2["k"], args2["v"], eps)) / (2 * h)
+            assert abs(fd - grad[pos]) <= 1e-6 * (1.0 + abs(fd)), (name, pos, fd, grad[pos])
+    fd = (loss(q, k, v, eps + h) - loss(q, k, v, eps - h)) / (2 * h)
+    assert abs(fd - deps) <= 1e-6 * (1.0 + abs(fd)), (fd, deps)
+
+
+def check_attend_bwd_invariants(orc):
+    """Shifting every q and k by one vector leaves each D unchanged, so
+    sum dq + sum dk = 0; the weights of a row sum to 1, so sum dv = sum of
+    dout over rows with candidates; a one-candidate row has o = v_j, so its q
+    gradient is 0."""
+    q, k, v, dout, idx = _bwd_problem(72, S=1, N=12, topk=5, causal=False)
+    idx[0, 3, 1:] = -1  # a one-candidate row
+    dq, dk, dv, deps = orc.attend_bwd(q, k, v, idx, 0.4, dout)
+    assert np.allclose(dq.sum(axis=(0, 1)) + dk.sum(axis=(0, 1)), 0.0, atol=1e-10)
+    assert np.allclose(dv.sum(axis=(0, 1)), dout.sum(axis=(0, 1)), atol=1e-10)
+    assert np.allclose(dq[0, 3], 0.0, atol=1e-14)
+
+
 ALL_PINS = [
     check_morton_golden,
     check_morton_bijection,
@@ -302,4 +388,7 @@ ALL_PINS = [
     check_attend_hand,
     check_attend_dense_limit,
     check_attend_special_cases,
+    check_attend_bwd_golden,
+    check_attend_bwd_finite_diff,
+    check_attend_bwd_invariants,
 ]

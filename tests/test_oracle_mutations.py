@@ -38,7 +38,23 @@ MUTATIONS = {
                     "score = np.where(valid, 1.0 / (dist + eps * eps), 0.0)"),
     "padding not masked": ("score = np.where(valid, 1.0 / (dist + eps), 0.0)", "score = 1.0 / (dist + eps)"),
     "not normalised": ("out[seg, r0:r0 + len(rr)] = num / z[:, None]", "out[seg, r0:r0 + len(rr)] = num"),
-    "query minus wrong row": ("diff = q[seg, rr][:, None, :] - k[seg][jj]", "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]"),
+    "bwd: o_i not subtracted": ('g = np.einsum("bd,bkd->bk", du, vj) - np.einsum("bd,bd->b", du, o)[:, None]',
+                                 'g = np.einsum("bd,bkd->bk", du, vj)'),
+    "bwd: delta not squared": ("w = np.where(valid, g / zs[:, None] / (delta * delta), 0.0)",
+                               "w = np.where(valid, g / zs[:, None] / delta, 0.0)"),
+    "bwd: not divided by Z": ("w = np.where(valid, g / zs[:, None] / (delta * delta), 0.0)",
+                              "w = np.where(valid, g / (delta * delta), 0.0)"),
+    "bwd: dq sign": ("dq[seg, rr] = -2.0 * np.einsum", "dq[seg, rr] = 2.0 * np.einsum"),
+    "bwd: dq factor": ("dq[seg, rr] = -2.0 * np.einsum", "dq[seg, rr] = -1.0 * np.einsum"),
+    "bwd: dk sign": ("(2.0 * w[:, :, None] * diff)", "(-2.0 * w[:, :, None] * diff)"),
+    "bwd: dv unnormalised": ("(a[:, :, None] * du[:, None, :])", "(score[:, :, None] * du[:, None, :])"),
+    "bwd: dv to query rows": ("np.add.at(dv[seg], jj.ravel()[sel]", "np.add.at(dv[seg], np.repeat(rr, jj.shape[1])[sel]"),
+    "bwd: deps sign": ("deps -= float(w.sum())", "deps += float(w.sum())"),
+    "bwd: padding not masked": ("score = np.where(valid, 1.0 / delta, 0.0)  # S_ij", "score = 1.0 / delta  # S_ij"),
+    "query minus wrong row": ("diff = q[seg, rr][:, None, :] - k[seg][jj]  # [b, k, dk]",
+                              "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]  # [b, k, dk]"),
+    "bwd: query minus wrong row": ("diff = q[seg, rr][:, None, :] - k[seg][jj]  # q_i - k_j",
+                                   "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]  # q_i - k_j"),
 }
 
 
