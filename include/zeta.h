@@ -1,5 +1,6 @@
 /*
- * zeta.h -- C ABI of the Z-order top-k attention forward pass (ZETA) for
+ * zeta.h -- C ABI of the Z-order top-k attention (ZETA): the forward pass and
+ * the attention gradients, for
  * AMD Instinct MI355X (gfx950).
  *
  * The forward pass has four calls, run in this order on one stream:
@@ -11,6 +12,8 @@
  *                          the next two calls
  *   zeta_select_topk    -> k candidate keys per query around its insertion point
  *   zeta_topk_attn_fwd  -> Cauchy-softmax attention over the candidates
+ *
+ * zeta_topk_attn_bwd gives the attention's gradients for the same windows.
  *
  * zeta_select_attend_fwd runs the last two in one pass (the candidates never
  * leave the chip); zeta_query_order prepares the fast processing order.
@@ -216,9 +219,39 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
                                      hipStream_t stream);
 
 /*
+ * zeta_topk_attn_bwd -- gradients of the attention of zeta_topk_attn_fwd
+ * with respect to q, k, v and eps, for fixed windows idx (Appendix E.2,
+ * summary of gradient computations; the selection has no gradient).  With
+ * S_ij = 1 / (||q_i - k_j||^2 + eps), Z_i = sum_j S_ij, A_ij = S_ij / Z_i,
+ * o_i = sum_j A_ij v_j and L the loss with dout = dL/do:
+ *   dv_j  = sum over queries i whose window holds j of A_ij dout_i
+ *   dq_i  = -2 sum_j w_ij (q_i - k_j),  w_ij = dout_i . (v_j - o_i) S_ij^2 / Z_i
+ *   dk_j  =  2 sum over i of w_ij (q_i - k_j)
+ *   deps  = -sum over all i, j of w_ij
+ * o_i is recomputed from the same terms (the forward output is not needed).
+ * All arithmetic and all gradients are float32.
+ *
+ *   q, k, v, dtype, B, H, N, d_k, d_v, topk, idx, q_order, eps: as for
+ *            zeta_topk_attn_fwd (q_order only changes the processing order).
+ *   dout     [B][H][N][d_v], `dtype`, 16-byte aligned: dL/do.
+ *   dq, dk   float32 [B][H][N][d_k] outputs; dv float32 [B][H][N][d_v].
+ *   deps     float32 [1] output: the gradient of the one eps of the call.
+ *   workspace  at least zeta_workspace_size(...) bytes.
+ * Every output element is written (rows without candidates get zeros).  dk
+ * and dv are accumulated with float32 atomics, so their last bits depend on
+ * the order of accumulation; dq and deps do not.  The outputs must be distinct
+ * buffers and none may be an input (INVALID_ARG).
+ */
+zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
+                                 int64_t H, int64_t N, int d_k, int d_v, int topk, const int32_t* idx,
+                                 const int32_t* q_order, const void* dout, float eps, float* dq, float* dk,
+                                 float* dv, float* deps, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/*
  * zeta_workspace_size -- bytes of device workspace enough for each of
- * zeta_morton_encode, zeta_sort_keys, zeta_query_order and zeta_select_topk
- * on this shape,
+ * zeta_morton_encode, zeta_sort_keys, zeta_query_order, zeta_select_topk,
+ * zeta_select_attend_fwd and zeta_topk_attn_bwd on this shape,
  * where the sort may cover the query codes together with the key codes
  * (2*B*H segments).  One buffer serves all calls run in order on one stream.
  * Returns 0 for invalid shapes.

@@ -1,4 +1,5 @@
-"""ZETA Z-order top-k attention forward for AMD Instinct MI355X (gfx950).
+"""ZETA Z-order top-k attention (forward pass and attention gradients) for AMD
+Instinct MI355X (gfx950).
 
 The compute lives in ``libzeta.so`` (hand-written HIP kernels behind the C ABI
 of ``include/zeta.h``); ``zeta`` is its thin Python binding.
@@ -18,6 +19,7 @@ from .zeta import (  # noqa: F401
     zeta_select_topk,
     zeta_sort_keys,
     zeta_status_string,
+    zeta_topk_attn_bwd,
     zeta_topk_attn_fwd,
     zeta_workspace_size,
 )

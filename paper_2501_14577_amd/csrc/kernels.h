@@ -67,4 +67,11 @@ hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf
 
 bool attend_supports(int dv);
 
+// Attention gradients for fixed windows (dq written, dk and dv accumulated
+// after being cleared, deps = one float).  Workspace: bwd_ws(S, N).
+hipError_t launch_attend_bwd(const void* q, const void* k, const void* v, const void* dout, bool is_bf16, int64_t S,
+                             int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
+                             float eps, float* dq, float* dkg, float* dvg, float* deps, void* workspace,
+                             hipStream_t stream);
+
 }  // namespace zeta

@@ -151,6 +151,19 @@ inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
+// Attention gradients: per-query partial sums of the eps gradient, then the
+// per-block sums of their fixed-order reduction.
+struct BwdWs {
+  size_t part_off, block_off, bytes;
+};
+inline BwdWs bwd_ws(int64_t S, int64_t N) {
+  BwdWs w;
+  w.part_off = 0;
+  w.block_off = align_up(size_t(S) * size_t(N) * sizeof(float));
+  w.bytes = w.block_off + align_up(256 * sizeof(float));
+  return w;
+}
+
 // Regrouping a processing order by list level: a copy of the given order
 // (when it is regrouped in place) and the radix pass's histograms.
 struct QueryOrderWs {

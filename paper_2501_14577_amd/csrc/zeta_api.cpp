@@ -146,6 +146,33 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
                                                sorted_codes, perm, q_order, eps, out, idx_out, workspace, stream));
 }
 
+zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B, int64_t H,
+                                 int64_t N, int d_k, int d_v, int topk, const int32_t* idx, const int32_t* q_order,
+                                 const void* dout, float eps, float* dq, float* dk, float* dv, float* deps,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!q || !k || !v || !idx || !dout || !dq || !dk || !dv || !deps) return ZETA_ERR_INVALID_ARG;
+  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || d_v < 1 || topk < 1) return ZETA_ERR_INVALID_ARG;
+  if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
+  if (!aligned16(v) || !aligned16(dout)) return ZETA_ERR_INVALID_ARG;
+  // Outputs are distinct buffers, none of them an input.
+  const void* outs[4] = {dq, dk, dv, deps};
+  const void* ins[6] = {q, k, v, dout, idx, q_order};
+  for (int a = 0; a < 4; ++a) {
+    for (int b = a + 1; b < 4; ++b)
+      if (outs[a] == outs[b]) return ZETA_ERR_INVALID_ARG;
+    for (int b = 0; b < 6; ++b)
+      if (outs[a] == ins[b]) return ZETA_ERR_INVALID_ARG;
+  }
+  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
+  if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
+  const int64_t S = B * H;
+  const zeta::BwdWs ws = zeta::bwd_ws(S, N);
+  if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
+  return hip_status(zeta::launch_attend_bwd(q, k, v, dout, dtype == ZETA_BF16, S, N, d_k, d_v, topk, idx, q_order, eps,
+                                            dq, dk, dv, deps, workspace, stream));
+}
+
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk, int causal) {
   if (bad_count(B, H, N) || d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32 || topk < 1) return 0;
   const int64_t S = B * H;
@@ -155,7 +182,9 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
   const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
   const size_t ob = zeta::query_order_ws(S, N).bytes;
   const size_t fb = zeta::fused_ws(S, N, topk, causal ? 1 : 0).bytes;
+  const size_t bb = zeta::bwd_ws(S, N).bytes;
   if (fb > bytes) bytes = fb;
+  if (bb > bytes) bytes = bb;
   if (sb > bytes) bytes = sb;
   if (lb > bytes) bytes = lb;
   if (ob > bytes) bytes = ob;

@@ -26,6 +26,7 @@ EXPORTED = (
     "zeta_select_topk",
     "zeta_topk_attn_fwd",
     "zeta_select_attend_fwd",
+    "zeta_topk_attn_bwd",
     "zeta_workspace_size",
     "zeta_status_string",
 )
@@ -59,10 +60,12 @@ def load_library() -> ctypes.CDLL:
     L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, f32, vp, vp]
     L.zeta_select_attend_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, f32,
                                          vp, vp, vp, sz, vp]
+    L.zeta_topk_attn_bwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, vp,
+                                     vp, sz, vp]
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
     for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
-                 "zeta_topk_attn_fwd", "zeta_select_attend_fwd"):
+                 "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_topk_attn_bwd"):
         getattr(L, name).restype = ctypes.c_int
     L.zeta_workspace_size.restype = sz
     L.zeta_status_string.restype = ctypes.c_char_p
@@ -211,6 +214,35 @@ def zeta_topk_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
                                            _ptr(idx), _ptr(q_order), float(eps), _ptr(out), _stream())
     _check("zeta_topk_attn_fwd", st)
     return out
+
+
+def zeta_topk_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, dout: torch.Tensor,
+                       eps: float, *, q_order: Optional[torch.Tensor] = None, dq: Optional[torch.Tensor] = None,
+                       dk: Optional[torch.Tensor] = None, dv: Optional[torch.Tensor] = None,
+                       deps: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """Gradients of the attention over idx -> (dq, dk, dv, deps), float32:
+    dq, dk [B,H,N,d_k], dv [B,H,N,d_v], deps [1]."""
+    B, H, N, dkk = q.shape
+    dvv = v.shape[-1]
+    topk = idx.shape[-1]
+    f32 = dict(dtype=torch.float32, device=q.device)
+    dq = torch.empty((B, H, N, dkk), **f32) if dq is None else dq
+    dk = torch.empty((B, H, N, dkk), **f32) if dk is None else dk
+    dv = torch.empty((B, H, N, dvv), **f32) if dv is None else dv
+    deps = torch.empty((1,), **f32) if deps is None else deps
+    if workspace is None:
+        workspace = workspace_for(B, H, N, dkk, 1, topk, True, q.device)
+    _need_device(q, k, v, idx, dout, q_order, dq, dk, dv, deps, workspace)
+    if not (q.dtype == k.dtype == v.dtype == dout.dtype):
+        raise ValueError("q, k, v and dout must share a dtype")
+    if any(t.dtype != torch.float32 for t in (dq, dk, dv, deps)):
+        raise ValueError("gradients are float32")
+    st = load_library().zeta_topk_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dkk, dvv, topk,
+                                           _ptr(idx), _ptr(q_order), _ptr(dout), float(eps), _ptr(dq), _ptr(dk),
+                                           _ptr(dv), _ptr(deps), _ptr(workspace),
+                                           workspace.numel() * workspace.element_size(), _stream())
+    _check("zeta_topk_attn_bwd", st)
+    return dq, dk, dv, deps
 
 
 def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_codes: torch.Tensor,

@@ -188,3 +188,30 @@ FUSED_CASES = [
 @pytest.mark.parametrize("kw,code", FUSED_CASES, ids=[str(c[0]) for c in FUSED_CASES])
 def test_select_attend_rejects(kw, code):
     assert _fused(**kw) == code
+
+
+def _bwd(**kw):
+    a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, idx=P4, q_order=NULL,
+             dout=ctypes.c_void_p(0x50000), eps=0.5, dq=ctypes.c_void_p(0x60000), dk=ctypes.c_void_p(0x70000),
+             dv=ctypes.c_void_p(0x80000), deps=ctypes.c_void_p(0x90000), ws=ctypes.c_void_p(0xA0000), ws_bytes=BIG,
+             stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_topk_attn_bwd(*a.values())
+
+
+BWD_CASES = [
+    (dict(q=NULL), INV), (dict(idx=NULL), INV), (dict(dout=NULL), INV), (dict(dq=NULL), INV), (dict(dk=NULL), INV),
+    (dict(dv=NULL), INV), (dict(deps=NULL), INV), (dict(B=0), INV), (dict(N=0), INV), (dict(d_k=0), INV),
+    (dict(topk=0), INV), (dict(eps=0.0), INV), (dict(eps=float("inf")), INV),
+    (dict(dout=ctypes.c_void_p(0x50004)), INV), (dict(v=ctypes.c_void_p(0x30008)), INV),
+    (dict(dk=ctypes.c_void_p(0x60000)), INV),  # dk aliases dq
+    (dict(dv=P3), INV),  # dv aliases v
+    (dict(deps=P4), INV),  # deps aliases idx
+    (dict(dtype=7), UNS), (dict(d_k=9), UNS), (dict(d_v=48), UNS), (dict(topk=1025), UNS),
+    (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP),
+]
+
+
+@pytest.mark.parametrize("kw,code", BWD_CASES, ids=[str(c[0]) for c in BWD_CASES])
+def test_attend_bwd_rejects(kw, code):
+    assert _bwd(**kw) == code

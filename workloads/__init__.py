@@ -124,3 +124,11 @@ def random_codes(seed: int, shape, code_bits: int) -> np.ndarray:
     """Uniform random codes below 2**code_bits (uint32), for sort and select tests."""
     return np.random.default_rng([seed, 5]).integers(0, 1 << code_bits, size=shape,
                                                     dtype=np.uint64).astype(np.uint32)
+
+
+def generate_dout(w: Workload, seed: Optional[int] = None) -> np.ndarray:
+    """Upstream gradient dL/do for the backward tests, [B,H,N,dv]: N(0,1) in
+    stream 6, float32 or bfloat16 bit patterns like v."""
+    seed = w.seed if seed is None else seed
+    d = _draw_normal(seed, 6, (w.B, w.H, w.N, w.dv))
+    return f32_to_bf16_bits(d) if w.dtype == "bf16" else d
