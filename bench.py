@@ -68,6 +68,17 @@ def step_bytes(w: workloads.Workload, causal: bool) -> int:
     return attend_bytes(w, causal) + rows * ((4 * d * s + 8) + 16 * passes + (4 + 8 * w.topk))
 
 
+def bwd_bytes(w: workloads.Workload, causal: bool) -> int:
+    """Algorithmic bytes of one attention-gradient launch: per query row its
+    q row, dout row, k indices, dq row and eps partial; per selected pair one
+    key row and one value row read, and a read-modify-write of the float32
+    dk and dv rows; no reuse across queries is assumed."""
+    s, d = elem_size(w.dtype), w.dk
+    rows = w.segments * w.N
+    return rows * (d * s + w.dv * s + 4 * w.topk + 4 * d + 4) + candidates(w, causal) * (
+        d * s + w.dv * s + 8 * d + 8 * w.dv)
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for path in KERNEL_SRCS:
@@ -217,6 +228,28 @@ def main() -> int:
 
     four_ms, attend_ms, _ = timed(step)
     ms_per_step, fused_ms, wall = timed(step_fused)
+
+    # Attention gradients (zeta_topk_attn_bwd) for the windows of the
+    # four-call step, timed on their own; not part of the forward metric.
+    dout = to_dev(workloads.generate_dout(w))
+    f32 = dict(dtype=torch.float32, device=dev)
+    gq = torch.empty((w.B, w.H, w.N, w.dk), **f32)
+    gk = torch.empty_like(gq)
+    gv = torch.empty((w.B, w.H, w.N, w.dv), **f32)
+    geps = torch.empty(1, **f32)
+    step()
+    torch.cuda.synchronize()
+
+    def bwd(ev=None):
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_topk_attn_bwd(q, k, v, bufs["idx"], dout, eps, q_order=bufs["order"], dq=gq, dk=gk, dv=gv,
+                                deps=geps, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+
+    bwd_ms, _, _ = timed(bwd)
+    b_bytes = bwd_bytes(w, causal)
     tokens = w.B * w.N
     a_bytes = attend_bytes(w, causal)
     f_bytes = a_bytes + w.segments * w.N * 4  # plus each query's code, read instead of an index row
@@ -266,6 +299,12 @@ def main() -> int:
             "value": tokens / (four_ms * 1e-3),
             "attend_ms": attend_ms,
             "attend_achieved_GBs": a_bytes / (attend_ms * 1e-3) / 1e9,
+        },
+        "backward": {
+            "ms": bwd_ms,
+            "algorithmic_bytes": b_bytes,
+            "achieved_GBs": b_bytes / (bwd_ms * 1e-3) / 1e9,
+            "frac": b_bytes / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         },
         "step_hbm_frac": s_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "step_algorithmic_bytes": s_bytes,

@@ -151,16 +151,29 @@ inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
-// Attention gradients: per-query partial sums of the eps gradient, then the
-// per-block sums of their fixed-order reduction.
+// Attention gradients: per-query partial sums of the eps gradient and the
+// per-block sums of their fixed-order reduction; per query (Z_i, c_i); the
+// key of every window slot, the slots sorted by key (keys and the sort's
+// permutation); each key's run of sorted slots; the sort's own workspace.
 struct BwdWs {
-  size_t part_off, block_off, bytes;
+  size_t part_off, block_off, zc_off, keys_off, sorted_off, slot_off, runs_off, sort_off, bytes;
+  int key_bits;  // bits of a slot key (keys run to N inclusive)
 };
-inline BwdWs bwd_ws(int64_t S, int64_t N) {
+inline BwdWs bwd_ws(int64_t S, int64_t N, int topk) {
   BwdWs w;
+  const size_t rows = size_t(S) * size_t(N);
+  const size_t slots = rows * size_t(topk);
+  w.key_bits = 1;
+  while ((int64_t(1) << w.key_bits) <= N) ++w.key_bits;
   w.part_off = 0;
-  w.block_off = align_up(size_t(S) * size_t(N) * sizeof(float));
-  w.bytes = w.block_off + align_up(256 * sizeof(float));
+  w.block_off = w.part_off + align_up(rows * sizeof(float));
+  w.zc_off = w.block_off + align_up(256 * sizeof(float));
+  w.keys_off = w.zc_off + align_up(rows * 2 * sizeof(float));
+  w.sorted_off = w.keys_off + align_up(slots * sizeof(uint32_t));
+  w.slot_off = w.sorted_off + align_up(slots * sizeof(uint32_t));
+  w.runs_off = w.slot_off + align_up(slots * sizeof(int32_t));
+  w.sort_off = w.runs_off + align_up(rows * 2 * sizeof(int32_t));
+  w.bytes = w.sort_off + sort_ws(S, N * topk, w.key_bits).bytes;
   return w;
 }
 

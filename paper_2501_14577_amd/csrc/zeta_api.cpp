@@ -29,6 +29,9 @@ bool overlaps(const void* a, const void* b, size_t bytes) {
   return x < y + bytes && y < x + bytes;
 }
 
+// Window slots per segment that the gradient's key sort can index (int32).
+constexpr int64_t zeta_max_bwd_slots() { return (int64_t(1) << 31) - 1; }
+
 bool bad_count(int64_t B, int64_t H, int64_t N) {
   if (B < 1 || H < 1 || N < 1) return true;
   if (B > kMaxElems / H) return true;
@@ -167,7 +170,8 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
   const int64_t S = B * H;
-  const zeta::BwdWs ws = zeta::bwd_ws(S, N);
+  if (N > zeta_max_bwd_slots() / topk) return ZETA_ERR_UNSUPPORTED;
+  const zeta::BwdWs ws = zeta::bwd_ws(S, N, topk);
   if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
   return hip_status(zeta::launch_attend_bwd(q, k, v, dout, dtype == ZETA_BF16, S, N, d_k, d_v, topk, idx, q_order, eps,
                                             dq, dk, dv, deps, workspace, stream));
@@ -182,7 +186,7 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
   const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
   const size_t ob = zeta::query_order_ws(S, N).bytes;
   const size_t fb = zeta::fused_ws(S, N, topk, causal ? 1 : 0).bytes;
-  const size_t bb = zeta::bwd_ws(S, N).bytes;
+  const size_t bb = (N <= zeta_max_bwd_slots() / topk) ? zeta::bwd_ws(S, N, topk).bytes : 0;
   if (fb > bytes) bytes = fb;
   if (bb > bytes) bytes = bb;
   if (sb > bytes) bytes = sb;

@@ -56,9 +56,11 @@ def test_workspace_size():
     assert ws(1, 1, 10, 3, 11, 4, 1) == 0  # 33 code bits
     assert ws(1, 1, 10, 0, 10, 4, 1) == 0
     assert ws(1, 1, 10, 3, 10, 0, 1) == 0
-    # Long-context shape: the sort's ping-pong buffer for query and key codes
-    # together (2 x 16 x 65536 x 8 B) dominates.
+    # Long-context shape: the gradients' window slots (keys, sorted keys, sorted
+    # slots: 3 x 16 x 65536 x 128 x 4 B, plus the key sort's own buffers)
+    # dominate; the forward's joint sort needs 2 x 16 x 65536 x 8 B.
     big = ws(1, 16, 65536, 3, 6, 128, 1)
+    assert big >= 3 * 16 * 65536 * 128 * 4
     assert big >= 2 * 16 * 65536 * 8
     assert big % 256 == 0
     assert ws(1, 16, 65536, 3, 6, 128, 0) <= big

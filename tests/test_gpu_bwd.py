@@ -137,9 +137,9 @@ def test_bwd_long_context():
 
 
 def test_bwd_processing_order_and_repeat():
-    """dq and deps are bit-identical across runs and processing orders (each
-    query's sums are its own; deps is reduced in a fixed order); dk and dv
-    agree to float32 rounding of their atomic sums."""
+    """Every gradient is bit-identical across runs and processing orders: a
+    query's sums are its own, a key's sums run over its queries in sorted
+    (query, slot) order, and deps is reduced in a fixed order."""
     cfg = 2
     w, x, _ = inputs(cfg)
     log("bwd processing order")
@@ -152,6 +152,5 @@ def test_bwd_processing_order_and_repeat():
             _run(raw["q"], raw["k"], raw["v"], dout_raw, idx, 0.5, w.dtype,
                  q_order=np.stack([rng.permutation(w.N) for _ in range(S)]).astype(np.int32))]
     a, b = runs
-    assert np.array_equal(a[0], b[0]) and np.array_equal(a[3], b[3])
-    for t in (1, 2):
-        _close(b[t], a[t], "dk/dv")
+    for t in range(4):
+        assert np.array_equal(a[t], b[t]), t
