@@ -140,6 +140,9 @@ def main() -> int:
                     help="segments in the oracle sample (0 skips the CPU baseline)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (for counter calibration)")
+    ap.add_argument("--skip-backward", action="store_true", help="time the forward only (for its profile)")
+    ap.add_argument("--backward-only", action="store_true",
+                    help="time the attention gradients only (for their profile); forward fields are null")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -226,8 +229,11 @@ def main() -> int:
         wall = time.perf_counter() - wall0
         return (start.elapsed_time(stop) / args.steps, float(np.mean([a.elapsed_time(b) for a, b in evs])), wall)
 
-    four_ms, attend_ms, _ = timed(step)
-    ms_per_step, fused_ms, wall = timed(step_fused)
+    if args.backward_only:
+        four_ms = attend_ms = ms_per_step = fused_ms = wall = None
+    else:
+        four_ms, attend_ms, _ = timed(step)
+        ms_per_step, fused_ms, wall = timed(step_fused)
 
     # Attention gradients (zeta_topk_attn_bwd) for the windows of the
     # four-call step, timed on their own; not part of the forward metric.
@@ -237,6 +243,7 @@ def main() -> int:
     gk = torch.empty_like(gq)
     gv = torch.empty((w.B, w.H, w.N, w.dv), **f32)
     geps = torch.empty(1, **f32)
+    bws = zeta.bwd_workspace_for(w.B, w.H, w.N, w.topk, dev)
     step()
     torch.cuda.synchronize()
 
@@ -244,18 +251,30 @@ def main() -> int:
         if ev is not None:
             ev[0].record()
         zeta.zeta_topk_attn_bwd(q, k, v, bufs["idx"], dout, eps, q_order=bufs["order"], dq=gq, dk=gk, dv=gv,
-                                deps=geps, workspace=ws)
+                                deps=geps, workspace=bws)
         if ev is not None:
             ev[1].record()
 
-    bwd_ms, _, _ = timed(bwd)
     b_bytes = bwd_bytes(w, causal)
+    bwd_ms = None if args.skip_backward else timed(bwd)[0]
     tokens = w.B * w.N
     a_bytes = attend_bytes(w, causal)
     f_bytes = a_bytes + w.segments * w.N * 4  # plus each query's code, read instead of an index row
-    achieved = f_bytes / (fused_ms * 1e-3) / 1e9
     s_bytes = step_bytes(w, causal)
     traffic = read_traffic()
+
+    def per_s(amount, ms):  # amount per second, None when the part was not timed
+        return None if ms is None else amount / (ms * 1e-3)
+
+    def gbs(nbytes, ms):
+        r = per_s(nbytes, ms)
+        return None if r is None else r / 1e9
+
+    def frac(nbytes, ms):
+        r = gbs(nbytes, ms)
+        return None if r is None else r / HBM_PEAK_GBS
+
+    achieved = gbs(f_bytes, fused_ms)
 
     cpu = None
     if args.cpu_heads > 0:
@@ -263,7 +282,7 @@ def main() -> int:
 
     line = {
         "metric": "query-tokens/sec for Z-order top-k attn fwd; % of HBM roofline",
-        "value": tokens / (ms_per_step * 1e-3),
+        "value": per_s(tokens, ms_per_step),
         "unit": "query-tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -287,28 +306,28 @@ def main() -> int:
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
+            "frac": frac(f_bytes, fused_ms),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": f_bytes,
             "kernel_ms": fused_ms,
             # Bytes that actually crossed HBM (calibrated counters) per second.
-            "traffic_GBs": (traffic / (fused_ms * 1e-3) / 1e9) if traffic else None,
+            "traffic_GBs": gbs(traffic, fused_ms) if traffic else None,
         },
         "four_call_path": {
             "ms_per_step": four_ms,
-            "value": tokens / (four_ms * 1e-3),
+            "value": per_s(tokens, four_ms),
             "attend_ms": attend_ms,
-            "attend_achieved_GBs": a_bytes / (attend_ms * 1e-3) / 1e9,
+            "attend_achieved_GBs": gbs(a_bytes, attend_ms),
         },
         "backward": {
             "ms": bwd_ms,
             "algorithmic_bytes": b_bytes,
-            "achieved_GBs": b_bytes / (bwd_ms * 1e-3) / 1e9,
-            "frac": b_bytes / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "achieved_GBs": gbs(b_bytes, bwd_ms),
+            "frac": frac(b_bytes, bwd_ms),
         },
-        "step_hbm_frac": s_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "step_hbm_frac": frac(s_bytes, ms_per_step),
         "step_algorithmic_bytes": s_bytes,
-        "query_rows_per_s": w.segments * w.N / (ms_per_step * 1e-3),
+        "query_rows_per_s": per_s(w.segments * w.N, ms_per_step),
         "timed_wall_s": wall,
         "cpu_baseline": cpu,
     }

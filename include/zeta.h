@@ -236,11 +236,13 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
  *   dout     [B][H][N][d_v], `dtype`, 16-byte aligned: dL/do.
  *   dq, dk   float32 [B][H][N][d_k] outputs; dv float32 [B][H][N][d_v].
  *   deps     float32 [1] output: the gradient of the one eps of the call.
- *   workspace  at least zeta_workspace_size(...) bytes.
- * Every output element is written (rows without candidates get zeros).  dk
- * and dv are accumulated with float32 atomics, so their last bits depend on
- * the order of accumulation; dq and deps do not.  The outputs must be distinct
- * buffers and none may be an input (INVALID_ARG).
+ *   workspace  at least zeta_bwd_workspace_size(B, H, N, topk) bytes (it
+ *            holds one key per window slot and their sorted copy).
+ * Every output element is written (rows without candidates and keys in no
+ * window get zeros).  No atomics: dk and dv are summed per key after a stable
+ * sort of the window slots by key, so every output is bit-identical from run
+ * to run and for every q_order.  N * topk above 2^31 - 1 is UNSUPPORTED.  The
+ * outputs must be distinct buffers and none may be an input (INVALID_ARG).
  */
 zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
                                  int64_t H, int64_t N, int d_k, int d_v, int topk, const int32_t* idx,
@@ -250,14 +252,22 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
 
 /*
  * zeta_workspace_size -- bytes of device workspace enough for each of
- * zeta_morton_encode, zeta_sort_keys, zeta_query_order, zeta_select_topk,
- * zeta_select_attend_fwd and zeta_topk_attn_bwd on this shape,
- * where the sort may cover the query codes together with the key codes
- * (2*B*H segments).  One buffer serves all calls run in order on one stream.
- * Returns 0 for invalid shapes.
+ * zeta_morton_encode, zeta_sort_keys, zeta_query_order, zeta_select_topk and
+ * zeta_select_attend_fwd on this shape, where the sort may cover the query
+ * codes together with the key codes (2*B*H segments).  One buffer serves all
+ * forward calls run in order on one stream.  Returns 0 for invalid shapes.
  */
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk,
                            int causal);
+
+/*
+ * zeta_bwd_workspace_size -- bytes of device workspace for zeta_topk_attn_bwd
+ * on this shape: about 22 bytes per window slot (B*H*N*topk slots: the slot
+ * keys, their sorted copy with slot numbers, the sort's ping-pong buffer)
+ * plus per-row partials and the sort's histograms.  Returns 0 for invalid
+ * shapes and for N * topk above 2^31 - 1.
+ */
+size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int topk);
 
 /* Static, human-readable name of a status code. */
 const char* zeta_status_string(zeta_status_t status);

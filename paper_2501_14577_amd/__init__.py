@@ -12,6 +12,7 @@ from .zeta import (  # noqa: F401
     forward,
     library_path,
     load_library,
+    bwd_workspace_for,
     workspace_for,
     zeta_morton_encode,
     zeta_query_order,
@@ -22,4 +23,5 @@ from .zeta import (  # noqa: F401
     zeta_topk_attn_bwd,
     zeta_topk_attn_fwd,
     zeta_workspace_size,
+    zeta_bwd_workspace_size,
 )

@@ -186,13 +186,17 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
   const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
   const size_t ob = zeta::query_order_ws(S, N).bytes;
   const size_t fb = zeta::fused_ws(S, N, topk, causal ? 1 : 0).bytes;
-  const size_t bb = (N <= zeta_max_bwd_slots() / topk) ? zeta::bwd_ws(S, N, topk).bytes : 0;
   if (fb > bytes) bytes = fb;
-  if (bb > bytes) bytes = bb;
   if (sb > bytes) bytes = sb;
   if (lb > bytes) bytes = lb;
   if (ob > bytes) bytes = ob;
   return bytes;
+}
+
+size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int topk) {
+  if (bad_count(B, H, N) || topk < 1 || topk > zeta::kMaxTopk) return 0;
+  if (N > zeta_max_bwd_slots() / topk) return 0;
+  return zeta::bwd_ws(B * H, N, topk).bytes;
 }
 
 const char* zeta_status_string(zeta_status_t status) {

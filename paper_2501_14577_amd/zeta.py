@@ -28,6 +28,7 @@ EXPORTED = (
     "zeta_select_attend_fwd",
     "zeta_topk_attn_bwd",
     "zeta_workspace_size",
+    "zeta_bwd_workspace_size",
     "zeta_status_string",
 )
 
@@ -63,11 +64,13 @@ def load_library() -> ctypes.CDLL:
     L.zeta_topk_attn_bwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, vp,
                                      vp, sz, vp]
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
+    L.zeta_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
     L.zeta_status_string.argtypes = [i32]
     for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
                  "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_topk_attn_bwd"):
         getattr(L, name).restype = ctypes.c_int
     L.zeta_workspace_size.restype = sz
+    L.zeta_bwd_workspace_size.restype = sz
     L.zeta_status_string.restype = ctypes.c_char_p
     _lib = L
     return L
@@ -114,6 +117,15 @@ def zeta_workspace_size(B: int, H: int, N: int, d_k: int, bits: int, topk: int, 
 
 def workspace_for(B, H, N, d_k, bits, topk, causal, device) -> torch.Tensor:
     n = max(zeta_workspace_size(B, H, N, d_k, bits, topk, causal), 256)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def zeta_bwd_workspace_size(B: int, H: int, N: int, topk: int) -> int:
+    return int(load_library().zeta_bwd_workspace_size(B, H, N, topk))
+
+
+def bwd_workspace_for(B, H, N, topk, device) -> torch.Tensor:
+    n = max(zeta_bwd_workspace_size(B, H, N, topk), 256)
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
@@ -231,7 +243,7 @@ def zeta_topk_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
     dv = torch.empty((B, H, N, dvv), **f32) if dv is None else dv
     deps = torch.empty((1,), **f32) if deps is None else deps
     if workspace is None:
-        workspace = workspace_for(B, H, N, dkk, 1, topk, True, q.device)
+        workspace = bwd_workspace_for(B, H, N, topk, q.device)
     _need_device(q, k, v, idx, dout, q_order, dq, dk, dv, deps, workspace)
     if not (q.dtype == k.dtype == v.dtype == dout.dtype):
         raise ValueError("q, k, v and dout must share a dtype")

@@ -56,16 +56,29 @@ def test_workspace_size():
     assert ws(1, 1, 10, 3, 11, 4, 1) == 0  # 33 code bits
     assert ws(1, 1, 10, 0, 10, 4, 1) == 0
     assert ws(1, 1, 10, 3, 10, 0, 1) == 0
-    # Long-context shape: the gradients' window slots (keys, sorted keys, sorted
-    # slots: 3 x 16 x 65536 x 128 x 4 B, plus the key sort's own buffers)
-    # dominate; the forward's joint sort needs 2 x 16 x 65536 x 8 B.
+    # Long-context shape: the forward's joint sort needs 2 x 16 x 65536 x 8 B;
+    # the one-pass call's lists, bounds and list-order key rows stay below 64 MB.
     big = ws(1, 16, 65536, 3, 6, 128, 1)
-    assert big >= 3 * 16 * 65536 * 128 * 4
     assert big >= 2 * 16 * 65536 * 8
+    assert big < 64 << 20
     assert big % 256 == 0
     assert ws(1, 16, 65536, 3, 6, 128, 0) <= big
     # One tiny segment still gets a buffer for the range partials.
     assert ws(1, 1, 1, 3, 10, 1, 1) > 0
+
+
+def test_bwd_workspace_size():
+    ws = zeta.zeta_bwd_workspace_size
+    assert ws(0, 1, 10, 4) == 0
+    assert ws(1, 1, 10, 0) == 0
+    assert ws(1, 1, 10, 1025) == 0
+    assert ws(1, 1, 1 << 22, 1024) == 0  # N * topk = 2^32 slots
+    # Long-context shape: the window slots (keys, sorted keys, sorted slots:
+    # 3 x 16 x 65536 x 128 x 4 B) plus the slot sort's own buffers.
+    big = ws(1, 16, 65536, 128)
+    assert big >= 3 * 16 * 65536 * 128 * 4
+    assert big % 256 == 0
+    assert ws(1, 1, 1, 1) > 0
 
 
 def _enc(**kw):
