@@ -1,4 +1,4 @@
-"""CPU oracle for the Z-order top-k attention forward (test infrastructure only).
+"""CPU oracle for the Z-order top-k attention and its gradients (test infrastructure only).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
 ``cpu_baseline`` leg may import this package; the product path never does.
@@ -10,6 +10,7 @@ from .zeta_oracle import (  # noqa: F401
     attend_bwd,
     bf16_bits_to_f32,
     forward,
+    history_mean,
     interleave,
     joint_range,
     morton_encode,

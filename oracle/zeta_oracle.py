@@ -1,4 +1,4 @@
-"""CPU oracle for the ZETA Z-order top-k attention forward pass.
+"""CPU oracle for the ZETA Z-order top-k attention forward pass and its gradients.
 
 TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import or run this module.  The
@@ -26,6 +26,10 @@ defines, one function per step, each citing the passage it follows:
 6. ``attend_bwd``: the gradients of that attention with respect to q, k, v
    and eps for fixed windows (Appendix E.2, summary of gradient
    computations).
+7. ``history_mean``: the mean key and mean value of each query's history,
+   which ``attend`` and ``attend_bwd`` can append to every window as one more
+   candidate (Section 3.4, last paragraph: the history mean appended to the
+   top-k tokens with a cumulative sum, as smoothing).
 
 Readings where the paper is silent or ambiguous (each is also listed in the
 design notes):
@@ -48,6 +52,11 @@ design notes):
   after p, shifted inward at the pool's ends; it is emitted in (code,
   position) order, padded with -1 to length k.
 * Distances use the unquantised q and k values; eps = gamma^2 > 0 is a scalar.
+* The history-mean candidate (optional) is the pair (mean of k_0..k_i, mean of
+  v_0..v_i) for causal query i, and the mean over all N rows when not causal.
+  It is scored like any other candidate and joins the normaliser; a row with
+  an empty window then attends to it alone.  Gradients flow through the means
+  back to every key and value of the history.
 
 Arithmetic: quantisation in float32 as above; attention in float64.
 """
@@ -229,18 +238,44 @@ def select_topk(q_codes: np.ndarray, k_codes: np.ndarray, k: int, causal: bool) 
 # (Section 3.3, equation cauchy; Section 3.4; Appendix E.1)
 # ----------------------------------------------------------------------------
 
+def history_mean(k: np.ndarray, v: np.ndarray, causal: bool) -> Tuple[np.ndarray, np.ndarray]:
+    """Mean key and mean value of each query's history (Section 3.4, last
+    paragraph: a cumulative sum gives the history's mean vector, appended to
+    the top-k candidates).
+
+    Causal: row i holds (k_0 + ... + k_i) / (i + 1) and likewise for v.  Not
+    causal: every row holds the mean over all N rows.  k: [S, N, dk], v:
+    [S, N, dv]; float64 results of the same shapes.
+    """
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    N = k.shape[1]
+    if causal:
+        count = np.arange(1, N + 1, dtype=np.float64)[None, :, None]
+        return np.cumsum(k, axis=1) / count, np.cumsum(v, axis=1) / count
+    mk = np.broadcast_to(k.mean(axis=1, keepdims=True), k.shape).copy()
+    mv = np.broadcast_to(v.mean(axis=1, keepdims=True), v.shape).copy()
+    return mk, mv
+
+
 def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: float,
-           rows: Optional[np.ndarray] = None, block: int = 512) -> np.ndarray:
+           rows: Optional[np.ndarray] = None, block: int = 512,
+           mean_k: Optional[np.ndarray] = None, mean_v: Optional[np.ndarray] = None) -> np.ndarray:
     """o_i = sum_j S_ij v_j / sum_j S_ij with S_ij = 1 / (||q_i - k_j||^2 + eps).
 
     q, k: [S, N, dk]; v: [S, N, dv] (float values of any float dtype); idx:
     int32 [S, N, k] with -1 for empty slots (or [S, R, k] when ``rows`` gives
     the R query positions it belongs to).  Computed in float64.  Returns
     float64 [S, N, dv] (or [S, R, dv]).
+
+    With ``mean_k`` and ``mean_v`` ([S, N, dk] and [S, N, dv], from
+    ``history_mean``), row i's window gains one more candidate, the pair
+    (mean_k[i], mean_v[i]), scored and normalised like the others.
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
+    with_mean = mean_k is not None
     S = q.shape[0]
     if rows is None:
         rows = np.arange(q.shape[1])
@@ -256,12 +291,17 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: fl
             score = np.where(valid, 1.0 / (dist + eps), 0.0)  # S_ij
             z = score.sum(axis=1)  # Z_i
             num = np.einsum("bk,bkd->bd", score, v[seg][jj])
+            if with_mean:  # the history-mean candidate
+                dm = q[seg, rr] - np.asarray(mean_k[seg, rr], dtype=np.float64)
+                sm = 1.0 / (np.sum(dm * dm, axis=-1) + eps)
+                z = z + sm
+                num = num + sm[:, None] * np.asarray(mean_v[seg, rr], dtype=np.float64)
             out[seg, r0:r0 + len(rr)] = num / z[:, None]
     return out
 
 
 def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: float, dout: np.ndarray,
-               block: int = 512):
+               block: int = 512, history: bool = False, causal: bool = True):
     """Gradients of L = sum_i dout_i . o_i through the attention of ``attend``
     (Appendix E.2, summary of gradient computations), for fixed windows idx.
 
@@ -277,6 +317,13 @@ def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps
     q, k: [S, N, dk]; v, dout: [S, N, dv]; idx: int32 [S, N, k] with -1 for
     empty slots.  Computed in float64.  Returns (dq [S, N, dk], dk [S, N, dk],
     dv [S, N, dv], deps float).
+
+    With ``history`` the windows also hold the history-mean candidate of
+    ``history_mean(k, v, causal)``.  Its terms are those of any candidate, with
+    (mean_k[i], mean_v[i]) in place of (k_j, v_j); the gradients that reach
+    mean_k[i] and mean_v[i] then pass to every row of query i's history, each
+    divided by the history's length: row j receives the sum over the queries
+    i >= j (causal) or over all queries (not causal).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -287,6 +334,10 @@ def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps
     dk = np.zeros_like(k)
     dv = np.zeros_like(v)
     deps = 0.0
+    if history:
+        mean_k, mean_v = history_mean(k, v, causal)
+        dmk = np.zeros_like(k)  # gradient reaching mean_k[i]
+        dmv = np.zeros_like(v)  # gradient reaching mean_v[i]
     for seg in range(S):
         for r0 in range(0, N, block):
             rr = np.arange(r0, min(N, r0 + block))
@@ -297,11 +348,18 @@ def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps
             delta = np.sum(diff * diff, axis=-1) + eps  # delta_ij
             score = np.where(valid, 1.0 / delta, 0.0)  # S_ij
             z = score.sum(axis=1)  # Z_i
+            if history:
+                dm = q[seg, rr] - mean_k[seg, rr]  # q_i - mean_k[i]
+                delta_m = np.sum(dm * dm, axis=-1) + eps
+                z = z + 1.0 / delta_m
             has = z > 0
             zs = np.where(has, z, 1.0)
             a = score / zs[:, None]  # A_ij
             vj = v[seg][jj]  # [b, k, dv]
             o = np.einsum("bk,bkd->bd", a, vj)  # o_i
+            if history:
+                a_m = 1.0 / delta_m / zs
+                o = o + a_m[:, None] * mean_v[seg, rr]
             du = dout[seg, rr]  # [b, dv]
             g = np.einsum("bd,bkd->bk", du, vj) - np.einsum("bd,bd->b", du, o)[:, None]  # dout_i . (v_j - o_i)
             w = np.where(valid, g / zs[:, None] / (delta * delta), 0.0)
@@ -310,6 +368,22 @@ def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps
             np.add.at(dk[seg], jj.ravel()[sel], (2.0 * w[:, :, None] * diff).reshape(-1, diff.shape[-1])[sel])
             np.add.at(dv[seg], jj.ravel()[sel], (a[:, :, None] * du[:, None, :]).reshape(-1, du.shape[-1])[sel])
             deps -= float(w.sum())
+            if history:
+                g_m = np.einsum("bd,bd->b", du, mean_v[seg, rr] - o)
+                w_m = g_m / zs / (delta_m * delta_m)
+                dq[seg, rr] -= 2.0 * w_m[:, None] * dm
+                dmk[seg, rr] = 2.0 * w_m[:, None] * dm
+                dmv[seg, rr] = a_m[:, None] * du
+                deps -= float(w_m.sum())
+    if history:
+        # Row j of the history receives d(mean)/d(row j) = 1 / (history length).
+        if causal:
+            count = np.arange(1, N + 1, dtype=np.float64)[None, :, None]
+            dk += np.cumsum((dmk / count)[:, ::-1], axis=1)[:, ::-1]
+            dv += np.cumsum((dmv / count)[:, ::-1], axis=1)[:, ::-1]
+        else:
+            dk += dmk.sum(axis=1, keepdims=True) / N
+            dv += dmv.sum(axis=1, keepdims=True) / N
     return dq, dk, dv, deps
 
 
@@ -318,11 +392,13 @@ def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps
 # ----------------------------------------------------------------------------
 
 def forward(q: np.ndarray, k: np.ndarray, v: np.ndarray, topk: int, eps: float, causal: bool,
-            bits: int, range_lohi=None) -> dict:
-    """All five steps for float32 inputs shaped [S, N, d]; returns every intermediate."""
+            bits: int, range_lohi=None, history: bool = False) -> dict:
+    """All five steps for float32 inputs shaped [S, N, d]; returns every
+    intermediate.  ``history`` appends the history-mean candidate."""
     qc, kc, lo, hi = morton_encode(q, k, bits, range_lohi)
     sorted_codes, perm = sort_keys(kc)
     idx = select_topk(qc, kc, topk, causal)
-    out = attend(q, k, v, idx, eps)
+    mk, mv = history_mean(k, v, causal) if history else (None, None)
+    out = attend(q, k, v, idx, eps, mean_k=mk, mean_v=mv)
     return dict(q_codes=qc, k_codes=kc, lo=lo, hi=hi, sorted_codes=sorted_codes, perm=perm,
-                idx=idx, out=out)
+                idx=idx, mean_k=mk, mean_v=mv, out=out)

@@ -373,6 +373,126 @@ def check_attend_bwd_invariants(orc):
     assert np.allclose(dq[0, 3], 0.0, atol=1e-14)
 
 
+# ----------------------------------------------------------------------------
+# History-mean candidate (Section 3.4, last paragraph)
+# ----------------------------------------------------------------------------
+
+def _history_example():
+    rows = {}
+    for line in open(os.path.join(GOLDEN, "history_mean_example.txt")):
+        if line.strip() and not line.startswith("#"):
+            key, *vals = line.split()
+            rows[key] = vals
+    q = np.array([[[float(x) for x in rows["q"]]] * 2])
+    k = np.array([[[float(x) for x in rows["k0"]], [float(x) for x in rows["k1"]]]])
+    v = np.array([[[float(x)] for x in rows["v"]]])
+    idx = np.array([[[0, -1], [1, -1]]], dtype=np.int32)
+    return rows, q, k, v, idx, float(rows["eps"][0])
+
+
+def check_history_mean_golden(orc):
+    """The hand-worked example in golden/history_mean_example.txt: the means,
+    the outputs in both modes and every gradient of the causal case."""
+    rows, q, k, v, idx, eps = _history_example()
+    fr = lambda key: np.array([_frac(x) for x in rows[key]])  # noqa: E731
+    mk, mv = orc.history_mean(k, v, True)
+    assert np.allclose(mk[0, 0], fr("mean_k_causal0"), atol=1e-15) and np.allclose(mk[0, 1], fr("mean_k_causal1"), atol=1e-15)
+    assert np.allclose(mv[0, :, 0], fr("mean_v_causal"), atol=1e-15)
+    out = orc.attend(q, k, v, idx, eps, mean_k=mk, mean_v=mv)
+    assert np.allclose(out[0, :, 0], fr("out_causal"), atol=1e-14), out
+    fk, fv = orc.history_mean(k, v, False)
+    assert np.allclose(fk[0], fr("mean_k_full")[None, :], atol=1e-15) and np.allclose(fv[0, :, 0], fr("mean_v_full")[0])
+    out = orc.attend(q, k, v, idx, eps, mean_k=fk, mean_v=fv)
+    assert np.allclose(out[0, :, 0], fr("out_full"), atol=1e-14), out
+    dq, dk, dv, deps = orc.attend_bwd(q, k, v, idx, eps, np.ones((1, 2, 1)), history=True, causal=True)
+    assert np.allclose(dq[0, 0], fr("dq0"), atol=1e-14) and np.allclose(dq[0, 1], fr("dq1"), atol=1e-14), dq
+    assert np.allclose(dk[0, 0], fr("dk0"), atol=1e-14) and np.allclose(dk[0, 1], fr("dk1"), atol=1e-14), dk
+    assert np.allclose(dv[0, :, 0], fr("dv"), atol=1e-14), dv
+    assert abs(deps - _frac(rows["deps"][0])) < 1e-14, deps
+
+
+def check_history_mean_brute(orc):
+    """Each row's means summed term by term (math.fsum) over its history:
+    rows 0..i when causal, all rows otherwise."""
+    import math
+    rng = np.random.default_rng(81)
+    k = rng.normal(size=(2, 13, 3))
+    v = rng.normal(size=(2, 13, 5))
+    for causal in (True, False):
+        mk, mv = orc.history_mean(k, v, causal)
+        for seg in range(2):
+            for i in range(13):
+                hist = range(i + 1) if causal else range(13)
+                for arr, mean in ((k, mk), (v, mv)):
+                    for c in range(arr.shape[-1]):
+                        want = math.fsum(arr[seg, j, c] for j in hist) / len(hist)
+                        assert abs(mean[seg, i, c] - want) < 1e-14, (causal, seg, i, c)
+
+
+def check_history_attend_augmented(orc):
+    """The history-mean candidate is one more key/value pair: attending with
+    it equals attending, without it, over keys and values extended by the
+    mean rows, with row i's window extended by the index of its own mean row."""
+    q, k, v, dout, idx = _bwd_problem(83, S=2, N=11, topk=4, causal=True)
+    for causal in (True, False):
+        mk, mv = orc.history_mean(k, v, causal)
+        N = k.shape[1]
+        k2 = np.concatenate([k, mk], axis=1)
+        v2 = np.concatenate([v, mv], axis=1)
+        extra = np.broadcast_to(N + np.arange(N, dtype=np.int32)[None, :, None], (2, N, 1))
+        idx2 = np.concatenate([idx, extra], axis=2)
+        q2 = np.concatenate([q, np.zeros_like(q)], axis=1)
+        idx2 = np.concatenate([idx2, np.full((2, N, idx2.shape[2]), -1, dtype=np.int32)], axis=1)
+        idx2[:, N:, 0] = 0  # the padding rows need a candidate; their output is not compared
+        want = orc.attend(q2, k2, v2, idx2, 0.6)[:, :N]
+        got = orc.attend(q, k, v, idx, 0.6, mean_k=mk, mean_v=mv)
+        assert np.allclose(got, want, atol=1e-13), causal
+
+
+def check_history_bwd_finite_diff(orc):
+    """With the history-mean candidate, every gradient equals the central
+    difference of L = sum dout . o, where o comes from orc.attend with the means
+    of orc.history_mean recomputed from the perturbed k and v (so the
+    difference also carries the means' dependence on every history row)."""
+    eps = 0.45
+    for causal in (True, False):
+        q, k, v, dout, idx = _bwd_problem(84, S=1, N=8, topk=3, causal=causal)
+        idx[0, 2, :] = -1  # a row that attends to its history mean alone
+        dq, dk, dv, deps = orc.attend_bwd(q, k, v, idx, eps, dout, history=True, causal=causal)
+
+        def loss(qx, kx, vx, e):
+            mk, mv = orc.history_mean(kx, vx, causal)
+            return float(np.sum(dout * orc.attend(qx, kx, vx, idx, e, mean_k=mk, mean_v=mv)))
+
+        h = 1e-6
+        for name, arr, grad in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+            for flat in range(arr.size):
+                pos = np.unravel_index(flat, arr.shape)
+                a1, a2 = arr.copy(), arr.copy()
+                a1[pos] += h
+                a2[pos] -= h
+                args1 = {"q": q, "k": k, "v": v}
+                args2 = dict(args1)
+                args1[name], args2[name] = a1, a2
+                fd = (loss(args1["q"], args1["k"], args1["v"], eps) - loss(args2["q"], args2["k"], args2["v"], eps)) / (2 * h)
+                assert abs(fd - grad[pos]) <= 1e-6 * (1.0 + abs(fd)), (causal, name, pos, fd, grad[pos])
+        fd = (loss(q, k, v, eps + h) - loss(q, k, v, eps - h)) / (2 * h)
+        assert abs(fd - deps) <= 1e-6 * (1.0 + abs(fd)), (causal, fd, deps)
+
+
+def check_history_bwd_invariants(orc):
+    """With the history-mean candidate every row has a candidate and its
+    weights (the mean's spread over the history) still sum to 1, so
+    sum dv = sum dout over all rows; a common shift of q and k shifts the
+    means too, so sum dq + sum dk = 0."""
+    for causal in (True, False):
+        q, k, v, dout, idx = _bwd_problem(85, S=2, N=10, topk=4, causal=causal)
+        idx[1, 4, :] = -1
+        dq, dk, dv, deps = orc.attend_bwd(q, k, v, idx, 0.3, dout, history=True, causal=causal)
+        assert np.allclose(dv.sum(axis=(0, 1)), dout.sum(axis=(0, 1)), atol=1e-10), causal
+        assert np.allclose(dq.sum(axis=(0, 1)) + dk.sum(axis=(0, 1)), 0.0, atol=1e-10), causal
+
+
 ALL_PINS = [
     check_morton_golden,
     check_morton_bijection,
@@ -391,4 +511,9 @@ ALL_PINS = [
     check_attend_bwd_golden,
     check_attend_bwd_finite_diff,
     check_attend_bwd_invariants,
+    check_history_mean_golden,
+    check_history_mean_brute,
+    check_history_attend_augmented,
+    check_history_bwd_finite_diff,
+    check_history_bwd_invariants,
 ]

@@ -55,6 +55,25 @@ MUTATIONS = {
                               "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]  # [b, k, dk]"),
     "bwd: query minus wrong row": ("diff = q[seg, rr][:, None, :] - k[seg][jj]  # q_i - k_j",
                                    "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]  # q_i - k_j"),
+    "history: sums instead of means": ("return np.cumsum(k, axis=1) / count, np.cumsum(v, axis=1) / count",
+                                       "return np.cumsum(k, axis=1), np.cumsum(v, axis=1)"),
+    "history: current row excluded": ("return np.cumsum(k, axis=1) / count, np.cumsum(v, axis=1) / count",
+                                      "return (np.cumsum(k, axis=1) - k) / np.maximum(count - 1, 1), "
+                                      "(np.cumsum(v, axis=1) - v) / np.maximum(count - 1, 1)"),
+    "history: non-causal uses prefix": ("    mk = np.broadcast_to(k.mean(axis=1, keepdims=True), k.shape).copy()\n",
+                                        "    mk = np.cumsum(k, axis=1) / np.arange(1, N + 1)[None, :, None]\n"),
+    "history: mean not in normaliser": ("                z = z + sm\n", ""),
+    "history: mean value unweighted": ("num = num + sm[:, None] * np.asarray(mean_v[seg, rr], dtype=np.float64)",
+                                       "num = num + np.asarray(mean_v[seg, rr], dtype=np.float64)"),
+    "history bwd: means not passed back": ("            dk += np.cumsum((dmk / count)[:, ::-1], axis=1)[:, ::-1]\n", ""),
+    "history bwd: prefix instead of suffix": ("dv += np.cumsum((dmv / count)[:, ::-1], axis=1)[:, ::-1]",
+                                              "dv += np.cumsum(dmv / count, axis=1)"),
+    "history bwd: not divided by length": ("dv += np.cumsum((dmv / count)[:, ::-1], axis=1)[:, ::-1]",
+                                           "dv += np.cumsum(dmv[:, ::-1], axis=1)[:, ::-1]"),
+    "history bwd: mean missing from o": ("                o = o + a_m[:, None] * mean_v[seg, rr]\n", ""),
+    "history bwd: dq term sign": ("dq[seg, rr] -= 2.0 * w_m[:, None] * dm", "dq[seg, rr] += 2.0 * w_m[:, None] * dm"),
+    "history bwd: deps term missing": ("                deps -= float(w_m.sum())\n", ""),
+    "history bwd: non-causal spread": ("dk += dmk.sum(axis=1, keepdims=True) / N", "dk += dmk / N"),
 }
 
 
