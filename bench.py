@@ -140,10 +140,15 @@ def main() -> int:
                     help="segments in the oracle sample (0 skips the CPU baseline)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (for counter calibration)")
-    ap.add_argument("--skip-backward", action="store_true", help="time the forward only (for its profile)")
-    ap.add_argument("--backward-only", action="store_true",
-                    help="time the attention gradients only (for their profile); forward fields are null")
+    ap.add_argument("--parts", default="forward,backward,history",
+                    help="comma list of the parts to time: forward (the metric), backward (attention gradients), "
+                         "history (the history-mean candidate, forward and gradients); fields of parts not "
+                         "timed are null, so that each part's profile holds only its own kernels")
     args = ap.parse_args()
+    parts = set(args.parts.split(","))
+    if not parts <= {"forward", "backward", "history"}:
+        print(f"unknown part in --parts {args.parts}", file=sys.stderr)
+        return 2
 
     if args.gpus != 1:
         print("bench.py runs on one GPU only: every (batch, head) segment is independent, "
@@ -229,11 +234,11 @@ def main() -> int:
         wall = time.perf_counter() - wall0
         return (start.elapsed_time(stop) / args.steps, float(np.mean([a.elapsed_time(b) for a, b in evs])), wall)
 
-    if args.backward_only:
-        four_ms = attend_ms = ms_per_step = fused_ms = wall = None
-    else:
+    if "forward" in parts:
         four_ms, attend_ms, _ = timed(step)
         ms_per_step, fused_ms, wall = timed(step_fused)
+    else:
+        four_ms = attend_ms = ms_per_step = fused_ms = wall = None
 
     # Attention gradients (zeta_topk_attn_bwd) for the windows of the
     # four-call step, timed on their own; not part of the forward metric.
@@ -243,7 +248,7 @@ def main() -> int:
     gk = torch.empty_like(gq)
     gv = torch.empty((w.B, w.H, w.N, w.dv), **f32)
     geps = torch.empty(1, **f32)
-    bws = zeta.bwd_workspace_for(w.B, w.H, w.N, w.topk, dev)
+    bws = zeta.bwd_workspace_for(w.B, w.H, w.N, w.dk, w.dv, w.topk, "history" in parts, dev)
     step()
     torch.cuda.synchronize()
 
@@ -256,7 +261,48 @@ def main() -> int:
             ev[1].record()
 
     b_bytes = bwd_bytes(w, causal)
-    bwd_ms = None if args.skip_backward else timed(bwd)[0]
+    bwd_ms = timed(bwd)[0] if "backward" in parts else None
+
+    # The history-mean candidate: the means (zeta_history_mean) timed alone,
+    # the one-pass step with the candidate, and the gradients with it.
+    mk = torch.empty((w.B, w.H, w.N, w.dk), **f32)
+    mv = torch.empty((w.B, w.H, w.N, w.dv), **f32)
+
+    def hist_means(ev=None):
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_history_mean(k, v, causal, mean_k=mk, mean_v=mv, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+
+    def step_hist(ev=None):
+        qc, kc = zeta.zeta_morton_encode(q, k, w.bits, q_codes=codes[0], k_codes=codes[1], workspace=ws)
+        zeta.zeta_sort_keys(codes, w.code_bits, sorted_codes=sorted2, perm=perm2, workspace=ws)
+        order = zeta.zeta_query_order(perm2[0], w.N, w.segments, w.topk, causal, order_out=bufs["order"],
+                                      workspace=ws)
+        zeta.zeta_history_mean(k, v, causal, mean_k=mk, mean_v=mv, workspace=ws)
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_select_attend_fwd(q, k, v, qc, sorted2[1], perm2[1], w.topk, causal, eps, q_order=order,
+                                    mean_k=mk, mean_v=mv, out=bufs["out"], workspace=ws)
+        if ev is not None:
+            ev[1].record()
+
+    def bwd_hist(ev=None):
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_topk_attn_bwd(q, k, v, bufs["idx"], dout, eps, q_order=bufs["order"], mean_k=mk, mean_v=mv,
+                                causal=causal, dq=gq, dk=gk, dv=gv, deps=geps, workspace=bws)
+        if ev is not None:
+            ev[1].record()
+
+    h_bytes = w.segments * w.N * (w.dk + w.dv) * (elem_size(w.dtype) + 4)  # read k, v once; write the means
+    if "history" in parts:
+        hist_ms = timed(hist_means)[1]
+        hist_step_ms, hist_fused_ms, _ = timed(step_hist)
+        hist_bwd_ms = timed(bwd_hist)[0]
+    else:
+        hist_ms = hist_step_ms = hist_fused_ms = hist_bwd_ms = None
     tokens = w.B * w.N
     a_bytes = attend_bytes(w, causal)
     f_bytes = a_bytes + w.segments * w.N * 4  # plus each query's code, read instead of an index row
@@ -324,6 +370,16 @@ def main() -> int:
             "algorithmic_bytes": b_bytes,
             "achieved_GBs": gbs(b_bytes, bwd_ms),
             "frac": frac(b_bytes, bwd_ms),
+        },
+        "history_mean": {
+            "step_ms": hist_step_ms,
+            "value": per_s(tokens, hist_step_ms),
+            "select_attend_ms": hist_fused_ms,
+            "means_ms": hist_ms,
+            "means_algorithmic_bytes": h_bytes,
+            "means_achieved_GBs": gbs(h_bytes, hist_ms),
+            "means_frac": frac(h_bytes, hist_ms),
+            "backward_ms": hist_bwd_ms,
         },
         "step_hbm_frac": frac(s_bytes, ms_per_step),
         "step_algorithmic_bytes": s_bytes,

@@ -14,6 +14,8 @@
  *   zeta_topk_attn_fwd  -> Cauchy-softmax attention over the candidates
  *
  * zeta_topk_attn_bwd gives the attention's gradients for the same windows.
+ * zeta_history_mean prepares the optional history-mean candidate that the
+ * attention calls (and the gradients) add to every window.
  *
  * zeta_select_attend_fwd runs the last two in one pass (the candidates never
  * leave the chip); zeta_query_order prepares the fast processing order.
@@ -172,6 +174,10 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  * Distances use the unquantised q and k.  Accumulation is float32; a
  * bfloat16 output is rounded to nearest even.  A row whose idx holds no
  * valid entry is written as zeros.
+ * With mean_k and mean_v (both given, or both NULL) every window gains the
+ * history-mean candidate of Section 3.4: the pair (mean_k[i], mean_v[i])
+ * scored and normalised like the other candidates (a row with no valid
+ * entry then attends to it alone).
  *
  *   q, k   [B][H][N][d_k], v [B][H][N][d_v], out [B][H][N][d_v], all `dtype`.
  *   idx      int32 [B*H][N][topk]; valid entries (0 <= j < N) first, then -1.
@@ -180,13 +186,16 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  *            of zeta_query_order's order gather mostly the same value rows,
  *            which then come from cache; the output bits do not depend on it.
  *   eps      gamma^2: finite and > 0.
+ *   mean_k, mean_v  optional float32 [B*H][N][d_k] and [B*H][N][d_v] (as
+ *            zeta_history_mean writes them); mean_v 16-byte aligned.
  *
  * Supported d_v: 32, 64, 128, 256.  v and out must be 16-byte aligned; out
  * must not overlap the inputs.
  */
 zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
                                  int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
-                                 const int32_t* idx, const int32_t* q_order, float eps, void* out,
+                                 const int32_t* idx, const int32_t* q_order, float eps,
+                                 const float* mean_k, const float* mean_v, void* out,
                                  hipStream_t stream);
 
 /*
@@ -202,10 +211,11 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
  * runs on the matrix cores (scores split into two bfloat16 parts, float32
  * accumulation).  The output agrees with the two calls to float32 rounding,
  * and a query's bits depend only on its own window, so they are the same for
- * every processing order.
+ * every processing order.  The history-mean candidate, when given, is added
+ * per query in float32.
  *
- *   q, k, v, dtype, B, H, N, d_k, d_v, topk, eps, out: as for
- *            zeta_topk_attn_fwd; causal as for zeta_select_topk.
+ *   q, k, v, dtype, B, H, N, d_k, d_v, topk, eps, mean_k, mean_v, out: as
+ *            for zeta_topk_attn_fwd; causal as for zeta_select_topk.
  *   q_codes, sorted_codes, perm, q_order: as for zeta_select_topk.
  *   idx_out  optional int32 [B*H][N][topk]: receives the windows, exactly as
  *            zeta_select_topk writes them.
@@ -214,9 +224,31 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
 zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
                                      int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
                                      int causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
-                                     const int32_t* perm, const int32_t* q_order, float eps, void* out,
+                                     const int32_t* perm, const int32_t* q_order, float eps,
+                                     const float* mean_k, const float* mean_v, void* out,
                                      int32_t* idx_out, void* workspace, size_t workspace_bytes,
                                      hipStream_t stream);
+
+/*
+ * zeta_history_mean -- the history-mean candidate (Section 3.4, last
+ * paragraph: the mean vector of the history, from a cumulative sum, is added
+ * to the top-k candidates as smoothing).  For causal calls row i holds the
+ * means of rows 0..i,
+ *   mean_k[i] = (k_0 + ... + k_i) / (i + 1),  mean_v[i] likewise;
+ * otherwise every row holds the means over all N rows.  Sums are float32,
+ * formed per chunk of 64 rows and then across chunks, in a fixed order.
+ *
+ *   k        [B][H][N][d_k], v [B][H][N][d_v], `dtype`; v 16-byte aligned.
+ *   causal   0 or 1.
+ *   mean_k   float32 [B*H][N][d_k] output; mean_v float32 [B*H][N][d_v]
+ *            output, 16-byte aligned; neither may be an input.
+ *   workspace  at least zeta_workspace_size(...) bytes.
+ * Supported d_v: 32, 64, 128, 256; d_k up to ZETA_MAX_DK.
+ */
+zeta_status_t zeta_history_mean(const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
+                                int64_t H, int64_t N, int d_k, int d_v, int causal, float* mean_k,
+                                float* mean_v, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /*
  * zeta_topk_attn_bwd -- gradients of the attention of zeta_topk_attn_fwd
@@ -229,15 +261,24 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
  *   dk_j  =  2 sum over i of w_ij (q_i - k_j)
  *   deps  = -sum over all i, j of w_ij
  * o_i is recomputed from the same terms (the forward output is not needed).
+ * With mean_k and mean_v the history-mean candidate takes part as in the
+ * forward: its terms join Z_i, o_i, dq_i and deps, and the gradients that
+ * reach mean_k[i] and mean_v[i] pass to every row j of query i's history,
+ * divided by its length: dk_j, dv_j gain the sum over i >= j (causal) or
+ * over all i of those, divided by i + 1 (causal) or N.
  * All arithmetic and all gradients are float32.
  *
  *   q, k, v, dtype, B, H, N, d_k, d_v, topk, idx, q_order, eps: as for
  *            zeta_topk_attn_fwd (q_order only changes the processing order).
  *   dout     [B][H][N][d_v], `dtype`, 16-byte aligned: dL/do.
- *   dq, dk   float32 [B][H][N][d_k] outputs; dv float32 [B][H][N][d_v].
+ *   mean_k, mean_v  optional, as for zeta_topk_attn_fwd; causal (0 or 1)
+ *            says how zeta_history_mean formed them (read only with them).
+ *   dq, dk   float32 [B][H][N][d_k] outputs; dv float32 [B][H][N][d_v]
+ *            (16-byte aligned when the means are given).
  *   deps     float32 [1] output: the gradient of the one eps of the call.
- *   workspace  at least zeta_bwd_workspace_size(B, H, N, topk) bytes (it
- *            holds one key per window slot and their sorted copy).
+ *   workspace  at least zeta_bwd_workspace_size(B, H, N, d_k, d_v, topk,
+ *            means given) bytes (it holds one key per window slot and their
+ *            sorted copy).
  * Every output element is written (rows without candidates and keys in no
  * window get zeros).  No atomics: dk and dv are summed per key after a stable
  * sort of the window slots by key, so every output is bit-identical from run
@@ -246,8 +287,9 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
  */
 zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
                                  int64_t H, int64_t N, int d_k, int d_v, int topk, const int32_t* idx,
-                                 const int32_t* q_order, const void* dout, float eps, float* dq, float* dk,
-                                 float* dv, float* deps, void* workspace, size_t workspace_bytes,
+                                 const int32_t* q_order, const void* dout, float eps, const float* mean_k,
+                                 const float* mean_v, int causal, float* dq, float* dk, float* dv,
+                                 float* deps, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
 /*
@@ -255,7 +297,8 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
  * zeta_morton_encode, zeta_sort_keys, zeta_query_order, zeta_select_topk and
  * zeta_select_attend_fwd on this shape, where the sort may cover the query
  * codes together with the key codes (2*B*H segments).  One buffer serves all
- * forward calls run in order on one stream.  Returns 0 for invalid shapes.
+ * forward calls run in order on one stream, and zeta_history_mean.  Returns
+ * 0 for invalid shapes.
  */
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk,
                            int causal);
@@ -264,10 +307,13 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
  * zeta_bwd_workspace_size -- bytes of device workspace for zeta_topk_attn_bwd
  * on this shape: about 22 bytes per window slot (B*H*N*topk slots: the slot
  * keys, their sorted copy with slot numbers, the sort's ping-pong buffer)
- * plus per-row partials and the sort's histograms.  Returns 0 for invalid
- * shapes and for N * topk above 2^31 - 1.
+ * plus per-row partials and the sort's histograms; with history_mean
+ * nonzero also 4 * (d_k + d_v) bytes per row for the gradients reaching the
+ * means.  Returns 0 for invalid or unsupported shapes and for N * topk above
+ * 2^31 - 1.
  */
-size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int topk);
+size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
+                               int history_mean);
 
 /* Static, human-readable name of a status code. */
 const char* zeta_status_string(zeta_status_t status);

@@ -14,6 +14,7 @@ from .zeta import (  # noqa: F401
     load_library,
     bwd_workspace_for,
     workspace_for,
+    zeta_history_mean,
     zeta_morton_encode,
     zeta_query_order,
     zeta_select_attend_fwd,

@@ -27,7 +27,8 @@ COMMON = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
-SOURCES = ["encode.hip", "sort.hip", "select.hip", "attend.hip", "fused.hip", "tile.hip", "attend_bwd.hip", "zeta_api.cpp"]
+SOURCES = ["encode.hip", "sort.hip", "select.hip", "attend.hip", "fused.hip", "tile.hip", "attend_bwd.hip", "history.hip",
+           "zeta_api.cpp"]
 
 
 def hipcc() -> str:

@@ -16,8 +16,10 @@
 //            eight rows in flight per lane, accumulating in float32.  Loads
 //            address the segment's values through a wave-uniform base and a
 //            32-bit per-lane offset.
-//   Phase 3: xor-shuffles fold the groups; the first group scales by the
-//            normaliser and stores the row (bfloat16 rounded to nearest even).
+//   Phase 3: xor-shuffles fold the groups; the first group adds the
+//            history-mean candidate when given (its score joins the
+//            normaliser), scales by the normaliser and stores the row
+//            (bfloat16 rounded to nearest even).
 // Distances and the accumulation use explicit fused multiply-adds.
 //
 // Queries are taken in an optional processing order (a permutation per
@@ -36,7 +38,8 @@ template <typename T, int DV, int DK, bool kOff32>
 __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
     attend_kernel(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                   const int32_t* __restrict__ idx, const int32_t* __restrict__ q_order, int64_t total,
-                  int64_t N, int dk_rt, int topk, float eps, T* __restrict__ out) {
+                  int64_t N, int dk_rt, int topk, float eps, const float* __restrict__ mk,
+                  const float* __restrict__ mv, T* __restrict__ out) {
   constexpr int kE = Vec16<T>::kElems;  // elements per lane load
   constexpr int kLpr = DV / kE;         // lanes per value row
   constexpr int kGroups = 64 / kLpr;    // rows per wavefront load
@@ -128,6 +131,11 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
     }
     zsum = wave_sum(zsum);
     m = wave_max(m);
+    float s_mean = 0.0f;
+    if (mk != nullptr) {
+      s_mean = mean_score<(DK > 0 ? DK : kMaxDk)>(mk, g, dk, qv, eps);
+      zsum += s_mean;
+    }
     wave_lds_sync();
 
     // Phase 2: weighted gather of value rows.
@@ -167,6 +175,7 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
 #pragma unroll
       for (int e = 0; e < kE; ++e) acc[e] += __shfl_xor(acc[e], off, 64);
     if (grp == 0) {
+      if (mv != nullptr) add_mean_value<kE>(mv + g * DV + sub * kE, s_mean, acc);
       const float inv = zsum > 0.0f ? 1.0f / zsum : 0.0f;
 #pragma unroll
       for (int e = 0; e < kE; ++e) acc[e] *= inv;
@@ -178,7 +187,7 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
 
 template <typename T, int DV, int DK>
 hipError_t launch_attend_t(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk,
-                           int topk, const int32_t* idx, const int32_t* q_order, float eps, void* out,
+                           int topk, const int32_t* idx, const int32_t* q_order, float eps, HistMean hm, void* out,
                            hipStream_t stream) {
   const int64_t total = S * N;
   const int64_t want = ceil_div(total, kAttWavesPerBlock);
@@ -188,20 +197,20 @@ hipError_t launch_attend_t(const void* q, const void* k, const void* v, int64_t 
   if (off32)
     hipLaunchKernelGGL((attend_kernel<T, DV, DK, true>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx,
-                       q_order, total, N, dk, topk, eps, static_cast<T*>(out));
+                       q_order, total, N, dk, topk, eps, hm.k, hm.v, static_cast<T*>(out));
   else
     hipLaunchKernelGGL((attend_kernel<T, DV, DK, false>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx,
-                       q_order, total, N, dk, topk, eps, static_cast<T*>(out));
+                       q_order, total, N, dk, topk, eps, hm.k, hm.v, static_cast<T*>(out));
   return hipGetLastError();
 }
 
 template <typename T, int DV>
 hipError_t launch_attend_dk(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk,
-                            int topk, const int32_t* idx, const int32_t* q_order, float eps, void* out,
+                            int topk, const int32_t* idx, const int32_t* q_order, float eps, HistMean hm, void* out,
                             hipStream_t stream) {
-  if (dk == 3) return launch_attend_t<T, DV, 3>(q, k, v, S, N, dk, topk, idx, q_order, eps, out, stream);
-  return launch_attend_t<T, DV, 0>(q, k, v, S, N, dk, topk, idx, q_order, eps, out, stream);
+  if (dk == 3) return launch_attend_t<T, DV, 3>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream);
+  return launch_attend_t<T, DV, 0>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream);
 }
 
 }  // namespace
@@ -210,12 +219,12 @@ bool attend_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv ==
 
 hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
                          int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
-                         float eps, void* out, hipStream_t stream) {
+                         float eps, HistMean hm, void* out, hipStream_t stream) {
 #define ZETA_ATTEND_CASE(DVV)                                                                            \
   case DVV:                                                                                              \
     return is_bf16                                                                                       \
-               ? launch_attend_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, idx, q_order, eps, out, stream) \
-               : launch_attend_dk<float, DVV>(q, k, v, S, N, dk, topk, idx, q_order, eps, out, stream);
+               ? launch_attend_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream) \
+               : launch_attend_dk<float, DVV>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream);
   switch (dv) {
     ZETA_ATTEND_CASE(32)
     ZETA_ATTEND_CASE(64)

@@ -25,6 +25,13 @@
 //      dv_j and dk_j accumulate in registers and are written once.
 // deps is the fixed-order sum of the per-query parts.  Every sum runs in a
 // fixed order, so all gradients are bit-reproducible.
+//
+// With the history-mean candidate (Section 3.4, last paragraph) each window
+// also holds the pair (mean_k[i], mean_v[i]); the query pass treats it like
+// any candidate for Z_i, c_i, dq_i and deps, and writes the gradients that
+// reach mean_k[i] and mean_v[i], divided by the history's length.  A reverse
+// scan then adds to every row j the sum of those over the queries whose
+// history holds j (i >= j when causal, all i otherwise).
 #include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -49,8 +56,10 @@ template <typename T, int DV, int DK>
 __global__ void __launch_bounds__(kBwdWaves * 64)
     bwd_query_kernel(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                      const T* __restrict__ dout, const int32_t* __restrict__ idx, const int32_t* __restrict__ q_order,
-                     int64_t total, int64_t N, int dk_rt, int topk, float eps, float* __restrict__ dq,
-                     float* __restrict__ deps_part, float2* __restrict__ zc, uint32_t* __restrict__ slot_keys) {
+                     int64_t total, int64_t N, int dk_rt, int topk, float eps, const float* __restrict__ mk,
+                     const float* __restrict__ mv, int causal, float* __restrict__ dq,
+                     float* __restrict__ deps_part, float2* __restrict__ zc, uint32_t* __restrict__ slot_keys,
+                     float* __restrict__ hk, float* __restrict__ hv) {
   constexpr int kE = Vec16<T>::kElems;  // elements per lane load
   constexpr int kLpr = DV / kE;         // lanes per value row
   constexpr int kGroups = 64 / kLpr;    // rows per wavefront load
@@ -125,12 +134,25 @@ __global__ void __launch_bounds__(kBwdWaves * 64)
     }
     zsum = wave_sum(zsum);
     m = wave_max(m);
+    float s_mean = 0.0f;  // the history-mean candidate's score
+    if (mk != nullptr) {
+      s_mean = mean_score<KD>(mk, g, dk_n, qv, eps);
+      zsum += s_mean;
+    }
     const float inv_z = zsum > 0.0f ? 1.0f / zsum : 0.0f;
     wave_lds_sync();
 
-    // Phase 2: dout_i . v_j per pair.
+    // Phase 2: dout_i . v_j per pair (and dout_i . mean_v[i]).
     float du[kE];
     Vec16<T>::widen(*reinterpret_cast<const uint4*>(dout + g * DV + sub * kE), du);
+    float dot_mean = 0.0f;
+    if (mv != nullptr) {
+      const float* mrow = mv + g * DV + sub * kE;
+#pragma unroll
+      for (int e = 0; e < kE; ++e) dot_mean = fmaf(du[e], mrow[e], dot_mean);
+#pragma unroll
+      for (int off = 1; off < kLpr; off <<= 1) dot_mean += __shfl_xor(dot_mean, off, 64);
+    }
     for (int c0 = grp; c0 < m; c0 += kUnroll * kGroups) {
       uint4 raw[kUnroll];
       int32_t jj[kUnroll];
@@ -158,7 +180,7 @@ __global__ void __launch_bounds__(kBwdWaves * 64)
     // dout_i . o_i = sum_j A_ij (dout_i . v_j).
     float cdot = 0.0f;
     for (int c = lane; c < m; c += 64) cdot = fmaf(s_s[c], s_g[c], cdot);
-    cdot = wave_sum(cdot) * inv_z;
+    cdot = fmaf(s_mean, dot_mean, wave_sum(cdot)) * inv_z;
 
     // Phase 3: w_ij, dq, dk, deps.
     float dqa[KD];
@@ -185,6 +207,34 @@ __global__ void __launch_bounds__(kBwdWaves * 64)
 #pragma unroll
     for (int a = 0; a < KD; ++a) dqa[a] = wave_sum(dqa[a]);
     wsum = wave_sum(wsum);
+    if (mk != nullptr) {
+      // The history-mean candidate's terms, and the gradients reaching
+      // mean_k[i] and mean_v[i] divided by the history's length.
+      const float w = (dot_mean - cdot) * s_mean * s_mean * inv_z;
+      const float inv_cnt = 1.0f / float(causal ? i + 1 : N);
+      float diff[KD];
+#pragma unroll
+      for (int a = 0; a < KD; ++a) {
+        diff[a] = a < dk_n ? qv[a] - mk[g * dk_n + a] : 0.0f;
+        dqa[a] = fmaf(w, diff[a], dqa[a]);
+      }
+      wsum += w;
+      if (lane == 0) {
+#pragma unroll
+        for (int a = 0; a < KD; ++a)
+          if (a < dk_n) hk[g * dk_n + a] = 2.0f * w * diff[a] * inv_cnt;
+      }
+      if (grp == 0) {
+        const float am = s_mean * inv_z * inv_cnt;
+        float hvv[kE];
+#pragma unroll
+        for (int e = 0; e < kE; ++e) hvv[e] = am * du[e];
+#pragma unroll
+        for (int e = 0; e < kE; e += 4)
+          *reinterpret_cast<float4*>(hv + g * DV + sub * kE + e) =
+              make_float4(hvv[e], hvv[e + 1], hvv[e + 2], hvv[e + 3]);
+      }
+    }
     if (lane == 0) {
 #pragma unroll
       for (int a = 0; a < KD; ++a)
@@ -402,8 +452,8 @@ void fill_zero(float* p, int64_t n, hipStream_t stream) {
 
 template <typename T, int DV>
 hipError_t launch_bwd_t(const T* q, const T* k, const T* v, const T* dout, int64_t S, int64_t N, int dk, int topk,
-                        const int32_t* idx, const int32_t* q_order, float eps, float* dq, float* dkg, float* dv,
-                        float* deps, const BwdWs& ws, char* wsb, hipStream_t stream) {
+                        const int32_t* idx, const int32_t* q_order, float eps, HistMean hm, bool causal, float* dq,
+                        float* dkg, float* dv, float* deps, const BwdWs& ws, char* wsb, hipStream_t stream) {
   const int64_t total = S * N;
   const int64_t M = N * topk;  // window slots per segment
   float* part = reinterpret_cast<float*>(wsb + ws.part_off);
@@ -413,7 +463,14 @@ hipError_t launch_bwd_t(const T* q, const T* k, const T* v, const T* dout, int64
   uint32_t* sorted_keys = reinterpret_cast<uint32_t*>(wsb + ws.sorted_off);
   int32_t* sorted_slot = reinterpret_cast<int32_t*>(wsb + ws.slot_off);
   int2* runs = reinterpret_cast<int2*>(wsb + ws.runs_off);
+  float* hk = reinterpret_cast<float*>(wsb + ws.hist_k_off);
+  float* hv = reinterpret_cast<float*>(wsb + ws.hist_v_off);
+  const bool history = hm.k != nullptr;
   fill_zero(dq, total * dk, stream);
+  if (history && q_order != nullptr) {  // rows absent from q_order pass nothing back
+    fill_zero(hk, total * dk, stream);
+    fill_zero(hv, total * DV, stream);
+  }
   fill_zero(part, total, stream);
   fill_zero(reinterpret_cast<float*>(zc), total * 2, stream);
   fill_zero(reinterpret_cast<float*>(runs), total * 2, stream);
@@ -429,10 +486,12 @@ hipError_t launch_bwd_t(const T* q, const T* k, const T* v, const T* dout, int64
     const size_t lds = size_t(kBwdWaves) * topk * 12;
     if (dk == 3)
       hipLaunchKernelGGL((bwd_query_kernel<T, DV, 3>), dim3(blocks), dim3(kBwdWaves * 64), lds, stream, q, k, v,
-                         dout, idx, q_order, total, N, dk, topk, eps, dq, part, zc, slot_keys);
+                         dout, idx, q_order, total, N, dk, topk, eps, hm.k, hm.v, causal ? 1 : 0, dq, part, zc,
+                         slot_keys, hk, hv);
     else
       hipLaunchKernelGGL((bwd_query_kernel<T, DV, 0>), dim3(blocks), dim3(kBwdWaves * 64), lds, stream, q, k, v,
-                         dout, idx, q_order, total, N, dk, topk, eps, dq, part, zc, slot_keys);
+                         dout, idx, q_order, total, N, dk, topk, eps, hm.k, hm.v, causal ? 1 : 0, dq, part, zc,
+                         slot_keys, hk, hv);
   }
   hipError_t e = launch_sort(slot_keys, S, M, ws.key_bits, sorted_keys, sorted_slot, wsb + ws.sort_off, stream);
   if (e != hipSuccess) return e;
@@ -448,6 +507,10 @@ hipError_t launch_bwd_t(const T* q, const T* k, const T* v, const T* dout, int64
       hipLaunchKernelGGL((bwd_key_kernel<T, DV, 0>), dim3(blocks), dim3(kBwdWaves * 64), 0, stream, q, k, v, dout,
                          total, N, dk, topk, eps, sorted_slot, runs, zc, dkg, dv);
   }
+  if (history) {
+    e = launch_history_spread(hv, dv, DV, hk, dkg, dk, S, N, causal, wsb + ws.hist_scan_off, stream);
+    if (e != hipSuccess) return e;
+  }
   const int nred = int(total < kRedBlocks ? total : kRedBlocks);
   hipLaunchKernelGGL(reduce_partials_kernel, dim3(unsigned(nred)), dim3(256), 0, stream, part, total, block_sums);
   hipLaunchKernelGGL(reduce_final_kernel, dim3(1), dim3(256), 0, stream, block_sums, nred, deps);
@@ -456,25 +519,26 @@ hipError_t launch_bwd_t(const T* q, const T* k, const T* v, const T* dout, int64
 
 template <typename T>
 hipError_t launch_bwd_dv(const void* q, const void* k, const void* v, const void* dout, int64_t S, int64_t N, int dk,
-                         int dv, int topk, const int32_t* idx, const int32_t* q_order, float eps, float* dq,
-                         float* dkg, float* dvg, float* deps, const BwdWs& ws, char* wsb, hipStream_t stream) {
+                         int dv, int topk, const int32_t* idx, const int32_t* q_order, float eps, HistMean hm,
+                         bool causal, float* dq, float* dkg, float* dvg, float* deps, const BwdWs& ws, char* wsb,
+                         hipStream_t stream) {
   const T* qq = static_cast<const T*>(q);
   const T* kk = static_cast<const T*>(k);
   const T* vv = static_cast<const T*>(v);
   const T* dd = static_cast<const T*>(dout);
   switch (dv) {
     case 32:
-      return launch_bwd_t<T, 32>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, dq, dkg, dvg, deps, ws, wsb,
-                                 stream);
+      return launch_bwd_t<T, 32>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, hm, causal, dq, dkg, dvg, deps,
+                                  ws, wsb, stream);
     case 64:
-      return launch_bwd_t<T, 64>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, dq, dkg, dvg, deps, ws, wsb,
-                                 stream);
+      return launch_bwd_t<T, 64>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, hm, causal, dq, dkg, dvg, deps,
+                                  ws, wsb, stream);
     case 128:
-      return launch_bwd_t<T, 128>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, dq, dkg, dvg, deps, ws, wsb,
-                                  stream);
+      return launch_bwd_t<T, 128>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, hm, causal, dq, dkg, dvg, deps,
+                                  ws, wsb, stream);
     case 256:
-      return launch_bwd_t<T, 256>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, dq, dkg, dvg, deps, ws, wsb,
-                                  stream);
+      return launch_bwd_t<T, 256>(qq, kk, vv, dd, S, N, dk, topk, idx, q_order, eps, hm, causal, dq, dkg, dvg, deps,
+                                  ws, wsb, stream);
     default:
       return hipErrorInvalidValue;
   }
@@ -484,15 +548,15 @@ hipError_t launch_bwd_dv(const void* q, const void* k, const void* v, const void
 
 hipError_t launch_attend_bwd(const void* q, const void* k, const void* v, const void* dout, bool is_bf16, int64_t S,
                              int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
-                             float eps, float* dq, float* dkg, float* dvg, float* deps, void* workspace,
-                             hipStream_t stream) {
-  const BwdWs ws = bwd_ws(S, N, topk);
+                             float eps, HistMean hm, bool causal, float* dq, float* dkg, float* dvg, float* deps,
+                             void* workspace, hipStream_t stream) {
+  const BwdWs ws = bwd_ws(S, N, topk, dk, dv, hm.k != nullptr);
   char* wsb = static_cast<char*>(workspace);
   if (is_bf16)
-    return launch_bwd_dv<uint16_t>(q, k, v, dout, S, N, dk, dv, topk, idx, q_order, eps, dq, dkg, dvg, deps, ws, wsb,
-                                   stream);
-  return launch_bwd_dv<float>(q, k, v, dout, S, N, dk, dv, topk, idx, q_order, eps, dq, dkg, dvg, deps, ws, wsb,
-                              stream);
+    return launch_bwd_dv<uint16_t>(q, k, v, dout, S, N, dk, dv, topk, idx, q_order, eps, hm, causal, dq, dkg, dvg,
+                                   deps, ws, wsb, stream);
+  return launch_bwd_dv<float>(q, k, v, dout, S, N, dk, dv, topk, idx, q_order, eps, hm, causal, dq, dkg, dvg, deps,
+                              ws, wsb, stream);
 }
 
 }  // namespace zeta

@@ -107,5 +107,34 @@ struct RowOff<true> {
   using type = uint32_t;
 };
 
+// Score of the history-mean candidate of query row g (Section 3.4): the
+// Cauchy score against the float32 mean key row mk[g].
+template <int KD>
+__device__ __forceinline__ float mean_score(const float* __restrict__ mk, int64_t g, int dk, const float* qv,
+                                            float eps) {
+  float d2 = 0.0f;
+#pragma unroll
+  for (int a = 0; a < KD; ++a) {
+    if (a < dk) {
+      const float diff = qv[a] - mk[g * dk + a];
+      d2 = fmaf(diff, diff, d2);
+    }
+  }
+  return 1.0f / (d2 + eps);
+}
+
+// acc[e] += s * mean value row elements [0, n) at p (16-byte aligned float32).
+template <int n>
+__device__ __forceinline__ void add_mean_value(const float* __restrict__ p, float s, float* acc) {
+#pragma unroll
+  for (int e = 0; e < n; e += 4) {
+    const float4 m = *reinterpret_cast<const float4*>(p + e);
+    acc[e] = fmaf(s, m.x, acc[e]);
+    acc[e + 1] = fmaf(s, m.y, acc[e + 1]);
+    acc[e + 2] = fmaf(s, m.z, acc[e + 2]);
+    acc[e + 3] = fmaf(s, m.w, acc[e + 3]);
+  }
+}
+
 }  // namespace
 }  // namespace zeta

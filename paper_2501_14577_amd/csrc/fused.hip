@@ -30,7 +30,8 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
                          const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                          const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
                          int64_t N, int dk_rt, int topk, int causal, int t0, int t_hi, int64_t cap, float eps,
-                         T* __restrict__ out, int32_t* __restrict__ idx_out) {
+                         const float* __restrict__ mk, const float* __restrict__ mv, T* __restrict__ out,
+                         int32_t* __restrict__ idx_out) {
   constexpr int kE = Vec16<T>::kElems;
   constexpr int kLpr = DV / kE;
   constexpr int kGroups = 64 / kLpr;
@@ -151,6 +152,11 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
         }
       }
       zsum = wave_sum(zsum);
+      float s_mean = 0.0f;
+      if (mk != nullptr) {
+        s_mean = mean_score<(DK > 0 ? DK : kMaxDk)>(mk, g, dk, qv, eps);
+        zsum += s_mean;
+      }
       wave_lds_sync();
 
       // Weighted gather of value rows.
@@ -188,6 +194,7 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
 #pragma unroll
         for (int e = 0; e < kE; ++e) acc[e] += __shfl_xor(acc[e], off, 64);
       if (grp == 0) {
+        if (mv != nullptr) add_mean_value<kE>(mv + g * DV + sub * kE, s_mean, acc);
         const float inv = zsum > 0.0f ? 1.0f / zsum : 0.0f;
 #pragma unroll
         for (int e = 0; e < kE; ++e) acc[e] *= inv;
@@ -201,8 +208,8 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
 template <typename T, int DV, int DK>
 hipError_t launch_t(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int topk, bool causal,
                     const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                    const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, float eps, void* out,
-                    int32_t* idx_out, hipStream_t stream) {
+                    const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, float eps, HistMean hm,
+                    void* out, int32_t* idx_out, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   const int64_t runs = ceil_div(total, kFusedRun);
@@ -214,25 +221,25 @@ hipError_t launch_t(const void* q, const void* k, const void* v, int64_t S, int6
     hipLaunchKernelGGL((select_attend_kernel<T, DV, DK, true>), dim3(blocks), dim3(kFusedWaves * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), q_codes,
                        sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, lp.t0,
-                       lp.t_hi, lp.cap, eps, static_cast<T*>(out), idx_out);
+                       lp.t_hi, lp.cap, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
   else
     hipLaunchKernelGGL((select_attend_kernel<T, DV, DK, false>), dim3(blocks), dim3(kFusedWaves * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), q_codes,
                        sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, lp.t0,
-                       lp.t_hi, lp.cap, eps, static_cast<T*>(out), idx_out);
+                       lp.t_hi, lp.cap, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
   return hipGetLastError();
 }
 
 template <typename T, int DV>
 hipError_t launch_dk(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int topk, bool causal,
                      const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                     const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, float eps, void* out,
-                     int32_t* idx_out, hipStream_t stream) {
+                     const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, float eps,
+                     HistMean hm, void* out, int32_t* idx_out, hipStream_t stream) {
   if (dk == 3)
     return launch_t<T, DV, 3>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
-                              q_order, eps, out, idx_out, stream);
+                              q_order, eps, hm, out, idx_out, stream);
   return launch_t<T, DV, 0>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
-                            q_order, eps, out, idx_out, stream);
+                            q_order, eps, hm, out, idx_out, stream);
 }
 
 }  // namespace
@@ -240,7 +247,8 @@ hipError_t launch_dk(const void* q, const void* k, const void* v, int64_t S, int
 hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,
                                 int dk, int dv, int topk, bool causal, const uint32_t* q_codes,
                                 const uint32_t* sorted_codes, const int32_t* perm, const int32_t* q_order,
-                                float eps, void* out, int32_t* idx_out, void* workspace, hipStream_t stream) {
+                                float eps, HistMean hm, void* out, int32_t* idx_out, void* workspace,
+                                hipStream_t stream) {
   const uint32_t* list_codes = nullptr;
   const int32_t* list_pos = nullptr;
   if (causal) {
@@ -254,14 +262,14 @@ hipError_t launch_select_attend(const void* q, const void* k, const void* v, boo
     uint2* keys_full = reinterpret_cast<uint2*>(wsb + fw.keys_full_off);
     uint2* keys_list = reinterpret_cast<uint2*>(wsb + fw.keys_list_off);
     return launch_select_attend_tile(q, k, v, S, N, dk, dv, topk, causal, q_codes, sorted_codes, perm, list_codes,
-                                     list_pos, q_order, eps, out, idx_out, bounds, keys_full, keys_list, stream);
+                                     list_pos, q_order, eps, hm, out, idx_out, bounds, keys_full, keys_list, stream);
   }
 #define ZETA_FUSED_CASE(DVV)                                                                                    \
   case DVV:                                                                                                     \
     return is_bf16 ? launch_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm,    \
-                                              list_codes, list_pos, q_order, eps, out, idx_out, stream)         \
+                                              list_codes, list_pos, q_order, eps, hm, out, idx_out, stream)     \
                    : launch_dk<float, DVV>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm,       \
-                                           list_codes, list_pos, q_order, eps, out, idx_out, stream);
+                                           list_codes, list_pos, q_order, eps, hm, out, idx_out, stream);
   switch (dv) {
     ZETA_FUSED_CASE(32)
     ZETA_FUSED_CASE(64)

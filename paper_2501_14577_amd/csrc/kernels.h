@@ -8,6 +8,24 @@
 
 namespace zeta {
 
+// The history-mean candidate (optional): float32 mean keys [S][N][d_k] and
+// mean values [S][N][d_v], row i holding query i's; both NULL when off.
+struct HistMean {
+  const float* k;
+  const float* v;
+};
+
+// History means of k and v (causal: rows 0..i; else all N rows) into
+// mean_k and mean_v.  Workspace: hist_ws(S, N, dk + dv).
+hipError_t launch_history_mean(const void* k, const void* v, bool is_bf16, int64_t S, int64_t N, int dk, int dv,
+                               bool causal, float* mean_k, float* mean_v, void* workspace, hipStream_t stream);
+
+// For two float32 matrices ([S][N][Da] and [S][N][Db]) at once: adds to
+// out[j] the sum of x[i] over i >= j (causal) or over all i, per segment and
+// column.  Workspace: hist_ws(S, N, Da + Db).
+hipError_t launch_history_spread(const float* xa, float* outa, int Da, const float* xb, float* outb, int Db, int64_t S,
+                                 int64_t N, bool causal, void* workspace, hipStream_t stream);
+
 // Encode: optional joint-range reduction, then quantise + interleave.
 // is_bf16: q and k hold bfloat16 bit patterns, else float32.
 hipError_t launch_encode(const void* q, const void* k, bool is_bf16, int64_t S, int64_t N, int dk,
@@ -51,27 +69,31 @@ bool tile_supports(int dv);
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
                                      int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out, int2* bounds,
-                                     uint2* keys_full, uint2* keys_list, hipStream_t stream);
+                                     const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
+                                     int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream);
 
 // Select and attend in one pass (idx_out optional).
 hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,
                                 int dk, int dv, int topk, bool causal, const uint32_t* q_codes,
                                 const uint32_t* sorted_codes, const int32_t* perm, const int32_t* q_order,
-                                float eps, void* out, int32_t* idx_out, void* workspace, hipStream_t stream);
+                                float eps, HistMean hm, void* out, int32_t* idx_out, void* workspace,
+                                hipStream_t stream);
 
-// Cauchy-softmax attention over the selected rows.
+// Cauchy-softmax attention over the selected rows (and the history-mean
+// candidate when hm is given).
 hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
                          int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
-                         float eps, void* out, hipStream_t stream);
+                         float eps, HistMean hm, void* out, hipStream_t stream);
 
 bool attend_supports(int dv);
 
-// Attention gradients for fixed windows (dq written, dk and dv accumulated
-// after being cleared, deps = one float).  Workspace: bwd_ws(S, N).
+// Attention gradients for fixed windows (dq, dk, dv written, deps = one
+// float); with hm, the history-mean candidate's share too, passed back to the
+// history's rows (causal: rows 0..i of query i).  Workspace:
+// bwd_ws(S, N, topk, dk, dv, hm given).
 hipError_t launch_attend_bwd(const void* q, const void* k, const void* v, const void* dout, bool is_bf16, int64_t S,
                              int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
-                             float eps, float* dq, float* dkg, float* dvg, float* deps, void* workspace,
-                             hipStream_t stream);
+                             float eps, HistMean hm, bool causal, float* dq, float* dkg, float* dvg, float* deps,
+                             void* workspace, hipStream_t stream);
 
 }  // namespace zeta

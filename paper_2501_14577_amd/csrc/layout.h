@@ -151,15 +151,38 @@ inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
+// ---- history mean ---------------------------------------------------------
+// Segmented scans over [S][N][D] matrices (values and keys together): rows
+// per chunk, and the most columns scanned at once (d_k + d_v).
+constexpr int64_t kHistRows = 32;
+constexpr int kHistMaxCols = kMaxDk + 256;
+
+// Per (segment, chunk, column) sums, turned in place into exclusive prefix
+// (or suffix) sums, and per (segment, column) totals.
+struct HistWs {
+  size_t sums_off, totals_off, bytes;
+};
+inline HistWs hist_ws(int64_t S, int64_t N, int D) {
+  HistWs w;
+  w.sums_off = 0;
+  w.totals_off = align_up(size_t(S) * size_t(ceil_div(N, kHistRows)) * size_t(D) * sizeof(float));
+  w.bytes = w.totals_off + align_up(size_t(S) * size_t(D) * sizeof(float));
+  return w;
+}
+
 // Attention gradients: per-query partial sums of the eps gradient and the
 // per-block sums of their fixed-order reduction; per query (Z_i, c_i); the
 // key of every window slot, the slots sorted by key (keys and the sort's
 // permutation); each key's run of sorted slots; the sort's own workspace.
+// With the history-mean candidate also the gradients reaching each query's
+// mean key and mean value (divided by the history's length) and the scan
+// that passes them back to the history's rows.
 struct BwdWs {
-  size_t part_off, block_off, zc_off, keys_off, sorted_off, slot_off, runs_off, sort_off, bytes;
+  size_t part_off, block_off, zc_off, keys_off, sorted_off, slot_off, runs_off, sort_off;
+  size_t hist_k_off, hist_v_off, hist_scan_off, bytes;
   int key_bits;  // bits of a slot key (keys run to N inclusive)
 };
-inline BwdWs bwd_ws(int64_t S, int64_t N, int topk) {
+inline BwdWs bwd_ws(int64_t S, int64_t N, int topk, int dk = 0, int dv = 0, bool history = false) {
   BwdWs w;
   const size_t rows = size_t(S) * size_t(N);
   const size_t slots = rows * size_t(topk);
@@ -173,7 +196,15 @@ inline BwdWs bwd_ws(int64_t S, int64_t N, int topk) {
   w.slot_off = w.sorted_off + align_up(slots * sizeof(uint32_t));
   w.runs_off = w.slot_off + align_up(slots * sizeof(int32_t));
   w.sort_off = w.runs_off + align_up(rows * 2 * sizeof(int32_t));
-  w.bytes = w.sort_off + sort_ws(S, N * topk, w.key_bits).bytes;
+  w.hist_k_off = w.sort_off + align_up(sort_ws(S, N * topk, w.key_bits).bytes);
+  w.hist_v_off = w.hist_k_off;
+  w.hist_scan_off = w.hist_k_off;
+  w.bytes = w.hist_k_off;
+  if (history) {
+    w.hist_v_off = w.hist_k_off + align_up(rows * size_t(dk) * sizeof(float));
+    w.hist_scan_off = w.hist_v_off + align_up(rows * size_t(dv) * sizeof(float));
+    w.bytes = w.hist_scan_off + hist_ws(S, N, dk + dv).bytes;
+  }
   return w;
 }
 

@@ -34,7 +34,9 @@
 // bfloat16 high part and a bfloat16 remainder, and both products are
 // accumulated, so the weights carry 16 significant bits and the products are
 // exact in the float32 accumulator.
-// The normaliser sums the float32 scores.
+// The normaliser sums the float32 scores.  The optional history-mean
+// candidate (Section 3.4, last paragraph) is each query's own row, so each
+// lane starts its accumulators and the normaliser from it, in float32.
 //
 // Operand layout of the 16x16x16 product (lane l, kg = l / 16):
 //   A (value columns x entries): lane l holds entries 4kg..4kg+3 of column
@@ -389,14 +391,15 @@ __global__ void __launch_bounds__(256)
 
 // ---- attention over the windows ----------------------------------------------
 
-template <int DV, int DK, bool kOff32>
+template <int DV, int DK, bool kOff32, bool kHist>
 __global__ void __launch_bounds__(kTileWaves * 64)
     select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                               const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
                               const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
                               const int2* __restrict__ bounds, const uint2* __restrict__ keys_full,
                               const uint2* __restrict__ keys_list, int64_t total, int64_t N, int dk_rt, int causal,
-                              int t0, int t_hi, int64_t cap, float eps, uint16_t* __restrict__ out) {
+                              int t0, int t_hi, int64_t cap, float eps, const float* __restrict__ mk,
+                              const float* __restrict__ mv, uint16_t* __restrict__ out) {
   constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
   constexpr int W = E / 2;    // 32-bit words per lane and row
   constexpr int KD = DK > 0 ? DK : kMaxDk;
@@ -466,10 +469,11 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 
       // A window outside the list (not produced by the bounds kernel) counts
       // as empty.
-      const bool mine = ((gmask >> qn) & 1u) != 0u && 0 <= my_a && my_a <= my_b && my_b < ln;
+      const bool in_grp = ((gmask >> qn) & 1u) != 0u;
+      const bool mine = in_grp && 0 <= my_a && my_a <= my_b && my_b < ln;
       const int32_t my_lim = causal ? my_i : int32_t(N - 1);
       float qv[KD];
-      if (mine) {
+      if (kHist ? in_grp : mine) {
         if constexpr (DK == 3) {
           Row3<uint16_t>::load(q, g_seg * N + my_i, total, qv);
         } else {
@@ -485,6 +489,27 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
       for (int j = 0; j < E; ++j) acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
       float zpart = 0.0f;
+      // The history-mean candidate starts the sums, in float32: its score
+      // (counted once, by the kg = 0 lanes) and its weighted mean value in
+      // this lane's output elements kg*4E .. kg*4E + 4E - 1.
+      if constexpr (kHist) {
+        if (in_grp) {
+          const int64_t gq = g_seg * N + my_i;
+          const float s_mean = mean_score<KD>(mk, gq, dk, qv, eps);
+          if (kg == 0) zpart = s_mean;
+          const float* mrow = mv + gq * DV + kg * 4 * E;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < E; j += 4) {
+              const float4 m = *reinterpret_cast<const float4*>(mrow + i * E + j);
+              acc[j][i] = s_mean * m.x;
+              acc[j + 1][i] = s_mean * m.y;
+              acc[j + 2][i] = s_mean * m.z;
+              acc[j + 3][i] = s_mean * m.w;
+            }
+        }
+      }
       const uint16_t* vseg = v + g_seg * N * DV;
       const uint16_t* kseg = k + g_seg * N * dk;
       const Off col = Off(qn * E);
@@ -654,7 +679,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       float z = zpart;
       z += __shfl_xor(z, 16, 64);
       z += __shfl_xor(z, 32, 64);
-      if (((gmask >> qn) & 1u) != 0u) {
+      if (in_grp) {
         const float inv = z > 0.0f ? 1.0f / z : 0.0f;
         float o[4 * E];
 #pragma unroll
@@ -680,21 +705,30 @@ template <int DV, int DK>
 hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
                          int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
                          const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
-                         float eps, uint16_t* out, hipStream_t stream) {
+                         float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   const int64_t tiles = ceil_div(total, kTileQ);
   const int64_t want = ceil_div(tiles, kTileWaves);
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
-  if (off32)
-    hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, true>), dim3(blocks), dim3(kTileWaves * 64), 0, stream, q,
-                       k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk, causal ? 1 : 0, lp.t0,
-                       lp.t_hi, lp.cap, eps, out);
-  else
-    hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, false>), dim3(blocks), dim3(kTileWaves * 64), 0, stream,
-                       q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk, causal ? 1 : 0,
-                       lp.t0, lp.t_hi, lp.cap, eps, out);
+#define ZETA_TILE_LAUNCH(OFF, HIST)                                                                                  \
+  hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST>), dim3(blocks), dim3(kTileWaves * 64), 0, stream, \
+                     q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk, causal ? 1 : 0,    \
+                     lp.t0, lp.t_hi, lp.cap, eps, hm.k, hm.v, out)
+  const bool hist = hm.k != nullptr;
+  if (off32) {
+    if (hist)
+      ZETA_TILE_LAUNCH(true, true);
+    else
+      ZETA_TILE_LAUNCH(true, false);
+  } else {
+    if (hist)
+      ZETA_TILE_LAUNCH(false, true);
+    else
+      ZETA_TILE_LAUNCH(false, false);
+  }
+#undef ZETA_TILE_LAUNCH
   return hipGetLastError();
 }
 
@@ -702,12 +736,12 @@ template <int DV>
 hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
                           int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
                           const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
-                          float eps, uint16_t* out, hipStream_t stream) {
+                          float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
   if (dk == 3)
     return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, keys_list,
-                                eps, out, stream);
+                                eps, hm, out, stream);
   return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, keys_list,
-                              eps, out, stream);
+                              eps, hm, out, stream);
 }
 
 }  // namespace
@@ -717,8 +751,8 @@ bool tile_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 2
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
                                      int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out, int2* bounds,
-                                     uint2* keys_full, uint2* keys_list, hipStream_t stream) {
+                                     const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
+                                     int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   if (dk == 3) {
@@ -744,7 +778,7 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
 #define ZETA_TILE_CASE(DVV) \
   case DVV:                 \
     return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, \
-                               keys_list, eps, oo, stream);
+                               keys_list, eps, hm, oo, stream);
   switch (dv) {
     ZETA_TILE_CASE(32)
     ZETA_TILE_CASE(64)

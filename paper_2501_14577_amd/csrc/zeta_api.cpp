@@ -1,5 +1,5 @@
-// C ABI of the Z-order top-k attention forward: argument validation on the
-// host, then the kernel launchers.  Validation touches no HIP runtime call, so
+// C ABI of the Z-order top-k attention and its gradients: argument
+// validation on the host, then the kernel launchers.  Validation touches no HIP runtime call, so
 // every error path can be exercised without a GPU.
 #include <math.h>
 
@@ -36,6 +36,13 @@ bool bad_count(int64_t B, int64_t H, int64_t N) {
   if (B < 1 || H < 1 || N < 1) return true;
   if (B > kMaxElems / H) return true;
   return !shape_ok(B * H, N);
+}
+
+// The history-mean rows are given together or not at all; mean values are
+// read with 16-byte loads.
+bool bad_means(const float* mean_k, const float* mean_v) {
+  if ((mean_k == nullptr) != (mean_v == nullptr)) return true;
+  return mean_v != nullptr && !aligned16(mean_v);
 }
 
 }  // namespace
@@ -107,32 +114,54 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
                                         idx, workspace, stream));
 }
 
+zeta_status_t zeta_history_mean(const void* k, const void* v, zeta_dtype_t dtype, int64_t B, int64_t H, int64_t N,
+                                int d_k, int d_v, int causal, float* mean_k, float* mean_v, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
+  if (!k || !v || !mean_k || !mean_v) return ZETA_ERR_INVALID_ARG;
+  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || d_v < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (!aligned16(v) || !aligned16(mean_v)) return ZETA_ERR_INVALID_ARG;
+  if (mean_k == mean_v || static_cast<const void*>(mean_k) == k || static_cast<const void*>(mean_v) == v)
+    return ZETA_ERR_INVALID_ARG;
+  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
+  if (d_k > zeta::kMaxDk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
+  const int64_t S = B * H;
+  const zeta::HistWs ws = zeta::hist_ws(S, N, d_k + d_v);
+  if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
+  return hip_status(zeta::launch_history_mean(k, v, dtype == ZETA_BF16, S, N, d_k, d_v, causal != 0, mean_k, mean_v,
+                                              workspace, stream));
+}
+
 zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
                                  int64_t H, int64_t N, int d_k, int d_v, int topk, const int32_t* idx,
-                                 const int32_t* q_order, float eps, void* out, hipStream_t stream) {
+                                 const int32_t* q_order, float eps, const float* mean_k, const float* mean_v,
+                                 void* out, hipStream_t stream) {
   if (!q || !k || !v || !idx || !out) return ZETA_ERR_INVALID_ARG;
   if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
   if (d_k < 1 || d_v < 1 || topk < 1) return ZETA_ERR_INVALID_ARG;
   if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
   if (!aligned16(v) || !aligned16(out)) return ZETA_ERR_INVALID_ARG;
   if (out == q || out == k || out == v) return ZETA_ERR_INVALID_ARG;
+  if (bad_means(mean_k, mean_v)) return ZETA_ERR_INVALID_ARG;
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
   return hip_status(zeta::launch_attend(q, k, v, dtype == ZETA_BF16, B * H, N, d_k, d_v, topk, idx, q_order, eps,
-                                        out, stream));
+                                        zeta::HistMean{mean_k, mean_v}, out, stream));
 }
 
 zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
                                      int64_t H, int64_t N, int d_k, int d_v, int topk, int causal,
                                      const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                                     const int32_t* q_order, float eps, void* out, int32_t* idx_out,
-                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                                     const int32_t* q_order, float eps, const float* mean_k, const float* mean_v,
+                                     void* out, int32_t* idx_out, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
   if (!q || !k || !v || !out || !q_codes || !sorted_codes || !perm) return ZETA_ERR_INVALID_ARG;
   if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
   if (d_k < 1 || d_v < 1 || topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
   if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
   if (!aligned16(v) || !aligned16(out)) return ZETA_ERR_INVALID_ARG;
   if (out == q || out == k || out == v) return ZETA_ERR_INVALID_ARG;
+  if (bad_means(mean_k, mean_v)) return ZETA_ERR_INVALID_ARG;
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
   const int64_t S = B * H;
@@ -146,35 +175,41 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
     if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
   }
   return hip_status(zeta::launch_select_attend(q, k, v, dtype == ZETA_BF16, S, N, d_k, d_v, topk, causal != 0, q_codes,
-                                               sorted_codes, perm, q_order, eps, out, idx_out, workspace, stream));
+                                               sorted_codes, perm, q_order, eps, zeta::HistMean{mean_k, mean_v}, out,
+                                               idx_out, workspace, stream));
 }
 
 zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B, int64_t H,
                                  int64_t N, int d_k, int d_v, int topk, const int32_t* idx, const int32_t* q_order,
-                                 const void* dout, float eps, float* dq, float* dk, float* dv, float* deps,
-                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                                 const void* dout, float eps, const float* mean_k, const float* mean_v, int causal,
+                                 float* dq, float* dk, float* dv, float* deps, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
   if (!q || !k || !v || !idx || !dout || !dq || !dk || !dv || !deps) return ZETA_ERR_INVALID_ARG;
   if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
-  if (d_k < 1 || d_v < 1 || topk < 1) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || d_v < 1 || topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
   if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
   if (!aligned16(v) || !aligned16(dout)) return ZETA_ERR_INVALID_ARG;
+  if (bad_means(mean_k, mean_v)) return ZETA_ERR_INVALID_ARG;
+  const bool history = mean_k != nullptr;
+  if (history && !aligned16(dv)) return ZETA_ERR_INVALID_ARG;
   // Outputs are distinct buffers, none of them an input.
   const void* outs[4] = {dq, dk, dv, deps};
-  const void* ins[6] = {q, k, v, dout, idx, q_order};
+  const void* ins[8] = {q, k, v, dout, idx, q_order, mean_k, mean_v};
   for (int a = 0; a < 4; ++a) {
     for (int b = a + 1; b < 4; ++b)
       if (outs[a] == outs[b]) return ZETA_ERR_INVALID_ARG;
-    for (int b = 0; b < 6; ++b)
-      if (outs[a] == ins[b]) return ZETA_ERR_INVALID_ARG;
+    for (int b = 0; b < 8; ++b)
+      if (ins[b] != nullptr && outs[a] == ins[b]) return ZETA_ERR_INVALID_ARG;
   }
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
   const int64_t S = B * H;
   if (N > zeta_max_bwd_slots() / topk) return ZETA_ERR_UNSUPPORTED;
-  const zeta::BwdWs ws = zeta::bwd_ws(S, N, topk);
+  const zeta::BwdWs ws = zeta::bwd_ws(S, N, topk, d_k, d_v, history);
   if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
   return hip_status(zeta::launch_attend_bwd(q, k, v, dout, dtype == ZETA_BF16, S, N, d_k, d_v, topk, idx, q_order, eps,
-                                            dq, dk, dv, deps, workspace, stream));
+                                            zeta::HistMean{mean_k, mean_v}, causal != 0, dq, dk, dv, deps, workspace,
+                                            stream));
 }
 
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk, int causal) {
@@ -186,17 +221,20 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
   const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
   const size_t ob = zeta::query_order_ws(S, N).bytes;
   const size_t fb = zeta::fused_ws(S, N, topk, causal ? 1 : 0).bytes;
+  const size_t hb = zeta::hist_ws(S, N, zeta::kHistMaxCols).bytes;
   if (fb > bytes) bytes = fb;
+  if (hb > bytes) bytes = hb;
   if (sb > bytes) bytes = sb;
   if (lb > bytes) bytes = lb;
   if (ob > bytes) bytes = ob;
   return bytes;
 }
 
-size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int topk) {
+size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk, int history_mean) {
   if (bad_count(B, H, N) || topk < 1 || topk > zeta::kMaxTopk) return 0;
+  if (d_k < 1 || d_k > zeta::kMaxDk || !zeta::attend_supports(d_v)) return 0;
   if (N > zeta_max_bwd_slots() / topk) return 0;
-  return zeta::bwd_ws(B * H, N, topk).bytes;
+  return zeta::bwd_ws(B * H, N, topk, d_k, d_v, history_mean != 0).bytes;
 }
 
 const char* zeta_status_string(zeta_status_t status) {

@@ -26,6 +26,7 @@ EXPORTED = (
     "zeta_select_topk",
     "zeta_topk_attn_fwd",
     "zeta_select_attend_fwd",
+    "zeta_history_mean",
     "zeta_topk_attn_bwd",
     "zeta_workspace_size",
     "zeta_bwd_workspace_size",
@@ -58,16 +59,17 @@ def load_library() -> ctypes.CDLL:
     L.zeta_sort_keys.argtypes = [vp, i64, i64, i32, vp, vp, vp, sz, vp]
     L.zeta_query_order.argtypes = [vp, i64, i64, i32, i32, vp, vp, sz, vp]
     L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp]
-    L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, f32, vp, vp]
+    L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, f32, vp, vp, vp, vp]
     L.zeta_select_attend_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, f32,
-                                         vp, vp, vp, sz, vp]
-    L.zeta_topk_attn_bwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, vp,
-                                     vp, sz, vp]
+                                         vp, vp, vp, vp, vp, sz, vp]
+    L.zeta_history_mean.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, sz, vp]
+    L.zeta_topk_attn_bwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, f32, vp, vp, i32,
+                                     vp, vp, vp, vp, vp, sz, vp]
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
-    L.zeta_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
+    L.zeta_bwd_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
     for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
-                 "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_topk_attn_bwd"):
+                 "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_history_mean", "zeta_topk_attn_bwd"):
         getattr(L, name).restype = ctypes.c_int
     L.zeta_workspace_size.restype = sz
     L.zeta_bwd_workspace_size.restype = sz
@@ -120,12 +122,12 @@ def workspace_for(B, H, N, d_k, bits, topk, causal, device) -> torch.Tensor:
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-def zeta_bwd_workspace_size(B: int, H: int, N: int, topk: int) -> int:
-    return int(load_library().zeta_bwd_workspace_size(B, H, N, topk))
+def zeta_bwd_workspace_size(B: int, H: int, N: int, d_k: int, d_v: int, topk: int, history_mean: bool) -> int:
+    return int(load_library().zeta_bwd_workspace_size(B, H, N, d_k, d_v, topk, int(bool(history_mean))))
 
 
-def bwd_workspace_for(B, H, N, topk, device) -> torch.Tensor:
-    n = max(zeta_bwd_workspace_size(B, H, N, topk), 256)
+def bwd_workspace_for(B, H, N, d_k, d_v, topk, history_mean, device) -> torch.Tensor:
+    n = max(zeta_bwd_workspace_size(B, H, N, d_k, d_v, topk, history_mean), 256)
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
@@ -211,29 +213,68 @@ def zeta_select_topk(q_codes: torch.Tensor, sorted_codes: torch.Tensor, perm: to
     return idx
 
 
+def _means(mean_k, mean_v):
+    if (mean_k is None) != (mean_v is None):
+        raise ValueError("mean_k and mean_v are given together")
+    for t in (mean_k, mean_v):
+        if t is not None and t.dtype != torch.float32:
+            raise ValueError("history means are float32")
+
+
+def zeta_history_mean(k: torch.Tensor, v: torch.Tensor, causal: bool, *, mean_k: Optional[torch.Tensor] = None,
+                      mean_v: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Mean key and mean value of each query's history -> (mean_k [B,H,N,d_k],
+    mean_v [B,H,N,d_v]) float32: rows 0..i when causal, all rows otherwise."""
+    B, H, N, dk = k.shape
+    dv = v.shape[-1]
+    f32 = dict(dtype=torch.float32, device=k.device)
+    mean_k = torch.empty((B, H, N, dk), **f32) if mean_k is None else mean_k
+    mean_v = torch.empty((B, H, N, dv), **f32) if mean_v is None else mean_v
+    if workspace is None:
+        workspace = workspace_for(B, H, N, dk, 1, 1, causal, k.device)
+    _need_device(k, v, mean_k, mean_v, workspace)
+    _means(mean_k, mean_v)
+    if k.dtype != v.dtype:
+        raise ValueError("k and v must share a dtype")
+    st = load_library().zeta_history_mean(_ptr(k), _ptr(v), _dtype_code(k), B, H, N, dk, dv, int(bool(causal)),
+                                          _ptr(mean_k), _ptr(mean_v), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(), _stream())
+    _check("zeta_history_mean", st)
+    return mean_k, mean_v
+
+
 def zeta_topk_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, eps: float, *,
-                       q_order: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Cauchy-softmax attention over idx -> out [B,H,N,d_v] in v's dtype."""
+                       q_order: Optional[torch.Tensor] = None, mean_k: Optional[torch.Tensor] = None,
+                       mean_v: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Cauchy-softmax attention over idx -> out [B,H,N,d_v] in v's dtype;
+    with mean_k and mean_v (``zeta_history_mean``) each window also holds the
+    history-mean candidate."""
     B, H, N, dk = q.shape
     dv = v.shape[-1]
     topk = idx.shape[-1]
     if out is None:
         out = torch.empty((B, H, N, dv), dtype=v.dtype, device=v.device)
-    _need_device(q, k, v, idx, q_order, out)
+    _need_device(q, k, v, idx, q_order, mean_k, mean_v, out)
+    _means(mean_k, mean_v)
     if not (q.dtype == k.dtype == v.dtype == out.dtype):
         raise ValueError("q, k, v and out must share a dtype")
     st = load_library().zeta_topk_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dk, dv, topk,
-                                           _ptr(idx), _ptr(q_order), float(eps), _ptr(out), _stream())
+                                           _ptr(idx), _ptr(q_order), float(eps), _ptr(mean_k), _ptr(mean_v),
+                                           _ptr(out), _stream())
     _check("zeta_topk_attn_fwd", st)
     return out
 
 
 def zeta_topk_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, dout: torch.Tensor,
-                       eps: float, *, q_order: Optional[torch.Tensor] = None, dq: Optional[torch.Tensor] = None,
+                       eps: float, *, q_order: Optional[torch.Tensor] = None, mean_k: Optional[torch.Tensor] = None,
+                       mean_v: Optional[torch.Tensor] = None, causal: bool = True, dq: Optional[torch.Tensor] = None,
                        dk: Optional[torch.Tensor] = None, dv: Optional[torch.Tensor] = None,
                        deps: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
     """Gradients of the attention over idx -> (dq, dk, dv, deps), float32:
-    dq, dk [B,H,N,d_k], dv [B,H,N,d_v], deps [1]."""
+    dq, dk [B,H,N,d_k], dv [B,H,N,d_v], deps [1].  With mean_k and mean_v
+    the history-mean candidate takes part, and ``causal`` says how its
+    history was formed."""
     B, H, N, dkk = q.shape
     dvv = v.shape[-1]
     topk = idx.shape[-1]
@@ -243,14 +284,16 @@ def zeta_topk_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
     dv = torch.empty((B, H, N, dvv), **f32) if dv is None else dv
     deps = torch.empty((1,), **f32) if deps is None else deps
     if workspace is None:
-        workspace = bwd_workspace_for(B, H, N, topk, q.device)
-    _need_device(q, k, v, idx, dout, q_order, dq, dk, dv, deps, workspace)
+        workspace = bwd_workspace_for(B, H, N, dkk, dvv, topk, mean_k is not None, q.device)
+    _need_device(q, k, v, idx, dout, q_order, mean_k, mean_v, dq, dk, dv, deps, workspace)
+    _means(mean_k, mean_v)
     if not (q.dtype == k.dtype == v.dtype == dout.dtype):
         raise ValueError("q, k, v and dout must share a dtype")
     if any(t.dtype != torch.float32 for t in (dq, dk, dv, deps)):
         raise ValueError("gradients are float32")
     st = load_library().zeta_topk_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dkk, dvv, topk,
-                                           _ptr(idx), _ptr(q_order), _ptr(dout), float(eps), _ptr(dq), _ptr(dk),
+                                           _ptr(idx), _ptr(q_order), _ptr(dout), float(eps), _ptr(mean_k),
+                                           _ptr(mean_v), int(bool(causal)), _ptr(dq), _ptr(dk),
                                            _ptr(dv), _ptr(deps), _ptr(workspace),
                                            workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_topk_attn_bwd", st)
@@ -259,7 +302,8 @@ def zeta_topk_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
 
 def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_codes: torch.Tensor,
                            sorted_codes: torch.Tensor, perm: torch.Tensor, topk: int, causal: bool, eps: float, *,
-                           q_order: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                           q_order: Optional[torch.Tensor] = None, mean_k: Optional[torch.Tensor] = None,
+                           mean_v: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                            idx_out: Optional[torch.Tensor] = None,
                            workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Select and attend in one pass -> out [B,H,N,d_v]; ``idx_out`` (int32
@@ -270,12 +314,14 @@ def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_
         out = torch.empty((B, H, N, dv), dtype=v.dtype, device=v.device)
     if workspace is None:
         workspace = workspace_for(B, H, N, dk, 1, topk, causal, q.device)
-    _need_device(q, k, v, q_codes, sorted_codes, perm, q_order, out, idx_out, workspace)
+    _need_device(q, k, v, q_codes, sorted_codes, perm, q_order, mean_k, mean_v, out, idx_out, workspace)
+    _means(mean_k, mean_v)
     if not (q.dtype == k.dtype == v.dtype == out.dtype):
         raise ValueError("q, k, v and out must share a dtype")
     st = load_library().zeta_select_attend_fwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dk, dv, topk,
                                                int(bool(causal)), _ptr(q_codes), _ptr(sorted_codes), _ptr(perm),
-                                               _ptr(q_order), float(eps), _ptr(out), _ptr(idx_out), _ptr(workspace),
+                                               _ptr(q_order), float(eps), _ptr(mean_k), _ptr(mean_v), _ptr(out),
+                                               _ptr(idx_out), _ptr(workspace),
                                                workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_select_attend_fwd", st)
     return out
@@ -283,13 +329,14 @@ def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_
 
 def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: float, causal: bool = True,
             bits: int = 10, *, workspace: Optional[torch.Tensor] = None, buffers: Optional[dict] = None,
-            zorder: bool = True, fused: bool = False, return_intermediates: bool = False):
+            zorder: bool = True, fused: bool = False, history: bool = False, return_intermediates: bool = False):
     """The whole forward: encode, sort, select, attend (four calls, one stream).
 
     The query codes are sorted together with the key codes (one call over
     2*B*H segments); their Z-order, regrouped by list level, drives select
     and attend (``zorder``).  ``fused`` runs select and attend as one pass.
-    The result is the same either way.  ``buffers`` (from ``alloc_buffers``)
+    The result is the same either way.  ``history`` adds the history-mean
+    candidate to every window.  ``buffers`` (from ``alloc_buffers``)
     holds preallocated outputs so that repeated calls allocate nothing.
     """
     B, H, N, dk = q.shape
@@ -306,15 +353,19 @@ def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: f
         sc, perm = zeta_sort_keys(kc, dk * bits, sorted_codes=b["sorted_codes2"][1], perm=b["perm2"][1],
                                   workspace=workspace)
         order = None
+    mk = mv = None
+    if history:
+        mk, mv = zeta_history_mean(k, v, causal, workspace=workspace)
     if fused:
         idx = b["idx"] if return_intermediates else None
-        out = zeta_select_attend_fwd(q, k, v, qc, sc, perm, topk, causal, eps, q_order=order, out=b["out"],
-                                     idx_out=idx, workspace=workspace)
+        out = zeta_select_attend_fwd(q, k, v, qc, sc, perm, topk, causal, eps, q_order=order, mean_k=mk, mean_v=mv,
+                                     out=b["out"], idx_out=idx, workspace=workspace)
     else:
         idx = zeta_select_topk(qc, sc, perm, topk, causal, q_order=order, idx=b["idx"], workspace=workspace)
-        out = zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, out=b["out"])
+        out = zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, mean_k=mk, mean_v=mv, out=b["out"])
     if return_intermediates:
-        return dict(q_codes=qc, k_codes=kc, sorted_codes=sc, perm=perm, q_order=order, idx=idx, out=out)
+        return dict(q_codes=qc, k_codes=kc, sorted_codes=sc, perm=perm, q_order=order, idx=idx, mean_k=mk,
+                    mean_v=mv, out=out)
     return out
 
 

@@ -21,6 +21,7 @@ P3 = ctypes.c_void_p(0x30000)
 P4 = ctypes.c_void_p(0x40000)
 NULL = None
 BIG = 1 << 40
+INV, UNS, WSP = zb.ZETA_ERR_INVALID_ARG, zb.ZETA_ERR_UNSUPPORTED, zb.ZETA_ERR_WORKSPACE
 
 
 def declared_symbols():
@@ -69,16 +70,53 @@ def test_workspace_size():
 
 def test_bwd_workspace_size():
     ws = zeta.zeta_bwd_workspace_size
-    assert ws(0, 1, 10, 4) == 0
-    assert ws(1, 1, 10, 0) == 0
-    assert ws(1, 1, 10, 1025) == 0
-    assert ws(1, 1, 1 << 22, 1024) == 0  # N * topk = 2^32 slots
+    assert ws(0, 1, 10, 3, 64, 4, 0) == 0
+    assert ws(1, 1, 10, 3, 64, 0, 0) == 0
+    assert ws(1, 1, 10, 3, 64, 1025, 0) == 0
+    assert ws(1, 1, 10, 9, 64, 4, 0) == 0
+    assert ws(1, 1, 10, 3, 48, 4, 0) == 0
+    assert ws(1, 1, 1 << 22, 3, 64, 1024, 0) == 0  # N * topk = 2^32 slots
     # Long-context shape: the window slots (keys, sorted keys, sorted slots:
-    # 3 x 16 x 65536 x 128 x 4 B) plus the slot sort's own buffers.
-    big = ws(1, 16, 65536, 128)
+    # 3 x 16 x 65536 x 128 x 4 B) plus the slot sort's own buffers; the
+    # history-mean candidate adds (3 + 128) x 4 B per row.
+    big = ws(1, 16, 65536, 3, 128, 128, 0)
     assert big >= 3 * 16 * 65536 * 128 * 4
     assert big % 256 == 0
-    assert ws(1, 1, 1, 1) > 0
+    assert ws(1, 16, 65536, 3, 128, 128, 1) >= big + 16 * 65536 * 131 * 4
+    assert ws(1, 1, 1, 1, 32, 1, 0) > 0
+
+
+def _hist(**kw):
+    a = dict(k=P, v=P2, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, causal=1,
+             mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0000), ws=ctypes.c_void_p(0x80000),
+             ws_bytes=BIG, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_history_mean(*a.values())
+
+
+HIST_CASES = [
+    (dict(k=NULL), INV), (dict(v=NULL), INV), (dict(mean_k=NULL), INV), (dict(mean_v=NULL), INV),
+    (dict(B=0), INV), (dict(N=0), INV), (dict(d_k=0), INV), (dict(d_v=0), INV), (dict(causal=2), INV),
+    (dict(v=ctypes.c_void_p(0x20008)), INV), (dict(mean_v=ctypes.c_void_p(0xC0004)), INV),
+    (dict(mean_v=ctypes.c_void_p(0xB0000)), INV),  # mean_v is mean_k
+    (dict(mean_k=P), INV),  # mean_k is k
+    (dict(dtype=4), UNS), (dict(d_k=9), UNS), (dict(d_v=100), UNS),
+    (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP),
+]
+
+
+@pytest.mark.parametrize("kw,code", HIST_CASES, ids=[str(c[0]) for c in HIST_CASES])
+def test_history_mean_rejects(kw, code):
+    assert _hist(**kw) == code
+
+
+def test_workspace_covers_history_mean():
+    # The forward workspace also serves zeta_history_mean at the widest d_v:
+    # float32 sums per (segment, chunk of 32 rows, column of k and v) and totals.
+    for B, H, N in ((1, 16, 65536), (32, 4, 2048), (1, 1, 1), (3, 1, 65)):
+        ws = zeta.zeta_workspace_size(B, H, N, 3, 10, 32, 1)
+        assert ws >= B * H * (-(-N // 32) + 1) * (8 + 256) * 4
+    assert _hist(d_v=256, ws_bytes=64) == WSP
 
 
 def _enc(**kw):
@@ -109,12 +147,10 @@ def _sel(**kw):
 
 def _att(**kw):
     a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, idx=P4,
-             q_order=NULL, eps=0.5, out=ctypes.c_void_p(0x50000), stream=NULL)
+             q_order=NULL, eps=0.5, mean_k=NULL, mean_v=NULL, out=ctypes.c_void_p(0x50000), stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_topk_attn_fwd(*a.values())
 
-
-INV, UNS, WSP = zb.ZETA_ERR_INVALID_ARG, zb.ZETA_ERR_UNSUPPORTED, zb.ZETA_ERR_WORKSPACE
 
 ENCODE_CASES = [
     (dict(q=NULL), INV), (dict(k=NULL), INV), (dict(q_codes=NULL), INV), (dict(k_codes=NULL), INV),
@@ -161,6 +197,9 @@ ATTEND_CASES = [
     (dict(eps=0.0), INV), (dict(eps=-1.0), INV), (dict(eps=float("inf")), INV), (dict(eps=float("nan")), INV),
     (dict(v=ctypes.c_void_p(0x30008)), INV), (dict(out=ctypes.c_void_p(0x50004)), INV), (dict(out=P3), INV),
     (dict(dtype=5), UNS), (dict(d_k=9), UNS), (dict(d_v=96), UNS), (dict(d_v=512), UNS), (dict(topk=2000), UNS),
+    (dict(mean_k=ctypes.c_void_p(0xB0000)), INV),  # history means come in pairs
+    (dict(mean_v=ctypes.c_void_p(0xC0000)), INV),
+    (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0004)), INV),  # mean_v misaligned
 ]
 
 
@@ -184,7 +223,8 @@ def test_query_order_rejects(kw, code):
 def _fused(**kw):
     a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, causal=1, q_codes=P4,
              sorted_codes=ctypes.c_void_p(0x60000), perm=ctypes.c_void_p(0x70000), q_order=NULL, eps=0.5,
-             out=ctypes.c_void_p(0x50000), idx_out=NULL, ws=ctypes.c_void_p(0x80000), ws_bytes=BIG, stream=NULL)
+             mean_k=NULL, mean_v=NULL, out=ctypes.c_void_p(0x50000), idx_out=NULL, ws=ctypes.c_void_p(0x80000),
+             ws_bytes=BIG, stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_select_attend_fwd(*a.values())
 
@@ -197,6 +237,8 @@ FUSED_CASES = [
     (dict(dtype=9), UNS), (dict(d_k=9), UNS), (dict(d_v=48), UNS), (dict(topk=1025), UNS),
     (dict(ws=NULL), WSP), (dict(ws_bytes=32), WSP),
     (dict(ws=ctypes.c_void_p(0x80008)), INV),  # bf16 one pass keeps 8-byte bounds in the workspace
+    (dict(mean_v=ctypes.c_void_p(0xC0000)), INV),
+    (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0008)), INV),
 ]
 
 
@@ -207,7 +249,8 @@ def test_select_attend_rejects(kw, code):
 
 def _bwd(**kw):
     a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, idx=P4, q_order=NULL,
-             dout=ctypes.c_void_p(0x50000), eps=0.5, dq=ctypes.c_void_p(0x60000), dk=ctypes.c_void_p(0x70000),
+             dout=ctypes.c_void_p(0x50000), eps=0.5, mean_k=NULL, mean_v=NULL, causal=1,
+             dq=ctypes.c_void_p(0x60000), dk=ctypes.c_void_p(0x70000),
              dv=ctypes.c_void_p(0x80000), deps=ctypes.c_void_p(0x90000), ws=ctypes.c_void_p(0xA0000), ws_bytes=BIG,
              stream=NULL)
     a.update(kw)
@@ -223,7 +266,10 @@ BWD_CASES = [
     (dict(dv=P3), INV),  # dv aliases v
     (dict(deps=P4), INV),  # deps aliases idx
     (dict(dtype=7), UNS), (dict(d_k=9), UNS), (dict(d_v=48), UNS), (dict(topk=1025), UNS),
-    (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP),
+    (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP), (dict(causal=2), INV),
+    (dict(mean_k=ctypes.c_void_p(0xB0000)), INV),
+    (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0000), dv=ctypes.c_void_p(0x80004)), INV),
+    (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0000), dq=ctypes.c_void_p(0xB0000)), INV),
 ]
 
 
