@@ -5,6 +5,7 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
 """
 
 from .zeta_oracle import (  # noqa: F401
+    SCORE_MODES,
     as_f32,
     attend,
     attend_bwd,
@@ -14,6 +15,7 @@ from .zeta_oracle import (  # noqa: F401
     interleave,
     joint_range,
     morton_encode,
+    pool_end,
     quantise,
     select_one,
     select_topk,

@@ -30,6 +30,10 @@ defines, one function per step, each citing the passage it follows:
    which ``attend`` and ``attend_bwd`` can append to every window as one more
    candidate (Section 3.4, last paragraph: the history mean appended to the
    top-k tokens with a cumulative sum, as smoothing).
+8. Variants: ``pool_end`` with a chunk size gives the paper's chunked causal
+   rule (Section 3.2.2; Algorithm 1, Step 4), and ``attend``'s ``mode`` the
+   score variants it compares with the Cauchy score (Section 4.3; Appendix
+   G.2; the dot-product softmax of equation 3).
 
 Readings where the paper is silent or ambiguous (each is also listed in the
 design notes):
@@ -186,14 +190,30 @@ def _window(p: int, pool_size: int, k: int) -> Tuple[int, int]:
     return s, m
 
 
-def select_one(q_code: int, k_codes: np.ndarray, i: int, k: int, causal: bool) -> np.ndarray:
+def pool_end(i: int, n: int, causal: bool, chunk: int = 0) -> int:
+    """One past the largest key position query i may see.
+
+    Exact causal prefix (chunk 0): i + 1, the diagonal included.  The paper's
+    chunked rule with chunk size M = chunk (Section 3.2.2; Algorithm 1, Step
+    4): the first floor(i / M) chunks of positions, i.e. positions below
+    floor(i / M) * M, so queries of the first chunk see no key.  Without
+    causality: n.
+    """
+    if not causal:
+        return n
+    if chunk > 0:
+        return (i // chunk) * chunk
+    return i + 1
+
+
+def select_one(q_code: int, k_codes: np.ndarray, i: int, k: int, causal: bool, chunk: int = 0) -> np.ndarray:
     """Window of one query, straight from the definition (no incremental state).
 
     k_codes: uint32 [N] of one segment; i: the query's position.  Returns
     int32 [k]: key positions in (code, position) order, padded with -1.
     """
     n = len(k_codes)
-    pool = np.arange(i + 1 if causal else n, dtype=np.int64)
+    pool = np.arange(pool_end(i, n, causal, chunk), dtype=np.int64)
     pc = k_codes[pool].astype(np.int64)
     order = pool[np.lexsort((pool, pc))]  # by code, then by position
     p = int(np.count_nonzero(pc < int(q_code)))
@@ -203,13 +223,15 @@ def select_one(q_code: int, k_codes: np.ndarray, i: int, k: int, causal: bool) -
     return out
 
 
-def select_topk(q_codes: np.ndarray, k_codes: np.ndarray, k: int, causal: bool) -> np.ndarray:
+def select_topk(q_codes: np.ndarray, k_codes: np.ndarray, k: int, causal: bool, chunk: int = 0) -> np.ndarray:
     """Windows of every query of every segment.
 
     q_codes, k_codes: uint32 [S, N].  Returns int32 [S, N, k].  The causal
-    case keeps the pool {0..i} as a sorted Python list of (code, position)
-    keys, adding key i before answering query i; the non-causal case sorts
-    all keys once.  Both give exactly what ``select_one`` gives.
+    case keeps the pool as a sorted Python list of (code, position) keys,
+    adding keys up to ``pool_end`` before answering each query (the pool only
+    grows with i); the non-causal case sorts all keys once.  Both give
+    exactly what ``select_one`` gives.  ``chunk`` > 0 selects the paper's
+    chunked causal rule (see ``pool_end``).
     """
     S, n = k_codes.shape
     idx = np.full((S, n, k), -1, dtype=np.int32)
@@ -219,9 +241,12 @@ def select_topk(q_codes: np.ndarray, k_codes: np.ndarray, k: int, causal: bool) 
         if causal:
             pool = []  # sorted keys code * 2^32 + position, i.e. (code, position) order
             for i in range(n):
-                bisect.insort(pool, (int(kc[i]) << 32) | i)
+                end = pool_end(i, n, True, chunk)
+                while len(pool) < end:
+                    j = len(pool)
+                    bisect.insort(pool, (int(kc[j]) << 32) | j)
                 p = bisect.bisect_left(pool, int(qc[i]) << 32)
-                s, m = _window(p, i + 1, k)
+                s, m = _window(p, end, k)
                 idx[seg, i, :m] = [e & 0xFFFFFFFF for e in pool[s:s + m]]
         else:
             order = np.argsort(kc, kind="stable")
@@ -258,9 +283,61 @@ def history_mean(k: np.ndarray, v: np.ndarray, causal: bool) -> Tuple[np.ndarray
     return mk, mv
 
 
+SCORE_MODES = ("cauchy", "dot", "neg_euclid", "inv_euclid", "norm_dot")
+
+
+def _variant_weights(mode: str, qr: np.ndarray, kr: np.ndarray, dist: np.ndarray, valid: np.ndarray, eps: float,
+                     mk: Optional[np.ndarray]):
+    """Unnormalised weights of the score variants compared in Section 4.3 and
+    Appendix G.2, over one block of windows (qr [b, d], kr [b, c, d], dist
+    [b, c] = ||q - k||^2), and of the history-mean candidate (mk [b, d]) or
+    None.
+
+      dot         softmax of q.k / sqrt(d)                    (equation 3)
+      neg_euclid  softmax of -||q - k||^2 / sqrt(d)
+      norm_dot    softmax of (q/|q|).(k/|k|) / sqrt(d)         (a zero vector stays zero)
+      inv_euclid  1 / (||q - k|| + eps)
+
+    Softmax weights are exponentials shifted by the row's largest logit
+    (the mean candidate's included), which leaves the normalised result
+    unchanged.
+    """
+    d = qr.shape[-1]
+
+    def unit(x):
+        n = np.linalg.norm(x, axis=-1, keepdims=True)
+        return x / np.where(n > 0, n, 1.0)
+
+    def terms(keys, dd):
+        if mode == "inv_euclid":
+            return 1.0 / (np.sqrt(dd) + eps)
+        if mode == "dot":
+            return np.einsum("bd,bcd->bc", qr, keys) / np.sqrt(d)
+        if mode == "neg_euclid":
+            return -dd / np.sqrt(d)
+        if mode == "norm_dot":
+            return np.einsum("bd,bcd->bc", unit(qr), unit(keys)) / np.sqrt(d)
+        raise ValueError(f"unknown score mode {mode!r}")
+
+    t = terms(kr, dist)
+    tm = None
+    if mk is not None:
+        dm = qr - mk
+        tm = terms(mk[:, None, :], np.sum(dm * dm, axis=-1)[:, None])[:, 0]
+    if mode == "inv_euclid":
+        return np.where(valid, t, 0.0), tm
+    zmax = np.max(np.where(valid, t, -np.inf), axis=1)
+    if tm is not None:
+        zmax = np.maximum(zmax, tm)
+    zmax = np.where(np.isfinite(zmax), zmax, 0.0)
+    w = np.where(valid, np.exp(t - zmax[:, None]), 0.0)
+    return w, (None if tm is None else np.exp(tm - zmax))
+
+
 def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: float,
            rows: Optional[np.ndarray] = None, block: int = 512,
-           mean_k: Optional[np.ndarray] = None, mean_v: Optional[np.ndarray] = None) -> np.ndarray:
+           mean_k: Optional[np.ndarray] = None, mean_v: Optional[np.ndarray] = None,
+           mode: str = "cauchy") -> np.ndarray:
     """o_i = sum_j S_ij v_j / sum_j S_ij with S_ij = 1 / (||q_i - k_j||^2 + eps).
 
     q, k: [S, N, dk]; v: [S, N, dv] (float values of any float dtype); idx:
@@ -271,6 +348,9 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: fl
     With ``mean_k`` and ``mean_v`` ([S, N, dk] and [S, N, dv], from
     ``history_mean``), row i's window gains one more candidate, the pair
     (mean_k[i], mean_v[i]), scored and normalised like the others.
+
+    ``mode`` picks the score: "cauchy" (equation cauchy, the method's own) or
+    one of the variants of ``_variant_weights``; the selection is the same.
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -288,12 +368,17 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: fl
             jj = np.where(valid, ii, 0)
             diff = q[seg, rr][:, None, :] - k[seg][jj]  # [b, k, dk]
             dist = np.sum(diff * diff, axis=-1)  # D_ij
-            score = np.where(valid, 1.0 / (dist + eps), 0.0)  # S_ij
+            mk = np.asarray(mean_k[seg, rr], dtype=np.float64) if with_mean else None
+            if mode == "cauchy":
+                score = np.where(valid, 1.0 / (dist + eps), 0.0)  # S_ij
+                if with_mean:
+                    dm = q[seg, rr] - mk
+                    sm = 1.0 / (np.sum(dm * dm, axis=-1) + eps)
+            else:
+                score, sm = _variant_weights(mode, q[seg, rr], k[seg][jj], dist, valid, eps, mk)
             z = score.sum(axis=1)  # Z_i
             num = np.einsum("bk,bkd->bd", score, v[seg][jj])
             if with_mean:  # the history-mean candidate
-                dm = q[seg, rr] - np.asarray(mean_k[seg, rr], dtype=np.float64)
-                sm = 1.0 / (np.sum(dm * dm, axis=-1) + eps)
                 z = z + sm
                 num = num + sm[:, None] * np.asarray(mean_v[seg, rr], dtype=np.float64)
             out[seg, r0:r0 + len(rr)] = num / z[:, None]
@@ -392,13 +477,14 @@ def attend_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps
 # ----------------------------------------------------------------------------
 
 def forward(q: np.ndarray, k: np.ndarray, v: np.ndarray, topk: int, eps: float, causal: bool,
-            bits: int, range_lohi=None, history: bool = False) -> dict:
+            bits: int, range_lohi=None, history: bool = False, chunk: int = 0, mode: str = "cauchy") -> dict:
     """All five steps for float32 inputs shaped [S, N, d]; returns every
-    intermediate.  ``history`` appends the history-mean candidate."""
+    intermediate.  ``history`` appends the history-mean candidate; ``chunk``
+    and ``mode`` pick the chunked causal rule and a score variant."""
     qc, kc, lo, hi = morton_encode(q, k, bits, range_lohi)
     sorted_codes, perm = sort_keys(kc)
-    idx = select_topk(qc, kc, topk, causal)
+    idx = select_topk(qc, kc, topk, causal, chunk=chunk)
     mk, mv = history_mean(k, v, causal) if history else (None, None)
-    out = attend(q, k, v, idx, eps, mean_k=mk, mean_v=mv)
+    out = attend(q, k, v, idx, eps, mean_k=mk, mean_v=mv, mode=mode)
     return dict(q_codes=qc, k_codes=kc, lo=lo, hi=hi, sorted_codes=sorted_codes, perm=perm,
                 idx=idx, mean_k=mk, mean_v=mv, out=out)

@@ -374,6 +374,161 @@ def check_attend_bwd_invariants(orc):
 
 
 # ----------------------------------------------------------------------------
+# The paper's chunked causal rule (Section 3.2.2; Algorithm 1, Step 4)
+# ----------------------------------------------------------------------------
+
+def check_select_chunk_golden(orc):
+    """The hand-worked example in golden/select_chunk_example.txt."""
+    rows = {}
+    want = {}
+    for line in open(os.path.join(GOLDEN, "select_chunk_example.txt")):
+        if line.strip() and not line.startswith("#"):
+            key, *vals = line.split()
+            if key == "row":
+                want[int(vals[0])] = [int(x) for x in vals[1:]]
+            else:
+                rows[key] = [int(x) for x in vals]
+    chunk, k = rows["chunk"][0], rows["k"][0]
+    kc = np.array([rows["k_codes"]], dtype=np.uint32)
+    qc = np.array([rows["q_codes"]], dtype=np.uint32)
+    idx = orc.select_topk(qc, kc, k, True, chunk=chunk)
+    for i, w in want.items():
+        assert list(idx[0, i]) == w, (i, list(idx[0, i]), w)
+        assert list(orc.select_one(int(qc[0, i]), kc[0], i, k, True, chunk=chunk)) == w, i
+
+
+def check_select_chunk_brute(orc):
+    """Brute force on tiny inputs: query i's pool is every key whose chunk
+    index j // M is below the query's own i // M; the window is the rank
+    window of the definition over that pool, in (code, position) order."""
+    rng = np.random.default_rng(61)
+    for n, M, k, bits in ((13, 3, 4, 2), (20, 4, 5, 3), (9, 1, 3, 2), (16, 16, 4, 2), (11, 20, 2, 2), (30, 7, 8, 2)):
+        kc = rng.integers(0, 1 << bits, size=(1, n)).astype(np.uint32)
+        qc = rng.integers(0, 1 << bits, size=(1, n)).astype(np.uint32)
+        idx = orc.select_topk(qc, kc, k, True, chunk=M)
+        for i in range(n):
+            pool = sorted((int(kc[0, j]), j) for j in range(n) if j // M < i // M)
+            p = sum(1 for c, _ in pool if c < int(qc[0, i]))
+            m = min(k, len(pool))
+            st = min(max(p - k // 2, 0), len(pool) - m)
+            want = [j for _, j in pool[st:st + m]] + [-1] * (k - m)
+            assert list(idx[0, i]) == want, (n, M, k, i, list(idx[0, i]), want)
+
+
+def check_select_chunk_invariants(orc):
+    """Queries of the first chunk see nothing; the queries of one chunk share
+    one pool (so a common query code gives a common window); M = 1 is the
+    exact prefix without the diagonal."""
+    rng = np.random.default_rng(62)
+    n, k = 64, 6
+    kc = rng.integers(0, 16, size=(2, n)).astype(np.uint32)
+    qc = rng.integers(0, 16, size=(2, n)).astype(np.uint32)
+    for M in (5, 8, 64, 100):
+        idx = orc.select_topk(qc, kc, k, True, chunk=M)
+        assert np.all(idx[:, :min(M, n)] == -1), M
+        same = np.broadcast_to(qc[:, :1], qc.shape).copy()
+        idx_same = orc.select_topk(same, kc, k, True, chunk=M)
+        for i in range(n):
+            first = (i // M) * M
+            assert np.array_equal(idx_same[:, i], idx_same[:, first]), (M, i)
+            assert np.all(idx[:, i][idx[:, i] >= 0] < first), (M, i)
+    one = orc.select_topk(qc, kc, k, True, chunk=1)
+    for s in range(2):
+        for i in range(1, n):
+            pool = sorted((int(kc[s, j]), j) for j in range(i))
+            p = sum(1 for c, _ in pool if c < int(qc[s, i]))
+            m = min(k, len(pool))
+            st = min(max(p - k // 2, 0), len(pool) - m)
+            assert list(one[s, i, :m]) == [j for _, j in pool[st:st + m]], (s, i)
+
+
+# ----------------------------------------------------------------------------
+# Score variants (Section 4.3; Appendix G.2; equation 3)
+# ----------------------------------------------------------------------------
+
+def check_attend_modes_hand(orc):
+    """Two candidates, q = (1,0,0), k_0 = (1,0,0), k_1 = (0,1,0), v = (1, 0),
+    d = 3, eps = 1: each variant's output is the weight of k_0, in closed form."""
+    import math
+    q = np.array([[[1.0, 0.0, 0.0]]])
+    k = np.array([[[1.0, 0.0, 0.0], [0.0, 1.0, 0.0]]])
+    v = np.array([[[1.0], [0.0]]])
+    idx = np.array([[[0, 1]]], dtype=np.int32)
+    r3 = math.sqrt(3.0)
+    want = {
+        "dot": 1.0 / (1.0 + math.exp(-1.0 / r3)),  # logits 1/sqrt(3) and 0
+        "norm_dot": 1.0 / (1.0 + math.exp(-1.0 / r3)),  # unit vectors: as dot
+        "neg_euclid": 1.0 / (1.0 + math.exp(-2.0 / r3)),  # distances 0 and 2
+        "inv_euclid": 1.0 / (1.0 + 1.0 / (math.sqrt(2.0) + 1.0)),  # 1/(0+1) and 1/(sqrt(2)+1)
+        "cauchy": 1.0 / (1.0 + 1.0 / 3.0),  # 1/(0+1) and 1/(2+1)
+    }
+    for mode, w in want.items():
+        got = float(orc.attend(q, k, v, idx, 1.0, mode=mode)[0, 0, 0])
+        assert abs(got - w) < 1e-14, (mode, got, w)
+
+
+def check_attend_modes_dense_limit(orc):
+    """Softmax variants with every key in the window (k >= N, causal) equal
+    masked softmax attention over the full score matrix (scipy's softmax of
+    q K^T / sqrt(d), -D / sqrt(d) or the cosine matrix / sqrt(d))."""
+    from scipy.special import softmax
+    rng = np.random.default_rng(66)
+    n, d, dv = 40, 3, 5
+    q = rng.normal(size=(1, n, d))
+    k = rng.normal(size=(1, n, d))
+    v = rng.normal(size=(1, n, dv))
+    qc, kc, _, _ = orc.morton_encode(q.astype(np.float32), k.astype(np.float32), 6)
+    idx = orc.select_topk(qc, kc, n, True)
+    mask = np.tril(np.ones((n, n), dtype=bool))
+    qu = q[0] / np.linalg.norm(q[0], axis=1, keepdims=True)
+    ku = k[0] / np.linalg.norm(k[0], axis=1, keepdims=True)
+    d2 = ((q[0][:, None, :] - k[0][None, :, :]) ** 2).sum(-1)
+    logits = {"dot": q[0] @ k[0].T / np.sqrt(d), "neg_euclid": -d2 / np.sqrt(d), "norm_dot": qu @ ku.T / np.sqrt(d)}
+    for mode, z in logits.items():
+        want = softmax(np.where(mask, z, -np.inf), axis=1) @ v[0]
+        got = orc.attend(q, k, v, idx, 0.5, mode=mode)[0]
+        assert np.allclose(got, want, atol=1e-12), mode
+
+
+def check_attend_modes_invariants(orc):
+    """neg_euclid on keys of one norm equals dot with the query doubled
+    (-|q - k|^2 = 2 q.k - |q|^2 - |k|^2, the last two constant per row);
+    norm_dot ignores the lengths of q and k; inv_euclid with a huge eps is
+    the window mean; no variant depends on the history mean's place."""
+    rng = np.random.default_rng(67)
+    n, d, dv, kk = 30, 3, 4, 6
+    q = rng.normal(size=(1, n, d))
+    k = rng.normal(size=(1, n, d))
+    k_sphere = 1.7 * k / np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.normal(size=(1, n, dv))
+    qc, kc, _, _ = orc.morton_encode(q.astype(np.float32), k.astype(np.float32), 6)
+    idx = orc.select_topk(qc, kc, kk, True)
+    a = orc.attend(q, k_sphere, v, idx, 0.5, mode="neg_euclid")
+    b = orc.attend(2.0 * q, k_sphere, v, idx, 0.5, mode="dot")
+    assert np.allclose(a, b, atol=1e-12)
+    scale_q = rng.uniform(0.2, 5.0, size=(1, n, 1))
+    scale_k = rng.uniform(0.2, 5.0, size=(1, n, 1))
+    a = orc.attend(q, k, v, idx, 0.5, mode="norm_dot")
+    b = orc.attend(q * scale_q, k * scale_k, v, idx, 0.5, mode="norm_dot")
+    assert np.allclose(a, b, atol=1e-12)
+    big = orc.attend(q, k, v, idx, 1e13, mode="inv_euclid")[0]
+    for i in range(n):
+        sel = idx[0, i][idx[0, i] >= 0]
+        assert np.allclose(big[i], v[0][sel].mean(axis=0), atol=1e-9), i
+    # The history-mean candidate is one more key/value pair in every variant.
+    mk, mv = orc.history_mean(k, v, True)
+    k2 = np.concatenate([k, mk], axis=1)
+    v2 = np.concatenate([v, mv], axis=1)
+    idx2 = np.concatenate([idx, n + np.arange(n, dtype=np.int32)[None, :, None]], axis=2)
+    q2 = np.concatenate([q, np.ones_like(q)], axis=1)
+    idx2 = np.concatenate([idx2, np.zeros((1, n, kk + 1), dtype=np.int32)], axis=1)
+    for mode in orc.SCORE_MODES:
+        want = orc.attend(q2, k2, v2, idx2, 0.5, mode=mode)[:, :n]
+        got = orc.attend(q, k, v, idx, 0.5, mean_k=mk, mean_v=mv, mode=mode)
+        assert np.allclose(got, want, atol=1e-12), mode
+
+
+# ----------------------------------------------------------------------------
 # History-mean candidate (Section 3.4, last paragraph)
 # ----------------------------------------------------------------------------
 
@@ -511,6 +666,12 @@ ALL_PINS = [
     check_attend_bwd_golden,
     check_attend_bwd_finite_diff,
     check_attend_bwd_invariants,
+    check_attend_modes_hand,
+    check_attend_modes_dense_limit,
+    check_attend_modes_invariants,
+    check_select_chunk_golden,
+    check_select_chunk_brute,
+    check_select_chunk_invariants,
     check_history_mean_golden,
     check_history_mean_brute,
     check_history_attend_augmented,

@@ -29,10 +29,9 @@ MUTATIONS = {
     "window leans right": ("s = min(max(p - k // 2, 0), pool_size - m)",
                            "s = min(max(p - (k + 1) // 2, 0), pool_size - m)"),
     "window truncated at end": ("s = min(max(p - k // 2, 0), pool_size - m)", "s = max(p - k // 2, 0)"),
-    "diagonal excluded": ("                bisect.insort(pool, (int(kc[i]) << 32) | i)\n"
-                          "                p = bisect.bisect_left(pool, int(qc[i]) << 32)\n",
-                          "                p = bisect.bisect_left(pool, int(qc[i]) << 32)\n"
-                          "                bisect.insort(pool, (int(kc[i]) << 32) | i)\n"),
+    "diagonal excluded": ("    return i + 1\n", "    return i\n"),
+    "chunk rule keeps own chunk": ("        return (i // chunk) * chunk\n", "        return min(n, (i // chunk + 1) * chunk)\n"),
+    "chunk rule off by one": ("        return (i // chunk) * chunk\n", "        return (i // chunk) * chunk + 1\n"),
     "distance not squared": ("dist = np.sum(diff * diff, axis=-1)", "dist = np.sqrt(np.sum(diff * diff, axis=-1))"),
     "eps squared": ("score = np.where(valid, 1.0 / (dist + eps), 0.0)",
                     "score = np.where(valid, 1.0 / (dist + eps * eps), 0.0)"),
@@ -55,6 +54,14 @@ MUTATIONS = {
                               "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]  # [b, k, dk]"),
     "bwd: query minus wrong row": ("diff = q[seg, rr][:, None, :] - k[seg][jj]  # q_i - k_j",
                                    "diff = q[seg, rr][:, None, :] - k[seg][rr][:, None, :]  # q_i - k_j"),
+    "dot: no 1/sqrt(d)": ('return np.einsum("bd,bcd->bc", qr, keys) / np.sqrt(d)',
+                          'return np.einsum("bd,bcd->bc", qr, keys)'),
+    "neg_euclid: sign": ("return -dd / np.sqrt(d)", "return dd / np.sqrt(d)"),
+    "norm_dot: keys not normalised": ('return np.einsum("bd,bcd->bc", unit(qr), unit(keys)) / np.sqrt(d)',
+                                      'return np.einsum("bd,bcd->bc", unit(qr), keys) / np.sqrt(d)'),
+    "inv_euclid: squared distance": ("return 1.0 / (np.sqrt(dd) + eps)", "return 1.0 / (dd + eps)"),
+    "softmax: padding not masked": ("w = np.where(valid, np.exp(t - zmax[:, None]), 0.0)",
+                                    "w = np.exp(t - zmax[:, None])"),
     "history: sums instead of means": ("return np.cumsum(k, axis=1) / count, np.cumsum(v, axis=1) / count",
                                        "return np.cumsum(k, axis=1), np.cumsum(v, axis=1)"),
     "history: current row excluded": ("return np.cumsum(k, axis=1) / count, np.cumsum(v, axis=1) / count",
