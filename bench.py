@@ -140,13 +140,14 @@ def main() -> int:
                     help="segments in the oracle sample (0 skips the CPU baseline)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (for counter calibration)")
-    ap.add_argument("--parts", default="forward,backward,history",
+    ap.add_argument("--parts", default="forward,backward,history,variants",
                     help="comma list of the parts to time: forward (the metric), backward (attention gradients), "
-                         "history (the history-mean candidate, forward and gradients); fields of parts not "
-                         "timed are null, so that each part's profile holds only its own kernels")
+                         "history (the history-mean candidate, forward and gradients), variants (the chunked "
+                         "causal rule and the score variants); fields of parts not timed are null, so that each "
+                         "part's profile holds only its own kernels")
     args = ap.parse_args()
     parts = set(args.parts.split(","))
-    if not parts <= {"forward", "backward", "history"}:
+    if not parts <= {"forward", "backward", "history", "variants"}:
         print(f"unknown part in --parts {args.parts}", file=sys.stderr)
         return 2
 
@@ -296,6 +297,39 @@ def main() -> int:
         if ev is not None:
             ev[1].record()
 
+    # Variants: the paper's chunked causal rule with 32 chunks (the one-pass
+    # step), and each score variant's one-pass call (per-query kernels).
+    variants = None
+    if "variants" in parts:
+        chunk = w.N // 32
+
+        def step_chunked(ev=None):
+            qc, kc = zeta.zeta_morton_encode(q, k, w.bits, q_codes=codes[0], k_codes=codes[1], workspace=ws)
+            zeta.zeta_sort_keys(codes, w.code_bits, sorted_codes=sorted2, perm=perm2, workspace=ws)
+            order = zeta.zeta_query_order(perm2[0], w.N, w.segments, w.topk, causal, order_out=bufs["order"],
+                                          workspace=ws)
+            if ev is not None:
+                ev[0].record()
+            zeta.zeta_select_attend_fwd(q, k, v, qc, sorted2[1], perm2[1], w.topk, causal, eps, chunk=chunk,
+                                        q_order=order, out=bufs["out"], workspace=ws)
+            if ev is not None:
+                ev[1].record()
+
+        chunk_step_ms, chunk_call_ms, _ = timed(step_chunked)
+        step_fused()
+        modes = {}
+        for mode in ("dot", "neg_euclid", "inv_euclid", "norm_dot"):
+            def call(ev=None, mode=mode):
+                if ev is not None:
+                    ev[0].record()
+                zeta.zeta_select_attend_fwd(q, k, v, codes[0], sorted2[1], perm2[1], w.topk, causal, eps, score=mode,
+                                            q_order=bufs["order"], out=bufs["out"], workspace=ws)
+                if ev is not None:
+                    ev[1].record()
+            modes[mode] = timed(call)[1]
+        variants = {"chunk": chunk, "chunked_step_ms": chunk_step_ms, "chunked_value": w.B * w.N / (chunk_step_ms * 1e-3),
+                    "chunked_select_attend_ms": chunk_call_ms, "score_select_attend_ms": modes}
+
     h_bytes = w.segments * w.N * (w.dk + w.dv) * (elem_size(w.dtype) + 4)  # read k, v once; write the means
     if "history" in parts:
         hist_ms = timed(hist_means)[1]
@@ -381,6 +415,7 @@ def main() -> int:
             "means_frac": frac(h_bytes, hist_ms),
             "backward_ms": hist_bwd_ms,
         },
+        "variants": variants,
         "step_hbm_frac": frac(s_bytes, ms_per_step),
         "step_algorithmic_bytes": s_bytes,
         "query_rows_per_s": per_s(w.segments * w.N, ms_per_step),

@@ -60,6 +60,26 @@ typedef enum {
 
 typedef enum { ZETA_F32 = 0, ZETA_BF16 = 1 } zeta_dtype_t;
 
+/*
+ * Attention scores over the selected candidates.  ZETA_SCORE_CAUCHY is the
+ * method's Adaptive Cauchy-Softmax (Section 3.3, equation cauchy); the others
+ * are the variants the paper compares it with (Section 4.3; Appendix G.2;
+ * the dot-product softmax of equation 3), each normalised over the window:
+ *   DOT         softmax of q.k / sqrt(d_k)
+ *   NEG_EUCLID  softmax of -||q - k||^2 / sqrt(d_k)
+ *   INV_EUCLID  weights 1 / (||q - k|| + eps)
+ *   NORM_DOT    softmax of (q/|q|).(k/|k|) / sqrt(d_k)  (a zero vector gives 0)
+ * Softmax weights are shifted by the window's largest logit.  Only the
+ * Cauchy score has gradients (zeta_topk_attn_bwd).
+ */
+typedef enum {
+  ZETA_SCORE_CAUCHY = 0,
+  ZETA_SCORE_DOT = 1,
+  ZETA_SCORE_NEG_EUCLID = 2,
+  ZETA_SCORE_INV_EUCLID = 3,
+  ZETA_SCORE_NORM_DOT = 4
+} zeta_score_t;
+
 /* Largest supported values of the size parameters. */
 #define ZETA_MAX_DK 8
 #define ZETA_MAX_TOPK 1024
@@ -144,7 +164,10 @@ zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64
  * query to past keys; Algorithm 1, Steps 3-5).
  *
  * For query i the pool is {0..i} when causal (the diagonal included) and all
- * N keys otherwise.  Let T be the pool in (code, position) order, L = |pool|,
+ * N keys otherwise.  With chunk = M > 0 (causal only) the pool follows the
+ * paper's chunked rule instead (Section 3.2.2; Algorithm 1, Step 4): the
+ * first floor(i / M) chunks of M positions, i.e. positions below
+ * floor(i / M) * M, so queries of the first chunk get no candidate.  Let T be the pool in (code, position) order, L = |pool|,
  * p = number of pool keys whose code is below the query's code,
  * m = min(topk, L) and s = min(max(p - floor(topk/2), 0), L - m).  Then
  * idx[seg][i][0..m) = positions of T[s .. s+m) in that order, and the rest of
@@ -159,12 +182,13 @@ zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64
  *                 gives neighbouring queries overlapping windows and makes the
  *                 call faster.  Entries outside 0..N-1 are skipped.
  *   idx           int32 [n_segments][N][topk] output, indexed by position.
- *   topk          1..ZETA_MAX_TOPK; causal 0 or 1.
+ *   topk          1..ZETA_MAX_TOPK; causal 0 or 1; chunk 0 (exact prefix) or
+ *                 a chunk size M >= 1 (requires causal; INVALID_ARG otherwise).
  */
 zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes,
                                const int32_t* perm, int64_t n_segments, int64_t N, int topk,
-                               int causal, const int32_t* q_order, int32_t* idx, void* workspace,
-                               size_t workspace_bytes, hipStream_t stream);
+                               int causal, int chunk, const int32_t* q_order, int32_t* idx,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * zeta_topk_attn_fwd -- Adaptive Cauchy-softmax attention over each query's
@@ -177,7 +201,8 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  * With mean_k and mean_v (both given, or both NULL) every window gains the
  * history-mean candidate of Section 3.4: the pair (mean_k[i], mean_v[i])
  * scored and normalised like the other candidates (a row with no valid
- * entry then attends to it alone).
+ * entry then attends to it alone).  `score` picks the Cauchy score or one of
+ * the variants of zeta_score_t (same candidates, other weights).
  *
  *   q, k   [B][H][N][d_k], v [B][H][N][d_v], out [B][H][N][d_v], all `dtype`.
  *   idx      int32 [B*H][N][topk]; valid entries (0 <= j < N) first, then -1.
@@ -185,7 +210,9 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  *            zeta_select_topk (NULL: position order).  Neighbouring queries
  *            of zeta_query_order's order gather mostly the same value rows,
  *            which then come from cache; the output bits do not depend on it.
- *   eps      gamma^2: finite and > 0.
+ *   score    a zeta_score_t (UNSUPPORTED otherwise).
+ *   eps      gamma^2: finite and > 0 (read by the Cauchy and inverse
+ *            Euclidean scores).
  *   mean_k, mean_v  optional float32 [B*H][N][d_k] and [B*H][N][d_v] (as
  *            zeta_history_mean writes them); mean_v 16-byte aligned.
  *
@@ -194,8 +221,8 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  */
 zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
                                  int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
-                                 const int32_t* idx, const int32_t* q_order, float eps,
-                                 const float* mean_k, const float* mean_v, void* out,
+                                 const int32_t* idx, const int32_t* q_order, zeta_score_t score,
+                                 float eps, const float* mean_k, const float* mean_v, void* out,
                                  hipStream_t stream);
 
 /*
@@ -212,10 +239,12 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
  * accumulation).  The output agrees with the two calls to float32 rounding,
  * and a query's bits depend only on its own window, so they are the same for
  * every processing order.  The history-mean candidate, when given, is added
- * per query in float32.
+ * per query in float32.  The score variants and float32 inputs take the
+ * per-query path.
  *
- *   q, k, v, dtype, B, H, N, d_k, d_v, topk, eps, mean_k, mean_v, out: as
- *            for zeta_topk_attn_fwd; causal as for zeta_select_topk.
+ *   q, k, v, dtype, B, H, N, d_k, d_v, topk, score, eps, mean_k, mean_v,
+ *            out: as for zeta_topk_attn_fwd; causal and chunk as for
+ *            zeta_select_topk.
  *   q_codes, sorted_codes, perm, q_order: as for zeta_select_topk.
  *   idx_out  optional int32 [B*H][N][topk]: receives the windows, exactly as
  *            zeta_select_topk writes them.
@@ -223,8 +252,9 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
  */
 zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
                                      int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
-                                     int causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
-                                     const int32_t* perm, const int32_t* q_order, float eps,
+                                     int causal, int chunk, const uint32_t* q_codes,
+                                     const uint32_t* sorted_codes, const int32_t* perm,
+                                     const int32_t* q_order, zeta_score_t score, float eps,
                                      const float* mean_k, const float* mean_v, void* out,
                                      int32_t* idx_out, void* workspace, size_t workspace_bytes,
                                      hipStream_t stream);
@@ -279,8 +309,9 @@ zeta_status_t zeta_history_mean(const void* k, const void* v, zeta_dtype_t dtype
  *   workspace  at least zeta_bwd_workspace_size(B, H, N, d_k, d_v, topk,
  *            means given) bytes (it holds one key per window slot and their
  *            sorted copy).
- * Every output element is written (rows without candidates and keys in no
- * window get zeros).  No atomics: dk and dv are summed per key after a stable
+ * The gradients are those of the Cauchy score.  Every output element is
+ * written (rows without candidates and keys in no window get zeros).  No
+ * atomics: dk and dv are summed per key after a stable
  * sort of the window slots by key, so every output is bit-identical from run
  * to run and for every q_order.  N * topk above 2^31 - 1 is UNSUPPORTED.  The
  * outputs must be distinct buffers and none may be an input (INVALID_ARG).

@@ -351,6 +351,8 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: fl
 
     ``mode`` picks the score: "cauchy" (equation cauchy, the method's own) or
     one of the variants of ``_variant_weights``; the selection is the same.
+    A row with no candidate at all (an empty pool under the chunked rule) is
+    zero.
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -381,7 +383,8 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, eps: fl
             if with_mean:  # the history-mean candidate
                 z = z + sm
                 num = num + sm[:, None] * np.asarray(mean_v[seg, rr], dtype=np.float64)
-            out[seg, r0:r0 + len(rr)] = num / z[:, None]
+            zs = np.where(z > 0, z, 1.0)  # a row without candidates is zero
+            out[seg, r0:r0 + len(rr)] = num / zs[:, None]
     return out
 
 

@@ -1,6 +1,8 @@
 // Adaptive Cauchy-softmax attention over each query's selected keys
 // (Section 3.3, equation cauchy; Section 3.4; Appendix E.1 steps 1-4):
-//   S_ij = 1 / (||q_i - k_j||^2 + eps),  o_i = sum_j S_ij v_j / sum_j S_ij.
+//   S_ij = 1 / (||q_i - k_j||^2 + eps),  o_i = sum_j S_ij v_j / sum_j S_ij,
+// or one of the score variants the paper compares it with (Section 4.3;
+// Appendix G.2): the same weighted sum with other weights.
 //
 // One wavefront per query.  d_k is 3, so scores are a handful of scalar FMAs
 // per candidate and there is no dense contraction for the matrix cores: the
@@ -38,7 +40,7 @@ template <typename T, int DV, int DK, bool kOff32>
 __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
     attend_kernel(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                   const int32_t* __restrict__ idx, const int32_t* __restrict__ q_order, int64_t total,
-                  int64_t N, int dk_rt, int topk, float eps, const float* __restrict__ mk,
+                  int64_t N, int dk_rt, int topk, int score, float eps, const float* __restrict__ mk,
                   const float* __restrict__ mv, T* __restrict__ out) {
   constexpr int kE = Vec16<T>::kElems;  // elements per lane load
   constexpr int kLpr = DV / kE;         // lanes per value row
@@ -47,7 +49,10 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
   constexpr int kRowBytes = DV * int(sizeof(T));
   static_assert(kLpr >= 1 && kLpr <= 64 && 64 % kLpr == 0, "row must split evenly over lanes");
   using Off = typename RowOff<kOff32>::type;
+  constexpr int KD = DK > 0 ? DK : kMaxDk;
   const int dk = DK > 0 ? DK : dk_rt;
+  const float rsd = 1.0f / sqrtf(float(dk));
+  const bool softmax = score_is_softmax(score);
 
   extern __shared__ unsigned char s_raw[];
   const int lane = threadIdx.x & 63;
@@ -82,8 +87,13 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
 
     // Phase 1: scores.  Lane l takes the slot pair (2l, 2l+1) of every block
     // of 128 slots, reading both indices with one 8-byte load when the row
-    // is 8-byte aligned (even topk).
+    // is 8-byte aligned (even topk).  The softmax variants store logits here
+    // and exponentiate once the window's largest is known.
+    const float qn = score == kScoreNormDot ? row_norm<KD>(qv, dk) : 0.0f;
     float zsum = 0.0f;
+    float zloc = -INFINITY;
+    uint32_t okmask = 0u;
+    int bit = 0;
     int m = 0;  // one past the last valid slot
     const int32_t* irow = idx + g * topk;
     for (int c0 = 2 * lane; c0 < topk; c0 += 128) {
@@ -97,7 +107,7 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
         jj[1] = c0 + 1 < topk ? irow[c0 + 1] : -1;
       }
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+      for (int h = 0; h < 2; ++h, ++bit) {
         const int c = c0 + h;
         const int32_t j = jj[h];
         const bool ok = c < topk && j >= 0 && j < N;
@@ -111,15 +121,21 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
             for (int a = 0; a < (DK > 0 ? DK : kMaxDk); ++a)
               kv[a] = a < dk ? Elem<T>::load(kseg + int64_t(j) * dk + a) : 0.0f;
           }
-          float d2 = 0.0f;
+          if (score == kScoreCauchy) {
+            float d2 = 0.0f;
 #pragma unroll
-          for (int a = 0; a < (DK > 0 ? DK : kMaxDk); ++a) {
-            if (a < dk) {
-              const float diff = qv[a] - kv[a];
-              d2 = fmaf(diff, diff, d2);
+            for (int a = 0; a < (DK > 0 ? DK : kMaxDk); ++a) {
+              if (a < dk) {
+                const float diff = qv[a] - kv[a];
+                d2 = fmaf(diff, diff, d2);
+              }
             }
+            s = 1.0f / (d2 + eps);
+          } else {
+            s = variant_term<KD>(score, qv, kv, dk, eps, rsd, qn);
+            zloc = fmaxf(zloc, s);
+            okmask |= 1u << bit;
           }
-          s = 1.0f / (d2 + eps);
           m = c + 1;
         }
         if (c < topk) {
@@ -129,12 +145,29 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
         zsum += s;
       }
     }
-    zsum = wave_sum(zsum);
     m = wave_max(m);
     float s_mean = 0.0f;
-    if (mk != nullptr) {
-      s_mean = mean_score<(DK > 0 ? DK : kMaxDk)>(mk, g, dk, qv, eps);
-      zsum += s_mean;
+    if (!softmax) {
+      zsum = wave_sum(zsum);
+      if (mk != nullptr) {
+        if (score == kScoreCauchy) {
+          s_mean = mean_score<KD>(mk, g, dk, qv, eps);
+        } else {
+          float mkv[KD];
+#pragma unroll
+          for (int a = 0; a < KD; ++a) mkv[a] = a < dk ? mk[g * dk + a] : 0.0f;
+          s_mean = variant_term<KD>(score, qv, mkv, dk, eps, rsd, qn);
+        }
+        zsum += s_mean;
+      }
+    } else {
+      if (mk != nullptr) {
+        float mkv[KD];
+#pragma unroll
+        for (int a = 0; a < KD; ++a) mkv[a] = a < dk ? mk[g * dk + a] : 0.0f;
+        s_mean = variant_term<KD>(score, qv, mkv, dk, eps, rsd, qn);
+      }
+      zsum = softmax_weights(s_w, topk, lane, okmask, zloc, mk != nullptr, s_mean);
     }
     wave_lds_sync();
 
@@ -187,8 +220,8 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
 
 template <typename T, int DV, int DK>
 hipError_t launch_attend_t(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk,
-                           int topk, const int32_t* idx, const int32_t* q_order, float eps, HistMean hm, void* out,
-                           hipStream_t stream) {
+                           int topk, const int32_t* idx, const int32_t* q_order, int score, float eps, HistMean hm,
+                           void* out, hipStream_t stream) {
   const int64_t total = S * N;
   const int64_t want = ceil_div(total, kAttWavesPerBlock);
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
@@ -197,20 +230,20 @@ hipError_t launch_attend_t(const void* q, const void* k, const void* v, int64_t 
   if (off32)
     hipLaunchKernelGGL((attend_kernel<T, DV, DK, true>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx,
-                       q_order, total, N, dk, topk, eps, hm.k, hm.v, static_cast<T*>(out));
+                       q_order, total, N, dk, topk, score, eps, hm.k, hm.v, static_cast<T*>(out));
   else
     hipLaunchKernelGGL((attend_kernel<T, DV, DK, false>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx,
-                       q_order, total, N, dk, topk, eps, hm.k, hm.v, static_cast<T*>(out));
+                       q_order, total, N, dk, topk, score, eps, hm.k, hm.v, static_cast<T*>(out));
   return hipGetLastError();
 }
 
 template <typename T, int DV>
 hipError_t launch_attend_dk(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk,
-                            int topk, const int32_t* idx, const int32_t* q_order, float eps, HistMean hm, void* out,
-                            hipStream_t stream) {
-  if (dk == 3) return launch_attend_t<T, DV, 3>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream);
-  return launch_attend_t<T, DV, 0>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream);
+                            int topk, const int32_t* idx, const int32_t* q_order, int score, float eps, HistMean hm,
+                            void* out, hipStream_t stream) {
+  if (dk == 3) return launch_attend_t<T, DV, 3>(q, k, v, S, N, dk, topk, idx, q_order, score, eps, hm, out, stream);
+  return launch_attend_t<T, DV, 0>(q, k, v, S, N, dk, topk, idx, q_order, score, eps, hm, out, stream);
 }
 
 }  // namespace
@@ -219,12 +252,13 @@ bool attend_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv ==
 
 hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
                          int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
-                         float eps, HistMean hm, void* out, hipStream_t stream) {
+                         int score, float eps, HistMean hm, void* out, hipStream_t stream) {
 #define ZETA_ATTEND_CASE(DVV)                                                                            \
   case DVV:                                                                                              \
     return is_bf16                                                                                       \
-               ? launch_attend_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream) \
-               : launch_attend_dk<float, DVV>(q, k, v, S, N, dk, topk, idx, q_order, eps, hm, out, stream);
+               ? launch_attend_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, idx, q_order, score, eps, hm, out, \
+                                                 stream)                                                 \
+               : launch_attend_dk<float, DVV>(q, k, v, S, N, dk, topk, idx, q_order, score, eps, hm, out, stream);
   switch (dv) {
     ZETA_ATTEND_CASE(32)
     ZETA_ATTEND_CASE(64)

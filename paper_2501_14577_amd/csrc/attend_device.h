@@ -123,6 +123,81 @@ __device__ __forceinline__ float mean_score(const float* __restrict__ mk, int64_
   return 1.0f / (d2 + eps);
 }
 
+// Score variants (Section 4.3; Appendix G.2; equation 3) over the same
+// candidates.  mode: 1 dot-product softmax, 2 negative-Euclidean softmax,
+// 3 inverse Euclidean, 4 normalised dot-product softmax (the Cauchy score,
+// mode 0, is computed inline by the kernels).  Returns the weight itself
+// (inverse Euclidean: 1 / (|q - k| + eps)) or the logit of a softmax
+// (q.k / sqrt(d), -|q - k|^2 / sqrt(d), (q/|q|).(k/|k|) / sqrt(d); a zero
+// vector gives 0).  rsd = 1 / sqrt(d); qn = |q|.
+template <int KD>
+__device__ __forceinline__ float variant_term(int mode, const float* qv, const float* kv, int dk, float eps, float rsd,
+                                              float qn) {
+  float d2 = 0.0f, dot = 0.0f, kk = 0.0f;
+#pragma unroll
+  for (int a = 0; a < KD; ++a) {
+    if (a < dk) {
+      const float diff = qv[a] - kv[a];
+      d2 = fmaf(diff, diff, d2);
+      dot = fmaf(qv[a], kv[a], dot);
+      kk = fmaf(kv[a], kv[a], kk);
+    }
+  }
+  switch (mode) {
+    case 1:
+      return dot * rsd;
+    case 2:
+      return -d2 * rsd;
+    case 3:
+      return 1.0f / (sqrtf(d2) + eps);
+    default: {
+      const float kn = sqrtf(kk);
+      return (qn > 0.0f && kn > 0.0f) ? dot / (qn * kn) * rsd : 0.0f;
+    }
+  }
+}
+
+// |q| of a query row (for the normalised dot product).
+template <int KD>
+__device__ __forceinline__ float row_norm(const float* qv, int dk) {
+  float s = 0.0f;
+#pragma unroll
+  for (int a = 0; a < KD; ++a)
+    if (a < dk) s = fmaf(qv[a], qv[a], s);
+  return sqrtf(s);
+}
+
+// Softmax variants: turns this lane's logits s_w[c] into exp(z - zmax) over
+// the slots it scored (slot pairs 2*lane, 2*lane + 1 of every 128; bit b of
+// okmask marks its b-th slot valid; zloc is its largest valid logit), and the
+// history-mean candidate's logit into its weight; returns the wavefront's
+// sum of the weights.  zmax is the largest logit of the window and the
+// candidate (0 when there is none).
+__device__ __forceinline__ float softmax_weights(float* s_w, int topk, int lane, uint32_t okmask, float zloc,
+                                                 bool has_mean, float& s_mean) {
+  float zmax = wave_max_f(zloc);
+  if (has_mean) zmax = fmaxf(zmax, s_mean);
+  if (!(zmax > -INFINITY)) zmax = 0.0f;
+  float zs = 0.0f;
+  int b = 0;
+  for (int c0 = 2 * lane; c0 < topk; c0 += 128) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h, ++b) {
+      if ((okmask >> b) & 1u) {
+        const float e = expf(s_w[c0 + h] - zmax);
+        s_w[c0 + h] = e;
+        zs += e;
+      }
+    }
+  }
+  float z = wave_sum(zs);
+  if (has_mean) {
+    s_mean = expf(s_mean - zmax);
+    z += s_mean;
+  }
+  return z;
+}
+
 // acc[e] += s * mean value row elements [0, n) at p (16-byte aligned float32).
 template <int n>
 __device__ __forceinline__ void add_mean_value(const float* __restrict__ p, float s, float* acc) {

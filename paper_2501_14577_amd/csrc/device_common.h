@@ -30,6 +30,12 @@ __device__ __forceinline__ int wave_max(int x) {
   return x;
 }
 
+__device__ __forceinline__ float wave_max_f(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+  return x;
+}
+
 // Orders this wave's earlier LDS writes before its later LDS reads (lanes of
 // one wavefront exchanging data through LDS without a block barrier).
 __device__ __forceinline__ void wave_lds_sync() {

@@ -10,7 +10,8 @@
 // scores the candidates and gathers their value rows exactly as the attend
 // kernel does (same lane mapping, same fused multiply-adds), so the output
 // bits equal those of select followed by attend.  The index row is written
-// only when the caller asks for it.
+// only when the caller asks for it.  The score variants (Section 4.3;
+// Appendix G.2) run here for both dtypes.
 #include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -29,9 +30,9 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
                          const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
                          const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                          const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
-                         int64_t N, int dk_rt, int topk, int causal, int t0, int t_hi, int64_t cap, float eps,
-                         const float* __restrict__ mk, const float* __restrict__ mv, T* __restrict__ out,
-                         int32_t* __restrict__ idx_out) {
+                         int64_t N, int dk_rt, int topk, int causal, int chunk, int t0, int t_hi, int64_t cap,
+                         int score, float eps, const float* __restrict__ mk, const float* __restrict__ mv,
+                         T* __restrict__ out, int32_t* __restrict__ idx_out) {
   constexpr int kE = Vec16<T>::kElems;
   constexpr int kLpr = DV / kE;
   constexpr int kGroups = 64 / kLpr;
@@ -39,7 +40,10 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
   constexpr int kRowBytes = DV * int(sizeof(T));
   static_assert(kLpr >= 1 && kLpr <= 64 && 64 % kLpr == 0, "row must split evenly over lanes");
   using Off = typename RowOff<kOff32>::type;
+  constexpr int KD = DK > 0 ? DK : kMaxDk;
   const int dk = DK > 0 ? DK : dk_rt;
+  const float rsd = 1.0f / sqrtf(float(dk));
+  const bool softmax = score_is_softmax(score);
 
   extern __shared__ unsigned char s_raw[];
   const int lane = threadIdx.x & 63;
@@ -84,14 +88,18 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
       const int64_t g = seg * N + i;
 
       // Window.
-      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap);
-      const int32_t p = (L.codes == prev_codes && key >= prev_key) ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
-                                                                   : wave_lower_bound(L.codes, 0, L.n, key, lane);
-      prev_codes = L.codes;
-      prev_key = key;
-      prev_p = p;
-      int got_l, got_r;
-      select_window(L, p, topk, lbuf, rbuf, lane, got_l, got_r);
+      const QueryList L =
+          query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap, chunk);
+      int got_l = 0, got_r = 0;
+      if (L.n > 0) {  // an empty pool (the chunked rule's first chunk) selects nothing
+        const int32_t p = (L.codes == prev_codes && key >= prev_key)
+                              ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
+                              : wave_lower_bound(L.codes, 0, L.n, key, lane);
+        prev_codes = L.codes;
+        prev_key = key;
+        prev_p = p;
+        select_window(L, p, topk, lbuf, rbuf, lane, got_l, got_r);
+      }
       wave_lds_sync();
       const int m = got_l + got_r;
       if (idx_out != nullptr) {
@@ -116,10 +124,14 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
 #pragma unroll
         for (int a = 0; a < (DK > 0 ? DK : kMaxDk); ++a) qv[a] = a < dk ? Elem<T>::load(q + g * dk + a) : 0.0f;
       }
+      const float qn = score == kScoreNormDot ? row_norm<KD>(qv, dk) : 0.0f;
       float zsum = 0.0f;
+      float zloc = -INFINITY;
+      uint32_t okmask = 0u;
+      int bit = 0;
       for (int c0 = 2 * lane; c0 < topk; c0 += 128) {
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < 2; ++h, ++bit) {
           const int c = c0 + h;
           const bool ok = c < m;
           float s = 0.0f;
@@ -134,15 +146,21 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
               for (int a = 0; a < (DK > 0 ? DK : kMaxDk); ++a)
                 kv[a] = a < dk ? Elem<T>::load(kseg + int64_t(j) * dk + a) : 0.0f;
             }
-            float d2 = 0.0f;
+            if (score == kScoreCauchy) {
+              float d2 = 0.0f;
 #pragma unroll
-            for (int a = 0; a < (DK > 0 ? DK : kMaxDk); ++a) {
-              if (a < dk) {
-                const float diff = qv[a] - kv[a];
-                d2 = fmaf(diff, diff, d2);
+              for (int a = 0; a < (DK > 0 ? DK : kMaxDk); ++a) {
+                if (a < dk) {
+                  const float diff = qv[a] - kv[a];
+                  d2 = fmaf(diff, diff, d2);
+                }
               }
+              s = 1.0f / (d2 + eps);
+            } else {
+              s = variant_term<KD>(score, qv, kv, dk, eps, rsd, qn);
+              zloc = fmaxf(zloc, s);
+              okmask |= 1u << bit;
             }
-            s = 1.0f / (d2 + eps);
           }
           if (c < topk) {
             s_off[c] = Off(j) * Off(kRowBytes);
@@ -151,11 +169,28 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
           zsum += s;
         }
       }
-      zsum = wave_sum(zsum);
       float s_mean = 0.0f;
-      if (mk != nullptr) {
-        s_mean = mean_score<(DK > 0 ? DK : kMaxDk)>(mk, g, dk, qv, eps);
-        zsum += s_mean;
+      if (!softmax) {
+        zsum = wave_sum(zsum);
+        if (mk != nullptr) {
+          if (score == kScoreCauchy) {
+            s_mean = mean_score<KD>(mk, g, dk, qv, eps);
+          } else {
+            float mkv[KD];
+#pragma unroll
+            for (int a = 0; a < KD; ++a) mkv[a] = a < dk ? mk[g * dk + a] : 0.0f;
+            s_mean = variant_term<KD>(score, qv, mkv, dk, eps, rsd, qn);
+          }
+          zsum += s_mean;
+        }
+      } else {
+        if (mk != nullptr) {
+          float mkv[KD];
+#pragma unroll
+          for (int a = 0; a < KD; ++a) mkv[a] = a < dk ? mk[g * dk + a] : 0.0f;
+          s_mean = variant_term<KD>(score, qv, mkv, dk, eps, rsd, qn);
+        }
+        zsum = softmax_weights(s_w, topk, lane, okmask, zloc, mk != nullptr, s_mean);
       }
       wave_lds_sync();
 
@@ -207,9 +242,9 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
 
 template <typename T, int DV, int DK>
 hipError_t launch_t(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int topk, bool causal,
-                    const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                    const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, float eps, HistMean hm,
-                    void* out, int32_t* idx_out, hipStream_t stream) {
+                    int chunk, const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                    const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, int score, float eps,
+                    HistMean hm, void* out, int32_t* idx_out, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   const int64_t runs = ceil_div(total, kFusedRun);
@@ -220,34 +255,34 @@ hipError_t launch_t(const void* q, const void* k, const void* v, int64_t S, int6
   if (off32)
     hipLaunchKernelGGL((select_attend_kernel<T, DV, DK, true>), dim3(blocks), dim3(kFusedWaves * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), q_codes,
-                       sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, lp.t0,
-                       lp.t_hi, lp.cap, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
+                       sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, chunk, lp.t0,
+                       lp.t_hi, lp.cap, score, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
   else
     hipLaunchKernelGGL((select_attend_kernel<T, DV, DK, false>), dim3(blocks), dim3(kFusedWaves * 64), lds, stream,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), q_codes,
-                       sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, lp.t0,
-                       lp.t_hi, lp.cap, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
+                       sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, chunk, lp.t0,
+                       lp.t_hi, lp.cap, score, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
   return hipGetLastError();
 }
 
 template <typename T, int DV>
 hipError_t launch_dk(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int topk, bool causal,
-                     const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                     const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, float eps,
+                     int chunk, const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                     const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order, int score, float eps,
                      HistMean hm, void* out, int32_t* idx_out, hipStream_t stream) {
   if (dk == 3)
-    return launch_t<T, DV, 3>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
-                              q_order, eps, hm, out, idx_out, stream);
-  return launch_t<T, DV, 0>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm, list_codes, list_pos,
-                            q_order, eps, hm, out, idx_out, stream);
+    return launch_t<T, DV, 3>(q, k, v, S, N, dk, topk, causal, chunk, q_codes, sorted_codes, perm, list_codes,
+                              list_pos, q_order, score, eps, hm, out, idx_out, stream);
+  return launch_t<T, DV, 0>(q, k, v, S, N, dk, topk, causal, chunk, q_codes, sorted_codes, perm, list_codes, list_pos,
+                            q_order, score, eps, hm, out, idx_out, stream);
 }
 
 }  // namespace
 
 hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,
-                                int dk, int dv, int topk, bool causal, const uint32_t* q_codes,
+                                int dk, int dv, int topk, bool causal, int chunk, const uint32_t* q_codes,
                                 const uint32_t* sorted_codes, const int32_t* perm, const int32_t* q_order,
-                                float eps, HistMean hm, void* out, int32_t* idx_out, void* workspace,
+                                int score, float eps, HistMean hm, void* out, int32_t* idx_out, void* workspace,
                                 hipStream_t stream) {
   const uint32_t* list_codes = nullptr;
   const int32_t* list_pos = nullptr;
@@ -255,21 +290,22 @@ hipError_t launch_select_attend(const void* q, const void* k, const void* v, boo
     const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
     if (e != hipSuccess) return e;
   }
-  if (is_bf16 && tile_supports(dv)) {
+  if (is_bf16 && tile_supports(dv) && score == kScoreCauchy) {
     const FusedWs fw = fused_ws(S, N, topk, causal ? 1 : 0);
     char* wsb = static_cast<char*>(workspace);
     int2* bounds = reinterpret_cast<int2*>(wsb + fw.bounds_off);
     uint2* keys_full = reinterpret_cast<uint2*>(wsb + fw.keys_full_off);
     uint2* keys_list = reinterpret_cast<uint2*>(wsb + fw.keys_list_off);
-    return launch_select_attend_tile(q, k, v, S, N, dk, dv, topk, causal, q_codes, sorted_codes, perm, list_codes,
-                                     list_pos, q_order, eps, hm, out, idx_out, bounds, keys_full, keys_list, stream);
+    return launch_select_attend_tile(q, k, v, S, N, dk, dv, topk, causal, chunk, q_codes, sorted_codes, perm,
+                                     list_codes, list_pos, q_order, eps, hm, out, idx_out, bounds, keys_full,
+                                     keys_list, stream);
   }
-#define ZETA_FUSED_CASE(DVV)                                                                                    \
-  case DVV:                                                                                                     \
-    return is_bf16 ? launch_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm,    \
-                                              list_codes, list_pos, q_order, eps, hm, out, idx_out, stream)     \
-                   : launch_dk<float, DVV>(q, k, v, S, N, dk, topk, causal, q_codes, sorted_codes, perm,       \
-                                           list_codes, list_pos, q_order, eps, hm, out, idx_out, stream);
+#define ZETA_FUSED_CASE(DVV)                                                                                       \
+  case DVV:                                                                                                        \
+    return is_bf16 ? launch_dk<uint16_t, DVV>(q, k, v, S, N, dk, topk, causal, chunk, q_codes, sorted_codes, perm, \
+                                              list_codes, list_pos, q_order, score, eps, hm, out, idx_out, stream) \
+                   : launch_dk<float, DVV>(q, k, v, S, N, dk, topk, causal, chunk, q_codes, sorted_codes, perm,    \
+                                           list_codes, list_pos, q_order, score, eps, hm, out, idx_out, stream);
   switch (dv) {
     ZETA_FUSED_CASE(32)
     ZETA_FUSED_CASE(64)

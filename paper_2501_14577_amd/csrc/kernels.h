@@ -8,6 +8,13 @@
 
 namespace zeta {
 
+// Attention scores: the method's Cauchy score and the variants compared with
+// it (the values match zeta_score_t).
+enum ScoreMode : int { kScoreCauchy = 0, kScoreDot = 1, kScoreNegEuclid = 2, kScoreInvEuclid = 3, kScoreNormDot = 4 };
+__host__ __device__ inline bool score_is_softmax(int mode) {
+  return mode == kScoreDot || mode == kScoreNegEuclid || mode == kScoreNormDot;
+}
+
 // The history-mean candidate (optional): float32 mean keys [S][N][d_k] and
 // mean values [S][N][d_v], row i holding query i's; both NULL when off.
 struct HistMean {
@@ -48,10 +55,11 @@ hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int
 hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int topk, bool causal, int32_t* order_out,
                               void* workspace, hipStream_t stream);
 
-// Causal prefix lists (when needed) and the window of every query.  q_order:
+// Causal prefix lists (when needed) and the window of every query.  chunk:
+// 0 for the exact causal prefix, M for the paper's chunked rule.  q_order:
 // optional processing order (a permutation of 0..N-1 per segment).
 hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                         int64_t S, int64_t N, int topk, bool causal, const int32_t* q_order, int32_t* idx,
+                         int64_t S, int64_t N, int topk, bool causal, int chunk, const int32_t* q_order, int32_t* idx,
                          void* workspace, hipStream_t stream);
 
 // Doubling prefix lists of causal selection in the workspace (none when
@@ -67,23 +75,25 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
 // tiles.
 bool tile_supports(int dv);
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
-                                     int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
+                                     int topk, bool causal, int chunk, const uint32_t* q_codes,
+                                     const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
                                      const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
                                      int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream);
 
-// Select and attend in one pass (idx_out optional).
+// Select and attend in one pass (idx_out optional); score: a ScoreMode (the
+// matrix-core tiles serve the Cauchy score of bfloat16 inputs).
 hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,
-                                int dk, int dv, int topk, bool causal, const uint32_t* q_codes,
+                                int dk, int dv, int topk, bool causal, int chunk, const uint32_t* q_codes,
                                 const uint32_t* sorted_codes, const int32_t* perm, const int32_t* q_order,
-                                float eps, HistMean hm, void* out, int32_t* idx_out, void* workspace,
+                                int score, float eps, HistMean hm, void* out, int32_t* idx_out, void* workspace,
                                 hipStream_t stream);
 
 // Cauchy-softmax attention over the selected rows (and the history-mean
 // candidate when hm is given).
 hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
                          int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
-                         float eps, HistMean hm, void* out, hipStream_t stream);
+                         int score, float eps, HistMean hm, void* out, hipStream_t stream);
 
 bool attend_supports(int dv);
 

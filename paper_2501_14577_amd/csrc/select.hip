@@ -155,7 +155,7 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
     select_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
                   const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                   const int32_t* __restrict__ list_pos, int64_t total, int64_t N, int topk, int causal,
-                  int t0, int t_hi, int64_t cap, const int32_t* __restrict__ order,
+                  int chunk, int t0, int t_hi, int64_t cap, const int32_t* __restrict__ order,
                   int32_t* __restrict__ idx) {
   extern __shared__ int32_t s_sel[];
   const int lane = threadIdx.x & 63;
@@ -195,14 +195,18 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
       const int64_t seg = slot / N;
       const int64_t g = seg * N + i;
 
-      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap);
-      const int32_t p = (L.codes == prev_codes && key >= prev_key) ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
-                                                                   : wave_lower_bound(L.codes, 0, L.n, key, lane);
-      prev_codes = L.codes;
-      prev_key = key;
-      prev_p = p;
-      int got_l, got_r;
-      select_window(L, p, topk, lbuf, rbuf, lane, got_l, got_r);
+      const QueryList L =
+          query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap, chunk);
+      int got_l = 0, got_r = 0;
+      if (L.n > 0) {  // an empty pool (the chunked rule's first chunk) selects nothing
+        const int32_t p = (L.codes == prev_codes && key >= prev_key)
+                              ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
+                              : wave_lower_bound(L.codes, 0, L.n, key, lane);
+        prev_codes = L.codes;
+        prev_key = key;
+        prev_p = p;
+        select_window(L, p, topk, lbuf, rbuf, lane, got_l, got_r);
+      }
       wave_lds_sync();
 
       int32_t* row = idx + g * topk;
@@ -268,7 +272,7 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
 }
 
 hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                         int64_t S, int64_t N, int topk, bool causal, const int32_t* q_order, int32_t* idx,
+                         int64_t S, int64_t N, int topk, bool causal, int chunk, const int32_t* q_order, int32_t* idx,
                          void* workspace, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
@@ -283,7 +287,7 @@ hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, 
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const size_t lds = size_t(kSelWavesPerBlock) * 2 * topk * sizeof(int32_t);
   hipLaunchKernelGGL(select_kernel, dim3(blocks), dim3(kSelWavesPerBlock * 64), lds, stream, q_codes,
-                     sorted_codes, perm, list_codes, list_pos, total, N, topk, causal ? 1 : 0, lp.t0,
+                     sorted_codes, perm, list_codes, list_pos, total, N, topk, causal ? 1 : 0, chunk, lp.t0,
                      lp.t_hi, lp.cap, q_order, idx);
   return hipGetLastError();
 }

@@ -125,8 +125,23 @@ __device__ __forceinline__ int query_level(int32_t i, int t0, int t_hi) {
   return t <= t_hi ? t : t_hi + 1;
 }
 
+// Largest key position in the causal pool of query i: i for the exact
+// prefix (chunk 0), floor(i / M) * M - 1 for the paper's chunked rule with
+// chunk size M = chunk (Section 3.2.2; Algorithm 1, Step 4); -1 when the
+// pool is empty (the first chunk).
+__device__ __forceinline__ int32_t pool_limit(int32_t i, int chunk) {
+  return chunk > 0 ? (i / chunk) * chunk - 1 : i;
+}
+
+// Level of the list searched for a causal pool ending at `limit` (t0 for an
+// empty pool, which reads no entry).
+__device__ __forceinline__ int pool_level(int32_t limit, int t0, int t_hi) {
+  return limit < 0 ? t0 : query_level(limit, t0, t_hi);
+}
+
 // Where a query's candidates live: the sorted list it searches (codes and
-// positions, n entries) and the largest position in its pool.
+// positions, n entries) and the largest position in its pool.  An empty
+// causal pool gives n = 0.
 struct QueryList {
   const uint32_t* codes;
   const int32_t* pos;
@@ -138,15 +153,20 @@ __device__ __forceinline__ QueryList query_list(const uint32_t* __restrict__ sor
                                                 const int32_t* __restrict__ perm,
                                                 const uint32_t* __restrict__ list_codes,
                                                 const int32_t* __restrict__ list_pos, int64_t seg, int64_t N,
-                                                int32_t i, int causal, int t0, int t_hi, int64_t cap) {
+                                                int32_t i, int causal, int t0, int t_hi, int64_t cap,
+                                                int chunk = 0) {
   QueryList L;
   L.codes = sorted_codes + seg * N;
   L.pos = perm + seg * N;
   L.n = int32_t(N);
   L.limit = int32_t(N - 1);  // every position is in the non-causal pool
   if (causal) {
-    L.limit = i;
-    const int t = query_level(i, t0, t_hi);
+    L.limit = pool_limit(i, chunk);
+    if (L.limit < 0) {
+      L.n = 0;
+      return L;
+    }
+    const int t = query_level(L.limit, t0, t_hi);
     if (t <= t_hi) {
       const int64_t off = seg * cap + ((int64_t(1) << t) - (int64_t(1) << t0));
       L.codes = list_codes + off;

@@ -208,8 +208,8 @@ __global__ void __launch_bounds__(kBndWaves * 64)
     window_bounds_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
                          const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                          const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
-                         int64_t N, int topk, int causal, int t0, int t_hi, int64_t cap, int2* __restrict__ bounds,
-                         int32_t* __restrict__ idx_out) {
+                         int64_t N, int topk, int causal, int chunk, int t0, int t_hi, int64_t cap,
+                         int2* __restrict__ bounds, int32_t* __restrict__ idx_out) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t runs = (total + 63) / 64;
@@ -229,94 +229,101 @@ __global__ void __launch_bounds__(kBndWaves * 64)
         key = q_codes[seg * N + ii];
       }
     }
-    const bool valid = my_i >= 0;
+    // A query with an empty pool (the chunked rule's first chunk) gets an
+    // empty window and takes no part in the search.
+    const bool has_q = my_i >= 0;
+    const bool valid = has_q && (causal == 0 || pool_limit(my_i, chunk) >= 0);
+    const uint64_t qmask = wave_ballot(has_q);
+    if (qmask == 0ull) continue;
     const uint64_t vmask = wave_ballot(valid);
-    if (vmask == 0ull) continue;
     const QueryList Lq = query_list(sorted_codes, perm, list_codes, list_pos, seg, N, valid ? my_i : 0, causal, t0,
-                                    t_hi, cap);
-
-    // Stage the leader's list around the leader's insertion point.
-    const int leader = __ffsll((unsigned long long)vmask) - 1;
-    const uint32_t* g_codes = readlane_ptr(Lq.codes, leader);
-    const int32_t* g_pos = readlane_ptr(Lq.pos, leader);
-    const int32_t g_n = __builtin_amdgcn_readlane(Lq.n, leader);
-    const uint32_t g_key = uint32_t(__builtin_amdgcn_readlane(int32_t(key), leader));
-    const int32_t p0 = wave_lower_bound(g_codes, 0, g_n, g_key, lane);
-    const int32_t r0 = p0 - kMargin > 0 ? p0 - kMargin : 0;
-    const int32_t r1 = r0 + kRegion < g_n ? r0 + kRegion : g_n;
-    {
-      uint32_t cv[kRegion / 64];
-      int32_t pv[kRegion / 64];
-#pragma unroll
-      for (int t = 0; t < kRegion / 64; ++t) {
-        const int32_t e = r0 + t * 64 + lane;
-        cv[t] = e < r1 ? g_codes[e] : 0u;
-        pv[t] = e < r1 ? g_pos[e] : 0;
-      }
-#pragma unroll
-      for (int t = 0; t < kRegion / 64; ++t) {
-        s_bnd_codes[wave][t * 64 + lane] = cv[t];
-        s_bnd_pos[wave][t * 64 + lane] = pv[t];
-      }
-    }
-    wave_lds_sync();
-
+                                    t_hi, cap, valid ? chunk : 0);
     LaneList L;
     L.codes = Lq.codes;
     L.pos = Lq.pos;
     L.wave = wave;
     L.n = Lq.n;
     L.limit = Lq.limit;
-    const bool staged = Lq.codes == g_codes;
-    L.r0 = staged ? r0 : 0;
-    L.r1 = staged ? r1 : 0;
-
-    // Lower bound of the code: in the staged range when it brackets the key.
-    int32_t p = 0;
-    bool found = false;
-    if (valid && staged && (r0 == 0 || s_bnd_codes[wave][0] < key) && (r1 == L.n || s_bnd_codes[wave][r1 - r0 - 1] >= key)) {
-      int32_t lo = r0, hi = r1;
-      while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (s_bnd_codes[wave][mid - r0] < key)
-          lo = mid + 1;
-        else
-          hi = mid;
-      }
-      p = lo;
-      found = true;
-    }
-    // The rest search the list itself, one query at a time, wavefront-wide.
-    for (uint64_t m = wave_ballot(valid && !found); m != 0ull; m &= m - 1ull) {
-      const int u = __ffsll((unsigned long long)m) - 1;
-      const uint32_t* uc_p = readlane_ptr(L.codes, u);
-      const int32_t un = __builtin_amdgcn_readlane(L.n, u);
-      const uint32_t uk = uint32_t(__builtin_amdgcn_readlane(int32_t(key), u));
-      const int32_t up = wave_lower_bound(uc_p, 0, un, uk, lane);
-      if (lane == u) p = up;
-    }
-
-    // The window, entry by entry.
+    L.r0 = 0;
+    L.r1 = 0;
     int2 res = make_int2(0, -1);
-    if (valid) {
-      const int half = topk / 2;
-      const int need_r = topk - half;
-      // Right side: first and last entry taken; left side: nearest and
-      // farthest entry taken.
-      int32_t r_first = 0, r_last = -1, l_near = -1, l_far = 0;
-      int32_t cur_r = p;
-      int got_r = lane_scan(L, cur_r, +1, need_r, 0, r_first, r_last);
-      const int need_l = half + (need_r - got_r);
-      int32_t cur_l = p - 1;
-      const int got_l = lane_scan(L, cur_l, -1, need_l, 0, l_near, l_far);
-      if (got_l < need_l && got_r == need_r) got_r = lane_scan(L, cur_r, +1, topk - got_l, got_r, r_first, r_last);
-      if (got_l + got_r > 0) res = make_int2(got_l > 0 ? l_far : r_first, got_r > 0 ? r_last : l_near);
-    }
+    if (vmask != 0ull) {
+      // Stage the leader's list around the leader's insertion point.
+      const int leader = __ffsll((unsigned long long)vmask) - 1;
+      const uint32_t* g_codes = readlane_ptr(Lq.codes, leader);
+      const int32_t* g_pos = readlane_ptr(Lq.pos, leader);
+      const int32_t g_n = __builtin_amdgcn_readlane(Lq.n, leader);
+      const uint32_t g_key = uint32_t(__builtin_amdgcn_readlane(int32_t(key), leader));
+      const int32_t p0 = wave_lower_bound(g_codes, 0, g_n, g_key, lane);
+      const int32_t r0 = p0 - kMargin > 0 ? p0 - kMargin : 0;
+      const int32_t r1 = r0 + kRegion < g_n ? r0 + kRegion : g_n;
+      {
+        uint32_t cv[kRegion / 64];
+        int32_t pv[kRegion / 64];
+#pragma unroll
+        for (int t = 0; t < kRegion / 64; ++t) {
+          const int32_t e = r0 + t * 64 + lane;
+          cv[t] = e < r1 ? g_codes[e] : 0u;
+          pv[t] = e < r1 ? g_pos[e] : 0;
+        }
+#pragma unroll
+        for (int t = 0; t < kRegion / 64; ++t) {
+          s_bnd_codes[wave][t * 64 + lane] = cv[t];
+          s_bnd_pos[wave][t * 64 + lane] = pv[t];
+        }
+      }
+      wave_lds_sync();
+
+      const bool staged = Lq.codes == g_codes;
+      L.r0 = staged ? r0 : 0;
+      L.r1 = staged ? r1 : 0;
+
+      // Lower bound of the code: in the staged range when it brackets the key.
+      int32_t p = 0;
+      bool found = false;
+      if (valid && staged && (r0 == 0 || s_bnd_codes[wave][0] < key) && (r1 == L.n || s_bnd_codes[wave][r1 - r0 - 1] >= key)) {
+        int32_t lo = r0, hi = r1;
+        while (lo < hi) {
+          const int32_t mid = (lo + hi) >> 1;
+          if (s_bnd_codes[wave][mid - r0] < key)
+            lo = mid + 1;
+          else
+            hi = mid;
+        }
+        p = lo;
+        found = true;
+      }
+      // The rest search the list itself, one query at a time, wavefront-wide.
+      for (uint64_t m = wave_ballot(valid && !found); m != 0ull; m &= m - 1ull) {
+        const int u = __ffsll((unsigned long long)m) - 1;
+        const uint32_t* uc_p = readlane_ptr(L.codes, u);
+        const int32_t un = __builtin_amdgcn_readlane(L.n, u);
+        const uint32_t uk = uint32_t(__builtin_amdgcn_readlane(int32_t(key), u));
+        const int32_t up = wave_lower_bound(uc_p, 0, un, uk, lane);
+        if (lane == u) p = up;
+      }
+
+      // The window, entry by entry.
+      if (valid) {
+        const int half = topk / 2;
+        const int need_r = topk - half;
+        // Right side: first and last entry taken; left side: nearest and
+        // farthest entry taken.
+        int32_t r_first = 0, r_last = -1, l_near = -1, l_far = 0;
+        int32_t cur_r = p;
+        int got_r = lane_scan(L, cur_r, +1, need_r, 0, r_first, r_last);
+        const int need_l = half + (need_r - got_r);
+        int32_t cur_l = p - 1;
+        const int got_l = lane_scan(L, cur_l, -1, need_l, 0, l_near, l_far);
+        if (got_l < need_l && got_r == need_r) got_r = lane_scan(L, cur_r, +1, topk - got_l, got_r, r_first, r_last);
+        if (got_l + got_r > 0) res = make_int2(got_l > 0 ? l_far : r_first, got_r > 0 ? r_last : l_near);
+      }
+    }  // some lane has a pool
     if (slot < total) bounds[slot] = res;
 
     if (idx_out != nullptr) {
       // The windows' positions in list order, then -1: one query at a time.
-      for (uint64_t m = vmask; m != 0ull; m &= m - 1ull) {
+      for (uint64_t m = qmask; m != 0ull; m &= m - 1ull) {
         const int u = __ffsll((unsigned long long)m) - 1;
         const int32_t* upos = readlane_ptr(L.pos, u);
         const int32_t ua = __builtin_amdgcn_readlane(res.x, u), ub = __builtin_amdgcn_readlane(res.y, u);
@@ -398,7 +405,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                               const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
                               const int2* __restrict__ bounds, const uint2* __restrict__ keys_full,
                               const uint2* __restrict__ keys_list, int64_t total, int64_t N, int dk_rt, int causal,
-                              int t0, int t_hi, int64_t cap, float eps, const float* __restrict__ mk,
+                              int chunk, int t0, int t_hi, int64_t cap, float eps, const float* __restrict__ mk,
                               const float* __restrict__ mv, uint16_t* __restrict__ out) {
   constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
   constexpr int W = E / 2;    // 32-bit words per lane and row
@@ -440,7 +447,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         if (ii >= 0 && ii < N) {
           my_i = int32_t(ii);
           my_seg = sg;
-          my_lvl = causal ? query_level(my_i, t0, t_hi) : 0;
+          my_lvl = causal ? pool_level(pool_limit(my_i, chunk), t0, t_hi) : 0;
           const int2 bb = bounds[sl];
           my_a = bb.x;
           my_b = bb.y;
@@ -471,7 +478,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // as empty.
       const bool in_grp = ((gmask >> qn) & 1u) != 0u;
       const bool mine = in_grp && 0 <= my_a && my_a <= my_b && my_b < ln;
-      const int32_t my_lim = causal ? my_i : int32_t(N - 1);
+      const int32_t my_lim = causal ? pool_limit(my_i, chunk) : int32_t(N - 1);
       float qv[KD];
       if (kHist ? in_grp : mine) {
         if constexpr (DK == 3) {
@@ -703,7 +710,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 
 template <int DV, int DK>
 hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
-                         int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
+                         int topk, bool causal, int chunk, const int32_t* perm, const int32_t* list_pos,
                          const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
                          float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
@@ -715,7 +722,7 @@ hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v
 #define ZETA_TILE_LAUNCH(OFF, HIST)                                                                                  \
   hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST>), dim3(blocks), dim3(kTileWaves * 64), 0, stream, \
                      q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk, causal ? 1 : 0,    \
-                     lp.t0, lp.t_hi, lp.cap, eps, hm.k, hm.v, out)
+                     chunk, lp.t0, lp.t_hi, lp.cap, eps, hm.k, hm.v, out)
   const bool hist = hm.k != nullptr;
   if (off32) {
     if (hist)
@@ -734,14 +741,14 @@ hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v
 
 template <int DV>
 hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
-                          int topk, bool causal, const int32_t* perm, const int32_t* list_pos,
+                          int topk, bool causal, int chunk, const int32_t* perm, const int32_t* list_pos,
                           const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
                           float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
   if (dk == 3)
-    return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, keys_list,
-                                eps, hm, out, stream);
-  return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, keys_list,
-                              eps, hm, out, stream);
+    return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, chunk, perm, list_pos, q_order, bounds, keys_full,
+                                keys_list, eps, hm, out, stream);
+  return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, chunk, perm, list_pos, q_order, bounds, keys_full,
+                              keys_list, eps, hm, out, stream);
 }
 
 }  // namespace
@@ -749,7 +756,8 @@ hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* 
 bool tile_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 256; }
 
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
-                                     int topk, bool causal, const uint32_t* q_codes, const uint32_t* sorted_codes,
+                                     int topk, bool causal, int chunk, const uint32_t* q_codes,
+                                     const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
                                      const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
                                      int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream) {
@@ -768,8 +776,8 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
     const int64_t want = ceil_div(runs, kBndWaves);
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
     hipLaunchKernelGGL(window_bounds_kernel, dim3(blocks), dim3(kBndWaves * 64), 0, stream, q_codes, sorted_codes,
-                       perm, list_codes, list_pos, q_order, total, N, topk, causal ? 1 : 0, lp.t0, lp.t_hi, lp.cap,
-                       bounds, idx_out);
+                       perm, list_codes, list_pos, q_order, total, N, topk, causal ? 1 : 0, chunk, lp.t0, lp.t_hi,
+                       lp.cap, bounds, idx_out);
   }
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);
@@ -777,7 +785,7 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
   uint16_t* oo = static_cast<uint16_t*>(out);
 #define ZETA_TILE_CASE(DVV) \
   case DVV:                 \
-    return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, perm, list_pos, q_order, bounds, keys_full, \
+    return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, chunk, perm, list_pos, q_order, bounds, keys_full, \
                                keys_list, eps, hm, oo, stream);
   switch (dv) {
     ZETA_TILE_CASE(32)

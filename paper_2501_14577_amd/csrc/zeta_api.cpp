@@ -10,6 +10,11 @@
 static_assert(ZETA_MAX_DK == zeta::kMaxDk, "d_k limit mismatch");
 static_assert(ZETA_MAX_TOPK == zeta::kMaxTopk, "topk limit mismatch");
 static_assert(ZETA_MAX_BITS == zeta::kMaxBits, "bits limit mismatch");
+static_assert(int(ZETA_SCORE_CAUCHY) == zeta::kScoreCauchy && int(ZETA_SCORE_DOT) == zeta::kScoreDot &&
+                  int(ZETA_SCORE_NEG_EUCLID) == zeta::kScoreNegEuclid &&
+                  int(ZETA_SCORE_INV_EUCLID) == zeta::kScoreInvEuclid &&
+                  int(ZETA_SCORE_NORM_DOT) == zeta::kScoreNormDot,
+              "score mode mismatch");
 
 namespace {
 
@@ -18,6 +23,12 @@ constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;  // B*H*N limit (int32 pos
 bool shape_ok(int64_t S, int64_t N) { return S >= 1 && N >= 1 && N <= kMaxElems && S <= kMaxElems / N; }
 
 bool dtype_known(zeta_dtype_t d) { return d == ZETA_F32 || d == ZETA_BF16; }
+
+bool score_known(zeta_score_t s) { return int(s) >= int(ZETA_SCORE_CAUCHY) && int(s) <= int(ZETA_SCORE_NORM_DOT); }
+
+// The causal mode and the chunked rule's chunk size: 0 (exact prefix) or a
+// positive chunk size, the latter only for causal calls.
+bool bad_pool(int causal, int chunk) { return (causal != 0 && causal != 1) || chunk < 0 || (chunk > 0 && !causal); }
 
 zeta_status_t hip_status(hipError_t e) { return e == hipSuccess ? ZETA_OK : ZETA_ERR_HIP; }
 
@@ -102,16 +113,17 @@ zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64
 }
 
 zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                               int64_t n_segments, int64_t N, int topk, int causal, const int32_t* q_order,
-                               int32_t* idx, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                               int64_t n_segments, int64_t N, int topk, int causal, int chunk,
+                               const int32_t* q_order, int32_t* idx, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
   if (!q_codes || !sorted_codes || !perm || !idx) return ZETA_ERR_INVALID_ARG;
   if (!shape_ok(n_segments, N)) return ZETA_ERR_INVALID_ARG;
-  if (topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (topk < 1 || bad_pool(causal, chunk)) return ZETA_ERR_INVALID_ARG;
   if (topk > zeta::kMaxTopk) return ZETA_ERR_UNSUPPORTED;
   const zeta::SelectWs ws = zeta::select_ws(n_segments, N, topk, causal);
   if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
-  return hip_status(zeta::launch_select(q_codes, sorted_codes, perm, n_segments, N, topk, causal != 0, q_order,
-                                        idx, workspace, stream));
+  return hip_status(zeta::launch_select(q_codes, sorted_codes, perm, n_segments, N, topk, causal != 0, chunk,
+                                        q_order, idx, workspace, stream));
 }
 
 zeta_status_t zeta_history_mean(const void* k, const void* v, zeta_dtype_t dtype, int64_t B, int64_t H, int64_t N,
@@ -134,8 +146,8 @@ zeta_status_t zeta_history_mean(const void* k, const void* v, zeta_dtype_t dtype
 
 zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
                                  int64_t H, int64_t N, int d_k, int d_v, int topk, const int32_t* idx,
-                                 const int32_t* q_order, float eps, const float* mean_k, const float* mean_v,
-                                 void* out, hipStream_t stream) {
+                                 const int32_t* q_order, zeta_score_t score, float eps, const float* mean_k,
+                                 const float* mean_v, void* out, hipStream_t stream) {
   if (!q || !k || !v || !idx || !out) return ZETA_ERR_INVALID_ARG;
   if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
   if (d_k < 1 || d_v < 1 || topk < 1) return ZETA_ERR_INVALID_ARG;
@@ -145,27 +157,30 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
   if (bad_means(mean_k, mean_v)) return ZETA_ERR_INVALID_ARG;
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
-  return hip_status(zeta::launch_attend(q, k, v, dtype == ZETA_BF16, B * H, N, d_k, d_v, topk, idx, q_order, eps,
-                                        zeta::HistMean{mean_k, mean_v}, out, stream));
+  if (!score_known(score)) return ZETA_ERR_UNSUPPORTED;
+  return hip_status(zeta::launch_attend(q, k, v, dtype == ZETA_BF16, B * H, N, d_k, d_v, topk, idx, q_order,
+                                        int(score), eps, zeta::HistMean{mean_k, mean_v}, out, stream));
 }
 
 zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
-                                     int64_t H, int64_t N, int d_k, int d_v, int topk, int causal,
+                                     int64_t H, int64_t N, int d_k, int d_v, int topk, int causal, int chunk,
                                      const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                                     const int32_t* q_order, float eps, const float* mean_k, const float* mean_v,
-                                     void* out, int32_t* idx_out, void* workspace, size_t workspace_bytes,
+                                     const int32_t* q_order, zeta_score_t score, float eps, const float* mean_k,
+                                     const float* mean_v, void* out, int32_t* idx_out, void* workspace,
+                                     size_t workspace_bytes,
                                      hipStream_t stream) {
   if (!q || !k || !v || !out || !q_codes || !sorted_codes || !perm) return ZETA_ERR_INVALID_ARG;
   if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
-  if (d_k < 1 || d_v < 1 || topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || d_v < 1 || topk < 1 || bad_pool(causal, chunk)) return ZETA_ERR_INVALID_ARG;
   if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
   if (!aligned16(v) || !aligned16(out)) return ZETA_ERR_INVALID_ARG;
   if (out == q || out == k || out == v) return ZETA_ERR_INVALID_ARG;
   if (bad_means(mean_k, mean_v)) return ZETA_ERR_INVALID_ARG;
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
+  if (!score_known(score)) return ZETA_ERR_UNSUPPORTED;
   const int64_t S = B * H;
-  if (dtype == ZETA_BF16 && zeta::tile_supports(d_v)) {
+  if (dtype == ZETA_BF16 && zeta::tile_supports(d_v) && score == ZETA_SCORE_CAUCHY) {
     // Lists and per-slot window bounds.
     const zeta::FusedWs ws = zeta::fused_ws(S, N, topk, causal);
     if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
@@ -174,9 +189,9 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
     const zeta::SelectWs ws = zeta::select_ws(S, N, topk, causal);
     if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
   }
-  return hip_status(zeta::launch_select_attend(q, k, v, dtype == ZETA_BF16, S, N, d_k, d_v, topk, causal != 0, q_codes,
-                                               sorted_codes, perm, q_order, eps, zeta::HistMean{mean_k, mean_v}, out,
-                                               idx_out, workspace, stream));
+  return hip_status(zeta::launch_select_attend(q, k, v, dtype == ZETA_BF16, S, N, d_k, d_v, topk, causal != 0, chunk,
+                                               q_codes, sorted_codes, perm, q_order, int(score), eps,
+                                               zeta::HistMean{mean_k, mean_v}, out, idx_out, workspace, stream));
 }
 
 zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B, int64_t H,

@@ -19,6 +19,8 @@ _lib = None
 
 ZETA_OK, ZETA_ERR_INVALID_ARG, ZETA_ERR_UNSUPPORTED, ZETA_ERR_WORKSPACE, ZETA_ERR_HIP = range(5)
 ZETA_F32, ZETA_BF16 = 0, 1
+# Attention scores (zeta_score_t): the method's Cauchy score and the variants.
+SCORES = {"cauchy": 0, "dot": 1, "neg_euclid": 2, "inv_euclid": 3, "norm_dot": 4}
 EXPORTED = (
     "zeta_morton_encode",
     "zeta_sort_keys",
@@ -58,10 +60,11 @@ def load_library() -> ctypes.CDLL:
     L.zeta_morton_encode.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     L.zeta_sort_keys.argtypes = [vp, i64, i64, i32, vp, vp, vp, sz, vp]
     L.zeta_query_order.argtypes = [vp, i64, i64, i32, i32, vp, vp, sz, vp]
-    L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp]
-    L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, f32, vp, vp, vp, vp]
-    L.zeta_select_attend_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, f32,
-                                         vp, vp, vp, vp, vp, sz, vp]
+    L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, vp, vp, vp, sz, vp]
+    L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, i32, f32, vp, vp, vp,
+                                     vp]
+    L.zeta_select_attend_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp,
+                                         i32, f32, vp, vp, vp, vp, vp, sz, vp]
     L.zeta_history_mean.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, sz, vp]
     L.zeta_topk_attn_bwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, f32, vp, vp, i32,
                                      vp, vp, vp, vp, vp, sz, vp]
@@ -192,13 +195,23 @@ def zeta_query_order(q_order: Optional[torch.Tensor], N: int, S: int, topk: int,
     return order_out
 
 
+def _score_code(score) -> int:
+    if isinstance(score, str):
+        if score not in SCORES:
+            raise ValueError(f"unknown score {score!r}; one of {sorted(SCORES)}")
+        return SCORES[score]
+    return int(score)
+
+
 def zeta_select_topk(q_codes: torch.Tensor, sorted_codes: torch.Tensor, perm: torch.Tensor, topk: int,
-                     causal: bool, *, q_order: Optional[torch.Tensor] = None, idx: Optional[torch.Tensor] = None,
-                     workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+                     causal: bool, *, chunk: int = 0, q_order: Optional[torch.Tensor] = None,
+                     idx: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Candidate window of every query -> idx int32 [..., N, topk] (-1 padded).
 
-    ``q_order`` (int32, shaped like ``q_codes``) is an optional processing
-    order; it does not change the result."""
+    ``chunk`` > 0 selects the paper's chunked causal rule (pool: positions
+    below floor(i / chunk) * chunk).  ``q_order`` (int32, shaped like
+    ``q_codes``) is an optional processing order; it does not change the
+    result."""
     N = q_codes.shape[-1]
     S = q_codes.numel() // N
     if idx is None:
@@ -207,7 +220,7 @@ def zeta_select_topk(q_codes: torch.Tensor, sorted_codes: torch.Tensor, perm: to
         workspace = workspace_for(S, 1, N, 1, 1, topk, causal, q_codes.device)
     _need_device(q_codes, sorted_codes, perm, q_order, idx, workspace)
     st = load_library().zeta_select_topk(_ptr(q_codes), _ptr(sorted_codes), _ptr(perm), S, N, topk,
-                                         int(bool(causal)), _ptr(q_order), _ptr(idx), _ptr(workspace),
+                                         int(bool(causal)), int(chunk), _ptr(q_order), _ptr(idx), _ptr(workspace),
                                          workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_select_topk", st)
     return idx
@@ -245,11 +258,13 @@ def zeta_history_mean(k: torch.Tensor, v: torch.Tensor, causal: bool, *, mean_k:
 
 
 def zeta_topk_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, eps: float, *,
-                       q_order: Optional[torch.Tensor] = None, mean_k: Optional[torch.Tensor] = None,
-                       mean_v: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Cauchy-softmax attention over idx -> out [B,H,N,d_v] in v's dtype;
-    with mean_k and mean_v (``zeta_history_mean``) each window also holds the
-    history-mean candidate."""
+                       q_order: Optional[torch.Tensor] = None, score="cauchy",
+                       mean_k: Optional[torch.Tensor] = None, mean_v: Optional[torch.Tensor] = None,
+                       out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Cauchy-softmax attention over idx (or a score variant, ``score`` a
+    name of SCORES) -> out [B,H,N,d_v] in v's dtype; with mean_k and mean_v
+    (``zeta_history_mean``) each window also holds the history-mean
+    candidate."""
     B, H, N, dk = q.shape
     dv = v.shape[-1]
     topk = idx.shape[-1]
@@ -260,8 +275,8 @@ def zeta_topk_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
     if not (q.dtype == k.dtype == v.dtype == out.dtype):
         raise ValueError("q, k, v and out must share a dtype")
     st = load_library().zeta_topk_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dk, dv, topk,
-                                           _ptr(idx), _ptr(q_order), float(eps), _ptr(mean_k), _ptr(mean_v),
-                                           _ptr(out), _stream())
+                                           _ptr(idx), _ptr(q_order), _score_code(score), float(eps), _ptr(mean_k),
+                                           _ptr(mean_v), _ptr(out), _stream())
     _check("zeta_topk_attn_fwd", st)
     return out
 
@@ -302,6 +317,7 @@ def zeta_topk_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
 
 def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_codes: torch.Tensor,
                            sorted_codes: torch.Tensor, perm: torch.Tensor, topk: int, causal: bool, eps: float, *,
+                           chunk: int = 0, score="cauchy",
                            q_order: Optional[torch.Tensor] = None, mean_k: Optional[torch.Tensor] = None,
                            mean_v: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                            idx_out: Optional[torch.Tensor] = None,
@@ -319,8 +335,9 @@ def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_
     if not (q.dtype == k.dtype == v.dtype == out.dtype):
         raise ValueError("q, k, v and out must share a dtype")
     st = load_library().zeta_select_attend_fwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dk, dv, topk,
-                                               int(bool(causal)), _ptr(q_codes), _ptr(sorted_codes), _ptr(perm),
-                                               _ptr(q_order), float(eps), _ptr(mean_k), _ptr(mean_v), _ptr(out),
+                                               int(bool(causal)), int(chunk), _ptr(q_codes), _ptr(sorted_codes),
+                                               _ptr(perm), _ptr(q_order), _score_code(score), float(eps),
+                                               _ptr(mean_k), _ptr(mean_v), _ptr(out),
                                                _ptr(idx_out), _ptr(workspace),
                                                workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_select_attend_fwd", st)
@@ -329,14 +346,16 @@ def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_
 
 def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: float, causal: bool = True,
             bits: int = 10, *, workspace: Optional[torch.Tensor] = None, buffers: Optional[dict] = None,
-            zorder: bool = True, fused: bool = False, history: bool = False, return_intermediates: bool = False):
+            zorder: bool = True, fused: bool = False, history: bool = False, chunk: int = 0, score="cauchy",
+            return_intermediates: bool = False):
     """The whole forward: encode, sort, select, attend (four calls, one stream).
 
     The query codes are sorted together with the key codes (one call over
     2*B*H segments); their Z-order, regrouped by list level, drives select
     and attend (``zorder``).  ``fused`` runs select and attend as one pass.
     The result is the same either way.  ``history`` adds the history-mean
-    candidate to every window.  ``buffers`` (from ``alloc_buffers``)
+    candidate to every window; ``chunk`` picks the paper's chunked causal
+    rule and ``score`` a score variant.  ``buffers`` (from ``alloc_buffers``)
     holds preallocated outputs so that repeated calls allocate nothing.
     """
     B, H, N, dk = q.shape
@@ -358,11 +377,12 @@ def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: f
         mk, mv = zeta_history_mean(k, v, causal, workspace=workspace)
     if fused:
         idx = b["idx"] if return_intermediates else None
-        out = zeta_select_attend_fwd(q, k, v, qc, sc, perm, topk, causal, eps, q_order=order, mean_k=mk, mean_v=mv,
-                                     out=b["out"], idx_out=idx, workspace=workspace)
+        out = zeta_select_attend_fwd(q, k, v, qc, sc, perm, topk, causal, eps, chunk=chunk, score=score, q_order=order,
+                                     mean_k=mk, mean_v=mv, out=b["out"], idx_out=idx, workspace=workspace)
     else:
-        idx = zeta_select_topk(qc, sc, perm, topk, causal, q_order=order, idx=b["idx"], workspace=workspace)
-        out = zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, mean_k=mk, mean_v=mv, out=b["out"])
+        idx = zeta_select_topk(qc, sc, perm, topk, causal, chunk=chunk, q_order=order, idx=b["idx"],
+                               workspace=workspace)
+        out = zeta_topk_attn_fwd(q, k, v, idx, eps, q_order=order, score=score, mean_k=mk, mean_v=mv, out=b["out"])
     if return_intermediates:
         return dict(q_codes=qc, k_codes=kc, sorted_codes=sc, perm=perm, q_order=order, idx=idx, mean_k=mk,
                     mean_v=mv, out=out)

@@ -260,7 +260,8 @@ def check_attend_dense_limit(orc):
 
 
 def check_attend_special_cases(orc):
-    """Causal o_0 = v_0; huge eps gives the plain mean over the window;
+    """Causal o_0 = v_0; huge eps gives the plain mean over the window; a
+    row without candidates is zero;
     identical keys give uniform weights; outputs stay inside the window's
     per-component range."""
     rng = np.random.default_rng(37)
@@ -285,6 +286,10 @@ def check_attend_special_cases(orc):
     for i in range(n):
         sel = idx[i][idx[i] >= 0]
         assert np.allclose(out_same[i], v[0][sel].astype(np.float64).mean(axis=0), atol=1e-12)
+    # A row without candidates (the chunked rule's first chunk) is zero.
+    empty = res["idx"].copy()
+    empty[0, 5] = -1
+    assert np.all(orc.attend(q, kk, v, empty, 0.5)[0, 5] == 0.0)
 
 
 def _frac(t):

@@ -139,7 +139,7 @@ def _qord(**kw):
 
 
 def _sel(**kw):
-    a = dict(q_codes=P, sorted_codes=P2, perm=P3, S=2, N=100, topk=8, causal=1, q_order=NULL, idx=P4, ws=P,
+    a = dict(q_codes=P, sorted_codes=P2, perm=P3, S=2, N=100, topk=8, causal=1, chunk=0, q_order=NULL, idx=P4, ws=P,
              ws_bytes=BIG, stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_select_topk(*a.values())
@@ -147,7 +147,7 @@ def _sel(**kw):
 
 def _att(**kw):
     a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, idx=P4,
-             q_order=NULL, eps=0.5, mean_k=NULL, mean_v=NULL, out=ctypes.c_void_p(0x50000), stream=NULL)
+             q_order=NULL, score=0, eps=0.5, mean_k=NULL, mean_v=NULL, out=ctypes.c_void_p(0x50000), stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_topk_attn_fwd(*a.values())
 
@@ -182,6 +182,7 @@ def test_sort_rejects(kw, code):
 SELECT_CASES = [
     (dict(q_codes=NULL), INV), (dict(sorted_codes=NULL), INV), (dict(perm=NULL), INV), (dict(idx=NULL), INV),
     (dict(S=0), INV), (dict(N=0), INV), (dict(topk=0), INV), (dict(causal=2), INV),
+    (dict(chunk=-1), INV), (dict(causal=0, chunk=4), INV),  # the chunked rule is causal
     (dict(topk=1025), UNS), (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP),
 ]
 
@@ -197,6 +198,7 @@ ATTEND_CASES = [
     (dict(eps=0.0), INV), (dict(eps=-1.0), INV), (dict(eps=float("inf")), INV), (dict(eps=float("nan")), INV),
     (dict(v=ctypes.c_void_p(0x30008)), INV), (dict(out=ctypes.c_void_p(0x50004)), INV), (dict(out=P3), INV),
     (dict(dtype=5), UNS), (dict(d_k=9), UNS), (dict(d_v=96), UNS), (dict(d_v=512), UNS), (dict(topk=2000), UNS),
+    (dict(score=5), UNS), (dict(score=-1), UNS),
     (dict(mean_k=ctypes.c_void_p(0xB0000)), INV),  # history means come in pairs
     (dict(mean_v=ctypes.c_void_p(0xC0000)), INV),
     (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0004)), INV),  # mean_v misaligned
@@ -221,8 +223,9 @@ def test_query_order_rejects(kw, code):
 
 
 def _fused(**kw):
-    a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, causal=1, q_codes=P4,
-             sorted_codes=ctypes.c_void_p(0x60000), perm=ctypes.c_void_p(0x70000), q_order=NULL, eps=0.5,
+    a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, causal=1, chunk=0,
+             q_codes=P4, sorted_codes=ctypes.c_void_p(0x60000), perm=ctypes.c_void_p(0x70000), q_order=NULL, score=0,
+             eps=0.5,
              mean_k=NULL, mean_v=NULL, out=ctypes.c_void_p(0x50000), idx_out=NULL, ws=ctypes.c_void_p(0x80000),
              ws_bytes=BIG, stream=NULL)
     a.update(kw)
@@ -239,6 +242,7 @@ FUSED_CASES = [
     (dict(ws=ctypes.c_void_p(0x80008)), INV),  # bf16 one pass keeps 8-byte bounds in the workspace
     (dict(mean_v=ctypes.c_void_p(0xC0000)), INV),
     (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0008)), INV),
+    (dict(chunk=-2), INV), (dict(causal=0, chunk=16), INV), (dict(score=7), UNS),
 ]
 
 

@@ -36,7 +36,7 @@ MUTATIONS = {
     "eps squared": ("score = np.where(valid, 1.0 / (dist + eps), 0.0)",
                     "score = np.where(valid, 1.0 / (dist + eps * eps), 0.0)"),
     "padding not masked": ("score = np.where(valid, 1.0 / (dist + eps), 0.0)", "score = 1.0 / (dist + eps)"),
-    "not normalised": ("out[seg, r0:r0 + len(rr)] = num / z[:, None]", "out[seg, r0:r0 + len(rr)] = num"),
+    "not normalised": ("out[seg, r0:r0 + len(rr)] = num / zs[:, None]", "out[seg, r0:r0 + len(rr)] = num"),
     "bwd: o_i not subtracted": ('g = np.einsum("bd,bkd->bk", du, vj) - np.einsum("bd,bd->b", du, o)[:, None]',
                                  'g = np.einsum("bd,bkd->bk", du, vj)'),
     "bwd: delta not squared": ("w = np.where(valid, g / zs[:, None] / (delta * delta), 0.0)",
