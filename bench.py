@@ -306,7 +306,7 @@ def main() -> int:
         def step_chunked(ev=None):
             qc, kc = zeta.zeta_morton_encode(q, k, w.bits, q_codes=codes[0], k_codes=codes[1], workspace=ws)
             zeta.zeta_sort_keys(codes, w.code_bits, sorted_codes=sorted2, perm=perm2, workspace=ws)
-            order = zeta.zeta_query_order(perm2[0], w.N, w.segments, w.topk, causal, order_out=bufs["order"],
+            order = zeta.zeta_query_order(perm2[0], w.N, w.segments, w.topk, causal, chunk=chunk, order_out=bufs["order"],
                                           workspace=ws)
             if ev is not None:
                 ev[0].record()
@@ -327,7 +327,8 @@ def main() -> int:
                 if ev is not None:
                     ev[1].record()
             modes[mode] = timed(call)[1]
-        variants = {"chunk": chunk, "chunked_step_ms": chunk_step_ms, "chunked_value": w.B * w.N / (chunk_step_ms * 1e-3),
+        variants = {"chunk": chunk, "chunked_step_ms": chunk_step_ms,
+                    "chunked_value": w.B * w.N / (chunk_step_ms * 1e-3),
                     "chunked_select_attend_ms": chunk_call_ms, "score_select_attend_ms": modes}
 
     h_bytes = w.segments * w.N * (w.dk + w.dv) * (elem_size(w.dtype) + 4)  # read k, v once; write the means
@@ -415,7 +416,8 @@ def main() -> int:
             "means_frac": frac(h_bytes, hist_ms),
             "backward_ms": hist_bwd_ms,
         },
-        "variants": variants,
+        "variants": None if variants is None else dict(
+            variants, score_select_attend_GBs={m: gbs(f_bytes, t) for m, t in variants["score_select_attend_ms"].items()}),
         "step_hbm_frac": frac(s_bytes, ms_per_step),
         "step_algorithmic_bytes": s_bytes,
         "query_rows_per_s": per_s(w.segments * w.N, ms_per_step),

@@ -150,11 +150,13 @@ zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_
  *              position order.
  *   order_out  int32 [n_segments][N] output; may be the same buffer as
  *              q_order, but must not otherwise overlap it (INVALID_ARG).
- *   topk, causal  as for zeta_select_topk (non-causal: a copy of q_order).
+ *   topk, causal, chunk  as for zeta_select_topk (non-causal: a copy of
+ *              q_order); the levels follow the pool each query has under
+ *              the causal rule the later calls use.
  *   workspace  at least zeta_workspace_size(...) bytes.
  */
 zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64_t N, int topk,
-                               int causal, int32_t* order_out, void* workspace,
+                               int causal, int chunk, int32_t* order_out, void* workspace,
                                size_t workspace_bytes, hipStream_t stream);
 
 /*

@@ -44,16 +44,17 @@ hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_b
                        uint32_t* sorted_codes, int32_t* perm, void* workspace, hipStream_t stream);
 
 // One stable radix pass whose digit is the prefix-list level class of each
-// carried value (a query position; vals NULL: the positions 0..N-1): a stable
-// partition of each segment by list level.  hist holds
-// S * (ceil(N / kSortTile) + 1) * kRadixMax words.  vals_out must not alias vals.
-hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels,
+// carried value (a query position; vals NULL: the positions 0..N-1) under the
+// causal rule `chunk` (0: exact prefix): a stable partition of each segment
+// by list level.  hist holds S * (ceil(N / kSortTile) + 1) * kRadixMax words.
+// vals_out must not alias vals.
+hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels, int chunk,
                                   int32_t* vals_out, uint32_t* hist, hipStream_t stream);
 
 // Regroup a processing order (NULL: position order) by the list level each
 // query searches in select, keeping the given order inside each level.
-hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int topk, bool causal, int32_t* order_out,
-                              void* workspace, hipStream_t stream);
+hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int topk, bool causal, int chunk,
+                              int32_t* order_out, void* workspace, hipStream_t stream);
 
 // Causal prefix lists (when needed) and the window of every query.  chunk:
 // 0 for the exact causal prefix, M for the paper's chunked rule.  q_order:

@@ -226,8 +226,8 @@ __global__ void __launch_bounds__(kSelWavesPerBlock * 64)
 
 }  // namespace
 
-hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int topk, bool causal, int32_t* order_out,
-                              void* workspace, hipStream_t stream) {
+hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int topk, bool causal, int chunk,
+                              int32_t* order_out, void* workspace, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   const unsigned blocks = unsigned(ceil_div(total, 256));
@@ -246,7 +246,7 @@ hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int 
     hipLaunchKernelGGL(copy_order_kernel, dim3(blocks), dim3(256), 0, stream, q_order, total, N, copy);
     given = copy;
   }
-  return launch_level_partition(given, S, N, lp.t0, lp.t_hi, lp.levels, order_out, phist, stream);
+  return launch_level_partition(given, S, N, lp.t0, lp.t_hi, lp.levels, chunk, order_out, phist, stream);
 }
 
 hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm, int64_t S, int64_t N, int topk,

@@ -25,18 +25,19 @@ namespace {
 
 // Digit of an element: the key's bits [shift, shift+nbits) (kByLevel false), or
 // the prefix-list level class of the carried position (kByLevel true; the
-// level regrouping of a processing order, see query_level).
+// level regrouping of a processing order: the level of the list that
+// position's causal pool is searched in, see pool_limit and pool_level).
 template <bool kByLevel>
 __device__ __forceinline__ uint32_t radix_digit(uint32_t key, int32_t val, int shift, uint32_t mask, int t0,
-                                                int t_hi, int64_t N) {
-  if (kByLevel) return (val >= 0 && val < N) ? uint32_t(query_level(val, t0, t_hi) - t0) : 0u;
+                                                int t_hi, int chunk, int64_t N) {
+  if (kByLevel) return (val >= 0 && val < N) ? uint32_t(pool_level(pool_limit(val, chunk), t0, t_hi) - t0) : 0u;
   return (key >> shift) & mask;
 }
 
 template <bool kByLevel>
 __global__ void __launch_bounds__(kSortThreads)
     radix_hist_kernel(const uint32_t* __restrict__ keys, const int32_t* __restrict__ vals, int64_t N, int64_t tiles,
-                      int shift, int nbits, int t0, int t_hi, uint32_t* __restrict__ hist) {
+                      int shift, int nbits, int t0, int t_hi, int chunk, uint32_t* __restrict__ hist) {
   const int64_t seg = blockIdx.x / tiles;
   const int64_t tile = blockIdx.x % tiles;
   const int tid = threadIdx.x;
@@ -49,7 +50,7 @@ __global__ void __launch_bounds__(kSortThreads)
   for (int64_t e = e0 + tid; e < e1; e += kSortThreads) {
     const uint32_t key = kByLevel ? 0u : keys[seg * N + e];
     const int32_t val = kByLevel ? (vals != nullptr ? vals[seg * N + e] : int32_t(e)) : 0;
-    atomicAdd(&h[radix_digit<kByLevel>(key, val, shift, mask, t0, t_hi, N)], 1u);
+    atomicAdd(&h[radix_digit<kByLevel>(key, val, shift, mask, t0, t_hi, chunk, N)], 1u);
   }
   __syncthreads();
   for (int d = tid; d < kRadixMax; d += kSortThreads) hist[(seg * tiles + tile) * kRadixMax + d] = h[d];
@@ -106,7 +107,7 @@ __global__ void __launch_bounds__(kSortThreads)
 template <bool kHasPos, bool kByLevel>
 __global__ void __launch_bounds__(kSortThreads)
     radix_scatter_kernel(const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ pos_in,
-                         int64_t N, int64_t tiles, int shift, int nbits, int t0, int t_hi,
+                         int64_t N, int64_t tiles, int shift, int nbits, int t0, int t_hi, int chunk,
                          const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals,
                          uint32_t* __restrict__ keys_out, int32_t* __restrict__ pos_out) {
   const int64_t seg = blockIdx.x / tiles;
@@ -157,7 +158,7 @@ __global__ void __launch_bounds__(kSortThreads)
       pp = valid ? pos_in[seg_off + e] : 0;
     else
       pp = int32_t(e);
-    const uint32_t d = radix_digit<kByLevel>(kk, pp, shift, mask, t0, t_hi, N);
+    const uint32_t d = radix_digit<kByLevel>(kk, pp, shift, mask, t0, t_hi, chunk, N);
     uint64_t peers = wave_ballot(valid);
     for (int b = 0; b < nbits; ++b) {
       const bool bit = (d >> b) & 1u;
@@ -187,7 +188,7 @@ __global__ void __launch_bounds__(kSortThreads)
   for (int c = 0; c < kSortChunks; ++c) {
     const int64_t e = first + c * 64 + lane;
     if (e < N) {
-      const uint32_t d = radix_digit<kByLevel>(key[c], pos[c], shift, mask, t0, t_hi, N);
+      const uint32_t d = radix_digit<kByLevel>(key[c], pos[c], shift, mask, t0, t_hi, chunk, N);
       const int64_t dst = int64_t(s_base[d]) + s_wcnt[wave][d] + rank[c];
       if (!kByLevel) keys_out[seg_off + dst] = key[c];
       pos_out[seg_off + dst] = pos[c];
@@ -197,7 +198,7 @@ __global__ void __launch_bounds__(kSortThreads)
 
 }  // namespace
 
-hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels,
+hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels, int chunk,
                                   int32_t* vals_out, uint32_t* hist, hipStream_t stream) {
   const int64_t tiles = ceil_div(N, kSortTile);
   const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
@@ -205,14 +206,14 @@ hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int
   while ((1 << nbits) < levels + 1) ++nbits;
   uint32_t* totals = hist + S * tiles * kRadixMax;
   hipLaunchKernelGGL(radix_hist_kernel<true>, grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits, t0, t_hi,
-                     hist);
+                     chunk, hist);
   hipLaunchKernelGGL(radix_scan_kernel, dim3(unsigned(S * (kRadixMax / 64))), block, 0, stream, tiles, hist, totals);
   if (vals != nullptr)
     hipLaunchKernelGGL((radix_scatter_kernel<true, true>), grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits,
-                       t0, t_hi, hist, totals, nullptr, vals_out);
+                       t0, t_hi, chunk, hist, totals, nullptr, vals_out);
   else
     hipLaunchKernelGGL((radix_scatter_kernel<false, true>), grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits,
-                       t0, t_hi, hist, totals, nullptr, vals_out);
+                       t0, t_hi, chunk, hist, totals, nullptr, vals_out);
   return hipGetLastError();
 }
 
@@ -237,15 +238,15 @@ hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_b
     uint32_t* dst_keys = to_out ? sorted_codes : tmp_keys;
     int32_t* dst_pos = to_out ? perm : tmp_pos;
     hipLaunchKernelGGL(radix_hist_kernel<false>, grid, block, 0, stream, src_keys, nullptr, N, plan.tiles, shift,
-                       nbits, 0, 0, hist);
+                       nbits, 0, 0, 0, hist);
     hipLaunchKernelGGL(radix_scan_kernel, dim3(unsigned(S * (kRadixMax / 64))), block, 0, stream, plan.tiles, hist,
                        totals);
     if (src_pos == nullptr)
       hipLaunchKernelGGL((radix_scatter_kernel<false, false>), grid, block, 0, stream, src_keys, src_pos, N,
-                         plan.tiles, shift, nbits, 0, 0, hist, totals, dst_keys, dst_pos);
+                         plan.tiles, shift, nbits, 0, 0, 0, hist, totals, dst_keys, dst_pos);
     else
       hipLaunchKernelGGL((radix_scatter_kernel<true, false>), grid, block, 0, stream, src_keys, src_pos, N,
-                         plan.tiles, shift, nbits, 0, 0, hist, totals, dst_keys, dst_pos);
+                         plan.tiles, shift, nbits, 0, 0, 0, hist, totals, dst_keys, dst_pos);
     src_keys = dst_keys;
     src_pos = dst_pos;
   }

@@ -95,10 +95,11 @@ zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_
 }
 
 zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64_t N, int topk, int causal,
-                               int32_t* order_out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                               int chunk, int32_t* order_out, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
   if (!order_out) return ZETA_ERR_INVALID_ARG;
   if (!shape_ok(n_segments, N)) return ZETA_ERR_INVALID_ARG;
-  if (topk < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (topk < 1 || bad_pool(causal, chunk)) return ZETA_ERR_INVALID_ARG;
   if (topk > zeta::kMaxTopk) return ZETA_ERR_UNSUPPORTED;
   // In place is allowed; a partial overlap is not.
   if (q_order != nullptr && q_order != order_out &&
@@ -109,7 +110,8 @@ zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64
     const zeta::QueryOrderWs ws = zeta::query_order_ws(n_segments, N);
     if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
   }
-  return hip_status(zeta::launch_query_order(q_order, n_segments, N, topk, causal != 0, order_out, workspace, stream));
+  return hip_status(
+      zeta::launch_query_order(q_order, n_segments, N, topk, causal != 0, chunk, order_out, workspace, stream));
 }
 
 zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,

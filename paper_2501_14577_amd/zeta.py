@@ -59,7 +59,7 @@ def load_library() -> ctypes.CDLL:
     vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     L.zeta_morton_encode.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     L.zeta_sort_keys.argtypes = [vp, i64, i64, i32, vp, vp, vp, sz, vp]
-    L.zeta_query_order.argtypes = [vp, i64, i64, i32, i32, vp, vp, sz, vp]
+    L.zeta_query_order.argtypes = [vp, i64, i64, i32, i32, i32, vp, vp, sz, vp]
     L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, vp, vp, vp, sz, vp]
     L.zeta_topk_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, i32, f32, vp, vp, vp,
                                      vp]
@@ -178,10 +178,11 @@ def zeta_sort_keys(k_codes: torch.Tensor, code_bits: int, *, sorted_codes: Optio
 
 
 def zeta_query_order(q_order: Optional[torch.Tensor], N: int, S: int, topk: int, causal: bool, *,
-                     order_out: Optional[torch.Tensor] = None, device=None,
+                     chunk: int = 0, order_out: Optional[torch.Tensor] = None, device=None,
                      workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Regroup a processing order (int32 [..., N]; None: position order) by the
-    list level each query searches -> int32 order of the same shape."""
+    list level each query searches (under the causal rule ``chunk``) -> int32
+    order of the same shape."""
     dev = q_order.device if q_order is not None else device
     if order_out is None:
         shape = q_order.shape if q_order is not None else (S, N)
@@ -189,7 +190,7 @@ def zeta_query_order(q_order: Optional[torch.Tensor], N: int, S: int, topk: int,
     if workspace is None:
         workspace = workspace_for(S, 1, N, 1, 1, topk, causal, dev)
     _need_device(q_order, order_out, workspace)
-    st = load_library().zeta_query_order(_ptr(q_order), S, N, topk, int(bool(causal)), _ptr(order_out),
+    st = load_library().zeta_query_order(_ptr(q_order), S, N, topk, int(bool(causal)), int(chunk), _ptr(order_out),
                                          _ptr(workspace), workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_query_order", st)
     return order_out
@@ -367,7 +368,8 @@ def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: f
         sc2, perm2 = zeta_sort_keys(b["codes"], dk * bits, sorted_codes=b["sorted_codes2"], perm=b["perm2"],
                                     workspace=workspace)
         sc, perm = sc2[1], perm2[1]
-        order = zeta_query_order(perm2[0], N, B * H, topk, causal, order_out=b["order"], workspace=workspace)
+        order = zeta_query_order(perm2[0], N, B * H, topk, causal, chunk=chunk, order_out=b["order"],
+                                 workspace=workspace)
     else:
         sc, perm = zeta_sort_keys(kc, dk * bits, sorted_codes=b["sorted_codes2"][1], perm=b["perm2"][1],
                                   workspace=workspace)

@@ -133,7 +133,7 @@ def _sort(**kw):
 
 
 def _qord(**kw):
-    a = dict(q_order=P, S=2, N=100, topk=8, causal=1, order_out=P2, ws=P3, ws_bytes=BIG, stream=NULL)
+    a = dict(q_order=P, S=2, N=100, topk=8, causal=1, chunk=0, order_out=P2, ws=P3, ws_bytes=BIG, stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_query_order(*a.values())
 
@@ -212,6 +212,7 @@ def test_attend_rejects(kw, code):
 
 QORDER_CASES = [
     (dict(order_out=NULL), INV), (dict(S=0), INV), (dict(N=0), INV), (dict(topk=0), INV), (dict(causal=3), INV),
+    (dict(chunk=-1), INV), (dict(causal=0, chunk=8), INV),
     (dict(topk=1025), UNS), (dict(ws=NULL), WSP), (dict(ws_bytes=16), WSP),
     (dict(order_out=ctypes.c_void_p(0x10000 + 64)), INV),  # partial overlap with q_order
 ]

@@ -402,27 +402,37 @@ def test_forward_zorder_matches_position_order():
 # Query order by list level
 # ----------------------------------------------------------------------------
 
-def _expected_level_order(z, N, topk, causal):
-    """Regroup a per-segment order by the level of the list each query searches."""
+def _expected_level_order(z, N, topk, causal, chunk=0):
+    """Regroup a per-segment order by the level of the list each query's
+    pool is searched in: the largest pool position is i, or
+    floor(i / chunk) * chunk - 1 under the chunked rule (an empty pool counts
+    as the first level)."""
     t0 = max(0, (topk - 1).bit_length())
     t_hi = (N - 1).bit_length() - 1
     if not causal or t0 > t_hi:
         return z
-    lvl = np.array([min(max(t0, i.bit_length()), t_hi + 1) for i in range(N)])
+
+    def level(i):
+        lim = (i // chunk) * chunk - 1 if chunk else i
+        return t0 if lim < 0 else min(max(t0, lim.bit_length()), t_hi + 1)
+
+    lvl = np.array([level(i) for i in range(N)])
     return np.stack([zs[np.argsort(lvl[zs], kind="stable")] for zs in z])
 
 
-@pytest.mark.parametrize("N,topk,causal", [(65536, 128, True), (5000, 64, True), (300, 1024, True), (777, 8, False),
-                                           (1, 1, True), (4097, 1, True)])
-def test_query_order(N, topk, causal):
-    log(f"query order N={N} k={topk} causal={causal}")
+@pytest.mark.parametrize("N,topk,causal,chunk", [(65536, 128, True, 0), (5000, 64, True, 0), (300, 1024, True, 0),
+                                                 (777, 8, False, 0), (1, 1, True, 0), (4097, 1, True, 0),
+                                                 (65536, 128, True, 2048), (5000, 64, True, 313), (300, 16, True, 1)])
+def test_query_order(N, topk, causal, chunk):
+    log(f"query order N={N} k={topk} causal={causal} chunk={chunk}")
     S = 3
     rng = np.random.default_rng(N + topk)
     z = np.stack([rng.permutation(N) for _ in range(S)]).astype(np.int32)
-    got = host(zeta.zeta_query_order(i32_to_dev(z), N, S, topk, causal))
-    assert np.array_equal(got, _expected_level_order(z, N, topk, causal))
-    pos = host(zeta.zeta_query_order(None, N, S, topk, causal, device=device()))
-    assert np.array_equal(pos, _expected_level_order(np.tile(np.arange(N, dtype=np.int32), (S, 1)), N, topk, causal))
+    got = host(zeta.zeta_query_order(i32_to_dev(z), N, S, topk, causal, chunk=chunk))
+    assert np.array_equal(got, _expected_level_order(z, N, topk, causal, chunk))
+    pos = host(zeta.zeta_query_order(None, N, S, topk, causal, chunk=chunk, device=device()))
+    want = _expected_level_order(np.tile(np.arange(N, dtype=np.int32), (S, 1)), N, topk, causal, chunk)
+    assert np.array_equal(pos, want)
 
 
 

@@ -130,6 +130,7 @@ def test_chunked_processing_order():
     z = np.argsort(oc["q_codes"], axis=1, kind="stable").astype(np.int32)
     rng = np.random.default_rng(21)
     orders = [None, zeta.zeta_query_order(i32_to_dev(z), w.N, S, w.topk, True),
+              zeta.zeta_query_order(i32_to_dev(z), w.N, S, w.topk, True, chunk=M),
               i32_to_dev(np.stack([rng.permutation(w.N) for _ in range(S)]))]
     q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
     idxs = [zeta.zeta_select_topk(qc, sc, perm, w.topk, True, chunk=M, q_order=o) for o in orders]
