@@ -10,10 +10,13 @@ from .zeta_oracle import (  # noqa: F401
     attend,
     attend_bwd,
     bf16_bits_to_f32,
+    exact_knn,
     forward,
     history_mean,
+    index_overlap,
     interleave,
     joint_range,
+    locality_overlap,
     morton_encode,
     pool_end,
     quantise,

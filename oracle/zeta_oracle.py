@@ -34,6 +34,9 @@ defines, one function per step, each citing the passage it follows:
    rule (Section 3.2.2; Algorithm 1, Step 4), and ``attend``'s ``mode`` the
    score variants it compares with the Cauchy score (Section 4.3; Appendix
    G.2; the dot-product softmax of equation 3).
+9. The locality experiment (Section 4.4): ``exact_knn`` (the exact Euclidean
+   nearest keys of each query), ``index_overlap`` and ``locality_overlap``
+   (how many of them the Z-order window holds).
 
 Readings where the paper is silent or ambiguous (each is also listed in the
 design notes):
@@ -491,3 +494,58 @@ def forward(q: np.ndarray, k: np.ndarray, v: np.ndarray, topk: int, eps: float, 
     out = attend(q, k, v, idx, eps, mean_k=mk, mean_v=mv, mode=mode)
     return dict(q_codes=qc, k_codes=kc, lo=lo, hi=hi, sorted_codes=sorted_codes, perm=perm,
                 idx=idx, mean_k=mk, mean_v=mv, out=out)
+
+
+# ----------------------------------------------------------------------------
+# Locality preservation (Section 4.4)
+# ----------------------------------------------------------------------------
+
+def exact_knn(q: np.ndarray, k: np.ndarray, kn: int, causal: bool) -> np.ndarray:
+    """The kn keys nearest to each query in Euclidean distance, among the
+    query's pool ({0..i} when causal, all keys otherwise), ordered by
+    (distance, position) and padded with -1.
+
+    The squared distance is computed in float32 as the GPU computes it (one
+    rounding per subtraction, product and sum, axes in order, no fused
+    multiply-add), so that both take the same decision where distances tie
+    or nearly tie.  q, k: float32 [S, N, d].  Returns int32 [S, N, kn].
+    """
+    q = np.asarray(q, dtype=np.float32)
+    k = np.asarray(k, dtype=np.float32)
+    S, N, d = q.shape
+    out = np.full((S, N, kn), -1, dtype=np.int32)
+    for seg in range(S):
+        for i in range(N):
+            end = i + 1 if causal else N
+            d2 = np.zeros(end, dtype=np.float32)
+            for a in range(d):
+                diff = (q[seg, i, a] - k[seg, :end, a]).astype(np.float32)
+                d2 = (d2 + (diff * diff).astype(np.float32)).astype(np.float32)
+            order = np.lexsort((np.arange(end), d2))  # by distance, then position
+            m = min(kn, end)
+            out[seg, i, :m] = order[:m]
+    return out
+
+
+def index_overlap(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Per row, the number of indices (not -1) that rows a and b share.
+    a: int32 [..., ka], b: int32 [..., kb] with distinct valid entries per
+    row.  Returns int32 [...]."""
+    a2 = a.reshape(-1, a.shape[-1])
+    b2 = b.reshape(-1, b.shape[-1])
+    out = np.zeros(a2.shape[0], dtype=np.int32)
+    for r in range(a2.shape[0]):
+        out[r] = len(set(int(x) for x in a2[r] if x >= 0) & set(int(x) for x in b2[r] if x >= 0))
+    return out.reshape(a.shape[:-1])
+
+
+def locality_overlap(q: np.ndarray, k: np.ndarray, bits: int, kn: int = 64, causal: bool = False) -> float:
+    """The locality measure of Section 4.4: the mean, over queries, of the
+    fraction of the kn exact nearest keys (``exact_knn``) that the Z-order
+    window of the same size (``select_topk`` on ``morton_encode``'s codes)
+    also holds.  q, k: float32 [S, N, d]."""
+    qc, kc, _, _ = morton_encode(q, k, bits)
+    win = select_topk(qc, kc, kn, causal)
+    nn = exact_knn(q, k, kn, causal)
+    return float(index_overlap(win, nn).sum()) / float(np.count_nonzero(nn >= 0))
+

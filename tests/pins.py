@@ -534,6 +534,81 @@ def check_attend_modes_invariants(orc):
 
 
 # ----------------------------------------------------------------------------
+# Locality preservation (Section 4.4)
+# ----------------------------------------------------------------------------
+
+def check_locality_golden(orc):
+    """The hand-worked example in golden/locality_example.txt: windows,
+    exact nearest keys (in order), shared counts and the mean share."""
+    rows = {"window": {}, "nearest": {}}
+    vals = {}
+    for line in open(os.path.join(GOLDEN, "locality_example.txt")):
+        if line.strip() and not line.startswith("#"):
+            key, *rest = line.split()
+            if key in rows:
+                rows[key][int(rest[0])] = [int(x) for x in rest[1:]]
+            else:
+                vals[key] = rest
+    bits, kn = int(vals["bits"][0]), int(vals["kn"][0])
+    k = np.array(vals["keys"], dtype=np.float32).reshape(1, -1, 1)
+    q = np.array(vals["queries"], dtype=np.float32).reshape(1, -1, 1)
+    qc, kc, _, _ = orc.morton_encode(q, k, bits)
+    win = orc.select_topk(qc, kc, kn, False)
+    nn = orc.exact_knn(q, k, kn, False)
+    for i, w in rows["window"].items():
+        assert sorted(win[0, i]) == sorted(w), (i, win[0, i], w)
+    for i, w in rows["nearest"].items():
+        assert list(nn[0, i]) == w, (i, nn[0, i], w)
+    assert list(orc.index_overlap(win, nn)[0]) == [int(x) for x in vals["shared"]]
+    assert abs(orc.locality_overlap(q, k, bits, kn) - _frac(vals["overlap"][0])) < 1e-15
+
+
+def check_knn_brute(orc):
+    """Integer coordinates (float32 distances exact, many ties): the nearest
+    keys of every query by exact integer arithmetic, ties by position, in
+    both modes, for kn below and beyond the pool."""
+    rng = np.random.default_rng(91)
+    for d, n, kn in ((1, 12, 3), (2, 20, 5), (3, 17, 30), (5, 9, 4)):
+        q = rng.integers(-3, 4, size=(2, n, d)).astype(np.float32)
+        k = rng.integers(-3, 4, size=(2, n, d)).astype(np.float32)
+        for causal in (False, True):
+            got = orc.exact_knn(q, k, kn, causal)
+            for s in range(2):
+                for i in range(n):
+                    pool = range(i + 1) if causal else range(n)
+                    dist = {j: sum((int(q[s, i, a]) - int(k[s, j, a])) ** 2 for a in range(d)) for j in pool}
+                    want = sorted(pool, key=lambda j: (dist[j], j))[:kn]
+                    want = want + [-1] * (kn - len(want))
+                    assert list(got[s, i]) == want, (d, n, kn, causal, s, i)
+
+
+def check_knn_kdtree(orc):
+    """Random float coordinates against scipy's k-d tree (float64), on the
+    queries whose kn-th and next distances are well apart."""
+    from scipy.spatial import cKDTree
+    rng = np.random.default_rng(92)
+    n, kn = 300, 16
+    for d in (1, 3, 6):
+        q = rng.normal(size=(1, n, d)).astype(np.float32)
+        k = rng.normal(size=(1, n, d)).astype(np.float32)
+        got = orc.exact_knn(q, k, kn, False)
+        dist, ind = cKDTree(k[0].astype(np.float64)).query(q[0].astype(np.float64), k=kn + 1)
+        checked = 0
+        for i in range(n):
+            if dist[i, kn] - dist[i, kn - 1] > 1e-4 * (1.0 + dist[i, kn]):
+                assert set(got[0, i]) == set(ind[i, :kn]), (d, i)
+                checked += 1
+        assert checked > n // 2
+
+
+def check_overlap_hand(orc):
+    """Shared entries of two index rows, -1 ignored."""
+    a = np.array([[1, 2, 3, -1], [5, -1, -1, -1], [-1, -1, -1, -1]], dtype=np.int32)
+    b = np.array([[3, 4, 1], [6, 7, -1], [-1, -1, -1]], dtype=np.int32)
+    assert list(orc.index_overlap(a, b)) == [2, 0, 0]
+
+
+# ----------------------------------------------------------------------------
 # History-mean candidate (Section 3.4, last paragraph)
 # ----------------------------------------------------------------------------
 
@@ -677,6 +752,10 @@ ALL_PINS = [
     check_select_chunk_golden,
     check_select_chunk_brute,
     check_select_chunk_invariants,
+    check_locality_golden,
+    check_knn_brute,
+    check_knn_kdtree,
+    check_overlap_hand,
     check_history_mean_golden,
     check_history_mean_brute,
     check_history_attend_augmented,

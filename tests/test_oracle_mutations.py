@@ -62,6 +62,16 @@ MUTATIONS = {
     "inv_euclid: squared distance": ("return 1.0 / (np.sqrt(dd) + eps)", "return 1.0 / (dd + eps)"),
     "softmax: padding not masked": ("w = np.where(valid, np.exp(t - zmax[:, None]), 0.0)",
                                     "w = np.exp(t - zmax[:, None])"),
+    "knn: ties not by position": ("order = np.lexsort((np.arange(end), d2))  # by distance, then position",
+                                  "order = np.lexsort((-np.arange(end), d2))  # by distance, then position"),
+    "knn: causal pool includes the future": ("            end = i + 1 if causal else N\n",
+                                            "            end = min(N, i + 2) if causal else N\n"),
+    "knn: unsquared distance": ("d2 = (d2 + (diff * diff).astype(np.float32)).astype(np.float32)",
+                                "d2 = (d2 + np.abs(diff)).astype(np.float32)"),
+    "overlap counts padding": ("set(int(x) for x in a2[r] if x >= 0) & set(int(x) for x in b2[r] if x >= 0)",
+                               "set(int(x) for x in a2[r]) & set(int(x) for x in b2[r])"),
+    "locality: wrong denominator": ("return float(index_overlap(win, nn).sum()) / float(np.count_nonzero(nn >= 0))",
+                                    "return float(index_overlap(win, nn).sum()) / float(nn.size + 1)"),
     "history: sums instead of means": ("return np.cumsum(k, axis=1) / count, np.cumsum(v, axis=1) / count",
                                        "return np.cumsum(k, axis=1), np.cumsum(v, axis=1)"),
     "history: current row excluded": ("return np.cumsum(k, axis=1) / count, np.cumsum(v, axis=1) / count",
