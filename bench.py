@@ -129,6 +129,46 @@ def cpu_baseline(w: workloads.Workload, causal: bool, x: dict, heads: int):
     }
 
 
+def locality_experiment(zeta, torch, dev) -> dict:
+    """Section 4.4's locality measure on synthetic N(0,1) queries and keys:
+    the mean share of each query's 64 exact nearest keys that its Z-order
+    window of 64 holds, for N in {512, 1024, 2048} and d_k = 1..8 (16
+    segments each, not causal, bits = min(24, 32 // d_k)), with queries drawn
+    apart from the keys and, second reading, with the keys as their own
+    queries; plus the GPU time of the exact search and of the window
+    selection at N = 2048, d_k = 3."""
+    table, table_self = {}, {}
+    for n in (512, 1024, 2048):
+        for d in range(1, 9):
+            w = workloads.custom(B=1, H=16, N=n, dk=d, dtype="f32", topk=64, bits=min(24, 32 // d), seed=n * 10 + d)
+            x = workloads.generate(w)
+            q, k = (torch.from_numpy(x[m]).to(dev) for m in ("q", "k"))
+            table[f"N={n} d_k={d}"] = round(zeta.locality_overlap(q, k, w.bits, 64), 4)
+            table_self[f"N={n} d_k={d}"] = round(zeta.locality_overlap(k, k, w.bits, 64), 4)
+    w = workloads.custom(B=1, H=16, N=2048, dk=3, dtype="f32", topk=64, bits=10, seed=20483)
+    x = workloads.generate(w)
+    q, k = (torch.from_numpy(x[m]).to(dev) for m in ("q", "k"))
+    ws = zeta.workspace_for(1, 16, 2048, 3, 10, 64, False, dev)
+    qc, kc = zeta.zeta_morton_encode(q, k, 10, workspace=ws)
+    sc, perm = zeta.zeta_sort_keys(kc, 30, workspace=ws)
+    nn = zeta.zeta_exact_knn(q, k, 64, False)
+    win = zeta.zeta_select_topk(qc, sc, perm, 64, False, workspace=ws)
+    times = {}
+    for name, fn in (("exact_knn_ms", lambda: zeta.zeta_exact_knn(q, k, 64, False, knn_idx=nn)),
+                     ("select_ms", lambda: zeta.zeta_select_topk(qc, sc, perm, 64, False, idx=win, workspace=ws))):
+        fn()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(10):
+            fn()
+        stop.record()
+        torch.cuda.synchronize()
+        times[name] = start.elapsed_time(stop) / 10
+    return {"measure": "mean share of the 64 exact nearest keys held by the Z-order window of 64",
+            "overlap": table, "overlap_keys_as_queries": table_self, "timing_N2048_dk3_16_segments": times}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,14 +180,14 @@ def main() -> int:
                     help="segments in the oracle sample (0 skips the CPU baseline)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (for counter calibration)")
-    ap.add_argument("--parts", default="forward,backward,history,variants",
+    ap.add_argument("--parts", default="forward,backward,history,variants,locality",
                     help="comma list of the parts to time: forward (the metric), backward (attention gradients), "
                          "history (the history-mean candidate, forward and gradients), variants (the chunked "
-                         "causal rule and the score variants); fields of parts not timed are null, so that each "
-                         "part's profile holds only its own kernels")
+                         "causal rule and the score variants), locality (the locality experiment); fields of "
+                         "parts not timed are null, so that each part's profile holds only its own kernels")
     args = ap.parse_args()
     parts = set(args.parts.split(","))
-    if not parts <= {"forward", "backward", "history", "variants"}:
+    if not parts <= {"forward", "backward", "history", "variants", "locality"}:
         print(f"unknown part in --parts {args.parts}", file=sys.stderr)
         return 2
 
@@ -331,6 +371,8 @@ def main() -> int:
                     "chunked_value": w.B * w.N / (chunk_step_ms * 1e-3),
                     "chunked_select_attend_ms": chunk_call_ms, "score_select_attend_ms": modes}
 
+    locality = locality_experiment(zeta, torch, dev) if "locality" in parts else None
+
     h_bytes = w.segments * w.N * (w.dk + w.dv) * (elem_size(w.dtype) + 4)  # read k, v once; write the means
     if "history" in parts:
         hist_ms = timed(hist_means)[1]
@@ -416,6 +458,7 @@ def main() -> int:
             "means_frac": frac(h_bytes, hist_ms),
             "backward_ms": hist_bwd_ms,
         },
+        "locality": locality,
         "variants": None if variants is None else dict(
             variants, score_select_attend_GBs={m: gbs(f_bytes, t) for m, t in variants["score_select_attend_ms"].items()}),
         "step_hbm_frac": frac(s_bytes, ms_per_step),

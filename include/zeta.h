@@ -15,7 +15,9 @@
  *
  * zeta_topk_attn_bwd gives the attention's gradients for the same windows.
  * zeta_history_mean prepares the optional history-mean candidate that the
- * attention calls (and the gradients) add to every window.
+ * attention calls (and the gradients) add to every window.  zeta_exact_knn
+ * and zeta_index_overlap measure how well the windows keep the exact nearest
+ * keys (the locality experiment).
  *
  * zeta_select_attend_fwd runs the last two in one pass (the candidates never
  * leave the chip); zeta_query_order prepares the fast processing order.
@@ -324,6 +326,38 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
                                  const float* mean_v, int causal, float* dq, float* dk, float* dv,
                                  float* deps, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/*
+ * zeta_exact_knn -- the locality experiment's reference (Section 4.4): the kn
+ * keys nearest to each query in Euclidean distance, among the query's pool
+ * ({0..i} when causal, all N keys otherwise), ordered by (distance,
+ * position) and padded with -1.  The squared distance is evaluated in
+ * float32 with one rounding per subtraction, product and sum, axes in order
+ * (no fused multiply-add).  An exact search over the pool: meant for the
+ * experiment's sizes, not for the attention path.
+ *
+ *   q, k     [B][H][N][d_k] of `dtype`.
+ *   kn       1..ZETA_MAX_TOPK; causal 0 or 1.
+ *   knn_idx  int32 [B*H][N][kn] output.
+ * Supported N: up to 4096 (UNSUPPORTED above).
+ */
+zeta_status_t zeta_exact_knn(const void* q, const void* k, zeta_dtype_t dtype, int64_t B, int64_t H,
+                             int64_t N, int d_k, int kn, int causal, int32_t* knn_idx,
+                             hipStream_t stream);
+
+/*
+ * zeta_index_overlap -- per row, the number of positions two index rows
+ * share (entries -1 and outside 0..N-1 ignored; each row's valid entries
+ * distinct): with the windows of zeta_select_topk and the nearest keys of
+ * zeta_exact_knn it gives Section 4.4's locality measure (shared / kn).
+ *
+ *   idx_a    int32 [n_rows][ka]; idx_b int32 [n_rows][kb]; ka, kb in
+ *            1..ZETA_MAX_TOPK.
+ *   N        positions per segment (up to 65536; UNSUPPORTED above).
+ *   counts   int32 [n_rows] output.
+ */
+zeta_status_t zeta_index_overlap(const int32_t* idx_a, int ka, const int32_t* idx_b, int kb,
+                                 int64_t n_rows, int64_t N, int32_t* counts, hipStream_t stream);
 
 /*
  * zeta_workspace_size -- bytes of device workspace enough for each of

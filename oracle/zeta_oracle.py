@@ -500,7 +500,7 @@ def forward(q: np.ndarray, k: np.ndarray, v: np.ndarray, topk: int, eps: float, 
 # Locality preservation (Section 4.4)
 # ----------------------------------------------------------------------------
 
-def exact_knn(q: np.ndarray, k: np.ndarray, kn: int, causal: bool) -> np.ndarray:
+def exact_knn(q: np.ndarray, k: np.ndarray, kn: int, causal: bool, rows: Optional[np.ndarray] = None) -> np.ndarray:
     """The kn keys nearest to each query in Euclidean distance, among the
     query's pool ({0..i} when causal, all keys otherwise), ordered by
     (distance, position) and padded with -1.
@@ -508,14 +508,17 @@ def exact_knn(q: np.ndarray, k: np.ndarray, kn: int, causal: bool) -> np.ndarray
     The squared distance is computed in float32 as the GPU computes it (one
     rounding per subtraction, product and sum, axes in order, no fused
     multiply-add), so that both take the same decision where distances tie
-    or nearly tie.  q, k: float32 [S, N, d].  Returns int32 [S, N, kn].
+    or nearly tie.  q, k: float32 [S, N, d].  Returns int32 [S, N, kn] (or
+    [S, R, kn] for the R query positions ``rows``).
     """
     q = np.asarray(q, dtype=np.float32)
     k = np.asarray(k, dtype=np.float32)
     S, N, d = q.shape
-    out = np.full((S, N, kn), -1, dtype=np.int32)
+    if rows is None:
+        rows = np.arange(N)
+    out = np.full((S, len(rows), kn), -1, dtype=np.int32)
     for seg in range(S):
-        for i in range(N):
+        for r, i in enumerate(rows):
             end = i + 1 if causal else N
             d2 = np.zeros(end, dtype=np.float32)
             for a in range(d):
@@ -523,7 +526,7 @@ def exact_knn(q: np.ndarray, k: np.ndarray, kn: int, causal: bool) -> np.ndarray
                 d2 = (d2 + (diff * diff).astype(np.float32)).astype(np.float32)
             order = np.lexsort((np.arange(end), d2))  # by distance, then position
             m = min(kn, end)
-            out[seg, i, :m] = order[:m]
+            out[seg, r, :m] = order[:m]
     return out
 
 

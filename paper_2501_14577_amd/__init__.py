@@ -13,8 +13,11 @@ from .zeta import (  # noqa: F401
     library_path,
     load_library,
     bwd_workspace_for,
+    locality_overlap,
     workspace_for,
+    zeta_exact_knn,
     zeta_history_mean,
+    zeta_index_overlap,
     zeta_morton_encode,
     zeta_query_order,
     zeta_select_attend_fwd,

@@ -107,4 +107,13 @@ hipError_t launch_attend_bwd(const void* q, const void* k, const void* v, const 
                              float eps, HistMean hm, bool causal, float* dq, float* dkg, float* dvg, float* deps,
                              void* workspace, hipStream_t stream);
 
+// The locality experiment: the kn keys nearest to each query in Euclidean
+// distance within its pool (N <= kKnnMaxN), ordered by (distance, position),
+// -1 padded; and per row the number of entries two index rows share
+// (N <= kOverlapMaxN).
+hipError_t launch_exact_knn(const void* q, const void* k, bool is_bf16, int64_t S, int64_t N, int dk, int kn,
+                            bool causal, int32_t* out, hipStream_t stream);
+hipError_t launch_index_overlap(const int32_t* a, int ka, const int32_t* b, int kb, int64_t rows, int64_t N,
+                                int32_t* counts, hipStream_t stream);
+
 }  // namespace zeta

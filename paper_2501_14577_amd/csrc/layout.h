@@ -151,6 +151,12 @@ inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
+// ---- locality experiment -------------------------------------------------------
+// Keys per query sorted in LDS by the exact nearest-key search, and segment
+// length covered by the overlap count's LDS bit set.
+constexpr int kKnnMaxN = 4096;
+constexpr int64_t kOverlapMaxN = 65536;
+
 // ---- history mean ---------------------------------------------------------
 // Segmented scans over [S][N][D] matrices (values and keys together): rows
 // per chunk, and the most columns scanned at once (d_k + d_v).

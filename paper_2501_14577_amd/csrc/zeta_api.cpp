@@ -229,6 +229,24 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
                                             stream));
 }
 
+zeta_status_t zeta_exact_knn(const void* q, const void* k, zeta_dtype_t dtype, int64_t B, int64_t H, int64_t N,
+                             int d_k, int kn, int causal, int32_t* knn_idx, hipStream_t stream) {
+  if (!q || !k || !knn_idx) return ZETA_ERR_INVALID_ARG;
+  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || kn < 1 || (causal != 0 && causal != 1)) return ZETA_ERR_INVALID_ARG;
+  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
+  if (d_k > zeta::kMaxDk || kn > zeta::kMaxTopk || N > zeta::kKnnMaxN) return ZETA_ERR_UNSUPPORTED;
+  return hip_status(zeta::launch_exact_knn(q, k, dtype == ZETA_BF16, B * H, N, d_k, kn, causal != 0, knn_idx, stream));
+}
+
+zeta_status_t zeta_index_overlap(const int32_t* idx_a, int ka, const int32_t* idx_b, int kb, int64_t n_rows,
+                                 int64_t N, int32_t* counts, hipStream_t stream) {
+  if (!idx_a || !idx_b || !counts) return ZETA_ERR_INVALID_ARG;
+  if (ka < 1 || kb < 1 || n_rows < 1 || N < 1 || n_rows > kMaxElems) return ZETA_ERR_INVALID_ARG;
+  if (ka > zeta::kMaxTopk || kb > zeta::kMaxTopk || N > zeta::kOverlapMaxN) return ZETA_ERR_UNSUPPORTED;
+  return hip_status(zeta::launch_index_overlap(idx_a, ka, idx_b, kb, n_rows, N, counts, stream));
+}
+
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk, int causal) {
   if (bad_count(B, H, N) || d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32 || topk < 1) return 0;
   const int64_t S = B * H;

@@ -30,6 +30,8 @@ EXPORTED = (
     "zeta_select_attend_fwd",
     "zeta_history_mean",
     "zeta_topk_attn_bwd",
+    "zeta_exact_knn",
+    "zeta_index_overlap",
     "zeta_workspace_size",
     "zeta_bwd_workspace_size",
     "zeta_status_string",
@@ -68,11 +70,14 @@ def load_library() -> ctypes.CDLL:
     L.zeta_history_mean.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, sz, vp]
     L.zeta_topk_attn_bwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp, vp, f32, vp, vp, i32,
                                      vp, vp, vp, vp, vp, sz, vp]
+    L.zeta_exact_knn.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, i32, vp, vp]
+    L.zeta_index_overlap.argtypes = [vp, i32, vp, i32, i64, i64, vp, vp]
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_bwd_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
     for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
-                 "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_history_mean", "zeta_topk_attn_bwd"):
+                 "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_history_mean", "zeta_topk_attn_bwd", "zeta_exact_knn",
+                 "zeta_index_overlap"):
         getattr(L, name).restype = ctypes.c_int
     L.zeta_workspace_size.restype = sz
     L.zeta_bwd_workspace_size.restype = sz
@@ -343,6 +348,53 @@ def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_
                                                workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_select_attend_fwd", st)
     return out
+
+
+def zeta_exact_knn(q: torch.Tensor, k: torch.Tensor, kn: int, causal: bool, *,
+                   knn_idx: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The kn keys nearest to each query in Euclidean distance within its
+    pool, by (distance, position) -> int32 [B,H,N,kn] (-1 padded)."""
+    B, H, N, dk = q.shape
+    if knn_idx is None:
+        knn_idx = torch.empty((B, H, N, kn), dtype=torch.int32, device=q.device)
+    _need_device(q, k, knn_idx)
+    if k.shape != q.shape or k.dtype != q.dtype:
+        raise ValueError("q and k must share shape and dtype")
+    st = load_library().zeta_exact_knn(_ptr(q), _ptr(k), _dtype_code(q), B, H, N, dk, kn, int(bool(causal)),
+                                       _ptr(knn_idx), _stream())
+    _check("zeta_exact_knn", st)
+    return knn_idx
+
+
+def zeta_index_overlap(idx_a: torch.Tensor, idx_b: torch.Tensor, N: int, *,
+                       counts: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Per row, the number of positions rows of idx_a [..., ka] and idx_b
+    [..., kb] share -> int32 [...]."""
+    ka, kb = idx_a.shape[-1], idx_b.shape[-1]
+    rows = idx_a.numel() // ka
+    if idx_b.numel() // kb != rows:
+        raise ValueError("idx_a and idx_b must have the same rows")
+    if counts is None:
+        counts = torch.empty(idx_a.shape[:-1], dtype=torch.int32, device=idx_a.device)
+    _need_device(idx_a, idx_b, counts)
+    st = load_library().zeta_index_overlap(_ptr(idx_a), ka, _ptr(idx_b), kb, rows, N, _ptr(counts), _stream())
+    _check("zeta_index_overlap", st)
+    return counts
+
+
+def locality_overlap(q: torch.Tensor, k: torch.Tensor, bits: int, kn: int = 64, causal: bool = False) -> float:
+    """Section 4.4's locality measure: the mean share of each query's kn
+    exact nearest keys that its Z-order window of kn keys holds (encode,
+    sort, select, exact search and overlap count, all on the GPU)."""
+    B, H, N, dk = q.shape
+    ws = workspace_for(B, H, N, dk, bits, kn, causal, q.device)
+    qc, kc = zeta_morton_encode(q, k, bits, workspace=ws)
+    sc, perm = zeta_sort_keys(kc, dk * bits, workspace=ws)
+    win = zeta_select_topk(qc, sc, perm, kn, causal, workspace=ws)
+    nn = zeta_exact_knn(q, k, kn, causal)
+    shared = zeta_index_overlap(win, nn, N)
+    valid = (nn >= 0).sum()
+    return float(shared.sum().item()) / float(valid.item())
 
 
 def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: float, causal: bool = True,

@@ -110,6 +110,41 @@ def test_history_mean_rejects(kw, code):
     assert _hist(**kw) == code
 
 
+def _knn(**kw):
+    a = dict(q=P, k=P2, dtype=zb.ZETA_F32, B=1, H=2, N=100, d_k=3, kn=8, causal=0, out=P3, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_exact_knn(*a.values())
+
+
+KNN_CASES = [
+    (dict(q=NULL), INV), (dict(k=NULL), INV), (dict(out=NULL), INV), (dict(B=0), INV), (dict(N=0), INV),
+    (dict(d_k=0), INV), (dict(kn=0), INV), (dict(causal=2), INV),
+    (dict(dtype=3), UNS), (dict(d_k=9), UNS), (dict(kn=1025), UNS), (dict(N=4097), UNS),
+]
+
+
+@pytest.mark.parametrize("kw,code", KNN_CASES, ids=[str(c[0]) for c in KNN_CASES])
+def test_exact_knn_rejects(kw, code):
+    assert _knn(**kw) == code
+
+
+def _ovl(**kw):
+    a = dict(a=P, ka=8, b=P2, kb=8, rows=100, N=100, counts=P3, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_index_overlap(*a.values())
+
+
+OVERLAP_CASES = [
+    (dict(a=NULL), INV), (dict(b=NULL), INV), (dict(counts=NULL), INV), (dict(ka=0), INV), (dict(kb=-1), INV),
+    (dict(rows=0), INV), (dict(N=0), INV), (dict(ka=1025), UNS), (dict(kb=2000), UNS), (dict(N=65537), UNS),
+]
+
+
+@pytest.mark.parametrize("kw,code", OVERLAP_CASES, ids=[str(c[0]) for c in OVERLAP_CASES])
+def test_index_overlap_rejects(kw, code):
+    assert _ovl(**kw) == code
+
+
 def test_workspace_covers_history_mean():
     # The forward workspace also serves zeta_history_mean at the widest d_v:
     # float32 sums per (segment, chunk of 32 rows, column of k and v) and totals.

@@ -1,0 +1,90 @@
+"""GPU parity of the locality experiment (Section 4.4) against the oracle:
+the exact nearest keys (zeta_exact_knn, bit for bit: both sides decide in
+float32 without fused multiply-adds), the shared counts (zeta_index_overlap,
+exact) and the whole measure (exactly equal: every step is an integer
+decision taken the same way).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2501_14577_amd as zeta
+import workloads
+from gpu_util import device, host, i32_to_dev, log, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    device()
+    zeta.load_library()
+
+
+KNN = [
+    dict(N=1, dk=3, kn=8, dtype="f32"),
+    dict(N=37, dk=1, kn=5, dtype="bf16"),
+    dict(N=512, dk=3, kn=64, dtype="f32"),
+    dict(N=700, dk=8, kn=1024, dtype="bf16"),
+    dict(N=2048, dk=2, kn=64, dtype="bf16"),
+    dict(N=4096, dk=5, kn=33, dtype="f32"),
+]
+
+
+@pytest.mark.parametrize("shape", KNN, ids=[f"N{e['N']}-dk{e['dk']}-kn{e['kn']}-{e['dtype']}" for e in KNN])
+@pytest.mark.parametrize("causal", [False, True])
+def test_exact_knn(shape, causal):
+    w = workloads.custom(B=1, H=2, N=shape["N"], dk=shape["dk"], dtype=shape["dtype"], topk=shape["kn"], bits=4,
+                         seed=shape["N"] + shape["dk"])
+    log(f"exact knn {shape} causal={causal}")
+    x = workloads.generate(w)
+    S = w.segments
+    got = host(zeta.zeta_exact_knn(to_dev(x["q"], w.dtype), to_dev(x["k"], w.dtype), shape["kn"], causal))
+    got = got.reshape(S, w.N, shape["kn"])
+    f = {n: oracle.as_f32(x[n], w.dtype).reshape(S, w.N, -1) for n in ("q", "k")}
+    # Every query up to N = 1024, sampled queries beyond.
+    rows = np.arange(w.N) if w.N <= 1024 else np.unique(np.r_[np.arange(8), np.linspace(0, w.N - 1, 300).astype(int)])
+    want = oracle.exact_knn(f["q"], f["k"], shape["kn"], causal, rows=rows)
+    assert np.array_equal(got[:, rows], want)
+
+
+def test_index_overlap():
+    log("index overlap")
+    rng = np.random.default_rng(3)
+    rows, N = 5000, 3000
+    for ka, kb in ((64, 64), (7, 130), (1024, 3)):
+        a = np.full((rows, ka), -1, dtype=np.int32)
+        b = np.full((rows, kb), -1, dtype=np.int32)
+        for r in range(rows):
+            na = rng.integers(0, ka + 1)
+            nb = rng.integers(0, kb + 1)
+            pool = rng.choice(N, size=na + nb, replace=False) if r % 3 else rng.choice(200, size=min(200, na + nb),
+                                                                                       replace=False)
+            a[r, :min(na, len(pool))] = pool[:min(na, len(pool))]
+            rest = np.concatenate([pool[:na // 2], pool[na:]])[:nb]  # shares about half of a's entries
+            b[r, :len(rest)] = rest
+        got = host(zeta.zeta_index_overlap(i32_to_dev(a), i32_to_dev(b), N))
+        assert np.array_equal(got, oracle.index_overlap(a, b)), (ka, kb)
+
+
+def _bits(d):
+    return min(24, 32 // d)
+
+
+LOCALITY = [(512, d) for d in range(1, 9)] + [(1024, 1), (1024, 8), (2048, 3)]
+
+
+@pytest.mark.parametrize("N,d", LOCALITY)
+def test_locality_overlap(N, d):
+    """The whole measure on the GPU equals the oracle's (top-64, two
+    segments, bits = min(24, 32 // d))."""
+    w = workloads.custom(B=1, H=2, N=N, dk=d, dtype="f32", topk=64, bits=_bits(d), seed=N * 10 + d)
+    log(f"locality N={N} d={d}")
+    x = workloads.generate(w)
+    got = zeta.locality_overlap(to_dev(x["q"], "f32"), to_dev(x["k"], "f32"), _bits(d), 64)
+    f = {n: x[n].reshape(w.segments, N, d) for n in ("q", "k")}
+    want = oracle.locality_overlap(f["q"], f["k"], _bits(d), 64)
+    assert got == want, (got, want)
+    assert 0.0 < got <= 1.0
