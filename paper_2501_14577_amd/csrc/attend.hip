@@ -36,11 +36,11 @@
 namespace zeta {
 namespace {
 
-template <typename T, int DV, int DK, bool kOff32>
+template <typename T, int DV, int DK, bool kOff32, bool kVariants>
 __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
     attend_kernel(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                   const int32_t* __restrict__ idx, const int32_t* __restrict__ q_order, int64_t total,
-                  int64_t N, int dk_rt, int topk, int score, float eps, const float* __restrict__ mk,
+                  int64_t N, int dk_rt, int topk, int score_rt, float eps, const float* __restrict__ mk,
                   const float* __restrict__ mv, T* __restrict__ out) {
   constexpr int kE = Vec16<T>::kElems;  // elements per lane load
   constexpr int kLpr = DV / kE;         // lanes per value row
@@ -51,6 +51,8 @@ __global__ void __launch_bounds__(kAttWavesPerBlock * 64)
   using Off = typename RowOff<kOff32>::type;
   constexpr int KD = DK > 0 ? DK : kMaxDk;
   const int dk = DK > 0 ? DK : dk_rt;
+  // The Cauchy instantiation (kVariants false) carries none of the variants' code.
+  const int score = kVariants ? score_rt : int(kScoreCauchy);
   const float rsd = 1.0f / sqrtf(float(dk));
   const bool softmax = score_is_softmax(score);
 
@@ -227,14 +229,23 @@ hipError_t launch_attend_t(const void* q, const void* k, const void* v, int64_t 
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const bool off32 = N * int64_t(DV) * int64_t(sizeof(T)) <= int64_t(0xFFFFFFFFu) - int64_t(DV) * int64_t(sizeof(T));
   const size_t lds = size_t(kAttWavesPerBlock) * topk * ((off32 ? 4 : 8) + 4);
-  if (off32)
-    hipLaunchKernelGGL((attend_kernel<T, DV, DK, true>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx,
-                       q_order, total, N, dk, topk, score, eps, hm.k, hm.v, static_cast<T*>(out));
-  else
-    hipLaunchKernelGGL((attend_kernel<T, DV, DK, false>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx,
-                       q_order, total, N, dk, topk, score, eps, hm.k, hm.v, static_cast<T*>(out));
+#define ZETA_ATTEND_LAUNCH(OFF, VAR)                                                                         \
+  hipLaunchKernelGGL((attend_kernel<T, DV, DK, OFF, VAR>), dim3(blocks), dim3(kAttWavesPerBlock * 64), lds, stream, \
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), idx, q_order,   \
+                     total, N, dk, topk, score, eps, hm.k, hm.v, static_cast<T*>(out))
+  const bool var = score != kScoreCauchy;
+  if (off32) {
+    if (var)
+      ZETA_ATTEND_LAUNCH(true, true);
+    else
+      ZETA_ATTEND_LAUNCH(true, false);
+  } else {
+    if (var)
+      ZETA_ATTEND_LAUNCH(false, true);
+    else
+      ZETA_ATTEND_LAUNCH(false, false);
+  }
+#undef ZETA_ATTEND_LAUNCH
   return hipGetLastError();
 }
 

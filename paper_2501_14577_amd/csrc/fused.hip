@@ -24,14 +24,14 @@ namespace {
 constexpr int kFusedWaves = 8;  // wavefronts per block
 constexpr int kFusedRun = 8;    // consecutive processing-order slots per wavefront
 
-template <typename T, int DV, int DK, bool kOff32>
+template <typename T, int DV, int DK, bool kOff32, bool kVariants>
 __global__ void __launch_bounds__(kFusedWaves * 64)
     select_attend_kernel(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                          const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
                          const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                          const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
                          int64_t N, int dk_rt, int topk, int causal, int chunk, int t0, int t_hi, int64_t cap,
-                         int score, float eps, const float* __restrict__ mk, const float* __restrict__ mv,
+                         int score_rt, float eps, const float* __restrict__ mk, const float* __restrict__ mv,
                          T* __restrict__ out, int32_t* __restrict__ idx_out) {
   constexpr int kE = Vec16<T>::kElems;
   constexpr int kLpr = DV / kE;
@@ -42,6 +42,8 @@ __global__ void __launch_bounds__(kFusedWaves * 64)
   using Off = typename RowOff<kOff32>::type;
   constexpr int KD = DK > 0 ? DK : kMaxDk;
   const int dk = DK > 0 ? DK : dk_rt;
+  // The Cauchy instantiation (kVariants false) carries none of the variants' code.
+  const int score = kVariants ? score_rt : int(kScoreCauchy);
   const float rsd = 1.0f / sqrtf(float(dk));
   const bool softmax = score_is_softmax(score);
 
@@ -252,16 +254,24 @@ hipError_t launch_t(const void* q, const void* k, const void* v, int64_t S, int6
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const bool off32 = N * int64_t(DV) * int64_t(sizeof(T)) <= int64_t(0xFFFFFFFFu) - int64_t(DV) * int64_t(sizeof(T));
   const size_t lds = size_t(kFusedWaves) * topk * (8 + (off32 ? 4 : 8) + 4);
-  if (off32)
-    hipLaunchKernelGGL((select_attend_kernel<T, DV, DK, true>), dim3(blocks), dim3(kFusedWaves * 64), lds, stream,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), q_codes,
-                       sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, chunk, lp.t0,
-                       lp.t_hi, lp.cap, score, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
-  else
-    hipLaunchKernelGGL((select_attend_kernel<T, DV, DK, false>), dim3(blocks), dim3(kFusedWaves * 64), lds, stream,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), q_codes,
-                       sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, chunk, lp.t0,
-                       lp.t_hi, lp.cap, score, eps, hm.k, hm.v, static_cast<T*>(out), idx_out);
+#define ZETA_FUSED_LAUNCH(OFF, VAR)                                                                            \
+  hipLaunchKernelGGL((select_attend_kernel<T, DV, DK, OFF, VAR>), dim3(blocks), dim3(kFusedWaves * 64), lds, stream, \
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), q_codes,          \
+                     sorted_codes, perm, list_codes, list_pos, q_order, total, N, dk, topk, causal ? 1 : 0, chunk,  \
+                     lp.t0, lp.t_hi, lp.cap, score, eps, hm.k, hm.v, static_cast<T*>(out), idx_out)
+  const bool var = score != kScoreCauchy;
+  if (off32) {
+    if (var)
+      ZETA_FUSED_LAUNCH(true, true);
+    else
+      ZETA_FUSED_LAUNCH(true, false);
+  } else {
+    if (var)
+      ZETA_FUSED_LAUNCH(false, true);
+    else
+      ZETA_FUSED_LAUNCH(false, false);
+  }
+#undef ZETA_FUSED_LAUNCH
   return hipGetLastError();
 }
 
