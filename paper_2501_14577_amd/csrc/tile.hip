@@ -518,12 +518,14 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         }
       }
       const uint16_t* vseg = v + g_seg * N * DV;
+      const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(vseg);
       const uint16_t* kseg = k + g_seg * N * dk;
       const Off col = Off(qn * E);
 
       // Window and pool tests as single unsigned compares: entry r is in the
       // window when r - a <= b - a, its position in the pool when
-      // pos <= limit (a missing entry holds -1, i.e. 0xFFFFFFFF).
+      // pos <= limit (an entry past the list's end holds position 0 and lies
+      // outside every window).
       const uint32_t span = mine ? uint32_t(my_b - my_a) : 0u;
       const int32_t a_eff = mine ? my_a : INT32_MIN;
       const uint32_t lim_u = uint32_t(my_lim);
@@ -554,7 +556,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         for (int kk = 0; kk < 4; ++kk) {
           const int32_t r = r0 + kg * 4 + kk;
           const int32_t pv = pvs[kk];
-          const bool in = live && uint32_t(r - a_eff) <= span && uint32_t(pv) <= lim_u;
+          const bool in = live && uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pv) <= lim_u;
           float d2 = 0.0f;
 #pragma unroll
           for (int a = 0; a < KD; ++a) {
@@ -576,9 +578,14 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           bh[t] = hw;
           bl[t] = __builtin_bit_cast(uint32_t, l);
         }
+        // A wave-uniform base and a 32-bit byte offset per lane (when the
+        // segment's values span under 4 GiB), so the loads need no 64-bit
+        // address arithmetic.
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-          load_words<W>(vseg + (Off(pvs[kk] < 0 ? 0 : pvs[kk]) * Off(DV) + col), raw[kk]);
+        for (int kk = 0; kk < 4; ++kk) {
+          const Off boff = (Off(pvs[kk]) * Off(DV) + col) * Off(2);
+          load_words<W>(reinterpret_cast<const uint16_t*>(vbytes + boff), raw[kk]);
+        }
       };
       // acc[j] += V^T (block j) * S^T for one chunk, high and low score parts.
       auto mma = [&](const uint32_t(&raw)[4][W], const uint32_t(&bh)[2], const uint32_t(&bl)[2]) {
@@ -592,8 +599,10 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           Frag a;
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
+            // One byte permute: element j of two consecutive rows, x below y
+            // (the low halves for even j, the high halves for odd j).
             const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
-            a.w[t] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+            a.w[t] = __builtin_amdgcn_perm(y, x, (j & 1) ? 0x07060302u : 0x05040100u);
           }
           acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.v, b_hi.v, acc[j], 0, 0, 0);
           acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.v, b_lo.v, acc[j], 0, 0, 0);
@@ -627,7 +636,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
           for (int t = 0; t < kStageEntries / 64; ++t) {
             const int e = t * 64 + lane;
-            pv[t] = -1;
+            pv[t] = 0;  // an entry past the list's end: outside every window
             kw[t] = make_uint2(0u, 0u);
             if (e < nch * kChunk) {
               const int32_t r = s_ch[wave][e / kChunk] * kChunk + (e % kChunk);
@@ -642,19 +651,14 @@ __global__ void __launch_bounds__(kTileWaves * 64)
             const int e = t * 64 + lane;
             if (e < nch * kChunk) {
               float kv[KD];
-              if (pv[t] >= 0) {
-                if constexpr (DK == 3) {
-                  kv[0] = __uint_as_float(kw[t].x << 16);
-                  kv[1] = __uint_as_float(kw[t].x & 0xFFFF0000u);
-                  kv[2] = __uint_as_float(kw[t].y << 16);
-                } else {
-#pragma unroll
-                  for (int a = 0; a < KD; ++a)
-                    kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv[t]) * dk + a]) : 0.0f;
-                }
+              if constexpr (DK == 3) {
+                kv[0] = __uint_as_float(kw[t].x << 16);
+                kv[1] = __uint_as_float(kw[t].x & 0xFFFF0000u);
+                kv[2] = __uint_as_float(kw[t].y << 16);
               } else {
 #pragma unroll
-                for (int a = 0; a < KD; ++a) kv[a] = 0.0f;
+                for (int a = 0; a < KD; ++a)
+                  kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv[t]) * dk + a]) : 0.0f;
               }
               s_pos[wave][e] = pv[t];
 #pragma unroll
