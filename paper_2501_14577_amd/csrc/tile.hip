@@ -134,8 +134,8 @@ __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t (&o)[W]) 
 // or when its query searches another list.  With idx_out the run's windows
 // are also written as position rows, one wavefront-wide pass per query.
 constexpr int kBndWaves = 4;
-constexpr int kRegion = 1024;  // list entries staged per wavefront
-constexpr int kMargin = 384;   // of them before the run's first insertion point
+constexpr int kRegion = 512;   // list entries staged per wavefront
+constexpr int kMargin = 192;    // of them before the run's first insertion point
 
 // Each wavefront's copy of a list range, in LDS.  Declared at file scope and
 // indexed directly, so that every access compiles to an LDS instruction (a
@@ -149,48 +149,63 @@ struct LaneList {
   const int32_t* pos;
   int wave;
   int32_t n, limit, r0, r1;  // [r0, r1): the range copied to LDS (empty when not staged)
-  __device__ __forceinline__ int32_t staged_position(int32_t e) const { return s_bnd_pos[wave][e - r0]; }
-  __device__ __forceinline__ int32_t position(int32_t e) const {
-    return (e >= r0 && e < r1) ? s_bnd_pos[wave][e - r0] : pos[e];
-  }
 };
+
+constexpr int kScanStep = 16;  // list entries examined per step of lane_scan
+
+// Bit j set when entry lo + j is in the query's pool.  A block inside the LDS
+// copy is read from there; any other block from the list itself, with entries
+// outside [0, n) counted out.  Both branches are straight-line code, so a
+// block's reads issue together and the lane waits once for them.
+__device__ __forceinline__ uint32_t pool_bits(const LaneList& L, int32_t lo) {
+  uint32_t mask = 0u;
+  if (lo >= L.r0 && lo + kScanStep <= L.r1) {
+    const int32_t b = lo - L.r0;
+#pragma unroll
+    for (int j = 0; j < kScanStep; ++j) mask |= (s_bnd_pos[L.wave][b + j] <= L.limit ? 1u : 0u) << j;
+  } else {
+    using G = __attribute__((address_space(1))) const int32_t;
+    G* gp = (G*)L.pos;
+    int32_t v[kScanStep];
+#pragma unroll
+    for (int j = 0; j < kScanStep; ++j) {
+      const int32_t x = lo + j;
+      v[j] = gp[x < 0 ? 0 : (x < L.n ? x : L.n - 1)];
+    }
+#pragma unroll
+    for (int j = 0; j < kScanStep; ++j) {
+      const int32_t x = lo + j;
+      mask |= (x >= 0 && x < L.n && v[j] <= L.limit ? 1u : 0u) << j;
+    }
+  }
+  return mask;
+}
 
 // Scan from entry e in direction dir (+1 or -1) for up to `need` in-pool
 // entries beyond the `got` already taken; records the first and last entry
 // taken (first only when got is 0).  Returns the new count; `e` ends just
 // past the last entry taken, or past the list's end.  Entries are examined
-// 8 at a time as a bit mask (bit j: entry e + dir*j is in the pool); only
-// the block where the count is reached is searched bit by bit.
+// kScanStep at a time as a bit mask (bit j: entry e + dir*j is in the pool);
+// only the block where the count is reached is searched bit by bit.  Called
+// only with n > 0.
 __device__ __forceinline__ int lane_scan(const LaneList& L, int32_t& e, int dir, int need, int got, int32_t& first,
                                          int32_t& last) {
-  constexpr int kStep = 8;
   while (got < need && e >= 0 && e < L.n) {
-    // Lowest index of the block and whether all of it is in the LDS copy.
-    const int32_t lo = dir > 0 ? e : e - (kStep - 1);
-    const bool local = lo >= L.r0 && lo + kStep <= L.r1;
-    uint32_t mask = 0u;
-#pragma unroll
-    for (int j = 0; j < kStep; ++j) {
-      const int32_t x = lo + j;  // ascending list order
-      int32_t v;
-      if (local)
-        v = L.staged_position(x);
-      else
-        v = (x >= 0 && x < L.n) ? L.position(x) : INT32_MAX;
-      mask |= (v <= L.limit ? 1u : 0u) << j;
-    }
+    // Lowest index of the block, in ascending list order.
+    const int32_t lo = dir > 0 ? e : e - (kScanStep - 1);
+    uint32_t mask = pool_bits(L, lo);
     // Bit j of `mask` is entry lo + j; reorder so bit j is entry e + dir*j.
-    if (dir < 0) mask = __builtin_bitreverse32(mask) >> (32 - kStep);
+    if (dir < 0) mask = __builtin_bitreverse32(mask) >> (32 - kScanStep);
     const int cnt = __popc(mask);
     if (cnt == 0) {
-      e += dir * kStep;
+      e += dir * kScanStep;
       continue;
     }
     if (got == 0) first = e + dir * (__ffs(int(mask)) - 1);
     if (got + cnt < need) {
       got += cnt;
       last = e + dir * (31 - __clz(int(mask)));
-      e += dir * kStep;
+      e += dir * kScanStep;
     } else {
       // The (need - got)-th set bit ends the scan.
       uint32_t m = mask;
