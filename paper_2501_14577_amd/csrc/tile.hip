@@ -79,7 +79,16 @@ __device__ __forceinline__ int wave_min_int(int x) {
     const int y = __shfl_xor(x, off, 64);
     x = y < x ? y : x;
   }
-  return x;
+  return __builtin_amdgcn_readfirstlane(x);
+}
+
+__device__ __forceinline__ int wave_max_int(int x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const int y = __shfl_xor(x, off, 64);
+    x = y > x ? y : x;
+  }
+  return __builtin_amdgcn_readfirstlane(x);
 }
 
 // Lane `src`'s value of a pointer, read by every lane.  Each 32-bit half goes
@@ -431,7 +440,6 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
 
-  __shared__ int32_t s_ch[kTileWaves][kStage];
   // Key rows padded to a multiple of 4 floats, so 4 consecutive entries'
   // positions and each key row are whole 16-byte LDS reads.
   constexpr int KD4 = (KD + 3) / 4 * 4;
@@ -553,10 +561,10 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // takes has weight 0).  The reciprocal is the hardware one (1 ulp).  A
       // score s is split as hi = bf16(s) and lo = bf16(s - hi), both rounded
       // to nearest even; s - hi is exact, so hi + lo is within 2^-17 of s.
-      auto prep = [&](int ch, int nch_, uint32_t(&raw)[4][W], uint32_t(&bh)[2], uint32_t(&bl)[2]) {
+      auto prep = [&](int cb, int ch, int nch_, uint32_t(&raw)[4][W], uint32_t(&bh)[2], uint32_t(&bl)[2]) {
         const bool live = ch < nch_;
         const int chc = live ? ch : 0;
-        const int32_t r0 = s_ch[wave][chc] * kChunk;
+        const int32_t r0 = (cb + chc) * kChunk;
         float sc[4];
         int32_t pvs[4];
         {
@@ -624,80 +632,77 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         }
       };
 
-      // The chunks that meet some window, in list order, kStage at a time.
-      int c = wave_min_int(mine ? my_a / kChunk : INT32_MAX);
-      while (c != INT32_MAX) {
-        int nch = 0;
-        while (c != INT32_MAX && nch < kStage) {
-          if (lane == 0) s_ch[wave][nch] = c;
-          ++nch;
-          // The next chunk: c + 1 when a window meets it (the common case),
-          // else the first chunk of the next window that lies beyond c.
-          const int nxt = c + 1;
-          const int32_t lo = nxt * kChunk;
-          if (wave_ballot(mine && my_a < lo + kChunk && my_b >= lo) != 0ull) {
-            c = nxt;
-          } else {
-            const int cand = (mine && my_b >= lo) ? (my_a / kChunk > nxt ? my_a / kChunk : nxt) : INT32_MAX;
-            c = wave_min_int(cand);
-          }
+      // The chunks that meet some window, in list order: run by run (a run is
+      // a stretch of chunks the windows cover without a gap; nearly always one
+      // per tile), each run kStage chunks at a time.
+      const int a_ch = mine ? my_a / kChunk : INT32_MAX;
+      const int b_ch = mine ? my_b / kChunk : INT32_MIN;
+      for (int c = wave_min_int(a_ch); c != INT32_MAX;) {
+        // Extend the run to the last chunk of every window that starts in it
+        // or right after it.
+        int e = c - 1;
+        for (;;) {
+          const int e2 = wave_max_int(a_ch <= e + 1 ? b_ch : e);
+          if (e2 == e) break;
+          e = e2;
         }
-        wave_lds_sync();
-
-        // Stage the positions, then the key rows, of all nch chunks.
-        {
-          int32_t pv[kStageEntries / 64];
-          uint2 kw[kStageEntries / 64];  // d_k = 3: key rows read in list order with the positions
+        for (int cb = c; cb <= e; cb += kStage) {
+          const int nch = e - cb + 1 < kStage ? e - cb + 1 : kStage;
+          // Stage the positions and key rows of list entries cb*kChunk ..
+          // (cb + nch)*kChunk - 1.
+          {
+            const int32_t base = cb * kChunk;
+            int32_t pv[kStageEntries / 64];
+            uint2 kw[kStageEntries / 64];  // d_k = 3: key rows read in list order with the positions
 #pragma unroll
-          for (int t = 0; t < kStageEntries / 64; ++t) {
-            const int e = t * 64 + lane;
-            pv[t] = 0;  // an entry past the list's end: outside every window
-            kw[t] = make_uint2(0u, 0u);
-            if (e < nch * kChunk) {
-              const int32_t r = s_ch[wave][e / kChunk] * kChunk + (e % kChunk);
-              if (r < ln) {
+            for (int t = 0; t < kStageEntries / 64; ++t) {
+              const int e_ = t * 64 + lane;
+              const int32_t r = base + e_;
+              pv[t] = 0;  // an entry past the list's end: outside every window
+              kw[t] = make_uint2(0u, 0u);
+              if (e_ < nch * kChunk && r < ln) {
                 pv[t] = lpos[r];
                 if constexpr (DK == 3) kw[t] = lkey[r];
               }
             }
-          }
 #pragma unroll
-          for (int t = 0; t < kStageEntries / 64; ++t) {
-            const int e = t * 64 + lane;
-            if (e < nch * kChunk) {
-              float kv[KD];
-              if constexpr (DK == 3) {
-                kv[0] = __uint_as_float(kw[t].x << 16);
-                kv[1] = __uint_as_float(kw[t].x & 0xFFFF0000u);
-                kv[2] = __uint_as_float(kw[t].y << 16);
-              } else {
+            for (int t = 0; t < kStageEntries / 64; ++t) {
+              const int e_ = t * 64 + lane;
+              if (e_ < nch * kChunk) {
+                float kv[KD];
+                if constexpr (DK == 3) {
+                  kv[0] = __uint_as_float(kw[t].x << 16);
+                  kv[1] = __uint_as_float(kw[t].x & 0xFFFF0000u);
+                  kv[2] = __uint_as_float(kw[t].y << 16);
+                } else {
 #pragma unroll
-                for (int a = 0; a < KD; ++a)
-                  kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv[t]) * dk + a]) : 0.0f;
+                  for (int a = 0; a < KD; ++a)
+                    kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv[t]) * dk + a]) : 0.0f;
+                }
+                s_pos[wave][e_] = pv[t];
+#pragma unroll
+                for (int a = 0; a < KD4; a += 4)
+                  *reinterpret_cast<float4*>(&s_k[wave][e_][a]) =
+                      make_float4(kv[a], a + 1 < KD ? kv[a + 1] : 0.0f, a + 2 < KD ? kv[a + 2] : 0.0f,
+                                  a + 3 < KD ? kv[a + 3] : 0.0f);
               }
-              s_pos[wave][e] = pv[t];
-#pragma unroll
-              for (int a = 0; a < KD4; a += 4)
-                *reinterpret_cast<float4*>(&s_k[wave][e][a]) =
-                    make_float4(kv[a], a + 1 < KD ? kv[a + 1] : 0.0f, a + 2 < KD ? kv[a + 2] : 0.0f,
-                                a + 3 < KD ? kv[a + 3] : 0.0f);
             }
           }
-        }
-        wave_lds_sync();
+          wave_lds_sync();
 
-        // Value rows of chunk ch+1 load while chunk ch is multiplied.
-        const int nchu = __builtin_amdgcn_readfirstlane(nch);
-        uint32_t rA[4][W], rB[4][W], hA[2], lA[2], hB[2], lB[2];
-        prep(0, nchu, rA, hA, lA);
-        for (int ch = 0; ch < nchu; ch += 2) {
-          prep(ch + 1, nchu, rB, hB, lB);
-          mma(rA, hA, lA);
-          if (ch + 1 >= nchu) break;
-          prep(ch + 2, nchu, rA, hA, lA);
-          mma(rB, hB, lB);
+          // Value rows of chunk ch+1 load while chunk ch is multiplied.
+          uint32_t rA[4][W], rB[4][W], hA[2], lA[2], hB[2], lB[2];
+          prep(cb, 0, nch, rA, hA, lA);
+          for (int ch = 0; ch < nch; ch += 2) {
+            prep(cb, ch + 1, nch, rB, hB, lB);
+            mma(rA, hA, lA);
+            if (ch + 1 >= nch) break;
+            prep(cb, ch + 2, nch, rA, hA, lA);
+            mma(rB, hB, lB);
+          }
+          wave_lds_sync();
         }
-        wave_lds_sync();
+        c = wave_min_int(a_ch > e ? a_ch : INT32_MAX);
       }
 
       // Normalise and store: lane holds columns 4kg..4kg+3 of every block,
