@@ -23,8 +23,8 @@
 //       - loads each entry's value row once for the whole tile (the next
 //         chunk's rows load while the current chunk is multiplied);
 //       - accumulates V^T (16 value columns x 16 entries) times S^T (16
-//         entries x 16 queries) with v_mfma_f32_16x16x16_bf16, once per 16
-//         value columns.
+//         entries x 16 queries), for the high and low score parts together,
+//         with one v_mfma_f32_16x16x32_bf16 per 16 value columns.
 // Only the weighted sum runs on the matrix cores: it is a dense contraction
 // with reuse, since each staged value row is loaded once and serves all 16
 // queries of the tile (about half of the 16 x chunk scores are nonzero).  The
@@ -32,16 +32,19 @@
 //
 // Scores are float32 (hardware reciprocal, 1 ulp); each is split into a
 // bfloat16 high part and a bfloat16 remainder, and both products are
-// accumulated, so the weights carry 16 significant bits and the products are
-// exact in the float32 accumulator.
+// accumulated (the product's 32 K slots hold the 16 entries twice), so the
+// weights carry 16 significant bits and the products are exact in the
+// float32 accumulator.
 // The normaliser sums the float32 scores.  The optional history-mean
 // candidate (Section 3.4, last paragraph) is each query's own row, so each
 // lane starts its accumulators and the normaliser from it, in float32.
 //
-// Operand layout of the 16x16x16 product (lane l, kg = l / 16):
-//   A (value columns x entries): lane l holds entries 4kg..4kg+3 of column
-//     l % 16;
-//   B (entries x queries): entries 4kg..4kg+3 of query l % 16;
+// Operand layout of the product (lane l, kg = l / 16; lane l holds 8 of the
+// 32 K slots):
+//   A (value columns x slots): lane l holds entries 4kg..4kg+3 of column
+//     l % 16, twice;
+//   B (slots x queries): the high parts of entries 4kg..4kg+3 of query l % 16,
+//     then their low parts;
 //   D (columns x queries): columns 4kg..4kg+3 of query l % 16.
 // Column c of block j is value element c * E + j (E = d_v / 16), so a lane
 // loads E consecutive elements of each of its 4 rows with one instruction and
@@ -68,9 +71,16 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
 union Frag {  // four bfloat16 values
   uint32_t w[2];
   s16x4_t v;
+};
+
+union Frag8 {  // eight bfloat16 values
+  uint32_t w[4];
+  bf16x8_t v;
 };
 
 __device__ __forceinline__ int wave_min_int(int x) {
@@ -610,25 +620,29 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           load_words<W>(reinterpret_cast<const uint16_t*>(vbytes + boff), raw[kk]);
         }
       };
-      // acc[j] += V^T (block j) * S^T for one chunk, high and low score parts.
+      // acc[j] += V^T (block j) * S^T for one chunk, high and low score parts
+      // in one 16x16x32 product: a lane's eight K slots hold its 4 entries'
+      // values twice, against their high and then their low score parts (A
+      // and B slots correspond lane by lane, so the sum pairs each value with
+      // both parts of its own score).
       auto mma = [&](const uint32_t(&raw)[4][W], const uint32_t(&bh)[2], const uint32_t(&bl)[2]) {
-        Frag b_hi, b_lo;
-        b_hi.w[0] = bh[0];
-        b_hi.w[1] = bh[1];
-        b_lo.w[0] = bl[0];
-        b_lo.w[1] = bl[1];
+        Frag8 b;
+        b.w[0] = bh[0];
+        b.w[1] = bh[1];
+        b.w[2] = bl[0];
+        b.w[3] = bl[1];
 #pragma unroll
         for (int j = 0; j < E; ++j) {
-          Frag a;
+          Frag8 a;
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
             // One byte permute: element j of two consecutive rows, x below y
             // (the low halves for even j, the high halves for odd j).
             const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
             a.w[t] = __builtin_amdgcn_perm(y, x, (j & 1) ? 0x07060302u : 0x05040100u);
+            a.w[t + 2] = a.w[t];
           }
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.v, b_hi.v, acc[j], 0, 0, 0);
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.v, b_lo.v, acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc[j], 0, 0, 0);
         }
       };
 
