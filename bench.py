@@ -304,6 +304,20 @@ def main() -> int:
     b_bytes = bwd_bytes(w, causal)
     bwd_ms = timed(bwd)[0] if "backward" in parts else None
 
+    # The one-pass call's gradients (zeta_select_attend_bwd): the same
+    # windows, from the lists, without an index tensor.
+    tws = zeta.select_attend_bwd_workspace_for(w.B, w.H, w.N, w.dv, w.topk, causal, dev)
+
+    def bwd_one_pass(ev=None):
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_select_attend_bwd(q, k, v, codes[0], sorted2[1], perm2[1], w.topk, causal, eps, dout,
+                                    q_order=bufs["order"], dq=gq, dk=gk, dv=gv, deps=geps, workspace=tws)
+        if ev is not None:
+            ev[1].record()
+
+    one_bwd_ms = timed(bwd_one_pass)[0] if "backward" in parts else None
+
     # The history-mean candidate: the means (zeta_history_mean) timed alone,
     # the one-pass step with the candidate, and the gradients with it.
     mk = torch.empty((w.B, w.H, w.N, w.dk), **f32)
@@ -447,6 +461,10 @@ def main() -> int:
             "algorithmic_bytes": b_bytes,
             "achieved_GBs": gbs(b_bytes, bwd_ms),
             "frac": frac(b_bytes, bwd_ms),
+            "one_pass_ms": one_bwd_ms,
+            "one_pass_achieved_GBs": gbs(b_bytes, one_bwd_ms),
+            "one_pass_frac": frac(b_bytes, one_bwd_ms),
+            "forward_backward_ms": (ms_per_step + one_bwd_ms) if (ms_per_step and one_bwd_ms) else None,
         },
         "history_mean": {
             "step_ms": hist_step_ms,

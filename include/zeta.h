@@ -328,6 +328,42 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
                                  hipStream_t stream);
 
 /*
+ * zeta_select_attend_bwd -- the gradients of zeta_topk_attn_bwd (same
+ * definitions, Appendix E.2) for the windows zeta_select_attend_fwd selects,
+ * computed from the lists as the one-pass call does, without an index tensor:
+ * bfloat16 inputs, d_k = 3, the Cauchy score, no history-mean candidate.
+ * 16 neighbouring queries of the processing order form a tile.  A query pass
+ * walks each tile's windows and gives dq, Z_i, c_i = dout_i . o_i and the
+ * tile's window range per list; a key pass per list then takes 16 list
+ * entries at a time and sums over the tiles whose windows meet them.  The dot
+ * products dout_i . v_j and the sums of A_ij dout_i over queries run on the
+ * matrix cores (A_ij split into two bfloat16 parts, float32 accumulation);
+ * everything else is float32.  dk and dv are summed per list, the full sorted
+ * list first and then the prefix lists, in a fixed order without atomics: the
+ * outputs are the same from run to run for a given q_order (the bits of dk
+ * and dv depend on which queries share a tile).  Any q_order is correct; with
+ * the one from zeta_query_order each list entry meets few tiles.
+ *
+ *   q, k, v, dtype, B, H, N, d_k, d_v, topk, causal, chunk, q_codes,
+ *            sorted_codes, perm, q_order, eps: as for zeta_select_attend_fwd.
+ *   dout     [B][H][N][d_v] bfloat16, 16-byte aligned: dL/do.
+ *   dq, dk   float32 [B][H][N][d_k] outputs; dv float32 [B][H][N][d_v],
+ *            16-byte aligned; deps float32 [1].  Every element is written.
+ *   workspace  at least zeta_select_attend_bwd_workspace_size(...) bytes,
+ *            16-byte aligned.
+ * Supported: dtype ZETA_BF16, d_k = 3, d_v 32, 64, 128 or 256 (otherwise
+ * UNSUPPORTED: zeta_topk_attn_bwd serves those).  The outputs must be
+ * distinct buffers and none may be an input (INVALID_ARG).
+ */
+zeta_status_t zeta_select_attend_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype,
+                                     int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
+                                     int causal, int chunk, const uint32_t* q_codes,
+                                     const uint32_t* sorted_codes, const int32_t* perm,
+                                     const int32_t* q_order, const void* dout, float eps, float* dq,
+                                     float* dk, float* dv, float* deps, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
+/*
  * zeta_exact_knn -- the locality experiment's reference (Section 4.4): the kn
  * keys nearest to each query in Euclidean distance, among the query's pool
  * ({0..i} when causal, all N keys otherwise), ordered by (distance,
@@ -381,6 +417,17 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
  */
 size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
                                int history_mean);
+
+/*
+ * zeta_select_attend_bwd_workspace_size -- bytes of device workspace for
+ * zeta_select_attend_bwd on this shape: the one-pass call's lists, window
+ * bounds and key rows, 36 + 2 * d_v bytes per row (a 32-byte record of the
+ * row's query, a copy of its dout row and its part of deps), 16 bytes per
+ * tile of 16 rows and list, and 4 KiB of sums.  Returns 0 for invalid shapes
+ * and unsupported d_v.
+ */
+size_t zeta_select_attend_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_v, int topk,
+                                             int causal);
 
 /* Static, human-readable name of a status code. */
 const char* zeta_status_string(zeta_status_t status);

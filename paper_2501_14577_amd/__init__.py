@@ -21,6 +21,9 @@ from .zeta import (  # noqa: F401
     zeta_morton_encode,
     zeta_query_order,
     zeta_select_attend_fwd,
+    zeta_select_attend_bwd,
+    zeta_select_attend_bwd_workspace_size,
+    select_attend_bwd_workspace_for,
     zeta_select_topk,
     zeta_sort_keys,
     zeta_status_string,

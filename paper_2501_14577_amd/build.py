@@ -28,7 +28,7 @@ COMMON = [
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 SOURCES = ["encode.hip", "sort.hip", "select.hip", "attend.hip", "fused.hip", "tile.hip", "attend_bwd.hip", "history.hip",
-           "locality.hip", "zeta_api.cpp"]
+           "locality.hip", "tile_bwd.hip", "zeta_api.cpp"]
 
 
 def hipcc() -> str:

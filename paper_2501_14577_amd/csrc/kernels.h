@@ -75,12 +75,28 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
 // key rows in list order into keys_full (S*N) and keys_list (S*cap); then the
 // tiles.
 bool tile_supports(int dv);
+// The tiles' inputs alone: key rows in list order (d_k = 3) and the window
+// bounds of every processing-order slot (idx_out optional).
+hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int topk, bool causal, int chunk,
+                               const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                               const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order,
+                               int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
+                               hipStream_t stream);
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
                                      int topk, bool causal, int chunk, const uint32_t* q_codes,
                                      const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
                                      const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
                                      int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream);
+
+// Gradients of the bfloat16 one-pass attention (d_k = 3, Cauchy score) over
+// its windows: prefix lists, window bounds, query pass, envelopes, key passes
+// and the deps sum; dq, dk, dv and deps float32.
+hipError_t launch_select_attend_bwd(const void* q, const void* k, const void* v, const void* dout, int64_t S,
+                                    int64_t N, int dk_, int dv_, int topk, bool causal, int chunk,
+                                    const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                                    const int32_t* q_order, float eps, float* dq, float* dk, float* dv,
+                                    float* deps, void* workspace, hipStream_t stream);
 
 // Select and attend in one pass (idx_out optional); score: a ScoreMode (the
 // matrix-core tiles serve the Cauchy score of bfloat16 inputs).

@@ -59,6 +59,7 @@
 #include "kernels.h"
 #include "layout.h"
 #include "select_device.h"
+#include "tile_device.h"
 
 namespace zeta {
 namespace {
@@ -66,77 +67,6 @@ namespace {
 constexpr int kTileQ = 16;     // queries per tile (product columns)
 constexpr int kChunk = 16;     // list entries per product step
 constexpr int kTileWaves = 4;  // wavefronts per block
-
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-
-union Frag {  // four bfloat16 values
-  uint32_t w[2];
-  s16x4_t v;
-};
-
-union Frag8 {  // eight bfloat16 values
-  uint32_t w[4];
-  bf16x8_t v;
-};
-
-__device__ __forceinline__ int wave_min_int(int x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const int y = __shfl_xor(x, off, 64);
-    x = y < x ? y : x;
-  }
-  return __builtin_amdgcn_readfirstlane(x);
-}
-
-__device__ __forceinline__ int wave_max_int(int x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const int y = __shfl_xor(x, off, 64);
-    x = y > x ? y : x;
-  }
-  return __builtin_amdgcn_readfirstlane(x);
-}
-
-// Lane `src`'s value of a pointer, read by every lane.  Each 32-bit half goes
-// through uint32_t: widening a negative int32 would sign-extend into the
-// high half.
-template <typename T>
-__device__ __forceinline__ T* readlane_ptr(T* p, int src) {
-  const uint64_t v = reinterpret_cast<uint64_t>(p);
-  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int32_t(uint32_t(v)), src));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int32_t(uint32_t(v >> 32)), src));
-  // Rebuilt as a global-memory pointer, so that loads through it are global
-  // loads rather than flat ones.
-  using G = __attribute__((address_space(1))) T;
-  G* g = (G*)((uint64_t(hi) << 32) | uint64_t(lo));
-  return (T*)g;
-}
-
-// E consecutive bfloat16 elements (E / 2 words) from a 2E-byte aligned address.
-template <int W>
-__device__ __forceinline__ void load_words(const uint16_t* p, uint32_t (&o)[W]) {
-  if constexpr (W % 4 == 0) {
-#pragma unroll
-    for (int t = 0; t < W / 4; ++t) {
-      const uint4 x = reinterpret_cast<const uint4*>(p)[t];
-      o[4 * t] = x.x;
-      o[4 * t + 1] = x.y;
-      o[4 * t + 2] = x.z;
-      o[4 * t + 3] = x.w;
-    }
-  } else if constexpr (W == 2) {
-    const uint2 x = *reinterpret_cast<const uint2*>(p);
-    o[0] = x.x;
-    o[1] = x.y;
-  } else {
-    static_assert(W == 1, "unsupported row slice");
-    o[0] = *reinterpret_cast<const uint32_t*>(p);
-  }
-}
 
 // ---- window bounds ---------------------------------------------------------
 // Each lane serves one slot of the processing order (a run of 64 consecutive
@@ -793,12 +723,11 @@ hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* 
 
 bool tile_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 256; }
 
-hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
-                                     int topk, bool causal, int chunk, const uint32_t* q_codes,
-                                     const uint32_t* sorted_codes,
-                                     const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                                     const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
-                                     int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream) {
+hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int topk, bool causal, int chunk,
+                               const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
+                               const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order,
+                               int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
+                               hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   if (dk == 3) {
@@ -817,6 +746,18 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
                        perm, list_codes, list_pos, q_order, total, N, topk, causal ? 1 : 0, chunk, lp.t0, lp.t_hi,
                        lp.cap, bounds, idx_out);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
+                                     int topk, bool causal, int chunk, const uint32_t* q_codes,
+                                     const uint32_t* sorted_codes,
+                                     const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
+                                     const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
+                                     int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream) {
+  const hipError_t e = launch_tile_windows(k, S, N, dk, topk, causal, chunk, q_codes, sorted_codes, perm, list_codes,
+                                           list_pos, q_order, idx_out, bounds, keys_full, keys_list, stream);
+  if (e != hipSuccess) return e;
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);
   const uint16_t* vv = static_cast<const uint16_t*>(v);

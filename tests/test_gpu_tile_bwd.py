@@ -1,0 +1,166 @@
+"""GPU parity of the one-pass attention's gradients (zeta_select_attend_bwd)
+against the float64 oracle (Appendix E.2), for the windows the one-pass call
+selects (the same windows, bit for bit, as the oracle's selection).
+
+Tolerance as for zeta_topk_attn_bwd: max-abs error at most
+1e-4 * (1 + max |oracle|) per tensor, relative 1e-4 for the eps gradient.
+The attention weights reach dv through two bfloat16 parts (16 significant
+bits), far inside that bound.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2501_14577_amd as zeta
+import workloads
+from gpu_util import device, host, i32_to_dev, inputs, log, oracle_select, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    device()
+    zeta.load_library()
+
+
+def _close(got, ref, name):
+    tol = 1e-4 * (1.0 + float(np.abs(ref).max()))
+    err = float(np.abs(got - ref).max())
+    assert err <= tol, (name, err, tol)
+
+
+def _gpu(raw, dout_raw, w, causal, eps, chunk=0, order="level"):
+    """Encode, sort, order and select on the GPU (one-pass forward, which also
+    returns the windows), then the one-pass gradients.  ``order``: "level"
+    (zeta_query_order), "position" (none) or a host permutation [S, N]."""
+    S = raw["q"].shape[0]
+    q, k, v, dout = (to_dev(a[None], w.dtype) for a in (raw["q"], raw["k"], raw["v"], dout_raw))
+    res = zeta.forward(q, k, v, w.topk, eps, causal, w.bits, fused=True, chunk=chunk, return_intermediates=True)
+    if isinstance(order, str):
+        q_order = res["q_order"] if order == "level" else None
+    else:
+        q_order = i32_to_dev(order[None])
+    grads = zeta.zeta_select_attend_bwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, causal,
+                                        eps, dout, chunk=chunk, q_order=q_order)
+    torch.cuda.synchronize()
+    idx = host(res["idx"]).reshape(S, w.N, w.topk)
+    dq, dk, dv, deps = (host(t) for t in grads)
+    return idx, dq.reshape(S, w.N, -1), dk.reshape(S, w.N, -1), dv.reshape(S, w.N, -1), float(deps[0])
+
+
+def _check(idx, got, f, dout, eps):
+    dq, dk, dv, deps = got
+    rq, rk, rv, reps = oracle.attend_bwd(f["q"], f["k"], f["v"], idx, eps, dout)
+    _close(dq, rq, "dq")
+    _close(dk, rk, "dk")
+    _close(dv, rv, "dv")
+    assert abs(deps - reps) <= 1e-4 * (1.0 + abs(reps)), (deps, reps)
+
+
+# (config, causal, segments compared)
+CFGS = [(2, True, 4), (3, False, 3), (3, True, 3), (4, True, 2)]
+
+
+@pytest.mark.parametrize("cfg,causal,nseg", CFGS)
+def test_tile_bwd_config(cfg, causal, nseg):
+    w, x, f = inputs(cfg)
+    log(f"tile bwd config {cfg} causal={causal} segments={nseg}")
+    S = w.segments
+    raw = {n: a.reshape(S, w.N, -1)[:nseg] for n, a in x.items()}
+    fs = {n: a[:nseg] for n, a in f.items()}
+    dout_raw = workloads.generate_dout(w).reshape(S, w.N, w.dv)[:nseg]
+    idx, *got = _gpu(raw, dout_raw, w, causal, 0.5)
+    assert np.array_equal(idx, oracle_select(cfg, causal)[:nseg])
+    _check(idx, got, fs, oracle.as_f32(dout_raw, w.dtype), 0.5)
+
+
+EDGE = [
+    dict(N=1, topk=8, dv=64),
+    dict(N=37, topk=7, dv=32),
+    dict(N=129, topk=1, dv=64),
+    dict(N=500, topk=64, dv=128),
+    dict(N=700, topk=1024, dv=256),
+    dict(N=1000, topk=16, dv=32, chunk=100),
+    dict(N=2000, topk=40, dv=64, chunk=256),
+]
+
+
+@pytest.mark.parametrize("shape", EDGE, ids=[f"N{e['N']}-k{e['topk']}-dv{e['dv']}-c{e.get('chunk', 0)}" for e in EDGE])
+@pytest.mark.parametrize("causal", [False, True])
+def test_tile_bwd_edges(shape, causal):
+    """Small and ragged shapes (tiles past the segment's end, N below one
+    tile), every d_v, k >= N, k = 1, the chunked rule (first chunk: empty
+    pools) and both modes, with eps != 0.5."""
+    chunk = shape.get("chunk", 0) if causal else 0
+    w = workloads.custom(B=1, H=3, N=shape["N"], dv=shape["dv"], topk=shape["topk"], dtype="bf16", bits=8,
+                         seed=shape["N"] * 3 + shape["topk"])
+    log(f"tile bwd edge {shape} causal={causal}")
+    x = workloads.generate(w)
+    S = w.segments
+    raw = {n: a.reshape(S, w.N, -1) for n, a in x.items()}
+    f = {n: oracle.as_f32(a, w.dtype) for n, a in raw.items()}
+    dout_raw = workloads.generate_dout(w).reshape(S, w.N, w.dv)
+    idx, *got = _gpu(raw, dout_raw, w, causal, 0.3, chunk=chunk)
+    qc, kc, _, _ = oracle.morton_encode(f["q"], f["k"], w.bits)
+    assert np.array_equal(idx, oracle.select_topk(qc, kc, w.topk, causal, chunk=chunk))
+    _check(idx, got, f, oracle.as_f32(dout_raw, w.dtype), 0.3)
+
+
+def test_tile_bwd_orders_and_repeat():
+    """Any processing order gives the oracle's gradients; dq and deps's parts
+    depend only on each query's own window, so dq is bit-identical across
+    orders; a repeated call gives the same bits for every output."""
+    cfg = 2
+    w, x, f = inputs(cfg)
+    log("tile bwd processing orders")
+    S = 4
+    raw = {n: a.reshape(w.segments, w.N, -1)[:S] for n, a in x.items()}
+    fs = {n: a[:S] for n, a in f.items()}
+    dout_raw = workloads.generate_dout(w).reshape(w.segments, w.N, w.dv)[:S]
+    dout = oracle.as_f32(dout_raw, w.dtype)
+    rng = np.random.default_rng(9)
+    perm = np.stack([rng.permutation(w.N) for _ in range(S)]).astype(np.int32)
+    runs = {o if isinstance(o, str) else "random": _gpu(raw, dout_raw, w, True, 0.5, order=o)
+            for o in ("level", "position", perm)}
+    for name, (idx, *got) in runs.items():
+        _check(idx, got, fs, dout, 0.5)
+    assert np.array_equal(runs["level"][1], runs["position"][1])
+    assert np.array_equal(runs["level"][1], runs["random"][1])
+    again = _gpu(raw, dout_raw, w, True, 0.5)
+    for t in range(1, 5):
+        assert np.array_equal(np.asarray(runs["level"][t]), np.asarray(again[t])), t
+
+
+def test_tile_bwd_long_context():
+    """The long-context workload at full size, as the benchmark runs it: every
+    gradient matches zeta_topk_attn_bwd (the per-query path, pinned to the
+    oracle above) on the same windows, and the invariants of the definition
+    hold (sum dq + sum dk = 0 per segment, sum dv = sum dout)."""
+    cfg = 5
+    w, x, _ = inputs(cfg)
+    log("tile bwd long context")
+    S = w.segments
+    raw = {n: a.reshape(S, w.N, -1) for n, a in x.items()}
+    dout_raw = workloads.generate_dout(w).reshape(S, w.N, w.dv)
+    q, k, v, dout = (to_dev(a[None], w.dtype) for a in (raw["q"], raw["k"], raw["v"], dout_raw))
+    res = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, return_intermediates=True)
+    ref = zeta.zeta_topk_attn_bwd(q, k, v, res["idx"], dout, 0.5, q_order=res["q_order"])
+    got = zeta.zeta_select_attend_bwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, True, 0.5,
+                                      dout, q_order=res["q_order"])
+    torch.cuda.synchronize()
+    names = ("dq", "dk", "dv", "deps")
+    for name, a, b in zip(names, got, ref):
+        a, b = host(a).astype(np.float64), host(b).astype(np.float64)
+        if name == "deps":
+            assert abs(a[0] - b[0]) <= 1e-4 * (1.0 + abs(b[0])), (a, b)
+        else:
+            _close(a, b, name)
+    dq, dk, dv = (host(t).reshape(S, w.N, -1).astype(np.float64) for t in got[:3])
+    dsum = dq.sum(axis=1) + dk.sum(axis=1)
+    scale = np.abs(dq).sum(axis=1) + np.abs(dk).sum(axis=1)
+    assert np.all(np.abs(dsum) <= 1e-4 * (1.0 + scale)), (dsum, scale)
+    dsv = oracle.as_f32(dout_raw, w.dtype).astype(np.float64).sum(axis=1)
+    assert np.allclose(dv.sum(axis=1), dsv, rtol=1e-4, atol=1e-2), np.abs(dv.sum(axis=1) - dsv).max()
