@@ -316,3 +316,51 @@ BWD_CASES = [
 @pytest.mark.parametrize("kw,code", BWD_CASES, ids=[str(c[0]) for c in BWD_CASES])
 def test_attend_bwd_rejects(kw, code):
     assert _bwd(**kw) == code
+
+
+def _obwd(**kw):
+    a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, causal=1, chunk=0,
+             q_codes=P4, sorted_codes=ctypes.c_void_p(0xD0000), perm=ctypes.c_void_p(0xE0000), q_order=NULL,
+             dout=ctypes.c_void_p(0x50000), eps=0.5, dq=ctypes.c_void_p(0x60000), dk=ctypes.c_void_p(0x70000),
+             dv=ctypes.c_void_p(0x80000), deps=ctypes.c_void_p(0x90000), ws=ctypes.c_void_p(0xA0000), ws_bytes=BIG,
+             stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_select_attend_bwd(*a.values())
+
+
+OBWD_CASES = [
+    (dict(q=NULL), INV), (dict(k=NULL), INV), (dict(dout=NULL), INV), (dict(q_codes=NULL), INV),
+    (dict(sorted_codes=NULL), INV), (dict(perm=NULL), INV), (dict(dq=NULL), INV), (dict(dk=NULL), INV),
+    (dict(dv=NULL), INV), (dict(deps=NULL), INV), (dict(B=0), INV), (dict(N=0), INV), (dict(d_k=0), INV),
+    (dict(topk=0), INV), (dict(causal=2), INV), (dict(chunk=-1), INV), (dict(causal=0, chunk=8), INV),
+    (dict(eps=0.0), INV), (dict(eps=float("nan")), INV),
+    (dict(dout=ctypes.c_void_p(0x50004)), INV), (dict(v=ctypes.c_void_p(0x30008)), INV),
+    (dict(dv=ctypes.c_void_p(0x80008)), INV),  # dv is written with 16-byte stores
+    (dict(dk=ctypes.c_void_p(0x60000)), INV),  # dk aliases dq
+    (dict(dv=P3), INV),  # dv aliases v
+    (dict(deps=ctypes.c_void_p(0xE0000)), INV),  # deps aliases perm
+    (dict(dtype=7), UNS), (dict(dtype=zb.ZETA_F32), UNS), (dict(d_k=2), UNS), (dict(d_k=4), UNS),
+    (dict(d_v=48), UNS), (dict(d_v=512), UNS), (dict(topk=1025), UNS),
+    (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP), (dict(ws=ctypes.c_void_p(0xA0008)), INV),
+]
+
+
+@pytest.mark.parametrize("kw,code", OBWD_CASES, ids=[str(c[0]) for c in OBWD_CASES])
+def test_select_attend_bwd_rejects(kw, code):
+    assert _obwd(**kw) == code
+
+
+def test_select_attend_bwd_workspace_size():
+    ws = zeta.zeta_select_attend_bwd_workspace_size
+    assert ws(0, 1, 10, 64, 4, 1) == 0
+    assert ws(1, 1, 10, 64, 0, 1) == 0
+    assert ws(1, 1, 10, 48, 4, 1) == 0
+    assert zeta.load_library().zeta_select_attend_bwd_workspace_size(1, 1, 10, 64, 4, 2) == 0  # causal not 0/1
+    # Long-context shape: the one-pass call's buffers plus, per row, the
+    # 32-byte record, the dout copy (2 x 128 B) and the deps part.
+    big = ws(1, 16, 65536, 128, 128, 1)
+    rows = 16 * 65536
+    assert big >= rows * (32 + 256 + 4)
+    assert big < rows * (32 + 256 + 4) + (96 << 20)
+    assert big % 256 == 0
+    assert ws(1, 1, 1, 32, 1, 0) > 0
