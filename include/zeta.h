@@ -422,7 +422,7 @@ size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int d_v
  * zeta_select_attend_bwd_workspace_size -- bytes of device workspace for
  * zeta_select_attend_bwd on this shape: the one-pass call's lists, window
  * bounds and key rows, 36 + 2 * d_v bytes per row (a 32-byte record of the
- * row's query, a copy of its dout row and its part of deps), 16 bytes per
+ * row's query, a copy of its dout row and its part of deps), 24 bytes per
  * tile of 16 rows and list, and 4 KiB of sums.  Returns 0 for invalid shapes
  * and unsupported d_v.
  */

@@ -154,7 +154,8 @@ inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
 // Gradients of the bfloat16 one-pass attention: the one-pass call's lists,
 // bounds and key rows, then per slot a 32-byte record, a copy of the dout row
 // and the deps part, each tile's window range per list and their envelopes,
-// and the block sums of deps.
+// each chunk's candidate tiles (in the envelopes' layout) and the block sums
+// of deps.
 constexpr int64_t kTileBwdRedPer = 4096;  // deps parts per block sum (at least)
 constexpr int64_t kTileBwdRedMax = 1024;  // block sums at most
 inline int tile_bwd_levels(int64_t N, int topk, bool causal) {
@@ -163,7 +164,7 @@ inline int tile_bwd_levels(int64_t N, int topk, bool causal) {
 }
 struct TileBwdWs {
   FusedWs fused;
-  size_t rec_off, dslot_off, part_off, env_off, env2_off, sums_off, bytes;
+  size_t rec_off, dslot_off, part_off, env_off, env2_off, ranges_off, sums_off, bytes;
 };
 inline TileBwdWs tile_bwd_ws(int64_t S, int64_t N, int dv, int topk, int causal) {
   TileBwdWs w;
@@ -176,7 +177,8 @@ inline TileBwdWs tile_bwd_ws(int64_t S, int64_t N, int dv, int topk, int causal)
   w.part_off = w.dslot_off + align_up(rows * size_t(dv) * 2);
   w.env_off = w.part_off + align_up(rows * sizeof(float));
   w.env2_off = w.env_off + align_up(env);
-  w.sums_off = w.env2_off + align_up(env);
+  w.ranges_off = w.env2_off + align_up(env);
+  w.sums_off = w.ranges_off + align_up(env);
   w.bytes = w.sums_off + align_up(size_t(kTileBwdRedMax) * sizeof(float));
   return w;
 }

@@ -21,7 +21,8 @@
 //  2. Envelopes, per segment and level: the running maximum (from the first
 //     tile) of the tiles' last indices and the running minimum (from the last
 //     tile) of their first indices.  Both are non-decreasing, so the tiles
-//     whose windows meet a chunk lie between two searched positions.
+//     whose windows meet a chunk lie between two positions, found by binary
+//     search per chunk.
 //  3. Key pass, one launch per list (the full sorted list first, then each
 //     prefix list), one wavefront per 16-entry chunk.  Over the candidate
 //     tiles (64 tiles' ranges tested at once) a lane takes one entry and 4 of
@@ -400,42 +401,59 @@ __global__ void __launch_bounds__(kEnvThreads)
   }
 }
 
-// First tile t in [0, ct) with key(t) >= want, for a non-decreasing key read
-// from p[t] (ct when none): two rounds of 64 probes.
+// First tile t in [0, ct) with key(t) >= want for a non-decreasing key
+// (ct when none): the running maximum of last indices (kHi) or the running
+// minimum of first indices.
 template <bool kHi>
-__device__ __forceinline__ int64_t first_at_least(const int2* p, int64_t ct, int want, int lane) {
-  auto key = [&](int64_t t) { return kHi ? p[t].y : p[t].x; };
-  const int64_t step = (ct + 63) / 64;
-  const int64_t t1 = int64_t(lane) * step;
-  // Round 1: the first probe at or above `want` bounds the answer from above.
-  const bool ge1 = t1 < ct && key(t1) >= want;
-  const uint64_t m1 = wave_ballot(ge1);
-  int64_t hi = m1 != 0ull ? int64_t(__ffsll((unsigned long long)m1) - 1) * step : ct;
-  int64_t lo = hi - step > 0 ? hi - step : 0;
-  if (m1 == 0ull) lo = ct - step > 0 ? (ct - 1) / step * step : 0;
-  // Round 2: the answer lies in (lo, hi]; probes of at most 64 tiles at a time.
-  for (int64_t base = lo; base < hi; base += 64) {
-    const int64_t t = base + lane;
-    const bool ge = t < hi && key(t) >= want;
-    const uint64_t m = wave_ballot(ge);
-    if (m != 0ull) return base + (__ffsll((unsigned long long)m) - 1);
+__device__ __forceinline__ int64_t first_at_least(const int2* p, int64_t ct, int want) {
+  int64_t lo = 0, hi = ct;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    const int2 r = p[mid];
+    if ((kHi ? r.y : r.x) >= want)
+      hi = mid;
+    else
+      lo = mid + 1;
   }
-  return hi;
+  return lo;
+}
+
+// Per list, segment and chunk: the candidate tiles [ta, tb).  Tiles before ta
+// end before the chunk; tiles from tb on start after it.  One thread per
+// (list, segment, chunk), in the envelopes' layout.
+__global__ void __launch_bounds__(256)
+    bwd_ranges_kernel(const int2* __restrict__ env2, int64_t S, int64_t N, int64_t ct, int causal, int t0, int t_hi,
+                      int levels, int nl, int2* __restrict__ ranges) {
+  const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= int64_t(nl) * S * ct) return;
+  const int64_t row = t / ct;
+  const int64_t c = t - row * ct;
+  const int li = int(row / S);
+  const int lvl = !causal ? 0 : (li == levels ? t_hi + 1 : t0 + li);
+  const int64_t ln = (causal && lvl <= t_hi) ? (int64_t(1) << lvl) : N;
+  if (c * 16 >= ln) return;
+  const int lo_c = int(c * 16);
+  const int hi_c = int(c * 16 + 15 < ln - 1 ? c * 16 + 15 : ln - 1);
+  const int2* ev2 = env2 + row * ct;
+  ranges[t] = make_int2(int(first_at_least<true>(ev2, ct, lo_c)), int(first_at_least<false>(ev2, ct, hi_c + 1)));
 }
 
 // ---- 3. key pass ------------------------------------------------------------------
-template <int DV>
+template <int DV, bool kOff32>
 __global__ void __launch_bounds__(kBtWaves * 64)
     bwd_tile_key_kernel(const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
                         const int32_t* __restrict__ list_pos, const uint2* __restrict__ keys_full,
                         const uint2* __restrict__ keys_list, const SlotRec* __restrict__ rec,
                         const uint16_t* __restrict__ dslot, const int2* __restrict__ env,
-                        const int2* __restrict__ env2, int64_t S, int64_t N, int64_t ct, int causal, int t0,
+                        const int2* __restrict__ ranges, int64_t S, int64_t N, int64_t ct, int causal, int t0,
                         int t_hi, int levels, int64_t cap, int lvl, int first, float eps, float* __restrict__ dk,
                         float* __restrict__ dv) {
   constexpr int NS = DV / 32;
   constexpr int E = DV / 16;  // value elements per lane and row in the dv product
   constexpr int W = E / 2;
+  // Byte offsets into a segment's records and dout rows: 32-bit when the
+  // segment's dout rows span under 4 GiB.
+  using Off = typename RowOff<kOff32>::type;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int ent = lane & 15;  // this lane's entry (B column, and A row of the dot products)
@@ -471,86 +489,117 @@ __global__ void __launch_bounds__(kBtWaves * 64)
     const int lo_c = int(c * kBtChunk);
     const int hi_c = int(c * kBtChunk + kBtChunk - 1 < ln - 1 ? c * kBtChunk + kBtChunk - 1 : ln - 1);
     const int2* ev = env + (int64_t(li) * S + seg) * ct;
-    const int2* ev2 = env2 + (int64_t(li) * S + seg) * ct;
-    const SlotRec* rseg = rec + seg * N;
-    const uint16_t* dseg = dslot + seg * N * DV;
-    // Tiles before ta end before the chunk; tiles from tb on start after it.
-    const int64_t ta = first_at_least<true>(ev2, ct, lo_c, lane);
-    const int64_t tb = first_at_least<false>(ev2, ct, hi_c + 1, lane);
-    for (int64_t base = ta; base < tb; base += 64) {
-      // The candidates whose windows meet the chunk, 64 at a time.
-      const int64_t tl = base + lane;
-      bool hit = false;
-      if (tl < tb) {
-        const int2 rg = ev[tl];
-        hit = rg.x <= hi_c && rg.y >= lo_c;
+    const unsigned char* rbase = reinterpret_cast<const unsigned char*>(rec + seg * N);
+    const unsigned char* dbase = reinterpret_cast<const unsigned char*>(dslot + seg * N * DV);
+    const int32_t n32 = int32_t(N);
+    const int2 tr = ranges[(int64_t(li) * S + seg) * ct + c];
+    const int64_t ta = tr.x, tb = tr.y;
+    // The candidates whose windows meet the chunk, found 64 at a time; the
+    // next tile's data loads while the current tile is summed.
+    int64_t blk_base = ta;   // next block of 64 candidates to test
+    int64_t cur_base = ta;   // block that `pend` belongs to
+    uint64_t pend = 0ull;    // untaken hits of that block
+    auto next_tile = [&]() -> int64_t {
+      while (pend == 0ull && blk_base < tb) {
+        const int64_t tl = blk_base + lane;
+        bool hit = false;
+        if (tl < tb) {
+          const int2 rg = ev[tl];
+          hit = (rg.x <= hi_c) & (rg.y >= lo_c);
+        }
+        pend = wave_ballot(hit);
+        cur_base = blk_base;
+        blk_base += 64;
       }
-      for (uint64_t m = wave_ballot(hit); m != 0ull; m &= m - 1ull) {
-        const int64_t tau = base + (__ffsll((unsigned long long)m) - 1);
-        touched = true;
-        // Slots of the tile past the segment's end read the segment's last
-        // slot (finite rows) and count as outside every window.
-        int64_t xq[4];
+      if (pend == 0ull) return -1;
+      const int64_t t = cur_base + (__ffsll((unsigned long long)pend) - 1);
+      pend &= pend - 1ull;
+      return t;
+    };
+    struct TileData {
+      SlotRec rq[4];        // records of the tile's queries 4kg..4kg+3
+      uint32_t dfr[NS][4];  // dout of the tile's query ent (A rows of the dot products)
+      uint32_t raw[4][W];   // dout rows of queries 4kg..4kg+3, elements ent*E .. ent*E + E - 1
+    };
+    // Slots of the tile past the segment's end read the segment's last slot
+    // (finite rows) and count as outside every window.
+    auto load_tile = [&](int64_t tau, TileData& td) {
+      const int32_t t16 = int32_t(tau) * 16;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t xs = tau * 16 + kg * 4 + r;
-          xq[r] = xs < N ? xs : N - 1;
-        }
-        const int64_t xe = tau * 16 + ent < N ? tau * 16 + ent : N - 1;
-        SlotRec rq[4];
+      for (int r = 0; r < 4; ++r) {
+        const int32_t xs = t16 + kg * 4 + r;
+        const Off xq = Off(xs < n32 ? xs : n32 - 1);
+        td.rq[r] = *reinterpret_cast<const SlotRec*>(rbase + xq * Off(sizeof(SlotRec)));
+        load_words<W>(reinterpret_cast<const uint16_t*>(dbase + (xq * Off(DV) + Off(ent * E)) * Off(2)), td.raw[r]);
+      }
+      const Off xe = Off(t16 + ent < n32 ? t16 + ent : n32 - 1);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) rq[r] = rseg[xq[r]];
-        uint32_t dfr[NS][4];  // dout of the tile's query ent (A rows of the dot products)
+      for (int s = 0; s < NS; ++s)
+        load8(reinterpret_cast<const uint16_t*>(dbase + (xe * Off(DV) + Off(32 * s + 8 * kg)) * Off(2)), td.dfr[s]);
+    };
+    auto sum_tile = [&](int64_t tau, const TileData& td) {
+      // Dot products: lane holds p for queries 4kg..4kg+3 and entry ent.
+      f32x4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int s = 0; s < NS; ++s) load8(dseg + xe * DV + 32 * s + 8 * kg, dfr[s]);
-        uint32_t raw[4][W];  // dout rows of queries 4kg..4kg+3, elements ent*E .. ent*E + E - 1
+      for (int s = 0; s < NS; ++s)
+        d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag8(td.dfr[s]).v, frag8(vfr[s]).v, d, 0, 0, 0);
+      float aw[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) load_words<W>(dseg + xq[r] * DV + ent * E, raw[r]);
-
-        // Dot products: lane holds p for queries 4kg..4kg+3 and entry ent.
-        f32x4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int r = 0; r < 4; ++r) {
+        const SlotRec& rr = td.rq[r];
+        const float qx = __uint_as_float(rr.q01 << 16);
+        const float qy = __uint_as_float(rr.q01 & 0xFFFF0000u);
+        const float qz = __uint_as_float(rr.q2_list << 16);
+        const float df[3] = {qx - kv[0], qy - kv[1], qz - kv[2]};
+        const float d2 = fmaf(df[2], df[2], fmaf(df[1], df[1], df[0] * df[0]));
+        const bool in = ((rr.q2_list >> 16) == li) & (int32_t(tau) * 16 + kg * 4 + r < n32) & valid_e &
+                        (uint32_t(e - rr.a) <= uint32_t(rr.b - rr.a)) & (uint32_t(pos_e) <= rr.lim);
+        const float sc = in ? __builtin_amdgcn_rcpf(d2 + eps) : 0.0f;
+        aw[r] = sc * rr.zinv;
+        const float w = (d[r] - rr.c) * sc * aw[r];
 #pragma unroll
-        for (int s = 0; s < NS; ++s)
-          d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag8(dfr[s]).v, frag8(vfr[s]).v, d, 0, 0, 0);
-        float aw[4];
+        for (int a = 0; a < 3; ++a) gk[a] = fmaf(w, df[a], gk[a]);
+      }
+      // dv^T += dout^T (columns x queries) * A (queries x entries), high and
+      // low parts of A in one product per 16 columns.
+      Frag8 b;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float qx = __uint_as_float(rq[r].q01 << 16);
-          const float qy = __uint_as_float(rq[r].q01 & 0xFFFF0000u);
-          const float qz = __uint_as_float(rq[r].q2_list << 16);
-          const float df[3] = {qx - kv[0], qy - kv[1], qz - kv[2]};
-          const float d2 = fmaf(df[2], df[2], fmaf(df[1], df[1], df[0] * df[0]));
-          const bool in = (rq[r].q2_list >> 16) == li && tau * 16 + kg * 4 + r < N && valid_e &&
-                          uint32_t(e - rq[r].a) <= uint32_t(rq[r].b - rq[r].a) && uint32_t(pos_e) <= rq[r].lim;
-          const float sc = in ? __builtin_amdgcn_rcpf(d2 + eps) : 0.0f;
-          aw[r] = sc * rq[r].zinv;
-          const float w = (d[r] - rq[r].c) * sc * aw[r];
+      for (int t = 0; t < 2; ++t) {
+        const bf16x2_t h = {(__bf16)aw[2 * t], (__bf16)aw[2 * t + 1]};
+        const uint32_t hw = __builtin_bit_cast(uint32_t, h);
+        const bf16x2_t l = {(__bf16)(aw[2 * t] - __uint_as_float(hw << 16)),
+                            (__bf16)(aw[2 * t + 1] - __uint_as_float(hw & 0xFFFF0000u))};
+        b.w[t] = hw;
+        b.w[t + 2] = __builtin_bit_cast(uint32_t, l);
+      }
 #pragma unroll
-          for (int a = 0; a < 3; ++a) gk[a] = fmaf(w, df[a], gk[a]);
-        }
-        // dv^T += dout^T (columns x queries) * A (queries x entries), high and
-        // low parts of A in one product per 16 columns.
-        Frag8 b;
+      for (int j = 0; j < E; ++j) {
+        Frag8 a;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          const bf16x2_t h = {(__bf16)aw[2 * t], (__bf16)aw[2 * t + 1]};
-          const uint32_t hw = __builtin_bit_cast(uint32_t, h);
-          const bf16x2_t l = {(__bf16)(aw[2 * t] - __uint_as_float(hw << 16)),
-                              (__bf16)(aw[2 * t + 1] - __uint_as_float(hw & 0xFFFF0000u))};
-          b.w[t] = hw;
-          b.w[t + 2] = __builtin_bit_cast(uint32_t, l);
+          const uint32_t x = td.raw[2 * t][j >> 1], y = td.raw[2 * t + 1][j >> 1];
+          a.w[t] = __builtin_amdgcn_perm(y, x, (j & 1) ? 0x07060302u : 0x05040100u);
+          a.w[t + 2] = a.w[t];
         }
-#pragma unroll
-        for (int j = 0; j < E; ++j) {
-          Frag8 a;
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-            const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
-            a.w[t] = __builtin_amdgcn_perm(y, x, (j & 1) ? 0x07060302u : 0x05040100u);
-            a.w[t + 2] = a.w[t];
-          }
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc[j], 0, 0, 0);
-        }
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc[j], 0, 0, 0);
+      }
+    };
+    {
+      TileData tA, tB;
+      int64_t cur = next_tile();
+      if (cur >= 0) {
+        touched = true;
+        load_tile(cur, tA);
+      }
+      while (cur >= 0) {
+        const int64_t nxt = next_tile();
+        load_tile(nxt >= 0 ? nxt : cur, tB);
+        sum_tile(cur, tA);
+        if (nxt < 0) break;
+        const int64_t nn = next_tile();
+        load_tile(nn >= 0 ? nn : nxt, tA);
+        sum_tile(nxt, tB);
+        cur = nn;
       }
     }
 
@@ -629,11 +678,13 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
   const ListPlan lp = list_plan(N, topk);
   const int64_t ct = ceil_div(N, int64_t(16));
   const int nl = tile_bwd_levels(N, topk, causal);
+  const bool off32 = N * int64_t(DV) * 2 <= int64_t(0xFFFFFFFF);
   SlotRec* rec = reinterpret_cast<SlotRec*>(wsb + ws.rec_off);
   uint16_t* dslot = reinterpret_cast<uint16_t*>(wsb + ws.dslot_off);
   float* part = reinterpret_cast<float*>(wsb + ws.part_off);
   int2* env = reinterpret_cast<int2*>(wsb + ws.env_off);
   int2* env2 = reinterpret_cast<int2*>(wsb + ws.env2_off);
+  int2* ranges = reinterpret_cast<int2*>(wsb + ws.ranges_off);
   float* sums = reinterpret_cast<float*>(wsb + ws.sums_off);
   const int64_t nenv = int64_t(nl) * S * ct;
   {
@@ -652,6 +703,8 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
   }
   hipLaunchKernelGGL(bwd_envelope_kernel, dim3(unsigned(int64_t(nl) * S)), dim3(kEnvThreads), 0, stream, env, ct,
                      env2);
+  hipLaunchKernelGGL(bwd_ranges_kernel, dim3(unsigned(ceil_div(nenv, int64_t(256)))), dim3(256), 0, stream, env2, S, N,
+                     ct, cz, lp.t0, lp.t_hi, lp.levels, nl, ranges);
   // The full list first (its launch writes every key's rows), then the prefix
   // lists from the longest down.
   for (int li = nl - 1; li >= 0; --li) {
@@ -660,9 +713,15 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
     const int64_t chunks = S * ceil_div(ln, int64_t(16));
     const int64_t want = ceil_div(chunks, int64_t(kBtWaves));
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
-    hipLaunchKernelGGL((bwd_tile_key_kernel<DV>), dim3(blocks), dim3(kBtWaves * 64), 0, stream, v, perm, list_pos,
-                       keys_full, keys_list, rec, dslot, env, env2, S, N, ct, cz, lp.t0, lp.t_hi, lp.levels, lp.cap,
-                       lvl, li == nl - 1 ? 1 : 0, eps, dk, dv);
+#define ZETA_BT_KEY(OFF)                                                                                       \
+  hipLaunchKernelGGL((bwd_tile_key_kernel<DV, OFF>), dim3(blocks), dim3(kBtWaves * 64), 0, stream, v, perm, list_pos, \
+                     keys_full, keys_list, rec, dslot, env, ranges, S, N, ct, cz, lp.t0, lp.t_hi, lp.levels, lp.cap,  \
+                     lvl, li == nl - 1 ? 1 : 0, eps, dk, dv)
+    if (off32)
+      ZETA_BT_KEY(true);
+    else
+      ZETA_BT_KEY(false);
+#undef ZETA_BT_KEY
   }
   const int64_t total = S * N;
   const int64_t nred = ceil_div(total, kTileBwdRedPer) < kTileBwdRedMax ? ceil_div(total, kTileBwdRedPer)
