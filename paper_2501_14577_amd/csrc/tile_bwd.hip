@@ -130,7 +130,7 @@ __device__ __forceinline__ int level_index(int lvl, int causal, int t0, int t_hi
 
 // ---- 1. query pass ----------------------------------------------------------
 template <int DV>
-__global__ void __launch_bounds__(kBtWaves * 64)
+__global__ void __launch_bounds__(kBtWaves * 64) __attribute__((amdgpu_waves_per_eu(DV <= 128 ? 3 : 1)))
     bwd_tile_query_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
                           const uint16_t* __restrict__ dout, const int32_t* __restrict__ sorted_pos,
                           const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
