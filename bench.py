@@ -31,8 +31,8 @@ import workloads  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2501_14577_amd", "csrc", n)
-               for n in ("fused.hip", "tile.hip", "select.hip", "select_device.h", "attend_device.h", "device_common.h",
-                         "layout.h")]
+               for n in ("fused.hip", "tile.hip", "tile_device.h", "select.hip", "select_device.h", "attend_device.h",
+                         "device_common.h", "layout.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "select_attend_long_context_traffic.txt")
 
 
