@@ -439,8 +439,17 @@ __global__ void __launch_bounds__(256)
 }
 
 // ---- 3. key pass ------------------------------------------------------------------
+// A block's 4 wavefronts take 4 consecutive chunks of one list and segment and
+// walk the union of their candidate tiles together.  Each tile's 16 records
+// and 16 dout rows are staged once in LDS for the 4 (two buffers: the next
+// tile's bytes load while the current tile is summed, one barrier per tile);
+// a wavefront skips the tiles its own chunk does not meet.  Dout rows are
+// padded by 16 bytes, so that lanes reading 16 different rows use different
+// banks.
+constexpr int kKeyThreads = kBtWaves * 64;
+
 template <int DV, bool kOff32>
-__global__ void __launch_bounds__(kBtWaves * 64)
+__global__ void __launch_bounds__(kKeyThreads) __attribute__((amdgpu_waves_per_eu(DV <= 128 ? 3 : 2)))
     bwd_tile_key_kernel(const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
                         const int32_t* __restrict__ list_pos, const uint2* __restrict__ keys_full,
                         const uint2* __restrict__ keys_list, const SlotRec* __restrict__ rec,
@@ -451,27 +460,36 @@ __global__ void __launch_bounds__(kBtWaves * 64)
   constexpr int NS = DV / 32;
   constexpr int E = DV / 16;  // value elements per lane and row in the dv product
   constexpr int W = E / 2;
+  constexpr int kRowU = DV / 8;                                   // 16-byte units per dout row
+  constexpr int kDoutU = 16 * kRowU;                              // units of a tile's dout rows
+  constexpr int kStU = (kDoutU + kKeyThreads - 1) / kKeyThreads;  // dout units staged per thread
   // Byte offsets into a segment's records and dout rows: 32-bit when the
   // segment's dout rows span under 4 GiB.
   using Off = typename RowOff<kOff32>::type;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  __shared__ __align__(16) uint32_t s_rec[2][16][8];
+  __shared__ __align__(16) uint16_t s_dout[2][16][DV + 8];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int ent = lane & 15;  // this lane's entry (B column, and A row of the dot products)
   const int kg = lane >> 4;   // this lane's queries 4kg..4kg+3 of a tile
   const uint32_t li = uint32_t(level_index(lvl, causal, t0, t_hi, levels));
   const int64_t ln = (causal && lvl <= t_hi) ? (int64_t(1) << lvl) : N;
   const int64_t cl = (ln + kBtChunk - 1) / kBtChunk;
-  const int64_t chunks = S * cl;
+  const int64_t gps = (cl + kBtWaves - 1) / kBtWaves;  // groups of 4 chunks per segment
+  const int64_t groups = S * gps;
   const int64_t nb = gridDim.x;
+  const int32_t n32 = int32_t(N);
 
-  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kBtWaves < chunks; blk += nb) {
-    const int64_t cid = blk * kBtWaves + wave;
-    if (cid >= chunks) continue;
-    const int64_t seg = cid / cl;
-    const int64_t c = cid - seg * cl;
+  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk < groups; blk += nb) {
+    const int64_t seg = blk / gps;
+    const int64_t c0 = (blk - seg * gps) * kBtWaves;
+    const int64_t c_last = (c0 + kBtWaves < cl ? c0 + kBtWaves : cl) - 1;
+    const int64_t c = c0 + wave;
+    const bool live = c < cl;
     const LevelList L = level_list(sorted_pos, list_pos, keys_full, keys_list, seg, N, causal, lvl, t0, t_hi, cap);
     const int32_t e = int32_t(c * kBtChunk + ent);
-    const bool valid_e = e < L.n;
+    const bool valid_e = live && e < L.n;
     const int32_t pos_e = valid_e ? L.pos[e] : 0;
     float kv[3] = {0.0f, 0.0f, 0.0f};
     if (valid_e) key_row(L.key[e], kv);
@@ -486,67 +504,88 @@ __global__ void __launch_bounds__(kBtWaves * 64)
     float gk[3] = {0.0f, 0.0f, 0.0f};
     bool touched = false;
 
-    const int lo_c = int(c * kBtChunk);
-    const int hi_c = int(c * kBtChunk + kBtChunk - 1 < ln - 1 ? c * kBtChunk + kBtChunk - 1 : ln - 1);
+    // This wave's chunk (empty when past the list) and the group's entries.
+    const int lo_c = live ? int(c * kBtChunk) : 1;
+    const int hi_c = live ? int(c * kBtChunk + kBtChunk - 1 < ln - 1 ? c * kBtChunk + kBtChunk - 1 : ln - 1) : 0;
+    const int lo_g = int(c0 * kBtChunk);
+    const int hi_g = int(c_last * kBtChunk + kBtChunk - 1 < ln - 1 ? c_last * kBtChunk + kBtChunk - 1 : ln - 1);
     const int2* ev = env + (int64_t(li) * S + seg) * ct;
+    const int2* rgs = ranges + (int64_t(li) * S + seg) * ct;
+    // The candidate ranges grow with the chunk: the group's is from its first
+    // chunk's start to its last chunk's end.
+    const int64_t ta = rgs[c0].x, tb = rgs[c_last].y;
     const unsigned char* rbase = reinterpret_cast<const unsigned char*>(rec + seg * N);
     const unsigned char* dbase = reinterpret_cast<const unsigned char*>(dslot + seg * N * DV);
-    const int32_t n32 = int32_t(N);
-    const int2 tr = ranges[(int64_t(li) * S + seg) * ct + c];
-    const int64_t ta = tr.x, tb = tr.y;
-    // The candidates whose windows meet the chunk, found 64 at a time; the
-    // next tile's data loads while the current tile is summed.
-    int64_t blk_base = ta;   // next block of 64 candidates to test
-    int64_t cur_base = ta;   // block that `pend` belongs to
-    uint64_t pend = 0ull;    // untaken hits of that block
-    auto next_tile = [&]() -> int64_t {
+
+    // The tiles whose windows meet the group, 64 candidates tested at once
+    // (the same in every wavefront); with each, whether it meets this wave's
+    // chunk.
+    int64_t blk_base = ta, cur_base = ta;
+    uint64_t pend = 0ull, mine = 0ull;
+    auto next_tile = [&](bool& hit_w) -> int64_t {
       while (pend == 0ull && blk_base < tb) {
         const int64_t tl = blk_base + lane;
-        bool hit = false;
+        bool hg = false, hw = false;
         if (tl < tb) {
           const int2 rg = ev[tl];
-          hit = (rg.x <= hi_c) & (rg.y >= lo_c);
+          hg = (rg.x <= hi_g) & (rg.y >= lo_g);
+          hw = (rg.x <= hi_c) & (rg.y >= lo_c);
         }
-        pend = wave_ballot(hit);
+        pend = wave_ballot(hg);
+        mine = wave_ballot(hw);
         cur_base = blk_base;
         blk_base += 64;
       }
       if (pend == 0ull) return -1;
-      const int64_t t = cur_base + (__ffsll((unsigned long long)pend) - 1);
+      const int b = __ffsll((unsigned long long)pend) - 1;
       pend &= pend - 1ull;
-      return t;
+      hit_w = ((mine >> b) & 1ull) != 0ull;
+      return cur_base + b;
     };
-    struct TileData {
-      SlotRec rq[4];        // records of the tile's queries 4kg..4kg+3
-      uint32_t dfr[NS][4];  // dout of the tile's query ent (A rows of the dot products)
-      uint32_t raw[4][W];   // dout rows of queries 4kg..4kg+3, elements ent*E .. ent*E + E - 1
-    };
-    // Slots of the tile past the segment's end read the segment's last slot
-    // (finite rows) and count as outside every window.
-    auto load_tile = [&](int64_t tau, TileData& td) {
+    uint4 st_rec = make_uint4(0u, 0u, 0u, 0u);  // 16 bytes of the records (threads 0..31)
+    uint4 st_dout[kStU];
+    auto stage = [&](int64_t tau) {
       const int32_t t16 = int32_t(tau) * 16;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int32_t xs = t16 + kg * 4 + r;
+      if (tid < 32) {
+        const int32_t xs = t16 + (tid >> 1);
         const Off xq = Off(xs < n32 ? xs : n32 - 1);
-        td.rq[r] = *reinterpret_cast<const SlotRec*>(rbase + xq * Off(sizeof(SlotRec)));
-        load_words<W>(reinterpret_cast<const uint16_t*>(dbase + (xq * Off(DV) + Off(ent * E)) * Off(2)), td.raw[r]);
+        st_rec = *reinterpret_cast<const uint4*>(rbase + xq * Off(sizeof(SlotRec)) + Off((tid & 1) * 16));
       }
-      const Off xe = Off(t16 + ent < n32 ? t16 + ent : n32 - 1);
 #pragma unroll
-      for (int s = 0; s < NS; ++s)
-        load8(reinterpret_cast<const uint16_t*>(dbase + (xe * Off(DV) + Off(32 * s + 8 * kg)) * Off(2)), td.dfr[s]);
+      for (int u = 0; u < kStU; ++u) {
+        const int unit = u * kKeyThreads + tid;
+        if (unit < kDoutU) {
+          const int32_t xs = t16 + unit / kRowU;
+          const Off xq = Off(xs < n32 ? xs : n32 - 1);
+          st_dout[u] = *reinterpret_cast<const uint4*>(dbase + (xq * Off(DV) + Off((unit % kRowU) * 8)) * Off(2));
+        }
+      }
     };
-    auto sum_tile = [&](int64_t tau, const TileData& td) {
-      // Dot products: lane holds p for queries 4kg..4kg+3 and entry ent.
+    auto store = [&](int buf) {
+      if (tid < 32) *reinterpret_cast<uint4*>(&s_rec[buf][tid >> 1][(tid & 1) * 4]) = st_rec;
+#pragma unroll
+      for (int u = 0; u < kStU; ++u) {
+        const int unit = u * kKeyThreads + tid;
+        if (unit < kDoutU) *reinterpret_cast<uint4*>(&s_dout[buf][unit / kRowU][(unit % kRowU) * 8]) = st_dout[u];
+      }
+    };
+    auto sum_tile = [&](int64_t tau, int buf) {
+      SlotRec rq[4];  // records of the tile's queries 4kg..4kg+3
+#pragma unroll
+      for (int r = 0; r < 4; ++r) rq[r] = *reinterpret_cast<const SlotRec*>(&s_rec[buf][kg * 4 + r][0]);
+      // Dot products: lane holds p for queries 4kg..4kg+3 and entry ent (A
+      // rows: dout of the tile's query ent).
       f32x4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int s = 0; s < NS; ++s)
-        d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag8(td.dfr[s]).v, frag8(vfr[s]).v, d, 0, 0, 0);
+      for (int s = 0; s < NS; ++s) {
+        const uint4 x = *reinterpret_cast<const uint4*>(&s_dout[buf][ent][32 * s + 8 * kg]);
+        const uint32_t dw[4] = {x.x, x.y, x.z, x.w};
+        d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag8(dw).v, frag8(vfr[s]).v, d, 0, 0, 0);
+      }
       float aw[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const SlotRec& rr = td.rq[r];
+        const SlotRec& rr = rq[r];
         const float qx = __uint_as_float(rr.q01 << 16);
         const float qy = __uint_as_float(rr.q01 & 0xFFFF0000u);
         const float qz = __uint_as_float(rr.q2_list << 16);
@@ -561,7 +600,8 @@ __global__ void __launch_bounds__(kBtWaves * 64)
         for (int a = 0; a < 3; ++a) gk[a] = fmaf(w, df[a], gk[a]);
       }
       // dv^T += dout^T (columns x queries) * A (queries x entries), high and
-      // low parts of A in one product per 16 columns.
+      // low parts of A in one product per 16 columns; A rows from the dout
+      // rows of queries 4kg..4kg+3, elements ent*E .. ent*E + E - 1.
       Frag8 b;
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -572,12 +612,15 @@ __global__ void __launch_bounds__(kBtWaves * 64)
         b.w[t] = hw;
         b.w[t + 2] = __builtin_bit_cast(uint32_t, l);
       }
+      uint32_t raw[4][W];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) load_words<W>(&s_dout[buf][kg * 4 + r][ent * E], raw[r]);
 #pragma unroll
       for (int j = 0; j < E; ++j) {
         Frag8 a;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          const uint32_t x = td.raw[2 * t][j >> 1], y = td.raw[2 * t + 1][j >> 1];
+          const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
           a.w[t] = __builtin_amdgcn_perm(y, x, (j & 1) ? 0x07060302u : 0x05040100u);
           a.w[t + 2] = a.w[t];
         }
@@ -585,21 +628,27 @@ __global__ void __launch_bounds__(kBtWaves * 64)
       }
     };
     {
-      TileData tA, tB;
-      int64_t cur = next_tile();
+      bool cur_hit = false;
+      int64_t cur = next_tile(cur_hit);
+      int buf = 0;
       if (cur >= 0) {
-        touched = true;
-        load_tile(cur, tA);
+        stage(cur);
+        store(0);
       }
+      __syncthreads();
       while (cur >= 0) {
-        const int64_t nxt = next_tile();
-        load_tile(nxt >= 0 ? nxt : cur, tB);
-        sum_tile(cur, tA);
-        if (nxt < 0) break;
-        const int64_t nn = next_tile();
-        load_tile(nn >= 0 ? nn : nxt, tA);
-        sum_tile(nxt, tB);
-        cur = nn;
+        bool nxt_hit = false;
+        const int64_t nxt = next_tile(nxt_hit);
+        if (nxt >= 0) stage(nxt);
+        if (cur_hit) {
+          touched = true;
+          sum_tile(cur, buf);
+        }
+        if (nxt >= 0) store(buf ^ 1);
+        __syncthreads();
+        cur = nxt;
+        cur_hit = nxt_hit;
+        buf ^= 1;
       }
     }
 
@@ -643,6 +692,8 @@ __global__ void __launch_bounds__(kBtWaves * 64)
         for (int a = 0; a < 3; ++a) krow[a] = first ? gk[a] : krow[a] + gk[a];
       }
     }
+    // The next group reuses the LDS buffers.
+    __syncthreads();
   }
 }
 
@@ -710,11 +761,10 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
   for (int li = nl - 1; li >= 0; --li) {
     const int lvl = !causal ? 0 : (li == lp.levels ? lp.t_hi + 1 : lp.t0 + li);
     const int64_t ln = (causal && lvl <= lp.t_hi) ? (int64_t(1) << lvl) : N;
-    const int64_t chunks = S * ceil_div(ln, int64_t(16));
-    const int64_t want = ceil_div(chunks, int64_t(kBtWaves));
+    const int64_t want = S * ceil_div(ceil_div(ln, int64_t(16)), int64_t(kBtWaves));  // groups of 4 chunks
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
 #define ZETA_BT_KEY(OFF)                                                                                       \
-  hipLaunchKernelGGL((bwd_tile_key_kernel<DV, OFF>), dim3(blocks), dim3(kBtWaves * 64), 0, stream, v, perm, list_pos, \
+  hipLaunchKernelGGL((bwd_tile_key_kernel<DV, OFF>), dim3(blocks), dim3(kKeyThreads), 0, stream, v, perm, list_pos,    \
                      keys_full, keys_list, rec, dslot, env, ranges, S, N, ct, cz, lp.t0, lp.t_hi, lp.levels, lp.cap,  \
                      lvl, li == nl - 1 ? 1 : 0, eps, dk, dv)
     if (off32)
