@@ -439,14 +439,15 @@ __global__ void __launch_bounds__(256)
 }
 
 // ---- 3. key pass ------------------------------------------------------------------
-// A block's 4 wavefronts take 4 consecutive chunks of one list and segment and
+// A block's wavefronts take consecutive chunks of one list and segment and
 // walk the union of their candidate tiles together.  Each tile's 16 records
-// and 16 dout rows are staged once in LDS for the 4 (two buffers: the next
+// and 16 dout rows are staged once in LDS for all of them (two buffers: the next
 // tile's bytes load while the current tile is summed, one barrier per tile);
 // a wavefront skips the tiles its own chunk does not meet.  Dout rows are
 // padded by 16 bytes, so that lanes reading 16 different rows use different
 // banks.
-constexpr int kKeyThreads = kBtWaves * 64;
+constexpr int kKeyWaves = 4;  // chunks per block (one per wavefront)
+constexpr int kKeyThreads = kKeyWaves * 64;
 
 template <int DV, bool kOff32>
 __global__ void __launch_bounds__(kKeyThreads) __attribute__((amdgpu_waves_per_eu(DV <= 128 ? 3 : 2)))
@@ -476,15 +477,15 @@ __global__ void __launch_bounds__(kKeyThreads) __attribute__((amdgpu_waves_per_e
   const uint32_t li = uint32_t(level_index(lvl, causal, t0, t_hi, levels));
   const int64_t ln = (causal && lvl <= t_hi) ? (int64_t(1) << lvl) : N;
   const int64_t cl = (ln + kBtChunk - 1) / kBtChunk;
-  const int64_t gps = (cl + kBtWaves - 1) / kBtWaves;  // groups of 4 chunks per segment
+  const int64_t gps = (cl + kKeyWaves - 1) / kKeyWaves;  // groups of 4 chunks per segment
   const int64_t groups = S * gps;
   const int64_t nb = gridDim.x;
   const int32_t n32 = int32_t(N);
 
   for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk < groups; blk += nb) {
     const int64_t seg = blk / gps;
-    const int64_t c0 = (blk - seg * gps) * kBtWaves;
-    const int64_t c_last = (c0 + kBtWaves < cl ? c0 + kBtWaves : cl) - 1;
+    const int64_t c0 = (blk - seg * gps) * kKeyWaves;
+    const int64_t c_last = (c0 + kKeyWaves < cl ? c0 + kKeyWaves : cl) - 1;
     const int64_t c = c0 + wave;
     const bool live = c < cl;
     const LevelList L = level_list(sorted_pos, list_pos, keys_full, keys_list, seg, N, causal, lvl, t0, t_hi, cap);
@@ -761,7 +762,7 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
   for (int li = nl - 1; li >= 0; --li) {
     const int lvl = !causal ? 0 : (li == lp.levels ? lp.t_hi + 1 : lp.t0 + li);
     const int64_t ln = (causal && lvl <= lp.t_hi) ? (int64_t(1) << lvl) : N;
-    const int64_t want = S * ceil_div(ceil_div(ln, int64_t(16)), int64_t(kBtWaves));  // groups of 4 chunks
+    const int64_t want = S * ceil_div(ceil_div(ln, int64_t(16)), int64_t(kKeyWaves));  // groups of chunks
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
 #define ZETA_BT_KEY(OFF)                                                                                       \
   hipLaunchKernelGGL((bwd_tile_key_kernel<DV, OFF>), dim3(blocks), dim3(kKeyThreads), 0, stream, v, perm, list_pos,    \
