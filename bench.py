@@ -351,6 +351,18 @@ def main() -> int:
         if ev is not None:
             ev[1].record()
 
+    hws = (zeta.select_attend_bwd_workspace_for(w.B, w.H, w.N, w.dv, w.topk, causal, dev, True)
+           if "history" in parts else None)
+
+    def bwd_hist_one_pass(ev=None):
+        if ev is not None:
+            ev[0].record()
+        zeta.zeta_select_attend_bwd(q, k, v, codes[0], sorted2[1], perm2[1], w.topk, causal, eps, dout,
+                                    q_order=bufs["order"], mean_k=mk, mean_v=mv, dq=gq, dk=gk, dv=gv, deps=geps,
+                                    workspace=hws)
+        if ev is not None:
+            ev[1].record()
+
     # Variants: the paper's chunked causal rule with 32 chunks (the one-pass
     # step), and each score variant's one-pass call (per-query kernels).
     variants = None
@@ -392,8 +404,9 @@ def main() -> int:
         hist_ms = timed(hist_means)[1]
         hist_step_ms, hist_fused_ms, _ = timed(step_hist)
         hist_bwd_ms = timed(bwd_hist)[0]
+        hist_one_bwd_ms = timed(bwd_hist_one_pass)[0]
     else:
-        hist_ms = hist_step_ms = hist_fused_ms = hist_bwd_ms = None
+        hist_ms = hist_step_ms = hist_fused_ms = hist_bwd_ms = hist_one_bwd_ms = None
     tokens = w.B * w.N
     a_bytes = attend_bytes(w, causal)
     f_bytes = a_bytes + w.segments * w.N * 4  # plus each query's code, read instead of an index row
@@ -475,6 +488,7 @@ def main() -> int:
             "means_achieved_GBs": gbs(h_bytes, hist_ms),
             "means_frac": frac(h_bytes, hist_ms),
             "backward_ms": hist_bwd_ms,
+            "one_pass_backward_ms": hist_one_bwd_ms,
         },
         "locality": locality,
         "variants": None if variants is None else dict(

@@ -331,7 +331,8 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
  * zeta_select_attend_bwd -- the gradients of zeta_topk_attn_bwd (same
  * definitions, Appendix E.2) for the windows zeta_select_attend_fwd selects,
  * computed from the lists as the one-pass call does, without an index tensor:
- * bfloat16 inputs, d_k = 3, the Cauchy score, no history-mean candidate.
+ * bfloat16 inputs, d_k = 3, the Cauchy score, with or without the
+ * history-mean candidate.
  * 16 neighbouring queries of the processing order form a tile.  A query pass
  * walks each tile's windows and gives dq, Z_i, c_i = dout_i . o_i and the
  * tile's window range per list; a key pass per list then takes 16 list
@@ -347,6 +348,10 @@ zeta_status_t zeta_topk_attn_bwd(const void* q, const void* k, const void* v, ze
  *   q, k, v, dtype, B, H, N, d_k, d_v, topk, causal, chunk, q_codes,
  *            sorted_codes, perm, q_order, eps: as for zeta_select_attend_fwd.
  *   dout     [B][H][N][d_v] bfloat16, 16-byte aligned: dL/do.
+ *   mean_k, mean_v  optional, as for zeta_topk_attn_bwd (from
+ *            zeta_history_mean with the same causal flag): the candidate
+ *            joins every query's sums and the gradients reaching the means
+ *            pass to the rows of each query's history.
  *   dq, dk   float32 [B][H][N][d_k] outputs; dv float32 [B][H][N][d_v],
  *            16-byte aligned; deps float32 [1].  Every element is written.
  *   workspace  at least zeta_select_attend_bwd_workspace_size(...) bytes,
@@ -359,9 +364,10 @@ zeta_status_t zeta_select_attend_bwd(const void* q, const void* k, const void* v
                                      int64_t B, int64_t H, int64_t N, int d_k, int d_v, int topk,
                                      int causal, int chunk, const uint32_t* q_codes,
                                      const uint32_t* sorted_codes, const int32_t* perm,
-                                     const int32_t* q_order, const void* dout, float eps, float* dq,
-                                     float* dk, float* dv, float* deps, void* workspace,
-                                     size_t workspace_bytes, hipStream_t stream);
+                                     const int32_t* q_order, const void* dout, float eps,
+                                     const float* mean_k, const float* mean_v, float* dq, float* dk,
+                                     float* dv, float* deps, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream);
 
 /*
  * zeta_exact_knn -- the locality experiment's reference (Section 4.4): the kn
@@ -423,11 +429,12 @@ size_t zeta_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int d_v
  * zeta_select_attend_bwd on this shape: the one-pass call's lists, window
  * bounds and key rows, 36 + 2 * d_v bytes per row (a 32-byte record of the
  * row's query, a copy of its dout row and its part of deps), 24 bytes per
- * tile of 16 rows and list, and 4 KiB of sums.  Returns 0 for invalid shapes
- * and unsupported d_v.
+ * tile of 16 rows and list, and 4 KiB of sums; with history_mean nonzero also
+ * 4 * (3 + d_v) bytes per row (the gradients reaching the means) and their
+ * scan's sums.  Returns 0 for invalid shapes and unsupported d_v.
  */
 size_t zeta_select_attend_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_v, int topk,
-                                             int causal);
+                                             int causal, int history_mean);
 
 /* Static, human-readable name of a status code. */
 const char* zeta_status_string(zeta_status_t status);

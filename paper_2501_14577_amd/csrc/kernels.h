@@ -90,13 +90,14 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
                                      int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream);
 
 // Gradients of the bfloat16 one-pass attention (d_k = 3, Cauchy score) over
-// its windows: prefix lists, window bounds, query pass, envelopes, key passes
-// and the deps sum; dq, dk, dv and deps float32.
+// its windows, with the optional history-mean candidate: prefix lists, window
+// bounds, query pass, envelopes, key passes, the means' spread and the deps
+// sum; dq, dk, dv and deps float32.
 hipError_t launch_select_attend_bwd(const void* q, const void* k, const void* v, const void* dout, int64_t S,
                                     int64_t N, int dk_, int dv_, int topk, bool causal, int chunk,
                                     const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                                    const int32_t* q_order, float eps, float* dq, float* dk, float* dv,
-                                    float* deps, void* workspace, hipStream_t stream);
+                                    const int32_t* q_order, float eps, HistMean hm, float* dq, float* dk,
+                                    float* dv, float* deps, void* workspace, hipStream_t stream);
 
 // Select and attend in one pass (idx_out optional); score: a ScoreMode (the
 // matrix-core tiles serve the Cauchy score of bfloat16 inputs).

@@ -151,38 +151,6 @@ inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
-// Gradients of the bfloat16 one-pass attention: the one-pass call's lists,
-// bounds and key rows, then per slot a 32-byte record, a copy of the dout row
-// and the deps part, each tile's window range per list and their envelopes,
-// each chunk's candidate tiles (in the envelopes' layout) and the block sums
-// of deps.
-constexpr int64_t kTileBwdRedPer = 4096;  // deps parts per block sum (at least)
-constexpr int64_t kTileBwdRedMax = 1024;  // block sums at most
-inline int tile_bwd_levels(int64_t N, int topk, bool causal) {
-  const ListPlan lp = list_plan(N, topk);
-  return causal ? lp.levels + 1 : 1;  // the prefix lists, then the full list
-}
-struct TileBwdWs {
-  FusedWs fused;
-  size_t rec_off, dslot_off, part_off, env_off, env2_off, ranges_off, sums_off, bytes;
-};
-inline TileBwdWs tile_bwd_ws(int64_t S, int64_t N, int dv, int topk, int causal) {
-  TileBwdWs w;
-  w.fused = fused_ws(S, N, topk, causal);
-  const size_t rows = size_t(S) * size_t(N);
-  const size_t tiles = size_t(S) * size_t((N + 15) / 16);
-  const size_t env = size_t(tile_bwd_levels(N, topk, causal != 0)) * tiles * 2 * sizeof(int32_t);
-  w.rec_off = align_up(w.fused.bytes);
-  w.dslot_off = w.rec_off + align_up(rows * 32);
-  w.part_off = w.dslot_off + align_up(rows * size_t(dv) * 2);
-  w.env_off = w.part_off + align_up(rows * sizeof(float));
-  w.env2_off = w.env_off + align_up(env);
-  w.ranges_off = w.env2_off + align_up(env);
-  w.sums_off = w.ranges_off + align_up(env);
-  w.bytes = w.sums_off + align_up(size_t(kTileBwdRedMax) * sizeof(float));
-  return w;
-}
-
 // ---- locality experiment -------------------------------------------------------
 // Keys per query sorted in LDS by the exact nearest-key search, and segment
 // length covered by the overlap count's LDS bit set.
@@ -256,6 +224,48 @@ inline QueryOrderWs query_order_ws(int64_t S, int64_t N) {
   w.given_off = 0;
   w.phist_off = align_up(size_t(S) * size_t(N) * sizeof(int32_t));
   w.bytes = w.phist_off + align_up(size_t(S) * size_t(ceil_div(N, kSortTile) + 1) * kRadixMax * sizeof(uint32_t));
+  return w;
+}
+
+// Gradients of the bfloat16 one-pass attention: the one-pass call's lists,
+// bounds and key rows, then per slot a 32-byte record, a copy of the dout row
+// and the deps part, each tile's window range per list and their envelopes,
+// each chunk's candidate tiles (in the envelopes' layout), the block sums of
+// deps and, with the history-mean candidate, the gradients reaching the means
+// and their scan's sums.
+constexpr int64_t kTileBwdRedPer = 4096;  // deps parts per block sum (at least)
+constexpr int64_t kTileBwdRedMax = 1024;  // block sums at most
+inline int tile_bwd_levels(int64_t N, int topk, bool causal) {
+  const ListPlan lp = list_plan(N, topk);
+  return causal ? lp.levels + 1 : 1;  // the prefix lists, then the full list
+}
+struct TileBwdWs {
+  FusedWs fused;
+  size_t rec_off, dslot_off, part_off, env_off, env2_off, ranges_off, sums_off;
+  size_t hist_k_off, hist_v_off, hist_scan_off, bytes;
+};
+inline TileBwdWs tile_bwd_ws(int64_t S, int64_t N, int dv, int topk, int causal, bool history = false) {
+  TileBwdWs w;
+  w.fused = fused_ws(S, N, topk, causal);
+  const size_t rows = size_t(S) * size_t(N);
+  const size_t tiles = size_t(S) * size_t((N + 15) / 16);
+  const size_t env = size_t(tile_bwd_levels(N, topk, causal != 0)) * tiles * 2 * sizeof(int32_t);
+  w.rec_off = align_up(w.fused.bytes);
+  w.dslot_off = w.rec_off + align_up(rows * 32);
+  w.part_off = w.dslot_off + align_up(rows * size_t(dv) * 2);
+  w.env_off = w.part_off + align_up(rows * sizeof(float));
+  w.env2_off = w.env_off + align_up(env);
+  w.ranges_off = w.env2_off + align_up(env);
+  w.sums_off = w.ranges_off + align_up(env);
+  w.hist_k_off = w.sums_off + align_up(size_t(kTileBwdRedMax) * sizeof(float));
+  w.hist_v_off = w.hist_k_off;
+  w.hist_scan_off = w.hist_k_off;
+  w.bytes = w.hist_k_off;
+  if (history) {  // the gradients reaching the means (d_k = 3) and their scan
+    w.hist_v_off = w.hist_k_off + align_up(rows * 3 * sizeof(float));
+    w.hist_scan_off = w.hist_v_off + align_up(rows * size_t(dv) * sizeof(float));
+    w.bytes = w.hist_scan_off + hist_ws(S, N, 3 + dv).bytes;
+  }
   return w;
 }
 

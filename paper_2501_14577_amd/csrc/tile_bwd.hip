@@ -37,6 +37,12 @@
 // order: no atomics, and the outputs are the same from run to run for a given
 // processing order.  Any processing order is correct; the one from
 // zeta_query_order keeps each chunk's candidate tiles few.
+//
+// With the history-mean candidate (Section 3.4, last paragraph) the query pass
+// adds the pair (mean_k[i], mean_v[i]) to its sums once per query (float32,
+// its dot product dout_i . mean_v[i] from the lanes' dout slices) and writes
+// the gradients reaching the means, divided by the history's length; after
+// the key passes a reverse scan adds them to the rows of every history.
 #include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -129,7 +135,7 @@ __device__ __forceinline__ int level_index(int lvl, int causal, int t0, int t_hi
 }
 
 // ---- 1. query pass ----------------------------------------------------------
-template <int DV>
+template <int DV, bool kHist>
 __global__ void __launch_bounds__(kBtWaves * 64) __attribute__((amdgpu_waves_per_eu(DV <= 128 ? 3 : 1)))
     bwd_tile_query_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
                           const uint16_t* __restrict__ dout, const int32_t* __restrict__ sorted_pos,
@@ -138,7 +144,8 @@ __global__ void __launch_bounds__(kBtWaves * 64) __attribute__((amdgpu_waves_per
                           const uint2* __restrict__ keys_list, int64_t S, int64_t N, int64_t ct, int causal,
                           int chunk, int t0, int t_hi, int levels, int64_t cap, float eps, float* __restrict__ dq,
                           SlotRec* __restrict__ rec, uint16_t* __restrict__ dslot, float* __restrict__ deps_part,
-                          int2* __restrict__ env) {
+                          int2* __restrict__ env, const float* __restrict__ mk, const float* __restrict__ mv,
+                          float* __restrict__ hk, float* __restrict__ hv) {
   constexpr int NS = DV / 32;  // 32-column slices of a row: one product each
   static_assert(DV % 32 == 0, "d_v must be a multiple of 32");
   __shared__ __align__(16) int32_t s_pos[kBtWaves][kBtStage];
@@ -207,7 +214,8 @@ __global__ void __launch_bounds__(kBtWaves * 64) __attribute__((amdgpu_waves_per
       uint32_t dfr[NS][4];  // dout of query qn, columns 32s + 8kg .. 32s + 8kg + 7
 #pragma unroll
       for (int s = 0; s < NS; ++s) dfr[s][0] = dfr[s][1] = dfr[s][2] = dfr[s][3] = 0u;
-      if (mine) {
+      // With the history-mean candidate every query has a candidate.
+      if (kHist ? in_grp : mine) {
         const int64_t gq = seg * N + my_i;
         Row3<uint16_t>::load(q, gq, S * N, qv);
 #pragma unroll
@@ -329,6 +337,64 @@ __global__ void __launch_bounds__(kBtWaves * 64) __attribute__((amdgpu_waves_per
       for (int a = 0; a < 3; ++a) {
         u[a] = kg_sum(u[a]);
         rr[a] = kg_sum(rr[a]);
+      }
+      // The history-mean candidate's terms, once per query (every lane of the
+      // query adds them to its totals).
+      float s_m = 0.0f, p_m = 0.0f, dm[3] = {0.0f, 0.0f, 0.0f};
+      if constexpr (kHist) {
+        if (in_grp) {
+          const int64_t gq = seg * N + my_i;
+          const float4* mrow = reinterpret_cast<const float4*>(mv + gq * DV);
+          float part = 0.0f;
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            const float4 m0 = mrow[(32 * s + 8 * kg) / 4], m1 = mrow[(32 * s + 8 * kg) / 4 + 1];
+            const float mvv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              part = fmaf(__uint_as_float(dfr[s][t] << 16), mvv[2 * t], part);
+              part = fmaf(__uint_as_float(dfr[s][t] & 0xFFFF0000u), mvv[2 * t + 1], part);
+            }
+          }
+          p_m = kg_sum(part);
+#pragma unroll
+          for (int a = 0; a < 3; ++a) dm[a] = qv[a] - mk[gq * 3 + a];
+          s_m = __builtin_amdgcn_rcpf(fmaf(dm[2], dm[2], fmaf(dm[1], dm[1], dm[0] * dm[0])) + eps);
+          const float s2 = s_m * s_m;
+          z += s_m;
+          pz = fmaf(s_m, p_m, pz);
+          yz += s2;
+          xz = fmaf(s2, p_m, xz);
+#pragma unroll
+          for (int a = 0; a < 3; ++a) {
+            u[a] = fmaf(s2 * p_m, dm[a], u[a]);
+            rr[a] = fmaf(s2, dm[a], rr[a]);
+          }
+        }
+      }
+      if constexpr (kHist) {
+        if (in_grp) {
+          // The gradients reaching mean_k[i] and mean_v[i], divided by the
+          // history's length.
+          const float inv = z > 0.0f ? 1.0f / z : 0.0f;
+          const float cc = pz * inv;
+          const float inv_cnt = 1.0f / float(causal ? my_i + 1 : N);
+          const int64_t gq = seg * N + my_i;
+          const float w_m = (p_m - cc) * s_m * s_m * inv;
+          if (kg == 0) {
+#pragma unroll
+            for (int a = 0; a < 3; ++a) hk[gq * 3 + a] = 2.0f * w_m * dm[a] * inv_cnt;
+          }
+          const float am = s_m * inv * inv_cnt;
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            float4* dst = reinterpret_cast<float4*>(hv + gq * DV + 32 * s + 8 * kg);
+            dst[0] = make_float4(am * __uint_as_float(dfr[s][0] << 16), am * __uint_as_float(dfr[s][0] & 0xFFFF0000u),
+                                 am * __uint_as_float(dfr[s][1] << 16), am * __uint_as_float(dfr[s][1] & 0xFFFF0000u));
+            dst[1] = make_float4(am * __uint_as_float(dfr[s][2] << 16), am * __uint_as_float(dfr[s][2] & 0xFFFF0000u),
+                                 am * __uint_as_float(dfr[s][3] << 16), am * __uint_as_float(dfr[s][3] & 0xFFFF0000u));
+          }
+        }
       }
       if (in_grp && kg == 0) {
         const float inv = z > 0.0f ? 1.0f / z : 0.0f;
@@ -725,8 +791,8 @@ template <int DV>
 hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_t* dout, int64_t S, int64_t N,
                              int topk, bool causal, int chunk, const int32_t* perm, const int32_t* list_pos,
                              const int32_t* q_order, const int2* bounds, const uint2* keys_full,
-                             const uint2* keys_list, float eps, float* dq, float* dk, float* dv, float* deps,
-                             const TileBwdWs& ws, char* wsb, hipStream_t stream) {
+                             const uint2* keys_list, float eps, HistMean hm, float* dq, float* dk, float* dv,
+                             float* deps, const TileBwdWs& ws, char* wsb, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t ct = ceil_div(N, int64_t(16));
   const int nl = tile_bwd_levels(N, topk, causal);
@@ -737,6 +803,8 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
   int2* env = reinterpret_cast<int2*>(wsb + ws.env_off);
   int2* env2 = reinterpret_cast<int2*>(wsb + ws.env2_off);
   int2* ranges = reinterpret_cast<int2*>(wsb + ws.ranges_off);
+  float* hk = reinterpret_cast<float*>(wsb + ws.hist_k_off);
+  float* hv = reinterpret_cast<float*>(wsb + ws.hist_v_off);
   float* sums = reinterpret_cast<float*>(wsb + ws.sums_off);
   const int64_t nenv = int64_t(nl) * S * ct;
   {
@@ -749,9 +817,15 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
     const int64_t tiles = S * ct;
     const int64_t want = ceil_div(tiles, int64_t(kBtWaves));
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
-    hipLaunchKernelGGL((bwd_tile_query_kernel<DV>), dim3(blocks), dim3(kBtWaves * 64), 0, stream, q, v, dout, perm,
-                       list_pos, q_order, bounds, keys_full, keys_list, S, N, ct, cz, chunk, lp.t0, lp.t_hi,
-                       lp.levels, lp.cap, eps, dq, rec, dslot, part, env);
+#define ZETA_BT_QUERY(HIST)                                                                                     \
+  hipLaunchKernelGGL((bwd_tile_query_kernel<DV, HIST>), dim3(blocks), dim3(kBtWaves * 64), 0, stream, q, v, dout, perm, \
+                     list_pos, q_order, bounds, keys_full, keys_list, S, N, ct, cz, chunk, lp.t0, lp.t_hi, lp.levels,   \
+                     lp.cap, eps, dq, rec, dslot, part, env, hm.k, hm.v, hk, hv)
+    if (hm.k != nullptr)
+      ZETA_BT_QUERY(true);
+    else
+      ZETA_BT_QUERY(false);
+#undef ZETA_BT_QUERY
   }
   hipLaunchKernelGGL(bwd_envelope_kernel, dim3(unsigned(int64_t(nl) * S)), dim3(kEnvThreads), 0, stream, env, ct,
                      env2);
@@ -774,6 +848,11 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
       ZETA_BT_KEY(false);
 #undef ZETA_BT_KEY
   }
+  if (hm.k != nullptr) {
+    // The gradients reaching the means pass to the rows of every history.
+    const hipError_t e = launch_history_spread(hv, dv, DV, hk, dk, 3, S, N, causal, wsb + ws.hist_scan_off, stream);
+    if (e != hipSuccess) return e;
+  }
   const int64_t total = S * N;
   const int64_t nred = ceil_div(total, kTileBwdRedPer) < kTileBwdRedMax ? ceil_div(total, kTileBwdRedPer)
                                                                         : kTileBwdRedMax;
@@ -789,15 +868,15 @@ hipError_t launch_tile_bwd_t(const uint16_t* q, const uint16_t* v, const uint16_
 hipError_t launch_select_attend_bwd(const void* q, const void* k, const void* v, const void* dout, int64_t S,
                                     int64_t N, int dk_, int dv_, int topk, bool causal, int chunk,
                                     const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                                    const int32_t* q_order, float eps, float* dq, float* dk, float* dv,
-                                    float* deps, void* workspace, hipStream_t stream) {
+                                    const int32_t* q_order, float eps, HistMean hm, float* dq, float* dk,
+                                    float* dv, float* deps, void* workspace, hipStream_t stream) {
   const uint32_t* list_codes = nullptr;
   const int32_t* list_pos = nullptr;
   if (causal) {
     const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
     if (e != hipSuccess) return e;
   }
-  const TileBwdWs ws = tile_bwd_ws(S, N, dv_, topk, causal ? 1 : 0);
+  const TileBwdWs ws = tile_bwd_ws(S, N, dv_, topk, causal ? 1 : 0, hm.k != nullptr);
   char* wsb = static_cast<char*>(workspace);
   int2* bounds = reinterpret_cast<int2*>(wsb + ws.fused.bounds_off);
   uint2* keys_full = reinterpret_cast<uint2*>(wsb + ws.fused.keys_full_off);
@@ -811,7 +890,7 @@ hipError_t launch_select_attend_bwd(const void* q, const void* k, const void* v,
 #define ZETA_TILE_BWD_CASE(DVV)                                                                                      \
   case DVV:                                                                                                          \
     return launch_tile_bwd_t<DVV>(qq, vv, dd, S, N, topk, causal, chunk, perm, list_pos, q_order, bounds, keys_full, \
-                                  keys_list, eps, dq, dk, dv, deps, ws, wsb, stream);
+                                  keys_list, eps, hm, dq, dk, dv, deps, ws, wsb, stream);
   switch (dv_) {
     ZETA_TILE_BWD_CASE(32)
     ZETA_TILE_BWD_CASE(64)

@@ -250,39 +250,42 @@ zeta_status_t zeta_index_overlap(const int32_t* idx_a, int ka, const int32_t* id
 zeta_status_t zeta_select_attend_bwd(const void* q, const void* k, const void* v, zeta_dtype_t dtype, int64_t B,
                                      int64_t H, int64_t N, int d_k, int d_v, int topk, int causal, int chunk,
                                      const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
-                                     const int32_t* q_order, const void* dout, float eps, float* dq, float* dk,
-                                     float* dv, float* deps, void* workspace, size_t workspace_bytes,
-                                     hipStream_t stream) {
+                                     const int32_t* q_order, const void* dout, float eps, const float* mean_k,
+                                     const float* mean_v, float* dq, float* dk, float* dv, float* deps,
+                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!q || !k || !v || !dout || !q_codes || !sorted_codes || !perm || !dq || !dk || !dv || !deps)
     return ZETA_ERR_INVALID_ARG;
   if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
   if (d_k < 1 || d_v < 1 || topk < 1 || bad_pool(causal, chunk)) return ZETA_ERR_INVALID_ARG;
   if (!(isfinite(eps) && eps > 0.0f)) return ZETA_ERR_INVALID_ARG;
   if (!aligned16(v) || !aligned16(dout) || !aligned16(dv)) return ZETA_ERR_INVALID_ARG;
+  if (bad_means(mean_k, mean_v)) return ZETA_ERR_INVALID_ARG;
   // Outputs are distinct buffers, none of them an input.
   const void* outs[4] = {dq, dk, dv, deps};
-  const void* ins[8] = {q, k, v, dout, q_codes, sorted_codes, perm, q_order};
+  const void* ins[10] = {q, k, v, dout, q_codes, sorted_codes, perm, q_order, mean_k, mean_v};
   for (int a = 0; a < 4; ++a) {
     for (int b = a + 1; b < 4; ++b)
       if (outs[a] == outs[b]) return ZETA_ERR_INVALID_ARG;
-    for (int b = 0; b < 8; ++b)
+    for (int b = 0; b < 10; ++b)
       if (ins[b] != nullptr && outs[a] == ins[b]) return ZETA_ERR_INVALID_ARG;
   }
   if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
   if (dtype != ZETA_BF16 || d_k != 3 || !zeta::tile_supports(d_v) || topk > zeta::kMaxTopk)
     return ZETA_ERR_UNSUPPORTED;
   const int64_t S = B * H;
-  const zeta::TileBwdWs ws = zeta::tile_bwd_ws(S, N, d_v, topk, causal);
+  const zeta::TileBwdWs ws = zeta::tile_bwd_ws(S, N, d_v, topk, causal, mean_k != nullptr);
   if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
   if (!aligned16(workspace)) return ZETA_ERR_INVALID_ARG;
   return hip_status(zeta::launch_select_attend_bwd(q, k, v, dout, S, N, d_k, d_v, topk, causal != 0, chunk, q_codes,
-                                                   sorted_codes, perm, q_order, eps, dq, dk, dv, deps, workspace,
+                                                   sorted_codes, perm, q_order, eps,
+                                                   zeta::HistMean{mean_k, mean_v}, dq, dk, dv, deps, workspace,
                                                    stream));
 }
 
-size_t zeta_select_attend_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_v, int topk, int causal) {
+size_t zeta_select_attend_bwd_workspace_size(int64_t B, int64_t H, int64_t N, int d_v, int topk, int causal,
+                                             int history_mean) {
   if (bad_count(B, H, N) || topk < 1 || (causal != 0 && causal != 1) || !zeta::tile_supports(d_v)) return 0;
-  return zeta::tile_bwd_ws(B * H, N, d_v, topk, causal).bytes;
+  return zeta::tile_bwd_ws(B * H, N, d_v, topk, causal, history_mean != 0).bytes;
 }
 
 size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, int topk, int causal) {

@@ -77,8 +77,8 @@ def load_library() -> ctypes.CDLL:
     L.zeta_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_bwd_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_select_attend_bwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp,
-                                         vp, f32, vp, vp, vp, vp, vp, sz, vp]
-    L.zeta_select_attend_bwd_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32]
+                                         vp, f32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.zeta_select_attend_bwd_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
     for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
                  "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_history_mean", "zeta_topk_attn_bwd",
@@ -145,12 +145,14 @@ def bwd_workspace_for(B, H, N, d_k, d_v, topk, history_mean, device) -> torch.Te
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-def zeta_select_attend_bwd_workspace_size(B: int, H: int, N: int, d_v: int, topk: int, causal: bool) -> int:
-    return int(load_library().zeta_select_attend_bwd_workspace_size(B, H, N, d_v, topk, int(bool(causal))))
+def zeta_select_attend_bwd_workspace_size(B: int, H: int, N: int, d_v: int, topk: int, causal: bool,
+                                          history_mean: bool = False) -> int:
+    return int(load_library().zeta_select_attend_bwd_workspace_size(B, H, N, d_v, topk, int(bool(causal)),
+                                                                      int(bool(history_mean))))
 
 
-def select_attend_bwd_workspace_for(B, H, N, d_v, topk, causal, device) -> torch.Tensor:
-    n = max(zeta_select_attend_bwd_workspace_size(B, H, N, d_v, topk, causal), 256)
+def select_attend_bwd_workspace_for(B, H, N, d_v, topk, causal, device, history_mean: bool = False) -> torch.Tensor:
+    n = max(zeta_select_attend_bwd_workspace_size(B, H, N, d_v, topk, causal, history_mean), 256)
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
@@ -368,12 +370,15 @@ def zeta_select_attend_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_
 def zeta_select_attend_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_codes: torch.Tensor,
                            sorted_codes: torch.Tensor, perm: torch.Tensor, topk: int, causal: bool, eps: float,
                            dout: torch.Tensor, *, chunk: int = 0, q_order: Optional[torch.Tensor] = None,
+                           mean_k: Optional[torch.Tensor] = None, mean_v: Optional[torch.Tensor] = None,
                            dq: Optional[torch.Tensor] = None, dk: Optional[torch.Tensor] = None,
                            dv: Optional[torch.Tensor] = None, deps: Optional[torch.Tensor] = None,
                            workspace: Optional[torch.Tensor] = None):
     """Gradients of zeta_select_attend_fwd's attention (bfloat16, d_k = 3,
     Cauchy score) -> (dq, dk, dv, deps), float32: dq, dk [B,H,N,3],
-    dv [B,H,N,d_v], deps [1]."""
+    dv [B,H,N,d_v], deps [1].  With mean_k and mean_v the history-mean
+    candidate takes part, and ``causal`` also says how its history was
+    formed."""
     B, H, N, dkk = q.shape
     dvv = v.shape[-1]
     f32 = dict(dtype=torch.float32, device=q.device)
@@ -382,16 +387,17 @@ def zeta_select_attend_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_
     dv = torch.empty((B, H, N, dvv), **f32) if dv is None else dv
     deps = torch.empty((1,), **f32) if deps is None else deps
     if workspace is None:
-        workspace = select_attend_bwd_workspace_for(B, H, N, dvv, topk, causal, q.device)
-    _need_device(q, k, v, q_codes, sorted_codes, perm, q_order, dout, dq, dk, dv, deps, workspace)
+        workspace = select_attend_bwd_workspace_for(B, H, N, dvv, topk, causal, q.device, mean_k is not None)
+    _need_device(q, k, v, q_codes, sorted_codes, perm, q_order, dout, mean_k, mean_v, dq, dk, dv, deps, workspace)
+    _means(mean_k, mean_v)
     if not (q.dtype == k.dtype == v.dtype == dout.dtype):
         raise ValueError("q, k, v and dout must share a dtype")
     if any(t.dtype != torch.float32 for t in (dq, dk, dv, deps)):
         raise ValueError("gradients are float32")
     st = load_library().zeta_select_attend_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, dkk, dvv, topk,
                                                int(bool(causal)), int(chunk), _ptr(q_codes), _ptr(sorted_codes),
-                                               _ptr(perm), _ptr(q_order), _ptr(dout), float(eps), _ptr(dq),
-                                               _ptr(dk), _ptr(dv), _ptr(deps), _ptr(workspace),
+                                               _ptr(perm), _ptr(q_order), _ptr(dout), float(eps), _ptr(mean_k),
+                                               _ptr(mean_v), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(deps), _ptr(workspace),
                                                workspace.numel() * workspace.element_size(), _stream())
     _check("zeta_select_attend_bwd", st)
     return dq, dk, dv, deps

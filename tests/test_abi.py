@@ -321,9 +321,9 @@ def test_attend_bwd_rejects(kw, code):
 def _obwd(**kw):
     a = dict(q=P, k=P2, v=P3, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, d_v=64, topk=8, causal=1, chunk=0,
              q_codes=P4, sorted_codes=ctypes.c_void_p(0xD0000), perm=ctypes.c_void_p(0xE0000), q_order=NULL,
-             dout=ctypes.c_void_p(0x50000), eps=0.5, dq=ctypes.c_void_p(0x60000), dk=ctypes.c_void_p(0x70000),
-             dv=ctypes.c_void_p(0x80000), deps=ctypes.c_void_p(0x90000), ws=ctypes.c_void_p(0xA0000), ws_bytes=BIG,
-             stream=NULL)
+             dout=ctypes.c_void_p(0x50000), eps=0.5, mean_k=NULL, mean_v=NULL, dq=ctypes.c_void_p(0x60000),
+             dk=ctypes.c_void_p(0x70000), dv=ctypes.c_void_p(0x80000), deps=ctypes.c_void_p(0x90000),
+             ws=ctypes.c_void_p(0xA0000), ws_bytes=BIG, stream=NULL)
     a.update(kw)
     return zeta.load_library().zeta_select_attend_bwd(*a.values())
 
@@ -342,6 +342,9 @@ OBWD_CASES = [
     (dict(dtype=7), UNS), (dict(dtype=zb.ZETA_F32), UNS), (dict(d_k=2), UNS), (dict(d_k=4), UNS),
     (dict(d_v=48), UNS), (dict(d_v=512), UNS), (dict(topk=1025), UNS),
     (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP), (dict(ws=ctypes.c_void_p(0xA0008)), INV),
+    (dict(mean_k=ctypes.c_void_p(0xB0000)), INV),  # means come in pairs
+    (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0008)), INV),  # mean_v 16-byte aligned
+    (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0000), dq=ctypes.c_void_p(0xB0000)), INV),
 ]
 
 
@@ -355,7 +358,7 @@ def test_select_attend_bwd_workspace_size():
     assert ws(0, 1, 10, 64, 4, 1) == 0
     assert ws(1, 1, 10, 64, 0, 1) == 0
     assert ws(1, 1, 10, 48, 4, 1) == 0
-    assert zeta.load_library().zeta_select_attend_bwd_workspace_size(1, 1, 10, 64, 4, 2) == 0  # causal not 0/1
+    assert zeta.load_library().zeta_select_attend_bwd_workspace_size(1, 1, 10, 64, 4, 2, 0) == 0  # causal not 0/1
     # Long-context shape: the one-pass call's buffers plus, per row, the
     # 32-byte record, the dout copy (2 x 128 B) and the deps part.
     big = ws(1, 16, 65536, 128, 128, 1)
@@ -364,3 +367,5 @@ def test_select_attend_bwd_workspace_size():
     assert big < rows * (32 + 256 + 4) + (96 << 20)
     assert big % 256 == 0
     assert ws(1, 1, 1, 32, 1, 0) > 0
+    # The history-mean candidate adds (3 + 128) x 4 B per row and the scan's sums.
+    assert ws(1, 16, 65536, 128, 128, 1, True) >= big + rows * 131 * 4

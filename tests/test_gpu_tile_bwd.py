@@ -164,3 +164,32 @@ def test_tile_bwd_long_context():
     assert np.all(np.abs(dsum) <= 1e-4 * (1.0 + scale)), (dsum, scale)
     dsv = oracle.as_f32(dout_raw, w.dtype).astype(np.float64).sum(axis=1)
     assert np.allclose(dv.sum(axis=1), dsv, rtol=1e-4, atol=1e-2), np.abs(dv.sum(axis=1) - dsv).max()
+
+
+HIST = [(2, True, 2), (3, False, 2), (3, True, 2)]
+
+
+@pytest.mark.parametrize("cfg,causal,nseg", HIST)
+def test_tile_bwd_history(cfg, causal, nseg):
+    """With the history-mean candidate (means from zeta_history_mean, the
+    same causal flag): the one-pass gradients match the oracle's, whose means
+    and gradients through them are its own (Section 3.4)."""
+    w, x, f = inputs(cfg)
+    log(f"tile bwd history config {cfg} causal={causal}")
+    S = w.segments
+    raw = {n: a.reshape(S, w.N, -1)[:nseg] for n, a in x.items()}
+    fs = {n: a[:nseg] for n, a in f.items()}
+    dout_raw = workloads.generate_dout(w).reshape(S, w.N, w.dv)[:nseg]
+    q, k, v, dout = (to_dev(a[None], w.dtype) for a in (raw["q"], raw["k"], raw["v"], dout_raw))
+    res = zeta.forward(q, k, v, w.topk, 0.5, causal, w.bits, fused=True, history=True, return_intermediates=True)
+    grads = zeta.zeta_select_attend_bwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, causal,
+                                        0.5, dout, q_order=res["q_order"], mean_k=res["mean_k"], mean_v=res["mean_v"])
+    torch.cuda.synchronize()
+    idx = host(res["idx"]).reshape(nseg, w.N, w.topk)
+    dq, dk, dv, deps = (host(t) for t in grads)
+    rq, rk, rv, reps = oracle.attend_bwd(fs["q"], fs["k"], fs["v"], idx, 0.5, oracle.as_f32(dout_raw, w.dtype),
+                                         history=True, causal=causal)
+    _close(dq.reshape(rq.shape), rq, "dq")
+    _close(dk.reshape(rk.shape), rk, "dk")
+    _close(dv.reshape(rv.shape), rv, "dv")
+    assert abs(float(deps[0]) - reps) <= 1e-4 * (1.0 + abs(reps)), (float(deps[0]), reps)
