@@ -86,8 +86,9 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
                                      int topk, bool causal, int chunk, const uint32_t* q_codes,
                                      const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                                     const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
-                                     int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream);
+                                     const int32_t* q_order, int score, float eps, HistMean hm, void* out,
+                                     int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
+                                     hipStream_t stream);
 
 // Gradients of the bfloat16 one-pass attention (d_k = 3, Cauchy score) over
 // its windows, with the optional history-mean candidate: prefix lists, window
@@ -100,7 +101,8 @@ hipError_t launch_select_attend_bwd(const void* q, const void* k, const void* v,
                                     float* dv, float* deps, void* workspace, hipStream_t stream);
 
 // Select and attend in one pass (idx_out optional); score: a ScoreMode (the
-// matrix-core tiles serve the Cauchy score of bfloat16 inputs).
+// matrix-core tiles serve bfloat16 inputs: the Cauchy score, and every score
+// when d_k = 3).
 hipError_t launch_select_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S, int64_t N,
                                 int dk, int dv, int topk, bool causal, int chunk, const uint32_t* q_codes,
                                 const uint32_t* sorted_codes, const int32_t* perm, const int32_t* q_order,

@@ -362,15 +362,15 @@ __global__ void __launch_bounds__(256)
 
 // ---- attention over the windows ----------------------------------------------
 
-template <int DV, int DK, bool kOff32, bool kHist>
+template <int DV, int DK, bool kOff32, bool kHist, bool kVar>
 __global__ void __launch_bounds__(kTileWaves * 64)
     select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                               const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
                               const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
                               const int2* __restrict__ bounds, const uint2* __restrict__ keys_full,
                               const uint2* __restrict__ keys_list, int64_t total, int64_t N, int dk_rt, int causal,
-                              int chunk, int t0, int t_hi, int64_t cap, float eps, const float* __restrict__ mk,
-                              const float* __restrict__ mv, uint16_t* __restrict__ out) {
+                              int chunk, int t0, int t_hi, int64_t cap, int score_rt, float eps,
+                              const float* __restrict__ mk, const float* __restrict__ mv, uint16_t* __restrict__ out) {
   constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
   constexpr int W = E / 2;    // 32-bit words per lane and row
   constexpr int KD = DK > 0 ? DK : kMaxDk;
@@ -379,6 +379,12 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   static_assert(E >= 2 && E % 2 == 0, "d_v must be a multiple of 32");
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
+  // Score: the Cauchy score, or with kVar a variant (softmax variants run
+  // an online softmax per query: a running maximum shared by the query's 4
+  // lanes, the accumulators and the normaliser rescaled when it grows).
+  const int score = kVar ? score_rt : kScoreCauchy;
+  const bool smax = kVar && score_is_softmax(score);
+  const float rsd = 1.0f / sqrtf(float(dk));
 
   // Key rows padded to a multiple of 4 floats, so 4 consecutive entries'
   // positions and each key row are whole 16-byte LDS reads.
@@ -459,13 +465,28 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
       for (int j = 0; j < E; ++j) acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
       float zpart = 0.0f;
+      float run_max = -INFINITY;  // softmax variants: the query's largest logit so far
+      const float qnorm = (kVar && score == kScoreNormDot) ? row_norm<KD>(qv, dk) : 0.0f;
       // The history-mean candidate starts the sums, in float32: its score
       // (counted once, by the kg = 0 lanes) and its weighted mean value in
-      // this lane's output elements kg*4E .. kg*4E + 4E - 1.
+      // this lane's output elements kg*4E .. kg*4E + 4E - 1.  Under a softmax
+      // variant its logit starts the running maximum and its weight is 1.
       if constexpr (kHist) {
         if (in_grp) {
           const int64_t gq = g_seg * N + my_i;
-          const float s_mean = mean_score<KD>(mk, gq, dk, qv, eps);
+          float s_mean;
+          if constexpr (kVar) {
+            float mkv[KD];
+#pragma unroll
+            for (int a = 0; a < KD; ++a) mkv[a] = a < dk ? mk[gq * dk + a] : 0.0f;
+            s_mean = variant_term<KD>(score, qv, mkv, dk, eps, rsd, qnorm);
+            if (smax) {
+              run_max = s_mean;
+              s_mean = 1.0f;
+            }
+          } else {
+            s_mean = mean_score<KD>(mk, gq, dk, qv, eps);
+          }
           if (kg == 0) zpart = s_mean;
           const float* mrow = mv + gq * DV + kg * 4 * E;
 #pragma unroll
@@ -501,7 +522,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // takes has weight 0).  The reciprocal is the hardware one (1 ulp).  A
       // score s is split as hi = bf16(s) and lo = bf16(s - hi), both rounded
       // to nearest even; s - hi is exact, so hi + lo is within 2^-17 of s.
-      auto prep = [&](int cb, int ch, int nch_, uint32_t(&raw)[4][W], uint32_t(&bh)[2], uint32_t(&bl)[2]) {
+      auto prep = [&](int cb, int ch, int nch_, uint32_t(&raw)[4][W], uint32_t(&bh)[2], uint32_t(&bl)[2],
+                      float& scl) {
         const bool live = ch < nch_;
         const int chc = live ? ch : 0;
         const int32_t r0 = (cb + chc) * kChunk;
@@ -515,22 +537,55 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           pvs[3] = p4.w;
         }
         const float* krow = &s_k[wave][chc * kChunk + kg * 4][0];
+        scl = 1.0f;
+        if constexpr (!kVar) {
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int32_t r = r0 + kg * 4 + kk;
-          const int32_t pv = pvs[kk];
-          const bool in = live && uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pv) <= lim_u;
-          float d2 = 0.0f;
+          for (int kk = 0; kk < 4; ++kk) {
+            const int32_t r = r0 + kg * 4 + kk;
+            const int32_t pv = pvs[kk];
+            const bool in = live && uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pv) <= lim_u;
+            float d2 = 0.0f;
 #pragma unroll
-          for (int a = 0; a < KD; ++a) {
-            if (a < dk) {
-              const float diff = qv[a] - krow[kk * KD4 + a];
-              d2 = fmaf(diff, diff, d2);
+            for (int a = 0; a < KD; ++a) {
+              if (a < dk) {
+                const float diff = qv[a] - krow[kk * KD4 + a];
+                d2 = fmaf(diff, diff, d2);
+              }
             }
+            const float rc = __builtin_amdgcn_rcpf(d2 + eps);
+            sc[kk] = in ? rc : 0.0f;
+            zpart += sc[kk];
           }
-          const float rc = __builtin_amdgcn_rcpf(d2 + eps);
-          sc[kk] = in ? rc : 0.0f;
-          zpart += sc[kk];
+        } else {
+          bool ins[4];
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) {
+            const int32_t r = r0 + kg * 4 + kk;
+            ins[kk] = live && uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
+            sc[kk] = variant_term<KD>(score, qv, krow + kk * KD4, dk, eps, rsd, qnorm);
+          }
+          if (smax) {
+            // Online softmax: the chunk's largest logit of the query (its 4
+            // lanes), the new running maximum, the factor for the sums so far.
+            float cm = -INFINITY;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) cm = ins[kk] ? fmaxf(cm, sc[kk]) : cm;
+            cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
+            cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+            const float nm = fmaxf(run_max, cm);
+            if (nm > run_max) {
+              scl = run_max > -INFINITY ? __expf(run_max - nm) : 0.0f;
+              run_max = nm;
+            }
+            zpart *= scl;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) sc[kk] = ins[kk] ? __expf(sc[kk] - run_max) : 0.0f;
+          } else {
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) sc[kk] = ins[kk] ? sc[kk] : 0.0f;
+          }
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) zpart += sc[kk];
         }
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -555,7 +610,12 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // values twice, against their high and then their low score parts (A
       // and B slots correspond lane by lane, so the sum pairs each value with
       // both parts of its own score).
-      auto mma = [&](const uint32_t(&raw)[4][W], const uint32_t(&bh)[2], const uint32_t(&bl)[2]) {
+      auto mma = [&](const uint32_t(&raw)[4][W], const uint32_t(&bh)[2], const uint32_t(&bl)[2], float scl) {
+        // Softmax variants: the sums so far to the chunk's running maximum.
+        if (smax && wave_ballot(scl != 1.0f) != 0ull) {
+#pragma unroll
+          for (int j = 0; j < E; ++j) acc[j] *= scl;
+        }
         Frag8 b;
         b.w[0] = bh[0];
         b.w[1] = bh[1];
@@ -636,13 +696,14 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 
           // Value rows of chunk ch+1 load while chunk ch is multiplied.
           uint32_t rA[4][W], rB[4][W], hA[2], lA[2], hB[2], lB[2];
-          prep(cb, 0, nch, rA, hA, lA);
+          float sA, sB;
+          prep(cb, 0, nch, rA, hA, lA, sA);
           for (int ch = 0; ch < nch; ch += 2) {
-            prep(cb, ch + 1, nch, rB, hB, lB);
-            mma(rA, hA, lA);
+            prep(cb, ch + 1, nch, rB, hB, lB, sB);
+            mma(rA, hA, lA, sA);
             if (ch + 1 >= nch) break;
-            prep(cb, ch + 2, nch, rA, hA, lA);
-            mma(rB, hB, lB);
+            prep(cb, ch + 2, nch, rA, hA, lA, sA);
+            mma(rB, hB, lB, sB);
           }
           wave_lds_sync();
         }
@@ -680,29 +741,39 @@ template <int DV, int DK>
 hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
                          int topk, bool causal, int chunk, const int32_t* perm, const int32_t* list_pos,
                          const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
-                         float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
+                         int score, float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
   const int64_t tiles = ceil_div(total, kTileQ);
   const int64_t want = ceil_div(tiles, kTileWaves);
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
-#define ZETA_TILE_LAUNCH(OFF, HIST)                                                                                  \
-  hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST>), dim3(blocks), dim3(kTileWaves * 64), 0, stream, \
-                     q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk, causal ? 1 : 0,    \
-                     chunk, lp.t0, lp.t_hi, lp.cap, eps, hm.k, hm.v, out)
-  const bool hist = hm.k != nullptr;
-  if (off32) {
-    if (hist)
-      ZETA_TILE_LAUNCH(true, true);
-    else
-      ZETA_TILE_LAUNCH(true, false);
-  } else {
-    if (hist)
-      ZETA_TILE_LAUNCH(false, true);
-    else
-      ZETA_TILE_LAUNCH(false, false);
+#define ZETA_TILE_LAUNCH(OFF, HIST, VAR)                                                                          \
+  hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST, VAR>), dim3(blocks), dim3(kTileWaves * 64), 0,     \
+                     stream, q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk,           \
+                     causal ? 1 : 0, chunk, lp.t0, lp.t_hi, lp.cap, score, eps, hm.k, hm.v, out)
+#define ZETA_TILE_LAUNCH4(VAR)             \
+  if (off32) {                             \
+    if (hist)                              \
+      ZETA_TILE_LAUNCH(true, true, VAR);   \
+    else                                   \
+      ZETA_TILE_LAUNCH(true, false, VAR);  \
+  } else {                                 \
+    if (hist)                              \
+      ZETA_TILE_LAUNCH(false, true, VAR);  \
+    else                                   \
+      ZETA_TILE_LAUNCH(false, false, VAR); \
   }
+  const bool hist = hm.k != nullptr;
+  // The score variants are compiled for d_k = 3 only.
+  if constexpr (DK == 3) {
+    if (score != kScoreCauchy) {
+      ZETA_TILE_LAUNCH4(true)
+      return hipGetLastError();
+    }
+  }
+  ZETA_TILE_LAUNCH4(false)
+#undef ZETA_TILE_LAUNCH4
 #undef ZETA_TILE_LAUNCH
   return hipGetLastError();
 }
@@ -711,12 +782,12 @@ template <int DV>
 hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N, int dk,
                           int topk, bool causal, int chunk, const int32_t* perm, const int32_t* list_pos,
                           const int32_t* q_order, const int2* bounds, const uint2* keys_full, const uint2* keys_list,
-                          float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
+                          int score, float eps, HistMean hm, uint16_t* out, hipStream_t stream) {
   if (dk == 3)
     return launch_tile_t<DV, 3>(q, k, v, S, N, dk, topk, causal, chunk, perm, list_pos, q_order, bounds, keys_full,
-                                keys_list, eps, hm, out, stream);
+                                keys_list, score, eps, hm, out, stream);
   return launch_tile_t<DV, 0>(q, k, v, S, N, dk, topk, causal, chunk, perm, list_pos, q_order, bounds, keys_full,
-                              keys_list, eps, hm, out, stream);
+                              keys_list, score, eps, hm, out, stream);
 }
 
 }  // namespace
@@ -753,8 +824,9 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
                                      int topk, bool causal, int chunk, const uint32_t* q_codes,
                                      const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
-                                     const int32_t* q_order, float eps, HistMean hm, void* out, int32_t* idx_out,
-                                     int2* bounds, uint2* keys_full, uint2* keys_list, hipStream_t stream) {
+                                     const int32_t* q_order, int score, float eps, HistMean hm, void* out,
+                                     int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
+                                     hipStream_t stream) {
   const hipError_t e = launch_tile_windows(k, S, N, dk, topk, causal, chunk, q_codes, sorted_codes, perm, list_codes,
                                            list_pos, q_order, idx_out, bounds, keys_full, keys_list, stream);
   if (e != hipSuccess) return e;
@@ -765,7 +837,7 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
 #define ZETA_TILE_CASE(DVV) \
   case DVV:                 \
     return launch_tile_dk<DVV>(qq, kk, vv, S, N, dk, topk, causal, chunk, perm, list_pos, q_order, bounds, keys_full, \
-                               keys_list, eps, hm, oo, stream);
+                               keys_list, score, eps, hm, oo, stream);
   switch (dv) {
     ZETA_TILE_CASE(32)
     ZETA_TILE_CASE(64)

@@ -225,3 +225,33 @@ def test_score_modes_long_context():
             ref = oracle.attend(f["q"][s:s + 1], f["k"][s:s + 1], f["v"][s:s + 1], idx[s:s + 1, rows], 0.5, rows=rows,
                                 mode=mode)[0]
             assert np.abs(out[s, rows] - ref).max() <= TOL[w.dtype], (mode, s)
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("history", [False, True])
+def test_score_modes_tiles(mode, history):
+    """The bfloat16 one-pass call with d_k = 3 runs every variant on the
+    matrix-core tiles (online softmax per query for the softmax variants):
+    it matches the oracle, with and without the history-mean candidate, and a
+    query's bits do not depend on the processing order (its running maximum
+    meets its own chunks in list order whatever tile it is in)."""
+    cfg = 2
+    w, x, f = inputs(cfg)
+    log(f"score {mode} tiles history={history}")
+    S = 4
+    raw = {n: a.reshape(w.segments, w.N, -1)[:S] for n, a in x.items()}
+    fs = {n: a[:S] for n, a in f.items()}
+    q, k, v = (to_dev(raw[n][None], w.dtype) for n in ("q", "k", "v"))
+    res = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, fused=True, score=mode, history=history,
+                       return_intermediates=True)
+    pos = zeta.zeta_select_attend_fwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, True, 0.5,
+                                      score=mode, mean_k=res["mean_k"], mean_v=res["mean_v"])
+    torch.cuda.synchronize()
+    assert torch.equal(res["out"].view(torch.int16), pos.view(torch.int16))
+    idx = host(res["idx"]).reshape(S, w.N, w.topk)
+    out = host(res["out"]).reshape(S, w.N, w.dv)
+    mk = mv = None
+    if history:
+        mk, mv = oracle.history_mean(fs["k"], fs["v"], True)
+    ref = oracle.attend(fs["q"], fs["k"], fs["v"], idx, 0.5, mean_k=mk, mean_v=mv, mode=mode)
+    assert np.abs(out - ref).max() <= TOL[w.dtype]
