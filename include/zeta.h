@@ -243,8 +243,10 @@ zeta_status_t zeta_topk_attn_fwd(const void* q, const void* k, const void* v, ze
  * accumulation).  The output agrees with the two calls to float32 rounding,
  * and a query's bits depend only on its own window, so they are the same for
  * every processing order.  The history-mean candidate, when given, is added
- * per query in float32.  The score variants and float32 inputs take the
- * per-query path.
+ * per query in float32.  With d_k = 3 the score variants run on the tiles
+ * too (softmax variants as an online softmax per query: running maximum,
+ * sums rescaled when it grows); float32 inputs, and the variants with other
+ * d_k, take the per-query path.
  *
  *   q, k, v, dtype, B, H, N, d_k, d_v, topk, score, eps, mean_k, mean_v,
  *            out: as for zeta_topk_attn_fwd; causal and chunk as for
