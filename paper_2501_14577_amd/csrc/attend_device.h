@@ -129,10 +129,13 @@ __device__ __forceinline__ float mean_score(const float* __restrict__ mk, int64_
 // mode 0, is computed inline by the kernels).  Returns the weight itself
 // (inverse Euclidean: 1 / (|q - k| + eps)) or the logit of a softmax
 // (q.k / sqrt(d), -|q - k|^2 / sqrt(d), (q/|q|).(k/|k|) / sqrt(d); a zero
-// vector gives 0).  rsd = 1 / sqrt(d); qn = |q|.
+// vector gives 0).  rsd = 1 / sqrt(d); qn = |q|.  The result is rounded as
+// written (no multiply fused into the caller's next add), so every inlined
+// copy of a kernel's scoring gives the same bits.
 template <int KD>
 __device__ __forceinline__ float variant_term(int mode, const float* qv, const float* kv, int dk, float eps, float rsd,
                                               float qn) {
+#pragma clang fp contract(off)
   float d2 = 0.0f, dot = 0.0f, kk = 0.0f;
 #pragma unroll
   for (int a = 0; a < KD; ++a) {

@@ -11,7 +11,7 @@ namespace zeta {
 // Attention scores: the method's Cauchy score and the variants compared with
 // it (the values match zeta_score_t).
 enum ScoreMode : int { kScoreCauchy = 0, kScoreDot = 1, kScoreNegEuclid = 2, kScoreInvEuclid = 3, kScoreNormDot = 4 };
-__host__ __device__ inline bool score_is_softmax(int mode) {
+__host__ __device__ constexpr bool score_is_softmax(int mode) {
   return mode == kScoreDot || mode == kScoreNegEuclid || mode == kScoreNormDot;
 }
 

@@ -362,14 +362,15 @@ __global__ void __launch_bounds__(256)
 
 // ---- attention over the windows ----------------------------------------------
 
-template <int DV, int DK, bool kOff32, bool kHist, bool kVar>
+template <int DV, int DK, bool kOff32, bool kHist, int kMode>
 __global__ void __launch_bounds__(kTileWaves * 64)
+    __attribute__((amdgpu_waves_per_eu((DV <= 128 && kMode != kScoreCauchy) ? 3 : 1)))
     select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                               const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
                               const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
                               const int2* __restrict__ bounds, const uint2* __restrict__ keys_full,
                               const uint2* __restrict__ keys_list, int64_t total, int64_t N, int dk_rt, int causal,
-                              int chunk, int t0, int t_hi, int64_t cap, int score_rt, float eps,
+                              int chunk, int t0, int t_hi, int64_t cap, float eps,
                               const float* __restrict__ mk, const float* __restrict__ mv, uint16_t* __restrict__ out) {
   constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
   constexpr int W = E / 2;    // 32-bit words per lane and row
@@ -379,11 +380,13 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   static_assert(E >= 2 && E % 2 == 0, "d_v must be a multiple of 32");
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
-  // Score: the Cauchy score, or with kVar a variant (softmax variants run
-  // an online softmax per query: a running maximum shared by the query's 4
-  // lanes, the accumulators and the normaliser rescaled when it grows).
-  const int score = kVar ? score_rt : kScoreCauchy;
-  const bool smax = kVar && score_is_softmax(score);
+  // Score (compile time): the Cauchy score, or a variant (softmax variants
+  // run an online softmax per query: a running maximum shared by the
+  // query's 4 lanes, the accumulators and the normaliser rescaled when it
+  // grows).
+  constexpr bool kVar = kMode != kScoreCauchy;
+  constexpr int score = kMode;
+  constexpr bool smax = kVar && score_is_softmax(kMode);
   const float rsd = 1.0f / sqrtf(float(dk));
 
   // Key rows padded to a multiple of 4 floats, so 4 consecutive entries'
@@ -557,6 +560,9 @@ __global__ void __launch_bounds__(kTileWaves * 64)
             zpart += sc[kk];
           }
         } else {
+          // Rounded as written: this lambda is inlined at several call sites,
+          // and a chunk's site depends on where its run starts.
+#pragma clang fp contract(off)
           bool ins[4];
 #pragma unroll
           for (int kk = 0; kk < 4; ++kk) {
@@ -748,31 +754,43 @@ hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v
   const int64_t want = ceil_div(tiles, kTileWaves);
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
-#define ZETA_TILE_LAUNCH(OFF, HIST, VAR)                                                                          \
-  hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST, VAR>), dim3(blocks), dim3(kTileWaves * 64), 0,     \
+#define ZETA_TILE_LAUNCH(OFF, HIST, MODE)                                                                         \
+  hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST, MODE>), dim3(blocks), dim3(kTileWaves * 64), 0,    \
                      stream, q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk,           \
-                     causal ? 1 : 0, chunk, lp.t0, lp.t_hi, lp.cap, score, eps, hm.k, hm.v, out)
-#define ZETA_TILE_LAUNCH4(VAR)             \
-  if (off32) {                             \
-    if (hist)                              \
-      ZETA_TILE_LAUNCH(true, true, VAR);   \
-    else                                   \
-      ZETA_TILE_LAUNCH(true, false, VAR);  \
-  } else {                                 \
-    if (hist)                              \
-      ZETA_TILE_LAUNCH(false, true, VAR);  \
-    else                                   \
-      ZETA_TILE_LAUNCH(false, false, VAR); \
+                     causal ? 1 : 0, chunk, lp.t0, lp.t_hi, lp.cap, eps, hm.k, hm.v, out)
+#define ZETA_TILE_LAUNCH4(MODE)             \
+  if (off32) {                              \
+    if (hist)                               \
+      ZETA_TILE_LAUNCH(true, true, MODE);   \
+    else                                    \
+      ZETA_TILE_LAUNCH(true, false, MODE);  \
+  } else {                                  \
+    if (hist)                               \
+      ZETA_TILE_LAUNCH(false, true, MODE);  \
+    else                                    \
+      ZETA_TILE_LAUNCH(false, false, MODE); \
   }
   const bool hist = hm.k != nullptr;
   // The score variants are compiled for d_k = 3 only.
   if constexpr (DK == 3) {
-    if (score != kScoreCauchy) {
-      ZETA_TILE_LAUNCH4(true)
-      return hipGetLastError();
+    switch (score) {
+      case kScoreDot:
+        ZETA_TILE_LAUNCH4(kScoreDot)
+        return hipGetLastError();
+      case kScoreNegEuclid:
+        ZETA_TILE_LAUNCH4(kScoreNegEuclid)
+        return hipGetLastError();
+      case kScoreInvEuclid:
+        ZETA_TILE_LAUNCH4(kScoreInvEuclid)
+        return hipGetLastError();
+      case kScoreNormDot:
+        ZETA_TILE_LAUNCH4(kScoreNormDot)
+        return hipGetLastError();
+      default:
+        break;
     }
   }
-  ZETA_TILE_LAUNCH4(false)
+  ZETA_TILE_LAUNCH4(kScoreCauchy)
 #undef ZETA_TILE_LAUNCH4
 #undef ZETA_TILE_LAUNCH
   return hipGetLastError();
