@@ -539,6 +539,16 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           pvs[2] = p4.z;
           pvs[3] = p4.w;
         }
+        // The entries' value rows first (a wave-uniform base and a 32-bit byte
+        // offset per lane when the segment's values span under 4 GiB, so no
+        // 64-bit address arithmetic), kept ahead of the scoring and of the
+        // previous chunk's products so that they load while those run.
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const Off boff = (Off(pvs[kk]) * Off(DV) + col) * Off(2);
+          load_words<W>(reinterpret_cast<const uint16_t*>(vbytes + boff), raw[kk]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
         const float* krow = &s_k[wave][chc * kChunk + kg * 4][0];
         scl = 1.0f;
         if constexpr (!kVar) {
@@ -601,14 +611,6 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                               (__bf16)(sc[2 * t + 1] - __uint_as_float(hw & 0xFFFF0000u))};
           bh[t] = hw;
           bl[t] = __builtin_bit_cast(uint32_t, l);
-        }
-        // A wave-uniform base and a 32-bit byte offset per lane (when the
-        // segment's values span under 4 GiB), so the loads need no 64-bit
-        // address arithmetic.
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const Off boff = (Off(pvs[kk]) * Off(DV) + col) * Off(2);
-          load_words<W>(reinterpret_cast<const uint16_t*>(vbytes + boff), raw[kk]);
         }
       };
       // acc[j] += V^T (block j) * S^T for one chunk, high and low score parts
