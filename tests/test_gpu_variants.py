@@ -255,3 +255,30 @@ def test_score_modes_tiles(mode, history):
         mk, mv = oracle.history_mean(fs["k"], fs["v"], True)
     ref = oracle.attend(fs["q"], fs["k"], fs["v"], idx, 0.5, mean_k=mk, mean_v=mv, mode=mode)
     assert np.abs(out - ref).max() <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("dv", [32, 256])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("mode", MODES)
+def test_score_modes_tiles_widths(mode, causal, dv):
+    """Every variant's tile kernel at the narrowest and widest value rows
+    (one product block pair per lane at d_v = 32, sixteen at 256), both
+    modes, on a ragged length: the oracle's outputs, and the same bits in
+    position order as in level order."""
+    w = workloads.custom(B=1, H=2, N=700, dv=dv, topk=40, dtype="bf16", bits=8, seed=dv + len(mode))
+    log(f"score {mode} tiles dv={dv} causal={causal}")
+    x = workloads.generate(w)
+    S = w.segments
+    f = {n: oracle.as_f32(a, w.dtype).reshape(S, w.N, -1) for n, a in x.items()}
+    q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
+    res = zeta.forward(q, k, v, w.topk, 0.5, causal, w.bits, fused=True, score=mode, return_intermediates=True)
+    pos = zeta.zeta_select_attend_fwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, causal, 0.5,
+                                      score=mode)
+    torch.cuda.synchronize()
+    assert torch.equal(res["out"].view(torch.int16), pos.view(torch.int16))
+    idx = host(res["idx"]).reshape(S, w.N, w.topk)
+    qc, kc, _, _ = oracle.morton_encode(f["q"], f["k"], w.bits)
+    assert np.array_equal(idx, oracle.select_topk(qc, kc, w.topk, causal))
+    ref = oracle.attend(f["q"], f["k"], f["v"], idx, 0.5, mode=mode)
+    out = host(res["out"]).reshape(S, w.N, w.dv)
+    assert np.abs(out - ref).max() <= TOL[w.dtype], (mode, causal, dv)
