@@ -274,3 +274,30 @@ def test_history_bwd_processing_order_and_repeat():
              q_order=np.stack([rng.permutation(w.N) for _ in range(S)]).astype(np.int32))
     for t in range(4):
         assert np.array_equal(a[t], b[t]), t
+
+
+@pytest.mark.parametrize("dv", [32, 128, 256])
+@pytest.mark.parametrize("causal", [True, False])
+def test_history_tile_widths(dv, causal):
+    """The bfloat16 one-pass call with the candidate at every other value
+    width of the matrix-core tiles (the configurations use d_v = 64), on a
+    ragged length: the oracle's attention with its own means, and the same
+    bits in position order as in level order."""
+    w = workloads.custom(B=1, H=2, N=650, dv=dv, topk=24, dtype="bf16", bits=8, seed=dv + 3)
+    log(f"history tiles dv={dv} causal={causal}")
+    x = workloads.generate(w)
+    S = w.segments
+    f = {n: oracle.as_f32(a, w.dtype).reshape(S, w.N, -1) for n, a in x.items()}
+    q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
+    res = zeta.forward(q, k, v, w.topk, 0.5, causal, w.bits, fused=True, history=True, return_intermediates=True)
+    pos = zeta.zeta_select_attend_fwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, causal, 0.5,
+                                      mean_k=res["mean_k"], mean_v=res["mean_v"])
+    torch.cuda.synchronize()
+    assert torch.equal(res["out"].view(torch.int16), pos.view(torch.int16))
+    idx = host(res["idx"]).reshape(S, w.N, w.topk)
+    qc, kc, _, _ = oracle.morton_encode(f["q"], f["k"], w.bits)
+    assert np.array_equal(idx, oracle.select_topk(qc, kc, w.topk, causal))
+    mk, mv = oracle.history_mean(f["k"], f["v"], causal)
+    ref = oracle.attend(f["q"], f["k"], f["v"], idx, 0.5, mean_k=mk, mean_v=mv)
+    out = host(res["out"]).reshape(S, w.N, w.dv)
+    assert np.abs(out - ref).max() <= TOL[w.dtype], (causal, dv)

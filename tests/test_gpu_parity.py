@@ -301,6 +301,7 @@ EDGE = [
     dict(N=300, topk=16, dk=3, dv=32, dtype="bf16", bits=10),
     dict(N=1000, topk=100, dk=5, dv=256, dtype="bf16", bits=5),
     dict(N=700, topk=1024, dk=3, dv=128, dtype="bf16", bits=10),
+    dict(N=900, topk=48, dk=3, dv=256, dtype="bf16", bits=7),
 ]
 
 
