@@ -193,3 +193,30 @@ def test_tile_bwd_history(cfg, causal, nseg):
     _close(dk.reshape(rk.shape), rk, "dk")
     _close(dv.reshape(rv.shape), rv, "dv")
     assert abs(float(deps[0]) - reps) <= 1e-4 * (1.0 + abs(reps)), (float(deps[0]), reps)
+
+
+@pytest.mark.parametrize("dv", [32, 128, 256])
+@pytest.mark.parametrize("causal", [True, False])
+def test_tile_bwd_history_widths(dv, causal):
+    """The one-pass gradients with the history-mean candidate at the value
+    widths the configurations do not use, on a ragged length, both modes."""
+    w = workloads.custom(B=1, H=2, N=650, dv=dv, topk=24, dtype="bf16", bits=8, seed=dv + 11)
+    log(f"tile bwd history dv={dv} causal={causal}")
+    x = workloads.generate(w)
+    S = w.segments
+    raw = {n: a.reshape(S, w.N, -1) for n, a in x.items()}
+    f = {n: oracle.as_f32(a, w.dtype) for n, a in raw.items()}
+    dout_raw = workloads.generate_dout(w).reshape(S, w.N, w.dv)
+    q, k, v, dout = (to_dev(a[None], w.dtype) for a in (raw["q"], raw["k"], raw["v"], dout_raw))
+    res = zeta.forward(q, k, v, w.topk, 0.5, causal, w.bits, fused=True, history=True, return_intermediates=True)
+    grads = zeta.zeta_select_attend_bwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, causal,
+                                        0.5, dout, q_order=res["q_order"], mean_k=res["mean_k"], mean_v=res["mean_v"])
+    torch.cuda.synchronize()
+    idx = host(res["idx"]).reshape(S, w.N, w.topk)
+    dq, dk, dv_, deps = (host(t) for t in grads)
+    rq, rk, rv, reps = oracle.attend_bwd(f["q"], f["k"], f["v"], idx, 0.5, oracle.as_f32(dout_raw, w.dtype),
+                                         history=True, causal=causal)
+    _close(dq.reshape(rq.shape), rq, "dq")
+    _close(dk.reshape(rk.shape), rk, "dk")
+    _close(dv_.reshape(rv.shape), rv, "dv")
+    assert abs(float(deps[0]) - reps) <= 1e-4 * (1.0 + abs(reps)), (float(deps[0]), reps)
