@@ -282,3 +282,35 @@ def test_score_modes_tiles_widths(mode, causal, dv):
     ref = oracle.attend(f["q"], f["k"], f["v"], idx, 0.5, mode=mode)
     out = host(res["out"]).reshape(S, w.N, w.dv)
     assert np.abs(out - ref).max() <= TOL[w.dtype], (mode, causal, dv)
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_score_modes_tiles_chunked(mode):
+    """Score variants on the tiles under the chunked causal rule (the first
+    chunk's queries have empty pools and give zero rows), with and without
+    the history-mean candidate: the oracle's outputs, and the same bits in
+    position order as in level order."""
+    w = workloads.custom(B=1, H=2, N=1000, dv=64, topk=32, dtype="bf16", bits=8, seed=41 + len(mode))
+    M = 125
+    x = workloads.generate(w)
+    S = w.segments
+    f = {n: oracle.as_f32(a, w.dtype).reshape(S, w.N, -1) for n, a in x.items()}
+    q, k, v = (to_dev(x[n], w.dtype) for n in ("q", "k", "v"))
+    qc, kc, _, _ = oracle.morton_encode(f["q"], f["k"], w.bits)
+    want = oracle.select_topk(qc, kc, w.topk, True, chunk=M)
+    for history in (False, True):
+        log(f"score {mode} tiles chunk={M} history={history}")
+        res = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, fused=True, score=mode, chunk=M, history=history,
+                           return_intermediates=True)
+        pos = zeta.zeta_select_attend_fwd(q, k, v, res["q_codes"], res["sorted_codes"], res["perm"], w.topk, True,
+                                          0.5, score=mode, chunk=M, mean_k=res["mean_k"], mean_v=res["mean_v"])
+        torch.cuda.synchronize()
+        assert torch.equal(res["out"].view(torch.int16), pos.view(torch.int16))
+        idx = host(res["idx"]).reshape(S, w.N, w.topk)
+        assert np.array_equal(idx, want)
+        mk = mv = None
+        if history:
+            mk, mv = oracle.history_mean(f["k"], f["v"], True)
+        ref = oracle.attend(f["q"], f["k"], f["v"], idx, 0.5, mean_k=mk, mean_v=mv, mode=mode)
+        out = host(res["out"]).reshape(S, w.N, w.dv)
+        assert np.abs(out - ref).max() <= TOL[w.dtype], (mode, history)
