@@ -96,6 +96,31 @@ struct Row3<uint16_t> {
   }
 };
 
+// Row `row` of a bfloat16 [rows][3] array as three bfloat16 bit patterns in
+// 8 bytes (x | y << 16, z), read the way Row3 reads it.
+__device__ __forceinline__ uint2 packed_key_row(const uint16_t* base, int64_t row, int64_t rows) {
+  const int64_t e = row * 3;
+  const int64_t a = e & ~int64_t(1);
+  uint32_t x, y, z;
+  if (a + 4 <= rows * 3) {
+    const Words2 w = *reinterpret_cast<const Words2*>(base + a);
+    if (e == a) {
+      x = w.a & 0xFFFFu;
+      y = w.a >> 16;
+      z = w.b & 0xFFFFu;
+    } else {
+      x = w.a >> 16;
+      y = w.b & 0xFFFFu;
+      z = w.b >> 16;
+    }
+  } else {
+    x = base[e];
+    y = base[e + 1];
+    z = base[e + 2];
+  }
+  return make_uint2(x | (y << 16), z);
+}
+
 // Byte offset of a value row inside its segment: 32-bit when the segment's
 // values span less than 4 GiB, else 64-bit.
 template <bool kOff32>

@@ -296,19 +296,24 @@ hipError_t launch_select_attend(const void* q, const void* k, const void* v, boo
                                 hipStream_t stream) {
   const uint32_t* list_codes = nullptr;
   const int32_t* list_pos = nullptr;
+  const bool tile = is_bf16 && tile_supports(dv) && (score == kScoreCauchy || dk == 3);
+  const FusedWs fw = fused_ws(S, N, topk, causal ? 1 : 0);
+  char* wsb = static_cast<char*>(workspace);
+  uint2* keys_full = reinterpret_cast<uint2*>(wsb + fw.keys_full_off);
+  uint2* keys_list = reinterpret_cast<uint2*>(wsb + fw.keys_list_off);
+  // The tiles' key rows in list order come with the prefix lists (d_k = 3).
+  const bool rows_with_lists = tile && dk == 3;
   if (causal) {
-    const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
+    const hipError_t e =
+        launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos,
+                            rows_with_lists ? static_cast<const uint16_t*>(k) : nullptr, keys_full, keys_list);
     if (e != hipSuccess) return e;
   }
-  if (is_bf16 && tile_supports(dv) && (score == kScoreCauchy || dk == 3)) {
-    const FusedWs fw = fused_ws(S, N, topk, causal ? 1 : 0);
-    char* wsb = static_cast<char*>(workspace);
+  if (tile) {
     int2* bounds = reinterpret_cast<int2*>(wsb + fw.bounds_off);
-    uint2* keys_full = reinterpret_cast<uint2*>(wsb + fw.keys_full_off);
-    uint2* keys_list = reinterpret_cast<uint2*>(wsb + fw.keys_list_off);
     return launch_select_attend_tile(q, k, v, S, N, dk, dv, topk, causal, chunk, q_codes, sorted_codes, perm,
                                      list_codes, list_pos, q_order, score, eps, hm, out, idx_out, bounds, keys_full,
-                                     keys_list, stream);
+                                     keys_list, rows_with_lists && list_codes != nullptr, stream);
   }
 #define ZETA_FUSED_CASE(DVV)                                                                                       \
   case DVV:                                                                                                        \

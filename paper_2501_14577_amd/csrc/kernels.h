@@ -64,10 +64,13 @@ hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, 
                          void* workspace, hipStream_t stream);
 
 // Doubling prefix lists of causal selection in the workspace (none when
-// every query searches the full list: *list_codes stays NULL).
+// every query searches the full list: *list_codes stays NULL).  With k_rows
+// (bfloat16 keys, d_k = 3) the same pass writes the key rows of the full
+// sorted lists and of the prefix lists in list order, as the tiles read them.
 hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm, int64_t S, int64_t N, int topk,
                                void* workspace, hipStream_t stream, const uint32_t** list_codes,
-                               const int32_t** list_pos);
+                               const int32_t** list_pos, const uint16_t* k_rows = nullptr,
+                               uint2* keys_full = nullptr, uint2* keys_list = nullptr);
 
 // bfloat16 one-pass select and attend on the matrix cores, 16 queries per
 // wavefront (the prefix lists already built when causal): window bounds per
@@ -81,14 +84,14 @@ hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int 
                                const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
                                const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order,
                                int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
-                               hipStream_t stream);
+                               bool keys_built, hipStream_t stream);
 hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dk, int dv,
                                      int topk, bool causal, int chunk, const uint32_t* q_codes,
                                      const uint32_t* sorted_codes,
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
                                      const int32_t* q_order, int score, float eps, HistMean hm, void* out,
                                      int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
-                                     hipStream_t stream);
+                                     bool keys_built, hipStream_t stream);
 
 // Gradients of the bfloat16 one-pass attention (d_k = 3, Cauchy score) over
 // its windows, with the optional history-mean candidate: prefix lists, window

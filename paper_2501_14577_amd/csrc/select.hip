@@ -34,6 +34,7 @@
 // the previous insertion point; attend's tiles share value rows the same way.
 #include <stdint.h>
 
+#include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"
 #include "layout.h"
@@ -70,7 +71,8 @@ __global__ void __launch_bounds__(kSortThreads)
     list_scatter_kernel(const uint32_t* __restrict__ sorted_codes, const int32_t* __restrict__ perm,
                         int64_t N, int64_t tiles, int t0, int levels, int64_t cap,
                         const uint32_t* __restrict__ cnt, uint32_t* __restrict__ list_codes,
-                        int32_t* __restrict__ list_pos) {
+                        int32_t* __restrict__ list_pos, const uint16_t* __restrict__ k_rows,
+                        uint2* __restrict__ keys_full, uint2* __restrict__ keys_list) {
   const int64_t seg = blockIdx.x / tiles;
   const int64_t tile = blockIdx.x % tiles;
   const int tid = threadIdx.x;
@@ -95,12 +97,18 @@ __global__ void __launch_bounds__(kSortThreads)
   const int64_t first = tile * kSortTile + int64_t(wave) * (kSortChunks * 64);
   uint32_t code[kSortChunks];
   int32_t pos[kSortChunks];
+  uint2 krow[kSortChunks];  // with k_rows: the entry's key row, written to every list it joins
 #pragma unroll
   for (int c = 0; c < kSortChunks; ++c) {
     const int64_t e = first + c * 64 + lane;
     const bool valid = e < N;
     code[c] = valid ? sorted_codes[seg_off + e] : 0u;
     pos[c] = valid ? perm[seg_off + e] : 0x7FFFFFFF;  // never below any 2^t
+    krow[c] = make_uint2(0u, 0u);
+    if (k_rows != nullptr && valid) {
+      krow[c] = packed_key_row(k_rows, seg_off + pos[c], int64_t(gridDim.x / tiles) * N);
+      keys_full[seg_off + e] = krow[c];
+    }
   }
   for (int l = 0; l < levels; ++l) {
     const int32_t lim = int32_t(1) << (t0 + l);
@@ -137,6 +145,7 @@ __global__ void __launch_bounds__(kSortThreads)
         const int64_t dst = list_off + run + lanes_below(bal);
         lc[dst] = code[c];
         lp[dst] = pos[c];
+        if (k_rows != nullptr) keys_list[seg * cap + dst] = krow[c];
       }
       run += uint32_t(__popcll(bal));
     }
@@ -251,7 +260,8 @@ hipError_t launch_query_order(const int32_t* q_order, int64_t S, int64_t N, int 
 
 hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm, int64_t S, int64_t N, int topk,
                                void* workspace, hipStream_t stream, const uint32_t** list_codes,
-                               const int32_t** list_pos) {
+                               const int32_t** list_pos, const uint16_t* k_rows, uint2* keys_full,
+                               uint2* keys_list) {
   const ListPlan lp = list_plan(N, topk);
   *list_codes = nullptr;
   *list_pos = nullptr;
@@ -265,7 +275,7 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
   const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
   hipLaunchKernelGGL(list_count_kernel, grid, block, 0, stream, perm, N, tiles, lp.t0, lp.levels, cnt);
   hipLaunchKernelGGL(list_scatter_kernel, grid, block, 0, stream, sorted_codes, perm, N, tiles, lp.t0, lp.levels,
-                     lp.cap, cnt, lc, lpos);
+                     lp.cap, cnt, lc, lpos, k_rows, keys_full, keys_list);
   *list_codes = lc;
   *list_pos = lpos;
   return hipGetLastError();

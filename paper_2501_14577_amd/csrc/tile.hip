@@ -338,26 +338,7 @@ __global__ void __launch_bounds__(256)
   } else {
     return;
   }
-  const int64_t e3 = (seg * N + pv) * 3;
-  const int64_t al = e3 & ~int64_t(1);
-  uint32_t x, y, z;
-  if (al + 4 <= total * 3) {
-    const Words2 w = *reinterpret_cast<const Words2*>(k + al);
-    if (e3 == al) {
-      x = w.a & 0xFFFFu;
-      y = w.a >> 16;
-      z = w.b & 0xFFFFu;
-    } else {
-      x = w.a >> 16;
-      y = w.b & 0xFFFFu;
-      z = w.b >> 16;
-    }
-  } else {
-    x = k[e3];
-    y = k[e3 + 1];
-    z = k[e3 + 2];
-  }
-  *dst = make_uint2(x | (y << 16), z);
+  *dst = packed_key_row(k, seg * N + pv, total);
 }
 
 // ---- attention over the windows ----------------------------------------------
@@ -817,11 +798,11 @@ bool tile_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 2
 hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int topk, bool causal, int chunk,
                                const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
                                const uint32_t* list_codes, const int32_t* list_pos, const int32_t* q_order,
-                               int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
+                               int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list, bool keys_built,
                                hipStream_t stream) {
   const ListPlan lp = list_plan(N, topk);
   const int64_t total = S * N;
-  if (dk == 3) {
+  if (dk == 3 && !keys_built) {
     // Prefix lists exist only for causal calls with levels.
     const bool have_lists = causal && lp.levels > 0 && list_pos != nullptr;
     const int64_t cap = have_lists ? lp.cap : 0;
@@ -846,9 +827,10 @@ hipError_t launch_select_attend_tile(const void* q, const void* k, const void* v
                                      const int32_t* perm, const uint32_t* list_codes, const int32_t* list_pos,
                                      const int32_t* q_order, int score, float eps, HistMean hm, void* out,
                                      int32_t* idx_out, int2* bounds, uint2* keys_full, uint2* keys_list,
-                                     hipStream_t stream) {
+                                     bool keys_built, hipStream_t stream) {
   const hipError_t e = launch_tile_windows(k, S, N, dk, topk, causal, chunk, q_codes, sorted_codes, perm, list_codes,
-                                           list_pos, q_order, idx_out, bounds, keys_full, keys_list, stream);
+                                           list_pos, q_order, idx_out, bounds, keys_full, keys_list, keys_built,
+                                           stream);
   if (e != hipSuccess) return e;
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);

@@ -872,17 +872,20 @@ hipError_t launch_select_attend_bwd(const void* q, const void* k, const void* v,
                                     float* dv, float* deps, void* workspace, hipStream_t stream) {
   const uint32_t* list_codes = nullptr;
   const int32_t* list_pos = nullptr;
-  if (causal) {
-    const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
-    if (e != hipSuccess) return e;
-  }
   const TileBwdWs ws = tile_bwd_ws(S, N, dv_, topk, causal ? 1 : 0, hm.k != nullptr);
   char* wsb = static_cast<char*>(workspace);
   int2* bounds = reinterpret_cast<int2*>(wsb + ws.fused.bounds_off);
   uint2* keys_full = reinterpret_cast<uint2*>(wsb + ws.fused.keys_full_off);
   uint2* keys_list = reinterpret_cast<uint2*>(wsb + ws.fused.keys_list_off);
+  if (causal) {
+    // The key rows in list order come with the prefix lists.
+    const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes,
+                                             &list_pos, static_cast<const uint16_t*>(k), keys_full, keys_list);
+    if (e != hipSuccess) return e;
+  }
   hipError_t e = launch_tile_windows(k, S, N, dk_, topk, causal, chunk, q_codes, sorted_codes, perm, list_codes,
-                                     list_pos, q_order, nullptr, bounds, keys_full, keys_list, stream);
+                                     list_pos, q_order, nullptr, bounds, keys_full, keys_list, list_codes != nullptr,
+                                     stream);
   if (e != hipSuccess) return e;
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* vv = static_cast<const uint16_t*>(v);
