@@ -296,7 +296,7 @@ hipError_t launch_select_attend(const void* q, const void* k, const void* v, boo
                                 hipStream_t stream) {
   const uint32_t* list_codes = nullptr;
   const int32_t* list_pos = nullptr;
-  const bool tile = is_bf16 && tile_supports(dv) && (score == kScoreCauchy || dk == 3);
+  const bool tile = tile_path(is_bf16, dv, score == kScoreCauchy, dk);
   const FusedWs fw = fused_ws(S, N, topk, causal ? 1 : 0);
   char* wsb = static_cast<char*>(workspace);
   uint2* keys_full = reinterpret_cast<uint2*>(wsb + fw.keys_full_off);

@@ -133,6 +133,17 @@ inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
   return w;
 }
 
+// Value widths compiled for the matrix-core tiles.
+inline bool tile_dv(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 256; }
+
+// Whether the one-pass call runs on the matrix-core tiles (and so needs the
+// fused_ws layout, 16-byte aligned): bfloat16 inputs, a compiled d_v, and the
+// Cauchy score, or any score when d_k = 3.  Validation and the launcher both
+// decide with this one test.
+inline bool tile_path(bool is_bf16, int dv, bool cauchy, int dk) {
+  return is_bf16 && tile_dv(dv) && (cauchy || dk == 3);
+}
+
 // One-pass select and attend on the matrix cores: the prefix lists (as for
 // select), then each processing-order slot's window bounds (two int32).
 // For d_k = 3 it also keeps the key rows of the full sorted lists and of the

@@ -793,7 +793,7 @@ hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* 
 
 }  // namespace
 
-bool tile_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 256; }
+bool tile_supports(int dv) { return tile_dv(dv); }
 
 hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int topk, bool causal, int chunk,
                                const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,

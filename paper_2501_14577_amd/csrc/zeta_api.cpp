@@ -182,8 +182,8 @@ zeta_status_t zeta_select_attend_fwd(const void* q, const void* k, const void* v
   if (d_k > zeta::kMaxDk || topk > zeta::kMaxTopk || !zeta::attend_supports(d_v)) return ZETA_ERR_UNSUPPORTED;
   if (!score_known(score)) return ZETA_ERR_UNSUPPORTED;
   const int64_t S = B * H;
-  if (dtype == ZETA_BF16 && zeta::tile_supports(d_v) && score == ZETA_SCORE_CAUCHY) {
-    // Lists and per-slot window bounds.
+  if (zeta::tile_path(dtype == ZETA_BF16, d_v, score == ZETA_SCORE_CAUCHY, d_k)) {
+    // Lists, per-slot window bounds and (d_k = 3) key rows in list order.
     const zeta::FusedWs ws = zeta::fused_ws(S, N, topk, causal);
     if (workspace == nullptr || workspace_bytes < ws.bytes) return ZETA_ERR_WORKSPACE;
     if (!aligned16(workspace)) return ZETA_ERR_INVALID_ARG;

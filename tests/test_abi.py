@@ -279,6 +279,12 @@ FUSED_CASES = [
     (dict(mean_v=ctypes.c_void_p(0xC0000)), INV),
     (dict(mean_k=ctypes.c_void_p(0xB0000), mean_v=ctypes.c_void_p(0xC0008)), INV),
     (dict(chunk=-2), INV), (dict(causal=0, chunk=16), INV), (dict(score=7), UNS),
+    # A score variant with d_k = 3 runs on the matrix-core tiles too, so it
+    # needs the one-pass layout: none at all (non-causal needs no lists),
+    # 2304 bytes (the select-only layout of this shape: 2 segments x 120 list
+    # entries, under the one-pass layout's 7936), or a misaligned buffer.
+    (dict(score=1, causal=0, ws=NULL), WSP), (dict(score=1, ws_bytes=2304), WSP),
+    (dict(score=2, ws=ctypes.c_void_p(0x80008)), INV),
 ]
 
 
