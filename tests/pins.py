@@ -26,6 +26,38 @@ def _rows(name):
 
 
 # ----------------------------------------------------------------------------
+# Input conversion: bfloat16 inputs read as the float32 values of their bits
+# ----------------------------------------------------------------------------
+
+def check_bf16_input(orc):
+    """Fixed bfloat16 bit patterns give their hand-worked values
+    (``tests/golden/bf16_values.txt``: normals, subnormals, the largest
+    finite value, signed zeros, infinities), through ``bf16_bits_to_f32``
+    and through ``as_f32(..., "bf16")`` on a multi-dimensional array; and
+    float32 values exact in bfloat16 survive the round trip through the
+    workload generator's rounding."""
+    import workloads
+
+    rows = list(_rows("bf16_values.txt"))
+    bits = np.array([int(b, 16) for b, _ in rows], dtype=np.uint16)
+    want = np.array([float(v) if "inf" in v else float.fromhex(v) for _, v in rows], dtype=np.float64)
+    for got in (orc.bf16_bits_to_f32(bits), orc.as_f32(bits.reshape(2, -1), "bf16").reshape(-1)):
+        assert got.dtype == np.float32
+        assert np.array_equal(got.astype(np.float64), want), (got, want)
+        assert np.array_equal(np.signbit(got), np.signbit(want))
+    # Every finite bfloat16 value, rebuilt from its fields, round-trips.
+    rng = np.random.default_rng(5)
+    sign = rng.integers(0, 2, 4000)
+    expo = rng.integers(1, 255, 4000)
+    frac = rng.integers(0, 128, 4000)
+    vals = np.where(sign == 1, -1.0, 1.0) * np.ldexp(1.0 + frac / 128.0, expo - 127)
+    vals = vals.astype(np.float32)
+    b = workloads.f32_to_bf16_bits(vals)
+    assert np.array_equal(b.astype(np.int64), (sign << 15) | (expo << 7) | frac)
+    assert np.array_equal(orc.as_f32(b, "bf16"), vals)
+
+
+# ----------------------------------------------------------------------------
 # Encode: equation Z and the discretisation (Section 3.1)
 # ----------------------------------------------------------------------------
 
@@ -729,6 +761,7 @@ def check_history_bwd_invariants(orc):
 
 
 ALL_PINS = [
+    check_bf16_input,
     check_morton_golden,
     check_morton_bijection,
     check_morton_axis_order,

@@ -14,6 +14,11 @@ import oracle.zeta_oracle as orc
 import pins
 
 MUTATIONS = {
+    "bf16: wrong shift": ("<< np.uint32(16)).view(np.float32)", "<< np.uint32(15)).view(np.float32)"),
+    "bf16: bits in the low half": ("astype(np.uint32) << np.uint32(16)).view(np.float32)",
+                                   "astype(np.uint32) << np.uint32(0)).view(np.float32)"),
+    "bf16: read as float16": ('    if dtype == "bf16":\n        return bf16_bits_to_f32(x)\n',
+                              '    if dtype == "bf16":\n        return np.asarray(x, dtype=np.uint16).view(np.float16).astype(np.float32)\n'),
     "axis order reversed": ("d * s + (d - 1 - a)", "d * s + a"),
     "least significant bit first": ("d * s + (d - 1 - a)", "d * (bits - 1 - s) + (d - 1 - a)"),
     "grid of 2^b cells scale": ("top = np.float32((1 << bits) - 1)", "top = np.float32(1 << bits)"),
