@@ -13,7 +13,7 @@ from .zeta import (  # noqa: F401
     library_path,
     load_library,
     bwd_workspace_for,
-    locality_overlap,
+    locality_counts,
     workspace_for,
     zeta_exact_knn,
     zeta_history_mean,

@@ -435,19 +435,20 @@ def zeta_index_overlap(idx_a: torch.Tensor, idx_b: torch.Tensor, N: int, *,
     return counts
 
 
-def locality_overlap(q: torch.Tensor, k: torch.Tensor, bits: int, kn: int = 64, causal: bool = False) -> float:
-    """Section 4.4's locality measure: the mean share of each query's kn
-    exact nearest keys that its Z-order window of kn keys holds (encode,
-    sort, select, exact search and overlap count, all on the GPU)."""
+def locality_counts(q: torch.Tensor, k: torch.Tensor, bits: int, kn: int = 64, causal: bool = False):
+    """The counts behind Section 4.4's locality measure, all on the GPU:
+    encode, sort and select each query's Z-order window of kn keys, the exact
+    kn nearest keys (``zeta_exact_knn``) and, per query, how many keys the two
+    share (``zeta_index_overlap``).  Returns (shared [B,H,N] int32, nearest
+    [B,H,N,kn] int32, -1 padded); the measure is shared.sum() over the number
+    of valid nearest entries."""
     B, H, N, dk = q.shape
     ws = workspace_for(B, H, N, dk, bits, kn, causal, q.device)
     qc, kc = zeta_morton_encode(q, k, bits, workspace=ws)
     sc, perm = zeta_sort_keys(kc, dk * bits, workspace=ws)
     win = zeta_select_topk(qc, sc, perm, kn, causal, workspace=ws)
     nn = zeta_exact_knn(q, k, kn, causal)
-    shared = zeta_index_overlap(win, nn, N)
-    valid = (nn >= 0).sum()
-    return float(shared.sum().item()) / float(valid.item())
+    return zeta_index_overlap(win, nn, N), nn
 
 
 def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, topk: int, eps: float, causal: bool = True,
