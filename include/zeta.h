@@ -119,6 +119,31 @@ zeta_status_t zeta_morton_encode(const void* q, const void* k, zeta_dtype_t dtyp
                                  hipStream_t stream);
 
 /*
+ * zeta_morton_encode_static -- zeta_morton_encode for callers that cannot
+ * allocate or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid device allocation.  Same arguments, layouts,
+ * results (bit for bit) and errors as zeta_morton_encode, without the
+ * workspace.
+ *
+ * The per-segment range partials (when range_lohi is NULL) go to a
+ * file-scope device array of ZETA_ENCODE_STATIC_SCRATCH_BYTES inside the
+ * library: one copy per GPU, looked up once per device on the first call
+ * that needs it on that device and held until the process ends.  The call
+ * itself allocates nothing (no hipMalloc, no allocating library routine).
+ * It needs 24 * B*H * ceil(N / 512) bytes there for d_k = 3 (8 * d_k per
+ * segment and 512-row chunk in general); a larger problem returns
+ * ZETA_ERR_UNSUPPORTED before any GPU work.  Every call on one GPU shares
+ * that GPU's array: calls that overlap in time on one GPU (other streams,
+ * other threads) race and must be serialised by the caller.  The stream's
+ * device (the current device for the null stream) is the one used.
+ */
+#define ZETA_ENCODE_STATIC_SCRATCH_BYTES (1u << 20)
+zeta_status_t zeta_morton_encode_static(const void* q, const void* k, zeta_dtype_t dtype, int64_t B,
+                                        int64_t H, int64_t N, int d_k, int bits,
+                                        const float* range_lohi, float* range_out, uint32_t* q_codes,
+                                        uint32_t* k_codes, hipStream_t stream);
+
+/*
  * zeta_sort_keys -- sort each segment's key codes ascending (Section 3.2.2,
  * keys sorted in the one-dimensional space; Algorithm 1, Step 2; Appendix B
  * names a radix sort).  Equal codes keep ascending position order (the sort is

@@ -19,6 +19,7 @@ from .zeta import (  # noqa: F401
     zeta_history_mean,
     zeta_index_overlap,
     zeta_morton_encode,
+    zeta_morton_encode_static,
     zeta_query_order,
     zeta_select_attend_fwd,
     zeta_select_attend_bwd,

@@ -14,6 +14,8 @@
 #include "kernels.h"
 #include "layout.h"
 
+#include <mutex>
+
 namespace zeta {
 namespace {
 
@@ -176,7 +178,61 @@ hipError_t launch_encode_t(const T* q, const T* k, int64_t S, int64_t N, int dk,
   return hipGetLastError();
 }
 
+// Range partials of the allocation-free entry point: one copy per GPU, held
+// until the process ends.  Host code never passes `scratch` itself (its name
+// is a host-side stand-in, not a device address); it passes the address that
+// hipGetSymbolAddress returns for the device, taken once per device.
+static __device__ __align__(256) unsigned char scratch[kEncStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the stream's device (the current device for
+// the null stream), looked up with that device current on its first use.
+hipError_t static_scratch(hipStream_t stream, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (stream != nullptr) {
+    hipDevice_t sd = 0;
+    e = hipStreamGetDevice(stream, &sd);
+    if (e != hipSuccess) return e;
+    dev = int(sd);
+  }
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    if (ptr == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
 }  // namespace
+
+hipError_t launch_encode_static(const void* q, const void* k, bool is_bf16, int64_t S, int64_t N, int dk, int bits,
+                                const float* range_lohi, float* range_out, uint32_t* q_codes, uint32_t* k_codes,
+                                hipStream_t stream) {
+  void* ws = nullptr;
+  if (range_lohi == nullptr) {
+    const hipError_t e = static_scratch(stream, &ws);
+    if (e != hipSuccess) return e;
+  }
+  return launch_encode(q, k, is_bf16, S, N, dk, bits, range_lohi, range_out, q_codes, k_codes, ws, stream);
+}
 
 hipError_t launch_encode(const void* q, const void* k, bool is_bf16, int64_t S, int64_t N, int dk,
                          int bits, const float* range_lohi, float* range_out, uint32_t* q_codes,

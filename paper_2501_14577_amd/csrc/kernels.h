@@ -39,6 +39,13 @@ hipError_t launch_encode(const void* q, const void* k, bool is_bf16, int64_t S, 
                          int bits, const float* range_lohi, float* range_out, uint32_t* q_codes,
                          uint32_t* k_codes, void* workspace, hipStream_t stream);
 
+// launch_encode with the range partials in the library's own per-GPU
+// scratch array (kEncStaticScratchBytes) instead of a caller workspace; the
+// caller has checked that they fit.
+hipError_t launch_encode_static(const void* q, const void* k, bool is_bf16, int64_t S, int64_t N, int dk, int bits,
+                                const float* range_lohi, float* range_out, uint32_t* q_codes, uint32_t* k_codes,
+                                hipStream_t stream);
+
 // Stable LSD radix sort of each segment's codes.
 hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_bits,
                        uint32_t* sorted_codes, int32_t* perm, void* workspace, hipStream_t stream);

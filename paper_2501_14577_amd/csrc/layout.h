@@ -17,6 +17,9 @@ constexpr int kMaxBits = 24;    // grid cells per axis stay exact in float32
 constexpr int64_t kEncRowsPerChunk = 512;
 // Rows of q (and of k) encoded by one block of the encode kernel.
 constexpr int64_t kEncRowsPerBlock = 256;
+// Bytes of the per-GPU array that holds the range partials of the
+// allocation-free encode call.
+constexpr size_t kEncStaticScratchBytes = size_t(1) << 20;
 
 // ---- sort -----------------------------------------------------------------
 // Keys per tile of the radix passes: 4 waves x 4 chunks of 64 keys (short

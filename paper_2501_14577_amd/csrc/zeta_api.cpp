@@ -10,6 +10,7 @@
 static_assert(ZETA_MAX_DK == zeta::kMaxDk, "d_k limit mismatch");
 static_assert(ZETA_MAX_TOPK == zeta::kMaxTopk, "topk limit mismatch");
 static_assert(ZETA_MAX_BITS == zeta::kMaxBits, "bits limit mismatch");
+static_assert(ZETA_ENCODE_STATIC_SCRATCH_BYTES == zeta::kEncStaticScratchBytes, "static scratch size mismatch");
 static_assert(int(ZETA_SCORE_CAUCHY) == zeta::kScoreCauchy && int(ZETA_SCORE_DOT) == zeta::kScoreDot &&
                   int(ZETA_SCORE_NEG_EUCLID) == zeta::kScoreNegEuclid &&
                   int(ZETA_SCORE_INV_EUCLID) == zeta::kScoreInvEuclid &&
@@ -56,6 +57,18 @@ bool bad_means(const float* mean_k, const float* mean_v) {
   return mean_v != nullptr && !aligned16(mean_v);
 }
 
+// Argument checks shared by both encode entry points.
+zeta_status_t encode_args(const void* q, const void* k, zeta_dtype_t dtype, int64_t B, int64_t H, int64_t N, int d_k,
+                          int bits, const uint32_t* q_codes, const uint32_t* k_codes) {
+  if (!q || !k || !q_codes || !k_codes) return ZETA_ERR_INVALID_ARG;
+  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
+  if (d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32) return ZETA_ERR_INVALID_ARG;
+  if (q_codes == k_codes) return ZETA_ERR_INVALID_ARG;
+  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
+  if (d_k > zeta::kMaxDk || bits > zeta::kMaxBits) return ZETA_ERR_UNSUPPORTED;
+  return ZETA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -64,12 +77,8 @@ zeta_status_t zeta_morton_encode(const void* q, const void* k, zeta_dtype_t dtyp
                                  int64_t N, int d_k, int bits, const float* range_lohi, float* range_out,
                                  uint32_t* q_codes, uint32_t* k_codes, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream) {
-  if (!q || !k || !q_codes || !k_codes) return ZETA_ERR_INVALID_ARG;
-  if (bad_count(B, H, N)) return ZETA_ERR_INVALID_ARG;
-  if (d_k < 1 || bits < 1 || int64_t(d_k) * bits > 32) return ZETA_ERR_INVALID_ARG;
-  if (q_codes == k_codes) return ZETA_ERR_INVALID_ARG;
-  if (!dtype_known(dtype)) return ZETA_ERR_UNSUPPORTED;
-  if (d_k > zeta::kMaxDk || bits > zeta::kMaxBits) return ZETA_ERR_UNSUPPORTED;
+  const zeta_status_t st = encode_args(q, k, dtype, B, H, N, d_k, bits, q_codes, k_codes);
+  if (st != ZETA_OK) return st;
   const int64_t S = B * H;
   if (range_lohi == nullptr) {
     const zeta::EncodeWs ws = zeta::encode_ws(S, N, d_k);
@@ -77,6 +86,18 @@ zeta_status_t zeta_morton_encode(const void* q, const void* k, zeta_dtype_t dtyp
   }
   return hip_status(zeta::launch_encode(q, k, dtype == ZETA_BF16, S, N, d_k, bits, range_lohi, range_out,
                                         q_codes, k_codes, workspace, stream));
+}
+
+zeta_status_t zeta_morton_encode_static(const void* q, const void* k, zeta_dtype_t dtype, int64_t B, int64_t H,
+                                        int64_t N, int d_k, int bits, const float* range_lohi, float* range_out,
+                                        uint32_t* q_codes, uint32_t* k_codes, hipStream_t stream) {
+  const zeta_status_t st = encode_args(q, k, dtype, B, H, N, d_k, bits, q_codes, k_codes);
+  if (st != ZETA_OK) return st;
+  const int64_t S = B * H;
+  if (range_lohi == nullptr && zeta::encode_ws(S, N, d_k).bytes > zeta::kEncStaticScratchBytes)
+    return ZETA_ERR_UNSUPPORTED;
+  return hip_status(zeta::launch_encode_static(q, k, dtype == ZETA_BF16, S, N, d_k, bits, range_lohi, range_out,
+                                               q_codes, k_codes, stream));
 }
 
 zeta_status_t zeta_sort_keys(const uint32_t* k_codes, int64_t n_segments, int64_t N, int code_bits,

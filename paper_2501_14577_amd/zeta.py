@@ -19,10 +19,12 @@ _lib = None
 
 ZETA_OK, ZETA_ERR_INVALID_ARG, ZETA_ERR_UNSUPPORTED, ZETA_ERR_WORKSPACE, ZETA_ERR_HIP = range(5)
 ZETA_F32, ZETA_BF16 = 0, 1
+ZETA_ENCODE_STATIC_SCRATCH_BYTES = 1 << 20  # the allocation-free encode's per-GPU array (include/zeta.h)
 # Attention scores (zeta_score_t): the method's Cauchy score and the variants.
 SCORES = {"cauchy": 0, "dot": 1, "neg_euclid": 2, "inv_euclid": 3, "norm_dot": 4}
 EXPORTED = (
     "zeta_morton_encode",
+    "zeta_morton_encode_static",
     "zeta_sort_keys",
     "zeta_query_order",
     "zeta_select_topk",
@@ -62,6 +64,7 @@ def load_library() -> ctypes.CDLL:
     L = ctypes.CDLL(_LIB_PATH)
     vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     L.zeta_morton_encode.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+    L.zeta_morton_encode_static.argtypes = [vp, vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp]
     L.zeta_sort_keys.argtypes = [vp, i64, i64, i32, vp, vp, vp, sz, vp]
     L.zeta_query_order.argtypes = [vp, i64, i64, i32, i32, i32, vp, vp, sz, vp]
     L.zeta_select_topk.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, vp, vp, vp, sz, vp]
@@ -80,7 +83,7 @@ def load_library() -> ctypes.CDLL:
                                          vp, f32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.zeta_select_attend_bwd_workspace_size.argtypes = [i64, i64, i64, i32, i32, i32, i32]
     L.zeta_status_string.argtypes = [i32]
-    for name in ("zeta_morton_encode", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
+    for name in ("zeta_morton_encode", "zeta_morton_encode_static", "zeta_sort_keys", "zeta_query_order", "zeta_select_topk",
                  "zeta_topk_attn_fwd", "zeta_select_attend_fwd", "zeta_history_mean", "zeta_topk_attn_bwd",
                  "zeta_select_attend_bwd", "zeta_exact_knn", "zeta_index_overlap"):
         getattr(L, name).restype = ctypes.c_int
@@ -177,6 +180,28 @@ def zeta_morton_encode(q: torch.Tensor, k: torch.Tensor, bits: int, *,
                                            _ptr(range_lohi), _ptr(range_out), _ptr(q_codes), _ptr(k_codes),
                                            _ptr(workspace), ws_bytes, _stream())
     _check("zeta_morton_encode", st)
+    return q_codes, k_codes
+
+
+def zeta_morton_encode_static(q: torch.Tensor, k: torch.Tensor, bits: int, *,
+                              range_lohi: Optional[torch.Tensor] = None,
+                              range_out: Optional[torch.Tensor] = None,
+                              q_codes: Optional[torch.Tensor] = None,
+                              k_codes: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """zeta_morton_encode without a workspace (the library's own per-GPU
+    scratch holds the range partials; the C call allocates nothing)."""
+    B, H, N, dk = q.shape
+    if k.shape != q.shape or k.dtype != q.dtype:
+        raise ValueError("q and k must share shape and dtype")
+    if q_codes is None:
+        q_codes = torch.empty((B, H, N), dtype=torch.uint32, device=q.device)
+    if k_codes is None:
+        k_codes = torch.empty((B, H, N), dtype=torch.uint32, device=q.device)
+    _need_device(q, k, range_lohi, range_out, q_codes, k_codes)
+    st = load_library().zeta_morton_encode_static(_ptr(q), _ptr(k), _dtype_code(q), B, H, N, dk, bits,
+                                                  _ptr(range_lohi), _ptr(range_out), _ptr(q_codes), _ptr(k_codes),
+                                                  _stream())
+    _check("zeta_morton_encode_static", st)
     return q_codes, k_codes
 
 

@@ -201,6 +201,31 @@ def test_encode_rejects(kw, code):
     assert _enc(**kw) == code
 
 
+def _enc_static(**kw):
+    a = dict(q=P, k=P2, dtype=zb.ZETA_BF16, B=1, H=2, N=100, d_k=3, bits=10, range_lohi=NULL,
+             range_out=NULL, q_codes=P3, k_codes=P4, stream=NULL)
+    a.update(kw)
+    return zeta.load_library().zeta_morton_encode_static(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [c for c in ENCODE_CASES if "ws" not in c[0] and "ws_bytes" not in c[0]],
+                         ids=[str(c[0]) for c in ENCODE_CASES if "ws" not in c[0] and "ws_bytes" not in c[0]])
+def test_encode_static_rejects(kw, code):
+    """The allocation-free encode validates exactly as the workspace one."""
+    assert _enc_static(**kw) == code
+
+
+def test_encode_static_scratch_limit():
+    """Range partials beyond the library's per-GPU array are refused before
+    any GPU work: 24 bytes per segment and 512-row chunk at d_k = 3."""
+    limit = zb.ZETA_ENCODE_STATIC_SCRATCH_BYTES
+    assert limit == 1 << 20
+    chunks = 500
+    over = limit // (24 * chunks) + 1  # segments whose partials just exceed the array
+    assert _enc_static(H=over, N=512 * chunks) == UNS
+    assert 24 * (over - 1) * chunks <= limit
+
+
 SORT_CASES = [
     (dict(k_codes=NULL), INV), (dict(sorted_codes=NULL), INV), (dict(perm=NULL), INV),
     (dict(S=0), INV), (dict(N=0), INV), (dict(N=1 << 31), INV), (dict(code_bits=0), INV), (dict(code_bits=33), INV),
