@@ -9,6 +9,15 @@
 //     quantises and interleaves 256 query rows and 256 key rows, each row read
 //     with one load.  Quantisation is float32 with one rounding per operation,
 //     matching the definition bit for bit.
+// For d_k = 3 with 16-byte aligned tensors and N a multiple of 8 (every
+// workload here) both kernels take a vector form instead: a thread owns 8
+// consecutive rows, read as whole 16-byte vectors (24 values: three loads of
+// bfloat16, six of float32) and written as two 16-byte code stores; a block
+// covers 1024 rows of one segment (grid: chunks x segments, no index
+// division; up to 65535 segments).  The quotient of the quantiser comes from the hardware
+// reciprocal unless it lies close enough to an integer that the correctly
+// rounded division could floor differently; then the IEEE division decides
+// (the codes are those of the definition either way).
 #include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -160,11 +169,206 @@ __global__ void __launch_bounds__(256) encode_kernel(const T* __restrict__ q, co
   }
 }
 
+// ---- d_k = 3, vector form ---------------------------------------------------
+
+constexpr int kEnc3Threads = 128;
+constexpr int kEnc3Rows = 8;                                  // rows per thread
+constexpr int64_t kEnc3Chunk = int64_t(kEnc3Threads) * kEnc3Rows;  // rows per block
+
+// Rows r .. r+7 of a [rows][3] array whose row r starts on a 16-byte
+// boundary: 24 values.
+template <typename T>
+__device__ __forceinline__ void load_rows8(const T* base, int64_t r, float (&x)[24]) {
+  const uint4* p = reinterpret_cast<const uint4*>(base + r * 3);
+  if constexpr (sizeof(T) == 2) {
+    const uint4 a = p[0], b = p[1], c = p[2];
+    const uint32_t w[12] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w, c.x, c.y, c.z, c.w};
+#pragma unroll
+    for (int i = 0; i < 12; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 6; ++i) {
+      const uint4 v = p[i];
+      x[4 * i] = __uint_as_float(v.x);
+      x[4 * i + 1] = __uint_as_float(v.y);
+      x[4 * i + 2] = __uint_as_float(v.z);
+      x[4 * i + 3] = __uint_as_float(v.w);
+    }
+  }
+}
+
+// Per-axis min and max of (lo[a], hi[a]) over the block (128 threads), result
+// in s_lo / s_hi.
+__device__ __forceinline__ void block128_range3(float (&lo)[3], float (&hi)[3], float* s_lo, float* s_hi) {
+  __shared__ float s_part[2][6];
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      lo[a] = fminf(lo[a], __shfl_xor(lo[a], off, 64));
+      hi[a] = fmaxf(hi[a], __shfl_xor(hi[a], off, 64));
+    }
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      s_part[wave][a] = lo[a];
+      s_part[wave][3 + a] = hi[a];
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    s_lo[threadIdx.x] = fminf(s_part[0][threadIdx.x], s_part[1][threadIdx.x]);
+    s_hi[threadIdx.x] = fmaxf(s_part[0][3 + threadIdx.x], s_part[1][3 + threadIdx.x]);
+  }
+  __syncthreads();
+}
+
+// Range partials: per (segment, 1024-row chunk), lo then hi of each axis.
+template <typename T>
+__global__ void __launch_bounds__(kEnc3Threads)
+    range3_kernel(const T* __restrict__ q, const T* __restrict__ k, int64_t N, float* __restrict__ partial) {
+  const int64_t chunk = blockIdx.x, seg = blockIdx.y;
+  const int64_t r = chunk * kEnc3Chunk + int64_t(threadIdx.x) * kEnc3Rows;
+  float lo[3], hi[3];
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    lo[a] = __builtin_huge_valf();
+    hi[a] = -__builtin_huge_valf();
+  }
+  if (r < N) {  // N is a multiple of 8: all 8 rows exist
+    float x[24], y[24];
+    load_rows8(q, seg * N + r, x);
+    load_rows8(k, seg * N + r, y);
+#pragma unroll
+    for (int i = 0; i < 24; ++i) {
+      lo[i % 3] = fminf(lo[i % 3], fminf(x[i], y[i]));
+      hi[i % 3] = fmaxf(hi[i % 3], fmaxf(x[i], y[i]));
+    }
+  }
+  __shared__ float s_lo[3], s_hi[3];
+  block128_range3(lo, hi, s_lo, s_hi);
+  if (threadIdx.x < 3) {
+    float* out = partial + (seg * int64_t(gridDim.x) + chunk) * 6;
+    out[threadIdx.x] = s_lo[threadIdx.x];
+    out[3 + threadIdx.x] = s_hi[threadIdx.x];
+  }
+}
+
+// quantise() with the division done by the hardware reciprocal where that
+// provably floors the same: w' = u * rcp(den) is within 2^-21.5 * w' of the
+// correctly rounded quotient, so when w' is farther than 2^-20 * w' from the
+// nearest integer both lie strictly on the same side of it, inside the same
+// unit interval, and floor alike.  Otherwise (or for w' >= 2^19, where that
+// margin reaches half a unit) the IEEE division is taken.
+__device__ __forceinline__ uint32_t quantise_fast(float x, float lo, float den, float rden, float topf, uint32_t top) {
+#pragma clang fp contract(off)
+  if (!(den > 0.0f)) return 0u;
+  const float t = x - lo;
+  const float u = t * topf;
+  float w = u * rden;
+  const float n = rintf(w);
+  const float margin = w * 0x1p-20f;
+  if (!(fabsf(w - n) > margin) || !(w < 0x1p19f)) w = __fdiv_rn(u, den);
+  const float f = floorf(w);
+  if (!(f > 0.0f)) return 0u;
+  if (f >= topf) return top;
+  return uint32_t(f);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kEnc3Threads)
+    encode3_kernel(const T* __restrict__ q, const T* __restrict__ k, int64_t N, int bits,
+                   const float* __restrict__ partial, const float* __restrict__ range_lohi,
+                   float* __restrict__ range_out, uint32_t* __restrict__ q_codes, uint32_t* __restrict__ k_codes) {
+  const int64_t chunk = blockIdx.x, seg = blockIdx.y;
+  const int64_t chunks = gridDim.x;
+  __shared__ float s_lo[3], s_hi[3];
+  if (range_lohi != nullptr) {
+    if (threadIdx.x < 3) {
+      s_lo[threadIdx.x] = range_lohi[seg * 6 + threadIdx.x];
+      s_hi[threadIdx.x] = range_lohi[seg * 6 + 3 + threadIdx.x];
+    }
+    __syncthreads();
+  } else {
+    // Fold the segment's partial ranges.
+    float lo[3], hi[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      lo[a] = __builtin_huge_valf();
+      hi[a] = -__builtin_huge_valf();
+    }
+    const float* p = partial + seg * chunks * 6;
+    for (int64_t c = threadIdx.x; c < chunks; c += kEnc3Threads) {
+#pragma unroll
+      for (int a = 0; a < 3; ++a) {
+        lo[a] = fminf(lo[a], p[c * 6 + a]);
+        hi[a] = fmaxf(hi[a], p[c * 6 + 3 + a]);
+      }
+    }
+    block128_range3(lo, hi, s_lo, s_hi);
+  }
+  if (range_out != nullptr && chunk == 0 && threadIdx.x < 3) {
+    range_out[seg * 6 + threadIdx.x] = s_lo[threadIdx.x];
+    range_out[seg * 6 + 3 + threadIdx.x] = s_hi[threadIdx.x];
+  }
+  const int64_t r = chunk * kEnc3Chunk + int64_t(threadIdx.x) * kEnc3Rows;
+  if (r >= N) return;
+  const uint32_t top = (1u << bits) - 1u;
+  const float topf = float(top);
+  float lo[3], den[3], rden[3];
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    lo[a] = s_lo[a];
+    {
+#pragma clang fp contract(off)
+      den[a] = s_hi[a] - s_lo[a];
+    }
+    rden[a] = __builtin_amdgcn_rcpf(den[a]);
+  }
+#pragma unroll
+  for (int which = 0; which < 2; ++which) {
+    float x[24];
+    load_rows8(which == 0 ? q : k, seg * N + r, x);
+    uint32_t c[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t c0 = quantise_fast(x[3 * i], lo[0], den[0], rden[0], topf, top);
+      const uint32_t c1 = quantise_fast(x[3 * i + 1], lo[1], den[1], rden[1], topf, top);
+      const uint32_t c2 = quantise_fast(x[3 * i + 2], lo[2], den[2], rden[2], topf, top);
+      c[i] = (spread3(c0) << 2) | (spread3(c1) << 1) | spread3(c2);
+    }
+    uint4* dst = reinterpret_cast<uint4*>((which == 0 ? q_codes : k_codes) + seg * N + r);
+    dst[0] = make_uint4(c[0], c[1], c[2], c[3]);
+    dst[1] = make_uint4(c[4], c[5], c[6], c[7]);
+  }
+}
+
+bool aligned16_ptr(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 template <typename T>
 hipError_t launch_encode_t(const T* q, const T* k, int64_t S, int64_t N, int dk, int bits,
                            const float* range_lohi, float* range_out, uint32_t* q_codes,
                            uint32_t* k_codes, void* workspace, hipStream_t stream) {
   const EncodeWs ws = encode_ws(S, N, dk);
+  if (dk == 3 && N % kEnc3Rows == 0 && S <= 65535 && aligned16_ptr(q) && aligned16_ptr(k) && aligned16_ptr(q_codes) &&
+      aligned16_ptr(k_codes)) {
+    // Vector form; its partials (one per 1024-row chunk) fit in the space
+    // sized for 512-row chunks.
+    const dim3 grid(unsigned(ceil_div(N, kEnc3Chunk)), unsigned(S));
+    float* partial = nullptr;
+    if (range_lohi == nullptr) {
+      partial = reinterpret_cast<float*>(static_cast<char*>(workspace) + ws.partial_off);
+      hipLaunchKernelGGL(range3_kernel<T>, grid, dim3(kEnc3Threads), 0, stream, q, k, N, partial);
+    }
+    hipLaunchKernelGGL(encode3_kernel<T>, grid, dim3(kEnc3Threads), 0, stream, q, k, N, bits, partial, range_lohi,
+                       range_out, q_codes, k_codes);
+    return hipGetLastError();
+  }
   float* partial = nullptr;
   if (range_lohi == nullptr) {
     partial = reinterpret_cast<float*>(static_cast<char*>(workspace) + ws.partial_off);

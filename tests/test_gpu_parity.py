@@ -60,11 +60,17 @@ def _edge_values(lo, hi, bits):
     return np.concatenate(vals).astype(np.float32)
 
 
+@pytest.mark.parametrize("pad8", [False, True])
 @pytest.mark.parametrize("bits,lo,hi", [(10, -1.7, 2.3), (6, -3.1, 0.9), (10, 0.1, 0.30000001), (2, -1.0, 1.0)])
-def test_encode_bucket_edges(bits, lo, hi):
-    log(f"encode edges bits={bits} lo={lo} hi={hi}")
+def test_encode_bucket_edges(bits, lo, hi, pad8):
+    """pad8: a length that is a multiple of 8 (the vector form of the d_k = 3
+    kernels), else a ragged one (the row-per-thread form)."""
+    log(f"encode edges bits={bits} lo={lo} hi={hi} pad8={pad8}")
     vals = _edge_values(lo, hi, bits)
     vals = np.concatenate([vals, np.float32([lo - 1, hi + 1])])  # outside the range: clamps
+    if pad8 != (len(vals) % 8 == 0):
+        extra = (-len(vals)) % 8 if pad8 else 1
+        vals = np.concatenate([vals, np.linspace(lo, hi, extra + 2, dtype=np.float32)[1:extra + 1]])
     n = len(vals)
     rng = np.random.default_rng(bits)
     q = np.stack([vals, rng.permutation(vals), rng.permutation(vals)], axis=-1)[None].astype(np.float32)
@@ -80,9 +86,10 @@ def test_encode_bucket_edges(bits, lo, hi):
 
 @pytest.mark.parametrize("dk,bits,dtype", [(1, 20, "f32"), (2, 16, "bf16"), (3, 10, "f32"), (3, 7, "bf16"),
                                            (4, 8, "f32"), (5, 6, "bf16"), (8, 4, "f32")])
-def test_encode_shapes(dk, bits, dtype):
-    log(f"encode dk={dk} bits={bits} {dtype}")
-    w = workloads.custom(B=2, H=3, N=5001, dk=dk, dtype=dtype, bits=bits, seed=dk * 100 + bits)
+@pytest.mark.parametrize("N", [5001, 5008])
+def test_encode_shapes(dk, bits, dtype, N):
+    log(f"encode dk={dk} bits={bits} {dtype} N={N}")
+    w = workloads.custom(B=2, H=3, N=N, dk=dk, dtype=dtype, bits=bits, seed=dk * 100 + bits)
     x = workloads.generate(w, with_v=False)
     S = w.segments
     qf = oracle.as_f32(x["q"], dtype).reshape(S, w.N, dk)
