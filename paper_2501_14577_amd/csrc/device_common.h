@@ -55,9 +55,11 @@ __device__ __forceinline__ int64_t xcd_contiguous_block(int64_t b, int64_t nb) {
   return (x < extra) ? x * (per + 1) + l : extra * (per + 1) + (x - extra) * per + l;
 }
 
-// Exclusive prefix sum over a block of exactly 256 threads (one value each).
-// `scratch` must hold 4 words.  Contains block barriers: every thread calls it.
-__device__ __forceinline__ uint32_t block256_exclusive_scan(uint32_t x, uint32_t* scratch) {
+// Exclusive prefix sum over a block of exactly 64 * kWaves threads (one value
+// each).  `scratch` must hold kWaves words.  Contains block barriers: every
+// thread calls it.
+template <int kWaves>
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* scratch) {
   const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
   uint32_t incl = x;
 #pragma unroll

@@ -53,7 +53,7 @@ hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_b
 // One stable radix pass whose digit is the prefix-list level class of each
 // carried value (a query position; vals NULL: the positions 0..N-1) under the
 // causal rule `chunk` (0: exact prefix): a stable partition of each segment
-// by list level.  hist holds S * (ceil(N / kSortTile) + 1) * kRadixMax words.
+// by list level.  hist holds S * (ceil(N / kLevelTile) + 1) * kRadixMax words.
 // vals_out must not alias vals.
 hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels, int chunk,
                                   int32_t* vals_out, uint32_t* hist, hipStream_t stream);

@@ -22,12 +22,22 @@ constexpr int64_t kEncRowsPerBlock = 256;
 constexpr size_t kEncStaticScratchBytes = size_t(1) << 20;
 
 // ---- sort -----------------------------------------------------------------
-// Keys per tile of the radix passes: 4 waves x 4 chunks of 64 keys (short
-// per-wave counting chains, many blocks in flight).
+// Keys per tile of the prefix-list kernels: 4 waves x 4 chunks of 64 keys.
 constexpr int kSortThreads = 256;
 constexpr int kSortChunks = 4;
 constexpr int64_t kSortTile = int64_t(kSortThreads) * kSortChunks;
+// Keys per tile of the radix passes: 8 waves x 8 chunks of 64 keys, so that a
+// tile holds about 8 keys of each of the 512 digit values and its reordered
+// output is written in runs.
+constexpr int kRadixThreads = 512;
+constexpr int kRadixChunks = 8;
+constexpr int64_t kRadixTile = int64_t(kRadixThreads) * kRadixChunks;
 constexpr int kRadixMax = 512;  // digits of at most 9 bits
+// Keys per tile of the level partition (zeta_query_order).
+constexpr int64_t kLevelTile = 2048;
+// Up to this many tiles per segment the scatter sums the earlier tiles' counts
+// itself; beyond it a scan kernel writes them first.
+constexpr int64_t kRadixInlineTiles = 32;
 
 // ---- select ---------------------------------------------------------------
 constexpr int kSelWavesPerBlock = 4;
@@ -58,7 +68,7 @@ inline SortPlan sort_plan(int64_t N, int code_bits) {
   SortPlan p;
   p.passes = (code_bits + 8) / 9;
   p.digit_bits = (code_bits + p.passes - 1) / p.passes;
-  p.tiles = ceil_div(N, kSortTile);
+  p.tiles = ceil_div(N, kRadixTile);
   return p;
 }
 
@@ -237,7 +247,7 @@ inline QueryOrderWs query_order_ws(int64_t S, int64_t N) {
   QueryOrderWs w;
   w.given_off = 0;
   w.phist_off = align_up(size_t(S) * size_t(N) * sizeof(int32_t));
-  w.bytes = w.phist_off + align_up(size_t(S) * size_t(ceil_div(N, kSortTile) + 1) * kRadixMax * sizeof(uint32_t));
+  w.bytes = w.phist_off + align_up(size_t(S) * size_t(ceil_div(N, kLevelTile) + 1) * kRadixMax * sizeof(uint32_t));
   return w;
 }
 

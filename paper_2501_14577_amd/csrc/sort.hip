@@ -1,17 +1,23 @@
 // Stable segmented LSD radix sort of (code, position) pairs (Section 3.2.2;
 // Algorithm 1, Step 2; Appendix B sorts the codes with a radix sort).
 //
-// Every segment is cut into tiles of 1024 keys.  One pass over a digit of at
-// most 9 bits runs three kernels:
+// Every segment is cut into tiles of 4096 keys (2048 for the level
+// partition of a processing order).  One pass over a digit of at
+// most 9 bits runs two kernels (three when a segment has more than 32 tiles):
 //   hist:    per tile, the count of each digit value (LDS atomics);
-//   scan:    per segment and digit value, the counts of earlier tiles
-//            (written over the tile counts) and the segment total;
-//   scatter: per tile, the digit's global base (an exclusive scan over digit
-//            values of the segment totals, plus the earlier tiles' counts),
-//            then a stable rank of every key inside the tile: each wavefront
-//            walks its 256 keys in order, 64 at a time, finding same-digit
-//            lanes with one ballot per digit bit and counting them with
-//            mbcnt; per-wave running counts live in LDS.
+//   [scan:   per segment and digit value, the counts of earlier tiles
+//            (written over the tile counts) and the segment total;]
+//   scatter: per tile, the digit's first output slot (an exclusive scan over
+//            digit values of the segment totals, plus the earlier tiles'
+//            counts, which the scatter sums itself for up to 32 tiles), a
+//            stable rank of every key inside the tile (each wavefront walks
+//            its 512 keys in order, 64 at a time, finding same-digit lanes
+//            with one ballot per digit bit and counting them with mbcnt), the
+//            tile reordered by digit in LDS, and then the tile written out in
+//            that order, so that each digit's keys leave as one run of
+//            consecutive addresses.
+// Tiles of one segment run on one XCD (xcd_contiguous_block): the runs
+// several tiles write into the same output lines merge in that XCD's L2.
 // A pass preserves the order of equal digits, so after the last pass equal
 // codes are in ascending position order.  ceil(code_bits / 9) passes split
 // the bits evenly (18-bit codes: two passes of 9).
@@ -22,6 +28,9 @@
 
 namespace zeta {
 namespace {
+
+constexpr int kRadixWaves = kRadixThreads / 64;
+static_assert(kRadixThreads == kRadixMax, "one digit value per thread");
 
 // Digit of an element: the key's bits [shift, shift+nbits) (kByLevel false), or
 // the prefix-list level class of the carried position (kByLevel true; the
@@ -34,36 +43,40 @@ __device__ __forceinline__ uint32_t radix_digit(uint32_t key, int32_t val, int s
   return (key >> shift) & mask;
 }
 
-template <bool kByLevel>
-__global__ void __launch_bounds__(kSortThreads)
+template <bool kByLevel, int kChunks>
+__global__ void __launch_bounds__(kRadixThreads)
     radix_hist_kernel(const uint32_t* __restrict__ keys, const int32_t* __restrict__ vals, int64_t N, int64_t tiles,
                       int shift, int nbits, int t0, int t_hi, int chunk, uint32_t* __restrict__ hist) {
-  const int64_t seg = blockIdx.x / tiles;
-  const int64_t tile = blockIdx.x % tiles;
+  // Tiles of one segment run under one L2 (see xcd_contiguous_block).
+  const int64_t blk = xcd_contiguous_block(blockIdx.x, gridDim.x);
+  const int64_t seg = blk / tiles;
+  const int64_t tile = blk % tiles;
   const int tid = threadIdx.x;
   __shared__ uint32_t h[kRadixMax];
-  for (int d = tid; d < kRadixMax; d += kSortThreads) h[d] = 0;
+  h[tid] = 0;
   __syncthreads();
   const uint32_t mask = (1u << nbits) - 1u;
-  const int64_t e0 = tile * kSortTile;
-  const int64_t e1 = (e0 + kSortTile < N) ? e0 + kSortTile : N;
-  for (int64_t e = e0 + tid; e < e1; e += kSortThreads) {
+  constexpr int64_t kTile = int64_t(kRadixThreads) * kChunks;
+  const int64_t e0 = tile * kTile;
+  const int64_t e1 = (e0 + kTile < N) ? e0 + kTile : N;
+  for (int64_t e = e0 + tid; e < e1; e += kRadixThreads) {
     const uint32_t key = kByLevel ? 0u : keys[seg * N + e];
     const int32_t val = kByLevel ? (vals != nullptr ? vals[seg * N + e] : int32_t(e)) : 0;
     atomicAdd(&h[radix_digit<kByLevel>(key, val, shift, mask, t0, t_hi, chunk, N)], 1u);
   }
   __syncthreads();
-  for (int d = tid; d < kRadixMax; d += kSortThreads) hist[(seg * tiles + tile) * kRadixMax + d] = h[d];
+  hist[(seg * tiles + tile) * kRadixMax + tid] = h[tid];
 }
 
 // Tiles of one segment are split into kScanGroups contiguous groups; wave g
 // of the block sums group g for 64 digit values, the groups' sums are
 // combined through LDS, and each wave then rewrites its tiles' counts as
-// exclusive prefixes.  Grid: S * (kRadixMax / 64) blocks.
-constexpr int kScanGroups = kSortThreads / 64;
+// exclusive prefixes.  Grid: S * (kRadixMax / 64) blocks of kScanThreads.
+constexpr int kScanThreads = 256;
+constexpr int kScanGroups = kScanThreads / 64;
 constexpr int kScanBatch = 16;
 
-__global__ void __launch_bounds__(kSortThreads)
+__global__ void __launch_bounds__(kScanThreads)
     radix_scan_kernel(int64_t tiles, uint32_t* __restrict__ hist, uint32_t* __restrict__ totals) {
   const int64_t seg = blockIdx.x / (kRadixMax / 64);
   const int d = int(blockIdx.x % (kRadixMax / 64)) * 64 + (threadIdx.x & 63);
@@ -104,52 +117,69 @@ __global__ void __launch_bounds__(kSortThreads)
   }
 }
 
-template <bool kHasPos, bool kByLevel>
-__global__ void __launch_bounds__(kSortThreads)
+// kInline: the tile counts in `hist` are raw (no scan ran) and the segment
+// has at most kRadixInlineTiles tiles; otherwise `hist` holds the earlier
+// tiles' counts and `totals` the segment totals.
+template <bool kHasPos, bool kByLevel, bool kInline, int kChunks>
+__global__ void __launch_bounds__(kRadixThreads)
     radix_scatter_kernel(const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ pos_in,
                          int64_t N, int64_t tiles, int shift, int nbits, int t0, int t_hi, int chunk,
                          const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals,
                          uint32_t* __restrict__ keys_out, int32_t* __restrict__ pos_out) {
-  const int64_t seg = blockIdx.x / tiles;
-  const int64_t tile = blockIdx.x % tiles;
+  const int64_t blk = xcd_contiguous_block(blockIdx.x, gridDim.x);
+  const int64_t seg = blk / tiles;
+  const int64_t tile = blk % tiles;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const uint32_t mask = (1u << nbits) - 1u;
 
-  __shared__ uint32_t s_base[kRadixMax];              // first output slot of each digit in this tile
-  __shared__ uint32_t s_wcnt[kSortThreads / 64][kRadixMax];  // per-wave running / prefix counts
-  __shared__ uint32_t s_scan[4];
+  __shared__ uint32_t s_base[kRadixMax];               // output slot of the tile's first key of each digit
+  __shared__ uint32_t s_lstart[kRadixMax];             // tile-local slot of the first key of each digit
+  __shared__ uint32_t s_wcnt[kRadixWaves][kRadixMax];  // per-wave running, then prefix, counts
+  constexpr int kTile = kRadixThreads * kChunks;
+  __shared__ uint32_t s_key[kByLevel ? 1 : kTile];
+  __shared__ int32_t s_val[kTile];
+  __shared__ uint32_t s_scan[kRadixWaves];
 
-  constexpr int kPer = kRadixMax / kSortThreads;  // digit values per thread: tid*kPer ..
   {
-    // Digit totals of the segment and counts of the tiles before this one.
-    uint32_t tot[kPer], bef[kPer], sum = 0;
+    // This thread's digit value: its count in earlier tiles and in the
+    // whole segment.
+    const int d = tid;
+    uint32_t before = 0, total = 0;
+    const uint32_t* h = hist + seg * tiles * kRadixMax + d;
+    if (kInline) {
+      // Independent loads in batches, so their latencies overlap.
+      constexpr int kBatch = 8;
+      for (int64_t t0 = 0; t0 < tiles; t0 += kBatch) {
+        uint32_t c[kBatch];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int d = tid * kPer + i;
-      tot[i] = totals[seg * kRadixMax + d];
-      bef[i] = hist[(seg * tiles + tile) * kRadixMax + d];
-      sum += tot[i];
+        for (int j = 0; j < kBatch; ++j) c[j] = t0 + j < tiles ? h[(t0 + j) * kRadixMax] : 0u;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          before += t0 + j < tile ? c[j] : 0u;
+          total += c[j];
+        }
+      }
+    } else {
+      before = h[tile * kRadixMax];
+      total = totals[seg * kRadixMax + d];
     }
-    uint32_t excl = block256_exclusive_scan(sum, s_scan);
+    const uint32_t excl = block_exclusive_scan<kRadixWaves>(total, s_scan);
+    s_base[d] = excl + before;
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      s_base[tid * kPer + i] = excl + bef[i];
-      excl += tot[i];
-#pragma unroll
-      for (int w = 0; w < kSortThreads / 64; ++w) s_wcnt[w][tid * kPer + i] = 0;
-    }
+    for (int w = 0; w < kRadixWaves; ++w) s_wcnt[w][d] = 0;
   }
   __syncthreads();
 
   const int64_t seg_off = seg * N;
-  const int64_t first = tile * kSortTile + int64_t(wave) * (kSortChunks * 64);
-  uint32_t key[kSortChunks];
-  int32_t pos[kSortChunks];
-  uint32_t rank[kSortChunks];
+  const int64_t tile0 = tile * kTile;
+  const int64_t first = tile0 + int64_t(wave) * (kChunks * 64);
+  uint32_t key[kChunks];
+  int32_t pos[kChunks];
+  uint32_t rank[kChunks];
 #pragma unroll
-  for (int c = 0; c < kSortChunks; ++c) {
+  for (int c = 0; c < kChunks; ++c) {
     const int64_t e = first + c * 64 + lane;
     const bool valid = e < N;
     const uint32_t kk = (valid && !kByLevel) ? keys_in[seg_off + e] : 0u;
@@ -173,26 +203,62 @@ __global__ void __launch_bounds__(kSortThreads)
     rank[c] = base + below;
   }
   __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kPer; ++i) {
+  {
+    // Per digit: earlier waves' counts, then the digit's first slot in the
+    // tile (exclusive scan of the tile's digit counts).
+    const int d = tid;
     uint32_t run = 0;
 #pragma unroll
-    for (int w = 0; w < kSortThreads / 64; ++w) {
-      const uint32_t t = s_wcnt[w][tid * kPer + i];
-      s_wcnt[w][tid * kPer + i] = run;
+    for (int w = 0; w < kRadixWaves; ++w) {
+      const uint32_t t = s_wcnt[w][d];
+      s_wcnt[w][d] = run;
       run += t;
     }
+    s_lstart[d] = block_exclusive_scan<kRadixWaves>(run, s_scan);
   }
   __syncthreads();
+  // The tile in digit order, in LDS.
 #pragma unroll
-  for (int c = 0; c < kSortChunks; ++c) {
+  for (int c = 0; c < kChunks; ++c) {
     const int64_t e = first + c * 64 + lane;
     if (e < N) {
       const uint32_t d = radix_digit<kByLevel>(key[c], pos[c], shift, mask, t0, t_hi, chunk, N);
-      const int64_t dst = int64_t(s_base[d]) + s_wcnt[wave][d] + rank[c];
-      if (!kByLevel) keys_out[seg_off + dst] = key[c];
-      pos_out[seg_off + dst] = pos[c];
+      const uint32_t slot = s_lstart[d] + s_wcnt[wave][d] + rank[c];
+      if (!kByLevel) s_key[slot] = key[c];
+      s_val[slot] = pos[c];
     }
+  }
+  __syncthreads();
+  // Written in that order: consecutive threads of one digit write
+  // consecutive slots.
+  const int n = int(N - tile0 < kTile ? N - tile0 : kTile);
+  for (int i = tid; i < n; i += kRadixThreads) {
+    const uint32_t kk = kByLevel ? 0u : s_key[i];
+    const int32_t vv = s_val[i];
+    const uint32_t d = radix_digit<kByLevel>(kk, vv, shift, mask, t0, t_hi, chunk, N);
+    const int64_t dst = int64_t(s_base[d]) + (uint32_t(i) - s_lstart[d]);
+    if (!kByLevel) keys_out[seg_off + dst] = kk;
+    pos_out[seg_off + dst] = vv;
+  }
+}
+
+// One pass over tiles of kRadixThreads * kChunks keys: hist, [scan,] scatter.
+template <bool kHasPos, bool kByLevel, int kChunks>
+void radix_pass(const uint32_t* keys_in, const int32_t* pos_in, int64_t S, int64_t N, int64_t tiles, int shift,
+                int nbits, int t0, int t_hi, int chunk, uint32_t* hist, uint32_t* keys_out, int32_t* pos_out,
+                hipStream_t stream) {
+  const dim3 grid(unsigned(S * tiles)), block(kRadixThreads);
+  uint32_t* totals = hist + S * tiles * kRadixMax;
+  hipLaunchKernelGGL((radix_hist_kernel<kByLevel, kChunks>), grid, block, 0, stream, keys_in, pos_in, N, tiles, shift, nbits, t0,
+                     t_hi, chunk, hist);
+  if (tiles <= kRadixInlineTiles) {
+    hipLaunchKernelGGL((radix_scatter_kernel<kHasPos, kByLevel, true, kChunks>), grid, block, 0, stream, keys_in, pos_in, N,
+                       tiles, shift, nbits, t0, t_hi, chunk, hist, totals, keys_out, pos_out);
+  } else {
+    hipLaunchKernelGGL(radix_scan_kernel, dim3(unsigned(S * (kRadixMax / 64))), dim3(kScanThreads), 0, stream, tiles,
+                       hist, totals);
+    hipLaunchKernelGGL((radix_scatter_kernel<kHasPos, kByLevel, false, kChunks>), grid, block, 0, stream, keys_in, pos_in, N,
+                       tiles, shift, nbits, t0, t_hi, chunk, hist, totals, keys_out, pos_out);
   }
 }
 
@@ -200,20 +266,18 @@ __global__ void __launch_bounds__(kSortThreads)
 
 hipError_t launch_level_partition(const int32_t* vals, int64_t S, int64_t N, int t0, int t_hi, int levels, int chunk,
                                   int32_t* vals_out, uint32_t* hist, hipStream_t stream) {
-  const int64_t tiles = ceil_div(N, kSortTile);
-  const dim3 grid(unsigned(S * tiles)), block(kSortThreads);
+  // Smaller tiles than the sort's: few digit values, long runs, and more
+  // blocks in flight.
+  constexpr int kChunks = int(kLevelTile / kRadixThreads);
+  const int64_t tiles = ceil_div(N, kLevelTile);
   int nbits = 1;
   while ((1 << nbits) < levels + 1) ++nbits;
-  uint32_t* totals = hist + S * tiles * kRadixMax;
-  hipLaunchKernelGGL(radix_hist_kernel<true>, grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits, t0, t_hi,
-                     chunk, hist);
-  hipLaunchKernelGGL(radix_scan_kernel, dim3(unsigned(S * (kRadixMax / 64))), block, 0, stream, tiles, hist, totals);
   if (vals != nullptr)
-    hipLaunchKernelGGL((radix_scatter_kernel<true, true>), grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits,
-                       t0, t_hi, chunk, hist, totals, nullptr, vals_out);
+    radix_pass<true, true, kChunks>(nullptr, vals, S, N, tiles, 0, nbits, t0, t_hi, chunk, hist, nullptr, vals_out,
+                                    stream);
   else
-    hipLaunchKernelGGL((radix_scatter_kernel<false, true>), grid, block, 0, stream, nullptr, vals, N, tiles, 0, nbits,
-                       t0, t_hi, chunk, hist, totals, nullptr, vals_out);
+    radix_pass<false, true, kChunks>(nullptr, vals, S, N, tiles, 0, nbits, t0, t_hi, chunk, hist, nullptr, vals_out,
+                                     stream);
   return hipGetLastError();
 }
 
@@ -223,10 +287,8 @@ hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_b
   const SortWs ws = sort_ws(S, N, code_bits);
   char* wsb = static_cast<char*>(workspace);
   uint32_t* hist = reinterpret_cast<uint32_t*>(wsb + ws.hist_off);
-  uint32_t* totals = hist + S * plan.tiles * kRadixMax;
   uint32_t* tmp_keys = reinterpret_cast<uint32_t*>(wsb + ws.keys_off);
   int32_t* tmp_pos = reinterpret_cast<int32_t*>(wsb + ws.pos_off);
-  const dim3 grid(unsigned(S * plan.tiles)), block(kSortThreads);
 
   const uint32_t* src_keys = k_codes;
   const int32_t* src_pos = nullptr;
@@ -237,16 +299,12 @@ hipError_t launch_sort(const uint32_t* k_codes, int64_t S, int64_t N, int code_b
     const bool to_out = ((plan.passes - 1 - p) % 2) == 0;
     uint32_t* dst_keys = to_out ? sorted_codes : tmp_keys;
     int32_t* dst_pos = to_out ? perm : tmp_pos;
-    hipLaunchKernelGGL(radix_hist_kernel<false>, grid, block, 0, stream, src_keys, nullptr, N, plan.tiles, shift,
-                       nbits, 0, 0, 0, hist);
-    hipLaunchKernelGGL(radix_scan_kernel, dim3(unsigned(S * (kRadixMax / 64))), block, 0, stream, plan.tiles, hist,
-                       totals);
     if (src_pos == nullptr)
-      hipLaunchKernelGGL((radix_scatter_kernel<false, false>), grid, block, 0, stream, src_keys, src_pos, N,
-                         plan.tiles, shift, nbits, 0, 0, 0, hist, totals, dst_keys, dst_pos);
+      radix_pass<false, false, kRadixChunks>(src_keys, src_pos, S, N, plan.tiles, shift, nbits, 0, 0, 0, hist,
+                                             dst_keys, dst_pos, stream);
     else
-      hipLaunchKernelGGL((radix_scatter_kernel<true, false>), grid, block, 0, stream, src_keys, src_pos, N,
-                         plan.tiles, shift, nbits, 0, 0, 0, hist, totals, dst_keys, dst_pos);
+      radix_pass<true, false, kRadixChunks>(src_keys, src_pos, S, N, plan.tiles, shift, nbits, 0, 0, 0, hist,
+                                            dst_keys, dst_pos, stream);
     src_keys = dst_keys;
     src_pos = dst_pos;
   }

@@ -125,8 +125,12 @@ def test_sort_config(cfg):
 
 
 @pytest.mark.parametrize("S,N,code_bits", [(1, 1, 30), (3, 63, 2), (2, 4095, 7), (2, 4096, 18), (2, 4097, 1),
-                                            (3, 10000, 32), (1, 70001, 18), (5, 12289, 9), (1, 8192, 16)])
+                                            (3, 10000, 32), (1, 70001, 18), (5, 12289, 9), (1, 8192, 16),
+                                            (1, 131072, 18), (2, 135169, 12), (1, 300001, 27)])
 def test_sort_shapes(S, N, code_bits):
+    """Ragged tails, one to three passes, and segments of up to 32 tiles of
+    4096 keys (the scatter sums the earlier tiles' counts itself) or more
+    (a scan kernel does)."""
     log(f"sort S={S} N={N} bits={code_bits}")
     kc = workloads.random_codes(S * 1000 + N + code_bits, (S, N), code_bits)
     esc, eperm = oracle.sort_keys(kc)
