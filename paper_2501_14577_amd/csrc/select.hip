@@ -47,8 +47,10 @@ namespace {
 __global__ void __launch_bounds__(kSortThreads)
     list_count_kernel(const int32_t* __restrict__ perm, int64_t N, int64_t tiles, int t0, int levels,
                       uint32_t* __restrict__ cnt) {
-  const int64_t seg = blockIdx.x / tiles;
-  const int64_t tile = blockIdx.x % tiles;
+  // Tiles of one segment run under one L2 (see xcd_contiguous_block).
+  const int64_t blk = xcd_contiguous_block(blockIdx.x, gridDim.x);
+  const int64_t seg = blk / tiles;
+  const int64_t tile = blk % tiles;
   const int tid = threadIdx.x;
   __shared__ uint32_t h[kMaxLevels + 1];  // keys per bit length of their position
   if (tid <= kMaxLevels) h[tid] = 0;
@@ -73,8 +75,11 @@ __global__ void __launch_bounds__(kSortThreads)
                         const uint32_t* __restrict__ cnt, uint32_t* __restrict__ list_codes,
                         int32_t* __restrict__ list_pos, const uint16_t* __restrict__ k_rows,
                         uint2* __restrict__ keys_full, uint2* __restrict__ keys_list) {
-  const int64_t seg = blockIdx.x / tiles;
-  const int64_t tile = blockIdx.x % tiles;
+  // Tiles of one segment run under one L2: its key rows, gathered by
+  // position, and the list lines several tiles write then stay there.
+  const int64_t blk = xcd_contiguous_block(blockIdx.x, gridDim.x);
+  const int64_t seg = blk / tiles;
+  const int64_t tile = blk % tiles;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -88,8 +93,16 @@ __global__ void __launch_bounds__(kSortThreads)
     const int l = tid % kMaxLevels, g = tid / kMaxLevels;
     uint32_t b = 0;
     if (l < levels) {
+      // Independent loads in batches, so their latencies overlap.
+      constexpr int kBatch = 4;
       const uint32_t* c = cnt + seg * tiles * kMaxLevels + l;
-      for (int64_t t = g; t < tile; t += kGroups) b += c[t * kMaxLevels];
+      for (int64_t t = g; t < tile; t += kBatch * kGroups) {
+        uint32_t x[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) x[j] = t + j * kGroups < tile ? c[(t + j * kGroups) * kMaxLevels] : 0u;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) b += x[j];
+      }
     }
     s_before[g][l] = b;
   }
