@@ -61,6 +61,8 @@
 #include "select_device.h"
 #include "tile_device.h"
 
+#include <type_traits>
+
 namespace zeta {
 namespace {
 
@@ -186,7 +188,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
     uint32_t key = 0;
     int64_t seg = 0;
     if (slot < total) {
-      seg = slot / N;
+      seg = int64_t(uint32_t(slot) / uint32_t(N));  // slots < B*H*N < 2^31
       const int64_t ii = order != nullptr ? int64_t(order[slot]) : slot - seg * N;
       if (ii >= 0 && ii < N) {
         my_i = int32_t(ii);
@@ -343,6 +345,113 @@ __global__ void __launch_bounds__(256)
 
 // ---- attention over the windows ----------------------------------------------
 
+// Value rows reach the matrix cores through LDS.  Per chunk of 16 entries the
+// wavefront copies the 16 value rows straight from global memory into LDS
+// (global_load_lds_dwordx4: lane L's 16 bytes land at byte 16 L of the
+// instruction's 1 KiB), then reads each product's A operand with one
+// transposing LDS read (ds_read_b64_tr_b16: within each group of 16 lanes,
+// output lane i receives element i % 4 of the 8-byte reads of lanes
+// 4j + i / 4, j = 0..3).  With lane (g, s) of a group pointing at entry row
+// 4g + s / 4, columns 16 blk + 4 (s % 4) .. + 3, output lane i holds column
+// 16 blk + i of entries 4g .. 4g + 3: the A operand (value columns x
+// entries) of a 16 x 16 x 16 product, with no register shuffling (the kernel
+// repeats it in the upper K half of a 16 x 16 x 32 product, against the low
+// score parts).
+//
+// LDS row order.  One copy instruction fills R = 512 / d_v consecutive LDS
+// rows (P = d_v / 8 pieces of 16 bytes each).  For d_v <= 128 the lanes that
+// fill one LDS row share a tile-entry group kg, so each lane copies one of its
+// own 4 entries (whose position it already holds): LDS row
+// rho = j R + q (instruction j, q = lane / P) holds entry
+// 4 kg + j (16 / P) + q % (16 / P).  For d_v = 256 row rho holds entry rho.
+// Pieces are XOR-swizzled by row (sw below): physical piece p of row rho
+// holds logical piece p ^ sw(rho), so that the transposing reads are free of
+// bank conflicts.
+// E transposing LDS reads (ds_read_b64_tr_b16) at addr[j] + kOff, issued
+// once the copies into LDS made before the last kPending copy instructions
+// have landed (kPending -1: no wait here); read_tr_wait then waits for the
+// results.  Written as inline
+// assembly, with the waits, because the compiler would otherwise wait for
+// every copy still in flight (including the next chunk's, which must keep
+// loading meanwhile) before any such read.  LDS operations of one wavefront
+// complete in order, so the compiler's own waits on its later LDS reads stay
+// correct with these older ones in flight.
+template <int E, uint32_t kOff, int kPending>
+__device__ __forceinline__ void read_tr_issue(const uint32_t (&addr)[E], s16x4_t (&a)[E]) {
+  static_assert(kPending >= -1 && kPending < 16, "vmcnt immediate (-1: no wait)");
+  if constexpr (kPending >= 0) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kPending) : "memory");
+#pragma unroll
+  for (int j = 0; j < E; ++j)
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(a[j]) : "v"(addr[j]), "n"(kOff) : "memory");
+}
+
+template <int E>
+__device__ __forceinline__ void read_tr_wait(s16x4_t (&a)[E]) {
+  if constexpr (E == 2) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1])::"memory");
+  } else if constexpr (E == 4) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3])::"memory");
+  } else if constexpr (E == 8) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(a[4]), "+v"(a[5]), "+v"(a[6]), "+v"(a[7])::
+                     "memory");
+  } else {
+    static_assert(E == 16, "d_v must be 32, 64, 128 or 256");
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(a[4]), "+v"(a[5]), "+v"(a[6]), "+v"(a[7]),
+                   "+v"(a[8]), "+v"(a[9]), "+v"(a[10]), "+v"(a[11]), "+v"(a[12]), "+v"(a[13]), "+v"(a[14]),
+                   "+v"(a[15])::"memory");
+  }
+}
+
+template <int DV>
+struct VStage {
+  static constexpr int kRowBytes = 2 * DV;
+  static constexpr int kP = DV / 8;                   // 16-byte pieces per row
+  static constexpr int kR = 64 / kP;                  // LDS rows per copy instruction
+  static constexpr int kLoads = kChunk / kR;          // copy instructions per chunk
+  static constexpr int kOwn = kP <= 16 ? 16 / kP : 0; // rows of one entry group per instruction
+  static constexpr int kBlocks = DV / 16;             // products (16 value columns each) per chunk
+  static constexpr int kBytes = kChunk * kRowBytes;   // one chunk's rows
+  static_assert(kR >= 2 && kChunk % kR == 0, "d_v must be 32, 64, 128 or 256");
+  // Piece swizzle of LDS row rho.  A transposing read is served in two
+  // halves of 32 lanes (entry groups kg = 0, 1 and kg = 2, 3), each reading
+  // 256 bytes: the 16 (row, piece) pairs of one half must fall in 16
+  // different 16-byte bank groups.  Row rho's bank group is set by the row's
+  // offset within 256 bytes and the physical piece; the swizzle puts the
+  // row bits that the offset does not separate into the piece bits that the
+  // block index leaves free.
+  __device__ static constexpr int sw(int rho) {
+    if constexpr (kP == 16) {  // rho = 4u + kg: u into piece bits 2-3, kg's low bit into bit 1
+      return (rho & 12) | ((rho & 1) << 1);
+    } else if constexpr (kP == 8) {  // rho = 8(u >> 1) + 2kg + (u & 1)
+      return (((rho >> 1) & 1) << 1) | (((rho >> 3) & 1) << 2);
+    } else if constexpr (kP == 4) {  // rho = 4kg + u
+      return ((rho >> 2) & 1) << 1;
+    } else {  // kP == 32, rho = 4kg + u
+      return ((rho & 3) << 1) | (((rho >> 2) & 1) << 3);
+    }
+  }
+  // Chunk entry held by LDS row rho.
+  __device__ static constexpr int entry_of_row(int rho) {
+    if constexpr (kP > 16) {
+      return rho;
+    } else {
+      const int j = rho / kR, q = rho % kR;
+      return 4 * (q / kOwn) + j * kOwn + q % kOwn;
+    }
+  }
+  // LDS row holding chunk entry e.
+  __device__ static constexpr int row_of_entry(int e) {
+    if constexpr (kP > 16) {
+      return e;
+    } else {
+      const int kg = e / 4, u = e % 4;
+      return (u / kOwn) * kR + kg * kOwn + u % kOwn;
+    }
+  }
+};
+
 template <int DV, int DK, bool kOff32, bool kHist, int kMode>
 __global__ void __launch_bounds__(kTileWaves * 64)
     __attribute__((amdgpu_waves_per_eu((DV <= 128 && kMode != kScoreCauchy) ? 3 : 1)))
@@ -353,12 +462,14 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                               const uint2* __restrict__ keys_list, int64_t total, int64_t N, int dk_rt, int causal,
                               int chunk, int t0, int t_hi, int64_t cap, float eps,
                               const float* __restrict__ mk, const float* __restrict__ mv, uint16_t* __restrict__ out) {
-  constexpr int E = DV / 16;  // value elements per lane and row; also product blocks per chunk
-  constexpr int W = E / 2;    // 32-bit words per lane and row
+  using VS = VStage<DV>;
+  constexpr int E = VS::kBlocks;  // products per chunk; a lane ends with 4 columns of each block
   constexpr int KD = DK > 0 ? DK : kMaxDk;
-  constexpr int kStageEntries = DK == 3 ? 512 : 128;  // entries whose positions and key rows are staged at once
+  // Entries whose key rows and positions are staged at once (LDS per wave:
+  // these plus two chunks of value rows).
+  constexpr int kStageEntries = (DK == 3 && DV <= 128) ? 320 : 128;
   constexpr int kStage = kStageEntries / kChunk;
-  static_assert(E >= 2 && E % 2 == 0, "d_v must be a multiple of 32");
+  static_assert(E >= 2, "d_v must be a multiple of 32");
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
   // Score (compile time): the Cauchy score, or a variant (softmax variants
@@ -370,18 +481,43 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   constexpr bool smax = kVar && score_is_softmax(kMode);
   const float rsd = 1.0f / sqrtf(float(dk));
 
-  // Key rows padded to a multiple of 4 floats, so 4 consecutive entries'
-  // positions and each key row are whole 16-byte LDS reads.
+  // One record per staged entry: its key row, then its position (as the bits
+  // of a float), padded to whole 16-byte LDS reads; for d_k = 3 one read
+  // (x, y, z, position).
   constexpr int KD4 = (KD + 3) / 4 * 4;
-  __shared__ __align__(16) int32_t s_pos[kTileWaves][kStageEntries];
-  __shared__ __align__(16) float s_k[kTileWaves][kStageEntries][KD4];
+  constexpr int kPosSlot = DK == 3 ? 3 : KD4;
+  constexpr int KREC = DK == 3 ? 4 : KD4 + 4;
+  __shared__ __align__(16) float s_ent[kTileWaves][kStageEntries][KREC];
+  // Two chunks of value rows per wave (even chunks, then odd chunks).
+  __shared__ __align__(16) unsigned char s_v[kTileWaves][2 * VS::kBytes];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int qn = lane & (kTileQ - 1);  // this lane's query in the tile; also its value column in a block
+  // Wave-uniform (the LDS destination of a copy instruction must be).
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+  const int qn = lane & (kTileQ - 1);  // this lane's query in the tile
   const int kg = lane >> 4;            // this lane's entries in a chunk: 4kg .. 4kg+3
   const int64_t tiles = (total + kTileQ - 1) / kTileQ;
   const int64_t nb = gridDim.x;
+
+  // Copy instruction j: this lane's LDS row, and its byte offset within the
+  // value row it copies (its piece, swizzled).
+  const int vq = lane / VS::kP, vp = lane % VS::kP;
+  uint32_t copy_off[VS::kLoads];
+#pragma unroll
+  for (int j = 0; j < VS::kLoads; ++j) copy_off[j] = uint32_t(16 * (vp ^ VS::sw(j * VS::kR + vq)));
+  // Transposing read of block blk: this lane points at entry 4kg + qn / 4,
+  // columns 16 blk + 4 (qn % 4) .. +3 (LDS address in the wave's even-chunk
+  // buffer; the odd-chunk buffer follows it).
+  uint32_t tr_addr[E];
+  {
+    const int rho = VS::row_of_entry(4 * kg + qn / 4);
+    const int x = (qn % 4) / 2, half = qn % 2;
+    const uint32_t base = uint32_t(reinterpret_cast<uintptr_t>(
+        (const __attribute__((address_space(3))) unsigned char*)(&s_v[wave][0])));
+#pragma unroll
+    for (int blk = 0; blk < E; ++blk)
+      tr_addr[blk] = base + uint32_t(rho * VS::kRowBytes + 16 * ((2 * blk + x) ^ VS::sw(rho)) + 8 * half);
+  }
 
   for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kTileWaves < tiles; blk += nb) {
     const int64_t tile = blk * kTileWaves + wave;
@@ -395,7 +531,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
     {
       const int64_t sl = tile * kTileQ + qn;
       if (sl < total) {
-        const int64_t sg = sl / N;
+        const int64_t sg = int64_t(uint32_t(sl) / uint32_t(N));  // slots < B*H*N < 2^31
         const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
         if (ii >= 0 && ii < N) {
           my_i = int32_t(ii);
@@ -445,6 +581,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         for (int a = 0; a < KD; ++a) qv[a] = 0.0f;
       }
 
+      // acc[blk]: value columns 16 blk + 4kg .. 16 blk + 4kg + 3 of query qn.
       f32x4_t acc[E];
 #pragma unroll
       for (int j = 0; j < E; ++j) acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
@@ -453,8 +590,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       const float qnorm = (kVar && score == kScoreNormDot) ? row_norm<KD>(qv, dk) : 0.0f;
       // The history-mean candidate starts the sums, in float32: its score
       // (counted once, by the kg = 0 lanes) and its weighted mean value in
-      // this lane's output elements kg*4E .. kg*4E + 4E - 1.  Under a softmax
-      // variant its logit starts the running maximum and its weight is 1.
+      // this lane's output columns.  Under a softmax variant its logit
+      // starts the running maximum and its weight is 1.
       if constexpr (kHist) {
         if (in_grp) {
           const int64_t gq = g_seg * N + my_i;
@@ -472,23 +609,16 @@ __global__ void __launch_bounds__(kTileWaves * 64)
             s_mean = mean_score<KD>(mk, gq, dk, qv, eps);
           }
           if (kg == 0) zpart = s_mean;
-          const float* mrow = mv + gq * DV + kg * 4 * E;
+          const float* mrow = mv + gq * DV + 4 * kg;
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < E; j += 4) {
-              const float4 m = *reinterpret_cast<const float4*>(mrow + i * E + j);
-              acc[j][i] = s_mean * m.x;
-              acc[j + 1][i] = s_mean * m.y;
-              acc[j + 2][i] = s_mean * m.z;
-              acc[j + 3][i] = s_mean * m.w;
-            }
+          for (int j = 0; j < E; ++j) {
+            const float4 m = *reinterpret_cast<const float4*>(mrow + 16 * j);
+            acc[j] = f32x4_t{s_mean * m.x, s_mean * m.y, s_mean * m.z, s_mean * m.w};
+          }
         }
       }
-      const uint16_t* vseg = v + g_seg * N * DV;
-      const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(vseg);
+      const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(v + g_seg * N * DV);
       const uint16_t* kseg = k + g_seg * N * dk;
-      const Off col = Off(qn * E);
 
       // Window and pool tests as single unsigned compares: entry r is in the
       // window when r - a <= b - a, its position in the pool when
@@ -498,51 +628,61 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       const int32_t a_eff = mine ? my_a : INT32_MIN;
       const uint32_t lim_u = uint32_t(my_lim);
 
-      // Scores of this lane's 4 entries of staged chunk `ch` for its query,
-      // split into bfloat16 parts, and the loads of the entries' value rows.
-      // Branch-free, so that loads in flight can be counted across chunks: a
-      // chunk index at or past nch scores nothing, and every lane loads a
-      // row (a missing entry reads row 0, finite by contract; a row no query
-      // takes has weight 0).  The reciprocal is the hardware one (1 ulp).  A
-      // score s is split as hi = bf16(s) and lo = bf16(s - hi), both rounded
-      // to nearest even; s - hi is exact, so hi + lo is within 2^-17 of s.
-      auto prep = [&](int cb, int ch, int nch_, uint32_t(&raw)[4][W], uint32_t(&bh)[2], uint32_t(&bl)[2],
-                      float& scl) {
-        const bool live = ch < nch_;
-        const int chc = live ? ch : 0;
-        const int32_t r0 = (cb + chc) * kChunk;
-        float sc[4];
-        int32_t pvs[4];
-        {
-          const int4 p4 = *reinterpret_cast<const int4*>(&s_pos[wave][chc * kChunk + kg * 4]);
-          pvs[0] = p4.x;
-          pvs[1] = p4.y;
-          pvs[2] = p4.z;
-          pvs[3] = p4.w;
-        }
-        // The entries' value rows first (a wave-uniform base and a 32-bit byte
-        // offset per lane when the segment's values span under 4 GiB, so no
-        // 64-bit address arithmetic), kept ahead of the scoring and of the
-        // previous chunk's products so that they load while those run.
+      // Positions of this lane's 4 entries of staged chunk ch.
+      auto entry_pos = [&](int ch, int32_t(&pvs)[4]) {
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const Off boff = (Off(pvs[kk]) * Off(DV) + col) * Off(2);
-          load_words<W>(reinterpret_cast<const uint16_t*>(vbytes + boff), raw[kk]);
+        for (int kk = 0; kk < 4; ++kk) pvs[kk] = __float_as_int(s_ent[wave][ch * kChunk + kg * 4 + kk][kPosSlot]);
+      };
+      // Copy the value rows of staged chunk ch into LDS buffer `buf` (every
+      // lane copies one piece of one row per instruction; a missing entry
+      // reads row 0, finite by contract, and has weight 0).
+      auto copy_rows = [&](int ch, unsigned char* buf, const int32_t(&pvs)[4]) {
+#pragma unroll
+        for (int j = 0; j < VS::kLoads; ++j) {
+          int32_t pv;
+          if constexpr (VS::kP > 16) {
+            pv = __float_as_int(s_ent[wave][ch * kChunk + VS::entry_of_row(j * VS::kR + vq)][kPosSlot]);
+          } else {
+            // Entry 4kg + j*kOwn + vq % kOwn: one of this lane's own four.
+            const int u0 = j * VS::kOwn;
+            if constexpr (VS::kOwn == 1) {
+              pv = pvs[u0];
+            } else {
+              const int r = vq % VS::kOwn;
+              pv = pvs[u0];
+#pragma unroll
+              for (int t = 1; t < VS::kOwn; ++t) pv = r == t ? pvs[u0 + t] : pv;
+            }
+          }
+          const Off boff = Off(pv) * Off(VS::kRowBytes) + Off(copy_off[j]);
+          __builtin_amdgcn_global_load_lds(
+              (const __attribute__((address_space(1))) void*)(vbytes + boff),
+              (__attribute__((address_space(3))) void*)(buf + 1024 * j), 16, 0, 0);
         }
-        __builtin_amdgcn_sched_barrier(0);
-        const float* krow = &s_k[wave][chc * kChunk + kg * 4][0];
+      };
+      // Scores of this lane's 4 entries of staged chunk ch for its query,
+      // split into bfloat16 parts.  The reciprocal is the hardware one
+      // (1 ulp).  A score s is split as hi = bf16(s) and lo = bf16(s - hi),
+      // both rounded to nearest even; s - hi is exact, so hi + lo is within
+      // 2^-17 of s.
+      auto score4 = [&](int cb, int ch, uint32_t(&bh)[2], uint32_t(&bl)[2], float& scl) {
+        const int32_t r0 = (cb + ch) * kChunk;
+        float sc[4];
+        const float* krow = &s_ent[wave][ch * kChunk + kg * 4][0];
+        int32_t pvs[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) pvs[kk] = __float_as_int(krow[kk * KREC + kPosSlot]);
         scl = 1.0f;
         if constexpr (!kVar) {
 #pragma unroll
           for (int kk = 0; kk < 4; ++kk) {
             const int32_t r = r0 + kg * 4 + kk;
-            const int32_t pv = pvs[kk];
-            const bool in = live && uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pv) <= lim_u;
+            const bool in = uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
             float d2 = 0.0f;
 #pragma unroll
             for (int a = 0; a < KD; ++a) {
               if (a < dk) {
-                const float diff = qv[a] - krow[kk * KD4 + a];
+                const float diff = qv[a] - krow[kk * KREC + a];
                 d2 = fmaf(diff, diff, d2);
               }
             }
@@ -551,15 +691,14 @@ __global__ void __launch_bounds__(kTileWaves * 64)
             zpart += sc[kk];
           }
         } else {
-          // Rounded as written: this lambda is inlined at several call sites,
-          // and a chunk's site depends on where its run starts.
+          // Rounded as written: this lambda is inlined at several call sites.
 #pragma clang fp contract(off)
           bool ins[4];
 #pragma unroll
           for (int kk = 0; kk < 4; ++kk) {
             const int32_t r = r0 + kg * 4 + kk;
-            ins[kk] = live && uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
-            sc[kk] = variant_term<KD>(score, qv, krow + kk * KD4, dk, eps, rsd, qnorm);
+            ins[kk] = uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
+            sc[kk] = variant_term<KD>(score, qv, krow + kk * KREC, dk, eps, rsd, qnorm);
           }
           if (smax) {
             // Online softmax: the chunk's largest logit of the query (its 4
@@ -594,34 +733,34 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           bl[t] = __builtin_bit_cast(uint32_t, l);
         }
       };
-      // acc[j] += V^T (block j) * S^T for one chunk, high and low score parts
-      // in one 16x16x32 product: a lane's eight K slots hold its 4 entries'
-      // values twice, against their high and then their low score parts (A
-      // and B slots correspond lane by lane, so the sum pairs each value with
-      // both parts of its own score).
-      auto mma = [&](const uint32_t(&raw)[4][W], const uint32_t(&bh)[2], const uint32_t(&bl)[2], float scl) {
+      // acc[blk] += V^T (columns 16 blk .. +15 x the chunk's 16 entries) *
+      // S^T (entries x queries), the high then the low score parts; `a`
+      // holds the chunk's transposing reads, issued before its scoring.
+      auto mma = [&](s16x4_t(&a)[E], const uint32_t(&bh)[2], const uint32_t(&bl)[2], float scl) {
         // Softmax variants: the sums so far to the chunk's running maximum.
         if (smax && wave_ballot(scl != 1.0f) != 0ull) {
 #pragma unroll
           for (int j = 0; j < E; ++j) acc[j] *= scl;
         }
+        // One 16 x 16 x 32 product per block: its 32 K slots hold the 4
+        // entries' values twice (A: the read fragment, duplicated) against
+        // their high, then their low score parts (B).
         Frag8 b;
         b.w[0] = bh[0];
         b.w[1] = bh[1];
         b.w[2] = bl[0];
         b.w[3] = bl[1];
+        read_tr_wait<E>(a);
 #pragma unroll
         for (int j = 0; j < E; ++j) {
-          Frag8 a;
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-            // One byte permute: element j of two consecutive rows, x below y
-            // (the low halves for even j, the high halves for odd j).
-            const uint32_t x = raw[2 * t][j >> 1], y = raw[2 * t + 1][j >> 1];
-            a.w[t] = __builtin_amdgcn_perm(y, x, (j & 1) ? 0x07060302u : 0x05040100u);
-            a.w[t + 2] = a.w[t];
-          }
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc[j], 0, 0, 0);
+          Frag fa;
+          fa.v = a[j];
+          Frag8 a8;
+          a8.w[0] = fa.w[0];
+          a8.w[1] = fa.w[1];
+          a8.w[2] = fa.w[0];
+          a8.w[3] = fa.w[1];
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8.v, b.v, acc[j], 0, 0, 0);
         }
       };
 
@@ -630,6 +769,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // per tile), each run kStage chunks at a time.
       const int a_ch = mine ? my_a / kChunk : INT32_MAX;
       const int b_ch = mine ? my_b / kChunk : INT32_MIN;
+      unsigned char* const v0 = s_v[wave];
+      unsigned char* const v1 = s_v[wave] + VS::kBytes;
       for (int c = wave_min_int(a_ch); c != INT32_MAX;) {
         // Extend the run to the last chunk of every window that starts in it
         // or right after it.
@@ -672,55 +813,72 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                   for (int a = 0; a < KD; ++a)
                     kv[a] = a < dk ? bf16_bits_to_float(kseg[int64_t(pv[t]) * dk + a]) : 0.0f;
                 }
-                s_pos[wave][e_] = pv[t];
+                if constexpr (DK == 3) {
+                  *reinterpret_cast<float4*>(&s_ent[wave][e_][0]) = make_float4(kv[0], kv[1], kv[2], __int_as_float(pv[t]));
+                } else {
 #pragma unroll
-                for (int a = 0; a < KD4; a += 4)
-                  *reinterpret_cast<float4*>(&s_k[wave][e_][a]) =
-                      make_float4(kv[a], a + 1 < KD ? kv[a + 1] : 0.0f, a + 2 < KD ? kv[a + 2] : 0.0f,
-                                  a + 3 < KD ? kv[a + 3] : 0.0f);
+                  for (int a = 0; a < KD4; a += 4)
+                    *reinterpret_cast<float4*>(&s_ent[wave][e_][a]) =
+                        make_float4(kv[a], a + 1 < KD ? kv[a + 1] : 0.0f, a + 2 < KD ? kv[a + 2] : 0.0f,
+                                    a + 3 < KD ? kv[a + 3] : 0.0f);
+                  s_ent[wave][e_][kPosSlot] = __int_as_float(pv[t]);
+                }
               }
             }
           }
           wave_lds_sync();
 
-          // Value rows of chunk ch+1 load while chunk ch is multiplied.
-          uint32_t rA[4][W], rB[4][W], hA[2], lA[2], hB[2], lB[2];
-          float sA, sB;
-          prep(cb, 0, nch, rA, hA, lA, sA);
+          // Chunk ch+1's value rows are copied while chunk ch is scored and
+          // multiplied (even chunks in v0, odd chunks in v1).
+          // Past the stage's last chunk the other buffer receives a copy of
+          // the current chunk's rows again, so that exactly one chunk's
+          // copies are always in flight behind the one being read.
+          // Chunk ch's transposing reads are issued before its scoring and
+          // waited for after it.
+          int32_t pv4[4];
+          uint32_t bh[2], bl[2];
+          float scl;
+          s16x4_t a[E];
+          entry_pos(0, pv4);
+          copy_rows(0, v0, pv4);
           for (int ch = 0; ch < nch; ch += 2) {
-            prep(cb, ch + 1, nch, rB, hB, lB, sB);
-            mma(rA, hA, lA, sA);
+            const int c1 = ch + 1 < nch ? ch + 1 : ch;
+            entry_pos(c1, pv4);
+            copy_rows(c1, v1, pv4);
+            read_tr_issue<E, 0, VS::kLoads>(tr_addr, a);
+            score4(cb, ch, bh, bl, scl);
+            mma(a, bh, bl, scl);
             if (ch + 1 >= nch) break;
-            prep(cb, ch + 2, nch, rA, hA, lA, sA);
-            mma(rB, hB, lB, sB);
+            const int c2 = ch + 2 < nch ? ch + 2 : ch + 1;
+            entry_pos(c2, pv4);
+            copy_rows(c2, v0, pv4);
+            read_tr_issue<E, VS::kBytes, VS::kLoads>(tr_addr, a);
+            score4(cb, ch + 1, bh, bl, scl);
+            mma(a, bh, bl, scl);
           }
+          // Every copy has landed before the buffers are refilled.
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
           wave_lds_sync();
         }
         c = wave_min_int(a_ch > e ? a_ch : INT32_MAX);
       }
 
-      // Normalise and store: lane holds columns 4kg..4kg+3 of every block,
-      // i.e. value elements 4kg*E .. 4kg*E + 4E - 1 of query qn.
+      // Normalise and store: lane holds columns 16 blk + 4kg .. + 3 of
+      // query qn for every block.
       float z = zpart;
       z += __shfl_xor(z, 16, 64);
       z += __shfl_xor(z, 32, 64);
       if (in_grp) {
         const float inv = z > 0.0f ? 1.0f / z : 0.0f;
-        float o[4 * E];
+        uint16_t* orow = out + (g_seg * N + my_i) * int64_t(DV) + 4 * kg;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < E; ++j) o[i * E + j] = acc[j][i] * inv;
-        // Rounded to bfloat16 (nearest even), two values per conversion.
-        uint32_t w[2 * E];
-#pragma unroll
-        for (int t = 0; t < 2 * E; ++t) {
-          const bf16x2_t pr = {(__bf16)o[2 * t], (__bf16)o[2 * t + 1]};
-          w[t] = __builtin_bit_cast(uint32_t, pr);
+        for (int j = 0; j < E; ++j) {
+          // Rounded to bfloat16 (nearest even), two values per conversion.
+          const bf16x2_t p0 = {(__bf16)(acc[j][0] * inv), (__bf16)(acc[j][1] * inv)};
+          const bf16x2_t p1 = {(__bf16)(acc[j][2] * inv), (__bf16)(acc[j][3] * inv)};
+          *reinterpret_cast<uint2*>(orow + 16 * j) =
+              make_uint2(__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1));
         }
-        uint4* dst = reinterpret_cast<uint4*>(out + (g_seg * N + my_i) * int64_t(DV) + kg * 4 * E);
-#pragma unroll
-        for (int t = 0; t < 2 * E; t += 4) dst[t / 4] = make_uint4(w[t], w[t + 1], w[t + 2], w[t + 3]);
       }
     }
   }

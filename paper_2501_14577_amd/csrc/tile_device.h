@@ -24,23 +24,27 @@ union Frag8 {  // eight bfloat16 values
   bf16x8_t v;
 };
 
-__device__ __forceinline__ int wave_min_int(int x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const int y = __shfl_xor(x, off, 64);
-    x = y < x ? y : x;
-  }
-  return __builtin_amdgcn_readfirstlane(x);
+// Minimum / maximum over the wavefront, read by every lane: within each row
+// of 16 lanes by four DPP exchanges (swap neighbours, swap pairs, mirror the
+// half row, mirror the row), then rows 1 and 3 take row 0's and row 2's
+// result (row_bcast:15) and rows 2 and 3 take lane 31's (row_bcast:31), so
+// lane 63 holds the wavefront's result.  No LDS round trip (unlike a
+// shuffle through ds_bpermute).
+template <bool kMax>
+__device__ __forceinline__ int wave_reduce_minmax(int x) {
+  auto op = [](int a, int b) { return kMax ? (a > b ? a : b) : (a < b ? a : b); };
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));  // row_mirror
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false));  // row_bcast:15 into rows 1, 3
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x143, 0xC, 0xF, false));  // row_bcast:31 into rows 2, 3
+  return __builtin_amdgcn_readlane(x, 63);
 }
 
-__device__ __forceinline__ int wave_max_int(int x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const int y = __shfl_xor(x, off, 64);
-    x = y > x ? y : x;
-  }
-  return __builtin_amdgcn_readfirstlane(x);
-}
+__device__ __forceinline__ int wave_min_int(int x) { return wave_reduce_minmax<false>(x); }
+
+__device__ __forceinline__ int wave_max_int(int x) { return wave_reduce_minmax<true>(x); }
 
 // Lane `src`'s value of a pointer, read by every lane.  Each 32-bit half goes
 // through uint32_t: widening a negative int32 would sign-extend into the
