@@ -367,41 +367,36 @@ __global__ void __launch_bounds__(256)
 // Pieces are XOR-swizzled by row (sw below): physical piece p of row rho
 // holds logical piece p ^ sw(rho), so that the transposing reads are free of
 // bank conflicts.
-// E transposing LDS reads (ds_read_b64_tr_b16) at addr[j] + kOff, issued
-// once the copies into LDS made before the last kPending copy instructions
-// have landed (kPending -1: no wait here); read_tr_wait then waits for the
-// results.  Written as inline
-// assembly, with the waits, because the compiler would otherwise wait for
-// every copy still in flight (including the next chunk's, which must keep
-// loading meanwhile) before any such read.  LDS operations of one wavefront
-// complete in order, so the compiler's own waits on its later LDS reads stay
-// correct with these older ones in flight.
-template <int E, uint32_t kOff, int kPending>
-__device__ __forceinline__ void read_tr_issue(const uint32_t (&addr)[E], s16x4_t (&a)[E]) {
+// Transposing LDS reads (ds_read_b64_tr_b16) at addr[j] + kOff, kCopies of
+// each (into a[kCopies j] .. a[kCopies j + kCopies - 1]), issued once the
+// copies into LDS made before the last kPending copy instructions have landed
+// (kPending -1: no wait here); read_tr_wait then waits for the results.
+// Written as inline assembly, with the waits, because the compiler would
+// otherwise wait for every copy still in flight (including the next chunk's,
+// which must keep loading meanwhile) before any such read.  LDS operations of
+// one wavefront complete in order, so the compiler's own waits on its later
+// LDS reads stay correct with these older ones in flight.
+template <int E, int kCopies, uint32_t kOff, int kPending>
+__device__ __forceinline__ void read_tr_issue(const uint32_t (&addr)[E], s16x4_t (&a)[E * kCopies]) {
   static_assert(kPending >= -1 && kPending < 16, "vmcnt immediate (-1: no wait)");
   if constexpr (kPending >= 0) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kPending) : "memory");
 #pragma unroll
   for (int j = 0; j < E; ++j)
-    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(a[j]) : "v"(addr[j]), "n"(kOff) : "memory");
+#pragma unroll
+    for (int c = 0; c < kCopies; ++c)
+      asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                   : "=v"(a[kCopies * j + c])
+                   : "v"(addr[j]), "n"(kOff)
+                   : "memory");
 }
 
-template <int E>
-__device__ __forceinline__ void read_tr_wait(s16x4_t (&a)[E]) {
-  if constexpr (E == 2) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1])::"memory");
-  } else if constexpr (E == 4) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3])::"memory");
-  } else if constexpr (E == 8) {
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(a[4]), "+v"(a[5]), "+v"(a[6]), "+v"(a[7])::
-                     "memory");
-  } else {
-    static_assert(E == 16, "d_v must be 32, 64, 128 or 256");
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(a[4]), "+v"(a[5]), "+v"(a[6]), "+v"(a[7]),
-                   "+v"(a[8]), "+v"(a[9]), "+v"(a[10]), "+v"(a[11]), "+v"(a[12]), "+v"(a[13]), "+v"(a[14]),
-                   "+v"(a[15])::"memory");
-  }
+// Waits for every LDS read of this wavefront; the reads' results are then
+// used only after the wait (each passes through an ordered empty statement).
+template <int N>
+__device__ __forceinline__ void read_tr_wait(s16x4_t (&a)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0])::"memory");
+#pragma unroll
+  for (int j = 1; j < N; ++j) asm volatile("" : "+v"(a[j]));
 }
 
 template <int DV>
@@ -454,7 +449,7 @@ struct VStage {
 
 template <int DV, int DK, bool kOff32, bool kHist, int kMode>
 __global__ void __launch_bounds__(kTileWaves * 64)
-    __attribute__((amdgpu_waves_per_eu((DV <= 128 && kMode != kScoreCauchy) ? 3 : 1)))
+    __attribute__((amdgpu_waves_per_eu((kOff32 && (DV == 128 || (DV < 128 && kMode != kScoreCauchy))) ? 3 : 1)))
     select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                               const uint16_t* __restrict__ v, const int32_t* __restrict__ sorted_pos,
                               const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order,
@@ -470,6 +465,9 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   constexpr int kStageEntries = (DK == 3 && DV <= 128) ? 320 : 128;
   constexpr int kStage = kStageEntries / kChunk;
   static_assert(E >= 2, "d_v must be a multiple of 32");
+  // Each A fragment is read from LDS twice (both K halves of a product) where
+  // the registers allow it, else read once and copied.
+  constexpr int kTrCopies = (DV <= 128 && kOff32) ? 2 : 1;
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
   // Score (compile time): the Cauchy score, or a variant (softmax variants
@@ -519,9 +517,26 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       tr_addr[blk] = base + uint32_t(rho * VS::kRowBytes + 16 * ((2 * blk + x) ^ VS::sw(rho)) + 8 * half);
   }
 
-  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kTileWaves < tiles; blk += nb) {
+  // The processing-order entry and window bounds of this lane's slot in a
+  // tile, loaded one tile ahead: they arrive while the tile before is
+  // processed.
+  int32_t nx_o = 0;
+  int2 nx_b = make_int2(0, -1);
+  auto fetch_slot = [&](int64_t t_) {
+    const int64_t sl = t_ * kTileQ + qn;
+    if (sl < total) {
+      if (order != nullptr) nx_o = order[sl];
+      nx_b = bounds[sl];
+    }
+  };
+  const int64_t blk0 = xcd_contiguous_block(blockIdx.x, nb);
+  fetch_slot(blk0 * kTileWaves + wave);
+  for (int64_t blk = blk0; blk * kTileWaves < tiles; blk += nb) {
     const int64_t tile = blk * kTileWaves + wave;
     if (tile >= tiles) continue;
+    const int32_t cur_o = nx_o;
+    const int2 cur_b = nx_b;
+    fetch_slot(tile + nb * kTileWaves);
 
     // The tile's queries and windows: lanes with equal qn hold the same one.
     int32_t my_i = -1;
@@ -532,18 +547,20 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       const int64_t sl = tile * kTileQ + qn;
       if (sl < total) {
         const int64_t sg = int64_t(uint32_t(sl) / uint32_t(N));  // slots < B*H*N < 2^31
-        const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
+        const int64_t ii = order != nullptr ? int64_t(cur_o) : sl - sg * N;
         if (ii >= 0 && ii < N) {
           my_i = int32_t(ii);
           my_seg = sg;
           my_lvl = causal ? pool_level(pool_limit(my_i, chunk), t0, t_hi) : 0;
-          const int2 bb = bounds[sl];
-          my_a = bb.x;
-          my_b = bb.y;
+          my_a = cur_b.x;
+          my_b = cur_b.y;
         }
       }
     }
     uint32_t pending = uint32_t(wave_ballot(my_i >= 0)) & 0xFFFFu;
+    // d_k = 3 (Cauchy score, no history candidate): the query row is read
+    // with the staged entries, so that one wait covers both.
+    constexpr bool kLateQ = DK == 3 && !kVar && !kHist;
 
     // Queries that search one list form a group (nearly always the whole tile).
     while (pending != 0u) {
@@ -569,7 +586,10 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       const bool mine = in_grp && 0 <= my_a && my_a <= my_b && my_b < ln;
       const int32_t my_lim = causal ? pool_limit(my_i, chunk) : int32_t(N - 1);
       float qv[KD];
-      if (kHist ? in_grp : mine) {
+      if constexpr (kLateQ) {
+#pragma unroll
+        for (int a = 0; a < KD; ++a) qv[a] = 0.0f;
+      } else if (kHist ? in_grp : mine) {
         if constexpr (DK == 3) {
           Row3<uint16_t>::load(q, g_seg * N + my_i, total, qv);
         } else {
@@ -678,7 +698,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           for (int kk = 0; kk < 4; ++kk) {
             const int32_t r = r0 + kg * 4 + kk;
             const bool in = uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
-            float d2 = 0.0f;
+            // eps + the squared distance, eps first (one addition fewer).
+            float d2 = eps;
 #pragma unroll
             for (int a = 0; a < KD; ++a) {
               if (a < dk) {
@@ -686,7 +707,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                 d2 = fmaf(diff, diff, d2);
               }
             }
-            const float rc = __builtin_amdgcn_rcpf(d2 + eps);
+            const float rc = __builtin_amdgcn_rcpf(d2);
             sc[kk] = in ? rc : 0.0f;
             zpart += sc[kk];
           }
@@ -726,7 +747,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const bf16x2_t h = {(__bf16)sc[2 * t], (__bf16)sc[2 * t + 1]};
-          const uint32_t hw = __builtin_bit_cast(uint32_t, h);
+          uint32_t hw = __builtin_bit_cast(uint32_t, h);
+          asm("" : "+v"(hw));  // the packed pair, reused as is (one conversion)
           const bf16x2_t l = {(__bf16)(sc[2 * t] - __uint_as_float(hw << 16)),
                               (__bf16)(sc[2 * t + 1] - __uint_as_float(hw & 0xFFFF0000u))};
           bh[t] = hw;
@@ -736,31 +758,27 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // acc[blk] += V^T (columns 16 blk .. +15 x the chunk's 16 entries) *
       // S^T (entries x queries), the high then the low score parts; `a`
       // holds the chunk's transposing reads, issued before its scoring.
-      auto mma = [&](s16x4_t(&a)[E], const uint32_t(&bh)[2], const uint32_t(&bl)[2], float scl) {
+      auto mma = [&](s16x4_t(&a)[kTrCopies * E], const uint32_t(&bh)[2], const uint32_t(&bl)[2], float scl) {
         // Softmax variants: the sums so far to the chunk's running maximum.
         if (smax && wave_ballot(scl != 1.0f) != 0ull) {
 #pragma unroll
           for (int j = 0; j < E; ++j) acc[j] *= scl;
         }
         // One 16 x 16 x 32 product per block: its 32 K slots hold the 4
-        // entries' values twice (A: the read fragment, duplicated) against
-        // their high, then their low score parts (B).
+        // entries' values twice (A: the fragment read twice, or read once and
+        // copied) against their high, then their low score parts (B).
         Frag8 b;
         b.w[0] = bh[0];
         b.w[1] = bh[1];
         b.w[2] = bl[0];
         b.w[3] = bl[1];
-        read_tr_wait<E>(a);
+        read_tr_wait<kTrCopies * E>(a);
 #pragma unroll
         for (int j = 0; j < E; ++j) {
-          Frag fa;
-          fa.v = a[j];
-          Frag8 a8;
-          a8.w[0] = fa.w[0];
-          a8.w[1] = fa.w[1];
-          a8.w[2] = fa.w[0];
-          a8.w[3] = fa.w[1];
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8.v, b.v, acc[j], 0, 0, 0);
+          const bf16x8_t a8 = __builtin_bit_cast(
+              bf16x8_t, __builtin_shufflevector(a[kTrCopies * j], a[kTrCopies * j + kTrCopies - 1], 0, 1, 2, 3, 4, 5,
+                                                6, 7));
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8, b.v, acc[j], 0, 0, 0);
         }
       };
 
@@ -786,6 +804,18 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           // (cb + nch)*kChunk - 1.
           {
             const int32_t base = cb * kChunk;
+            // This lane's query row as bfloat16 bits (row 0 for a lane
+            // without a window: read, not used).  The opaque row index keeps
+            // the read here rather than hoisted out of the loop, where it
+            // would wait alone.
+            uint32_t q3[3];
+            if constexpr (kLateQ) {
+              int32_t qr = mine ? int32_t(g_seg * N + my_i) : 0;  // rows < 2^31
+              asm volatile("" : "+v"(qr));
+              const int64_t qe = int64_t(qr) * 3;
+#pragma unroll
+              for (int a = 0; a < 3; ++a) q3[a] = q[qe + a];
+            }
             int32_t pv[kStageEntries / 64];
             uint2 kw[kStageEntries / 64];  // d_k = 3: key rows read in list order with the positions
 #pragma unroll
@@ -798,6 +828,13 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                 pv[t] = lpos[r];
                 if constexpr (DK == 3) kw[t] = lkey[r];
               }
+            }
+            if constexpr (kLateQ) {
+              // Converted here, before any value-row copy is issued (a wait
+              // for the row after one would also wait for that copy).
+#pragma unroll
+              for (int a = 0; a < 3; ++a) qv[a] = mine ? __uint_as_float(q3[a] << 16) : 0.0f;
+              asm volatile("" ::"v"(qv[0]), "v"(qv[1]), "v"(qv[2]));
             }
 #pragma unroll
             for (int t = 0; t < kStageEntries / 64; ++t) {
@@ -838,21 +875,21 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           int32_t pv4[4];
           uint32_t bh[2], bl[2];
           float scl;
-          s16x4_t a[E];
+          s16x4_t a[kTrCopies * E];
           entry_pos(0, pv4);
           copy_rows(0, v0, pv4);
           for (int ch = 0; ch < nch; ch += 2) {
             const int c1 = ch + 1 < nch ? ch + 1 : ch;
             entry_pos(c1, pv4);
             copy_rows(c1, v1, pv4);
-            read_tr_issue<E, 0, VS::kLoads>(tr_addr, a);
+            read_tr_issue<E, kTrCopies, 0, VS::kLoads>(tr_addr, a);
             score4(cb, ch, bh, bl, scl);
             mma(a, bh, bl, scl);
             if (ch + 1 >= nch) break;
             const int c2 = ch + 2 < nch ? ch + 2 : ch + 1;
             entry_pos(c2, pv4);
             copy_rows(c2, v0, pv4);
-            read_tr_issue<E, VS::kBytes, VS::kLoads>(tr_addr, a);
+            read_tr_issue<E, kTrCopies, VS::kBytes, VS::kLoads>(tr_addr, a);
             score4(cb, ch + 1, bh, bl, scl);
             mma(a, bh, bl, scl);
           }
@@ -863,23 +900,42 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         c = wave_min_int(a_ch > e ? a_ch : INT32_MAX);
       }
 
-      // Normalise and store: lane holds columns 16 blk + 4kg .. + 3 of
-      // query qn for every block.
+      // Normalise and store.  Lane (qn, kg) holds columns 16 blk + 4kg .. + 3
+      // of query qn for every block; the rows pass through LDS (the value-row
+      // buffers, free now: every copy has landed and been read) so that each
+      // query's row leaves as whole 16-byte pieces, P = d_v / 8 lanes per row
+      // and full cache lines, instead of 8-byte pieces from 4 lanes.  Piece p
+      // of LDS row r sits at physical piece p ^ (r % P): the 8-byte writes
+      // and the 16-byte reads are both spread evenly over the banks.
       float z = zpart;
       z += __shfl_xor(z, 16, 64);
       z += __shfl_xor(z, 32, 64);
-      if (in_grp) {
-        const float inv = z > 0.0f ? 1.0f / z : 0.0f;
-        uint16_t* orow = out + (g_seg * N + my_i) * int64_t(DV) + 4 * kg;
+      const float inv = z > 0.0f ? 1.0f / z : 0.0f;
+      constexpr int kP = DV / 8;        // 16-byte pieces per output row
+      constexpr int kRows = 64 / kP;    // rows per store instruction
+      constexpr int kRowB = 2 * DV;     // bytes per output row
+      static_assert(kTileQ * kRowB <= 2 * VS::kBytes, "the output rows fit in the value-row buffers");
+      unsigned char* const so = s_v[wave];
 #pragma unroll
-        for (int j = 0; j < E; ++j) {
-          // Rounded to bfloat16 (nearest even), two values per conversion.
-          const bf16x2_t p0 = {(__bf16)(acc[j][0] * inv), (__bf16)(acc[j][1] * inv)};
-          const bf16x2_t p1 = {(__bf16)(acc[j][2] * inv), (__bf16)(acc[j][3] * inv)};
-          *reinterpret_cast<uint2*>(orow + 16 * j) =
-              make_uint2(__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1));
-        }
+      for (int j = 0; j < E; ++j) {
+        // Rounded to bfloat16 (nearest even), two values per conversion.
+        const bf16x2_t p0 = {(__bf16)(acc[j][0] * inv), (__bf16)(acc[j][1] * inv)};
+        const bf16x2_t p1 = {(__bf16)(acc[j][2] * inv), (__bf16)(acc[j][3] * inv)};
+        const int piece = 2 * j + (kg >> 1);
+        *reinterpret_cast<uint2*>(so + qn * kRowB + 16 * (piece ^ (qn % kP)) + 8 * (kg & 1)) =
+            make_uint2(__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1));
       }
+      wave_lds_sync();
+#pragma unroll
+      for (int t = 0; t < kTileQ / kRows; ++t) {
+        const int r = t * kRows + lane / kP, c = lane % kP;
+        const uint4 piece = *reinterpret_cast<const uint4*>(so + r * kRowB + 16 * (c ^ (r % kP)));
+        const int32_t ri = __shfl(my_i, r, 64);  // query r's position (held by lane r)
+        if (((gmask >> r) & 1u) != 0u)
+          *reinterpret_cast<uint4*>(out + (g_seg * N + ri) * int64_t(DV) + 8 * c) = piece;
+      }
+      // The next writes into these buffers come after this wavefront's reads.
+      wave_lds_sync();
     }
   }
 }
