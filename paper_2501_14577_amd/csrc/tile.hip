@@ -529,6 +529,41 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       nx_b = bounds[sl];
     }
   };
+  // Output rows of the last group of queries wait in this wavefront's
+  // value-row buffers (s_orow[wave][r]: the output row of LDS row r, -1 for
+  // none) and are stored once the next staged entries are being loaded: the
+  // stores then overlap those loads instead of holding up the next tile.
+  // Piece p of LDS row r sits at physical piece p ^ (r % kOutP), so that the
+  // 8-byte writes and the 16-byte reads are both spread evenly over the banks.
+  constexpr int kOutP = DV / 8;       // 16-byte pieces per output row
+  constexpr int kOutRows = 64 / kOutP;  // rows per store instruction
+  constexpr int kOutRowB = 2 * DV;    // bytes per output row
+  static_assert(kTileQ * kOutRowB <= 2 * VS::kBytes, "the output rows fit in the value-row buffers");
+  __shared__ int32_t s_orow[kTileWaves][kTileQ];
+  bool out_pending = false;
+  auto flush_out = [&]() {
+    if (out_pending) {
+      const unsigned char* so = s_v[wave];
+#pragma unroll
+      for (int t = 0; t < kTileQ / kOutRows; ++t) {
+        const int r = t * kOutRows + lane / kOutP, c = lane % kOutP;
+        const uint4 piece = *reinterpret_cast<const uint4*>(so + r * kOutRowB + 16 * (c ^ (r % kOutP)));
+        const int32_t orow = s_orow[wave][r];
+        // Streaming stores: the output is not read again here, and keeping
+        // it out of L2 leaves room for value rows that later tiles reuse.
+        if (orow >= 0) {
+          uint32_t* dst = reinterpret_cast<uint32_t*>(out + int64_t(orow) * DV + 8 * c);
+          __builtin_nontemporal_store(piece.x, dst);
+          __builtin_nontemporal_store(piece.y, dst + 1);
+          __builtin_nontemporal_store(piece.z, dst + 2);
+          __builtin_nontemporal_store(piece.w, dst + 3);
+        }
+      }
+      out_pending = false;
+      // Every read of the rows is done before the buffers are written again.
+      wave_lds_sync();
+    }
+  };
   const int64_t blk0 = xcd_contiguous_block(blockIdx.x, nb);
   fetch_slot(blk0 * kTileWaves + wave);
   for (int64_t blk = blk0; blk * kTileWaves < tiles; blk += nb) {
@@ -664,14 +699,22 @@ __global__ void __launch_bounds__(kTileWaves * 64)
             pv = __float_as_int(s_ent[wave][ch * kChunk + VS::entry_of_row(j * VS::kR + vq)][kPosSlot]);
           } else {
             // Entry 4kg + j*kOwn + vq % kOwn: one of this lane's own four.
+            // Selected by the bits of r, among values first made opaque
+            // (selects among the array's elements themselves are folded into
+            // an indexed private array, which lives in scratch memory).
             const int u0 = j * VS::kOwn;
+            const int r = vq % VS::kOwn;
             if constexpr (VS::kOwn == 1) {
               pv = pvs[u0];
+            } else if constexpr (VS::kOwn == 2) {
+              int32_t p0 = pvs[u0], p1 = pvs[u0 + 1];
+              asm("" : "+v"(p0), "+v"(p1));
+              pv = (r & 1) ? p1 : p0;
             } else {
-              const int r = vq % VS::kOwn;
-              pv = pvs[u0];
-#pragma unroll
-              for (int t = 1; t < VS::kOwn; ++t) pv = r == t ? pvs[u0 + t] : pv;
+              static_assert(VS::kOwn == 4, "d_v >= 32");
+              int32_t p0 = pvs[u0], p1 = pvs[u0 + 1], p2 = pvs[u0 + 2], p3 = pvs[u0 + 3];
+              asm("" : "+v"(p0), "+v"(p1), "+v"(p2), "+v"(p3));
+              pv = (r & 2) ? ((r & 1) ? p3 : p2) : ((r & 1) ? p1 : p0);
             }
           }
           const Off boff = Off(pv) * Off(VS::kRowBytes) + Off(copy_off[j]);
@@ -829,6 +872,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                 if constexpr (DK == 3) kw[t] = lkey[r];
               }
             }
+            flush_out();
             if constexpr (kLateQ) {
               // Converted here, before any value-row copy is issued (a wait
               // for the row after one would also wait for that copy).
@@ -900,21 +944,15 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         c = wave_min_int(a_ch > e ? a_ch : INT32_MAX);
       }
 
-      // Normalise and store.  Lane (qn, kg) holds columns 16 blk + 4kg .. + 3
-      // of query qn for every block; the rows pass through LDS (the value-row
-      // buffers, free now: every copy has landed and been read) so that each
-      // query's row leaves as whole 16-byte pieces, P = d_v / 8 lanes per row
-      // and full cache lines, instead of 8-byte pieces from 4 lanes.  Piece p
-      // of LDS row r sits at physical piece p ^ (r % P): the 8-byte writes
-      // and the 16-byte reads are both spread evenly over the banks.
+      // Normalise, then leave the rows in LDS for flush_out.  Lane (qn, kg)
+      // holds columns 16 blk + 4kg .. + 3 of query qn for every block; each
+      // query's row will leave as whole 16-byte pieces, kOutP lanes per row
+      // and full cache lines.
       float z = zpart;
       z += __shfl_xor(z, 16, 64);
       z += __shfl_xor(z, 32, 64);
       const float inv = z > 0.0f ? 1.0f / z : 0.0f;
-      constexpr int kP = DV / 8;        // 16-byte pieces per output row
-      constexpr int kRows = 64 / kP;    // rows per store instruction
-      constexpr int kRowB = 2 * DV;     // bytes per output row
-      static_assert(kTileQ * kRowB <= 2 * VS::kBytes, "the output rows fit in the value-row buffers");
+      flush_out();  // an earlier group's rows, when this group staged nothing
       unsigned char* const so = s_v[wave];
 #pragma unroll
       for (int j = 0; j < E; ++j) {
@@ -922,22 +960,15 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         const bf16x2_t p0 = {(__bf16)(acc[j][0] * inv), (__bf16)(acc[j][1] * inv)};
         const bf16x2_t p1 = {(__bf16)(acc[j][2] * inv), (__bf16)(acc[j][3] * inv)};
         const int piece = 2 * j + (kg >> 1);
-        *reinterpret_cast<uint2*>(so + qn * kRowB + 16 * (piece ^ (qn % kP)) + 8 * (kg & 1)) =
+        *reinterpret_cast<uint2*>(so + qn * kOutRowB + 16 * (piece ^ (qn % kOutP)) + 8 * (kg & 1)) =
             make_uint2(__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1));
       }
+      if (lane < kTileQ) s_orow[wave][lane] = in_grp ? int32_t(g_seg * N + my_i) : -1;  // rows < 2^31
       wave_lds_sync();
-#pragma unroll
-      for (int t = 0; t < kTileQ / kRows; ++t) {
-        const int r = t * kRows + lane / kP, c = lane % kP;
-        const uint4 piece = *reinterpret_cast<const uint4*>(so + r * kRowB + 16 * (c ^ (r % kP)));
-        const int32_t ri = __shfl(my_i, r, 64);  // query r's position (held by lane r)
-        if (((gmask >> r) & 1u) != 0u)
-          *reinterpret_cast<uint4*>(out + (g_seg * N + ri) * int64_t(DV) + 8 * c) = piece;
-      }
-      // The next writes into these buffers come after this wavefront's reads.
-      wave_lds_sync();
+      out_pending = true;
     }
   }
+  flush_out();
 }
 
 template <int DV, int DK>
