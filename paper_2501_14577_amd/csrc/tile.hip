@@ -85,15 +85,15 @@ constexpr int kTileWaves = 4;  // wavefronts per block
 // or when its query searches another list.  With idx_out the run's windows
 // are also written as position rows, one wavefront-wide pass per query.
 constexpr int kBndWaves = 4;
-constexpr int kRegion = 512;   // list entries staged per wavefront
-constexpr int kMargin = 192;    // of them before the run's first insertion point
+constexpr int kRegion = 512;   // list entries staged per wavefront (a multiple of 32)
+constexpr int kMargin = 192;    // of them before the run's first insertion point (about)
 
 // Each wavefront's copy of a list range, in LDS.  Declared at file scope and
 // indexed directly, so that every access compiles to an LDS instruction (a
 // pointer kept in a struct would lose the address space and go through the
 // slower flat path).
 __shared__ uint32_t s_bnd_codes[kBndWaves][kRegion];
-__shared__ int32_t s_bnd_pos[kBndWaves][kRegion];
+__shared__ __align__(16) int32_t s_bnd_pos[kBndWaves][kRegion];
 
 struct LaneList {
   const uint32_t* codes;
@@ -102,67 +102,84 @@ struct LaneList {
   int32_t n, limit, r0, r1;  // [r0, r1): the range copied to LDS (empty when not staged)
 };
 
-constexpr int kScanStep = 16;  // list entries examined per step of lane_scan
+constexpr int kScanStep = 32;  // list entries examined per step of lane_scan
 
-// Bit j set when entry lo + j is in the query's pool.  A block inside the LDS
-// copy is read from there; any other block from the list itself, with entries
-// outside [0, n) counted out.  Both branches are straight-line code, so a
-// block's reads issue together and the lane waits once for them.
-__device__ __forceinline__ uint32_t pool_bits(const LaneList& L, int32_t lo) {
+// Bit j set when entry B + j is in the query's pool (B a multiple of
+// kScanStep).  A block inside the staged range is read from LDS (entries past
+// the list's end hold INT32_MAX, in no pool); any other block from the list
+// itself, with entries outside [0, n) counted out.
+__device__ __forceinline__ uint32_t pool_bits(const LaneList& L, int32_t B) {
   uint32_t mask = 0u;
-  if (lo >= L.r0 && lo + kScanStep <= L.r1) {
-    const int32_t b = lo - L.r0;
+  if (L.r1 > L.r0 && B >= L.r0 && B + kScanStep <= L.r0 + kRegion) {
+    const int4* blk = reinterpret_cast<const int4*>(&s_bnd_pos[L.wave][B - L.r0]);
 #pragma unroll
-    for (int j = 0; j < kScanStep; ++j) mask |= (s_bnd_pos[L.wave][b + j] <= L.limit ? 1u : 0u) << j;
+    for (int t = 0; t < kScanStep / 4; ++t) {
+      const int4 v = blk[t];
+      mask |= v.x <= L.limit ? (1u << (4 * t)) : 0u;
+      mask |= v.y <= L.limit ? (2u << (4 * t)) : 0u;
+      mask |= v.z <= L.limit ? (4u << (4 * t)) : 0u;
+      mask |= v.w <= L.limit ? (8u << (4 * t)) : 0u;
+    }
   } else {
     using G = __attribute__((address_space(1))) const int32_t;
     G* gp = (G*)L.pos;
-    int32_t v[kScanStep];
 #pragma unroll
     for (int j = 0; j < kScanStep; ++j) {
-      const int32_t x = lo + j;
-      v[j] = gp[x < 0 ? 0 : (x < L.n ? x : L.n - 1)];
-    }
-#pragma unroll
-    for (int j = 0; j < kScanStep; ++j) {
-      const int32_t x = lo + j;
-      mask |= (x >= 0 && x < L.n && v[j] <= L.limit ? 1u : 0u) << j;
+      const int32_t x = B + j;
+      const int32_t v = gp[x < 0 ? 0 : (x < L.n ? x : L.n - 1)];
+      mask |= (x >= 0 && x < L.n && v <= L.limit ? 1u : 0u) << j;
     }
   }
   return mask;
 }
 
+// Index of the n-th set bit of m (n from 1 to popcount(m)), by halving.
+__device__ __forceinline__ int nth_set_bit(uint32_t m, int n) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 16; w >= 1; w >>= 1) {
+    const int c = __popc(m & ((1u << w) - 1u));
+    if (n > c) {
+      n -= c;
+      m >>= w;
+      pos += w;
+    }
+  }
+  return pos;
+}
+
 // Scan from entry e in direction dir (+1 or -1) for up to `need` in-pool
 // entries beyond the `got` already taken; records the first and last entry
 // taken (first only when got is 0).  Returns the new count; `e` ends just
-// past the last entry taken, or past the list's end.  Entries are examined
-// kScanStep at a time as a bit mask (bit j: entry e + dir*j is in the pool);
-// only the block where the count is reached is searched bit by bit.  Called
-// only with n > 0.
+// past the last entry taken, or past the list's end.  Entries are examined in
+// aligned blocks of kScanStep as a bit mask (bit k: entry base + dir*k); only
+// the block where the count is reached is searched for its bit.  Called only
+// with n > 0.
 __device__ __forceinline__ int lane_scan(const LaneList& L, int32_t& e, int dir, int need, int got, int32_t& first,
                                          int32_t& last) {
   while (got < need && e >= 0 && e < L.n) {
-    // Lowest index of the block, in ascending list order.
-    const int32_t lo = dir > 0 ? e : e - (kScanStep - 1);
-    uint32_t mask = pool_bits(L, lo);
-    // Bit j of `mask` is entry lo + j; reorder so bit j is entry e + dir*j.
-    if (dir < 0) mask = __builtin_bitreverse32(mask) >> (32 - kScanStep);
+    const int32_t B = e & ~(kScanStep - 1);
+    uint32_t mask = pool_bits(L, B);
+    int32_t base;
+    if (dir > 0) {
+      base = B;
+      mask &= ~0u << (e - B);
+    } else {
+      base = B + kScanStep - 1;
+      mask = __builtin_bitreverse32(mask) & (~0u << (base - e));
+    }
     const int cnt = __popc(mask);
     if (cnt == 0) {
-      e += dir * kScanStep;
+      e = base + dir * kScanStep;
       continue;
     }
-    if (got == 0) first = e + dir * (__ffs(int(mask)) - 1);
+    if (got == 0) first = base + dir * (__ffs(int(mask)) - 1);
     if (got + cnt < need) {
       got += cnt;
-      last = e + dir * (31 - __clz(int(mask)));
-      e += dir * kScanStep;
+      last = base + dir * (31 - __clz(int(mask)));
+      e = base + dir * kScanStep;
     } else {
-      // The (need - got)-th set bit ends the scan.
-      uint32_t m = mask;
-      for (int t = 1; t < need - got; ++t) m &= m - 1u;
-      const int j = __ffs(int(m)) - 1;
-      last = e + dir * j;
+      last = base + dir * nth_set_bit(mask, need - got);
       e = last + dir;
       got = need;
     }
@@ -221,7 +238,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
       const int32_t g_n = __builtin_amdgcn_readlane(Lq.n, leader);
       const uint32_t g_key = uint32_t(__builtin_amdgcn_readlane(int32_t(key), leader));
       const int32_t p0 = wave_lower_bound(g_codes, 0, g_n, g_key, lane);
-      const int32_t r0 = p0 - kMargin > 0 ? p0 - kMargin : 0;
+      const int32_t r0 = (p0 - kMargin > 0 ? p0 - kMargin : 0) & ~(kScanStep - 1);
       const int32_t r1 = r0 + kRegion < g_n ? r0 + kRegion : g_n;
       {
         uint32_t cv[kRegion / 64];
@@ -230,7 +247,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
         for (int t = 0; t < kRegion / 64; ++t) {
           const int32_t e = r0 + t * 64 + lane;
           cv[t] = e < r1 ? g_codes[e] : 0u;
-          pv[t] = e < r1 ? g_pos[e] : 0;
+          pv[t] = e < r1 ? g_pos[e] : INT32_MAX;  // past the list's end: in no pool
         }
 #pragma unroll
         for (int t = 0; t < kRegion / 64; ++t) {
