@@ -102,23 +102,28 @@ struct LaneList {
   int32_t n, limit, r0, r1;  // [r0, r1): the range copied to LDS (empty when not staged)
 };
 
-constexpr int kScanStep = 32;  // list entries examined per step of lane_scan
+constexpr int kScanStep = 32;  // list entries examined per step of lane_scan (one bit each of a 32-bit mask)
+static_assert(kScanStep == 32, "the scan masks are 32-bit words");
 
-// Bit j set when entry B + j is in the query's pool (B a multiple of
-// kScanStep).  A block inside the staged range is read from LDS (entries past
-// the list's end hold INT32_MAX, in no pool); any other block from the list
-// itself, with entries outside [0, n) counted out.
+// The query's in-pool entries B .. B + kScanStep - 1 (B a multiple of
+// kScanStep) as a bit mask, first entry in the highest bit: bit 31 - j is
+// entry B + j.  An entry is in the pool when pos <= limit, i.e. when
+// pos - limit - 1 is negative; each entry's sign bit is shifted in with one
+// funnel shift.  A block inside the staged range is read from LDS (entries
+// past the list's end hold INT32_MAX, in no pool); any other block from the
+// list itself, with entries outside [0, n) counted out.
 __device__ __forceinline__ uint32_t pool_bits(const LaneList& L, int32_t B) {
+  const uint32_t nl = uint32_t(-1 - L.limit);  // pos + nl < 0 exactly when pos <= limit (no overflow)
   uint32_t mask = 0u;
   if (L.r1 > L.r0 && B >= L.r0 && B + kScanStep <= L.r0 + kRegion) {
     const int4* blk = reinterpret_cast<const int4*>(&s_bnd_pos[L.wave][B - L.r0]);
 #pragma unroll
     for (int t = 0; t < kScanStep / 4; ++t) {
       const int4 v = blk[t];
-      mask |= v.x <= L.limit ? (1u << (4 * t)) : 0u;
-      mask |= v.y <= L.limit ? (2u << (4 * t)) : 0u;
-      mask |= v.z <= L.limit ? (4u << (4 * t)) : 0u;
-      mask |= v.w <= L.limit ? (8u << (4 * t)) : 0u;
+      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.x) + nl, 31);
+      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.y) + nl, 31);
+      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.z) + nl, 31);
+      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.w) + nl, 31);
     }
   } else {
     using G = __attribute__((address_space(1))) const int32_t;
@@ -127,7 +132,7 @@ __device__ __forceinline__ uint32_t pool_bits(const LaneList& L, int32_t B) {
     for (int j = 0; j < kScanStep; ++j) {
       const int32_t x = B + j;
       const int32_t v = gp[x < 0 ? 0 : (x < L.n ? x : L.n - 1)];
-      mask |= (x >= 0 && x < L.n && v <= L.limit ? 1u : 0u) << j;
+      mask = __builtin_amdgcn_alignbit(mask, (x >= 0 && x < L.n) ? uint32_t(v) + nl : 0u, 31);
     }
   }
   return mask;
@@ -159,14 +164,14 @@ __device__ __forceinline__ int lane_scan(const LaneList& L, int32_t& e, int dir,
                                          int32_t& last) {
   while (got < need && e >= 0 && e < L.n) {
     const int32_t B = e & ~(kScanStep - 1);
-    uint32_t mask = pool_bits(L, B);
+    uint32_t mask = pool_bits(L, B);  // bit 31 - j: entry B + j
     int32_t base;
     if (dir > 0) {
       base = B;
-      mask &= ~0u << (e - B);
+      mask = __builtin_bitreverse32(mask) & (~0u << (e - B));
     } else {
       base = B + kScanStep - 1;
-      mask = __builtin_bitreverse32(mask) & (~0u << (base - e));
+      mask &= ~0u << (base - e);
     }
     const int cnt = __popc(mask);
     if (cnt == 0) {
@@ -312,7 +317,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
         const int32_t ua = __builtin_amdgcn_readlane(res.x, u), ub = __builtin_amdgcn_readlane(res.y, u);
         const int32_t ulim = __builtin_amdgcn_readlane(L.limit, u);
         const int32_t ui = __builtin_amdgcn_readlane(my_i, u);
-        const int64_t useg = (run * 64 + u) / N;
+        const int64_t useg = int64_t(uint32_t(run * 64 + u) / uint32_t(N));  // slots < B*H*N < 2^31
         int32_t* row = idx_out + (useg * N + ui) * int64_t(topk);
         int cnt = 0;
         for (int32_t e0 = ua; e0 <= ub; e0 += 64) {
