@@ -140,6 +140,24 @@ def test_sort_shapes(S, N, code_bits):
     assert np.array_equal(host(sc), esc)
 
 
+@pytest.mark.parametrize("S,N,code_bits,high_values", [(2, 20000, 18, 4), (1, 9000, 18, 1), (3, 4097, 16, 2)])
+def test_sort_clustered(S, N, code_bits, high_values):
+    """Codes whose high digit takes only a few values (one value: every key
+    shares it): heavily repeated digits in every tile of both passes, and
+    long runs of equal high digit with the low digit deciding the order."""
+    log(f"sort clustered S={S} N={N} bits={code_bits} high values={high_values}")
+    low = (code_bits + 1) // 2
+    rng = np.random.default_rng([S, N, code_bits, high_values])
+    hi = rng.integers(0, high_values, size=(S, N), dtype=np.uint64) << np.uint64(low)
+    lo = rng.integers(0, 1 << low, size=(S, N), dtype=np.uint64)
+    kc = (hi | lo).astype(np.uint32)
+    esc, eperm = oracle.sort_keys(kc)
+    sc, perm = zeta.zeta_sort_keys(u32_to_dev(kc), code_bits)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(perm), eperm)
+    assert np.array_equal(host(sc), esc)
+
+
 # ----------------------------------------------------------------------------
 # Select
 # ----------------------------------------------------------------------------
