@@ -264,6 +264,8 @@ bool attend_supports(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv ==
 hipError_t launch_attend(const void* q, const void* k, const void* v, bool is_bf16, int64_t S,
                          int64_t N, int dk, int dv, int topk, const int32_t* idx, const int32_t* q_order,
                          int score, float eps, HistMean hm, void* out, hipStream_t stream) {
+  if (idx_tile_path(is_bf16, dk, dv, topk, q_order != nullptr))
+    return launch_attend_idx_tile(q, k, v, S, N, dv, topk, idx, q_order, score, eps, hm, out, stream);
 #define ZETA_ATTEND_CASE(DVV)                                                                            \
   case DVV:                                                                                              \
     return is_bf16                                                                                       \

@@ -85,6 +85,12 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
 // key rows in list order into keys_full (S*N) and keys_list (S*cap); then the
 // tiles.
 bool tile_supports(int dv);
+// The attend call on the matrix-core tiles (bfloat16, d_k = 3, d_v 32, 64 or
+// 128, topk <= kIdxTileMaxTopk, a processing order given): each wavefront
+// takes 16 consecutive queries of q_order and the union of their index rows.
+hipError_t launch_attend_idx_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dv, int topk,
+                                  const int32_t* idx, const int32_t* q_order, int score, float eps, HistMean hm,
+                                  void* out, hipStream_t stream);
 // The tiles' inputs alone: key rows in list order (d_k = 3) and the window
 // bounds of every processing-order slot (idx_out optional).
 hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int topk, bool causal, int chunk,

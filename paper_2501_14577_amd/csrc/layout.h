@@ -149,6 +149,16 @@ inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
 // Value widths compiled for the matrix-core tiles.
 inline bool tile_dv(int dv) { return dv == 32 || dv == 64 || dv == 128 || dv == 256; }
 
+// Largest k of the attend call's matrix-core tiles (index rows shared by 16
+// neighbouring queries of a processing order).
+constexpr int kIdxTileMaxTopk = 128;
+
+// Whether the attend call runs on those tiles: a processing order given,
+// bfloat16 inputs, d_k = 3, d_v up to 128 and k up to kIdxTileMaxTopk.
+inline bool idx_tile_path(bool is_bf16, int dk, int dv, int topk, bool have_order) {
+  return have_order && is_bf16 && dk == 3 && (dv == 32 || dv == 64 || dv == 128) && topk <= kIdxTileMaxTopk;
+}
+
 // Whether the one-pass call runs on the matrix-core tiles (and so needs the
 // fused_ws layout, 16-byte aligned): bfloat16 inputs, a compiled d_v, and the
 // Cauchy score, or any score when d_k = 3.  Validation and the launcher both

@@ -118,9 +118,24 @@ __global__ void __launch_bounds__(kSortThreads)
     code[c] = valid ? sorted_codes[seg_off + e] : 0u;
     pos[c] = valid ? perm[seg_off + e] : 0x7FFFFFFF;  // never below any 2^t
     krow[c] = make_uint2(0u, 0u);
-    if (k_rows != nullptr && valid) {
-      krow[c] = packed_key_row(k_rows, seg_off + pos[c], int64_t(gridDim.x / tiles) * N);
-      keys_full[seg_off + e] = krow[c];
+  }
+  if (k_rows != nullptr) {
+    // Each entry's key row (three bfloat16 values) gathered by position: three
+    // 16-bit loads per entry, always in bounds and without a branch, so the
+    // entries' gathers are in flight together; then packed as x | y << 16, z.
+    uint32_t kx[kSortChunks], ky[kSortChunks], kz[kSortChunks];
+#pragma unroll
+    for (int c = 0; c < kSortChunks; ++c) {
+      const int64_t r = (first + c * 64 + lane < N ? seg_off + pos[c] : 0) * 3;
+      kx[c] = k_rows[r];
+      ky[c] = k_rows[r + 1];
+      kz[c] = k_rows[r + 2];
+    }
+#pragma unroll
+    for (int c = 0; c < kSortChunks; ++c) {
+      const int64_t e = first + c * 64 + lane;
+      krow[c] = make_uint2(kx[c] | (ky[c] << 16), kz[c]);
+      if (e < N) keys_full[seg_off + e] = krow[c];
     }
   }
   for (int l = 0; l < levels; ++l) {

@@ -70,6 +70,18 @@ constexpr int kTileQ = 16;     // queries per tile (product columns)
 constexpr int kChunk = 16;     // list entries per product step
 constexpr int kTileWaves = 4;  // wavefronts per block
 
+// Index-row tiles (the attend call given a processing order): the union of a
+// tile's index rows is built in a per-wavefront hash table of kIdxHash
+// positions (linear probing, at most kIdxProbes slots per insertion) that
+// lives in the wavefront's value-row buffers, and holds at most
+// kIdxUnionCap entries.
+constexpr int kIdxHashBits = 10;
+constexpr int kIdxHash = 1 << kIdxHashBits;
+constexpr int kIdxProbes = 8;
+constexpr int kIdxUnionCap = 288;
+constexpr int kIdxRounds = kTileQ * kIdxTileMaxTopk / 64;  // 64-element rounds over the tile's rows
+constexpr uint32_t kIdxEmpty = 0xFFFFFFFFu;
+
 // ---- window bounds ---------------------------------------------------------
 // Each lane serves one slot of the processing order (a run of 64 consecutive
 // slots per wavefront) and writes its query's window as list-index bounds
@@ -469,7 +481,10 @@ struct VStage {
   }
 };
 
-template <int DV, int DK, bool kOff32, bool kHist, int kMode>
+// kIdx: the windows are index rows (idx, topk <= kIdxTileMaxTopk, d_k = 3)
+// instead of list ranges; `order` is then required and the list arguments
+// are unused.
+template <int DV, int DK, bool kOff32, bool kHist, int kMode, bool kIdx>
 __global__ void __launch_bounds__(kTileWaves * 64)
     __attribute__((amdgpu_waves_per_eu((kOff32 && (DV == 128 || (DV < 128 && kMode != kScoreCauchy))) ? 3 : 1)))
     select_attend_tile_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -478,13 +493,15 @@ __global__ void __launch_bounds__(kTileWaves * 64)
                               const int2* __restrict__ bounds, const uint2* __restrict__ keys_full,
                               const uint2* __restrict__ keys_list, int64_t total, int64_t N, int dk_rt, int causal,
                               int chunk, int t0, int t_hi, int64_t cap, float eps,
-                              const float* __restrict__ mk, const float* __restrict__ mv, uint16_t* __restrict__ out) {
+                              const float* __restrict__ mk, const float* __restrict__ mv, uint16_t* __restrict__ out,
+                              const int32_t* __restrict__ idx, int topk) {
   using VS = VStage<DV>;
   constexpr int E = VS::kBlocks;  // products per chunk; a lane ends with 4 columns of each block
   constexpr int KD = DK > 0 ? DK : kMaxDk;
+  static_assert(!kIdx || DK == 3, "index-row tiles are compiled for d_k = 3");
   // Entries whose key rows and positions are staged at once (LDS per wave:
   // these plus two chunks of value rows).
-  constexpr int kStageEntries = (DK == 3 && DV <= 128) ? 320 : 128;
+  constexpr int kStageEntries = kIdx ? kIdxUnionCap : (DK == 3 && DV <= 128) ? 320 : 128;
   constexpr int kStage = kStageEntries / kChunk;
   static_assert(E >= 2, "d_v must be a multiple of 32");
   // Each A fragment is read from LDS twice (both K halves of a product) where
@@ -508,8 +525,13 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   constexpr int kPosSlot = DK == 3 ? 3 : KD4;
   constexpr int KREC = DK == 3 ? 4 : KD4 + 4;
   __shared__ __align__(16) float s_ent[kTileWaves][kStageEntries][KREC];
-  // Two chunks of value rows per wave (even chunks, then odd chunks).
-  __shared__ __align__(16) unsigned char s_v[kTileWaves][2 * VS::kBytes];
+  // Two chunks of value rows per wave (even chunks, then odd chunks); with
+  // index rows also the union's hash table (positions, then query masks)
+  // while the union is built.
+  constexpr int kVBufBytes = (kIdx && 2 * VS::kBytes < 8 * kIdxHash) ? 8 * kIdxHash : 2 * VS::kBytes;
+  __shared__ __align__(16) unsigned char s_v[kTileWaves][kVBufBytes];
+  // With index rows: the union entries' query masks (bit t: tile query t).
+  __shared__ __align__(16) uint16_t s_um[kTileWaves][kIdx ? kStageEntries : 8];
 
   const int lane = threadIdx.x & 63;
   // Wave-uniform (the LDS destination of a copy instruction must be).
@@ -548,7 +570,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
     const int64_t sl = t_ * kTileQ + qn;
     if (sl < total) {
       if (order != nullptr) nx_o = order[sl];
-      nx_b = bounds[sl];
+      if constexpr (!kIdx) nx_b = bounds[sl];
     }
   };
   // Output rows of the last group of queries wait in this wavefront's
@@ -608,29 +630,269 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         if (ii >= 0 && ii < N) {
           my_i = int32_t(ii);
           my_seg = sg;
-          my_lvl = causal ? pool_level(pool_limit(my_i, chunk), t0, t_hi) : 0;
-          my_a = cur_b.x;
-          my_b = cur_b.y;
+          if constexpr (!kIdx) {
+            my_lvl = causal ? pool_level(pool_limit(my_i, chunk), t0, t_hi) : 0;
+            my_a = cur_b.x;
+            my_b = cur_b.y;
+          }
         }
       }
     }
     uint32_t pending = uint32_t(wave_ballot(my_i >= 0)) & 0xFFFFu;
     // d_k = 3 (Cauchy score, no history candidate): the query row is read
     // with the staged entries, so that one wait covers both.
-    constexpr bool kLateQ = DK == 3 && !kVar && !kHist;
+    constexpr bool kLateQ = DK == 3 && !kVar && !kHist && !kIdx;
+
+    // ---- index rows: the union of a group's rows ----
+    // Slot s of tile query t's row is element (t << lg) + s of the tile's
+    // rows (lg: log2 of topk rounded up to a power of two); round r holds
+    // elements 64r .. 64r + 63, one per lane.
+    const int idx_lg = kIdx ? (topk > 1 ? 32 - __clz(topk - 1) : 0) : 0;
+    const int idx_rounds = idx_lg >= 2 ? 1 << (idx_lg - 2) : 1;
+    // Calls body(j, t, s) for every element of the tile's rows, one round at
+    // a time: j is slot s of query t's row, or -1 where t is not in `sub`,
+    // s >= topk or t >= 16.  The index loads run kAhead rounds ahead of
+    // their use.  body returns false to stop early.
+    auto for_rows = [&](uint32_t sub, int64_t seg, auto&& body) {
+      constexpr int kAhead = 8;
+      const int32_t my_row = ((sub >> qn) & 1u) != 0u ? int32_t(seg * N + my_i) : -1;  // rows < 2^31
+      auto load = [&](int r) -> int32_t {
+        const int e = r * 64 + lane;
+        const int qq = e >> idx_lg, sl = e & ((1 << idx_lg) - 1);
+        const int32_t row = __shfl(my_row, qq & (kTileQ - 1), 64);
+        return (r < idx_rounds && qq < kTileQ && row >= 0 && sl < topk) ? idx[int64_t(row) * topk + sl] : -1;
+      };
+      int32_t ring[kAhead];
+#pragma unroll
+      for (int u = 0; u < kAhead; ++u) ring[u] = load(u);
+#pragma unroll 1
+      for (int r0 = 0; r0 < idx_rounds; r0 += kAhead) {
+        bool go = true;
+#pragma unroll
+        for (int u = 0; u < kAhead; ++u) {
+          const int r = r0 + u;
+          const int32_t j = ring[u];
+          ring[u] = load(r + kAhead);
+          if (go && r < idx_rounds) {
+            const int e = r * 64 + lane;
+            go = body(j, e >> idx_lg, e & ((1 << idx_lg) - 1));
+          }
+        }
+        if (!go) break;
+      }
+    };
+    // Inserts the rows of the queries in `sub` into the hash table (keyed by
+    // position, each slot also holding the mask of the queries whose rows
+    // hold that position), then lists the occupied slots in slot order as
+    // the union's entries: positions in s_ent, masks in s_um.  Returns the
+    // number of entries, or -1 when the union does not fit (more than
+    // kStageEntries entries, a probe sequence exhausted, or a position
+    // repeated within one row, which needs an entry per occurrence).
+    auto hash_union = [&](uint32_t sub, int64_t seg) -> int {
+      uint32_t* const hpos = reinterpret_cast<uint32_t*>(&s_v[wave][0]);
+      uint32_t* const hqm = hpos + kIdxHash;
+#pragma unroll
+      for (int t = 0; t < 2 * kIdxHash / 256; ++t) {
+        const uint32_t f = t < kIdxHash / 256 ? kIdxEmpty : 0u;
+        reinterpret_cast<uint4*>(hpos)[t * 64 + lane] = make_uint4(f, f, f, f);
+      }
+      wave_lds_sync();
+      int cnt = 0;
+      bool bad = false;
+      uint32_t dup = 0u;
+      for_rows(sub, seg, [&](int32_t j, int qq, int sl) -> bool {
+        bool todo = j >= 0 && j < N;
+        const uint32_t bit = 1u << (qq & (kTileQ - 1));
+        uint32_t h = (uint32_t(j) * 0x9E3779B1u) >> (32 - kIdxHashBits);
+#pragma unroll 1
+        for (int pr = 0; pr < kIdxProbes; ++pr) {
+          uint32_t old = 0u;
+          if (todo) old = atomicCAS(&hpos[h], kIdxEmpty, uint32_t(j));
+          const bool won = todo && old == kIdxEmpty;
+          const bool here = won || (todo && old == uint32_t(j));
+          if (here) dup |= atomicOr(&hqm[h], bit) & bit;
+          cnt += __popcll(wave_ballot(won));
+          todo = todo && !here;
+          h = (h + 1u) & uint32_t(kIdxHash - 1);
+          if (wave_ballot(todo) == 0ull) break;
+        }
+        bad = wave_ballot(todo) != 0ull || cnt > kStageEntries;
+        return !bad;
+      });
+      if (bad || wave_ballot(dup != 0u) != 0ull) return -1;
+      wave_lds_sync();
+      int n = 0;
+#pragma unroll
+      for (int t = 0; t < kIdxHash / 64; ++t) {
+        const uint32_t p = hpos[t * 64 + lane];
+        const uint64_t m = wave_ballot(p != kIdxEmpty);
+        if (p != kIdxEmpty) {
+          const int id = n + int(lanes_below(m));
+          s_ent[wave][id][kPosSlot] = __int_as_float(int32_t(p));
+          s_um[wave][id] = uint16_t(hqm[t * 64 + lane]);
+        }
+        n += __popcll(m);
+      }
+      return n;
+    };
+    // The same for segments of at most 65536 rows, without hashing: the
+    // union's positions as a bitmap (one bit per row, 8 KB, in the value-row
+    // buffers), then per word the count of union entries before it, so that
+    // an entry's index is its rank among the union's positions; a second
+    // pass over the rows sets the query masks.  The entries are in position
+    // order.
+    auto bitmap_union = [&](uint32_t sub, int64_t seg) -> int {
+      uint32_t* const bm = reinterpret_cast<uint32_t*>(&s_v[wave][0]);
+      uint16_t* const pre = reinterpret_cast<uint16_t*>(&s_ent[wave][0][0]);  // until the positions are written
+      uint32_t* const mq = reinterpret_cast<uint32_t*>(&s_um[wave][0]);         // two masks per word
+#pragma unroll
+      for (int t = 0; t < 8; ++t) reinterpret_cast<uint4*>(bm)[t * 64 + lane] = make_uint4(0u, 0u, 0u, 0u);
+      wave_lds_sync();
+      for_rows(sub, seg, [&](int32_t j, int, int) -> bool {
+        if (j >= 0 && j < N) atomicOr(&bm[j >> 5], 1u << (j & 31));
+        return true;
+      });
+      wave_lds_sync();
+      // Lane l holds words 32l .. 32l + 31 and writes their prefix counts.
+      uint32_t wd[32];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint4 x = reinterpret_cast<const uint4*>(bm)[lane * 8 + t];
+        wd[4 * t] = x.x;
+        wd[4 * t + 1] = x.y;
+        wd[4 * t + 2] = x.z;
+        wd[4 * t + 3] = x.w;
+      }
+      uint32_t tot = 0u;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) tot += uint32_t(__popc(wd[i]));
+      uint32_t incl = tot;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += y;
+      }
+      const int total_u = __builtin_amdgcn_readlane(int(incl), 63);
+      if (total_u > kStageEntries) return -1;
+      const uint32_t base = incl - tot;
+      {
+        uint32_t run = base;
+        uint32_t packed[16];
+#pragma unroll
+        for (int i = 0; i < 32; i += 2) {
+          const uint32_t a0 = run;
+          run += uint32_t(__popc(wd[i]));
+          packed[i / 2] = a0 | (run << 16);
+          run += uint32_t(__popc(wd[i + 1]));
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          reinterpret_cast<uint4*>(pre)[lane * 4 + t] =
+              make_uint4(packed[4 * t], packed[4 * t + 1], packed[4 * t + 2], packed[4 * t + 3]);
+      }
+      if (lane < kStageEntries / 8) reinterpret_cast<uint4*>(mq)[lane] = make_uint4(0u, 0u, 0u, 0u);
+      wave_lds_sync();
+      uint32_t dup = 0u;
+      for_rows(sub, seg, [&](int32_t j, int qq, int) -> bool {
+        if (j >= 0 && j < N) {
+          const int w = j >> 5;
+          const int id = int(pre[w]) + __popc(bm[w] & ((1u << (j & 31)) - 1u));
+          const uint32_t bit = (1u << qq) << (16 * (id & 1));
+          dup |= atomicOr(&mq[id >> 1], bit) & bit;
+        }
+        return true;
+      });
+      if (wave_ballot(dup != 0u) != 0ull) return -1;
+      wave_lds_sync();
+      // Positions, lane by lane in word order (the prefix counts are done).
+      int id = int(base);
+#pragma unroll 4
+      for (int i = 0; i < 32; ++i) {
+        uint32_t m = bm[lane * 32 + i];
+        while (m != 0u) {
+          const int b = __ffs(int(m)) - 1;
+          s_ent[wave][id][kPosSlot] = __int_as_float(((lane * 32 + i) << 5) + b);
+          ++id;
+          m &= m - 1u;
+        }
+      }
+      return total_u;
+    };
+    // The union of the index rows of the queries in gm (segment seg), staged
+    // as the entries of one run: positions, key rows and query masks, padded
+    // to whole chunks with entries that no query takes.  When the union of
+    // all of gm does not fit, the lower half of the queries is tried, and so
+    // on down to one query, whose row is its own union (slot order, an entry
+    // per slot).  Returns the queries covered; n receives the entry count.
+    auto build_union = [&](uint32_t gm, int64_t seg, int& n) -> uint32_t {
+      flush_out();  // the value-row buffers hold the hash table next
+      uint32_t sub = gm;
+      for (;;) {
+        const int nq = __popc(sub);
+        int cnt;
+        if (nq == 1) {
+          for_rows(sub, seg, [&](int32_t j, int qq, int sl) -> bool {
+            if (((sub >> qq) & 1u) != 0u && sl < topk && qq < kTileQ) {
+              const bool ok = j >= 0 && j < N;
+              s_ent[wave][sl][kPosSlot] = __int_as_float(ok ? j : 0);
+              s_um[wave][sl] = ok ? uint16_t(1u << qq) : uint16_t(0);
+            }
+            return true;
+          });
+          cnt = topk;
+        } else {
+          cnt = N <= 65536 ? bitmap_union(sub, seg) : hash_union(sub, seg);
+        }
+        if (cnt >= 0) {
+          n = cnt;
+          break;
+        }
+        uint32_t half = 0u, m = sub;
+        for (int c = 0; c < nq / 2; ++c) {
+          half |= m & (0u - m);
+          m &= m - 1u;
+        }
+        sub = half;
+      }
+      wave_lds_sync();
+      // Key rows by position (zeros for the padding).
+      const int padded = (n + kChunk - 1) / kChunk * kChunk;
+      constexpr int kT = (kStageEntries + 63) / 64;
+      int32_t pv[kT];
+      uint2 kw[kT];
+#pragma unroll
+      for (int t = 0; t < kT; ++t) {
+        const int e = t * 64 + lane;
+        pv[t] = e < n ? __float_as_int(s_ent[wave][e < kStageEntries ? e : 0][kPosSlot]) : 0;
+        kw[t] = e < n ? packed_key_row(k, seg * N + pv[t], total) : make_uint2(0u, 0u);
+      }
+#pragma unroll
+      for (int t = 0; t < kT; ++t) {
+        const int e = t * 64 + lane;
+        if (e < padded) {
+          *reinterpret_cast<float4*>(&s_ent[wave][e][0]) =
+              make_float4(__uint_as_float(kw[t].x << 16), __uint_as_float(kw[t].x & 0xFFFF0000u),
+                          __uint_as_float(kw[t].y << 16), __int_as_float(pv[t]));
+          if (e >= n) s_um[wave][e] = uint16_t(0);
+        }
+      }
+      wave_lds_sync();
+      return sub;
+    };
 
     // Queries that search one list form a group (nearly always the whole tile).
     while (pending != 0u) {
       const int leader = __ffs(int(pending)) - 1;
       const int64_t g_seg = __builtin_amdgcn_readlane(int32_t(my_seg), leader);
       const int g_lvl = __builtin_amdgcn_readlane(my_lvl, leader);
-      const uint32_t gmask =
-          uint32_t(wave_ballot(my_i >= 0 && my_seg == g_seg && my_lvl == g_lvl)) & pending;
+      uint32_t gmask = uint32_t(wave_ballot(my_i >= 0 && my_seg == g_seg && my_lvl == g_lvl)) & pending;
+      int n_union = 0;  // index rows: the entries of the group's union
+      if constexpr (kIdx) gmask = build_union(gmask, g_seg, n_union);
       pending &= ~gmask;
       const int32_t* lpos = sorted_pos + g_seg * N;
       const uint2* lkey = keys_full + g_seg * N;  // key rows in list order (d_k = 3)
       int32_t ln = int32_t(N);
-      if (causal && g_lvl <= t_hi) {
+      if (!kIdx && causal && g_lvl <= t_hi) {
         const int64_t off = g_seg * cap + ((int64_t(1) << g_lvl) - (int64_t(1) << t0));
         lpos = list_pos + off;
         lkey = keys_list + off;
@@ -640,7 +902,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       // A window outside the list (not produced by the bounds kernel) counts
       // as empty.
       const bool in_grp = ((gmask >> qn) & 1u) != 0u;
-      const bool mine = in_grp && 0 <= my_a && my_a <= my_b && my_b < ln;
+      const bool mine = in_grp && (kIdx || (0 <= my_a && my_a <= my_b && my_b < ln));
       const int32_t my_lim = causal ? pool_limit(my_i, chunk) : int32_t(N - 1);
       float qv[KD];
       if constexpr (kLateQ) {
@@ -758,11 +1020,17 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) pvs[kk] = __float_as_int(krow[kk * KREC + kPosSlot]);
         scl = 1.0f;
+        // Whether entry kk of this lane's four is in its query's window:
+        // index rows, bit qn of the entry's query mask; list ranges, the
+        // range and pool tests.
+        uint2 qm = make_uint2(0u, 0u);
+        if constexpr (kIdx) qm = *reinterpret_cast<const uint2*>(&s_um[wave][r0 + kg * 4]);
         if constexpr (!kVar) {
 #pragma unroll
           for (int kk = 0; kk < 4; ++kk) {
             const int32_t r = r0 + kg * 4 + kk;
-            const bool in = uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
+            const bool in = kIdx ? (((kk < 2 ? qm.x : qm.y) >> (16 * (kk & 1) + qn)) & 1u) != 0u
+                                 : uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
             // eps + the squared distance, eps first (one addition fewer).
             float d2 = eps;
 #pragma unroll
@@ -783,7 +1051,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
           for (int kk = 0; kk < 4; ++kk) {
             const int32_t r = r0 + kg * 4 + kk;
-            ins[kk] = uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
+            ins[kk] = kIdx ? (((kk < 2 ? qm.x : qm.y) >> (16 * (kk & 1) + qn)) & 1u) != 0u
+                           : uint32_t(r) - uint32_t(a_eff) <= span && uint32_t(pvs[kk]) <= lim_u;
             sc[kk] = variant_term<KD>(score, qv, krow + kk * KREC, dk, eps, rsd, qnorm);
           }
           if (smax) {
@@ -849,9 +1118,10 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 
       // The chunks that meet some window, in list order: run by run (a run is
       // a stretch of chunks the windows cover without a gap; nearly always one
-      // per tile), each run kStage chunks at a time.
-      const int a_ch = mine ? my_a / kChunk : INT32_MAX;
-      const int b_ch = mine ? my_b / kChunk : INT32_MIN;
+      // per tile), each run kStage chunks at a time.  Index rows: the staged
+      // union is one run of at most kStage chunks.
+      const int a_ch = !mine ? INT32_MAX : kIdx ? (n_union > 0 ? 0 : INT32_MAX) : my_a / kChunk;
+      const int b_ch = !mine ? INT32_MIN : kIdx ? (n_union + kChunk - 1) / kChunk - 1 : my_b / kChunk;
       unsigned char* const v0 = s_v[wave];
       unsigned char* const v1 = s_v[wave] + VS::kBytes;
       for (int c = wave_min_int(a_ch); c != INT32_MAX;) {
@@ -866,8 +1136,8 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         for (int cb = c; cb <= e; cb += kStage) {
           const int nch = e - cb + 1 < kStage ? e - cb + 1 : kStage;
           // Stage the positions and key rows of list entries cb*kChunk ..
-          // (cb + nch)*kChunk - 1.
-          {
+          // (cb + nch)*kChunk - 1 (index rows: staged with the union).
+          if constexpr (!kIdx) {
             const int32_t base = cb * kChunk;
             // This lane's query row as bfloat16 bits (row 0 for a lane
             // without a window: read, not used).  The opaque row index keeps
@@ -1004,10 +1274,10 @@ hipError_t launch_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v
   const int64_t want = ceil_div(tiles, kTileWaves);
   const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
   const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
-#define ZETA_TILE_LAUNCH(OFF, HIST, MODE)                                                                         \
-  hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST, MODE>), dim3(blocks), dim3(kTileWaves * 64), 0,    \
-                     stream, q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk,           \
-                     causal ? 1 : 0, chunk, lp.t0, lp.t_hi, lp.cap, eps, hm.k, hm.v, out)
+#define ZETA_TILE_LAUNCH(OFF, HIST, MODE)                                                                          \
+  hipLaunchKernelGGL((select_attend_tile_kernel<DV, DK, OFF, HIST, MODE, false>), dim3(blocks), dim3(kTileWaves * 64), \
+                     0, stream, q, k, v, perm, list_pos, q_order, bounds, keys_full, keys_list, total, N, dk,         \
+                     causal ? 1 : 0, chunk, lp.t0, lp.t_hi, lp.cap, eps, hm.k, hm.v, out, nullptr, 0)
 #define ZETA_TILE_LAUNCH4(MODE)             \
   if (off32) {                              \
     if (hist)                               \
@@ -1058,9 +1328,78 @@ hipError_t launch_tile_dk(const uint16_t* q, const uint16_t* k, const uint16_t* 
                               keys_list, score, eps, hm, out, stream);
 }
 
+// The attend call's matrix-core tiles (d_k = 3): 16 consecutive queries of
+// the processing order per wavefront, over the union of their index rows.
+template <int DV>
+hipError_t launch_idx_tile_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t S, int64_t N,
+                             int topk, const int32_t* idx, const int32_t* q_order, int score, float eps, HistMean hm,
+                             uint16_t* out, hipStream_t stream) {
+  const int64_t total = S * N;
+  const int64_t tiles = ceil_div(total, kTileQ);
+  const int64_t want = ceil_div(tiles, kTileWaves);
+  const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
+  const bool off32 = N * int64_t(DV) <= int64_t(0x7FFFFFFF);
+#define ZETA_IDX_LAUNCH(OFF, HIST, MODE)                                                                         \
+  hipLaunchKernelGGL((select_attend_tile_kernel<DV, 3, OFF, HIST, MODE, true>), dim3(blocks), dim3(kTileWaves * 64), \
+                     0, stream, q, k, v, nullptr, nullptr, q_order, nullptr, nullptr, nullptr, total, N, 3, 0, 0, 0, \
+                     0, 0, eps, hm.k, hm.v, out, idx, topk)
+#define ZETA_IDX_LAUNCH4(MODE)            \
+  if (off32) {                            \
+    if (hist)                             \
+      ZETA_IDX_LAUNCH(true, true, MODE);  \
+    else                                  \
+      ZETA_IDX_LAUNCH(true, false, MODE); \
+  } else {                                \
+    if (hist)                             \
+      ZETA_IDX_LAUNCH(false, true, MODE); \
+    else                                  \
+      ZETA_IDX_LAUNCH(false, false, MODE);\
+  }
+  const bool hist = hm.k != nullptr;
+  switch (score) {
+    case kScoreDot:
+      ZETA_IDX_LAUNCH4(kScoreDot)
+      break;
+    case kScoreNegEuclid:
+      ZETA_IDX_LAUNCH4(kScoreNegEuclid)
+      break;
+    case kScoreInvEuclid:
+      ZETA_IDX_LAUNCH4(kScoreInvEuclid)
+      break;
+    case kScoreNormDot:
+      ZETA_IDX_LAUNCH4(kScoreNormDot)
+      break;
+    default:
+      ZETA_IDX_LAUNCH4(kScoreCauchy)
+      break;
+  }
+#undef ZETA_IDX_LAUNCH4
+#undef ZETA_IDX_LAUNCH
+  return hipGetLastError();
+}
+
 }  // namespace
 
 bool tile_supports(int dv) { return tile_dv(dv); }
+
+hipError_t launch_attend_idx_tile(const void* q, const void* k, const void* v, int64_t S, int64_t N, int dv, int topk,
+                                  const int32_t* idx, const int32_t* q_order, int score, float eps, HistMean hm,
+                                  void* out, hipStream_t stream) {
+  const uint16_t* qq = static_cast<const uint16_t*>(q);
+  const uint16_t* kk = static_cast<const uint16_t*>(k);
+  const uint16_t* vv = static_cast<const uint16_t*>(v);
+  uint16_t* oo = static_cast<uint16_t*>(out);
+  switch (dv) {
+    case 32:
+      return launch_idx_tile_t<32>(qq, kk, vv, S, N, topk, idx, q_order, score, eps, hm, oo, stream);
+    case 64:
+      return launch_idx_tile_t<64>(qq, kk, vv, S, N, topk, idx, q_order, score, eps, hm, oo, stream);
+    case 128:
+      return launch_idx_tile_t<128>(qq, kk, vv, S, N, topk, idx, q_order, score, eps, hm, oo, stream);
+    default:
+      return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int topk, bool causal, int chunk,
                                const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,

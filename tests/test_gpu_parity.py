@@ -376,9 +376,11 @@ def test_forward_deterministic_and_complete():
 
 @pytest.mark.parametrize("causal", [True, False])
 def test_processing_order_changes_nothing(causal):
-    """select and attend give bit-identical results in position order, in the
-    queries' Z-order and in a random order; entries outside 0..N-1 are
-    skipped."""
+    """select gives bit-identical results in position order, in the queries'
+    Z-order and in a random order; entries outside 0..N-1 are skipped.  The
+    bfloat16 attend call shares each 16 queries' rows when given an order:
+    its outputs agree with the per-query ones to float32 rounding (one
+    bfloat16 unit in the last place)."""
     cfg = 2
     w, x, _ = inputs(cfg)
     log(f"processing order config {cfg} causal={causal}")
@@ -397,7 +399,8 @@ def test_processing_order_changes_nothing(causal):
         torch.cuda.synchronize()
         torch.cuda.synchronize()
         assert torch.equal(idx0, idx1)
-        assert torch.equal(out0.view(torch.int16), out1.view(torch.int16))
+        a, b = host(out0).astype(np.float64), host(out1).astype(np.float64)
+        assert np.all(np.abs(a - b) <= 2.0 ** -7 * np.maximum(np.abs(a), np.abs(b)) + 1e-5)
     # A partial order: rows whose slot holds an out-of-range entry stay untouched.
     part = np.argsort(oc["q_codes"], axis=1, kind="stable").astype(np.int32)
     part[:, ::3] = -1
@@ -421,7 +424,10 @@ def test_forward_zorder_matches_position_order():
     b = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, zorder=False, return_intermediates=True)
     torch.cuda.synchronize()
     assert torch.equal(a["idx"], b["idx"])
-    assert torch.equal(a["out"].view(torch.int16), b["out"].view(torch.int16))
+    # The four calls: with the Z-order the attend call runs on shared tiles
+    # (float32 rounding apart, one bfloat16 unit in the last place).
+    oa, ob = host(a["out"]).astype(np.float64), host(b["out"]).astype(np.float64)
+    assert np.all(np.abs(oa - ob) <= 2.0 ** -7 * np.maximum(np.abs(oa), np.abs(ob)) + 1e-5)
     c = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, zorder=True, fused=True)
     d = zeta.forward(q, k, v, w.topk, 0.5, True, w.bits, zorder=False, fused=True)
     torch.cuda.synchronize()
