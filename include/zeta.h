@@ -236,9 +236,20 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
  *   q, k   [B][H][N][d_k], v [B][H][N][d_v], out [B][H][N][d_v], all `dtype`.
  *   idx      int32 [B*H][N][topk]; valid entries (0 <= j < N) first, then -1.
  *   q_order  optional int32 [B*H][N] processing order, as for
- *            zeta_select_topk (NULL: position order).  Neighbouring queries
- *            of zeta_query_order's order gather mostly the same value rows,
- *            which then come from cache; the output bits do not depend on it.
+ *            zeta_select_topk (NULL: position order; entries outside 0..N-1
+ *            are skipped and leave their rows untouched).  Without it each
+ *            query is computed alone, over its row in slot order, and its
+ *            bits depend only on its own row.  With it, for bfloat16 inputs
+ *            with d_k = 3, d_v of 32, 64 or 128 and topk <= 128, each 16
+ *            consecutive queries of the order form a tile: the union of
+ *            their rows is loaded once and the weighted sums run on the
+ *            matrix cores (scores split into two bfloat16 parts, float32
+ *            accumulation), as in zeta_select_attend_fwd.  The outputs then
+ *            agree with the per-query ones to float32 rounding and repeat
+ *            bit for bit for the same order, but a query's last bits follow
+ *            the tile it shares.  zeta_query_order's order gives tiles whose
+ *            rows overlap and makes the call fastest; in other orders the
+ *            tiles split (down to single queries) until their unions fit.
  *   score    a zeta_score_t (UNSUPPORTED otherwise).
  *   eps      gamma^2: finite and > 0 (read by the Cauchy and inverse
  *            Euclidean scores).

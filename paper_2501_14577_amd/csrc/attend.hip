@@ -27,7 +27,10 @@
 // Queries are taken in an optional processing order (a permutation per
 // segment).  Walking queries in Z-order makes neighbouring wavefronts gather
 // overlapping rows; the logical blocks of each XCD are contiguous, so those
-// wavefronts share one L2.  The order never changes any result.
+// wavefronts share one L2.  The order never changes a result of this kernel.
+// Given an order, bfloat16 calls with d_k = 3, d_v <= 128 and k <= 128 run on
+// the matrix-core tiles instead (tile.hip), which share each 16 queries'
+// rows.
 #include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"

@@ -54,6 +54,19 @@
 // zero outside its range, so its output depends only on its own window: the
 // result is the same whatever tile the query falls in, i.e. for any
 // processing order.
+//
+// The attend call given index rows and a processing order runs the same
+// chunk pipeline (kIdx): a wavefront takes 16 consecutive queries of the
+// order and stages the union of their index rows as one run of chunks, each
+// entry with the mask of the tile's queries whose rows hold it (a query's
+// score is zero where its bit is clear).  The union is found without
+// barriers, per wavefront: for segments of at most 65536 rows as a bitmap of
+// positions (entries in position order, each entry's index its rank), else
+// in a hash table keyed by position (entries in slot order).  A union larger
+// than the stage, or a row that repeats a position (each occurrence is its
+// own term), splits the tile in halves, down to one query, whose row is
+// staged slot by slot.  A query's sums are then grouped by the union it
+// shares, so its last bits depend on its tile.
 #include "attend_device.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -79,7 +92,6 @@ constexpr int kIdxHashBits = 10;
 constexpr int kIdxHash = 1 << kIdxHashBits;
 constexpr int kIdxProbes = 8;
 constexpr int kIdxUnionCap = 288;
-constexpr int kIdxRounds = kTileQ * kIdxTileMaxTopk / 64;  // 64-element rounds over the tile's rows
 constexpr uint32_t kIdxEmpty = 0xFFFFFFFFu;
 
 // ---- window bounds ---------------------------------------------------------
@@ -644,41 +656,46 @@ __global__ void __launch_bounds__(kTileWaves * 64)
     constexpr bool kLateQ = DK == 3 && !kVar && !kHist && !kIdx;
 
     // ---- index rows: the union of a group's rows ----
-    // Slot s of tile query t's row is element (t << lg) + s of the tile's
-    // rows (lg: log2 of topk rounded up to a power of two); round r holds
-    // elements 64r .. 64r + 63, one per lane.
-    const int idx_lg = kIdx ? (topk > 1 ? 32 - __clz(topk - 1) : 0) : 0;
-    const int idx_rounds = idx_lg >= 2 ? 1 << (idx_lg - 2) : 1;
+    // Slot s of tile query t's row is element 128t + s of the tile's rows;
+    // round r holds elements 64r .. 64r + 63 (slots of one row), one per
+    // lane.
+    constexpr int kRowStride = kIdxTileMaxTopk;
+    constexpr int kRounds = kTileQ * kRowStride / 64;
     // Calls body(j, t, s) for every element of the tile's rows, one round at
-    // a time: j is slot s of query t's row, or -1 where t is not in `sub`,
-    // s >= topk or t >= 16.  The index loads run kAhead rounds ahead of
-    // their use.  body returns false to stop early.
+    // a time: j is slot s of query t's row, or -1 where t is not in `sub` or
+    // s >= topk.  The index loads run kAhead rounds ahead of their use; each
+    // is issued whatever its slot (one outside the rows reads a slot that
+    // exists and is replaced by -1), so that the loads in flight are counted
+    // exactly and a round waits only for its own.
     auto for_rows = [&](uint32_t sub, int64_t seg, auto&& body) {
-      constexpr int kAhead = 8;
+      constexpr int kAhead = 8;  // divides kRounds
       const int32_t my_row = ((sub >> qn) & 1u) != 0u ? int32_t(seg * N + my_i) : -1;  // rows < 2^31
+      // The raw loaded value; whether it is a slot of a row is decided where
+      // it is used, so that nothing waits for a load before its round.
       auto load = [&](int r) -> int32_t {
-        const int e = r * 64 + lane;
-        const int qq = e >> idx_lg, sl = e & ((1 << idx_lg) - 1);
-        const int32_t row = __shfl(my_row, qq & (kTileQ - 1), 64);
-        return (r < idx_rounds && qq < kTileQ && row >= 0 && sl < topk) ? idx[int64_t(row) * topk + sl] : -1;
+        const int rr = r < kRounds ? r : 0;
+        const int qq = rr * 64 / kRowStride, sl = rr * 64 % kRowStride + lane;
+        const int32_t row = __builtin_amdgcn_readlane(my_row, qq);
+        return idx[int64_t(row >= 0 ? row : 0) * topk + (sl < topk ? sl : 0)];
       };
       int32_t ring[kAhead];
 #pragma unroll
       for (int u = 0; u < kAhead; ++u) ring[u] = load(u);
-#pragma unroll 1
-      for (int r0 = 0; r0 < idx_rounds; r0 += kAhead) {
-        bool go = true;
+      // Straight-line code (all rounds unrolled): the wait before each round
+      // is then exactly for its own load.
+#pragma unroll
+      for (int r0 = 0; r0 < kRounds; r0 += kAhead) {
 #pragma unroll
         for (int u = 0; u < kAhead; ++u) {
           const int r = r0 + u;
-          const int32_t j = ring[u];
-          ring[u] = load(r + kAhead);
-          if (go && r < idx_rounds) {
-            const int e = r * 64 + lane;
-            go = body(j, e >> idx_lg, e & ((1 << idx_lg) - 1));
-          }
+          const int qq = r * 64 / kRowStride, sl = r * 64 % kRowStride + lane;
+          const bool ok = __builtin_amdgcn_readlane(my_row, qq) >= 0 && sl < topk;
+          int32_t x = ring[u];
+          asm volatile("" : "+v"(x));  // used here, after this round's wait
+          const int32_t j = ok ? x : -1;
+          if (r + kAhead < kRounds) ring[u] = load(r + kAhead);
+          body(j, qq, sl);
         }
-        if (!go) break;
       }
     };
     // Inserts the rows of the queries in `sub` into the hash table (keyed by
@@ -700,8 +717,9 @@ __global__ void __launch_bounds__(kTileWaves * 64)
       int cnt = 0;
       bool bad = false;
       uint32_t dup = 0u;
-      for_rows(sub, seg, [&](int32_t j, int qq, int sl) -> bool {
-        bool todo = j >= 0 && j < N;
+      for_rows(sub, seg, [&](int32_t j, int qq, int) {
+        if (bad) return;
+        bool todo = uint32_t(j) < uint32_t(N);
         const uint32_t bit = 1u << (qq & (kTileQ - 1));
         uint32_t h = (uint32_t(j) * 0x9E3779B1u) >> (32 - kIdxHashBits);
 #pragma unroll 1
@@ -717,7 +735,6 @@ __global__ void __launch_bounds__(kTileWaves * 64)
           if (wave_ballot(todo) == 0ull) break;
         }
         bad = wave_ballot(todo) != 0ull || cnt > kStageEntries;
-        return !bad;
       });
       if (bad || wave_ballot(dup != 0u) != 0ull) return -1;
       wave_lds_sync();
@@ -740,29 +757,39 @@ __global__ void __launch_bounds__(kTileWaves * 64)
     // buffers), then per word the count of union entries before it, so that
     // an entry's index is its rank among the union's positions; a second
     // pass over the rows sets the query masks.  The entries are in position
-    // order.
+    // order.  Lane l owns bitmap words 32l .. 32l + 31 (and their counts);
+    // the 16-byte pieces of each lane's words are stored XOR-swizzled by
+    // lane so that the wavefront's piece-wise reads and writes fall in
+    // different bank groups.
     auto bitmap_union = [&](uint32_t sub, int64_t seg) -> int {
       uint32_t* const bm = reinterpret_cast<uint32_t*>(&s_v[wave][0]);
       uint16_t* const pre = reinterpret_cast<uint16_t*>(&s_ent[wave][0][0]);  // until the positions are written
       uint32_t* const mq = reinterpret_cast<uint32_t*>(&s_um[wave][0]);         // two masks per word
+      // Physical index of bitmap word w (pieces of 4 words) and of count w
+      // (pieces of 8 counts).
+      // (Piece bits of w XORed with bits of its owner lane w >> 5.)
+      auto bm_at = [](uint32_t w) -> uint32_t { return w ^ ((w >> 4) & 0x1Cu); };
+      auto pre_at = [](uint32_t w) -> uint32_t { return w ^ ((w >> 4) & 0x18u); };
+      const int bsw = (lane >> 1) & 7, psw = (lane >> 2) & 3;
+      uint32_t wd[32];
+      auto read_words = [&]() {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const uint4 x = reinterpret_cast<const uint4*>(bm)[lane * 8 + (t ^ bsw)];
+          wd[4 * t] = x.x;
+          wd[4 * t + 1] = x.y;
+          wd[4 * t + 2] = x.z;
+          wd[4 * t + 3] = x.w;
+        }
+      };
 #pragma unroll
       for (int t = 0; t < 8; ++t) reinterpret_cast<uint4*>(bm)[t * 64 + lane] = make_uint4(0u, 0u, 0u, 0u);
       wave_lds_sync();
-      for_rows(sub, seg, [&](int32_t j, int, int) -> bool {
-        if (j >= 0 && j < N) atomicOr(&bm[j >> 5], 1u << (j & 31));
-        return true;
+      for_rows(sub, seg, [&](int32_t j, int, int) {
+        if (uint32_t(j) < uint32_t(N)) atomicOr(&bm[bm_at(uint32_t(j) >> 5)], 1u << (j & 31));
       });
       wave_lds_sync();
-      // Lane l holds words 32l .. 32l + 31 and writes their prefix counts.
-      uint32_t wd[32];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const uint4 x = reinterpret_cast<const uint4*>(bm)[lane * 8 + t];
-        wd[4 * t] = x.x;
-        wd[4 * t + 1] = x.y;
-        wd[4 * t + 2] = x.z;
-        wd[4 * t + 3] = x.w;
-      }
+      read_words();
       uint32_t tot = 0u;
 #pragma unroll
       for (int i = 0; i < 32; ++i) tot += uint32_t(__popc(wd[i]));
@@ -787,28 +814,28 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         }
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-          reinterpret_cast<uint4*>(pre)[lane * 4 + t] =
+          reinterpret_cast<uint4*>(pre)[lane * 4 + (t ^ psw)] =
               make_uint4(packed[4 * t], packed[4 * t + 1], packed[4 * t + 2], packed[4 * t + 3]);
       }
       if (lane < kStageEntries / 8) reinterpret_cast<uint4*>(mq)[lane] = make_uint4(0u, 0u, 0u, 0u);
       wave_lds_sync();
       uint32_t dup = 0u;
-      for_rows(sub, seg, [&](int32_t j, int qq, int) -> bool {
-        if (j >= 0 && j < N) {
-          const int w = j >> 5;
-          const int id = int(pre[w]) + __popc(bm[w] & ((1u << (j & 31)) - 1u));
+      for_rows(sub, seg, [&](int32_t j, int qq, int) {
+        if (uint32_t(j) < uint32_t(N)) {
+          const uint32_t w = uint32_t(j) >> 5;
+          const int id = int(pre[pre_at(w)]) + __popc(bm[bm_at(w)] & ((1u << (j & 31)) - 1u));
           const uint32_t bit = (1u << qq) << (16 * (id & 1));
           dup |= atomicOr(&mq[id >> 1], bit) & bit;
         }
-        return true;
       });
       if (wave_ballot(dup != 0u) != 0ull) return -1;
       wave_lds_sync();
-      // Positions, lane by lane in word order (the prefix counts are done).
+      // Positions, lane by lane in word order (the counts are no longer read).
+      read_words();
       int id = int(base);
-#pragma unroll 4
+#pragma unroll
       for (int i = 0; i < 32; ++i) {
-        uint32_t m = bm[lane * 32 + i];
+        uint32_t m = wd[i];
         while (m != 0u) {
           const int b = __ffs(int(m)) - 1;
           s_ent[wave][id][kPosSlot] = __int_as_float(((lane * 32 + i) << 5) + b);
@@ -831,13 +858,12 @@ __global__ void __launch_bounds__(kTileWaves * 64)
         const int nq = __popc(sub);
         int cnt;
         if (nq == 1) {
-          for_rows(sub, seg, [&](int32_t j, int qq, int sl) -> bool {
-            if (((sub >> qq) & 1u) != 0u && sl < topk && qq < kTileQ) {
-              const bool ok = j >= 0 && j < N;
+          for_rows(sub, seg, [&](int32_t j, int qq, int sl) {
+            if (((sub >> qq) & 1u) != 0u && sl < topk) {
+              const bool ok = uint32_t(j) < uint32_t(N);
               s_ent[wave][sl][kPosSlot] = __int_as_float(ok ? j : 0);
               s_um[wave][sl] = ok ? uint16_t(1u << qq) : uint16_t(0);
             }
-            return true;
           });
           cnt = topk;
         } else {
