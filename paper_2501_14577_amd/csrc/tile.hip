@@ -116,8 +116,12 @@ constexpr int kMargin = 192;    // of them before the run's first insertion poin
 // indexed directly, so that every access compiles to an LDS instruction (a
 // pointer kept in a struct would lose the address space and go through the
 // slower flat path).
+// Positions are stored in blocks of kScanStep entries at a stride of
+// kPosStride: block b starts in 16-byte bank group 9b mod 16, so the scans of
+// lanes in different blocks of the region read different bank groups.
+constexpr int kPosStride = 36;
 __shared__ uint32_t s_bnd_codes[kBndWaves][kRegion];
-__shared__ __align__(16) int32_t s_bnd_pos[kBndWaves][kRegion];
+__shared__ __align__(16) int32_t s_bnd_pos[kBndWaves][kRegion / 32 * kPosStride];
 
 struct LaneList {
   const uint32_t* codes;
@@ -128,6 +132,7 @@ struct LaneList {
 
 constexpr int kScanStep = 32;  // list entries examined per step of lane_scan (one bit each of a 32-bit mask)
 static_assert(kScanStep == 32, "the scan masks are 32-bit words");
+static_assert(kRegion % 64 == 0, "staged in whole rounds of 64 entries, two blocks each");
 
 // The query's in-pool entries B .. B + kScanStep - 1 (B a multiple of
 // kScanStep) as a bit mask, first entry in the highest bit: bit 31 - j is
@@ -140,7 +145,7 @@ __device__ __forceinline__ uint32_t pool_bits(const LaneList& L, int32_t B) {
   const uint32_t nl = uint32_t(-1 - L.limit);  // pos + nl < 0 exactly when pos <= limit (no overflow)
   uint32_t mask = 0u;
   if (L.r1 > L.r0 && B >= L.r0 && B + kScanStep <= L.r0 + kRegion) {
-    const int4* blk = reinterpret_cast<const int4*>(&s_bnd_pos[L.wave][B - L.r0]);
+    const int4* blk = reinterpret_cast<const int4*>(&s_bnd_pos[L.wave][(B - L.r0) / kScanStep * kPosStride]);
 #pragma unroll
     for (int t = 0; t < kScanStep / 4; ++t) {
       const int4 v = blk[t];
@@ -281,7 +286,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
 #pragma unroll
         for (int t = 0; t < kRegion / 64; ++t) {
           s_bnd_codes[wave][t * 64 + lane] = cv[t];
-          s_bnd_pos[wave][t * 64 + lane] = pv[t];
+          s_bnd_pos[wave][(2 * t + lane / kScanStep) * kPosStride + lane % kScanStep] = pv[t];
         }
       }
       wave_lds_sync();
