@@ -213,6 +213,10 @@ zeta_status_t zeta_query_order(const int32_t* q_order, int64_t n_segments, int64
  *   idx           int32 [n_segments][N][topk] output, indexed by position.
  *   topk          1..ZETA_MAX_TOPK; causal 0 or 1; chunk 0 (exact prefix) or
  *                 a chunk size M >= 1 (requires causal; INVALID_ARG otherwise).
+ *   workspace     at least zeta_workspace_size(...) bytes, 16-byte aligned
+ *                 (the prefix lists and each query's window as list-index
+ *                 bounds, 8 bytes per query; WORKSPACE / INVALID_ARG
+ *                 otherwise).
  */
 zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_codes,
                                const int32_t* perm, int64_t n_segments, int64_t N, int topk,

@@ -40,8 +40,6 @@ constexpr int64_t kLevelTile = 2048;
 constexpr int64_t kRadixInlineTiles = 32;
 
 // ---- select ---------------------------------------------------------------
-constexpr int kSelWavesPerBlock = 4;
-constexpr int kSelRun = 32;  // consecutive processing-order slots served by one wavefront
 constexpr int kMaxLevels = 32;
 
 // ---- attend ---------------------------------------------------------------
@@ -129,20 +127,25 @@ inline SortWs sort_ws(int64_t S, int64_t N, int code_bits) {
   return w;
 }
 
+// bytes: the prefix lists (none for non-causal calls or short segments);
+// call_bytes: zeta_select_topk's need, the lists and then the window bounds
+// (8 bytes per query) at bounds_off.
 struct SelectWs {
-  size_t cnt_off, codes_off, pos_off, bytes;
+  size_t cnt_off, codes_off, pos_off, bytes, bounds_off, call_bytes;
 };
 inline SelectWs select_ws(int64_t S, int64_t N, int topk, int causal) {
   SelectWs w;
   w.cnt_off = w.codes_off = w.pos_off = w.bytes = 0;
-  if (!causal) return w;
   ListPlan lp = list_plan(N, topk);
-  if (lp.levels == 0) return w;
-  const int64_t tiles = ceil_div(N, kSortTile);
-  const size_t list = align_up(size_t(S) * size_t(lp.cap) * sizeof(uint32_t));
-  w.codes_off = align_up(size_t(S) * size_t(tiles) * kMaxLevels * sizeof(uint32_t));
-  w.pos_off = w.codes_off + list;
-  w.bytes = w.pos_off + list;
+  if (causal && lp.levels > 0) {
+    const int64_t tiles = ceil_div(N, kSortTile);
+    const size_t list = align_up(size_t(S) * size_t(lp.cap) * sizeof(uint32_t));
+    w.codes_off = align_up(size_t(S) * size_t(tiles) * kMaxLevels * sizeof(uint32_t));
+    w.pos_off = w.codes_off + list;
+    w.bytes = w.pos_off + list;
+  }
+  w.bounds_off = align_up(w.bytes);
+  w.call_bytes = w.bounds_off + align_up(size_t(S) * size_t(N) * 2 * sizeof(int32_t));
   return w;
 }
 
@@ -176,8 +179,9 @@ struct FusedWs {
 };
 inline FusedWs fused_ws(int64_t S, int64_t N, int topk, int causal) {
   FusedWs w;
-  w.bounds_off = align_up(select_ws(S, N, topk, causal).bytes);
-  w.keys_full_off = w.bounds_off + align_up(size_t(S) * size_t(N) * 2 * sizeof(int32_t));
+  const SelectWs sel = select_ws(S, N, topk, causal);
+  w.bounds_off = sel.bounds_off;
+  w.keys_full_off = sel.call_bytes;
   w.keys_list_off = w.keys_full_off + align_up(size_t(S) * size_t(N) * 8);
   const ListPlan lp = list_plan(N, topk);
   const size_t lists = (causal && lp.levels > 0) ? size_t(S) * size_t(lp.cap) : 0;

@@ -18,13 +18,9 @@
 //   list_scatter: stable compaction of each tile into every F_t it feeds
 //                 (one ballot per level and 64 keys; earlier tiles' counts
 //                 give the base);
-//   select:       one wavefront serves a run of 32 consecutive queries of the
-//                 processing order, one after another: a 64-way search for
-//                 the insertion point (three rounds for 2^16 keys, or one
-//                 probe after the previous query's point when the list is
-//                 the same and the code no smaller), then ballot-compacted
-//                 scans to the right and left collecting the in-pool keys,
-//                 staged in LDS and written as one coalesced row.
+// The windows themselves are found by the one-pass call's kernels (tile.hip):
+// window_bounds gives each query's list-index bounds, and idx_rows writes the
+// rows from them.
 //
 // query_order (the zeta_query_order entry point) regroups a processing order,
 // typically the Z-order of the query codes, by the list each query searches,
@@ -188,78 +184,6 @@ __global__ void __launch_bounds__(256)
   order_out[slot] = q_order != nullptr ? q_order[slot] : int32_t(slot % N);
 }
 
-__global__ void __launch_bounds__(kSelWavesPerBlock * 64)
-    select_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
-                  const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
-                  const int32_t* __restrict__ list_pos, int64_t total, int64_t N, int topk, int causal,
-                  int chunk, int t0, int t_hi, int64_t cap, const int32_t* __restrict__ order,
-                  int32_t* __restrict__ idx) {
-  extern __shared__ int32_t s_sel[];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  int32_t* lbuf = s_sel + wave * 2 * topk;  // left part, filled from its end
-  int32_t* rbuf = lbuf + topk;              // right part, filled from its start
-  const int64_t runs = (total + kSelRun - 1) / kSelRun;
-
-  const int64_t nb = gridDim.x;
-  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kSelWavesPerBlock < runs; blk += nb) {
-    const int64_t run = blk * kSelWavesPerBlock + wave;
-    if (run >= runs) continue;
-    const int64_t slot0 = run * kSelRun;
-    // This run's query positions and codes, one per lane, fetched together.
-    int32_t my_i = -1;
-    uint32_t my_key = 0;
-    {
-      const int64_t sl = slot0 + lane;
-      if (lane < kSelRun && sl < total) {
-        const int64_t sg = sl / N;
-        const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
-        if (ii >= 0 && ii < N) {
-          my_i = int32_t(ii);
-          my_key = q_codes[sg * N + ii];
-        }
-      }
-    }
-    const uint32_t* prev_codes = nullptr;
-    uint32_t prev_key = 0;
-    int32_t prev_p = 0;
-    for (int u = 0; u < kSelRun; ++u) {
-      const int64_t slot = slot0 + u;
-      if (slot >= total) break;
-      const int32_t i = __builtin_amdgcn_readlane(my_i, u);
-      const uint32_t key = uint32_t(__builtin_amdgcn_readlane(int32_t(my_key), u));
-      if (i < 0) continue;  // not a permutation entry: nothing to do
-      const int64_t seg = slot / N;
-      const int64_t g = seg * N + i;
-
-      const QueryList L =
-          query_list(sorted_codes, perm, list_codes, list_pos, seg, N, i, causal, t0, t_hi, cap, chunk);
-      int got_l = 0, got_r = 0;
-      if (L.n > 0) {  // an empty pool (the chunked rule's first chunk) selects nothing
-        const int32_t p = (L.codes == prev_codes && key >= prev_key)
-                              ? wave_lower_bound_near(L.codes, prev_p, L.n, key, lane)
-                              : wave_lower_bound(L.codes, 0, L.n, key, lane);
-        prev_codes = L.codes;
-        prev_key = key;
-        prev_p = p;
-        select_window(L, p, topk, lbuf, rbuf, lane, got_l, got_r);
-      }
-      wave_lds_sync();
-
-      int32_t* row = idx + g * topk;
-      const int total_sel = got_l + got_r;
-      for (int c = lane; c < topk; c += 64) {
-        int32_t v = -1;
-        if (c < got_l)
-          v = lbuf[topk - got_l + c];
-        else if (c < total_sel)
-          v = rbuf[c - got_l];
-        row[c] = v;
-      }
-      wave_lds_sync();
-    }
-  }
-}
 
 }  // namespace
 
@@ -312,22 +236,16 @@ hipError_t launch_prefix_lists(const uint32_t* sorted_codes, const int32_t* perm
 hipError_t launch_select(const uint32_t* q_codes, const uint32_t* sorted_codes, const int32_t* perm,
                          int64_t S, int64_t N, int topk, bool causal, int chunk, const int32_t* q_order, int32_t* idx,
                          void* workspace, hipStream_t stream) {
-  const ListPlan lp = list_plan(N, topk);
-  const int64_t total = S * N;
   const uint32_t* list_codes = nullptr;
   const int32_t* list_pos = nullptr;
   if (causal) {
     const hipError_t e = launch_prefix_lists(sorted_codes, perm, S, N, topk, workspace, stream, &list_codes, &list_pos);
     if (e != hipSuccess) return e;
   }
-  const int64_t runs = ceil_div(total, kSelRun);
-  const int64_t want = ceil_div(runs, kSelWavesPerBlock);
-  const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
-  const size_t lds = size_t(kSelWavesPerBlock) * 2 * topk * sizeof(int32_t);
-  hipLaunchKernelGGL(select_kernel, dim3(blocks), dim3(kSelWavesPerBlock * 64), lds, stream, q_codes,
-                     sorted_codes, perm, list_codes, list_pos, total, N, topk, causal ? 1 : 0, chunk, lp.t0,
-                     lp.t_hi, lp.cap, q_order, idx);
-  return hipGetLastError();
+  // The windows as list-index bounds, then the rows from the bounds.
+  int2* bounds = reinterpret_cast<int2*>(static_cast<char*>(workspace) + select_ws(S, N, topk, causal).bounds_off);
+  return launch_tile_windows(nullptr, S, N, 0, topk, causal, chunk, q_codes, sorted_codes, perm, list_codes, list_pos,
+                             q_order, idx, bounds, nullptr, nullptr, true, stream);
 }
 
 }  // namespace zeta

@@ -217,136 +217,5 @@ __device__ __forceinline__ void select_window(const QueryList& L, int32_t p, int
   got_r_out = got_r;
 }
 
-// ---- window bounds ---------------------------------------------------------
-// The same window as select_window, reported as a range of list indices: the
-// pool entries of the window are exactly the in-pool entries of L[a..b]
-// (the left part is every in-pool entry of [a, p), the right part every one
-// of [p, b]).  Used where the window is consumed chunk by chunk of the list.
-
-struct WindowBounds {
-  int32_t a, b;  // first and last list index of the window (a > b: empty)
-  int m;         // in-pool entries in [a, b]
-};
-
-// take_right without the stores: records the list index of the first entry
-// taken (when got is 0) and of the last one.
-__device__ __forceinline__ int take_right_bounds(int32_t pv, int32_t limit, int32_t n, int32_t& cur, int need,
-                                                 int got, int32_t& first, int32_t& last) {
-  const bool ok = pv <= limit;
-  const uint64_t bal = wave_ballot(ok);
-  const int avail = __popcll(bal);
-  const int want = need - got;
-  const int take = avail < want ? avail : want;
-  if (take > 0) {
-    if (got == 0) first = cur + (__ffsll((unsigned long long)bal) - 1);
-    const uint64_t lb = wave_ballot(ok && int(lanes_below(bal)) == take - 1);
-    last = cur + (__ffsll((unsigned long long)lb) - 1);
-  }
-  if (take < avail)
-    cur = last + 1;
-  else
-    cur = cur + 64 < n ? cur + 64 : n;
-  return got + take;
-}
-
-// take_left without the stores: entries cur-64 .. cur-1 in pv, nearest taken
-// first; records the nearest entry taken (when got is 0) as `last` and the
-// farthest as `first`.
-__device__ __forceinline__ int take_left_bounds(int32_t pv, int32_t limit, int32_t cur, int need, int got,
-                                                int32_t& first, int32_t& last) {
-  const bool ok = pv <= limit;
-  const uint64_t bal = wave_ballot(ok);
-  const int avail = __popcll(bal);
-  const int want = need - got;
-  const int take = avail < want ? avail : want;
-  if (take > 0) {
-    if (got == 0) last = cur - 64 + (63 - __clzll((long long)bal));
-    const uint64_t fb = wave_ballot(ok && int(lanes_below(bal)) == avail - take);
-    first = cur - 64 + (__ffsll((unsigned long long)fb) - 1);
-  }
-  return got + take;
-}
-
-// Position readers for the bounds scans: straight from the list, or from a
-// copy of the list range [r0, r1) in LDS with the list itself outside it.
-struct GlobalPos {
-  const int32_t* p;
-  __device__ __forceinline__ int32_t operator()(int32_t e) const { return p[e]; }
-};
-struct RegionPos {
-  const int32_t* g;
-  const int32_t* l;
-  int32_t r0, r1;
-  __device__ __forceinline__ int32_t operator()(int32_t e) const { return (e >= r0 && e < r1) ? l[e - r0] : g[e]; }
-};
-
-template <class Pos>
-__device__ __forceinline__ int scan_right_bounds(const Pos& pos, int32_t n, int32_t limit, int32_t& cur, int need,
-                                                 int got, int32_t& first, int32_t& last, int lane) {
-  while (got < need && cur < n) {
-    const int32_t e = cur + lane;
-    const int32_t pv = e < n ? pos(e) : INT32_MAX;
-    got = take_right_bounds(pv, limit, n, cur, need, got, first, last);
-  }
-  return got;
-}
-
-template <class Pos>
-__device__ __forceinline__ int scan_left_bounds(const Pos& pos, int32_t limit, int32_t cur, int need, int got,
-                                                int32_t& first, int32_t& last, int lane) {
-  while (got < need && cur > 0) {
-    const int32_t e = cur - 64 + lane;
-    const int32_t pv = e >= 0 ? pos(e) : INT32_MAX;
-    got = take_left_bounds(pv, limit, cur, need, got, first, last);
-    cur -= 64;
-  }
-  return got;
-}
-
-// select_window's window as list-index bounds (same scans, same order), with
-// the list's positions read through `pos`.
-template <class Pos>
-__device__ __forceinline__ WindowBounds select_window_bounds(const QueryList& L, const Pos& pos, int32_t p, int topk,
-                                                             int lane) {
-  const int half = topk / 2;
-  int32_t pre_r[kPre], pre_l[kPre];
-#pragma unroll
-  for (int c = 0; c < kPre; ++c) {
-    const int32_t er = p + c * 64 + lane;
-    const int32_t el = p - (c + 1) * 64 + lane;
-    pre_r[c] = er < L.n ? pos(er) : INT32_MAX;
-    pre_l[c] = el >= 0 ? pos(el) : INT32_MAX;
-  }
-  const int need_r = topk - half;
-  int32_t cur_r = p, rf = 0, rl = -1;
-  int got_r = 0;
-#pragma unroll
-  for (int c = 0; c < kPre; ++c)
-    if (got_r < need_r && cur_r < L.n) got_r = take_right_bounds(pre_r[c], L.limit, L.n, cur_r, need_r, got_r, rf, rl);
-  got_r = scan_right_bounds(pos, L.n, L.limit, cur_r, need_r, got_r, rf, rl, lane);
-  const int need_l = half + (need_r - got_r);
-  int got_l = 0;
-  int32_t cur_l = p, lf = 0, ll = -1;
-#pragma unroll
-  for (int c = 0; c < kPre; ++c) {
-    if (got_l < need_l && cur_l > 0) {
-      got_l = take_left_bounds(pre_l[c], L.limit, cur_l, need_l, got_l, lf, ll);
-      cur_l -= 64;
-    }
-  }
-  got_l = scan_left_bounds(pos, L.limit, cur_l, need_l, got_l, lf, ll, lane);
-  if (got_l < need_l && got_r == need_r)
-    got_r = scan_right_bounds(pos, L.n, L.limit, cur_r, topk - got_l, got_r, rf, rl, lane);
-  WindowBounds w;
-  w.m = got_l + got_r;
-  w.a = got_l > 0 ? lf : rf;
-  w.b = got_r > 0 ? rl : ll;
-  if (w.m == 0) {
-    w.a = 0;
-    w.b = -1;
-  }
-  return w;
-}
-
 }  // namespace
 }  // namespace zeta

@@ -4,11 +4,11 @@
 // Appendix E.1 for the attention).
 //
 // A query's window is a run of its sorted list: every in-pool entry of the
-// list range [a, b] around its insertion point (select_window_bounds).  In the
-// processing order of zeta_query_order, 16 consecutive queries search one list
-// at nearby insertion points, so their ranges overlap: together they span
-// about twice the window length where gathering per query would read 16
-// windows.
+// list range [a, b] around its insertion point (select_window's window as
+// list-index bounds).  In the processing order of zeta_query_order, 16
+// consecutive queries search one list at nearby insertion points, so their
+// ranges overlap: together they span about twice the window length where
+// gathering per query would read 16 windows.
 //
 // Two kernels:
 //  1. window_bounds: each query's range [a, b], 8 bytes per processing-order
@@ -106,8 +106,7 @@ constexpr uint32_t kIdxEmpty = 0xFFFFFFFFu;
 // Consecutive slots search one list at nearby insertion points.  The list
 // range of kRegion entries around the run's first insertion point is copied
 // to LDS (codes and positions); a lane reads the list itself only outside it
-// or when its query searches another list.  With idx_out the run's windows
-// are also written as position rows, one wavefront-wide pass per query.
+// or when its query searches another list.
 constexpr int kBndWaves = 4;
 constexpr int kRegion = 512;   // list entries staged per wavefront (a multiple of 32)
 constexpr int kMargin = 192;    // of them before the run's first insertion point (about)
@@ -226,7 +225,7 @@ __global__ void __launch_bounds__(kBndWaves * 64)
                          const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
                          const int32_t* __restrict__ list_pos, const int32_t* __restrict__ order, int64_t total,
                          int64_t N, int topk, int causal, int chunk, int t0, int t_hi, int64_t cap,
-                         int2* __restrict__ bounds, int32_t* __restrict__ idx_out) {
+                         int2* __restrict__ bounds) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t runs = (total + 63) / 64;
@@ -338,29 +337,113 @@ __global__ void __launch_bounds__(kBndWaves * 64)
     }  // some lane has a pool
     if (slot < total) bounds[slot] = res;
 
-    if (idx_out != nullptr) {
-      // The windows' positions in list order, then -1: one query at a time.
-      for (uint64_t m = qmask; m != 0ull; m &= m - 1ull) {
-        const int u = __ffsll((unsigned long long)m) - 1;
-        const int32_t* upos = readlane_ptr(L.pos, u);
-        const int32_t ua = __builtin_amdgcn_readlane(res.x, u), ub = __builtin_amdgcn_readlane(res.y, u);
-        const int32_t ulim = __builtin_amdgcn_readlane(L.limit, u);
-        const int32_t ui = __builtin_amdgcn_readlane(my_i, u);
-        const int64_t useg = int64_t(uint32_t(run * 64 + u) / uint32_t(N));  // slots < B*H*N < 2^31
-        int32_t* row = idx_out + (useg * N + ui) * int64_t(topk);
-        int cnt = 0;
-        for (int32_t e0 = ua; e0 <= ub; e0 += 64) {
-          const int32_t e = e0 + lane;
-          const int32_t pv = e <= ub ? upos[e] : INT32_MAX;
-          const bool ok = pv <= ulim;
-          const uint64_t bal = wave_ballot(ok);
-          if (ok) row[cnt + int(lanes_below(bal))] = pv;
-          cnt += __popcll(bal);
+    wave_lds_sync();
+  }
+}
+
+// ---- index rows from window bounds -------------------------------------------
+// Writes each query's window as positions: its in-pool entries of the list
+// range [a, b] in list order, then -1 (select_window's row, from the bounds
+// window_bounds wrote).  A wavefront takes 16 consecutive slots of the
+// processing order.  Queries searching one list (nearly always all 16) have
+// overlapping ranges: their union's positions are read once into LDS (up to
+// kRowsStage entries; a longer union is read from the list itself).  Each
+// query's row is then written 64 entries at a time, the in-pool ones by
+// ballot compaction into consecutive slots of the row.
+constexpr int kRowsWaves = 4;
+constexpr int kRowsStage = 1024;
+__shared__ int32_t s_rows_pos[kRowsWaves][kRowsStage];
+
+__global__ void __launch_bounds__(kRowsWaves * 64)
+    idx_rows_kernel(const uint32_t* __restrict__ sorted_codes, const int32_t* __restrict__ perm,
+                    const uint32_t* __restrict__ list_codes, const int32_t* __restrict__ list_pos,
+                    const int32_t* __restrict__ order, const int2* __restrict__ bounds, int64_t total, int64_t N,
+                    int topk, int causal, int chunk, int t0, int t_hi, int64_t cap, int32_t* __restrict__ idx) {
+  constexpr int kQ = 16;  // slots per wavefront
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+  const int64_t groups = (total + kQ - 1) / kQ;
+  const int64_t nb = gridDim.x;
+  for (int64_t blk = xcd_contiguous_block(blockIdx.x, nb); blk * kRowsWaves < groups; blk += nb) {
+    const int64_t grp = blk * kRowsWaves + wave;
+    if (grp >= groups) continue;
+    // Lanes 0..15: one slot each (its query, list, pool limit and window).
+    int32_t my_i = -1, my_lvl = 0, my_a = 0, my_b = -1;
+    int64_t my_seg = 0;
+    if (lane < kQ) {
+      const int64_t sl = grp * kQ + lane;
+      if (sl < total) {
+        const int64_t sg = int64_t(uint32_t(sl) / uint32_t(N));  // slots < B*H*N < 2^31
+        const int64_t ii = order != nullptr ? int64_t(order[sl]) : sl - sg * N;
+        if (ii >= 0 && ii < N) {
+          my_i = int32_t(ii);
+          my_seg = sg;
+          const int2 bd = bounds[sl];
+          my_a = bd.x;
+          my_b = bd.y;
+          const int32_t lim = causal ? pool_limit(my_i, chunk) : int32_t(N - 1);
+          my_lvl = causal ? (lim < 0 ? -1 : query_level(lim, t0, t_hi)) : 0;
         }
-        for (int c = cnt + lane; c < topk; c += 64) row[c] = -1;
       }
     }
-    wave_lds_sync();
+    uint32_t pending = uint32_t(wave_ballot(my_i >= 0)) & 0xFFFFu;
+    while (pending != 0u) {
+      const int leader = __ffs(int(pending)) - 1;
+      const int64_t g_seg = __builtin_amdgcn_readlane(int32_t(my_seg), leader);
+      const int g_lvl = __builtin_amdgcn_readlane(my_lvl, leader);
+      const uint32_t gmask =
+          uint32_t(wave_ballot(my_i >= 0 && my_seg == g_seg && my_lvl == g_lvl)) & pending;
+      pending &= ~gmask;
+      const int32_t g_i = __builtin_amdgcn_readlane(my_i, leader);
+      const QueryList L = query_list(sorted_codes, perm, list_codes, list_pos, g_seg, N, g_i, causal, t0, t_hi,
+                                     cap, chunk);
+      // The union of the group's windows (a window outside the list counts
+      // as empty).
+      const bool in_grp = ((gmask >> lane) & 1u) != 0u;
+      const bool has = in_grp && 0 <= my_a && my_a <= my_b && my_b < L.n;
+      const int32_t ua = wave_min_int(has ? my_a : INT32_MAX);
+      const int32_t ub = wave_max_int(has ? my_b : INT32_MIN);
+      const bool staged = ua <= ub && ub - ua < kRowsStage;
+      if (staged) {
+        for (int32_t e0 = ua; e0 <= ub; e0 += 4 * 64) {
+          int32_t pv[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int32_t e = e0 + t * 64 + lane;
+            pv[t] = e <= ub ? L.pos[e] : 0;
+          }
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int32_t e = e0 + t * 64 + lane;
+            if (e <= ub) s_rows_pos[wave][e - ua] = pv[t];
+          }
+        }
+      }
+      wave_lds_sync();
+      for (uint32_t m = gmask; m != 0u; m &= m - 1u) {
+        const int u = __ffs(int(m)) - 1;
+        const int32_t a = __builtin_amdgcn_readlane(my_a, u), b = __builtin_amdgcn_readlane(my_b, u);
+        const int32_t i = __builtin_amdgcn_readlane(my_i, u);
+        const int32_t lim = causal ? pool_limit(i, chunk) : int32_t(N - 1);
+        int32_t* row = idx + (g_seg * N + i) * int64_t(topk);
+        int cnt = 0;
+        if (0 <= a && a <= b && b < L.n) {
+          for (int32_t e0 = a; e0 <= b; e0 += 64) {
+            const int32_t e = e0 + lane;
+            const int32_t pv = e <= b ? (staged ? s_rows_pos[wave][e - ua] : L.pos[e]) : INT32_MAX;
+            const bool ok = pv <= lim;
+            const uint64_t bal = wave_ballot(ok);
+            const int at = cnt + int(lanes_below(bal));
+            if (ok && at < topk) row[at] = pv;
+            cnt += __popcll(bal);
+          }
+        }
+        if (cnt < topk)
+          for (int c = cnt + lane; c < topk; c += 64) row[c] = -1;
+      }
+      // Every read of the staged positions is done before they are replaced.
+      wave_lds_sync();
+    }
   }
 }
 
@@ -1453,7 +1536,15 @@ hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int 
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
     hipLaunchKernelGGL(window_bounds_kernel, dim3(blocks), dim3(kBndWaves * 64), 0, stream, q_codes, sorted_codes,
                        perm, list_codes, list_pos, q_order, total, N, topk, causal ? 1 : 0, chunk, lp.t0, lp.t_hi,
-                       lp.cap, bounds, idx_out);
+                       lp.cap, bounds);
+  }
+  if (idx_out != nullptr) {
+    const int64_t groups = ceil_div(total, 16);
+    const int64_t want = ceil_div(groups, kRowsWaves);
+    const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
+    hipLaunchKernelGGL(idx_rows_kernel, dim3(blocks), dim3(kRowsWaves * 64), 0, stream, sorted_codes, perm,
+                       list_codes, list_pos, q_order, bounds, total, N, topk, causal ? 1 : 0, chunk, lp.t0, lp.t_hi,
+                       lp.cap, idx_out);
   }
   return hipGetLastError();
 }

@@ -144,7 +144,8 @@ zeta_status_t zeta_select_topk(const uint32_t* q_codes, const uint32_t* sorted_c
   if (topk < 1 || bad_pool(causal, chunk)) return ZETA_ERR_INVALID_ARG;
   if (topk > zeta::kMaxTopk) return ZETA_ERR_UNSUPPORTED;
   const zeta::SelectWs ws = zeta::select_ws(n_segments, N, topk, causal);
-  if (ws.bytes > 0 && (workspace == nullptr || workspace_bytes < ws.bytes)) return ZETA_ERR_WORKSPACE;
+  if (workspace == nullptr || workspace_bytes < ws.call_bytes) return ZETA_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return ZETA_ERR_INVALID_ARG;
   return hip_status(zeta::launch_select(q_codes, sorted_codes, perm, n_segments, N, topk, causal != 0, chunk,
                                         q_order, idx, workspace, stream));
 }
@@ -315,7 +316,7 @@ size_t zeta_workspace_size(int64_t B, int64_t H, int64_t N, int d_k, int bits, i
   size_t bytes = zeta::encode_ws(S, N, d_k).bytes;
   // Room to sort the query codes together with the key codes (2*B*H segments).
   const size_t sb = zeta::sort_ws(2 * S, N, d_k * bits).bytes;
-  const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).bytes;
+  const size_t lb = zeta::select_ws(S, N, topk, causal ? 1 : 0).call_bytes;
   const size_t ob = zeta::query_order_ws(S, N).bytes;
   const size_t fb = zeta::fused_ws(S, N, topk, causal ? 1 : 0).bytes;
   const size_t hb = zeta::hist_ws(S, N, zeta::kHistMaxCols).bytes;

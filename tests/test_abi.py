@@ -244,6 +244,8 @@ SELECT_CASES = [
     (dict(S=0), INV), (dict(N=0), INV), (dict(topk=0), INV), (dict(causal=2), INV),
     (dict(chunk=-1), INV), (dict(causal=0, chunk=4), INV),  # the chunked rule is causal
     (dict(topk=1025), UNS), (dict(ws=NULL), WSP), (dict(ws_bytes=64), WSP),
+    (dict(causal=0, ws=NULL), WSP),  # the window bounds need room even without prefix lists
+    (dict(ws=ctypes.c_void_p(0x10008)), INV),  # not 16-byte aligned
 ]
 
 
