@@ -428,14 +428,34 @@ __global__ void __launch_bounds__(kRowsWaves * 64)
         int32_t* row = idx + (g_seg * N + i) * int64_t(topk);
         int cnt = 0;
         if (0 <= a && a <= b && b < L.n) {
-          for (int32_t e0 = a; e0 <= b; e0 += 64) {
-            const int32_t e = e0 + lane;
-            const int32_t pv = e <= b ? (staged ? s_rows_pos[wave][e - ua] : L.pos[e]) : INT32_MAX;
-            const bool ok = pv <= lim;
-            const uint64_t bal = wave_ballot(ok);
-            const int at = cnt + int(lanes_below(bal));
-            if (ok && at < topk) row[at] = pv;
-            cnt += __popcll(bal);
+          if (staged) {
+            // Two blocks per step, both read before either is compacted
+            // (indices past the union clamped into the stage, then masked).
+            for (int32_t e0 = a; e0 <= b; e0 += 128) {
+              const int32_t e1 = e0 + lane, e2 = e1 + 64;
+              const int32_t o1 = e1 - ua < kRowsStage ? e1 - ua : kRowsStage - 1;
+              const int32_t o2 = e2 - ua < kRowsStage ? e2 - ua : kRowsStage - 1;
+              int32_t p1 = s_rows_pos[wave][o1], p2 = s_rows_pos[wave][o2];
+              p1 = e1 <= b ? p1 : INT32_MAX;
+              p2 = e2 <= b ? p2 : INT32_MAX;
+              const bool ok1 = p1 <= lim, ok2 = p2 <= lim;
+              const uint64_t b1 = wave_ballot(ok1), b2 = wave_ballot(ok2);
+              const int at1 = cnt + int(lanes_below(b1));
+              const int at2 = cnt + __popcll(b1) + int(lanes_below(b2));
+              if (ok1 && at1 < topk) row[at1] = p1;
+              if (ok2 && at2 < topk) row[at2] = p2;
+              cnt += __popcll(b1) + __popcll(b2);
+            }
+          } else {
+            for (int32_t e0 = a; e0 <= b; e0 += 64) {
+              const int32_t e = e0 + lane;
+              const int32_t pv = e <= b ? L.pos[e] : INT32_MAX;
+              const bool ok = pv <= lim;
+              const uint64_t bal = wave_ballot(ok);
+              const int at = cnt + int(lanes_below(bal));
+              if (ok && at < topk) row[at] = pv;
+              cnt += __popcll(bal);
+            }
           }
         }
         if (cnt < topk)
@@ -940,7 +960,7 @@ __global__ void __launch_bounds__(kTileWaves * 64)
     // on down to one query, whose row is its own union (slot order, an entry
     // per slot).  Returns the queries covered; n receives the entry count.
     auto build_union = [&](uint32_t gm, int64_t seg, int& n) -> uint32_t {
-      flush_out();  // the value-row buffers hold the hash table next
+      flush_out();  // the value-row buffers hold the bitmap or the hash table next
       uint32_t sub = gm;
       for (;;) {
         const int nq = __popc(sub);
