@@ -26,8 +26,8 @@
 // typically the Z-order of the query codes, by the list each query searches,
 // keeping the given order inside each group (one stable radix pass on the
 // level).  A run of that order searches one list with non-decreasing codes, so
-// the queries reuse each other's cached entries and the search gallops from
-// the previous insertion point; attend's tiles share value rows the same way.
+// the window-bounds kernel stages one stretch of the list for 64 queries and
+// attend's tiles share value rows the same way.
 #include <stdint.h>
 
 #include "attend_device.h"
