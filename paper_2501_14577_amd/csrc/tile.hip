@@ -121,37 +121,88 @@ constexpr int kMargin = 192;    // of them before the run's first insertion poin
 constexpr int kPosStride = 36;
 __shared__ uint32_t s_bnd_codes[kBndWaves][kRegion];
 __shared__ __align__(16) int32_t s_bnd_pos[kBndWaves][kRegion / 32 * kPosStride];
+// Segments of at most 65536 rows: positions as 16-bit values, biased by
+// 2^15 (pos - 32768 as a signed 16-bit number), 40 to a block of 32 entries
+// (80 bytes: the 16 blocks of a region start in 16 different bank groups),
+// each entry at element pos16_slot(j) of its block.
+constexpr int kPos16Stride = 40;
+__shared__ __align__(16) uint16_t s_bnd_pos16[kBndWaves][kRegion / 32 * kPos16Stride];
 
 struct LaneList {
   const uint32_t* codes;
   const int32_t* pos;
   int wave;
   int32_t n, limit, r0, r1;  // [r0, r1): the range copied to LDS (empty when not staged)
+  uint32_t lim2;             // 16-bit positions: the biased limit in both halves
 };
 
 constexpr int kScanStep = 32;  // list entries examined per step of lane_scan (one bit each of a 32-bit mask)
 static_assert(kScanStep == 32, "the scan masks are 32-bit words");
 static_assert(kRegion % 64 == 0, "staged in whole rounds of 64 entries, two blocks each");
 
+// Element of its block that holds entry j of the block (16-bit positions).
+// The gather in pool_bits sets bit 8c + k from element 4k + c; entry j
+// belongs in bit 31 - j.
+__device__ __forceinline__ int pos16_slot(int j) {
+  const int q = 31 - j;
+  return 4 * (q & 7) + (q >> 3);
+}
+
+typedef short short2_t __attribute__((ext_vector_type(2)));
+
 // The query's in-pool entries B .. B + kScanStep - 1 (B a multiple of
-// kScanStep) as a bit mask, first entry in the highest bit: bit 31 - j is
-// entry B + j.  An entry is in the pool when pos <= limit, i.e. when
+// kScanStep, B < n) as a bit mask, first entry in the highest bit: bit 31 - j
+// is entry B + j.  A block inside the staged range is read from LDS, any other
+// block from the list itself, with entries outside [0, n) counted out.
+//
+// 32-bit positions: an entry is in the pool when pos <= limit, i.e. when
 // pos - limit - 1 is negative; each entry's sign bit is shifted in with one
-// funnel shift.  A block inside the staged range is read from LDS (entries
-// past the list's end hold INT32_MAX, in no pool); any other block from the
-// list itself, with entries outside [0, n) counted out.
+// funnel shift (staged entries past the list's end hold INT32_MAX, in no
+// pool).
+// 16-bit positions (biased by 2^15): one saturating packed subtraction
+// limit - pos covers two entries, negative exactly when pos > limit (the
+// clamp keeps the sign); a byte permute spreads the sign bits of four entries
+// into four bytes, and one masked OR per four entries packs them.  Entries
+// past the list's end are cleared from the mask.
+template <bool kPos16>
 __device__ __forceinline__ uint32_t pool_bits(const LaneList& L, int32_t B) {
   const uint32_t nl = uint32_t(-1 - L.limit);  // pos + nl < 0 exactly when pos <= limit (no overflow)
   uint32_t mask = 0u;
   if (L.r1 > L.r0 && B >= L.r0 && B + kScanStep <= L.r0 + kRegion) {
-    const int4* blk = reinterpret_cast<const int4*>(&s_bnd_pos[L.wave][(B - L.r0) / kScanStep * kPosStride]);
+    if constexpr (kPos16) {
+      const uint4* blk = reinterpret_cast<const uint4*>(&s_bnd_pos16[L.wave][(B - L.r0) / kScanStep * kPos16Stride]);
+      uint32_t w[16];
 #pragma unroll
-    for (int t = 0; t < kScanStep / 4; ++t) {
-      const int4 v = blk[t];
-      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.x) + nl, 31);
-      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.y) + nl, 31);
-      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.z) + nl, 31);
-      mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.w) + nl, 31);
+      for (int t = 0; t < 4; ++t) {
+        const uint4 v = blk[t];
+        w[4 * t] = v.x;
+        w[4 * t + 1] = v.y;
+        w[4 * t + 2] = v.z;
+        w[4 * t + 3] = v.w;
+      }
+      const short2_t lim = __builtin_bit_cast(short2_t, L.lim2);
+      uint32_t out = 0u;  // bit set: entry out of the pool
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const uint32_t d0 = __builtin_bit_cast(uint32_t, __builtin_elementwise_sub_sat(lim, __builtin_bit_cast(short2_t, w[2 * k])));
+        const uint32_t d1 =
+            __builtin_bit_cast(uint32_t, __builtin_elementwise_sub_sat(lim, __builtin_bit_cast(short2_t, w[2 * k + 1])));
+        // Selectors 8..11: the sign bits of the four 16-bit halves, each as a byte.
+        out |= __builtin_amdgcn_perm(d1, d0, 0x0B0A0908u) & (0x01010101u << k);
+      }
+      const int32_t rem = L.n - B;  // >= 1
+      const int sh = rem < kScanStep ? kScanStep - rem : 0;
+      mask = ~out & (~0u << sh);
+    } else {
+      const int4* blk = reinterpret_cast<const int4*>(&s_bnd_pos[L.wave][(B - L.r0) / kScanStep * kPosStride]);
+#pragma unroll
+      for (int t = 0; t < kScanStep / 4; ++t) {
+        const int4 v = blk[t];
+        mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.x) + nl, 31);
+        mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.y) + nl, 31);
+        mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.z) + nl, 31);
+        mask = __builtin_amdgcn_alignbit(mask, uint32_t(v.w) + nl, 31);
+      }
     }
   } else {
     using G = __attribute__((address_space(1))) const int32_t;
@@ -186,13 +237,17 @@ __device__ __forceinline__ int nth_set_bit(uint32_t m, int n) {
 // taken (first only when got is 0).  Returns the new count; `e` ends just
 // past the last entry taken, or past the list's end.  Entries are examined in
 // aligned blocks of kScanStep as a bit mask (bit k: entry base + dir*k); only
-// the block where the count is reached is searched for its bit.  Called only
-// with n > 0.
+// the block where the count is reached is searched for its bit, once, after
+// the loop.  Called only with n > 0.
+template <bool kPos16>
 __device__ __forceinline__ int lane_scan(const LaneList& L, int32_t& e, int dir, int need, int got, int32_t& first,
                                          int32_t& last) {
+  uint32_t end_mask = 0u;  // the block where the count is reached, and the bit wanted there
+  int32_t end_base = 0;
+  int end_n = 0;
   while (got < need && e >= 0 && e < L.n) {
     const int32_t B = e & ~(kScanStep - 1);
-    uint32_t mask = pool_bits(L, B);  // bit 31 - j: entry B + j
+    uint32_t mask = pool_bits<kPos16>(L, B);  // bit 31 - j: entry B + j
     int32_t base;
     if (dir > 0) {
       base = B;
@@ -212,14 +267,20 @@ __device__ __forceinline__ int lane_scan(const LaneList& L, int32_t& e, int dir,
       last = base + dir * (31 - __clz(int(mask)));
       e = base + dir * kScanStep;
     } else {
-      last = base + dir * nth_set_bit(mask, need - got);
-      e = last + dir;
+      end_mask = mask;
+      end_base = base;
+      end_n = need - got;
       got = need;
     }
+  }
+  if (end_n > 0) {
+    last = end_base + dir * nth_set_bit(end_mask, end_n);
+    e = last + dir;
   }
   return got;
 }
 
+template <bool kPos16>
 __global__ void __launch_bounds__(kBndWaves * 64)
     window_bounds_kernel(const uint32_t* __restrict__ q_codes, const uint32_t* __restrict__ sorted_codes,
                          const int32_t* __restrict__ perm, const uint32_t* __restrict__ list_codes,
@@ -262,6 +323,11 @@ __global__ void __launch_bounds__(kBndWaves * 64)
     L.limit = Lq.limit;
     L.r0 = 0;
     L.r1 = 0;
+    {
+      const int32_t lc = Lq.limit < 0 ? 0 : (Lq.limit > 65535 ? 65535 : Lq.limit);
+      const uint32_t b16 = uint32_t(lc) ^ 0x8000u;
+      L.lim2 = b16 | (b16 << 16);
+    }
     int2 res = make_int2(0, -1);
     if (vmask != 0ull) {
       // Stage the leader's list around the leader's insertion point.
@@ -282,10 +348,14 @@ __global__ void __launch_bounds__(kBndWaves * 64)
           cv[t] = e < r1 ? g_codes[e] : 0u;
           pv[t] = e < r1 ? g_pos[e] : INT32_MAX;  // past the list's end: in no pool
         }
+        const int slot16 = pos16_slot(lane % kScanStep);
 #pragma unroll
         for (int t = 0; t < kRegion / 64; ++t) {
           s_bnd_codes[wave][t * 64 + lane] = cv[t];
-          s_bnd_pos[wave][(2 * t + lane / kScanStep) * kPosStride + lane % kScanStep] = pv[t];
+          if constexpr (kPos16)  // positions < 65536; past the list's end: counted out by pool_bits
+            s_bnd_pos16[wave][(2 * t + lane / kScanStep) * kPos16Stride + slot16] = uint16_t(uint32_t(pv[t]) ^ 0x8000u);
+          else
+            s_bnd_pos[wave][(2 * t + lane / kScanStep) * kPosStride + lane % kScanStep] = pv[t];
         }
       }
       wave_lds_sync();
@@ -327,11 +397,12 @@ __global__ void __launch_bounds__(kBndWaves * 64)
         // farthest entry taken.
         int32_t r_first = 0, r_last = -1, l_near = -1, l_far = 0;
         int32_t cur_r = p;
-        int got_r = lane_scan(L, cur_r, +1, need_r, 0, r_first, r_last);
+        int got_r = lane_scan<kPos16>(L, cur_r, +1, need_r, 0, r_first, r_last);
         const int need_l = half + (need_r - got_r);
         int32_t cur_l = p - 1;
-        const int got_l = lane_scan(L, cur_l, -1, need_l, 0, l_near, l_far);
-        if (got_l < need_l && got_r == need_r) got_r = lane_scan(L, cur_r, +1, topk - got_l, got_r, r_first, r_last);
+        const int got_l = lane_scan<kPos16>(L, cur_l, -1, need_l, 0, l_near, l_far);
+        if (got_l < need_l && got_r == need_r)
+          got_r = lane_scan<kPos16>(L, cur_r, +1, topk - got_l, got_r, r_first, r_last);
         if (got_l + got_r > 0) res = make_int2(got_l > 0 ? l_far : r_first, got_r > 0 ? r_last : l_near);
       }
     }  // some lane has a pool
@@ -623,6 +694,10 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   // these plus two chunks of value rows).
   constexpr int kStageEntries = kIdx ? kIdxUnionCap : (DK == 3 && DV <= 128) ? 320 : 128;
   constexpr int kStage = kStageEntries / kChunk;
+  // List ranges are staged in whole rounds of 64 entries (every staged
+  // entry written); index-row unions in whole chunks.
+  static_assert(kIdx || kStageEntries % 64 == 0, "list staging fills rounds of 64 entries");
+  static_assert(kStageEntries % kChunk == 0, "the stage holds whole chunks");
   static_assert(E >= 2, "d_v must be a multiple of 32");
   // Each A fragment is read from LDS twice (both K halves of a product) where
   // the registers allow it, else read once and copied.
@@ -1554,9 +1629,10 @@ hipError_t launch_tile_windows(const void* k, int64_t S, int64_t N, int dk, int 
     const int64_t runs = ceil_div(total, 64);
     const int64_t want = ceil_div(runs, kBndWaves);
     const unsigned blocks = unsigned(want < (int64_t(1) << 20) ? want : (int64_t(1) << 20));
-    hipLaunchKernelGGL(window_bounds_kernel, dim3(blocks), dim3(kBndWaves * 64), 0, stream, q_codes, sorted_codes,
-                       perm, list_codes, list_pos, q_order, total, N, topk, causal ? 1 : 0, chunk, lp.t0, lp.t_hi,
-                       lp.cap, bounds);
+    // Positions fit 16 bits when the segment has at most 65536 rows.
+    auto kern = N <= 65536 ? window_bounds_kernel<true> : window_bounds_kernel<false>;
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(kBndWaves * 64), 0, stream, q_codes, sorted_codes, perm, list_codes,
+                       list_pos, q_order, total, N, topk, causal ? 1 : 0, chunk, lp.t0, lp.t_hi, lp.cap, bounds);
   }
   if (idx_out != nullptr) {
     const int64_t groups = ceil_div(total, 16);
