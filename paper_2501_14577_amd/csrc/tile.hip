@@ -59,7 +59,8 @@
 // chunk pipeline (kIdx): a wavefront takes 16 consecutive queries of the
 // order and stages the union of their index rows as one run of chunks, each
 // entry with the mask of the tile's queries whose rows hold it (a query's
-// score is zero where its bit is clear).  The union is found without
+// score is zero where its bit is clear).  There the high and low score parts
+// are two 16 x 16 x 16 products on one read of each value fragment.  The union is found without
 // barriers, per wavefront: for segments of at most 65536 rows as a bitmap of
 // positions (entries in position order, each entry's index its rank), else
 // in a hash table keyed by position (entries in slot order).  A union larger
@@ -699,9 +700,13 @@ __global__ void __launch_bounds__(kTileWaves * 64)
   static_assert(kIdx || kStageEntries % 64 == 0, "list staging fills rounds of 64 entries");
   static_assert(kStageEntries % kChunk == 0, "the stage holds whole chunks");
   static_assert(E >= 2, "d_v must be a multiple of 32");
-  // Each A fragment is read from LDS twice (both K halves of a product) where
-  // the registers allow it, else read once and copied.
-  constexpr int kTrCopies = (DV <= 128 && kOff32) ? 2 : 1;
+  // The high and low score parts of a block: index-row tiles take two
+  // 16 x 16 x 16 products on one read of the A fragment; list ranges one
+  // 16 x 16 x 32 product whose K halves both hold the fragment, read from LDS
+  // twice where the registers allow it, else read once and copied (faster
+  // there, measured: the extra products cost more than the saved reads).
+  constexpr bool kSplitK = kIdx;
+  constexpr int kTrCopies = kSplitK ? 1 : (DV <= 128 && kOff32) ? 2 : 1;
   using Off = typename RowOff<kOff32>::type;
   const int dk = DK > 0 ? DK : dk_rt;
   // Score (compile time): the Cauchy score, or a variant (softmax variants
@@ -1307,21 +1312,38 @@ __global__ void __launch_bounds__(kTileWaves * 64)
 #pragma unroll
           for (int j = 0; j < E; ++j) acc[j] *= scl;
         }
-        // One 16 x 16 x 32 product per block: its 32 K slots hold the 4
-        // entries' values twice (A: the fragment read twice, or read once and
-        // copied) against their high, then their low score parts (B).
-        Frag8 b;
-        b.w[0] = bh[0];
-        b.w[1] = bh[1];
-        b.w[2] = bl[0];
-        b.w[3] = bl[1];
-        read_tr_wait<kTrCopies * E>(a);
+        if constexpr (kSplitK) {
+          // Two 16 x 16 x 16 products per block on the same A fragment (the
+          // 4 entries' values): against the high score parts of every block
+          // first, then against the low parts, so that consecutive products
+          // into one accumulator stand E products apart.
+          Frag b_hi, b_lo;
+          b_hi.w[0] = bh[0];
+          b_hi.w[1] = bh[1];
+          b_lo.w[0] = bl[0];
+          b_lo.w[1] = bl[1];
+          read_tr_wait<kTrCopies * E>(a);
 #pragma unroll
-        for (int j = 0; j < E; ++j) {
-          const bf16x8_t a8 = __builtin_bit_cast(
-              bf16x8_t, __builtin_shufflevector(a[kTrCopies * j], a[kTrCopies * j + kTrCopies - 1], 0, 1, 2, 3, 4, 5,
-                                                6, 7));
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8, b.v, acc[j], 0, 0, 0);
+          for (int j = 0; j < E; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a[j], b_hi.v, acc[j], 0, 0, 0);
+#pragma unroll
+          for (int j = 0; j < E; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a[j], b_lo.v, acc[j], 0, 0, 0);
+        } else {
+          // One 16 x 16 x 32 product per block: its 32 K slots hold the 4
+          // entries' values twice against their high, then their low score
+          // parts (B).
+          Frag8 b;
+          b.w[0] = bh[0];
+          b.w[1] = bh[1];
+          b.w[2] = bl[0];
+          b.w[3] = bl[1];
+          read_tr_wait<kTrCopies * E>(a);
+#pragma unroll
+          for (int j = 0; j < E; ++j) {
+            const bf16x8_t a8 = __builtin_bit_cast(
+                bf16x8_t, __builtin_shufflevector(a[kTrCopies * j], a[kTrCopies * j + kTrCopies - 1], 0, 1, 2, 3, 4,
+                                                  5, 6, 7));
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8, b.v, acc[j], 0, 0, 0);
+          }
         }
       };
 
