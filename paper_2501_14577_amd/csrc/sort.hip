@@ -58,11 +58,21 @@ __global__ void __launch_bounds__(kRadixThreads)
   const uint32_t mask = (1u << nbits) - 1u;
   constexpr int64_t kTile = int64_t(kRadixThreads) * kChunks;
   const int64_t e0 = tile * kTile;
-  const int64_t e1 = (e0 + kTile < N) ? e0 + kTile : N;
-  for (int64_t e = e0 + tid; e < e1; e += kRadixThreads) {
-    const uint32_t key = kByLevel ? 0u : keys[seg * N + e];
-    const int32_t val = kByLevel ? (vals != nullptr ? vals[seg * N + e] : int32_t(e)) : 0;
-    atomicAdd(&h[radix_digit<kByLevel>(key, val, shift, mask, t0, t_hi, chunk, N)], 1u);
+  // Every load issued first (an element past the segment's end reads its
+  // last one, then is left out), so that their latencies overlap.
+  uint32_t key[kChunks];
+  int32_t val[kChunks];
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int64_t e = e0 + c * kRadixThreads + tid;
+    const int64_t ec = e < N ? e : N - 1;
+    key[c] = kByLevel ? 0u : keys[seg * N + ec];
+    val[c] = kByLevel ? (vals != nullptr ? vals[seg * N + ec] : int32_t(e)) : 0;
+  }
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    if (e0 + c * kRadixThreads + tid < N)
+      atomicAdd(&h[radix_digit<kByLevel>(key[c], val[c], shift, mask, t0, t_hi, chunk, N)], 1u);
   }
   __syncthreads();
   hist[(seg * tiles + tile) * kRadixMax + tid] = h[tid];
@@ -142,6 +152,22 @@ __global__ void __launch_bounds__(kRadixThreads)
   __shared__ int32_t s_val[kTile];
   __shared__ uint32_t s_scan[kRadixWaves];
 
+  // This wavefront's keys, loaded before anything else so that their
+  // latency overlaps the digit offsets' loads: every load issued (an element
+  // past the segment's end reads its last one, then is left out).
+  const int64_t seg_off = seg * N;
+  const int64_t tile0 = tile * kTile;
+  const int64_t first = tile0 + int64_t(wave) * (kChunks * 64);
+  uint32_t key[kChunks];
+  int32_t pos[kChunks];
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int64_t e = first + c * 64 + lane;
+    const int64_t ec = e < N ? e : N - 1;
+    key[c] = kByLevel ? 0u : keys_in[seg_off + ec];
+    pos[c] = kHasPos ? pos_in[seg_off + ec] : int32_t(e);
+  }
+
   {
     // This thread's digit value: its count in earlier tiles and in the
     // whole segment.
@@ -172,22 +198,13 @@ __global__ void __launch_bounds__(kRadixThreads)
   }
   __syncthreads();
 
-  const int64_t seg_off = seg * N;
-  const int64_t tile0 = tile * kTile;
-  const int64_t first = tile0 + int64_t(wave) * (kChunks * 64);
-  uint32_t key[kChunks];
-  int32_t pos[kChunks];
   uint32_t rank[kChunks];
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
     const int64_t e = first + c * 64 + lane;
     const bool valid = e < N;
-    const uint32_t kk = (valid && !kByLevel) ? keys_in[seg_off + e] : 0u;
-    int32_t pp;
-    if (kHasPos)
-      pp = valid ? pos_in[seg_off + e] : 0;
-    else
-      pp = int32_t(e);
+    const uint32_t kk = (valid && !kByLevel) ? key[c] : 0u;
+    const int32_t pp = kHasPos ? (valid ? pos[c] : 0) : int32_t(e);
     const uint32_t d = radix_digit<kByLevel>(kk, pp, shift, mask, t0, t_hi, chunk, N);
     uint64_t peers = wave_ballot(valid);
     for (int b = 0; b < nbits; ++b) {
