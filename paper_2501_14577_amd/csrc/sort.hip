@@ -31,6 +31,8 @@ namespace {
 
 constexpr int kRadixWaves = kRadixThreads / 64;
 static_assert(kRadixThreads == kRadixMax, "one digit value per thread");
+constexpr int kDigitBits = 9;  // the most bits one pass takes
+static_assert((1 << kDigitBits) == kRadixMax, "a digit indexes the per-tile counts");
 
 // Digit of an element: the key's bits [shift, shift+nbits) (kByLevel false), or
 // the prefix-list level class of the carried position (kByLevel true; the
@@ -206,12 +208,22 @@ __global__ void __launch_bounds__(kRadixThreads)
     const uint32_t kk = (valid && !kByLevel) ? key[c] : 0u;
     const int32_t pp = kHasPos ? (valid ? pos[c] : 0) : int32_t(e);
     const uint32_t d = radix_digit<kByLevel>(kk, pp, shift, mask, t0, t_hi, chunk, N);
-    uint64_t peers = wave_ballot(valid);
-    for (int b = 0; b < nbits; ++b) {
-      const bool bit = (d >> b) & 1u;
-      const uint64_t ones = wave_ballot(bit);
-      peers &= bit ? ones : ~ones;
+    // Lanes with this lane's digit: for every digit bit, those whose bit
+    // equals this lane's, i.e. peers & ~(ones ^ s) per 32-bit half with s all
+    // ones where the bit is set (one three-input bit operation; its table
+    // 0x90 is that function of the operand patterns 0xF0, 0xCC, 0xAA).
+    const uint64_t valid_m = wave_ballot(valid);
+    uint32_t plo = uint32_t(valid_m), phi = uint32_t(valid_m >> 32);
+#pragma unroll
+    for (int b = 0; b < kDigitBits; ++b) {
+      if (b < nbits) {
+        const uint32_t s = uint32_t(int32_t(d << (31 - b)) >> 31);
+        const uint64_t ones = wave_ballot(s != 0u);
+        plo = __builtin_amdgcn_bitop3_b32(plo, uint32_t(ones), s, 0x90);
+        phi = __builtin_amdgcn_bitop3_b32(phi, uint32_t(ones >> 32), s, 0x90);
+      }
     }
+    const uint64_t peers = (uint64_t(phi) << 32) | plo;
     const uint32_t below = lanes_below(peers);
     const uint32_t base = s_wcnt[wave][d];
     if (valid && below == 0) s_wcnt[wave][d] = base + uint32_t(__popcll(peers));
