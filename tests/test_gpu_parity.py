@@ -213,9 +213,14 @@ def test_select_long_context_sampled():
 
 @pytest.mark.parametrize("N,topk,code_bits", [(1, 1, 6), (1, 8, 30), (2, 1, 2), (5, 3, 2), (100, 7, 3),
                                               (129, 64, 4), (300, 2, 30), (1000, 33, 3), (4097, 64, 6),
-                                              (5000, 1024, 9), (3000, 1000, 2), (20000, 16, 12), (9000, 5, 1)])
+                                              (5000, 1024, 9), (3000, 1000, 2), (20000, 16, 12), (9000, 5, 1),
+                                              (65536, 16, 12), (70001, 40, 6)])
 @pytest.mark.parametrize("causal", [True, False])
 def test_select_shapes(N, topk, code_bits, causal):
+    """Every row against the oracle (sampled rows past 4 M index slots).  The
+    window search tests positions as 16-bit values up to N = 65536 (the
+    largest position and pool limit 65535 included) and as 32-bit values
+    beyond."""
     log(f"select N={N} k={topk} bits={code_bits} causal={causal}")
     S = 2
     kc = workloads.random_codes(N * 7 + topk, (S, N), code_bits)
@@ -331,6 +336,9 @@ EDGE = [
     dict(N=1000, topk=100, dk=5, dv=256, dtype="bf16", bits=5),
     dict(N=700, topk=1024, dk=3, dv=128, dtype="bf16", bits=10),
     dict(N=900, topk=48, dk=3, dv=256, dtype="bf16", bits=7),
+    # The window search's 16-bit positions at their largest N, then 32-bit.
+    dict(N=65536, topk=16, dk=3, dv=32, dtype="bf16", bits=6),
+    dict(N=70001, topk=16, dk=3, dv=32, dtype="bf16", bits=6),
 ]
 
 
