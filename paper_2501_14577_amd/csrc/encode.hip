@@ -287,6 +287,14 @@ __global__ void __launch_bounds__(kEnc3Threads)
                    float* __restrict__ range_out, uint32_t* __restrict__ q_codes, uint32_t* __restrict__ k_codes) {
   const int64_t chunk = blockIdx.x, seg = blockIdx.y;
   const int64_t chunks = gridDim.x;
+  // This thread's rows are loaded first, so that their latency overlaps the
+  // range fold (a thread past the segment's end reads its first rows, and
+  // writes nothing).
+  const int64_t r = chunk * kEnc3Chunk + int64_t(threadIdx.x) * kEnc3Rows;
+  const int64_t rr = r < N ? r : 0;
+  float xq[24], xk[24];
+  load_rows8(q, seg * N + rr, xq);
+  load_rows8(k, seg * N + rr, xk);
   __shared__ float s_lo[3], s_hi[3];
   if (range_lohi != nullptr) {
     if (threadIdx.x < 3) {
@@ -316,7 +324,6 @@ __global__ void __launch_bounds__(kEnc3Threads)
     range_out[seg * 6 + threadIdx.x] = s_lo[threadIdx.x];
     range_out[seg * 6 + 3 + threadIdx.x] = s_hi[threadIdx.x];
   }
-  const int64_t r = chunk * kEnc3Chunk + int64_t(threadIdx.x) * kEnc3Rows;
   if (r >= N) return;
   const uint32_t top = (1u << bits) - 1u;
   const float topf = float(top);
@@ -332,8 +339,7 @@ __global__ void __launch_bounds__(kEnc3Threads)
   }
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
-    float x[24];
-    load_rows8(which == 0 ? q : k, seg * N + r, x);
+    const float(&x)[24] = which == 0 ? xq : xk;
     uint32_t c[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
