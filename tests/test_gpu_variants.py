@@ -66,6 +66,9 @@ CHUNK_EDGE = [
     dict(N=700, topk=1024, chunk=64, dtype="bf16"),
     dict(N=513, topk=64, chunk=2000, dtype="bf16"),
     dict(N=4097, topk=33, chunk=300, dtype="f32"),
+    # The window search's 16-bit positions at their largest N, then 32-bit.
+    dict(N=65536, topk=16, chunk=4096, dtype="bf16"),
+    dict(N=70001, topk=16, chunk=5000, dtype="bf16"),
 ]
 
 
