@@ -85,6 +85,8 @@ EDGE = [
     dict(N=700, topk=1024, dv=256),
     dict(N=1000, topk=16, dv=32, chunk=100),
     dict(N=2000, topk=40, dv=64, chunk=256),
+    # The window search's 32-bit positions (segments over 65536 rows).
+    dict(N=70001, topk=16, dv=32, chunk=5000),
 ]
 
 
